@@ -1,0 +1,374 @@
+"""Seeded synthetic inputs: execution graphs, pack tables and candidate policies.
+
+The paper evaluates on traces of real training and inference jobs (Sec. V-A) that are not
+available here, and publishes no graph statistics.  This module builds seeded stand-ins with
+the structure those traces have in Sec. IV-B: host (runtime-API) nodes in a launch chain,
+launch edges from host nodes to GPU packs, stream-order chains of packs, cross-stream event
+edges and all-stream synchronisation nodes.  Durations follow the distributions of the five
+benchmark workloads (tiny, inference-like, training-like, large packed, unpacked per-kernel).
+
+This module holds none of the method's arithmetic: no finish time, makespan, energy total,
+slack or selection is computed here.  Both the HIP path and the oracle consume what it makes.
+
+Conventions
+-----------
+* Time unit: microseconds.  Every duration and every table time lies on the dyadic grid
+  ``Q = 2**-4`` us (round half to even, at least one grid step), so sums of them stay exact in
+  fp32 while path lengths stay below ``2**20`` us.
+* Level ``j`` in ``[0, F)`` runs at frequency ratio ``r_j = 0.5 + 0.5*j/(F-1)``; level ``F-1`` is
+  the maximum frequency (1800 MHz-like), level 0 is half of it (900 MHz-like), matching the
+  900-1800 MHz range of the paper's random-policy experiment (Sec. V-B).
+* Pack latency ``t[p][j] = t_max*(a/r_j + 1 - a)`` with ``a ~ U(0,1)`` the frequency-sensitive
+  share; pack energy is the dynamic part ``e[p][j] = C_DYN * r_j**3 * t[p][j]`` of the power model
+  ``P(f) = Ps + c*(f/f_max)**3``; the static part ``Ps`` is charged over the whole makespan
+  through ``static_power``.
+* Node ids follow launch order, so every generated edge goes from a lower to a higher id.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Iterator
+
+import numpy as np
+
+Q = 1.0 / 16.0            # duration grid (us)
+STATIC_POWER = 0.3        # Ps, power units (P(f_max) = Ps + C_DYN = 1)
+C_DYN = 0.7               # dynamic power coefficient c
+POLICY_CHUNK = 1 << 16    # rows generated per independently seeded chunk
+
+
+@dataclasses.dataclass
+class Graph:
+    """Plain arrays describing one execution graph and its pack tables."""
+    name: str
+    num_nodes: int
+    edge_src: np.ndarray        # int32 [E]
+    edge_dst: np.ndarray        # int32 [E]
+    node_pack: np.ndarray       # int32 [V], pack id or -1
+    node_duration: np.ndarray   # float32 [V], used where node_pack == -1
+    num_packs: int
+    num_levels: int
+    pack_time: np.ndarray       # float32 [P, F]
+    pack_energy: np.ndarray     # float32 [P, F]
+    static_power: float
+    node_stream: np.ndarray | None = None   # int32 [V], -1 for host/sync nodes (informational)
+
+    @property
+    def num_edges(self) -> int:
+        return int(self.edge_src.shape[0])
+
+
+@dataclasses.dataclass(frozen=True)
+class ConfigSpec:
+    index: int
+    name: str
+    num_candidates: int
+    targets: tuple          # latency-target ratios relative to the all-max makespan
+    seed: int               # graph and table seed
+    policy_seed: int
+    exhaustive: bool = False
+    slack: bool = False     # the workload includes the backward slack pass for every candidate
+
+
+CONFIGS = {
+    1: ConfigSpec(1, "tiny-8p-2s-F4", 4 ** 8, (1.05,), 0, 1000, exhaustive=True, slack=True),
+    2: ConfigSpec(2, "inference-64p-1s-F8", 1 << 20, (1.05, 1.02), 1, 1001, slack=True),
+    3: ConfigSpec(3, "training-512p-4s-F16", 1 << 22, (1.02, 1.05), 2, 1002),
+    4: ConfigSpec(4, "packed-4096p-8s-F16", 1 << 18, (1.05,), 3, 1003, slack=True),
+    5: ConfigSpec(5, "unpacked-65536k-16s-F16", 1 << 14, (1.05,), 4, 1004, slack=True),
+}
+
+
+def quantize(x) -> np.ndarray:
+    """Round to the Q grid (half to even), at least one grid step, as float32."""
+    v = np.maximum(Q, np.round(np.asarray(x, dtype=np.float64) / Q) * Q)
+    return v.astype(np.float32)
+
+
+def level_ratios(num_levels: int) -> np.ndarray:
+    if num_levels == 1:
+        return np.ones(1)
+    return 0.5 + 0.5 * np.arange(num_levels) / (num_levels - 1)
+
+
+def pack_tables(rng: np.random.Generator, num_packs: int, num_levels: int,
+                median_us: float, sigma: float):
+    """Per-pack latency/energy tables, non-increasing in level (faster at higher level)."""
+    t_max = rng.lognormal(math.log(median_us), sigma, num_packs)
+    a = rng.random(num_packs)
+    r = level_ratios(num_levels)
+    t = quantize(t_max[:, None] * (a[:, None] / r[None, :] + 1.0 - a[:, None]))
+    e = (C_DYN * (r[None, :] ** 3) * t.astype(np.float64)).astype(np.float32)
+    return t, e
+
+
+def host_durations(rng: np.random.Generator, n: int) -> np.ndarray:
+    return quantize(rng.lognormal(math.log(10.0), 0.5, n))
+
+
+class _Builder:
+    def __init__(self):
+        self.pack_of: list[int] = []
+        self.stream_of: list[int] = []
+        self.src: list[int] = []
+        self.dst: list[int] = []
+
+    def node(self, pack: int = -1, stream: int = -1) -> int:
+        self.pack_of.append(pack)
+        self.stream_of.append(stream)
+        return len(self.pack_of) - 1
+
+    def edge(self, a: int, b: int) -> None:
+        self.src.append(a)
+        self.dst.append(b)
+
+
+def _cross_source(rng, pack_node, pack_stream, p, s):
+    """Uniformly random earlier pack on another stream than `s`, or None."""
+    earlier = np.nonzero(pack_stream[:p] != s)[0]
+    if earlier.size == 0:
+        return None
+    return int(pack_node[int(earlier[rng.integers(0, earlier.size)])])
+
+
+def _finish(b: _Builder, name, durations_fixed, t, e, static_power=STATIC_POWER) -> Graph:
+    V = len(b.pack_of)
+    node_pack = np.asarray(b.pack_of, dtype=np.int32)
+    dur = np.zeros(V, dtype=np.float32)
+    fixed = np.nonzero(node_pack < 0)[0]
+    dur[fixed] = durations_fixed
+    src = np.asarray(b.src, dtype=np.int32)
+    dst = np.asarray(b.dst, dtype=np.int32)
+    # drop duplicates (a cross edge may repeat a stream edge); keep first-seen order
+    key = src.astype(np.int64) * V + dst
+    _, first = np.unique(key, return_index=True)
+    keep = np.sort(first)
+    return Graph(name=name, num_nodes=V, edge_src=src[keep], edge_dst=dst[keep],
+                 node_pack=node_pack, node_duration=dur, num_packs=int(t.shape[0]),
+                 num_levels=int(t.shape[1]), pack_time=np.ascontiguousarray(t),
+                 pack_energy=np.ascontiguousarray(e), static_power=float(static_power),
+                 node_stream=np.asarray(b.stream_of, dtype=np.int32))
+
+
+def _launch_graph(seed, name, P, S, F, packs_per_host, cross_p, n_cross_exact,
+                  median_us, sigma, stream_mod=False) -> Graph:
+    """Host launch chain H_0 -> H_1 -> ..., each H_h launching `packs_per_host` packs;
+    stream-order chains; cross-stream edges."""
+    rng = np.random.default_rng(seed)
+    if stream_mod:
+        pack_stream = np.arange(P) % S
+    else:
+        pack_stream = rng.integers(0, S, P)
+    # cross edges: target pack -> source pack
+    cross = {}
+    if n_cross_exact is not None:
+        cand = [p for p in range(P) if np.any(pack_stream[:p] != pack_stream[p])]
+        targets = rng.choice(np.asarray(cand), size=n_cross_exact, replace=False)
+        for p in sorted(int(x) for x in targets):
+            cross[p] = None
+    else:
+        hit = rng.random(P) < cross_p
+        for p in np.nonzero(hit)[0]:
+            cross[int(p)] = None
+    H = P // packs_per_host
+    hdur = host_durations(rng, H)
+    t, e = pack_tables(rng, P, F, median_us, sigma)
+
+    b = _Builder()
+    pack_node = np.zeros(P, dtype=np.int64)
+    last_on_stream = {}
+    prev_host = None
+    p = 0
+    for h in range(H):
+        hn = b.node()
+        if prev_host is not None:
+            b.edge(prev_host, hn)
+        prev_host = hn
+        for _ in range(packs_per_host):
+            s = int(pack_stream[p])
+            pn = b.node(pack=p, stream=s)
+            pack_node[p] = pn
+            b.edge(hn, pn)
+            if s in last_on_stream:
+                b.edge(last_on_stream[s], pn)
+            last_on_stream[s] = pn
+            p += 1
+    # cross-stream event edges, drawn after the structure so the draw order is fixed
+    for p in sorted(cross):
+        src = _cross_source(rng, pack_node, pack_stream, p, int(pack_stream[p]))
+        if src is not None:
+            b.edge(src, int(pack_node[p]))
+    return _finish(b, name, hdur, t, e)
+
+
+def _packed_graph(seed, name, P=4096, S=8, F=16, sync_every=256, cross_p=0.03) -> Graph:
+    """Packs on S streams with periodic all-stream synchronisation nodes; no host nodes."""
+    rng = np.random.default_rng(seed)
+    pack_stream = rng.integers(0, S, P)
+    hit = rng.random(P) < cross_p
+    n_sync = P // sync_every
+    sdur = host_durations(rng, n_sync)
+    t, e = pack_tables(rng, P, F, 50.0, 1.0)
+
+    b = _Builder()
+    pack_node = np.zeros(P, dtype=np.int64)
+    last_on_stream: dict = {}
+    last_sync = None
+    for p in range(P):
+        s = int(pack_stream[p])
+        pn = b.node(pack=p, stream=s)
+        pack_node[p] = pn
+        if last_on_stream.get(s) is not None:
+            b.edge(last_on_stream[s], pn)
+        elif last_sync is not None:
+            b.edge(last_sync, pn)
+        last_on_stream[s] = pn
+        if (p + 1) % sync_every == 0:
+            sn = b.node()
+            for s2 in range(S):
+                if last_on_stream.get(s2) is not None:
+                    b.edge(last_on_stream[s2], sn)
+                last_on_stream[s2] = None
+            last_sync = sn
+    for p in np.nonzero(hit)[0]:
+        src = _cross_source(rng, pack_node, pack_stream, int(p), int(pack_stream[p]))
+        if src is not None:
+            b.edge(src, int(pack_node[p]))
+    return _finish(b, name, sdur, t, e)
+
+
+def config_graph(k: int) -> Graph:
+    """The execution graph and tables of benchmark workload `k` (1..5)."""
+    spec = CONFIGS[k]
+    if k == 1:
+        return _launch_graph(spec.seed, spec.name, P=8, S=2, F=4, packs_per_host=2,
+                             cross_p=None, n_cross_exact=2, median_us=50.0, sigma=1.0,
+                             stream_mod=True)
+    if k == 2:
+        return _launch_graph(spec.seed, spec.name, P=64, S=1, F=8, packs_per_host=1,
+                             cross_p=0.0, n_cross_exact=None, median_us=50.0, sigma=1.0)
+    if k == 3:
+        return _launch_graph(spec.seed, spec.name, P=512, S=4, F=16, packs_per_host=1,
+                             cross_p=0.05, n_cross_exact=None, median_us=50.0, sigma=1.0)
+    if k == 4:
+        return _packed_graph(spec.seed, spec.name)
+    if k == 5:
+        return _launch_graph(spec.seed, spec.name, P=65536, S=16, F=16, packs_per_host=1,
+                             cross_p=0.0, n_cross_exact=None, median_us=8.0, sigma=1.2)
+    raise ValueError(f"unknown config {k}")
+
+
+# ----------------------------------------------------------------------------- policies
+
+def exhaustive_policies(num_packs: int, num_levels: int, start: int, count: int) -> np.ndarray:
+    """Rows start..start+count of the full policy space in mixed radix, pack 0 least significant."""
+    c = np.arange(start, start + count, dtype=np.int64)
+    out = np.empty((count, num_packs), dtype=np.uint8)
+    for p in range(num_packs):
+        out[:, p] = (c // (num_levels ** p)) % num_levels
+    return out
+
+
+def _chunk(seed: int, chunk: int, rows: int, P: int, F: int, dist: str) -> np.ndarray:
+    rng = np.random.default_rng([seed, chunk])
+    if F == 1:
+        return np.zeros((rows, P), dtype=np.uint8)
+    if dist == "uniform":
+        return rng.integers(0, F, size=(rows, P), dtype=np.uint8)
+    if dist != "mixture":
+        raise ValueError(dist)
+    # mixture: candidate c lowers each pack independently with probability rho_c ~ U(0,1) to a
+    # uniform level in [0, F-2], else keeps it at F-1.  Given u < rho, u/rho is U(0,1).
+    rho = rng.random(rows, dtype=np.float32)[:, None]
+    u = rng.random((rows, P), dtype=np.float32)
+    low = np.minimum(np.floor(u / np.maximum(rho, 1e-30) * (F - 1)), F - 2).astype(np.uint8)
+    return np.where(u < rho, low, np.uint8(F - 1)).astype(np.uint8)
+
+
+def random_policies(seed: int, num_packs: int, num_levels: int, start: int, count: int,
+                    dist: str = "mixture") -> np.ndarray:
+    """Rows start..start+count of a seeded policy batch; row 0 is the all-max policy."""
+    out = np.empty((count, num_packs), dtype=np.uint8)
+    r = start
+    while r < start + count:
+        ch = r // POLICY_CHUNK
+        lo = ch * POLICY_CHUNK
+        hi = min(lo + POLICY_CHUNK, start + count)
+        blk = _chunk(seed, ch, POLICY_CHUNK, num_packs, num_levels, dist)
+        out[r - start:hi - start] = blk[r - lo:hi - lo]
+        r = hi
+    if start == 0 and count > 0:
+        out[0, :] = num_levels - 1
+    return out
+
+
+def iter_policy_chunks(k: int, graph: Graph, dist: str = "mixture",
+                       rows: int | None = None) -> Iterator[tuple[int, np.ndarray]]:
+    """Yield (start_row, block) over the whole candidate batch of workload `k`."""
+    spec = CONFIGS[k]
+    B = spec.num_candidates if rows is None else rows
+    step = POLICY_CHUNK
+    for s in range(0, B, step):
+        n = min(step, B - s)
+        yield s, config_policies(k, graph, s, n, dist)
+
+
+def config_policies(k: int, graph: Graph, start: int = 0, count: int | None = None,
+                    dist: str = "mixture") -> np.ndarray:
+    spec = CONFIGS[k]
+    if count is None:
+        count = spec.num_candidates - start
+    if spec.exhaustive:
+        return exhaustive_policies(graph.num_packs, graph.num_levels, start, count)
+    return random_policies(spec.policy_seed, graph.num_packs, graph.num_levels, start, count, dist)
+
+
+def sample_rows(num_candidates: int, n: int, seed: int = 7) -> np.ndarray:
+    """A seeded sample of candidate rows that always includes the first and last rows."""
+    rng = np.random.default_rng(seed)
+    n = min(n, num_candidates)
+    rows = set([0, num_candidates - 1])
+    if num_candidates > 2:
+        rows.update(int(x) for x in rng.choice(num_candidates, size=n, replace=False))
+    return np.asarray(sorted(rows), dtype=np.int64)
+
+
+# ----------------------------------------------------------------------------- small graphs
+
+def random_dag(rng: np.random.Generator, num_nodes: int, edge_prob: float, pack_frac: float,
+               num_levels: int, on_grid: bool = True, shuffle_ids: bool = True,
+               shuffle_packs: bool = True, name: str = "random") -> Graph:
+    """A random DAG with random node numbering and pack numbering.
+
+    Tables are non-increasing in level.  With `on_grid` every time is a multiple of Q.
+    """
+    V = num_nodes
+    order = rng.permutation(V) if shuffle_ids else np.arange(V)
+    src, dst = [], []
+    for i in range(V):
+        for j in range(i + 1, V):
+            if rng.random() < edge_prob:
+                src.append(int(order[i]))
+                dst.append(int(order[j]))
+    is_pack = rng.random(V) < pack_frac
+    pack_nodes = np.nonzero(is_pack)[0]
+    P = int(pack_nodes.size)
+    pids = rng.permutation(P) if shuffle_packs else np.arange(P)
+    node_pack = np.full(V, -1, dtype=np.int32)
+    node_pack[pack_nodes] = pids
+    if on_grid:
+        dur = quantize(rng.uniform(0.5, 40.0, V))
+        raw = rng.uniform(0.5, 60.0, (P, num_levels))
+        t = np.sort(quantize(raw), axis=1)[:, ::-1].copy()
+    else:
+        dur = rng.uniform(0.1, 40.0, V).astype(np.float32)
+        t = np.sort(rng.uniform(0.1, 60.0, (P, num_levels)).astype(np.float32), axis=1)[:, ::-1].copy()
+    dur[node_pack >= 0] = 0.0
+    e = np.sort(rng.uniform(0.0, 5.0, (P, num_levels)).astype(np.float32), axis=1).copy()
+    return Graph(name=name, num_nodes=V, edge_src=np.asarray(src, dtype=np.int32),
+                 edge_dst=np.asarray(dst, dtype=np.int32), node_pack=node_pack,
+                 node_duration=dur.astype(np.float32), num_packs=P, num_levels=num_levels,
+                 pack_time=np.ascontiguousarray(t, dtype=np.float32),
+                 pack_energy=np.ascontiguousarray(e, dtype=np.float32),
+                 static_power=float(np.float32(rng.uniform(0.0, 1.0))))
