@@ -1,0 +1,193 @@
+"""Benchmark: batched what-if evaluation of DVFS frequency policies on one MI355X.
+
+One step is the whole hot path over one batch of candidate policies of the inference-like
+workload (64 packs on one stream, 64 host launch nodes, 8 frequency levels, 2^20 candidates):
+  emo_slack               forward pass (finish times, makespan, energy) + backward pass
+                          (latest finish times, slack of every pack) for every candidate
+  emo_select_from_results feasibility mask and least-energy feasible candidate under the
+                          latency target 1.05 x the all-max makespan
+Inputs are resident in HBM before timing starts; level batches rotate over several copies so
+that the 256 MB last-level cache does not hold them across steps.
+
+Prints one JSON line.  `value` is candidate policies fully evaluated per second.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "candidate policies evaluated/sec (timing+energy+select); % of VALU/HBM roofline"
+HBM_PEAK_GBS = 8000.0
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in ("emo_kernels.hip", "emo_internal.h", "emo_host.cpp"):
+        with open(os.path.join(ROOT, "paper_2607_12324_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload_name: str, kernel: str, src_hash: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None when the
+    kernel changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_name}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("source_hash") != src_hash:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(k: int, budget_s: float = 12.0):
+    """The oracle (plain fp64 C, one thread) on a bounded prefix of the same workload: makespan
+    and energy, slack of every pack and the selection, per candidate."""
+    import numpy as np
+
+    import oracle
+    from paper_2607_12324_amd import synth
+    oracle.build()
+    g = synth.config_graph(k)
+    n = 2048
+    rows = synth.config_policies(k, g, 0, n)
+    t0 = time.perf_counter()
+    done = 0
+    while True:
+        T, E = oracle.eval_batch(g, rows, nthreads=1)
+        for c in range(n):
+            oracle.pack_slack(g, rows[c])
+        oracle.select(T, E, float(np.float32(1.05 * T[0])))
+        done += n
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "policies/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} candidates of the same batch, repeated {done // n}x for {dt:.1f} s "
+                      f"(eval + pack slack + select, fp64 C, 1 thread)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, help="benchmark workload 1..5 (default 2)")
+    ap.add_argument("--copies", type=int, default=5, help="rotated copies of the level batch")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build evaluates candidate policies on a single "
+              "MI355X (candidates would shard across GPUs with one MIN all-reduce of the "
+              "selection key; that path is not built).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_12324_amd import emo, synth
+
+    k = args.workload
+    spec = synth.CONFIGS[k]
+    g = synth.config_graph(k)
+    B = spec.num_candidates
+    P = g.num_packs
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    if spec.exhaustive:
+        rows = synth.config_policies(k, g)
+        rows = np.ascontiguousarray(rows[::-1])   # all-max row first
+    else:
+        rows = synth.random_policies_parallel(spec.policy_seed, P, g.num_levels, B, workers=8)
+    copies = max(1, args.copies if B * P < (1 << 30) else 1)
+    lv = [torch.from_numpy(rows).to(dev)]
+    for _ in range(copies - 1):
+        lv.append(lv[0].clone())
+    del rows
+    gh = emo.EmoGraph(g, device=0)
+    stream = torch.cuda.current_stream()
+    T = torch.empty(B, dtype=torch.float32, device=dev)
+    E = torch.empty(B, dtype=torch.float32, device=dev)
+    S = torch.empty((B, P), dtype=torch.float32, device=dev)
+    mask = torch.empty((B + 31) // 32, dtype=torch.int32, device=dev)
+    res = torch.empty(3, dtype=torch.int64, device=dev)
+    T0, _ = gh.eval_policies(lv[0][:1])
+    target = float(np.float32(spec.targets[0] * float(T0.item())))
+
+    def step(i):
+        x = lv[i % copies]
+        gh.slack(x, out=S, makespan=T, energy=E)
+        emo.select_from_results(T, E, target, mask=mask, result=res)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        x = lv[i % copies]
+        ev[i][0].record(stream)
+        gh.slack(x, out=S, makespan=T, energy=E)
+        ev[i][1].record(stream)
+        emo.select_from_results(T, E, target, mask=mask, result=res)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+    slack_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    sel = emo.parse_selection(res)
+
+    value = B / (ms_step / 1e3)
+    algo_bytes = B * (P + 4 * P + 8)          # level bytes in; slack, makespan, energy out
+    achieved = algo_bytes / (slack_ms / 1e3) / 1e9
+    src_hash = kernel_source_hash()
+    traffic = measured_traffic(spec.name, "slack_kernel", src_hash)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "policies/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": spec.name, "candidates": B, "nodes": g.num_nodes,
+                   "edges": g.num_edges, "packs": P, "levels": g.num_levels,
+                   "target_ratio": spec.targets[0], "step": "emo_slack + emo_select_from_results",
+                   "rotated_input_copies": copies},
+        "roofline": {"bound": "hbm", "kernel": "slack_kernel", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "algorithmic_bytes_per_launch": algo_bytes,
+                     "launch_ms": slack_ms},
+        "wall_s": wall,
+        "selected": {"index": sel.index, "energy": sel.energy, "makespan": sel.makespan,
+                     "num_feasible": sel.num_feasible},
+        "kernel_source_hash": src_hash,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(k)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,177 @@
+/*
+ * emo.h -- C ABI of an MI355X (gfx950) library for EMO's batched what-if evaluation of DVFS
+ * frequency policies over an execution graph.
+ *
+ * Paper: "EMO: Energy Efficiency Modeling and Optimization for AI Workloads".
+ *   The execution graph G = (V, E) and its precedence edges: Sec. IV-C (what-if analysis).
+ *   Completion time, makespan and energy: Sec. IV-C, Eq. 1 and Eq. 2.
+ *   Frequency-dependent node cost from per-pack latency/energy tables: Eq. 3, Sec. IV-E Eq. 7,
+ *   Alg. 1 (packs take T_f/E_f at their frequency, other nodes keep a fixed duration and no
+ *   energy).
+ *   The constrained problem (minimum energy subject to a latency target): Eq. 4.
+ *   Slack (time in which a kernel is off the critical path): Sec. I and Sec. IV-D.
+ *
+ * Model computed for one candidate policy (one frequency level per pack):
+ *   dur(v)  = pack_time[p][l_p]   if node v is pack p, else node_duration[v]
+ *   EST(v)  = 0 for a node without predecessors, else max over predecessors k of EFT(k)
+ *   EFT(v)  = EST(v) + dur(v)
+ *   T       = max over v of EFT(v)                                   (makespan)
+ *   E       = sum over packs p of pack_energy[p][l_p] + static_power * T
+ *   LFT(v)  = T for a node without successors, else min over successors u of LFT(u) - dur(u)
+ *   slack(v)= LFT(v) - EFT(v)
+ *   feasible= T <= latency_target
+ *   selected= the feasible candidate of least E, the lower index on equal E; -1 if none.
+ *
+ * Arithmetic is IEEE fp32 with round-to-nearest-even for times; the pack-energy sum is
+ * accumulated in fp32 blocks of at most 64 packs added into an fp64 total, then rounded to fp32.
+ *
+ * Units are the caller's (the tests use microseconds and power units with energy =
+ * power * time).  Level F-1 is conventionally the maximum frequency; nothing here depends on it.
+ *
+ * Memory: "host" pointers are ordinary CPU memory; "device" pointers are device memory of the
+ * GPU the graph was loaded on (e.g. a torch CUDA tensor's data_ptr()).  The caller owns every
+ * buffer.  Batch calls are asynchronous on `stream` (a hipStream_t; NULL means the default
+ * stream): the caller keeps inputs and outputs alive until the stream has completed.  Scratch
+ * device memory, when a call needs it, is taken with hipMallocAsync on the same stream.
+ *
+ * Errors: every entry point returns an emo_status.  Argument errors that the host can detect
+ * (sizes, null pointers, indices, non-finite or negative values, cycles, misaligned buffers)
+ * are reported synchronously and nothing is launched.  emo_last_error() returns a message for
+ * the last failure on the calling thread.  A level byte >= F in a candidate is not an error:
+ * that candidate's makespan, energy and slack are NaN and it is never feasible.
+ *
+ * Thread safety: a loaded graph is immutable; concurrent calls on different streams are safe.
+ */
+#ifndef EMO_H
+#define EMO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct emo_graph_s *emo_graph_t;
+
+typedef enum {
+    EMO_OK = 0,
+    EMO_ERR_INVALID_ARGUMENT = 1,
+    EMO_ERR_CYCLE = 2,
+    EMO_ERR_OUT_OF_MEMORY = 3,
+    EMO_ERR_DEVICE = 4,
+    EMO_ERR_UNSUPPORTED = 5
+} emo_status;
+
+/* Result of a selection (Eq. 4), written to device memory.  24 bytes, 8-byte aligned. */
+typedef struct {
+    int64_t index;          /* selected candidate, -1 when none is feasible */
+    float energy;           /* its energy, NaN when none */
+    float makespan;         /* its makespan, NaN when none */
+    int64_t num_feasible;   /* number of candidates with makespan <= target */
+} emo_selection;
+
+/* Facts about a loaded graph, for callers and tests. */
+typedef struct {
+    int32_t num_nodes;
+    int32_t num_edges;            /* after duplicate edges are merged */
+    int32_t num_packs;
+    int32_t num_levels;
+    int32_t num_dynamic_nodes;    /* packs and nodes with a pack ancestor */
+    int32_t num_dynamic_edges;    /* edges between dynamic nodes */
+    int32_t eval_slots;           /* finish-time slots the forward pass keeps live at once */
+    int32_t max_depth;            /* largest depth (longest path in edges) */
+    float const_makespan;         /* largest finish time among candidate-independent nodes */
+    int32_t device;               /* device ordinal, -1 for a host-only graph */
+    int32_t pack_order_monotone;  /* 1 if the kernels visit packs in increasing pack id */
+    int32_t reserved;
+} emo_graph_info;
+
+/*
+ * Load an execution graph and its pack tables (Sec. IV-C; Alg. 1 REQUIRE line).
+ *   num_nodes, num_edges  V >= 0, E >= 0.
+ *   edge_src, edge_dst    host int32 [E]: node edge_src[i] finishes before edge_dst[i] starts.
+ *                         Duplicates are merged.  A self-loop or cycle gives EMO_ERR_CYCLE.
+ *   node_pack             host int32 [V]: pack id in [0, P) or -1 for a fixed node.  Every pack
+ *                         id in [0, P) must appear on exactly one node.
+ *   node_duration         host float [V]: duration of fixed nodes, finite and >= 0 (ignored on
+ *                         pack nodes).
+ *   num_packs, num_levels P >= 0 packs, 1 <= F <= 256 frequency levels.
+ *   pack_time, pack_energy host float [P*F], row-major by pack: latency and energy of pack p at
+ *                         level l at index p*F + l; finite and >= 0.
+ *   static_power          finite, >= 0: energy per unit time charged over the makespan (the
+ *                         idle-energy term of Eq. 2 / Alg. 1).
+ *   device                GPU ordinal to hold the graph, or -1 for a host-only graph (analysis
+ *                         and emo_graph_topo_order only; batch calls then fail with
+ *                         EMO_ERR_UNSUPPORTED).
+ *   out                   receives the handle; the library deep-copies every input.
+ */
+emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *edge_src,
+                          const int32_t *edge_dst, const int32_t *node_pack,
+                          const float *node_duration, int32_t num_packs, int32_t num_levels,
+                          const float *pack_time, const float *pack_energy, float static_power,
+                          int32_t device, emo_graph_t *out);
+
+/* Release a graph and its device memory.  NULL is accepted.  Work still queued on a stream
+ * that uses the graph must have completed. */
+emo_status emo_free_graph(emo_graph_t g);
+
+/* Fill `info` (host). */
+emo_status emo_graph_get_info(emo_graph_t g, emo_graph_info *info);
+
+/*
+ * Canonical topological order (the traversal order of Alg. 1): nodes sorted by depth, then by
+ * node id, where depth is 0 for a node without predecessors and 1 + the largest predecessor
+ * depth otherwise.  order: host int32 [V]; depth: host int32 [V] or NULL.
+ */
+emo_status emo_graph_topo_order(emo_graph_t g, int32_t *order, int32_t *depth);
+
+/*
+ * Makespan and energy of B candidate policies (Eq. 1-3, Alg. 1 with one level per pack).
+ *   levels    device uint8 [B][P], row-major by candidate: level of pack p in candidate c at
+ *             c*P + p.
+ *   B         0 <= B < 2^32; B = 0 is a no-op.
+ *   makespan  device float [B];  energy  device float [B].  Either may be NULL.
+ */
+emo_status emo_eval_policies(emo_graph_t g, const uint8_t *levels, int64_t num_candidates,
+                             float *makespan, float *energy, void *stream);
+
+/*
+ * Slack of every pack (per_node = 0) or of every node (per_node = 1) for B candidates: the
+ * forward pass above followed by a backward pass in reverse topological order.
+ *   slack     device float, [B][P] indexed by pack id, or [B][V] indexed by node id.
+ *   makespan, energy  optional device float [B] outputs of the same forward pass (NULL to skip).
+ */
+emo_status emo_slack(emo_graph_t g, const uint8_t *levels, int64_t num_candidates, float *slack,
+                     int32_t per_node, float *makespan, float *energy, void *stream);
+
+/*
+ * Evaluate B candidates and select the least-energy one whose makespan is <= latency_target
+ * (Eq. 4 over the given candidate batch), ties to the lower index.
+ *   feasible_mask  device uint32 [ceil(B/32)] or NULL: bit (c % 32) of word c / 32 is set iff
+ *                  candidate c is feasible.
+ *   result         device emo_selection, 8-byte aligned.  It doubles as the reduction's
+ *                  accumulator while the call runs, so it must not alias another output.
+ */
+emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t num_candidates,
+                             float latency_target, uint32_t *feasible_mask,
+                             emo_selection *result, void *stream);
+
+/*
+ * The same selection from makespans and energies already computed (e.g. a second latency
+ * target over one evaluation).  makespan, energy: device float [B].
+ */
+emo_status emo_select_from_results(const float *makespan, const float *energy,
+                                   int64_t num_candidates, float latency_target,
+                                   uint32_t *feasible_mask, emo_selection *result, void *stream);
+
+/* Static string naming a status code. */
+const char *emo_status_string(emo_status s);
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char *emo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EMO_H */

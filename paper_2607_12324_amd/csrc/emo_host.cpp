@@ -1,0 +1,529 @@
+// Host side of the EMO policy-evaluation library: argument checking, graph analysis (merging
+// duplicate edges, Kahn topological sort with depths, cycle detection), folding of nodes whose
+// finish time does not depend on the candidate, compilation of the graph into kernel programs,
+// device upload, and the C ABI entry points declared in include/emo.h.
+//
+// The canonical topological order reported by emo_graph_topo_order sorts nodes by (depth, id)
+// (the traversal order of Alg. 1).  The kernels may walk any topological order: the forward
+// recurrence (Eq. 1) takes exact maxima and one rounded addition per node, so every
+// topological order yields bit-identical finish times.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <functional>
+#include <limits>
+#include <memory>
+#include <mutex>
+#include <new>
+#include <queue>
+#include <string>
+#include <vector>
+
+#include "emo.h"
+#include "emo_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+emo_status fail(emo_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+emo_status ok() {
+    g_last_error.clear();
+    return EMO_OK;
+}
+
+emo_status device_fail(hipError_t e, const char *where) {
+    return fail(EMO_ERR_DEVICE, "%s: %s", where, hipGetErrorString(e));
+}
+
+// Program compiled on the host before upload.
+struct HostProgram {
+    std::vector<emo::Op> op;
+    std::vector<int2> in_range;
+    std::vector<int32_t> ins;
+    std::vector<int2> succ_range;
+    std::vector<int32_t> succs;
+    std::vector<int32_t> out_col;
+    int32_t n_slots = 0;
+    float t_const = 0.f;
+    bool pack_monotone = true;
+};
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+    int prev = -1;
+    bool active = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) {
+            if (hipSetDevice(dev) == hipSuccess) active = true;
+        }
+    }
+    ~DeviceGuard() {
+        if (active) (void)hipSetDevice(prev);
+    }
+};
+
+}  // namespace
+
+struct emo_graph_s {
+    int32_t V = 0, E = 0, P = 0, F = 1;
+    float static_power = 0.f;
+    int32_t device = -1;
+    std::vector<int32_t> src, dst;           // merged edges
+    std::vector<int32_t> pack;
+    std::vector<float> dur;
+    std::vector<int32_t> pred_off, pred, succ_off, succ;
+    std::vector<int32_t> order, depth;       // canonical order, depths
+    std::vector<int32_t> kahn;               // a topological order (Kahn, FIFO)
+    std::vector<char> dyn;                   // depends on the candidate
+    std::vector<float> const_eft;            // finish time of candidate-independent nodes
+    float t_const = 0.f;
+    emo_graph_info info{};
+    std::vector<void *> allocations;         // device memory owned by the handle
+    emo::DevGraph dg;
+};
+
+namespace {
+
+// CSR adjacency: for each node, the list of `from` endpoints of edges ending there.
+void build_csr(int32_t V, const std::vector<int32_t> &from, const std::vector<int32_t> &to,
+               std::vector<int32_t> &off, std::vector<int32_t> &adj) {
+    off.assign(static_cast<size_t>(V) + 1, 0);
+    for (int32_t t : to) off[t + 1]++;
+    for (int32_t v = 0; v < V; ++v) off[v + 1] += off[v];
+    adj.assign(from.size(), 0);
+    std::vector<int32_t> fill(off.begin(), off.end() - 1);
+    for (size_t i = 0; i < from.size(); ++i) adj[fill[to[i]]++] = from[i];
+}
+
+// Kahn's algorithm (FIFO): a topological order and depths (longest path in edges).
+emo_status topo_sort(emo_graph_s &g) {
+    const int32_t V = g.V;
+    std::vector<int32_t> indeg(V, 0);
+    for (int32_t v = 0; v < V; ++v) indeg[v] = g.pred_off[v + 1] - g.pred_off[v];
+    g.kahn.clear();
+    g.kahn.reserve(V);
+    g.depth.assign(V, 0);
+    for (int32_t v = 0; v < V; ++v)
+        if (indeg[v] == 0) g.kahn.push_back(v);
+    for (size_t head = 0; head < g.kahn.size(); ++head) {
+        int32_t v = g.kahn[head];
+        for (int32_t j = g.succ_off[v]; j < g.succ_off[v + 1]; ++j) {
+            int32_t u = g.succ[j];
+            g.depth[u] = std::max(g.depth[u], g.depth[v] + 1);
+            if (--indeg[u] == 0) g.kahn.push_back(u);
+        }
+    }
+    if (static_cast<int32_t>(g.kahn.size()) != V)
+        return fail(EMO_ERR_CYCLE, "the graph has a cycle (%d of %d nodes are orderable)",
+                    static_cast<int>(g.kahn.size()), static_cast<int>(V));
+    // canonical order: stable bucket sort of node ids by depth
+    int32_t maxd = 0;
+    for (int32_t v = 0; v < V; ++v) maxd = std::max(maxd, g.depth[v]);
+    std::vector<int32_t> cnt(static_cast<size_t>(maxd) + 2, 0);
+    for (int32_t v = 0; v < V; ++v) cnt[g.depth[v] + 1]++;
+    for (int32_t d = 0; d <= maxd; ++d) cnt[d + 1] += cnt[d];
+    g.order.assign(V, 0);
+    for (int32_t v = 0; v < V; ++v) g.order[cnt[g.depth[v]]++] = v;
+    g.info.max_depth = V ? maxd : 0;
+    return EMO_OK;
+}
+
+// Marks candidate-dependent nodes and computes the fp32 finish times of the others.
+void fold_constants(emo_graph_s &g) {
+    const int32_t V = g.V;
+    g.dyn.assign(V, 0);
+    g.const_eft.assign(V, 0.f);
+    float tc = 0.f;
+    for (int32_t v : g.kahn) {
+        bool d = g.pack[v] >= 0;
+        float est = 0.f;
+        for (int32_t j = g.pred_off[v]; j < g.pred_off[v + 1]; ++j) {
+            int32_t k = g.pred[j];
+            if (g.dyn[k]) d = true;
+            else est = std::max(est, g.const_eft[k]);
+        }
+        g.dyn[v] = d;
+        if (!d) {
+            g.const_eft[v] = est + g.dur[v];
+            tc = std::max(tc, g.const_eft[v]);
+        }
+    }
+    g.t_const = tc;
+}
+
+uint32_t fbits(float x) {
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    return u;
+}
+
+// Compile a traversal.  fold: only candidate-dependent nodes become steps; backward: every step
+// keeps its own slot (needed for the reverse pass); per_node: slack columns are node ids.
+HostProgram build_program(const emo_graph_s &g, bool fold, bool backward, bool per_node) {
+    HostProgram hp;
+    const int32_t V = g.V;
+    auto included = [&](int32_t v) { return !fold || g.dyn[v]; };
+    // Kahn over included nodes; ready nodes are taken by (key, id) with key = pack id for packs
+    // and -1 for fixed nodes, so packs are visited in increasing pack id whenever the pack
+    // numbering is consistent with the precedence edges.
+    std::vector<int32_t> indeg(V, 0);
+    for (int32_t v = 0; v < V; ++v) {
+        if (!included(v)) continue;
+        for (int32_t j = g.pred_off[v]; j < g.pred_off[v + 1]; ++j)
+            if (included(g.pred[j])) indeg[v]++;
+    }
+    using Key = std::pair<int64_t, int32_t>;
+    std::priority_queue<Key, std::vector<Key>, std::greater<Key>> ready;
+    auto key = [&](int32_t v) -> int64_t { return g.pack[v] >= 0 ? g.pack[v] : -1; };
+    for (int32_t v = 0; v < V; ++v)
+        if (included(v) && indeg[v] == 0) ready.push({key(v), v});
+    std::vector<int32_t> seq;
+    while (!ready.empty()) {
+        int32_t v = ready.top().second;
+        ready.pop();
+        seq.push_back(v);
+        for (int32_t j = g.succ_off[v]; j < g.succ_off[v + 1]; ++j) {
+            int32_t u = g.succ[j];
+            if (included(u) && --indeg[u] == 0) ready.push({key(u), u});
+        }
+    }
+    const int32_t n = static_cast<int32_t>(seq.size());
+    std::vector<int32_t> pos(V, -1);
+    for (int32_t i = 0; i < n; ++i) pos[seq[i]] = i;
+
+    // last step that reads each node's finish time
+    std::vector<int32_t> last_use(V, -1);
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t v = seq[i];
+        for (int32_t j = g.pred_off[v]; j < g.pred_off[v + 1]; ++j) {
+            int32_t k = g.pred[j];
+            if (included(k)) last_use[k] = std::max(last_use[k], i);
+        }
+    }
+    std::vector<int32_t> slot(V, -1);
+    std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> free_slots;
+    int32_t next_slot = 0;
+    int32_t last_pack = -1;
+    hp.op.resize(n);
+    hp.in_range.resize(n);
+    hp.out_col.resize(n, -1);
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t v = seq[i];
+        float cst = 0.f;
+        int32_t begin = static_cast<int32_t>(hp.ins.size());
+        std::vector<int32_t> released;
+        for (int32_t j = g.pred_off[v]; j < g.pred_off[v + 1]; ++j) {
+            int32_t k = g.pred[j];
+            if (included(k)) {
+                hp.ins.push_back(backward ? pos[k] : slot[k]);
+                if (!backward && last_use[k] == i) released.push_back(slot[k]);
+            } else {
+                cst = std::max(cst, g.const_eft[k]);
+            }
+        }
+        hp.in_range[i] = make_int2(begin, static_cast<int32_t>(hp.ins.size()));
+        for (int32_t s : released) free_slots.push(s);
+        int32_t out = -1;
+        if (backward) {
+            out = i;
+        } else if (last_use[v] >= 0) {
+            if (!free_slots.empty()) {
+                out = free_slots.top();
+                free_slots.pop();
+            } else {
+                out = next_slot++;
+            }
+            slot[v] = out;
+        }
+        emo::Op op;
+        op.pack = g.pack[v];
+        op.cst = fbits(cst);
+        op.dur = fbits(g.pack[v] >= 0 ? 0.f : g.dur[v]);
+        op.out = out;
+        hp.op[i] = op;
+        if (per_node) hp.out_col[i] = v;
+        else hp.out_col[i] = g.pack[v];
+        if (g.pack[v] >= 0) {
+            if (g.pack[v] < last_pack) hp.pack_monotone = false;
+            last_pack = g.pack[v];
+        }
+    }
+    hp.n_slots = backward ? n : next_slot;
+    hp.t_const = fold ? g.t_const : 0.f;
+    if (backward) {
+        hp.succ_range.resize(n);
+        for (int32_t i = 0; i < n; ++i) {
+            int32_t v = seq[i];
+            int32_t begin = static_cast<int32_t>(hp.succs.size());
+            for (int32_t j = g.succ_off[v]; j < g.succ_off[v + 1]; ++j) {
+                int32_t u = g.succ[j];
+                if (included(u)) hp.succs.push_back(pos[u]);
+            }
+            hp.succ_range[i] = make_int2(begin, static_cast<int32_t>(hp.succs.size()));
+        }
+    }
+    return hp;
+}
+
+template <typename T>
+emo_status upload(emo_graph_s &g, const std::vector<T> &host, const T **dev) {
+    size_t bytes = std::max<size_t>(host.size() * sizeof(T), 16);
+    void *p = nullptr;
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess) return fail(EMO_ERR_OUT_OF_MEMORY, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+    g.allocations.push_back(p);
+    if (!host.empty()) {
+        e = hipMemcpy(p, host.data(), host.size() * sizeof(T), hipMemcpyHostToDevice);
+        if (e != hipSuccess) return device_fail(e, "hipMemcpy");
+    }
+    *dev = static_cast<const T *>(p);
+    return EMO_OK;
+}
+
+emo_status upload_program(emo_graph_s &g, const HostProgram &hp, emo::DevProgram &dp) {
+    dp.n_ops = static_cast<int32_t>(hp.op.size());
+    dp.n_slots = hp.n_slots;
+    dp.t_const = hp.t_const;
+    emo_status s;
+    if ((s = upload(g, hp.op, &dp.op)) != EMO_OK) return s;
+    if ((s = upload(g, hp.in_range, &dp.in_range)) != EMO_OK) return s;
+    if ((s = upload(g, hp.ins, &dp.ins)) != EMO_OK) return s;
+    if ((s = upload(g, hp.out_col, &dp.out_col)) != EMO_OK) return s;
+    if (!hp.succ_range.empty() || dp.n_ops == 0) {
+        if ((s = upload(g, hp.succ_range, &dp.succ_range)) != EMO_OK) return s;
+        if ((s = upload(g, hp.succs, &dp.succs)) != EMO_OK) return s;
+    }
+    return EMO_OK;
+}
+
+void release_device(emo_graph_s *g) {
+    if (g->device >= 0) {
+        DeviceGuard guard(g->device);
+        for (void *p : g->allocations) (void)hipFree(p);
+    }
+    g->allocations.clear();
+}
+
+bool finite_nonneg(float x) { return std::isfinite(x) && x >= 0.f; }
+
+emo_status check_batch(emo_graph_t g, int64_t B) {
+    if (!g) return fail(EMO_ERR_INVALID_ARGUMENT, "graph handle is NULL");
+    if (g->device < 0) return fail(EMO_ERR_UNSUPPORTED, "graph was loaded host-only (device -1)");
+    if (B < 0 || B >= (int64_t(1) << 32))
+        return fail(EMO_ERR_INVALID_ARGUMENT, "num_candidates %lld outside [0, 2^32)", (long long)B);
+    return EMO_OK;
+}
+
+emo_status after_launch(hipError_t e, const char *what) {
+    if (e != hipSuccess) return device_fail(e, what);
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *emo_status_string(emo_status s) {
+    switch (s) {
+        case EMO_OK: return "EMO_OK";
+        case EMO_ERR_INVALID_ARGUMENT: return "EMO_ERR_INVALID_ARGUMENT";
+        case EMO_ERR_CYCLE: return "EMO_ERR_CYCLE";
+        case EMO_ERR_OUT_OF_MEMORY: return "EMO_ERR_OUT_OF_MEMORY";
+        case EMO_ERR_DEVICE: return "EMO_ERR_DEVICE";
+        case EMO_ERR_UNSUPPORTED: return "EMO_ERR_UNSUPPORTED";
+    }
+    return "EMO_ERR_UNKNOWN";
+}
+
+const char *emo_last_error(void) { return g_last_error.c_str(); }
+
+emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *edge_src,
+                          const int32_t *edge_dst, const int32_t *node_pack,
+                          const float *node_duration, int32_t num_packs, int32_t num_levels,
+                          const float *pack_time, const float *pack_energy, float static_power,
+                          int32_t device, emo_graph_t *out) {
+    if (!out) return fail(EMO_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    const int32_t V = num_nodes, E = num_edges, P = num_packs, F = num_levels;
+    if (V < 0 || E < 0 || P < 0) return fail(EMO_ERR_INVALID_ARGUMENT, "negative size");
+    if (F < 1 || F > 256) return fail(EMO_ERR_INVALID_ARGUMENT, "num_levels %d outside [1, 256]", F);
+    if (P > V) return fail(EMO_ERR_INVALID_ARGUMENT, "more packs (%d) than nodes (%d)", P, V);
+    if (E > 0 && (!edge_src || !edge_dst)) return fail(EMO_ERR_INVALID_ARGUMENT, "edge arrays are NULL");
+    if (V > 0 && (!node_pack || !node_duration)) return fail(EMO_ERR_INVALID_ARGUMENT, "node arrays are NULL");
+    if (P > 0 && (!pack_time || !pack_energy)) return fail(EMO_ERR_INVALID_ARGUMENT, "table arrays are NULL");
+    if (int64_t(P) * F > (int64_t(1) << 28)) return fail(EMO_ERR_INVALID_ARGUMENT, "tables too large");
+    if (!finite_nonneg(static_power)) return fail(EMO_ERR_INVALID_ARGUMENT, "static_power must be finite and >= 0");
+    if (device < -1) return fail(EMO_ERR_INVALID_ARGUMENT, "device %d", device);
+    if (device >= 0) {
+        int n = 0;
+        hipError_t e = hipGetDeviceCount(&n);
+        if (e != hipSuccess || device >= n)
+            return fail(EMO_ERR_DEVICE, "device %d not available (%d devices)", device, n);
+    }
+    for (int32_t i = 0; i < E; ++i) {
+        if (edge_src[i] < 0 || edge_src[i] >= V || edge_dst[i] < 0 || edge_dst[i] >= V)
+            return fail(EMO_ERR_INVALID_ARGUMENT, "edge %d (%d -> %d) out of range", i, edge_src[i], edge_dst[i]);
+        if (edge_src[i] == edge_dst[i]) return fail(EMO_ERR_CYCLE, "self-loop on node %d", edge_src[i]);
+    }
+    std::vector<int32_t> seen(P, 0);
+    for (int32_t v = 0; v < V; ++v) {
+        int32_t p = node_pack[v];
+        if (p < -1 || p >= P) return fail(EMO_ERR_INVALID_ARGUMENT, "node %d has pack id %d outside [-1, %d)", v, p, P);
+        if (p >= 0) {
+            if (seen[p]++) return fail(EMO_ERR_INVALID_ARGUMENT, "pack %d appears on more than one node", p);
+        } else if (!finite_nonneg(node_duration[v])) {
+            return fail(EMO_ERR_INVALID_ARGUMENT, "node %d duration must be finite and >= 0", v);
+        }
+    }
+    for (int32_t p = 0; p < P; ++p)
+        if (!seen[p]) return fail(EMO_ERR_INVALID_ARGUMENT, "pack %d is on no node", p);
+    for (int64_t i = 0; i < int64_t(P) * F; ++i)
+        if (!finite_nonneg(pack_time[i]) || !finite_nonneg(pack_energy[i]))
+            return fail(EMO_ERR_INVALID_ARGUMENT, "table entry %lld must be finite and >= 0", (long long)i);
+
+    emo_graph_s *g = new (std::nothrow) emo_graph_s();
+    if (!g) return fail(EMO_ERR_OUT_OF_MEMORY, "host allocation");
+    std::unique_ptr<emo_graph_s, void (*)(emo_graph_s *)> holder(g, [](emo_graph_s *x) {
+        release_device(x);
+        delete x;
+    });
+    g->V = V; g->P = P; g->F = F; g->static_power = static_power; g->device = device;
+    g->pack.assign(node_pack, node_pack + V);
+    g->dur.assign(node_duration, node_duration + V);
+    for (int32_t v = 0; v < V; ++v)
+        if (g->pack[v] >= 0) g->dur[v] = 0.f;
+    // merge duplicate edges
+    {
+        std::vector<int64_t> keys(E);
+        for (int32_t i = 0; i < E; ++i) keys[i] = int64_t(edge_src[i]) * V + edge_dst[i];
+        std::sort(keys.begin(), keys.end());
+        keys.erase(std::unique(keys.begin(), keys.end()), keys.end());
+        g->src.resize(keys.size());
+        g->dst.resize(keys.size());
+        for (size_t i = 0; i < keys.size(); ++i) {
+            g->src[i] = static_cast<int32_t>(keys[i] / V);
+            g->dst[i] = static_cast<int32_t>(keys[i] % V);
+        }
+        g->E = static_cast<int32_t>(keys.size());
+    }
+    build_csr(V, g->src, g->dst, g->pred_off, g->pred);
+    build_csr(V, g->dst, g->src, g->succ_off, g->succ);
+    emo_status s = topo_sort(*g);
+    if (s != EMO_OK) return s;
+    fold_constants(*g);
+
+    HostProgram pe = build_program(*g, true, false, false);
+    HostProgram ps = build_program(*g, true, true, false);
+    HostProgram pn = build_program(*g, false, true, true);
+
+    emo_graph_info &in = g->info;
+    in.num_nodes = V; in.num_edges = g->E; in.num_packs = P; in.num_levels = F;
+    in.num_dynamic_nodes = static_cast<int32_t>(pe.op.size());
+    in.num_dynamic_edges = static_cast<int32_t>(pe.ins.size());
+    in.eval_slots = pe.n_slots;
+    in.const_makespan = g->t_const;
+    in.device = device;
+    in.pack_order_monotone = pe.pack_monotone ? 1 : 0;
+
+    if (device >= 0) {
+        DeviceGuard guard(device);
+        std::vector<float2> tab(static_cast<size_t>(P) * F);
+        for (size_t i = 0; i < tab.size(); ++i) tab[i] = make_float2(pack_time[i], pack_energy[i]);
+        g->dg.V = V; g->dg.P = P; g->dg.F = F; g->dg.static_power = static_power;
+        if ((s = upload(*g, tab, &g->dg.tab)) != EMO_OK) return s;
+        if ((s = upload_program(*g, pe, g->dg.eval)) != EMO_OK) return s;
+        if ((s = upload_program(*g, ps, g->dg.slack_pack)) != EMO_OK) return s;
+        if ((s = upload_program(*g, pn, g->dg.slack_node)) != EMO_OK) return s;
+    }
+    *out = holder.release();
+    return ok();
+}
+
+emo_status emo_free_graph(emo_graph_t g) {
+    if (!g) return ok();
+    release_device(g);
+    delete g;
+    return ok();
+}
+
+emo_status emo_graph_get_info(emo_graph_t g, emo_graph_info *info) {
+    if (!g || !info) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
+    *info = g->info;
+    return ok();
+}
+
+emo_status emo_graph_topo_order(emo_graph_t g, int32_t *order, int32_t *depth) {
+    if (!g || (!order && g->V > 0)) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
+    if (g->V > 0) std::memcpy(order, g->order.data(), sizeof(int32_t) * g->V);
+    if (depth && g->V > 0) std::memcpy(depth, g->depth.data(), sizeof(int32_t) * g->V);
+    return ok();
+}
+
+emo_status emo_eval_policies(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
+                             float *energy, void *stream) {
+    emo_status s = check_batch(g, B);
+    if (s != EMO_OK) return s;
+    if (B == 0 || (!makespan && !energy)) return ok();
+    if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
+    DeviceGuard guard(g->device);
+    return after_launch(emo::launch_eval(g->dg, levels, B, makespan, energy,
+                                         static_cast<hipStream_t>(stream)), "emo_eval_policies");
+}
+
+emo_status emo_slack(emo_graph_t g, const uint8_t *levels, int64_t B, float *slack,
+                     int32_t per_node, float *makespan, float *energy, void *stream) {
+    emo_status s = check_batch(g, B);
+    if (s != EMO_OK) return s;
+    if (B == 0) return ok();
+    if (!slack) return fail(EMO_ERR_INVALID_ARGUMENT, "slack is NULL");
+    if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
+    DeviceGuard guard(g->device);
+    const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
+    int32_t cols = per_node ? g->V : g->P;
+    return after_launch(emo::launch_slack(g->dg, prog, cols, levels, B, slack, makespan, energy,
+                                          static_cast<hipStream_t>(stream)), "emo_slack");
+}
+
+emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t B,
+                             float latency_target, uint32_t *feasible_mask,
+                             emo_selection *result, void *stream) {
+    emo_status s = check_batch(g, B);
+    if (s != EMO_OK) return s;
+    if (!result) return fail(EMO_ERR_INVALID_ARGUMENT, "result is NULL");
+    if (reinterpret_cast<uintptr_t>(result) % 8) return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
+    if (std::isnan(latency_target)) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
+    if (B > 0 && !levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
+    DeviceGuard guard(g->device);
+    return after_launch(emo::launch_select(g->dg, levels, B, latency_target, feasible_mask, result,
+                                           static_cast<hipStream_t>(stream)), "emo_select_policy");
+}
+
+emo_status emo_select_from_results(const float *makespan, const float *energy, int64_t B,
+                                   float latency_target, uint32_t *feasible_mask,
+                                   emo_selection *result, void *stream) {
+    if (B < 0 || B >= (int64_t(1) << 32))
+        return fail(EMO_ERR_INVALID_ARGUMENT, "num_candidates %lld outside [0, 2^32)", (long long)B);
+    if (!result) return fail(EMO_ERR_INVALID_ARGUMENT, "result is NULL");
+    if (reinterpret_cast<uintptr_t>(result) % 8) return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
+    if (B > 0 && (!makespan || !energy)) return fail(EMO_ERR_INVALID_ARGUMENT, "makespan/energy is NULL");
+    if (std::isnan(latency_target)) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
+    return after_launch(emo::launch_select_results(makespan, energy, B, latency_target, feasible_mask,
+                                                   result, static_cast<hipStream_t>(stream)),
+                        "emo_select_from_results");
+}
+
+}  // extern "C"

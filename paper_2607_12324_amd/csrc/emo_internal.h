@@ -1,0 +1,59 @@
+// Internal interface between the host side of the library (graph analysis, program
+// compilation, argument checking) and the HIP kernels.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#include "emo.h"
+
+namespace emo {
+
+// One step of a kernel program: a node visited in topological order.
+//   pack     pack id, or -1 for a node of fixed duration
+//   cst      fp32 bits: the latest finish time among the node's candidate-independent
+//            predecessors (0 when it has none); the start time is at least this
+//   dur      fp32 bits: the fixed duration (pack == -1)
+//   out      finish-time slot written by this step, or -1
+struct Op {
+    int32_t pack;
+    uint32_t cst;
+    uint32_t dur;
+    int32_t out;
+};
+
+// A compiled traversal.  Forward programs list candidate-dependent nodes in a topological
+// order; every predecessor that is itself candidate-dependent is read from a slot.
+struct DevProgram {
+    int32_t n_ops = 0;
+    int32_t n_slots = 0;
+    float t_const = 0.f;           // makespan floor from candidate-independent nodes
+    const Op *op = nullptr;        // [n_ops]
+    const int2 *in_range = nullptr;   // [n_ops] {begin, end} into ins
+    const int32_t *ins = nullptr;     // slot indices of candidate-dependent predecessors
+    // backward (slack) programs only: slot of step i is i
+    const int2 *succ_range = nullptr; // [n_ops] {begin, end} into succs
+    const int32_t *succs = nullptr;   // step indices of successors
+    const int32_t *out_col = nullptr; // [n_ops] column of the slack output, -1 for none
+};
+
+struct DevGraph {
+    int32_t V = 0, P = 0, F = 1;
+    float static_power = 0.f;
+    const float2 *tab = nullptr;   // [P*F] interleaved (time, energy)
+    DevProgram eval;               // forward, slots reused (live set only)
+    DevProgram slack_pack;         // forward + backward over candidate-dependent nodes
+    DevProgram slack_node;         // forward + backward over every node
+};
+
+hipError_t launch_eval(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
+                       hipStream_t s);
+hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
+                        const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
+                        hipStream_t s);
+hipError_t launch_select(const DevGraph &g, const uint8_t *levels, int64_t B, float target,
+                         uint32_t *mask, emo_selection *res, hipStream_t s);
+hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
+                                 uint32_t *mask, emo_selection *res, hipStream_t s);
+
+}  // namespace emo

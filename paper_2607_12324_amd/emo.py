@@ -1,0 +1,231 @@
+"""Thin Python binding of the C ABI in include/emo.h (argument marshalling only).
+
+Every computation runs in libemo.so (HIP kernels for gfx950).  PyTorch supplies device memory
+and the stream: tensors are passed by data_ptr() and calls are enqueued on
+torch.cuda.current_stream() unless a stream is given.  If the library is missing this module
+raises at import time; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libemo.so")
+
+OK = 0
+STATUS_NAMES = {0: "EMO_OK", 1: "EMO_ERR_INVALID_ARGUMENT", 2: "EMO_ERR_CYCLE",
+                3: "EMO_ERR_OUT_OF_MEMORY", 4: "EMO_ERR_DEVICE", 5: "EMO_ERR_UNSUPPORTED"}
+
+ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info", "emo_graph_topo_order",
+                "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_select_from_results",
+                "emo_status_string", "emo_last_error")
+
+
+class EmoError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class GraphInfo(ctypes.Structure):
+    _fields_ = [("num_nodes", ctypes.c_int32), ("num_edges", ctypes.c_int32),
+                ("num_packs", ctypes.c_int32), ("num_levels", ctypes.c_int32),
+                ("num_dynamic_nodes", ctypes.c_int32), ("num_dynamic_edges", ctypes.c_int32),
+                ("eval_slots", ctypes.c_int32), ("max_depth", ctypes.c_int32),
+                ("const_makespan", ctypes.c_float), ("device", ctypes.c_int32),
+                ("pack_order_monotone", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+
+
+def _load_library():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() or "
+                          "python -m paper_2607_12324_amd.build")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    sig = {
+        "emo_load_graph": [i32, i32, P, P, P, P, i32, i32, P, P, f32, i32, P],
+        "emo_free_graph": [P],
+        "emo_graph_get_info": [P, P],
+        "emo_graph_topo_order": [P, P, P],
+        "emo_eval_policies": [P, P, i64, P, P, P],
+        "emo_slack": [P, P, i64, P, i32, P, P, P],
+        "emo_select_policy": [P, P, i64, f32, P, P, P],
+        "emo_select_from_results": [P, P, i64, f32, P, P, P],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.emo_status_string.argtypes = [ctypes.c_int]
+    lib.emo_status_string.restype = ctypes.c_char_p
+    lib.emo_last_error.argtypes = []
+    lib.emo_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load_library()
+
+
+def _check(status: int):
+    if status != OK:
+        raise EmoError(status, lib.emo_last_error().decode())
+
+
+def _np(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _nptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None and a.size else None
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dptr(t, dtype=None, numel=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, needs {numel}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+@dataclass
+class Selection:
+    index: int
+    energy: float
+    makespan: float
+    num_feasible: int
+
+
+def parse_selection(res) -> Selection:
+    """Decode a 24-byte emo_selection held in a device int64 tensor of 3 elements."""
+    raw = res.detach().cpu().numpy().view(np.uint8)
+    idx = int(raw[0:8].view(np.int64)[0])
+    e, t = raw[8:16].view(np.float32).tolist()
+    n = int(raw[16:24].view(np.int64)[0])
+    return Selection(idx, float(e), float(t), n)
+
+
+class EmoGraph:
+    """A graph loaded into libemo (emo_load_graph).  `device=-1` loads host-only."""
+
+    def __init__(self, graph, device: int = 0):
+        self._h = ctypes.c_void_p()
+        src = _np(graph.edge_src, np.int32)
+        dst = _np(graph.edge_dst, np.int32)
+        pack = _np(graph.node_pack, np.int32)
+        dur = _np(graph.node_duration, np.float32)
+        tt = _np(graph.pack_time, np.float32).reshape(-1)
+        te = _np(graph.pack_energy, np.float32).reshape(-1)
+        _check(lib.emo_load_graph(int(graph.num_nodes), int(src.size), _nptr(src), _nptr(dst),
+                                  _nptr(pack), _nptr(dur), int(graph.num_packs),
+                                  int(graph.num_levels), _nptr(tt), _nptr(te),
+                                  float(graph.static_power), int(device), ctypes.byref(self._h)))
+        self.num_nodes = int(graph.num_nodes)
+        self.num_packs = int(graph.num_packs)
+        self.num_levels = int(graph.num_levels)
+        self.device = int(device)
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib.emo_free_graph(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def info(self) -> dict:
+        inf = GraphInfo()
+        _check(lib.emo_graph_get_info(self._h, ctypes.byref(inf)))
+        return inf.as_dict()
+
+    def topo_order(self):
+        order = np.empty(self.num_nodes, dtype=np.int32)
+        depth = np.empty(self.num_nodes, dtype=np.int32)
+        _check(lib.emo_graph_topo_order(self._h, _nptr(order), _nptr(depth)))
+        return order, depth
+
+    def _levels(self, levels):
+        import torch
+        if levels.dim() != 2 or levels.shape[1] != self.num_packs:
+            raise ValueError(f"levels must be [B, {self.num_packs}]")
+        return _dptr(levels, torch.uint8, name="levels"), int(levels.shape[0])
+
+    def eval_policies(self, levels, makespan=None, energy=None, stream=None):
+        import torch
+        lv, B = self._levels(levels)
+        if makespan is None:
+            makespan = torch.empty(B, dtype=torch.float32, device=levels.device)
+        if energy is None:
+            energy = torch.empty(B, dtype=torch.float32, device=levels.device)
+        _check(lib.emo_eval_policies(self._h, lv, B, _dptr(makespan, torch.float32, B, "makespan"),
+                                     _dptr(energy, torch.float32, B, "energy"), _stream(stream)))
+        return makespan, energy
+
+    def slack(self, levels, per_node: bool = False, out=None, makespan=None, energy=None,
+              stream=None):
+        import torch
+        lv, B = self._levels(levels)
+        cols = self.num_nodes if per_node else self.num_packs
+        if out is None:
+            out = torch.empty((B, cols), dtype=torch.float32, device=levels.device)
+        _check(lib.emo_slack(self._h, lv, B, _dptr(out, torch.float32, B * cols, "slack"),
+                             int(bool(per_node)), _dptr(makespan, torch.float32, B, "makespan"),
+                             _dptr(energy, torch.float32, B, "energy"), _stream(stream)))
+        return out
+
+    def select_policy(self, levels, latency_target: float, mask=None, result=None, stream=None,
+                      want_mask: bool = True):
+        import torch
+        lv, B = self._levels(levels)
+        if mask is None and want_mask:
+            mask = torch.empty(max(1, (B + 31) // 32), dtype=torch.int32, device=levels.device)
+        if result is None:
+            result = torch.empty(3, dtype=torch.int64, device=levels.device)
+        _check(lib.emo_select_policy(self._h, lv, B, float(latency_target),
+                                     _dptr(mask, torch.int32, (B + 31) // 32, "mask"),
+                                     _dptr(result, torch.int64, 3, "result"), _stream(stream)))
+        return result, mask
+
+
+def select_from_results(makespan, energy, latency_target: float, mask=None, result=None,
+                        stream=None, want_mask: bool = True):
+    import torch
+    B = int(makespan.numel())
+    if mask is None and want_mask:
+        mask = torch.empty(max(1, (B + 31) // 32), dtype=torch.int32, device=makespan.device)
+    if result is None:
+        result = torch.empty(3, dtype=torch.int64, device=makespan.device)
+    _check(lib.emo_select_from_results(_dptr(makespan, torch.float32, B, "makespan"),
+                                       _dptr(energy, torch.float32, B, "energy"), B,
+                                       float(latency_target),
+                                       _dptr(mask, torch.int32, (B + 31) // 32, "mask"),
+                                       _dptr(result, torch.int64, 3, "result"), _stream(stream)))
+    return result, mask
+
+
+def unpack_mask(mask, B: int) -> np.ndarray:
+    """Feasibility bits (bit c % 32 of word c // 32) as a bool array of length B."""
+    words = mask.detach().cpu().numpy().view(np.uint32)[: (B + 31) // 32]
+    bits = np.unpackbits(words.view(np.uint8), bitorder="little")
+    return bits[:B].astype(bool)

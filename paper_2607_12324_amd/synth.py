@@ -279,11 +279,19 @@ def _chunk(seed: int, chunk: int, rows: int, P: int, F: int, dist: str) -> np.nd
     if dist != "mixture":
         raise ValueError(dist)
     # mixture: candidate c lowers each pack independently with probability rho_c ~ U(0,1) to a
-    # uniform level in [0, F-2], else keeps it at F-1.  Given u < rho, u/rho is U(0,1).
-    rho = rng.random(rows, dtype=np.float32)[:, None]
-    u = rng.random((rows, P), dtype=np.float32)
-    low = np.minimum(np.floor(u / np.maximum(rho, 1e-30) * (F - 1)), F - 2).astype(np.uint8)
-    return np.where(u < rho, low, np.uint8(F - 1)).astype(np.uint8)
+    # uniform level in [0, F-2], else keeps it at F-1.  Each (candidate, pack) draws one 32-bit
+    # word: its high half against rho_c (16-bit fixed point) decides whether to lower, its low
+    # half picks the lowered level.
+    thresh = (rng.random(rows) * 65536.0).astype(np.uint32)
+    out = np.empty((rows, P), dtype=np.uint8)
+    sub = 512
+    for s in range(0, rows, sub):
+        n = min(sub, rows - s)
+        u = np.frombuffer(rng.bytes(n * P * 4), dtype=np.uint32).reshape(n, P)
+        low = (((u & np.uint32(0xFFFF)) * np.uint32(F - 1)) >> np.uint32(16)).astype(np.uint8)
+        keep = (u >> np.uint32(16)) >= thresh[s:s + n, None]
+        np.maximum(low, keep.view(np.uint8) * np.uint8(F - 1), out=out[s:s + n])
+    return out
 
 
 def random_policies(seed: int, num_packs: int, num_levels: int, start: int, count: int,
@@ -299,6 +307,33 @@ def random_policies(seed: int, num_packs: int, num_levels: int, start: int, coun
         out[r - start:hi - start] = blk[r - lo:hi - lo]
         r = hi
     if start == 0 and count > 0:
+        out[0, :] = num_levels - 1
+    return out
+
+
+def _chunk_job(args):
+    seed, ch, P, F, dist = args
+    return ch, _chunk(seed, ch, POLICY_CHUNK, P, F, dist)
+
+
+def random_policies_parallel(seed: int, num_packs: int, num_levels: int, count: int,
+                             dist: str = "mixture", workers: int = 8) -> np.ndarray:
+    """Rows 0..count of random_policies(...) generated by a pool of worker processes (spawned,
+    so that a parent that already holds a GPU context is never forked)."""
+    import multiprocessing as mp
+    from concurrent.futures import ProcessPoolExecutor
+    out = np.empty((count, num_packs), dtype=np.uint8)
+    nch = (count + POLICY_CHUNK - 1) // POLICY_CHUNK
+    if nch <= 2 or workers <= 1:
+        return random_policies(seed, num_packs, num_levels, 0, count, dist)
+    jobs = [(seed, ch, num_packs, num_levels, dist) for ch in range(nch)]
+    with ProcessPoolExecutor(max_workers=min(workers, nch),
+                             mp_context=mp.get_context("spawn")) as ex:
+        for ch, blk in ex.map(_chunk_job, jobs):
+            lo = ch * POLICY_CHUNK
+            hi = min(lo + POLICY_CHUNK, count)
+            out[lo:hi] = blk[:hi - lo]
+    if count > 0:
         out[0, :] = num_levels - 1
     return out
 

@@ -1,0 +1,147 @@
+"""The C-ABI library on the CPU: exported symbols, host-side validation, graph analysis and the
+canonical topological order (no device work)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import pins
+from paper_2607_12324_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "emo.h")
+
+
+@pytest.fixture(scope="module")
+def emo():
+    from paper_2607_12324_amd import emo as mod
+    return mod
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(emo_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol(emo):
+    names = declared_functions()
+    assert set(names) == set(emo.ENTRY_POINTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", emo.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (emo_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    for n in names:
+        assert getattr(emo.lib, n) is not None
+
+
+def test_status_strings(emo):
+    for code, name in emo.STATUS_NAMES.items():
+        assert emo.lib.emo_status_string(code).decode() == name
+
+
+def _load(emo, g):
+    return emo.EmoGraph(g, device=-1)
+
+
+def _raises(emo, g, status):
+    with pytest.raises(emo.EmoError) as ei:
+        _load(emo, g)
+    assert ei.value.status == status, str(ei.value)
+    return str(ei.value)
+
+
+def _base():
+    return pins.graph_from_golden(pins.load_golden())
+
+
+def _mod(g, **kw):
+    return synth.Graph(**{**g.__dict__, **kw})
+
+
+def test_validation_errors(emo):
+    g = _base()
+    INV, CYC = 1, 2
+    _raises(emo, _mod(g, edge_dst=np.asarray([1, 2, 3, 9], np.int32)), INV)
+    _raises(emo, _mod(g, edge_src=np.asarray([0, 0, 1, 3], np.int32)), CYC)  # 3 -> 3
+    _raises(emo, _mod(g, edge_src=np.asarray([0, 0, 1, 2, 3], np.int32),
+                      edge_dst=np.asarray([1, 2, 3, 3, 0], np.int32)), CYC)
+    _raises(emo, _mod(g, node_pack=np.asarray([-1, 0, 0, 2], np.int32)), INV)   # duplicate
+    _raises(emo, _mod(g, node_pack=np.asarray([-1, 0, 1, 5], np.int32)), INV)   # out of range
+    _raises(emo, _mod(g, node_pack=np.asarray([-1, 0, 1, -1], np.int32)), INV)  # pack 2 unused
+    _raises(emo, _mod(g, node_duration=np.asarray([-1, 0, 0, 0], np.float32)), INV)
+    _raises(emo, _mod(g, node_duration=np.asarray([np.inf, 0, 0, 0], np.float32)), INV)
+    t = g.pack_time.copy(); t[1, 0] = np.nan
+    _raises(emo, _mod(g, pack_time=t), INV)
+    e = g.pack_energy.copy(); e[2, 1] = -1
+    _raises(emo, _mod(g, pack_energy=e), INV)
+    _raises(emo, _mod(g, static_power=float("nan")), INV)
+    _raises(emo, _mod(g, static_power=-0.5), INV)
+    tt = np.zeros((3, 0), np.float32)
+    _raises(emo, _mod(g, num_levels=0, pack_time=tt, pack_energy=tt), INV)
+    big = np.zeros((3, 257), np.float32)
+    _raises(emo, _mod(g, num_levels=257, pack_time=big, pack_energy=big), INV)
+
+
+def test_host_only_graph_rejects_batch_calls(emo):
+    gh = _load(emo, _base())
+    st = emo.lib.emo_eval_policies(gh._h, None, 0, None, None, None)
+    assert st == 5
+
+
+def test_empty_and_degenerate_graphs_load(emo):
+    z = np.zeros(0, np.int32)
+    zf = np.zeros((0, 1), np.float32)
+    empty = synth.Graph("empty", 0, z, z, z, np.zeros(0, np.float32), 0, 1, zf, zf, 0.0)
+    gh = _load(emo, empty)
+    assert gh.info()["num_nodes"] == 0
+    order, depth = gh.topo_order()
+    assert order.size == 0
+    one = synth.Graph("one", 1, z, z, np.zeros(1, np.int32), np.zeros(1, np.float32), 1, 1,
+                      np.ones((1, 1), np.float32), np.ones((1, 1), np.float32), 0.0)
+    gh = _load(emo, one)
+    inf = gh.info()
+    assert inf["num_dynamic_nodes"] == 1 and inf["eval_slots"] == 0
+
+
+def test_duplicate_edges_are_merged(emo):
+    g = _base()
+    g2 = _mod(g, edge_src=np.concatenate([g.edge_src, g.edge_src[:2]]),
+              edge_dst=np.concatenate([g.edge_dst, g.edge_dst[:2]]))
+    assert _load(emo, g2).info()["num_edges"] == g.num_edges
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_topo_order_matches_oracle_on_random_dags(emo, oracle_lib, seed):
+    rng = np.random.default_rng(100 + seed)
+    for i in range(15):
+        g = synth.random_dag(rng, int(rng.integers(1, 60)), float(rng.uniform(0.02, 0.3)),
+                             float(rng.uniform(0.2, 0.9)), int(rng.integers(1, 5)))
+        order, depth = _load(emo, g).topo_order()
+        o2, d2 = oracle.topo_order(g.num_nodes, g.edge_src, g.edge_dst)
+        assert np.array_equal(order, o2) and np.array_equal(depth, d2)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_topo_order_and_analysis_on_workloads(emo, oracle_lib, k):
+    g = synth.config_graph(k)
+    gh = _load(emo, g)
+    order, depth = gh.topo_order()
+    o2, d2 = oracle.topo_order(g.num_nodes, g.edge_src, g.edge_dst)
+    assert np.array_equal(order, o2) and np.array_equal(depth, d2)
+    inf = gh.info()
+    assert inf["num_packs"] == g.num_packs and inf["num_levels"] == g.num_levels
+    assert inf["pack_order_monotone"] == 1
+    assert inf["max_depth"] == int(d2.max())
+    # candidate-independent nodes: those with no pack ancestor (host launch chains)
+    n_host_const = {1: 4, 2: 64, 3: 512, 4: 0, 5: 65536}[k]
+    assert inf["num_dynamic_nodes"] == g.num_nodes - n_host_const
+    # the finish time of the candidate-independent nodes is the host chain's total
+    if n_host_const:
+        host = np.nonzero(g.node_pack < 0)[0]
+        assert inf["const_makespan"] == float(np.sum(g.node_duration[host].astype(np.float64)))

@@ -1,0 +1,241 @@
+"""HIP path against the oracle, through the C ABI (needs an MI355X)."""
+import numpy as np
+import pytest
+
+import oracle
+import parity
+import pins
+from paper_2607_12324_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    return t
+
+
+@pytest.fixture(scope="module")
+def emo(torch):
+    from paper_2607_12324_amd import emo as mod
+    return mod
+
+
+def dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def run_all(torch, emo, g, rows, targets, exact=True, per_node=True, what=""):
+    """eval, slack (per pack and per node), fused select and select-from-results vs oracle."""
+    print(f"[case] {what}: V={g.num_nodes} P={g.num_packs} F={g.num_levels} B={len(rows)}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    lv = dev(torch, rows)
+    B = len(rows)
+    T, E = gh.eval_policies(lv)
+    torch.cuda.synchronize()
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    parity.assert_eval(host(T), host(E), T_or, E_or, exact, what)
+    # slack of every pack (+ makespan/energy from the same pass)
+    T2 = torch.empty_like(T)
+    E2 = torch.empty_like(E)
+    S = gh.slack(lv, makespan=T2, energy=E2)
+    parity.assert_eval(host(T2), host(E2), T_or, E_or, exact, what + " (slack pass)")
+    pick = synth.sample_rows(B, 48) if B else np.zeros(0, np.int64)
+    S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in pick]) if len(pick) else np.zeros((0, g.num_packs))
+    parity.assert_slack(host(S)[pick], S_or, T_or[pick], exact, what + " pack slack")
+    if per_node:
+        SN = gh.slack(lv, per_node=True)
+        SN_or = np.stack([oracle.slack(g, rows[c]).slack for c in pick]) if len(pick) else np.zeros((0, g.num_nodes))
+        parity.assert_slack(host(SN)[pick], SN_or, T_or[pick], exact, what + " node slack")
+    for tgt in targets:
+        tgt = float(np.float32(tgt))
+        res, mask = gh.select_policy(lv, tgt)
+        sel = emo.parse_selection(res)
+        bits = emo.unpack_mask(mask, B)
+        parity.assert_selection(sel, bits, T_or, E_or, tgt, exact, what + f" select@{tgt}")
+        res2, mask2 = emo.select_from_results(T, E, tgt)
+        sel2 = emo.parse_selection(res2)
+        parity.assert_selection(sel2, emo.unpack_mask(mask2, B), T_or, E_or, tgt, exact,
+                                what + f" select_from_results@{tgt}")
+    gh.close()
+
+
+def test_handworked_example(torch, emo):
+    d = pins.load_golden()
+    g = pins.graph_from_golden(d)
+    rows = synth.exhaustive_policies(g.num_packs, g.num_levels, 0, 8)
+    gh = emo.EmoGraph(g, device=0)
+    T, E = gh.eval_policies(dev(torch, rows))
+    assert host(T).tolist() == d["makespan"]
+    assert np.allclose(host(E), d["energy"], rtol=1e-6, atol=0)
+    SN = host(gh.slack(dev(torch, rows), per_node=True))
+    for c, expect in d["node_slack"].items():
+        assert SN[int(c)].tolist() == expect
+    for s in d["selection"]:
+        res, mask = gh.select_policy(dev(torch, rows), s["target"])
+        sel = emo.parse_selection(res)
+        assert sel.index == s["index"] and sel.num_feasible == s["num_feasible"], (s, sel)
+    run_all(torch, emo, g, rows, [16.8, 18.0, 20.0, 22.0, 15.9], what="handworked")
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_dags_on_grid(torch, emo, seed):
+    rng = np.random.default_rng(1000 + seed)
+    for i in range(4):
+        V = int(rng.integers(1, 300))
+        F = int(rng.integers(1, 20))
+        g = synth.random_dag(rng, V, float(rng.uniform(1.0, 6.0)) / max(V, 1),
+                             float(rng.uniform(0.2, 1.0)), F, shuffle_packs=bool(i % 2))
+        B = int(rng.integers(1, 1500))
+        rows = pins.random_rows(rng, g, B)
+        T_or, _ = oracle.eval_batch(g, rows)
+        targets = [float(np.quantile(T_or, q)) for q in (0.0, 0.3, 0.9)] + [float(T_or.min()) - 1.0]
+        run_all(torch, emo, g, rows, targets, exact=True, what=f"random seed={seed} i={i}")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_random_dags_off_grid(torch, emo, seed):
+    rng = np.random.default_rng(2000 + seed)
+    for i in range(3):
+        V = int(rng.integers(2, 200))
+        F = int(rng.integers(2, 9))
+        g = synth.random_dag(rng, V, 3.0 / V, 0.6, F, on_grid=False)
+        B = int(rng.integers(100, 3000))
+        rows = pins.random_rows(rng, g, B)
+        T_or, _ = oracle.eval_batch(g, rows)
+        run_all(torch, emo, g, rows, [float(np.quantile(T_or, 0.5))], exact=False,
+                what=f"offgrid seed={seed} i={i}")
+
+
+def test_large_slot_count_uses_device_scratch(torch, emo):
+    """A wide antichain of packs feeding one sink keeps many finish times live at once."""
+    rng = np.random.default_rng(5)
+    W = 3000
+    V = W + 2
+    src = [0] * W + list(range(1, W + 1))
+    dst = list(range(1, W + 1)) + [W + 1] * W
+    pack = np.full(V, -1, np.int32)
+    pack[1:W + 1] = np.arange(W)
+    F = 4
+    t = np.sort(synth.quantize(rng.uniform(1, 50, (W, F))), axis=1)[:, ::-1].copy()
+    e = rng.uniform(0, 3, (W, F)).astype(np.float32)
+    g = synth.Graph("antichain", V, np.asarray(src, np.int32), np.asarray(dst, np.int32), pack,
+                    synth.quantize(rng.uniform(1, 9, V)), W, F, t, e, 0.25)
+    rows = pins.random_rows(rng, g, 777)
+    gh = emo.EmoGraph(g, device=0)
+    assert gh.info()["eval_slots"] >= W
+    T_or, _ = oracle.eval_batch(g, rows)
+    run_all(torch, emo, g, rows, [float(np.median(T_or))], what="antichain")
+
+
+def test_edge_cases(torch, emo):
+    g = pins.graph_from_golden(pins.load_golden())
+    gh = emo.EmoGraph(g, device=0)
+    # B = 0
+    empty = torch.zeros((0, g.num_packs), dtype=torch.uint8, device="cuda")
+    T, E = gh.eval_policies(empty)
+    res, _ = gh.select_policy(empty, 100.0)
+    sel = emo.parse_selection(res)
+    assert sel.index == -1 and sel.num_feasible == 0 and np.isnan(sel.energy)
+    S = gh.slack(empty)
+    assert S.shape == (0, g.num_packs)
+    # invalid level bytes: NaN results, never feasible
+    rows = np.asarray([[1, 1, 1], [2, 0, 0], [1, 1, 255], [0, 0, 0]], np.uint8)
+    T, E = gh.eval_policies(dev(torch, rows))
+    Th, Eh = host(T), host(E)
+    assert np.isnan(Th[1]) and np.isnan(Th[2]) and np.isnan(Eh[1]) and np.isnan(Eh[2])
+    assert Th[0] == 16.0 and Th[3] == 22.0
+    S = host(gh.slack(dev(torch, rows)))
+    assert np.all(np.isnan(S[1])) and np.all(np.isnan(S[2])) and not np.any(np.isnan(S[0]))
+    res, mask = gh.select_policy(dev(torch, rows), 1e9)
+    sel = emo.parse_selection(res)
+    assert sel.num_feasible == 2 and emo.unpack_mask(mask, 4).tolist() == [True, False, False, True]
+    assert sel.index == 3 and sel.makespan == 22.0
+    # all rows identical: ties go to the lowest index
+    rows = np.tile(np.asarray([[0, 1, 0]], np.uint8), (1000, 1))
+    res, _ = gh.select_policy(dev(torch, rows), 1e9)
+    assert emo.parse_selection(res).index == 0
+    rows[:500] = 1   # slower... no: faster, more energy; the cheapest identical rows start at 500
+    res, _ = gh.select_policy(dev(torch, rows), 1e9)
+    T_or, E_or = oracle.eval_batch(g, rows)
+    assert emo.parse_selection(res).index == oracle.select(T_or, E_or, 1e9)[0]
+    # target below every makespan
+    res, mask = gh.select_policy(dev(torch, rows), 1.0)
+    sel = emo.parse_selection(res)
+    assert sel.index == -1 and sel.num_feasible == 0 and not emo.unpack_mask(mask, 1000).any()
+    # empty graph and a graph without packs
+    z = np.zeros(0, np.int32)
+    zf = np.zeros((0, 1), np.float32)
+    ge = synth.Graph("empty", 0, z, z, z, np.zeros(0, np.float32), 0, 1, zf, zf, 0.5)
+    gh0 = emo.EmoGraph(ge, device=0)
+    T, E = gh0.eval_policies(torch.zeros((5, 0), dtype=torch.uint8, device="cuda"))
+    assert host(T).tolist() == [0.0] * 5 and host(E).tolist() == [0.0] * 5
+    gn = synth.Graph("nopacks", 3, np.asarray([0, 1], np.int32), np.asarray([1, 2], np.int32),
+                     np.full(3, -1, np.int32), np.asarray([1.0, 2.0, 4.0], np.float32), 0, 1,
+                     zf, zf, 0.5)
+    ghn = emo.EmoGraph(gn, device=0)
+    T, E = ghn.eval_policies(torch.zeros((3, 0), dtype=torch.uint8, device="cuda"))
+    assert host(T).tolist() == [7.0] * 3 and host(E).tolist() == [3.5] * 3
+    SN = host(ghn.slack(torch.zeros((3, 0), dtype=torch.uint8, device="cuda"), per_node=True))
+    assert SN.tolist() == [[0.0, 0.0, 0.0]] * 3
+
+
+def test_determinism(torch, emo):
+    g = synth.config_graph(3)
+    rows = synth.config_policies(3, g, 0, 20000)
+    gh = emo.EmoGraph(g, device=0)
+    lv = dev(torch, rows)
+    a = [host(x).copy() for x in gh.eval_policies(lv)]
+    b = [host(x).copy() for x in gh.eval_policies(lv)]
+    assert all(np.array_equal(x.view(np.uint32), y.view(np.uint32)) for x, y in zip(a, b))
+    s1 = host(gh.slack(lv[:2000])).copy()
+    s2 = host(gh.slack(lv[:2000])).copy()
+    assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_workload_full_batch(torch, emo, k):
+    """Every candidate of workload k: makespan/energy of all rows, masks and selection for each
+    target, slack on sampled rows (slack of all rows is computed, as the benchmark does)."""
+    spec = synth.CONFIGS[k]
+    g = synth.config_graph(k)
+    B = spec.num_candidates
+    print(f"[case] workload {k} {spec.name} B={B}", flush=True)
+    if spec.exhaustive:
+        rows = synth.config_policies(k, g)
+    else:
+        rows = synth.random_policies_parallel(spec.policy_seed, g.num_packs, g.num_levels, B, workers=8)
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=16)
+    T0 = float(np.min(T_or)) if spec.exhaustive else float(T_or[0])
+    assert np.all(rows[0 if not spec.exhaustive else -1] == g.num_levels - 1)
+    gh = emo.EmoGraph(g, device=0)
+    lv = dev(torch, rows)
+    T, E = gh.eval_policies(lv)
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, spec.name)
+    for r in spec.targets:
+        tgt = float(np.float32(r * T0))
+        res, mask = gh.select_policy(lv, tgt)
+        parity.assert_selection(emo.parse_selection(res), emo.unpack_mask(mask, B), T_or, E_or,
+                                tgt, True, f"{spec.name} select@{r}")
+        res2, mask2 = emo.select_from_results(T, E, tgt)
+        parity.assert_selection(emo.parse_selection(res2), emo.unpack_mask(mask2, B), T_or, E_or,
+                                tgt, True, f"{spec.name} select_from_results@{r}")
+    pick = synth.sample_rows(B, 24)
+    S = gh.slack(lv)
+    S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in pick])
+    idx = torch.from_numpy(pick).cuda()
+    parity.assert_slack(host(S.index_select(0, idx)), S_or, T_or[pick], True, spec.name + " slack")
+    del S
+    # per-node slack over a leading slice
+    nb = min(B, 512)
+    SN = gh.slack(lv[:nb], per_node=True)
+    pick2 = synth.sample_rows(nb, 6)
+    SN_or = np.stack([oracle.slack(g, rows[c]).slack for c in pick2])
+    parity.assert_slack(host(SN)[pick2], SN_or, T_or[pick2], True, spec.name + " node slack")
+    gh.close()
