@@ -83,8 +83,26 @@ typedef struct {
     float const_makespan;         /* largest finish time among candidate-independent nodes */
     int32_t device;               /* device ordinal, -1 for a host-only graph */
     int32_t pack_order_monotone;  /* 1 if the kernels visit packs in increasing pack id */
-    int32_t reserved;
+    int32_t kernel_mode;          /* emo_kernel_mode in effect */
+    int32_t specialized;          /* bit 0: specialised eval/select kernels are compiled,
+                                     bit 1: a specialised slack kernel is compiled,
+                                     bit 2: specialisation was tried and failed */
+    float compile_seconds;        /* time spent compiling specialised kernels */
 } emo_graph_info;
+
+/* Which kernels evaluate a graph.
+ *   EMO_KERNELS_AUTO         kernels specialised to the graph (generated and compiled at run
+ *                            time on first use) when the graph is small enough, otherwise the
+ *                            precompiled interpreting kernels.  Default.
+ *   EMO_KERNELS_INTERPRETED  always the precompiled kernels that interpret a compiled program.
+ *   EMO_KERNELS_SPECIALIZED  like AUTO, but a failed specialisation is reported as
+ *                            EMO_ERR_DEVICE by the batch call instead of falling back.
+ * Both kinds compute bit-identical results. */
+typedef enum {
+    EMO_KERNELS_AUTO = 0,
+    EMO_KERNELS_INTERPRETED = 1,
+    EMO_KERNELS_SPECIALIZED = 2
+} emo_kernel_mode;
 
 /*
  * Load an execution graph and its pack tables (Sec. IV-C; Alg. 1 REQUIRE line).
@@ -117,6 +135,10 @@ emo_status emo_free_graph(emo_graph_t g);
 
 /* Fill `info` (host). */
 emo_status emo_graph_get_info(emo_graph_t g, emo_graph_info *info);
+
+/* Choose the kernels used by later batch calls on `g` (an emo_kernel_mode).  Not to be called
+ * while batch calls on `g` may run concurrently on another thread. */
+emo_status emo_graph_set_kernel_mode(emo_graph_t g, int32_t mode);
 
 /*
  * Canonical topological order (the traversal order of Alg. 1): nodes sorted by depth, then by
@@ -163,6 +185,12 @@ emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t num_c
 emo_status emo_select_from_results(const float *makespan, const float *energy,
                                    int64_t num_candidates, float latency_target,
                                    uint32_t *feasible_mask, emo_selection *result, void *stream);
+
+/* Diagnostics: the HIP source of the kernels specialised to `g` (the text EMO_KERNELS_AUTO
+ * compiles on first use), NUL-terminated.  With buf == NULL, *len receives the size needed
+ * including the NUL; otherwise at most *len bytes are written.  Works on host-only graphs.
+ * EMO_ERR_UNSUPPORTED when the graph is too large to specialise. */
+emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len);
 
 /* Static string naming a status code. */
 const char *emo_status_string(emo_status s);

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libemo.so")
-SOURCES = ["emo_host.cpp", "emo_kernels.hip"]
+SOURCES = ["emo_host.cpp", "emo_jit.cpp", "emo_kernels.hip"]
 ARCH = os.environ.get("EMO_OFFLOAD_ARCH", "gfx950")
 
 HIPCC_FLAGS = [
@@ -22,18 +22,29 @@ HIPCC_FLAGS = [
 ]
 
 
+def embed_select_source(build_dir: str) -> None:
+    """Embeds the text of csrc/emo_select.h into the library for the run-time compiler."""
+    with open(os.path.join(CSRC, "emo_select.h")) as f:
+        text = f.read()
+    assert ")EMO_SRC\"" not in text
+    with open(os.path.join(build_dir, "emo_select_src.inc"), "w") as f:
+        f.write("// generated from emo_select.h by build.py\n")
+        f.write('static const char kEmoSelectSource[] = R"EMO_SRC(\n' + text + '\n)EMO_SRC";\n')
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source and link libemo.so.  Always rebuilds."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     objs = []
     build_dir = os.path.join(PKG, "_build")
     os.makedirs(build_dir, exist_ok=True)
+    embed_select_source(build_dir)
     for src in SOURCES:
         obj = os.path.join(build_dir, src + ".o")
         cmd = [hipcc, *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]
         if src.endswith(".cpp"):
             cmd = [hipcc, "-O2", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC,
-                   "-D__HIP_PLATFORM_AMD__", "-c", os.path.join(CSRC, src), "-o", obj]
+                   "-I", build_dir, "-D__HIP_PLATFORM_AMD__", "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         res = subprocess.run(cmd, capture_output=True, text=True)
@@ -42,7 +53,7 @@ def build(verbose: bool = False) -> str:
             raise RuntimeError(f"hipcc failed on {src}")
         objs.append(obj)
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
+    cmd = [hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp, "-lhiprtc"]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)

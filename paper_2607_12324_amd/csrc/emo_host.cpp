@@ -57,10 +57,16 @@ struct HostProgram {
     std::vector<int2> succ_range;
     std::vector<int32_t> succs;
     std::vector<int32_t> out_col;
+    std::vector<int32_t> seq;   // node of each step
     int32_t n_slots = 0;
     float t_const = 0.f;
     bool pack_monotone = true;
 };
+
+constexpr int32_t kJitMaxOps = 2048;      // larger graphs compile too slowly to specialise
+constexpr int32_t kJitMaxSlackOps = 160;  // every finish time stays in a VGPR
+constexpr size_t kJitTableLds = 64 * 1024;
+constexpr size_t kJitTableLdsSlack = 40 * 1024;
 
 // Restores the caller's current device on scope exit.
 struct DeviceGuard {
@@ -94,6 +100,16 @@ struct emo_graph_s {
     emo_graph_info info{};
     std::vector<void *> allocations;         // device memory owned by the handle
     emo::DevGraph dg;
+    // graph-specialised kernels
+    int32_t kernel_mode = EMO_KERNELS_AUTO;
+    emo::JitGraph jg;
+    bool jit_eligible = false;
+    bool jit_slack_eligible = false;
+    bool jit_slack_staged = false;
+    std::mutex jit_mu;
+    int jit_state = 0;                       // 0 not tried, 1 compiled, -1 failed
+    emo::JitModule jm;
+    std::string jit_log;
 };
 
 namespace {
@@ -202,6 +218,7 @@ HostProgram build_program(const emo_graph_s &g, bool fold, bool backward, bool p
         }
     }
     const int32_t n = static_cast<int32_t>(seq.size());
+    hp.seq = seq;
     std::vector<int32_t> pos(V, -1);
     for (int32_t i = 0; i < n; ++i) pos[seq[i]] = i;
 
@@ -313,9 +330,89 @@ emo_status upload_program(emo_graph_s &g, const HostProgram &hp, emo::DevProgram
 void release_device(emo_graph_s *g) {
     if (g->device >= 0) {
         DeviceGuard guard(g->device);
+        emo::jit_unload(&g->jm);
         for (void *p : g->allocations) (void)hipFree(p);
     }
     g->allocations.clear();
+}
+
+bool is_pow2(int32_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+// The specialised kernels' view of the graph: the slack program's steps, with predecessors and
+// successors as step indices.
+emo::JitGraph make_jit_graph(const emo_graph_s &g, const HostProgram &ps) {
+    emo::JitGraph jg;
+    jg.P = g.P;
+    jg.F = g.F;
+    jg.static_power = g.static_power;
+    jg.t_const = ps.t_const;
+    jg.pack_monotone = ps.pack_monotone;
+    const size_t n = ps.op.size();
+    jg.ops.resize(n);
+    for (size_t i = 0; i < n; ++i) {
+        emo::JitOp &o = jg.ops[i];
+        o.pack = ps.op[i].pack;
+        std::memcpy(&o.cst, &ps.op[i].cst, 4);
+        std::memcpy(&o.dur, &ps.op[i].dur, 4);
+        o.in.assign(ps.ins.begin() + ps.in_range[i].x, ps.ins.begin() + ps.in_range[i].y);
+        o.out.assign(ps.succs.begin() + ps.succ_range[i].x, ps.succs.begin() + ps.succ_range[i].y);
+    }
+    return jg;
+}
+
+size_t jit_table_bytes(const emo_graph_s &g) {
+    return (static_cast<size_t>(g.P) * g.F + (is_pow2(g.F) ? 0 : emo::kTablePad)) * sizeof(float2);
+}
+
+// Source of the specialised kernels and the workgroup size they are written for.
+std::string jit_source(const emo_graph_s &g, int *block_out) {
+    const size_t tb = jit_table_bytes(g);
+    const bool with_slack = g.jit_slack_eligible;
+    const bool tab_lds = tb <= (with_slack ? kJitTableLdsSlack : kJitTableLds);
+    // one LDS copy of a large table serves a larger workgroup
+    const int block = !tab_lds || tb <= 16 * 1024 ? 256 : (tb <= 32 * 1024 ? 512 : 1024);
+    *block_out = block;
+    return emo::jit_generate(g.jg, with_slack, tab_lds, block);
+}
+
+// Generates and compiles the specialised kernels once; returns 1 when they are ready.
+int ensure_jit(emo_graph_s *g) {
+    std::lock_guard<std::mutex> lock(g->jit_mu);
+    if (g->jit_state != 0) return g->jit_state;
+    int block = 256;
+    std::string src = jit_source(*g, &block);
+    DeviceGuard guard(g->device);
+    emo::JitModule m;
+    std::string log;
+    if (emo::jit_compile(src, &m, &log) != 0) {
+        g->jit_log = log;
+        g->jit_state = -1;
+        g->info.specialized |= 4;
+        return -1;
+    }
+    m.block = block;
+    g->jm = m;
+    g->jit_state = 1;
+    g->info.specialized = 1 | (m.slack ? 2 : 0);
+    g->info.compile_seconds = static_cast<float>(m.compile_seconds);
+    return 1;
+}
+
+bool aligned(const void *p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
+
+// Whether a batch call uses the specialised kernels; may compile them.
+// Returns EMO_OK and sets *use, or an error in EMO_KERNELS_SPECIALIZED mode.
+emo_status want_jit(emo_graph_s *g, const uint8_t *levels, bool *use) {
+    *use = false;
+    if (g->kernel_mode == EMO_KERNELS_INTERPRETED || !g->jit_eligible) return EMO_OK;
+    if (!aligned(levels, static_cast<size_t>(emo::jit_level_width(g->P)))) return EMO_OK;
+    if (ensure_jit(g) != 1) {
+        if (g->kernel_mode == EMO_KERNELS_SPECIALIZED)
+            return fail(EMO_ERR_DEVICE, "specialised kernels failed to compile: %.400s", g->jit_log.c_str());
+        return EMO_OK;
+    }
+    *use = true;
+    return EMO_OK;
 }
 
 bool finite_nonneg(float x) { return std::isfinite(x) && x >= 0.f; }
@@ -438,11 +535,18 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     in.const_makespan = g->t_const;
     in.device = device;
     in.pack_order_monotone = pe.pack_monotone ? 1 : 0;
+    in.kernel_mode = EMO_KERNELS_AUTO;
+    g->jg = make_jit_graph(*g, ps);
+    const int32_t nops = static_cast<int32_t>(ps.op.size());
+    g->jit_eligible = nops >= 1 && nops <= kJitMaxOps;
+    g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;
+    g->jit_slack_staged = ps.pack_monotone && P % 16 == 0;
 
     if (device >= 0) {
         DeviceGuard guard(device);
-        std::vector<float2> tab(static_cast<size_t>(P) * F);
-        for (size_t i = 0; i < tab.size(); ++i) tab[i] = make_float2(pack_time[i], pack_energy[i]);
+        std::vector<float2> tab(static_cast<size_t>(P) * F + emo::kTablePad, make_float2(0.f, 0.f));
+        for (size_t i = 0; i < static_cast<size_t>(P) * F; ++i)
+            tab[i] = make_float2(pack_time[i], pack_energy[i]);
         g->dg.V = V; g->dg.P = P; g->dg.F = F; g->dg.static_power = static_power;
         if ((s = upload(*g, tab, &g->dg.tab)) != EMO_OK) return s;
         if ((s = upload_program(*g, pe, g->dg.eval)) != EMO_OK) return s;
@@ -466,6 +570,32 @@ emo_status emo_graph_get_info(emo_graph_t g, emo_graph_info *info) {
     return ok();
 }
 
+emo_status emo_graph_set_kernel_mode(emo_graph_t g, int32_t mode) {
+    if (!g) return fail(EMO_ERR_INVALID_ARGUMENT, "graph handle is NULL");
+    if (mode != EMO_KERNELS_AUTO && mode != EMO_KERNELS_INTERPRETED && mode != EMO_KERNELS_SPECIALIZED)
+        return fail(EMO_ERR_INVALID_ARGUMENT, "unknown kernel mode %d", mode);
+    g->kernel_mode = mode;
+    g->info.kernel_mode = mode;
+    return ok();
+}
+
+emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len) {
+    if (!g || !len) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
+    if (!g->jit_eligible) return fail(EMO_ERR_UNSUPPORTED, "graph too large to specialise");
+    int block = 256;
+    std::string src = jit_source(*g, &block);
+    const int64_t need = static_cast<int64_t>(src.size()) + 1;
+    if (!buf) {
+        *len = need;
+        return ok();
+    }
+    if (*len < need) return fail(EMO_ERR_INVALID_ARGUMENT, "buffer of %lld bytes, %lld needed",
+                                 (long long)*len, (long long)need);
+    std::memcpy(buf, src.c_str(), static_cast<size_t>(need));
+    *len = need;
+    return ok();
+}
+
 emo_status emo_graph_topo_order(emo_graph_t g, int32_t *order, int32_t *depth) {
     if (!g || (!order && g->V > 0)) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
     if (g->V > 0) std::memcpy(order, g->order.data(), sizeof(int32_t) * g->V);
@@ -479,9 +609,13 @@ emo_status emo_eval_policies(emo_graph_t g, const uint8_t *levels, int64_t B, fl
     if (s != EMO_OK) return s;
     if (B == 0 || (!makespan && !energy)) return ok();
     if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
+    bool jit = false;
+    if ((s = want_jit(g, levels, &jit)) != EMO_OK) return s;
     DeviceGuard guard(g->device);
-    return after_launch(emo::launch_eval(g->dg, levels, B, makespan, energy,
-                                         static_cast<hipStream_t>(stream)), "emo_eval_policies");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (jit) return after_launch(emo::jit_launch_eval(g->jm, levels, B, g->dg.tab, makespan, energy, st),
+                                 "emo_eval_policies");
+    return after_launch(emo::launch_eval(g->dg, levels, B, makespan, energy, st), "emo_eval_policies");
 }
 
 emo_status emo_slack(emo_graph_t g, const uint8_t *levels, int64_t B, float *slack,
@@ -491,7 +625,15 @@ emo_status emo_slack(emo_graph_t g, const uint8_t *levels, int64_t B, float *sla
     if (B == 0) return ok();
     if (!slack) return fail(EMO_ERR_INVALID_ARGUMENT, "slack is NULL");
     if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
+    bool jit = false;
+    if (!per_node && g->jit_slack_eligible) {
+        if ((s = want_jit(g, levels, &jit)) != EMO_OK) return s;
+        jit = jit && g->jm.slack && (!g->jit_slack_staged || aligned(slack, 16));
+    }
     DeviceGuard guard(g->device);
+    if (jit)
+        return after_launch(emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy,
+                                                  static_cast<hipStream_t>(stream)), "emo_slack");
     const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
     int32_t cols = per_node ? g->V : g->P;
     return after_launch(emo::launch_slack(g->dg, prog, cols, levels, B, slack, makespan, energy,
@@ -507,9 +649,18 @@ emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t B,
     if (reinterpret_cast<uintptr_t>(result) % 8) return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
     if (std::isnan(latency_target)) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
     if (B > 0 && !levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
+    bool jit = false;
+    if (B > 0 && (s = want_jit(g, levels, &jit)) != EMO_OK) return s;
     DeviceGuard guard(g->device);
-    return after_launch(emo::launch_select(g->dg, levels, B, latency_target, feasible_mask, result,
-                                           static_cast<hipStream_t>(stream)), "emo_select_policy");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (jit) {
+        hipError_t e = emo::launch_init_result(result, st);
+        if (e == hipSuccess)
+            e = emo::jit_launch_select(g->jm, levels, B, g->dg.tab, latency_target, feasible_mask, result, st);
+        return after_launch(e, "emo_select_policy");
+    }
+    return after_launch(emo::launch_select(g->dg, levels, B, latency_target, feasible_mask, result, st),
+                        "emo_select_policy");
 }
 
 emo_status emo_select_from_results(const float *makespan, const float *energy, int64_t B,

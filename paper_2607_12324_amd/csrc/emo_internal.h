@@ -5,9 +5,14 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include <string>
+#include <vector>
+
 #include "emo.h"
 
 namespace emo {
+
+constexpr int kTablePad = 256;   // extra zeroed table entries: any level byte stays in bounds
 
 // One step of a kernel program: a node visited in topological order.
 //   pack     pack id, or -1 for a node of fixed duration
@@ -53,7 +58,52 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
                         hipStream_t s);
 hipError_t launch_select(const DevGraph &g, const uint8_t *levels, int64_t B, float target,
                          uint32_t *mask, emo_selection *res, hipStream_t s);
+hipError_t launch_init_result(emo_selection *res, hipStream_t s);
+hipError_t launch_empty_result(emo_selection *res, hipStream_t s);
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
                                  uint32_t *mask, emo_selection *res, hipStream_t s);
+
+// ---------------------------------------------------------------- graph-specialised kernels
+
+// One candidate-dependent node of the graph in traversal order.
+struct JitOp {
+    int32_t pack;                  // pack id or -1
+    float cst;                     // start-time floor from candidate-independent predecessors
+    float dur;                     // fixed duration (pack == -1)
+    std::vector<int32_t> in;       // steps of candidate-dependent predecessors
+    std::vector<int32_t> out;      // steps of successors (all candidate-dependent)
+};
+
+struct JitGraph {
+    int32_t P = 0, F = 1;
+    float static_power = 0.f;
+    float t_const = 0.f;
+    bool pack_monotone = true;
+    std::vector<JitOp> ops;
+};
+
+struct JitModule {
+    hipModule_t module = nullptr;
+    hipFunction_t eval = nullptr;
+    hipFunction_t select = nullptr;
+    hipFunction_t slack = nullptr;   // only for graphs small enough to keep every finish time
+    double compile_seconds = 0.0;
+    int block = 256;
+};
+
+// Bytes per level load in generated kernels (16, 4 or 1): the alignment they need.
+inline int jit_level_width(int32_t P) { return P % 16 == 0 ? 16 : (P % 4 == 0 ? 4 : 1); }
+
+std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int block);
+// 0 on success; otherwise *log holds the compiler's or loader's message.
+int jit_compile(const std::string &src, JitModule *out, std::string *log);
+void jit_unload(JitModule *m);
+hipError_t jit_launch_eval(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
+                           float *T, float *E, hipStream_t s);
+hipError_t jit_launch_select(const JitModule &m, const uint8_t *levels, int64_t B,
+                             const float2 *tab, float target, uint32_t *mask, emo_selection *res,
+                             hipStream_t s);
+hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
+                            float *S, float *T, float *E, hipStream_t s);
 
 }  // namespace emo

@@ -18,13 +18,14 @@
 #include <stdint.h>
 
 #include "emo_internal.h"
+#include "emo_select.h"
 
 namespace emo {
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kWave = 64;
-constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kBlock = EMO_BLOCK;
+constexpr int kWave = EMO_WAVE;
+constexpr int kWavesPerBlock = EMO_WAVES_PER_BLOCK;
 constexpr int kEnergyBlock = 64;
 constexpr size_t kLdsBudget = 60 * 1024;   // dynamic LDS, leaves room for static LDS under 64 KB
 
@@ -202,23 +203,12 @@ slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict_
 }
 
 // ---------------------------------------------------------------- selection (Eq. 4)
-//
-// The caller's result struct is the accumulator while a selection runs:
-//   bytes 0..7   u64 key = (fp32 bits of E) << 32 | candidate, minimised (E >= 0, so the bit
-//                pattern orders like the value; ties go to the lower index)
-//   bytes 8..11  u32 count of blocks done (the last block finalises)
-//   bytes 16..23 u64 feasible count
 
-struct Acc {
-    unsigned long long key;
-    unsigned int done;
-    unsigned int pad;
-    unsigned long long count;
-};
-static_assert(sizeof(Acc) == sizeof(emo_selection), "accumulator must overlay emo_selection");
+static_assert(sizeof(EmoAcc) == sizeof(emo_selection), "accumulator must overlay emo_selection");
+static_assert(sizeof(EmoSel) == sizeof(emo_selection), "result layout");
 
 __global__ void init_result(emo_selection *res) {
-    Acc *a = reinterpret_cast<Acc *>(res);
+    EmoAcc *a = reinterpret_cast<EmoAcc *>(res);
     a->key = ~0ull;
     a->done = 0u;
     a->pad = 0u;
@@ -226,69 +216,7 @@ __global__ void init_result(emo_selection *res) {
 }
 
 __global__ void empty_result(emo_selection *res) {
-    res->index = -1;
-    res->energy = __builtin_nanf("");
-    res->makespan = __builtin_nanf("");
-    res->num_feasible = 0;
-}
-
-__device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        unsigned long long o = __shfl_xor(v, off, kWave);
-        v = o < v ? o : v;
-    }
-    return v;
-}
-
-// Block-level reduction of the feasibility mask, count and key.  Returns true in thread 0 of
-// the last block to finish, with *key_out/*count_out the grid-wide results.
-__device__ bool select_reduce(bool active, float T, float E, int64_t c, int64_t B, float target,
-                              uint32_t *mask, emo_selection *res, unsigned long long *key_out,
-                              unsigned long long *count_out) {
-    __shared__ unsigned long long s_key[kWavesPerBlock];
-    __shared__ unsigned int s_cnt[kWavesPerBlock];
-    __shared__ bool s_last;
-    const bool feas = active && (T <= target);
-    const unsigned long long bal = __ballot(feas);
-    const int lane = threadIdx.x % kWave;
-    const int wave = threadIdx.x / kWave;
-    const int64_t wbase = static_cast<int64_t>(blockIdx.x) * kBlock + wave * kWave;
-    if (mask && lane == 0 && wbase < B) {
-        const int64_t nwords = (B + 31) / 32;
-        const int64_t w = wbase / 32;
-        mask[w] = static_cast<uint32_t>(bal);
-        if (w + 1 < nwords) mask[w + 1] = static_cast<uint32_t>(bal >> 32);
-    }
-    unsigned long long key = feas ? (static_cast<unsigned long long>(__float_as_uint(E)) << 32) |
-                                        static_cast<unsigned long long>(static_cast<uint32_t>(c))
-                                  : ~0ull;
-    key = wave_min_u64(key);
-    if (lane == 0) {
-        s_key[wave] = key;
-        s_cnt[wave] = static_cast<unsigned int>(__popcll(bal));
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        unsigned long long bk = s_key[0];
-        unsigned long long bc = s_cnt[0];
-        for (int w = 1; w < kWavesPerBlock; ++w) {
-            bk = s_key[w] < bk ? s_key[w] : bk;
-            bc += s_cnt[w];
-        }
-        Acc *a = reinterpret_cast<Acc *>(res);
-        if (bk != ~0ull) atomicMin(&a->key, bk);
-        if (bc) atomicAdd(&a->count, bc);
-        __threadfence();
-        const unsigned int ticket = atomicAdd(&a->done, 1u);
-        s_last = ticket == gridDim.x - 1;
-        if (s_last) {
-            __threadfence();
-            *key_out = atomicAdd(&a->key, 0ull);
-            *count_out = atomicAdd(&a->count, 0ull);
-        }
-    }
-    __syncthreads();
-    return s_last;
+    emo_write_selection(res, ~0ull, 0ull, 0.f);
 }
 
 __global__ void __launch_bounds__(kBlock)
@@ -297,32 +225,13 @@ select_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float t
               float *gslots, int64_t bpad) {
     Ctx x = make_ctx(g, g.eval.n_slots, tab_lds, slot_lds, gslots, bpad, B);
     Fwd f = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + x.c * g.P, x.sl);
-    __shared__ unsigned long long s_res[2];
     unsigned long long key = 0, count = 0;
-    const bool last = select_reduce(x.active, f.T, f.E, x.c, B, target, mask, res, &key, &count);
-    if (threadIdx.x == 0 && last) {
-        s_res[0] = key;
-        s_res[1] = count;
-    }
-    if (!__syncthreads_or(last)) return;
+    const bool last = emo_select_reduce(x.active, f.T, f.E, x.c, B, target, mask, res, &key, &count);
+    if (!last || threadIdx.x >= kWave) return;
     // the last block re-evaluates the winner to report its makespan
-    key = s_res[0];
-    count = s_res[1];
-    if (threadIdx.x >= kWave) return;
-    const int64_t win = key == ~0ull ? 0 : static_cast<int64_t>(key & 0xffffffffull);
+    const int64_t win = emo_key_index(key);
     Fwd w = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + win * g.P, x.sl);
-    if (threadIdx.x == 0) {
-        if (key == ~0ull) {
-            res->index = -1;
-            res->energy = __builtin_nanf("");
-            res->makespan = __builtin_nanf("");
-        } else {
-            res->index = win;
-            res->energy = __uint_as_float(static_cast<uint32_t>(key >> 32));
-            res->makespan = w.T;
-        }
-        res->num_feasible = static_cast<int64_t>(count);
-    }
+    if (threadIdx.x == 0) emo_write_selection(res, key, count, w.T);
 }
 
 __global__ void __launch_bounds__(kBlock)
@@ -331,23 +240,9 @@ select_results_kernel(const float *__restrict__ T, const float *__restrict__ E, 
     const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const bool active = gid < B;
     const int64_t c = active ? gid : B - 1;
-    const float t = T[c];
-    const float e = E[c];
     unsigned long long key = 0, count = 0;
-    const bool last = select_reduce(active, t, e, c, B, target, mask, res, &key, &count);
-    if (threadIdx.x == 0 && last) {
-        if (key == ~0ull) {
-            res->index = -1;
-            res->energy = __builtin_nanf("");
-            res->makespan = __builtin_nanf("");
-        } else {
-            const int64_t win = static_cast<int64_t>(key & 0xffffffffull);
-            res->index = win;
-            res->energy = __uint_as_float(static_cast<uint32_t>(key >> 32));
-            res->makespan = T[win];
-        }
-        res->num_feasible = static_cast<int64_t>(count);
-    }
+    const bool last = emo_select_reduce(active, T[c], E[c], c, B, target, mask, res, &key, &count);
+    if (last && threadIdx.x == 0) emo_write_selection(res, key, count, T[emo_key_index(key)]);
 }
 
 int64_t grid_for(int64_t B) { return (B + kBlock - 1) / kBlock; }
@@ -419,6 +314,16 @@ hipError_t launch_select(const DevGraph &g, const uint8_t *levels, int64_t B, fl
         if (e == hipSuccess) e = e2;
     }
     return e;
+}
+
+hipError_t launch_init_result(emo_selection *res, hipStream_t s) {
+    hipLaunchKernelGGL(init_result, dim3(1), dim3(1), 0, s, res);
+    return hipGetLastError();
+}
+
+hipError_t launch_empty_result(emo_selection *res, hipStream_t s) {
+    hipLaunchKernelGGL(empty_result, dim3(1), dim3(1), 0, s, res);
+    return hipGetLastError();
 }
 
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,

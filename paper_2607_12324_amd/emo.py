@@ -20,9 +20,10 @@ OK = 0
 STATUS_NAMES = {0: "EMO_OK", 1: "EMO_ERR_INVALID_ARGUMENT", 2: "EMO_ERR_CYCLE",
                 3: "EMO_ERR_OUT_OF_MEMORY", 4: "EMO_ERR_DEVICE", 5: "EMO_ERR_UNSUPPORTED"}
 
-ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info", "emo_graph_topo_order",
+ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
+                "emo_graph_set_kernel_mode", "emo_graph_topo_order",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_select_from_results",
-                "emo_status_string", "emo_last_error")
+                "emo_graph_specialized_source", "emo_status_string", "emo_last_error")
 
 
 class EmoError(RuntimeError):
@@ -37,10 +38,14 @@ class GraphInfo(ctypes.Structure):
                 ("num_dynamic_nodes", ctypes.c_int32), ("num_dynamic_edges", ctypes.c_int32),
                 ("eval_slots", ctypes.c_int32), ("max_depth", ctypes.c_int32),
                 ("const_makespan", ctypes.c_float), ("device", ctypes.c_int32),
-                ("pack_order_monotone", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("pack_order_monotone", ctypes.c_int32), ("kernel_mode", ctypes.c_int32),
+                ("specialized", ctypes.c_int32), ("compile_seconds", ctypes.c_float)]
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+KERNELS_AUTO, KERNELS_INTERPRETED, KERNELS_SPECIALIZED = 0, 1, 2
 
 
 def _load_library():
@@ -53,11 +58,13 @@ def _load_library():
         "emo_load_graph": [i32, i32, P, P, P, P, i32, i32, P, P, f32, i32, P],
         "emo_free_graph": [P],
         "emo_graph_get_info": [P, P],
+        "emo_graph_set_kernel_mode": [P, i32],
         "emo_graph_topo_order": [P, P, P],
         "emo_eval_policies": [P, P, i64, P, P, P],
         "emo_slack": [P, P, i64, P, i32, P, P, P],
         "emo_select_policy": [P, P, i64, f32, P, P, P],
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
+        "emo_graph_specialized_source": [P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -126,7 +133,7 @@ def parse_selection(res) -> Selection:
 class EmoGraph:
     """A graph loaded into libemo (emo_load_graph).  `device=-1` loads host-only."""
 
-    def __init__(self, graph, device: int = 0):
+    def __init__(self, graph, device: int = 0, kernel_mode: int | None = None):
         self._h = ctypes.c_void_p()
         src = _np(graph.edge_src, np.int32)
         dst = _np(graph.edge_dst, np.int32)
@@ -142,6 +149,11 @@ class EmoGraph:
         self.num_packs = int(graph.num_packs)
         self.num_levels = int(graph.num_levels)
         self.device = int(device)
+        if kernel_mode is not None:
+            self.set_kernel_mode(kernel_mode)
+
+    def set_kernel_mode(self, mode: int):
+        _check(lib.emo_graph_set_kernel_mode(self._h, int(mode)))
 
     def close(self):
         if getattr(self, "_h", None) and self._h.value:
@@ -158,6 +170,13 @@ class EmoGraph:
         inf = GraphInfo()
         _check(lib.emo_graph_get_info(self._h, ctypes.byref(inf)))
         return inf.as_dict()
+
+    def specialized_source(self) -> str:
+        n = ctypes.c_int64(0)
+        _check(lib.emo_graph_specialized_source(self._h, None, ctypes.byref(n)))
+        buf = ctypes.create_string_buffer(n.value)
+        _check(lib.emo_graph_specialized_source(self._h, buf, ctypes.byref(n)))
+        return buf.value.decode()
 
     def topo_order(self):
         order = np.empty(self.num_nodes, dtype=np.int32)

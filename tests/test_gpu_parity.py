@@ -31,10 +31,14 @@ def host(t):
     return t.detach().cpu().numpy()
 
 
-def run_all(torch, emo, g, rows, targets, exact=True, per_node=True, what=""):
+MODES = {"auto": 0, "interpreted": 1}
+
+
+def run_all(torch, emo, g, rows, targets, exact=True, per_node=True, what="", mode=0):
     """eval, slack (per pack and per node), fused select and select-from-results vs oracle."""
-    print(f"[case] {what}: V={g.num_nodes} P={g.num_packs} F={g.num_levels} B={len(rows)}", flush=True)
-    gh = emo.EmoGraph(g, device=0)
+    print(f"[case] {what} mode={mode}: V={g.num_nodes} P={g.num_packs} F={g.num_levels} B={len(rows)}",
+          flush=True)
+    gh = emo.EmoGraph(g, device=0, kernel_mode=mode)
     lv = dev(torch, rows)
     B = len(rows)
     T, E = gh.eval_policies(lv)
@@ -81,7 +85,8 @@ def test_handworked_example(torch, emo):
         res, mask = gh.select_policy(dev(torch, rows), s["target"])
         sel = emo.parse_selection(res)
         assert sel.index == s["index"] and sel.num_feasible == s["num_feasible"], (s, sel)
-    run_all(torch, emo, g, rows, [16.8, 18.0, 20.0, 22.0, 15.9], what="handworked")
+    for mode in MODES.values():
+        run_all(torch, emo, g, rows, [16.8, 18.0, 20.0, 22.0, 15.9], what="handworked", mode=mode)
 
 
 @pytest.mark.parametrize("seed", range(8))
@@ -96,7 +101,8 @@ def test_random_dags_on_grid(torch, emo, seed):
         rows = pins.random_rows(rng, g, B)
         T_or, _ = oracle.eval_batch(g, rows)
         targets = [float(np.quantile(T_or, q)) for q in (0.0, 0.3, 0.9)] + [float(T_or.min()) - 1.0]
-        run_all(torch, emo, g, rows, targets, exact=True, what=f"random seed={seed} i={i}")
+        for mode in MODES.values():
+            run_all(torch, emo, g, rows, targets, exact=True, what=f"random seed={seed} i={i}", mode=mode)
 
 
 @pytest.mark.parametrize("seed", range(3))
@@ -109,8 +115,9 @@ def test_random_dags_off_grid(torch, emo, seed):
         B = int(rng.integers(100, 3000))
         rows = pins.random_rows(rng, g, B)
         T_or, _ = oracle.eval_batch(g, rows)
-        run_all(torch, emo, g, rows, [float(np.quantile(T_or, 0.5))], exact=False,
-                what=f"offgrid seed={seed} i={i}")
+        for mode in MODES.values():
+            run_all(torch, emo, g, rows, [float(np.quantile(T_or, 0.5))], exact=False,
+                    what=f"offgrid seed={seed} i={i}", mode=mode)
 
 
 def test_large_slot_count_uses_device_scratch(torch, emo):
@@ -134,9 +141,10 @@ def test_large_slot_count_uses_device_scratch(torch, emo):
     run_all(torch, emo, g, rows, [float(np.median(T_or))], what="antichain")
 
 
-def test_edge_cases(torch, emo):
+@pytest.mark.parametrize("mode", [0, 1], ids=["auto", "interpreted"])
+def test_edge_cases(torch, emo, mode):
     g = pins.graph_from_golden(pins.load_golden())
-    gh = emo.EmoGraph(g, device=0)
+    gh = emo.EmoGraph(g, device=0, kernel_mode=mode)
     # B = 0
     empty = torch.zeros((0, g.num_packs), dtype=torch.uint8, device="cuda")
     T, E = gh.eval_policies(empty)
@@ -161,7 +169,7 @@ def test_edge_cases(torch, emo):
     rows = np.tile(np.asarray([[0, 1, 0]], np.uint8), (1000, 1))
     res, _ = gh.select_policy(dev(torch, rows), 1e9)
     assert emo.parse_selection(res).index == 0
-    rows[:500] = 1   # slower... no: faster, more energy; the cheapest identical rows start at 500
+    rows[:500] = 1   # all packs at the higher level: more energy, so the cheapest rows start at 500
     res, _ = gh.select_policy(dev(torch, rows), 1e9)
     T_or, E_or = oracle.eval_batch(g, rows)
     assert emo.parse_selection(res).index == oracle.select(T_or, E_or, 1e9)[0]
@@ -173,23 +181,24 @@ def test_edge_cases(torch, emo):
     z = np.zeros(0, np.int32)
     zf = np.zeros((0, 1), np.float32)
     ge = synth.Graph("empty", 0, z, z, z, np.zeros(0, np.float32), 0, 1, zf, zf, 0.5)
-    gh0 = emo.EmoGraph(ge, device=0)
+    gh0 = emo.EmoGraph(ge, device=0, kernel_mode=mode)
     T, E = gh0.eval_policies(torch.zeros((5, 0), dtype=torch.uint8, device="cuda"))
     assert host(T).tolist() == [0.0] * 5 and host(E).tolist() == [0.0] * 5
     gn = synth.Graph("nopacks", 3, np.asarray([0, 1], np.int32), np.asarray([1, 2], np.int32),
                      np.full(3, -1, np.int32), np.asarray([1.0, 2.0, 4.0], np.float32), 0, 1,
                      zf, zf, 0.5)
-    ghn = emo.EmoGraph(gn, device=0)
+    ghn = emo.EmoGraph(gn, device=0, kernel_mode=mode)
     T, E = ghn.eval_policies(torch.zeros((3, 0), dtype=torch.uint8, device="cuda"))
     assert host(T).tolist() == [7.0] * 3 and host(E).tolist() == [3.5] * 3
     SN = host(ghn.slack(torch.zeros((3, 0), dtype=torch.uint8, device="cuda"), per_node=True))
     assert SN.tolist() == [[0.0, 0.0, 0.0]] * 3
 
 
-def test_determinism(torch, emo):
+@pytest.mark.parametrize("mode", [0, 1], ids=["auto", "interpreted"])
+def test_determinism(torch, emo, mode):
     g = synth.config_graph(3)
     rows = synth.config_policies(3, g, 0, 20000)
-    gh = emo.EmoGraph(g, device=0)
+    gh = emo.EmoGraph(g, device=0, kernel_mode=mode)
     lv = dev(torch, rows)
     a = [host(x).copy() for x in gh.eval_policies(lv)]
     b = [host(x).copy() for x in gh.eval_policies(lv)]
@@ -218,6 +227,19 @@ def test_workload_full_batch(torch, emo, k):
     lv = dev(torch, rows)
     T, E = gh.eval_policies(lv)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, spec.name)
+    inf = gh.info()
+    assert bool(inf["specialized"] & 1) == (k <= 3), inf
+    if k <= 3:
+        # the interpreting kernels on the same batch: bit-identical
+        gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+        Ti, Ei = gi.eval_policies(lv)
+        assert torch.equal(Ti.view(torch.int32), T.view(torch.int32))
+        assert torch.equal(Ei.view(torch.int32), E.view(torch.int32))
+        tgt = float(np.float32(spec.targets[0] * (float(np.min(T_or)) if spec.exhaustive else float(T_or[0]))))
+        res_i, mask_i = gi.select_policy(lv, tgt)
+        parity.assert_selection(emo.parse_selection(res_i), emo.unpack_mask(mask_i, B), T_or, E_or,
+                                tgt, True, f"{spec.name} interpreted select")
+        gi.close()
     for r in spec.targets:
         tgt = float(np.float32(r * T0))
         res, mask = gh.select_policy(lv, tgt)

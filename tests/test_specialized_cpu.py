@@ -1,0 +1,101 @@
+"""Graph-specialised kernels on the CPU: the generated HIP source compiles for gfx950 with the
+run-time compiler, spills no registers, and uses no packed fp32 instructions."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2607_12324_amd import synth
+
+OBJDUMP = "/opt/rocm/llvm/bin/llvm-objdump"
+READELF = "/opt/rocm/llvm/bin/llvm-readelf"
+OPTS = [b"--offload-arch=gfx950", b"-O3", b"-std=c++17", b"-Xclang", b"-target-feature", b"-Xclang",
+        b"-packed-fp32-ops"]
+
+
+@pytest.fixture(scope="module")
+def emo():
+    from paper_2607_12324_amd import emo as mod
+    return mod
+
+
+@pytest.fixture(scope="module")
+def hiprtc():
+    return ctypes.CDLL("libhiprtc.so")
+
+
+def compile_source(hiprtc, src: str, tmp_path) -> str:
+    prog = ctypes.c_void_p()
+    assert hiprtc.hiprtcCreateProgram(ctypes.byref(prog), src.encode(), b"k.hip", 0, None, None) == 0
+    opts = (ctypes.c_char_p * len(OPTS))(*OPTS)
+    rc = hiprtc.hiprtcCompileProgram(prog, len(OPTS), opts)
+    n = ctypes.c_size_t()
+    hiprtc.hiprtcGetProgramLogSize(prog, ctypes.byref(n))
+    log = ctypes.create_string_buffer(n.value + 1)
+    hiprtc.hiprtcGetProgramLog(prog, log)
+    assert rc == 0, log.value.decode()[-3000:]
+    hiprtc.hiprtcGetCodeSize(prog, ctypes.byref(n))
+    code = ctypes.create_string_buffer(n.value)
+    hiprtc.hiprtcGetCode(prog, code)
+    hiprtc.hiprtcDestroyProgram(ctypes.byref(prog))
+    path = os.path.join(str(tmp_path), "k.co")
+    with open(path, "wb") as f:
+        f.write(code.raw)
+    return path
+
+
+def kernel_notes(path):
+    out = subprocess.run([READELF, "--notes", path], capture_output=True, text=True, check=True).stdout
+    names = re.findall(r"\.name:\s+(\S+)", out)
+    spills = [int(x) for x in re.findall(r"\.vgpr_spill_count:\s+(\d+)", out)]
+    vgprs = [int(x) for x in re.findall(r"\.vgpr_count:\s+(\d+)", out)]
+    return dict(zip(names, zip(vgprs, spills)))
+
+
+def check_code_object(path, expect):
+    notes = kernel_notes(path)
+    for k in expect:
+        assert k in notes, (k, notes)
+    for name, (vgpr, spill) in notes.items():
+        assert spill == 0, f"{name} spills {spill} VGPRs"
+    asm = subprocess.run([OBJDUMP, "-d", "--mcpu=gfx950", path], capture_output=True, text=True,
+                         check=True).stdout
+    assert not re.search(r"v_pk_(add|mul|fma)_f32", asm), "packed fp32 arithmetic in specialised kernels"
+    assert "scratch_" not in asm
+    return notes, asm
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_workload_kernels_compile_without_spills(emo, hiprtc, tmp_path, k):
+    g = synth.config_graph(k)
+    src = emo.EmoGraph(g, device=-1).specialized_source()
+    path = compile_source(hiprtc, src, tmp_path)
+    expect = ["emo_sp_eval", "emo_sp_select"] + (["emo_sp_slack"] if g.num_packs <= 160 else [])
+    notes, asm = check_code_object(path, expect)
+    # the forward pass is straight-line: roughly five vector instructions per pack
+    body = asm.split("<emo_sp_select>:")[1].split("s_endpgm")[0]
+    valu = len(re.findall(r"^\s+v_", body, flags=re.M))
+    assert valu < 6.5 * g.num_packs + 200, valu
+
+
+def test_large_graph_is_not_specialised(emo):
+    g = synth.config_graph(4)
+    gh = emo.EmoGraph(g, device=-1)
+    with pytest.raises(emo.EmoError) as ei:
+        gh.specialized_source()
+    assert ei.value.status == 5
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_random_graph_kernels_compile(emo, hiprtc, tmp_path, seed):
+    """Odd shapes: pack counts not multiple of 4 or 16, non-power-of-two level counts,
+    shuffled pack ids (no staged slack output), fixed nodes between packs."""
+    rng = np.random.default_rng(300 + seed)
+    for i, (V, F) in enumerate([(7, 3), (40, 16), (90, 5), (150, 200)]):
+        g = synth.random_dag(rng, V, 3.0 / V, 0.7, F, shuffle_packs=bool(i % 2))
+        src = emo.EmoGraph(g, device=-1).specialized_source()
+        path = compile_source(hiprtc, src, tmp_path)
+        check_code_object(path, ["emo_sp_eval", "emo_sp_select"])
