@@ -384,7 +384,7 @@ int ensure_jit(emo_graph_s *g) {
     DeviceGuard guard(g->device);
     emo::JitModule m;
     std::string log;
-    if (emo::jit_compile(src, &m, &log) != 0) {
+    if (emo::jit_compile(src, g->jit_slack_eligible, &m, &log) != 0) {
         g->jit_log = log;
         g->jit_state = -1;
         g->info.specialized |= 4;

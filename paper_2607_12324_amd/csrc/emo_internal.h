@@ -96,7 +96,7 @@ inline int jit_level_width(int32_t P) { return P % 16 == 0 ? 16 : (P % 4 == 0 ? 
 
 std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int block);
 // 0 on success; otherwise *log holds the compiler's or loader's message.
-int jit_compile(const std::string &src, JitModule *out, std::string *log);
+int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log);
 void jit_unload(JitModule *m);
 hipError_t jit_launch_eval(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
                            float *T, float *E, hipStream_t s);

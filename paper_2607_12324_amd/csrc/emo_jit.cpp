@@ -371,7 +371,7 @@ __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_ba
     return o.str();
 }
 
-int jit_compile(const std::string &src, JitModule *out, std::string *log) {
+int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log) {
     hiprtcProgram prog;
     if (hiprtcCreateProgram(&prog, src.c_str(), "emo_specialised.hip", 0, nullptr, nullptr) !=
         HIPRTC_SUCCESS) {
@@ -403,19 +403,20 @@ int jit_compile(const std::string &src, JitModule *out, std::string *log) {
     hiprtcDestroyProgram(&prog);
     hipError_t e = hipModuleLoadData(&out->module, code.data());
     if (e != hipSuccess) {
+        (void)hipGetLastError();
         *log = std::string("hipModuleLoadData: ") + hipGetErrorString(e);
         out->module = nullptr;
         return 2;
     }
     if (hipModuleGetFunction(&out->eval, out->module, "emo_sp_eval") != hipSuccess ||
-        hipModuleGetFunction(&out->select, out->module, "emo_sp_select") != hipSuccess) {
+        hipModuleGetFunction(&out->select, out->module, "emo_sp_select") != hipSuccess ||
+        (with_slack && hipModuleGetFunction(&out->slack, out->module, "emo_sp_slack") != hipSuccess)) {
+        (void)hipGetLastError();   // clear the runtime's sticky error
         *log = "specialised kernels missing from the module";
         (void)hipModuleUnload(out->module);
-        out->module = nullptr;
+        *out = JitModule();
         return 2;
     }
-    if (hipModuleGetFunction(&out->slack, out->module, "emo_sp_slack") != hipSuccess)
-        out->slack = nullptr;
     return 0;
 }
 
