@@ -179,6 +179,19 @@ emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t num_c
                              emo_selection *result, void *stream);
 
 /*
+ * The whole hot path in one pass over the candidates, as one kernel launch (plus a tiny one
+ * that initialises the selection accumulator): makespan and energy (Eq. 1-3), slack of every
+ * pack or node when `slack` is given, and the feasibility mask and least-energy feasible
+ * candidate under `latency_target` (Eq. 4) when `feasible_mask` or `result` is given.
+ * Every output is optional (NULL); their layouts are those of emo_eval_policies, emo_slack and
+ * emo_select_policy.  latency_target is ignored without mask and result.
+ */
+emo_status emo_evaluate(emo_graph_t g, const uint8_t *levels, int64_t num_candidates,
+                        float *makespan, float *energy, float *slack, int32_t per_node,
+                        float latency_target, uint32_t *feasible_mask, emo_selection *result,
+                        void *stream);
+
+/*
  * The same selection from makespans and energies already computed (e.g. a second latency
  * target over one evaluation).  makespan, energy: device float [B].
  */

@@ -603,64 +603,85 @@ emo_status emo_graph_topo_order(emo_graph_t g, int32_t *order, int32_t *depth) {
     return ok();
 }
 
-emo_status emo_eval_policies(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
-                             float *energy, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The hot path for every batch entry point: forward pass, optional backward slack pass,
+// optional feasibility mask and selection, in one kernel launch (plus the initialisation of the
+// selection accumulator).
+emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
+                    float *energy, float *slack, int32_t per_node, float target, uint32_t *mask,
+                    emo_selection *result, void *stream) {
     emo_status s = check_batch(g, B);
     if (s != EMO_OK) return s;
-    if (B == 0 || (!makespan && !energy)) return ok();
+    if (result && reinterpret_cast<uintptr_t>(result) % 8)
+        return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
+    if ((result || mask) && std::isnan(target))
+        return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (B == 0) {
+        if (!result) return ok();
+        DeviceGuard guard(g->device);
+        return after_launch(emo::launch_empty_result(result, st), "empty selection");
+    }
+    if (!makespan && !energy && !slack && !mask && !result) return ok();
     if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
     bool jit = false;
-    if ((s = want_jit(g, levels, &jit)) != EMO_OK) return s;
+    if (!slack || (!per_node && g->jit_slack_eligible)) {
+        if ((s = want_jit(g, levels, &jit)) != EMO_OK) return s;
+        if (slack) jit = jit && g->jm.slack && (!g->jit_slack_staged || aligned(slack, 16));
+    }
     DeviceGuard guard(g->device);
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    if (jit) return after_launch(emo::jit_launch_eval(g->jm, levels, B, g->dg.tab, makespan, energy, st),
-                                 "emo_eval_policies");
-    return after_launch(emo::launch_eval(g->dg, levels, B, makespan, energy, st), "emo_eval_policies");
+    hipError_t e = hipSuccess;
+    if (result) e = emo::launch_init_result(result, st);
+    if (e != hipSuccess) return after_launch(e, "selection init");
+    if (slack) {
+        if (jit) {
+            e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy, target,
+                                      mask, result, st);
+        } else {
+            const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
+            e = emo::launch_slack(g->dg, prog, per_node ? g->V : g->P, levels, B, slack, makespan,
+                                  energy, target, mask, result, st);
+        }
+    } else if (jit) {
+        e = emo::jit_launch_forward(g->jm, levels, B, g->dg.tab, makespan, energy, target, mask,
+                                    result, st);
+    } else {
+        e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, result, st);
+    }
+    return after_launch(e, "evaluation");
+}
+
+}  // namespace
+
+extern "C" {
+
+emo_status emo_eval_policies(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
+                             float *energy, void *stream) {
+    return evaluate(g, levels, B, makespan, energy, nullptr, 0, 0.f, nullptr, nullptr, stream);
 }
 
 emo_status emo_slack(emo_graph_t g, const uint8_t *levels, int64_t B, float *slack,
                      int32_t per_node, float *makespan, float *energy, void *stream) {
-    emo_status s = check_batch(g, B);
-    if (s != EMO_OK) return s;
-    if (B == 0) return ok();
-    if (!slack) return fail(EMO_ERR_INVALID_ARGUMENT, "slack is NULL");
-    if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
-    bool jit = false;
-    if (!per_node && g->jit_slack_eligible) {
-        if ((s = want_jit(g, levels, &jit)) != EMO_OK) return s;
-        jit = jit && g->jm.slack && (!g->jit_slack_staged || aligned(slack, 16));
-    }
-    DeviceGuard guard(g->device);
-    if (jit)
-        return after_launch(emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy,
-                                                  static_cast<hipStream_t>(stream)), "emo_slack");
-    const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
-    int32_t cols = per_node ? g->V : g->P;
-    return after_launch(emo::launch_slack(g->dg, prog, cols, levels, B, slack, makespan, energy,
-                                          static_cast<hipStream_t>(stream)), "emo_slack");
+    if (!slack && B > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "slack is NULL");
+    return evaluate(g, levels, B, makespan, energy, slack, per_node, 0.f, nullptr, nullptr, stream);
 }
 
 emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t B,
                              float latency_target, uint32_t *feasible_mask,
                              emo_selection *result, void *stream) {
-    emo_status s = check_batch(g, B);
-    if (s != EMO_OK) return s;
     if (!result) return fail(EMO_ERR_INVALID_ARGUMENT, "result is NULL");
-    if (reinterpret_cast<uintptr_t>(result) % 8) return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
-    if (std::isnan(latency_target)) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
-    if (B > 0 && !levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
-    bool jit = false;
-    if (B > 0 && (s = want_jit(g, levels, &jit)) != EMO_OK) return s;
-    DeviceGuard guard(g->device);
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    if (jit) {
-        hipError_t e = emo::launch_init_result(result, st);
-        if (e == hipSuccess)
-            e = emo::jit_launch_select(g->jm, levels, B, g->dg.tab, latency_target, feasible_mask, result, st);
-        return after_launch(e, "emo_select_policy");
-    }
-    return after_launch(emo::launch_select(g->dg, levels, B, latency_target, feasible_mask, result, st),
-                        "emo_select_policy");
+    return evaluate(g, levels, B, nullptr, nullptr, nullptr, 0, latency_target, feasible_mask,
+                    result, stream);
+}
+
+emo_status emo_evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
+                        float *energy, float *slack, int32_t per_node, float latency_target,
+                        uint32_t *feasible_mask, emo_selection *result, void *stream) {
+    return evaluate(g, levels, B, makespan, energy, slack, per_node, latency_target,
+                    feasible_mask, result, stream);
 }
 
 emo_status emo_select_from_results(const float *makespan, const float *energy, int64_t B,

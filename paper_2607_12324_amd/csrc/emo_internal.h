@@ -51,13 +51,13 @@ struct DevGraph {
     DevProgram slack_node;         // forward + backward over every node
 };
 
-hipError_t launch_eval(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
-                       hipStream_t s);
+// Interpreting kernels.  T, E, mask, res may each be NULL; res != NULL requires an accumulator
+// initialised by launch_init_result on the same stream.
+hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
+                          float target, uint32_t *mask, emo_selection *res, hipStream_t s);
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
-                        hipStream_t s);
-hipError_t launch_select(const DevGraph &g, const uint8_t *levels, int64_t B, float target,
-                         uint32_t *mask, emo_selection *res, hipStream_t s);
+                        float target, uint32_t *mask, emo_selection *res, hipStream_t s);
 hipError_t launch_init_result(emo_selection *res, hipStream_t s);
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s);
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
@@ -84,8 +84,7 @@ struct JitGraph {
 
 struct JitModule {
     hipModule_t module = nullptr;
-    hipFunction_t eval = nullptr;
-    hipFunction_t select = nullptr;
+    hipFunction_t select = nullptr;  // forward pass with optional outputs and selection
     hipFunction_t slack = nullptr;   // only for graphs small enough to keep every finish time
     double compile_seconds = 0.0;
     int block = 256;
@@ -98,12 +97,14 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
 // 0 on success; otherwise *log holds the compiler's or loader's message.
 int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log);
 void jit_unload(JitModule *m);
-hipError_t jit_launch_eval(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                           float *T, float *E, hipStream_t s);
-hipError_t jit_launch_select(const JitModule &m, const uint8_t *levels, int64_t B,
-                             const float2 *tab, float target, uint32_t *mask, emo_selection *res,
-                             hipStream_t s);
+// Forward pass; T, E, mask, res may each be NULL (res != NULL requires an initialised
+// accumulator, see launch_init_result).
+hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,
+                              const float2 *tab, float *T, float *E, float target, uint32_t *mask,
+                              emo_selection *res, hipStream_t s);
+// Forward + backward slack pass with the same optional outputs.
 hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                            float *S, float *T, float *E, hipStream_t s);
+                            float *S, float *T, float *E, float target, uint32_t *mask,
+                            emo_selection *res, hipStream_t s);
 
 }  // namespace emo

@@ -174,9 +174,9 @@ std::string est_expr(const JitGraph &g, int i, const char *prefix) {
     return e;
 }
 
-// Forward pass: declares f<i> (finish time) for every step, t<i> (duration) for packs, and
-// T, E, bad.
-void emit_forward(std::ostringstream &o, const JitGraph &g, bool keep_t) {
+// Forward pass: declares f<i> (finish time) for every step, and T, E, bad; records the
+// expression of each pack step's level byte in *level_expr.
+void emit_forward(std::ostringstream &o, const JitGraph &g, std::vector<std::string> *level_expr) {
     LevelPlan lp;
     lp.P = g.P;
     lp.F = g.F;
@@ -203,12 +203,12 @@ void emit_forward(std::ostringstream &o, const JitGraph &g, bool keep_t) {
         }
         if (op.pack >= 0) {
             std::string b = lp.byte_of(op.pack);
+            if (level_expr) (*level_expr)[i] = b;
             o << "  const float2 te" << i << " = tab[" << static_cast<long long>(op.pack) * g.F
               << " + " << b << "];\n";
             o << "  float f" << i << " = " << est_expr(g, i, "f") << " + te" << i << ".x;\n";
             o << "  eb += te" << i << ".y;\n";
             if (++npk % 64 == 0) o << "  ed += (double)eb;\n  eb = 0.f;\n";
-            (void)keep_t;
         } else {
             o << "  float f" << i << " = " << est_expr(g, i, "f") << " + " << flit(op.dur) << ";\n";
         }
@@ -220,10 +220,14 @@ void emit_forward(std::ostringstream &o, const JitGraph &g, bool keep_t) {
     o << "  if (isbad) { T = __builtin_nanf(\"\"); E = __builtin_nanf(\"\"); }\n";
 }
 
-// Backward pass for per-pack slack (requires the forward's f<i>, te<i>, T).
-void emit_backward(std::ostringstream &o, const JitGraph &g, bool staged) {
+// Backward pass for per-pack slack (requires the forward's f<i>, T and the level words).
+// Pack durations are read from the table again through a pointer the compiler cannot
+// identify with the forward's, so the forward's loads are not kept alive for the whole pass.
+void emit_backward(std::ostringstream &o, const JitGraph &g, bool staged,
+                   const std::vector<std::string> &level_expr) {
     const int n = static_cast<int>(g.ops.size());
     o << "  const float Tb = isbad ? 0.f : T;\n";
+    o << "  const float2 *tabb = tab;\n  __asm__ __volatile__(\"\" : \"+v\"(tabb));\n";
     for (int i = n - 1; i >= 0; --i) {
         const JitOp &op = g.ops[i];
         std::string lft;
@@ -238,7 +242,12 @@ void emit_backward(std::ostringstream &o, const JitGraph &g, bool staged) {
             }
         }
         o << "  const float lf" << i << " = " << lft << ";\n";
-        std::string dur = op.pack >= 0 ? "te" + std::to_string(i) + ".x" : flit(op.dur);
+        std::string dur = flit(op.dur);
+        if (op.pack >= 0) {
+            o << "  const float t" << i << " = tabb[" << static_cast<long long>(op.pack) * g.F << " + "
+              << level_expr[i] << "].x;\n";
+            dur = "t" + std::to_string(i);
+        }
         if (!op.in.empty()) o << "  const float s" << i << " = lf" << i << " - " << dur << ";\n";
         if (op.pack >= 0) {
             const int p = op.pack;
@@ -281,23 +290,17 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
 
     // forward function body as a macro-free inline function over (row, tab)
     std::ostringstream fwd;
-    emit_forward(fwd, g, false);
+    emit_forward(fwd, g, nullptr);
 
     o << "struct EmoFwd { float T; float E; };\n";
     o << "__device__ __forceinline__ EmoFwd emo_forward(const u8 *__restrict__ row, "
          "const float2 *__restrict__ tab) {\n"
       << fwd.str() << "  EmoFwd r; r.T = T; r.E = E; return r;\n}\n";
 
-    o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
-         "emo_sp_eval(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
-         "            float *__restrict__ To, float *__restrict__ Eo) {\n"
-         "  EMO_TABLE_DECL\n  EMO_LANE_SETUP\n"
-         "  const EmoFwd r = emo_forward(lv + cand * "
-      << g.P << "LL, tab);\n"
-         "  if (active) { if (To) To[cand] = r.T; if (Eo) Eo[cand] = r.E; }\n}\n";
-
+    // forward pass, optional makespan/energy outputs, optional feasibility mask and selection
     o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
          "emo_sp_select(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
+         "              float *__restrict__ To, float *__restrict__ Eo,\n"
          "              float target, unsigned int *__restrict__ mask, void *res) {\n"
          "  EMO_TABLE_DECL\n  EMO_LANE_SETUP\n"
          "  unsigned long long key = 0, count = 0;\n"
@@ -306,6 +309,8 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
          "    const EmoFwd r = emo_forward(lv + cand * "
       << g.P << "LL, tab);\n"
          "    if (pass == 0) {\n"
+         "      if (active) { if (To) To[cand] = r.T; if (Eo) Eo[cand] = r.E; }\n"
+         "      if (!mask && !res) return;\n"
          "      if (!emo_select_reduce(active, r.T, r.E, cand, B, target, mask, res, &key, &count)) return;\n"
          "      if (threadIdx.x >= EMO_WAVE) return;\n"
          "      cand = emo_key_index(key);\n"
@@ -349,7 +354,8 @@ __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_ba
         }
         o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
              "emo_sp_slack(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
-             "             float *__restrict__ S, float *__restrict__ To, float *__restrict__ Eo) {\n"
+             "             float *__restrict__ S, float *__restrict__ To, float *__restrict__ Eo,\n"
+             "             float target, unsigned int *__restrict__ mask, void *res) {\n"
              "  EMO_TABLE_DECL\n  EMO_LANE_SETUP\n"
              "  const int lane = threadIdx.x % EMO_WAVE;\n"
              "  const int wave = threadIdx.x / EMO_WAVE;\n"
@@ -362,10 +368,19 @@ __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_ba
                  "  unsigned int *stg_bad = bad_all[wave];\n";
         }
         o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
-        emit_forward(o, g, true);
+        std::vector<std::string> level_expr(g.ops.size());
+        emit_forward(o, g, &level_expr);
         o << "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n";
         if (staged) o << "  stg_bad[lane] = isbad ? 1u : 0u;\n";
-        emit_backward(o, g, staged);
+        emit_backward(o, g, staged, level_expr);
+        // selection after the slack pass; the last block re-evaluates the winner's makespan
+        o << "  if (!mask && !res) return;\n"
+             "  unsigned long long key = 0, count = 0;\n"
+             "  if (!emo_select_reduce(active, T, E, cand, B, target, mask, res, &key, &count)) return;\n"
+             "  if (threadIdx.x >= EMO_WAVE) return;\n"
+             "  const EmoFwd w = emo_forward(lv + emo_key_index(key) * "
+          << g.P << "LL, tab);\n"
+             "  if (threadIdx.x == 0) emo_write_selection(res, key, count, w.T);\n";
         o << "}\n";
     }
     return o.str();
@@ -408,8 +423,7 @@ int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::st
         out->module = nullptr;
         return 2;
     }
-    if (hipModuleGetFunction(&out->eval, out->module, "emo_sp_eval") != hipSuccess ||
-        hipModuleGetFunction(&out->select, out->module, "emo_sp_select") != hipSuccess ||
+    if (hipModuleGetFunction(&out->select, out->module, "emo_sp_select") != hipSuccess ||
         (with_slack && hipModuleGetFunction(&out->slack, out->module, "emo_sp_slack") != hipSuccess)) {
         (void)hipGetLastError();   // clear the runtime's sticky error
         *log = "specialised kernels missing from the module";
@@ -429,26 +443,21 @@ namespace {
 unsigned grid_of(int64_t B, int block) { return static_cast<unsigned>((B + block - 1) / block); }
 }  // namespace
 
-hipError_t jit_launch_eval(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                           float *T, float *E, hipStream_t s) {
-    long long b = B;
-    void *args[] = {&levels, &b, &tab, &T, &E};
-    return hipModuleLaunchKernel(m.eval, grid_of(B, m.block), 1, 1, m.block, 1, 1, 0, s, args, nullptr);
-}
-
-hipError_t jit_launch_select(const JitModule &m, const uint8_t *levels, int64_t B,
-                             const float2 *tab, float target, uint32_t *mask, emo_selection *res,
-                             hipStream_t s) {
+hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,
+                              const float2 *tab, float *T, float *E, float target, uint32_t *mask,
+                              emo_selection *res, hipStream_t s) {
     long long b = B;
     void *r = res;
-    void *args[] = {&levels, &b, &tab, &target, &mask, &r};
+    void *args[] = {&levels, &b, &tab, &T, &E, &target, &mask, &r};
     return hipModuleLaunchKernel(m.select, grid_of(B, m.block), 1, 1, m.block, 1, 1, 0, s, args, nullptr);
 }
 
 hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                            float *S, float *T, float *E, hipStream_t s) {
+                            float *S, float *T, float *E, float target, uint32_t *mask,
+                            emo_selection *res, hipStream_t s) {
     long long b = B;
-    void *args[] = {&levels, &b, &tab, &S, &T, &E};
+    void *r = res;
+    void *args[] = {&levels, &b, &tab, &S, &T, &E, &target, &mask, &r};
     return hipModuleLaunchKernel(m.slack, grid_of(B, m.block), 1, 1, m.block, 1, 1, 0, s, args, nullptr);
 }
 

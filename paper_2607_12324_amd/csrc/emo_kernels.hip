@@ -152,21 +152,37 @@ __device__ Ctx make_ctx(const DevGraph &g, int n_slots, bool tab_lds, bool slot_
     return x;
 }
 
+// Winner's makespan for the selection record: the last block re-evaluates the winner.
+__device__ void finish_selection(const DevGraph &g, const Ctx &x, const uint8_t *levels,
+                                 unsigned long long key, unsigned long long count,
+                                 emo_selection *res) {
+    if (threadIdx.x >= kWave) return;
+    const int64_t win = emo_key_index(key);
+    Fwd w = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + win * g.P, x.sl);
+    if (threadIdx.x == 0) emo_write_selection(res, key, count, w.T);
+}
+
+// Forward pass; makespan/energy outputs, the mask and the selection are each optional.
 __global__ void __launch_bounds__(kBlock)
-eval_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ T_out,
-            float *__restrict__ E_out, bool tab_lds, bool slot_lds, float *gslots, int64_t bpad) {
+forward_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ T_out,
+               float *__restrict__ E_out, float target, uint32_t *__restrict__ mask,
+               emo_selection *res, bool tab_lds, bool slot_lds, float *gslots, int64_t bpad) {
     Ctx x = make_ctx(g, g.eval.n_slots, tab_lds, slot_lds, gslots, bpad, B);
-    const uint8_t *row = levels + x.c * g.P;
-    Fwd f = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, row, x.sl);
+    Fwd f = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + x.c * g.P, x.sl);
     if (x.active) {
         if (T_out) T_out[x.c] = f.T;
         if (E_out) E_out[x.c] = f.E;
     }
+    if (!mask && !res) return;
+    unsigned long long key = 0, count = 0;
+    if (!emo_select_reduce(x.active, f.T, f.E, x.c, B, target, mask, res, &key, &count)) return;
+    if (res) finish_selection(g, x, levels, key, count, res);
 }
 
 __global__ void __launch_bounds__(kBlock)
 slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict__ levels, int64_t B,
              float *__restrict__ slack, float *__restrict__ T_out, float *__restrict__ E_out,
+             float target, uint32_t *__restrict__ mask, emo_selection *res,
              bool tab_lds, bool slot_lds, float *gslots, int64_t bpad) {
     Ctx x = make_ctx(g, pr.n_slots, tab_lds, slot_lds, gslots, bpad, B);
     const uint8_t *row = levels + x.c * g.P;
@@ -200,6 +216,17 @@ slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict_
         const int col = pr.out_col[i];
         if (x.active && col >= 0) out_row[col] = f.bad ? __builtin_nanf("") : lft - eft;
     }
+    if (!mask && !res) return;
+    unsigned long long key = 0, count = 0;
+    if (!emo_select_reduce(x.active, f.T, f.E, x.c, B, target, mask, res, &key, &count)) return;
+    if (res) {
+        // the winner is re-evaluated with the forward-only program; its slots fit this block's
+        // slot space (the slack program keeps every step's slot, at least as many)
+        if (threadIdx.x >= kWave) return;
+        const int64_t win = emo_key_index(key);
+        Fwd w = forward(pr, x.tab_lds, g.tab, g.F, g.static_power, levels + win * g.P, x.sl);
+        if (threadIdx.x == 0) emo_write_selection(res, key, count, w.T);
+    }
 }
 
 // ---------------------------------------------------------------- selection (Eq. 4)
@@ -217,21 +244,6 @@ __global__ void init_result(emo_selection *res) {
 
 __global__ void empty_result(emo_selection *res) {
     emo_write_selection(res, ~0ull, 0ull, 0.f);
-}
-
-__global__ void __launch_bounds__(kBlock)
-select_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float target,
-              uint32_t *__restrict__ mask, emo_selection *res, bool tab_lds, bool slot_lds,
-              float *gslots, int64_t bpad) {
-    Ctx x = make_ctx(g, g.eval.n_slots, tab_lds, slot_lds, gslots, bpad, B);
-    Fwd f = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + x.c * g.P, x.sl);
-    unsigned long long key = 0, count = 0;
-    const bool last = emo_select_reduce(x.active, f.T, f.E, x.c, B, target, mask, res, &key, &count);
-    if (!last || threadIdx.x >= kWave) return;
-    // the last block re-evaluates the winner to report its makespan
-    const int64_t win = emo_key_index(key);
-    Fwd w = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + win * g.P, x.sl);
-    if (threadIdx.x == 0) emo_write_selection(res, key, count, w.T);
 }
 
 __global__ void __launch_bounds__(kBlock)
@@ -256,16 +268,16 @@ hipError_t scratch(size_t bytes, hipStream_t s, float **p) {
 
 }  // namespace
 
-hipError_t launch_eval(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
-                       hipStream_t s) {
+hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
+                          float target, uint32_t *mask, emo_selection *res, hipStream_t s) {
     LaunchShape sh = shape_for(g, g.eval.n_slots);
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
     float *gs = nullptr;
     hipError_t e = scratch(sh.slot_lds ? 0 : static_cast<size_t>(g.eval.n_slots) * bpad * 4, s, &gs);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(eval_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBlock), sh.lds_bytes, s,
-                       g, levels, B, T, E, sh.tab_lds, sh.slot_lds, gs, bpad);
+    hipLaunchKernelGGL(forward_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBlock), sh.lds_bytes, s,
+                       g, levels, B, T, E, target, mask, res, sh.tab_lds, sh.slot_lds, gs, bpad);
     e = hipGetLastError();
     if (gs) {
         hipError_t e2 = hipFreeAsync(gs, s);
@@ -276,7 +288,7 @@ hipError_t launch_eval(const DevGraph &g, const uint8_t *levels, int64_t B, floa
 
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
-                        hipStream_t s) {
+                        float target, uint32_t *mask, emo_selection *res, hipStream_t s) {
     LaunchShape sh = shape_for(g, prog.n_slots);
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
@@ -284,30 +296,8 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
     hipError_t e = scratch(sh.slot_lds ? 0 : static_cast<size_t>(prog.n_slots) * bpad * 4, s, &gs);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(slack_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBlock), sh.lds_bytes, s,
-                       g, prog, out_cols, levels, B, slack, T, E, sh.tab_lds, sh.slot_lds, gs, bpad);
-    e = hipGetLastError();
-    if (gs) {
-        hipError_t e2 = hipFreeAsync(gs, s);
-        if (e == hipSuccess) e = e2;
-    }
-    return e;
-}
-
-hipError_t launch_select(const DevGraph &g, const uint8_t *levels, int64_t B, float target,
-                         uint32_t *mask, emo_selection *res, hipStream_t s) {
-    if (B == 0) {
-        hipLaunchKernelGGL(empty_result, dim3(1), dim3(1), 0, s, res);
-        return hipGetLastError();
-    }
-    LaunchShape sh = shape_for(g, g.eval.n_slots);
-    const int64_t grid = grid_for(B);
-    const int64_t bpad = grid * kBlock;
-    float *gs = nullptr;
-    hipError_t e = scratch(sh.slot_lds ? 0 : static_cast<size_t>(g.eval.n_slots) * bpad * 4, s, &gs);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(init_result, dim3(1), dim3(1), 0, s, res);
-    hipLaunchKernelGGL(select_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBlock), sh.lds_bytes, s,
-                       g, levels, B, target, mask, res, sh.tab_lds, sh.slot_lds, gs, bpad);
+                       g, prog, out_cols, levels, B, slack, T, E, target, mask, res, sh.tab_lds,
+                       sh.slot_lds, gs, bpad);
     e = hipGetLastError();
     if (gs) {
         hipError_t e2 = hipFreeAsync(gs, s);

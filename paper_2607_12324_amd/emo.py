@@ -22,7 +22,8 @@ STATUS_NAMES = {0: "EMO_OK", 1: "EMO_ERR_INVALID_ARGUMENT", 2: "EMO_ERR_CYCLE",
 
 ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_kernel_mode", "emo_graph_topo_order",
-                "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_select_from_results",
+                "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
+                "emo_select_from_results",
                 "emo_graph_specialized_source", "emo_status_string", "emo_last_error")
 
 
@@ -63,6 +64,7 @@ def _load_library():
         "emo_eval_policies": [P, P, i64, P, P, P],
         "emo_slack": [P, P, i64, P, i32, P, P, P],
         "emo_select_policy": [P, P, i64, f32, P, P, P],
+        "emo_evaluate": [P, P, i64, P, P, P, i32, f32, P, P, P],
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
         "emo_graph_specialized_source": [P, P, P],
     }
@@ -212,6 +214,19 @@ class EmoGraph:
                              int(bool(per_node)), _dptr(makespan, torch.float32, B, "makespan"),
                              _dptr(energy, torch.float32, B, "energy"), _stream(stream)))
         return out
+
+    def evaluate(self, levels, makespan=None, energy=None, slack=None, per_node: bool = False,
+                 latency_target: float = 0.0, mask=None, result=None, stream=None):
+        """One pass of the whole hot path (emo_evaluate); every output is optional."""
+        import torch
+        lv, B = self._levels(levels)
+        cols = self.num_nodes if per_node else self.num_packs
+        _check(lib.emo_evaluate(self._h, lv, B, _dptr(makespan, torch.float32, B, "makespan"),
+                                _dptr(energy, torch.float32, B, "energy"),
+                                _dptr(slack, torch.float32, B * cols, "slack"), int(bool(per_node)),
+                                float(latency_target), _dptr(mask, torch.int32, (B + 31) // 32, "mask"),
+                                _dptr(result, torch.int64, 3, "result"), _stream(stream)))
+        return makespan, energy, slack, mask, result
 
     def select_policy(self, levels, latency_target: float, mask=None, result=None, stream=None,
                       want_mask: bool = True):

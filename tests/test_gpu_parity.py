@@ -57,6 +57,22 @@ def run_all(torch, emo, g, rows, targets, exact=True, per_node=True, what="", mo
         SN = gh.slack(lv, per_node=True)
         SN_or = np.stack([oracle.slack(g, rows[c]).slack for c in pick]) if len(pick) else np.zeros((0, g.num_nodes))
         parity.assert_slack(host(SN)[pick], SN_or, T_or[pick], exact, what + " node slack")
+    # the fused entry point: every output of the hot path from one launch
+    for pn in ((False, True) if per_node else (False,)):
+        cols = g.num_nodes if pn else g.num_packs
+        T3 = torch.empty_like(T)
+        E3 = torch.empty_like(E)
+        S3 = torch.empty((B, cols), dtype=torch.float32, device="cuda")
+        m3 = torch.empty(max(1, (B + 31) // 32), dtype=torch.int32, device="cuda")
+        r3 = torch.empty(3, dtype=torch.int64, device="cuda")
+        tgt = float(np.float32(targets[0]))
+        gh.evaluate(lv, makespan=T3, energy=E3, slack=S3, per_node=pn, latency_target=tgt,
+                    mask=m3, result=r3)
+        parity.assert_eval(host(T3), host(E3), T_or, E_or, exact, what + f" evaluate pn={pn}")
+        ref = S_or if not pn else np.stack([oracle.slack(g, rows[c]).slack for c in pick])
+        parity.assert_slack(host(S3)[pick], ref, T_or[pick], exact, what + f" evaluate slack pn={pn}")
+        parity.assert_selection(emo.parse_selection(r3), emo.unpack_mask(m3, B), T_or, E_or, tgt,
+                                exact, what + f" evaluate select pn={pn}")
     for tgt in targets:
         tgt = float(np.float32(tgt))
         res, mask = gh.select_policy(lv, tgt)

@@ -73,7 +73,7 @@ def test_workload_kernels_compile_without_spills(emo, hiprtc, tmp_path, k):
     g = synth.config_graph(k)
     src = emo.EmoGraph(g, device=-1).specialized_source()
     path = compile_source(hiprtc, src, tmp_path)
-    expect = ["emo_sp_eval", "emo_sp_select"] + (["emo_sp_slack"] if g.num_packs <= 160 else [])
+    expect = ["emo_sp_select"] + (["emo_sp_slack"] if g.num_packs <= 160 else [])
     notes, asm = check_code_object(path, expect)
     # the forward pass is straight-line: roughly five vector instructions per pack
     body = asm.split("<emo_sp_select>:")[1].split("s_endpgm")[0]
@@ -98,4 +98,4 @@ def test_random_graph_kernels_compile(emo, hiprtc, tmp_path, seed):
         g = synth.random_dag(rng, V, 3.0 / V, 0.7, F, shuffle_packs=bool(i % 2))
         src = emo.EmoGraph(g, device=-1).specialized_source()
         path = compile_source(hiprtc, src, tmp_path)
-        check_code_object(path, ["emo_sp_eval", "emo_sp_select"])
+        check_code_object(path, ["emo_sp_select"])
