@@ -90,6 +90,9 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="benchmark workload 1..5 (default 2)")
     ap.add_argument("--copies", type=int, default=5, help="rotated copies of the level batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB, --steps times (the reference "
+                         "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: this build evaluates candidate policies on a single "
@@ -101,6 +104,16 @@ def main():
     import torch
 
     from paper_2607_12324_amd import emo, synth
+
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n, "launches": args.steps}))
+        return
 
     k = args.workload
     spec = synth.CONFIGS[k]

@@ -171,8 +171,9 @@ emo_status emo_slack(emo_graph_t g, const uint8_t *levels, int64_t num_candidate
  * (Eq. 4 over the given candidate batch), ties to the lower index.
  *   feasible_mask  device uint32 [ceil(B/32)] or NULL: bit (c % 32) of word c / 32 is set iff
  *                  candidate c is feasible.
- *   result         device emo_selection, 8-byte aligned.  It doubles as the reduction's
- *                  accumulator while the call runs, so it must not alias another output.
+ *   result         device emo_selection, 8-byte aligned, written once at the end of the call
+ *                  (one partial record per workgroup goes to stream-ordered scratch memory and a
+ *                  single-workgroup kernel reduces them; there are no global atomics).
  */
 emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t num_candidates,
                              float latency_target, uint32_t *feasible_mask,

@@ -633,23 +633,33 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
         if (slack) jit = jit && g->jm.slack && (!g->jit_slack_staged || aligned(slack, 16));
     }
     DeviceGuard guard(g->device);
-    hipError_t e = hipSuccess;
-    if (result) e = emo::launch_init_result(result, st);
-    if (e != hipSuccess) return after_launch(e, "selection init");
+    // one selection partial record per block of the evaluating kernel
+    const int64_t nblocks = jit ? emo::jit_blocks(g->jm, B) : emo::forward_blocks(B);
+    void *part = nullptr;
+    if (result) {
+        hipError_t ea = hipMallocAsync(&part, static_cast<size_t>(nblocks) * emo::kPartialBytes, st);
+        if (ea != hipSuccess) return fail(EMO_ERR_OUT_OF_MEMORY, "hipMallocAsync: %s", hipGetErrorString(ea));
+    }
+    hipError_t e;
     if (slack) {
         if (jit) {
             e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy, target,
-                                      mask, result, st);
+                                      mask, part, st);
         } else {
             const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
             e = emo::launch_slack(g->dg, prog, per_node ? g->V : g->P, levels, B, slack, makespan,
-                                  energy, target, mask, result, st);
+                                  energy, target, mask, part, st);
         }
     } else if (jit) {
         e = emo::jit_launch_forward(g->jm, levels, B, g->dg.tab, makespan, energy, target, mask,
-                                    result, st);
+                                    part, st);
     } else {
-        e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, result, st);
+        e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, part, st);
+    }
+    if (result) {
+        if (e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
+        hipError_t ef = hipFreeAsync(part, st);
+        if (e == hipSuccess) e = ef;
     }
     return after_launch(e, "evaluation");
 }
@@ -693,9 +703,17 @@ emo_status emo_select_from_results(const float *makespan, const float *energy, i
     if (reinterpret_cast<uintptr_t>(result) % 8) return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
     if (B > 0 && (!makespan || !energy)) return fail(EMO_ERR_INVALID_ARGUMENT, "makespan/energy is NULL");
     if (std::isnan(latency_target)) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
-    return after_launch(emo::launch_select_results(makespan, energy, B, latency_target, feasible_mask,
-                                                   result, static_cast<hipStream_t>(stream)),
-                        "emo_select_from_results");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (B == 0) return after_launch(emo::launch_empty_result(result, st), "emo_select_from_results");
+    const int64_t nblocks = emo::forward_blocks(B);
+    void *part = nullptr;
+    hipError_t e = hipMallocAsync(&part, static_cast<size_t>(nblocks) * emo::kPartialBytes, st);
+    if (e != hipSuccess) return fail(EMO_ERR_OUT_OF_MEMORY, "hipMallocAsync: %s", hipGetErrorString(e));
+    e = emo::launch_select_results(makespan, energy, B, latency_target, feasible_mask, part, st);
+    if (e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
+    hipError_t ef = hipFreeAsync(part, st);
+    if (e == hipSuccess) e = ef;
+    return after_launch(e, "emo_select_from_results");
 }
 
 }  // extern "C"

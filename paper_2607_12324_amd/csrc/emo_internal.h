@@ -51,17 +51,24 @@ struct DevGraph {
     DevProgram slack_node;         // forward + backward over every node
 };
 
-// Interpreting kernels.  T, E, mask, res may each be NULL; res != NULL requires an accumulator
-// initialised by launch_init_result on the same stream.
+// Selection partial records: one per block of the evaluating kernel, reduced by
+// launch_select_finalize (16 bytes each: least key, feasible count, makespan).
+constexpr size_t kPartialBytes = 16;
+
+// Interpreting kernels.  T, E, mask, part may each be NULL; `part` receives one selection
+// partial record per block (forward_blocks(B) of them).
 hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
-                          float target, uint32_t *mask, emo_selection *res, hipStream_t s);
+                          float target, uint32_t *mask, void *part, hipStream_t s);
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
-                        float target, uint32_t *mask, emo_selection *res, hipStream_t s);
-hipError_t launch_init_result(emo_selection *res, hipStream_t s);
+                        float target, uint32_t *mask, void *part, hipStream_t s);
+int64_t forward_blocks(int64_t B);
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s);
+hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selection *res,
+                                  hipStream_t s);
+// Stage 1 of a selection from stored makespans and energies (forward_blocks(B) partials).
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
-                                 uint32_t *mask, emo_selection *res, hipStream_t s);
+                                 uint32_t *mask, void *part, hipStream_t s);
 
 // ---------------------------------------------------------------- graph-specialised kernels
 
@@ -97,14 +104,15 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
 // 0 on success; otherwise *log holds the compiler's or loader's message.
 int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log);
 void jit_unload(JitModule *m);
-// Forward pass; T, E, mask, res may each be NULL (res != NULL requires an initialised
-// accumulator, see launch_init_result).
+// Blocks of the specialised kernels' grid for B candidates (one selection partial each).
+int64_t jit_blocks(const JitModule &m, int64_t B);
+// Forward pass; T, E, mask, part may each be NULL.
 hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,
                               const float2 *tab, float *T, float *E, float target, uint32_t *mask,
-                              emo_selection *res, hipStream_t s);
+                              void *part, hipStream_t s);
 // Forward + backward slack pass with the same optional outputs.
 hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
                             float *S, float *T, float *E, float target, uint32_t *mask,
-                            emo_selection *res, hipStream_t s);
+                            void *part, hipStream_t s);
 
 }  // namespace emo

@@ -58,7 +58,11 @@ struct LevelPlan {
     bool pow2;
     std::vector<char> loaded, released;
     std::ostringstream *o;
-    static constexpr int kAhead = 2;
+    // Level words are loaded a whole 128-byte line of the row at a time (all of a group's
+    // loads back to back, so the line is fetched from L2 once) and one group ahead of use.
+    static constexpr int kGroupBytes = 128;
+
+    int group_words() const { return kGroupBytes / width; }
 
     unsigned fmask() const { return static_cast<unsigned>(F - 1) * 0x01010101u; }
     int nwords() const { return (P + width - 1) / width; }
@@ -84,7 +88,7 @@ struct LevelPlan {
         loaded.assign(nwords() + 1, 0);
         released.assign(nwords() + 1, 0);
         if (width == 1) return;
-        for (int q = 0; q < kAhead; ++q) load(q);
+        load_group(0);
     }
 
     void load(int q) {
@@ -93,14 +97,23 @@ struct LevelPlan {
         *o << "  " << (width == 16 ? "uint4" : "unsigned int") << " L" << q << " = rowp[" << q << "];\n";
     }
 
+    void load_group(int gidx) {
+        for (int q = gidx * group_words(); q < (gidx + 1) * group_words(); ++q) load(q);
+    }
+
     bool needs_release(int p) const { return width != 1 && !released[p / width]; }
 
     // Releases chunk q.  `ride` names values computed before this point (the energy partial
     // sum and the finish times still needed later) that pass through the same barrier, so the
     // arithmetic of the previous chunk completes before this chunk's table reads start.
     void release(int q, const std::vector<std::string> &ride) {
-        *o << "  __asm__ __volatile__(\"\" : \"+v\"(rowp));\n";
-        for (int k = q; k <= q + kAhead; ++k) load(k);
+        const int gidx = q / group_words();
+        if (!loaded[q] || (q % group_words() == 0 && (gidx + 1) * group_words() < nwords() &&
+                           !loaded[(gidx + 1) * group_words()])) {
+            *o << "  __asm__ __volatile__(\"\" : \"+v\"(rowp));\n";
+            load_group(gidx);
+            load_group(gidx + 1);
+        }
         std::string w = "L" + std::to_string(q);
         std::vector<std::string> ops;
         if (width == 16) {
@@ -220,14 +233,20 @@ void emit_forward(std::ostringstream &o, const JitGraph &g, std::vector<std::str
     o << "  if (isbad) { T = __builtin_nanf(\"\"); E = __builtin_nanf(\"\"); }\n";
 }
 
+// Slack output staging: packs [p0, p0 + kc) of the wave's 64 candidates are collected in LDS
+// as stg[pack - p0][lane] (row stride 65 floats, conflict-free writes) and written with 16-byte
+// stores; with kc = 32 each candidate's segment is one whole 128-byte line.
+int stage_chunk(int P) { return P % 32 == 0 ? 32 : 16; }
+
 // Backward pass for per-pack slack (requires the forward's f<i>, T and the level words).
-// Pack durations are read from the table again through a pointer the compiler cannot
-// identify with the forward's, so the forward's loads are not kept alive for the whole pass.
+// Pack durations are read from the table again at an index offset by a zero the compiler cannot
+// see through, so the forward's loads are not kept alive for the whole pass (and the reads stay
+// LDS reads with immediate offsets).
 void emit_backward(std::ostringstream &o, const JitGraph &g, bool staged,
                    const std::vector<std::string> &level_expr) {
     const int n = static_cast<int>(g.ops.size());
     o << "  const float Tb = isbad ? 0.f : T;\n";
-    o << "  const float2 *tabb = tab;\n  __asm__ __volatile__(\"\" : \"+v\"(tabb));\n";
+    o << "  unsigned int zb = 0u;\n  __asm__ __volatile__(\"\" : \"+v\"(zb));\n";
     for (int i = n - 1; i >= 0; --i) {
         const JitOp &op = g.ops[i];
         std::string lft;
@@ -244,16 +263,17 @@ void emit_backward(std::ostringstream &o, const JitGraph &g, bool staged,
         o << "  const float lf" << i << " = " << lft << ";\n";
         std::string dur = flit(op.dur);
         if (op.pack >= 0) {
-            o << "  const float t" << i << " = tabb[" << static_cast<long long>(op.pack) * g.F << " + "
+            o << "  const float t" << i << " = tab[zb + " << static_cast<long long>(op.pack) * g.F << " + "
               << level_expr[i] << "].x;\n";
             dur = "t" + std::to_string(i);
         }
         if (!op.in.empty()) o << "  const float s" << i << " = lf" << i << " - " << dur << ";\n";
         if (op.pack >= 0) {
             const int p = op.pack;
+            const int kc = stage_chunk(g.P);
             if (staged) {
-                o << "  stg[" << (p % 16) * 65 << " + lane] = lf" << i << " - f" << i << ";\n";
-                if (p % 16 == 0) o << "  emo_flush(stg, stg_bad, S, wbase, B, " << p << ");\n";
+                o << "  stg[" << (p % kc) * 65 << " + lane] = lf" << i << " - f" << i << ";\n";
+                if (p % kc == 0) o << "  emo_flush(stg, stg_bad, S, wbase, B, " << p << ");\n";
             } else {
                 o << "  if (active) S[cand * " << g.P << "LL + " << p << "] = isbad ? __builtin_nanf(\"\") : lf"
                   << i << " - f" << i << ";\n";
@@ -297,35 +317,25 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
          "const float2 *__restrict__ tab) {\n"
       << fwd.str() << "  EmoFwd r; r.T = T; r.E = E; return r;\n}\n";
 
-    // forward pass, optional makespan/energy outputs, optional feasibility mask and selection
+    // forward pass, optional makespan/energy outputs, feasibility mask and selection partials
     o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
          "emo_sp_select(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
          "              float *__restrict__ To, float *__restrict__ Eo,\n"
-         "              float target, unsigned int *__restrict__ mask, void *res) {\n"
+         "              float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n"
          "  EMO_TABLE_DECL\n  EMO_LANE_SETUP\n"
-         "  unsigned long long key = 0, count = 0;\n"
-         "#pragma clang loop unroll(disable)\n"
-         "  for (int pass = 0; pass < 2; ++pass) {\n"
-         "    const EmoFwd r = emo_forward(lv + cand * "
+         "  const EmoFwd r = emo_forward(lv + cand * "
       << g.P << "LL, tab);\n"
-         "    if (pass == 0) {\n"
-         "      if (active) { if (To) To[cand] = r.T; if (Eo) Eo[cand] = r.E; }\n"
-         "      if (!mask && !res) return;\n"
-         "      if (!emo_select_reduce(active, r.T, r.E, cand, B, target, mask, res, &key, &count)) return;\n"
-         "      if (threadIdx.x >= EMO_WAVE) return;\n"
-         "      cand = emo_key_index(key);\n"
-         "    } else if (threadIdx.x == 0) {\n"
-         "      emo_write_selection(res, key, count, r.T);\n"
-         "    }\n"
-         "  }\n}\n";
+         "  if (active) { if (To) To[cand] = r.T; if (Eo) Eo[cand] = r.E; }\n"
+         "  if (mask || part) emo_select_block(active, r.T, r.E, cand, B, target, mask, part);\n"
+         "}\n";
 
     if (with_slack) {
         const bool staged = g.pack_monotone && g.P % 16 == 0;
         if (staged) {
+            const int kc = stage_chunk(g.P);
+            o << "#define EMO_KC " << kc << "\n";
             o << R"(
-// Writes the slack of packs [p0, p0 + 16) of the wave's 64 candidates (staged in LDS as
-// stg[pack - p0][lane], row stride 65 floats) with 16-byte stores: each output row segment of
-// 16 floats is 64 contiguous bytes.
+// Writes the slack of packs [p0, p0 + EMO_KC) of the wave's 64 candidates, staged in LDS.
 __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_bad,
                                           float *__restrict__ S, long long wbase, long long B,
                                           int p0) {
@@ -333,10 +343,11 @@ __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_ba
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   const int lane = threadIdx.x % EMO_WAVE;
+  constexpr int per_row = EMO_KC / 4;          // 16-byte pieces per candidate segment
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
+  for (int m = 0; m < per_row; ++m) {
     const int j = lane + EMO_WAVE * m;
-    const int r = j >> 2, part = j & 3;
+    const int r = j / per_row, part = j % per_row;
     float4 v;
     v.x = stg[(4 * part + 0) * 65 + r];
     v.y = stg[(4 * part + 1) * 65 + r];
@@ -355,14 +366,14 @@ __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_ba
         o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
              "emo_sp_slack(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
              "             float *__restrict__ S, float *__restrict__ To, float *__restrict__ Eo,\n"
-             "             float target, unsigned int *__restrict__ mask, void *res) {\n"
+             "             float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n"
              "  EMO_TABLE_DECL\n  EMO_LANE_SETUP\n"
              "  const int lane = threadIdx.x % EMO_WAVE;\n"
              "  const int wave = threadIdx.x / EMO_WAVE;\n"
              "  const long long wbase = (long long)blockIdx.x * EMO_BLOCK + wave * EMO_WAVE;\n"
              "  (void)lane; (void)wbase;\n";
         if (staged) {
-            o << "  __shared__ float stg_all[EMO_WAVES_PER_BLOCK][16 * 65];\n"
+            o << "  __shared__ float stg_all[EMO_WAVES_PER_BLOCK][EMO_KC * 65];\n"
                  "  __shared__ unsigned int bad_all[EMO_WAVES_PER_BLOCK][EMO_WAVE];\n"
                  "  float *stg = stg_all[wave];\n"
                  "  unsigned int *stg_bad = bad_all[wave];\n";
@@ -373,14 +384,7 @@ __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_ba
         o << "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n";
         if (staged) o << "  stg_bad[lane] = isbad ? 1u : 0u;\n";
         emit_backward(o, g, staged, level_expr);
-        // selection after the slack pass; the last block re-evaluates the winner's makespan
-        o << "  if (!mask && !res) return;\n"
-             "  unsigned long long key = 0, count = 0;\n"
-             "  if (!emo_select_reduce(active, T, E, cand, B, target, mask, res, &key, &count)) return;\n"
-             "  if (threadIdx.x >= EMO_WAVE) return;\n"
-             "  const EmoFwd w = emo_forward(lv + emo_key_index(key) * "
-          << g.P << "LL, tab);\n"
-             "  if (threadIdx.x == 0) emo_write_selection(res, key, count, w.T);\n";
+        o << "  if (mask || part) emo_select_block(active, T, E, cand, B, target, mask, part);\n";
         o << "}\n";
     }
     return o.str();
@@ -443,21 +447,21 @@ namespace {
 unsigned grid_of(int64_t B, int block) { return static_cast<unsigned>((B + block - 1) / block); }
 }  // namespace
 
+int64_t jit_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.block); }
+
 hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,
                               const float2 *tab, float *T, float *E, float target, uint32_t *mask,
-                              emo_selection *res, hipStream_t s) {
+                              void *part, hipStream_t s) {
     long long b = B;
-    void *r = res;
-    void *args[] = {&levels, &b, &tab, &T, &E, &target, &mask, &r};
+    void *args[] = {&levels, &b, &tab, &T, &E, &target, &mask, &part};
     return hipModuleLaunchKernel(m.select, grid_of(B, m.block), 1, 1, m.block, 1, 1, 0, s, args, nullptr);
 }
 
 hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
                             float *S, float *T, float *E, float target, uint32_t *mask,
-                            emo_selection *res, hipStream_t s) {
+                            void *part, hipStream_t s) {
     long long b = B;
-    void *r = res;
-    void *args[] = {&levels, &b, &tab, &S, &T, &E, &target, &mask, &r};
+    void *args[] = {&levels, &b, &tab, &S, &T, &E, &target, &mask, &part};
     return hipModuleLaunchKernel(m.slack, grid_of(B, m.block), 1, 1, m.block, 1, 1, 0, s, args, nullptr);
 }
 

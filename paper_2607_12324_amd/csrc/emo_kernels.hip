@@ -152,37 +152,24 @@ __device__ Ctx make_ctx(const DevGraph &g, int n_slots, bool tab_lds, bool slot_
     return x;
 }
 
-// Winner's makespan for the selection record: the last block re-evaluates the winner.
-__device__ void finish_selection(const DevGraph &g, const Ctx &x, const uint8_t *levels,
-                                 unsigned long long key, unsigned long long count,
-                                 emo_selection *res) {
-    if (threadIdx.x >= kWave) return;
-    const int64_t win = emo_key_index(key);
-    Fwd w = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + win * g.P, x.sl);
-    if (threadIdx.x == 0) emo_write_selection(res, key, count, w.T);
-}
-
-// Forward pass; makespan/energy outputs, the mask and the selection are each optional.
+// Forward pass; makespan/energy outputs, the mask and the selection partials are each optional.
 __global__ void __launch_bounds__(kBlock)
 forward_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ T_out,
                float *__restrict__ E_out, float target, uint32_t *__restrict__ mask,
-               emo_selection *res, bool tab_lds, bool slot_lds, float *gslots, int64_t bpad) {
+               EmoPartial *part, bool tab_lds, bool slot_lds, float *gslots, int64_t bpad) {
     Ctx x = make_ctx(g, g.eval.n_slots, tab_lds, slot_lds, gslots, bpad, B);
     Fwd f = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + x.c * g.P, x.sl);
     if (x.active) {
         if (T_out) T_out[x.c] = f.T;
         if (E_out) E_out[x.c] = f.E;
     }
-    if (!mask && !res) return;
-    unsigned long long key = 0, count = 0;
-    if (!emo_select_reduce(x.active, f.T, f.E, x.c, B, target, mask, res, &key, &count)) return;
-    if (res) finish_selection(g, x, levels, key, count, res);
+    if (mask || part) emo_select_block(x.active, f.T, f.E, x.c, B, target, mask, part);
 }
 
 __global__ void __launch_bounds__(kBlock)
 slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict__ levels, int64_t B,
              float *__restrict__ slack, float *__restrict__ T_out, float *__restrict__ E_out,
-             float target, uint32_t *__restrict__ mask, emo_selection *res,
+             float target, uint32_t *__restrict__ mask, EmoPartial *part,
              bool tab_lds, bool slot_lds, float *gslots, int64_t bpad) {
     Ctx x = make_ctx(g, pr.n_slots, tab_lds, slot_lds, gslots, bpad, B);
     const uint8_t *row = levels + x.c * g.P;
@@ -216,45 +203,34 @@ slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict_
         const int col = pr.out_col[i];
         if (x.active && col >= 0) out_row[col] = f.bad ? __builtin_nanf("") : lft - eft;
     }
-    if (!mask && !res) return;
-    unsigned long long key = 0, count = 0;
-    if (!emo_select_reduce(x.active, f.T, f.E, x.c, B, target, mask, res, &key, &count)) return;
-    if (res) {
-        // the winner is re-evaluated with the forward-only program; its slots fit this block's
-        // slot space (the slack program keeps every step's slot, at least as many)
-        if (threadIdx.x >= kWave) return;
-        const int64_t win = emo_key_index(key);
-        Fwd w = forward(pr, x.tab_lds, g.tab, g.F, g.static_power, levels + win * g.P, x.sl);
-        if (threadIdx.x == 0) emo_write_selection(res, key, count, w.T);
-    }
+    if (mask || part) emo_select_block(x.active, f.T, f.E, x.c, B, target, mask, part);
 }
 
 // ---------------------------------------------------------------- selection (Eq. 4)
 
-static_assert(sizeof(EmoAcc) == sizeof(emo_selection), "accumulator must overlay emo_selection");
 static_assert(sizeof(EmoSel) == sizeof(emo_selection), "result layout");
-
-__global__ void init_result(emo_selection *res) {
-    EmoAcc *a = reinterpret_cast<EmoAcc *>(res);
-    a->key = ~0ull;
-    a->done = 0u;
-    a->pad = 0u;
-    a->count = 0ull;
-}
+static_assert(sizeof(EmoPartial) == kPartialBytes, "partial record layout");
 
 __global__ void empty_result(emo_selection *res) {
-    emo_write_selection(res, ~0ull, 0ull, 0.f);
+    EmoSel *r = reinterpret_cast<EmoSel *>(res);
+    r->index = -1;
+    r->energy = __builtin_nanf("");
+    r->makespan = __builtin_nanf("");
+    r->num_feasible = 0;
+}
+
+__global__ void __launch_bounds__(kBlock)
+select_finalize_kernel(const EmoPartial *__restrict__ part, int64_t n, emo_selection *res) {
+    emo_select_finalize(part, n, res);
 }
 
 __global__ void __launch_bounds__(kBlock)
 select_results_kernel(const float *__restrict__ T, const float *__restrict__ E, int64_t B,
-                      float target, uint32_t *__restrict__ mask, emo_selection *res) {
+                      float target, uint32_t *__restrict__ mask, EmoPartial *part) {
     const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const bool active = gid < B;
     const int64_t c = active ? gid : B - 1;
-    unsigned long long key = 0, count = 0;
-    const bool last = emo_select_reduce(active, T[c], E[c], c, B, target, mask, res, &key, &count);
-    if (last && threadIdx.x == 0) emo_write_selection(res, key, count, T[emo_key_index(key)]);
+    emo_select_block(active, T[c], E[c], c, B, target, mask, part);
 }
 
 int64_t grid_for(int64_t B) { return (B + kBlock - 1) / kBlock; }
@@ -269,7 +245,7 @@ hipError_t scratch(size_t bytes, hipStream_t s, float **p) {
 }  // namespace
 
 hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
-                          float target, uint32_t *mask, emo_selection *res, hipStream_t s) {
+                          float target, uint32_t *mask, void *part, hipStream_t s) {
     LaunchShape sh = shape_for(g, g.eval.n_slots);
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
@@ -277,7 +253,8 @@ hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, f
     hipError_t e = scratch(sh.slot_lds ? 0 : static_cast<size_t>(g.eval.n_slots) * bpad * 4, s, &gs);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(forward_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBlock), sh.lds_bytes, s,
-                       g, levels, B, T, E, target, mask, res, sh.tab_lds, sh.slot_lds, gs, bpad);
+                       g, levels, B, T, E, target, mask, static_cast<EmoPartial *>(part), sh.tab_lds,
+                       sh.slot_lds, gs, bpad);
     e = hipGetLastError();
     if (gs) {
         hipError_t e2 = hipFreeAsync(gs, s);
@@ -288,7 +265,7 @@ hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, f
 
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
-                        float target, uint32_t *mask, emo_selection *res, hipStream_t s) {
+                        float target, uint32_t *mask, void *part, hipStream_t s) {
     LaunchShape sh = shape_for(g, prog.n_slots);
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
@@ -296,8 +273,8 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
     hipError_t e = scratch(sh.slot_lds ? 0 : static_cast<size_t>(prog.n_slots) * bpad * 4, s, &gs);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(slack_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBlock), sh.lds_bytes, s,
-                       g, prog, out_cols, levels, B, slack, T, E, target, mask, res, sh.tab_lds,
-                       sh.slot_lds, gs, bpad);
+                       g, prog, out_cols, levels, B, slack, T, E, target, mask,
+                       static_cast<EmoPartial *>(part), sh.tab_lds, sh.slot_lds, gs, bpad);
     e = hipGetLastError();
     if (gs) {
         hipError_t e2 = hipFreeAsync(gs, s);
@@ -306,25 +283,24 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
     return e;
 }
 
-hipError_t launch_init_result(emo_selection *res, hipStream_t s) {
-    hipLaunchKernelGGL(init_result, dim3(1), dim3(1), 0, s, res);
-    return hipGetLastError();
-}
+int64_t forward_blocks(int64_t B) { return grid_for(B); }
 
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s) {
     hipLaunchKernelGGL(empty_result, dim3(1), dim3(1), 0, s, res);
     return hipGetLastError();
 }
 
+hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selection *res,
+                                  hipStream_t s) {
+    hipLaunchKernelGGL(select_finalize_kernel, dim3(1), dim3(kBlock), 0, s,
+                       static_cast<const EmoPartial *>(part), nparts, res);
+    return hipGetLastError();
+}
+
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
-                                 uint32_t *mask, emo_selection *res, hipStream_t s) {
-    if (B == 0) {
-        hipLaunchKernelGGL(empty_result, dim3(1), dim3(1), 0, s, res);
-        return hipGetLastError();
-    }
-    hipLaunchKernelGGL(init_result, dim3(1), dim3(1), 0, s, res);
+                                 uint32_t *mask, void *part, hipStream_t s) {
     hipLaunchKernelGGL(select_results_kernel, dim3(static_cast<unsigned>(grid_for(B))), dim3(kBlock), 0, s,
-                       T, E, B, target, mask, res);
+                       T, E, B, target, mask, static_cast<EmoPartial *>(part));
     return hipGetLastError();
 }
 

@@ -4,12 +4,14 @@
 // (its text is embedded into the library and prepended to the generated source), so it
 // includes no headers and uses only HIP built-ins.
 //
-// The caller's result record (24 bytes, see emo_selection) is the accumulator while a
-// selection runs:
-//   bytes 0..7   u64 key = (fp32 bits of E) << 32 | candidate; energies are >= 0, so the bit
-//                pattern orders like the value and equal energies order by index
-//   bytes 8..11  u32 number of blocks done; the last block to finish writes the final record
-//   bytes 16..23 u64 number of feasible candidates
+// Two stages, with no atomics (thousands of blocks updating one address would serialise):
+//   1. every block of the evaluating kernel writes the mask bits of its candidates and one
+//      partial record: its least key, its number of feasible candidates and the makespan of the
+//      candidate holding that key;
+//   2. one block reduces the partial records and writes the emo_selection record.
+// The key of a feasible candidate c is (fp32 bits of its energy) << 32 | c.  Energies are
+// >= 0, so the bit pattern orders like the value and equal energies order by index; an
+// infeasible candidate has the key ~0.
 #pragma once
 
 #ifndef EMO_BLOCK
@@ -18,11 +20,10 @@
 #define EMO_WAVE 64
 #define EMO_WAVES_PER_BLOCK (EMO_BLOCK / EMO_WAVE)
 
-struct EmoAcc {
+struct EmoPartial {
     unsigned long long key;
-    unsigned int done;
-    unsigned int pad;
-    unsigned long long count;
+    unsigned int count;
+    float makespan;
 };
 
 struct EmoSel {
@@ -32,24 +33,25 @@ struct EmoSel {
     long long num_feasible;
 };
 
-__device__ __forceinline__ unsigned long long emo_wave_min_u64(unsigned long long v) {
+// Least key over the wave, carrying the makespan of its candidate.
+__device__ __forceinline__ void emo_wave_min_key(unsigned long long *key, float *T) {
     for (int off = EMO_WAVE / 2; off > 0; off >>= 1) {
-        unsigned long long o = __shfl_xor(v, off, EMO_WAVE);
-        v = o < v ? o : v;
+        const unsigned long long ok = __shfl_xor(*key, off, EMO_WAVE);
+        const float oT = __shfl_xor(*T, off, EMO_WAVE);
+        if (ok < *key) {
+            *key = ok;
+            *T = oT;
+        }
     }
-    return v;
 }
 
-// Reduces feasibility, count and key over the block and the grid.  Returns true in every
-// thread of the last block to finish, with *key_out / *count_out holding the grid results.
-// Must be called by every thread of the block.
-__device__ bool emo_select_reduce(bool active, float T, float E, long long c, long long B,
-                                  float target, unsigned int *mask, void *res,
-                                  unsigned long long *key_out, unsigned long long *count_out) {
+// Stage 1.  Must be called by every thread of the block.  `part` (one record per block) and
+// `mask` may be NULL.
+__device__ void emo_select_block(bool active, float T, float E, long long c, long long B,
+                                 float target, unsigned int *mask, EmoPartial *part) {
     __shared__ unsigned long long s_key[EMO_WAVES_PER_BLOCK];
+    __shared__ float s_T[EMO_WAVES_PER_BLOCK];
     __shared__ unsigned int s_cnt[EMO_WAVES_PER_BLOCK];
-    __shared__ unsigned long long s_res[2];
-    __shared__ int s_last;
     const bool feas = active && (T <= target);   // false for NaN
     const unsigned long long bal = __ballot(feas);
     const int lane = threadIdx.x % EMO_WAVE;
@@ -61,48 +63,69 @@ __device__ bool emo_select_reduce(bool active, float T, float E, long long c, lo
         mask[w] = (unsigned int)bal;
         if (w + 1 < nwords) mask[w + 1] = (unsigned int)(bal >> 32);
     }
+    if (!part) return;
     unsigned long long key = feas ? (((unsigned long long)__float_as_uint(E)) << 32) |
                                         (unsigned long long)(unsigned int)c
                                   : ~0ull;
-    key = emo_wave_min_u64(key);
+    float kT = T;
+    emo_wave_min_key(&key, &kT);
     if (lane == 0) {
         s_key[wave] = key;
+        s_T[wave] = kT;
         s_cnt[wave] = (unsigned int)__popcll(bal);
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        unsigned long long bk = s_key[0];
-        unsigned long long bc = s_cnt[0];
+        EmoPartial p;
+        p.key = s_key[0];
+        p.makespan = s_T[0];
+        p.count = s_cnt[0];
         for (int w = 1; w < EMO_WAVES_PER_BLOCK; ++w) {
-            bk = s_key[w] < bk ? s_key[w] : bk;
-            bc += s_cnt[w];
+            if (s_key[w] < p.key) {
+                p.key = s_key[w];
+                p.makespan = s_T[w];
+            }
+            p.count += s_cnt[w];
         }
-        EmoAcc *a = (EmoAcc *)res;
-        if (bk != ~0ull) atomicMin(&a->key, bk);
-        if (bc) atomicAdd(&a->count, bc);
-        __threadfence();
-        const unsigned int ticket = atomicAdd(&a->done, 1u);
-        s_last = ticket == gridDim.x - 1;
-        if (s_last) {
-            __threadfence();
-            s_res[0] = atomicAdd(&a->key, 0ull);
-            s_res[1] = atomicAdd(&a->count, 0ull);
+        part[blockIdx.x] = p;
+    }
+}
+
+// Stage 2, run by one block of EMO_BLOCK threads: reduces n partial records into the
+// emo_selection record `res`.
+__device__ void emo_select_finalize(const EmoPartial *part, long long n, void *res) {
+    __shared__ unsigned long long s_key[EMO_WAVES_PER_BLOCK];
+    __shared__ float s_T[EMO_WAVES_PER_BLOCK];
+    __shared__ unsigned long long s_cnt[EMO_WAVES_PER_BLOCK];
+    unsigned long long key = ~0ull;
+    float T = 0.f;
+    unsigned long long cnt = 0;
+    for (long long i = threadIdx.x; i < n; i += EMO_BLOCK) {
+        const EmoPartial p = part[i];
+        cnt += p.count;
+        if (p.key < key) {
+            key = p.key;
+            T = p.makespan;
         }
     }
+    emo_wave_min_key(&key, &T);
+    for (int off = EMO_WAVE / 2; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, EMO_WAVE);
+    const int lane = threadIdx.x % EMO_WAVE;
+    const int wave = threadIdx.x / EMO_WAVE;
+    if (lane == 0) {
+        s_key[wave] = key;
+        s_T[wave] = T;
+        s_cnt[wave] = cnt;
+    }
     __syncthreads();
-    *key_out = s_res[0];
-    *count_out = s_res[1];
-    return s_last != 0;
-}
-
-// Winner index from a grid key (0 when nothing is feasible, so that it can be re-evaluated
-// safely).
-__device__ __forceinline__ long long emo_key_index(unsigned long long key) {
-    return key == ~0ull ? 0 : (long long)(key & 0xffffffffull);
-}
-
-__device__ __forceinline__ void emo_write_selection(void *res, unsigned long long key,
-                                                    unsigned long long count, float T_winner) {
+    if (threadIdx.x != 0) return;
+    for (int w = 1; w < EMO_WAVES_PER_BLOCK; ++w) {
+        if (s_key[w] < key) {
+            key = s_key[w];
+            T = s_T[w];
+        }
+        cnt += s_cnt[w];
+    }
     EmoSel *r = (EmoSel *)res;
     if (key == ~0ull) {
         r->index = -1;
@@ -111,7 +134,7 @@ __device__ __forceinline__ void emo_write_selection(void *res, unsigned long lon
     } else {
         r->index = (long long)(key & 0xffffffffull);
         r->energy = __uint_as_float((unsigned int)(key >> 32));
-        r->makespan = T_winner;
+        r->makespan = T;
     }
-    r->num_feasible = (long long)count;
+    r->num_feasible = (long long)cnt;
 }
