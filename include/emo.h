@@ -200,6 +200,13 @@ emo_status emo_select_from_results(const float *makespan, const float *energy,
                                    int64_t num_candidates, float latency_target,
                                    uint32_t *feasible_mask, emo_selection *result, void *stream);
 
+/* Profiling hook: while set, batch calls on `g` record `begin_event` on their stream right
+ * before the kernel that evaluates the candidates and `end_event` right after it (before the
+ * single-workgroup kernel that completes a selection).  Both are hipEvent_t handles (NULL
+ * disables); the caller owns them.  Not to be called while batch calls on `g` may run
+ * concurrently on another thread. */
+emo_status emo_graph_set_timing_events(emo_graph_t g, void *begin_event, void *end_event);
+
 /* Diagnostics: the HIP source of the kernels specialised to `g` (the text EMO_KERNELS_AUTO
  * compiles on first use), NUL-terminated.  With buf == NULL, *len receives the size needed
  * including the NUL; otherwise at most *len bytes are written.  Works on host-only graphs.

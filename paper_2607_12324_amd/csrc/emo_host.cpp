@@ -110,6 +110,9 @@ struct emo_graph_s {
     int jit_state = 0;                       // 0 not tried, 1 compiled, -1 failed
     emo::JitModule jm;
     std::string jit_log;
+    // profiling hook (hipEvent_t handles owned by the caller)
+    hipEvent_t ev_begin = nullptr;
+    hipEvent_t ev_end = nullptr;
 };
 
 namespace {
@@ -579,6 +582,13 @@ emo_status emo_graph_set_kernel_mode(emo_graph_t g, int32_t mode) {
     return ok();
 }
 
+emo_status emo_graph_set_timing_events(emo_graph_t g, void *begin_event, void *end_event) {
+    if (!g) return fail(EMO_ERR_INVALID_ARGUMENT, "graph handle is NULL");
+    g->ev_begin = static_cast<hipEvent_t>(begin_event);
+    g->ev_end = static_cast<hipEvent_t>(end_event);
+    return ok();
+}
+
 emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len) {
     if (!g || !len) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
     if (!g->jit_eligible) return fail(EMO_ERR_UNSUPPORTED, "graph too large to specialise");
@@ -640,7 +650,11 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
         hipError_t ea = hipMallocAsync(&part, static_cast<size_t>(nblocks) * emo::kPartialBytes, st);
         if (ea != hipSuccess) return fail(EMO_ERR_OUT_OF_MEMORY, "hipMallocAsync: %s", hipGetErrorString(ea));
     }
-    hipError_t e;
+    hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
+    if (e != hipSuccess) {
+        if (part) (void)hipFreeAsync(part, st);
+        return after_launch(e, "hipEventRecord");
+    }
     if (slack) {
         if (jit) {
             e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy, target,
@@ -656,6 +670,7 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     } else {
         e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, part, st);
     }
+    if (e == hipSuccess && g->ev_end) e = hipEventRecord(g->ev_end, st);
     if (result) {
         if (e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
         hipError_t ef = hipFreeAsync(part, st);

@@ -100,12 +100,27 @@ __device__ void emo_select_finalize(const EmoPartial *part, long long n, void *r
     unsigned long long key = ~0ull;
     float T = 0.f;
     unsigned long long cnt = 0;
-    for (long long i = threadIdx.x; i < n; i += EMO_BLOCK) {
-        const EmoPartial p = part[i];
-        cnt += p.count;
-        if (p.key < key) {
-            key = p.key;
-            T = p.makespan;
+    // four independent loads in flight per thread: the single workgroup is latency-bound
+    for (long long base = threadIdx.x; base < n; base += 4 * EMO_BLOCK) {
+        EmoPartial p[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const long long i = base + k * EMO_BLOCK;
+            if (i < n) {
+                p[k] = part[i];
+            } else {
+                p[k].key = ~0ull;
+                p[k].count = 0;
+                p[k].makespan = 0.f;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            cnt += p[k].count;
+            if (p[k].key < key) {
+                key = p[k].key;
+                T = p[k].makespan;
+            }
         }
     }
     emo_wave_min_key(&key, &T);

@@ -24,7 +24,8 @@ ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_kernel_mode", "emo_graph_topo_order",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
                 "emo_select_from_results",
-                "emo_graph_specialized_source", "emo_status_string", "emo_last_error")
+                "emo_graph_set_timing_events", "emo_graph_specialized_source", "emo_status_string",
+                "emo_last_error")
 
 
 class EmoError(RuntimeError):
@@ -67,6 +68,7 @@ def _load_library():
         "emo_evaluate": [P, P, i64, P, P, P, i32, f32, P, P, P],
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
         "emo_graph_specialized_source": [P, P, P],
+        "emo_graph_set_timing_events": [P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -172,6 +174,13 @@ class EmoGraph:
         inf = GraphInfo()
         _check(lib.emo_graph_get_info(self._h, ctypes.byref(inf)))
         return inf.as_dict()
+
+    def set_timing_events(self, begin=None, end=None):
+        """Record torch.cuda.Event `begin`/`end` around the evaluating kernel of later calls
+        (events that have been recorded once, so that they exist); None disables."""
+        hb = ctypes.c_void_p(begin.cuda_event) if begin is not None else None
+        he = ctypes.c_void_p(end.cuda_event) if end is not None else None
+        _check(lib.emo_graph_set_timing_events(self._h, hb, he))
 
     def specialized_source(self) -> str:
         n = ctypes.c_int64(0)
