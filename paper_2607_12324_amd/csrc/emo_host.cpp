@@ -49,19 +49,28 @@ emo_status device_fail(hipError_t e, const char *where) {
     return fail(EMO_ERR_DEVICE, "%s: %s", where, hipGetErrorString(e));
 }
 
-// Program compiled on the host before upload.
-struct HostProgram {
-    std::vector<emo::Op> op;
-    std::vector<int2> in_range;
-    std::vector<int32_t> ins;
-    std::vector<int2> succ_range;
-    std::vector<int32_t> succs;
-    std::vector<int32_t> out_col;
-    std::vector<int32_t> seq;   // node of each step
-    int32_t n_slots = 0;
-    float t_const = 0.f;
-    bool pack_monotone = true;
+// Topological schedule of a traversal: the node of each step and, per step, the steps of its
+// candidate-dependent predecessors and successors.
+struct Schedule {
+    std::vector<int32_t> seq;
+    std::vector<std::vector<int32_t>> in, out;
+    std::vector<float> cst;      // latest finish among candidate-independent predecessors
+    bool monotone = true;        // packs in increasing id
 };
+
+// Interpreter program compiled on the host before upload.
+struct HostProgram {
+    std::vector<emo::FwdStep> fwd;
+    std::vector<uint32_t> ins;
+    std::vector<emo::BwdStep> bwd;
+    std::vector<uint32_t> succs;
+    int32_t n_cold = 0, n_cold_bwd = 0, n_hot = 0, n_hot_bwd = 0;
+    float t_const = 0.f;
+    bool monotone = true;
+};
+
+// A value read again within this many steps is kept in the register bank when a slot is free.
+constexpr int32_t kHotSpan = 96;
 
 constexpr int32_t kJitMaxOps = 2048;      // larger graphs compile too slowly to specialise
 constexpr int32_t kJitMaxSlackOps = 160;  // every finish time stays in a VGPR
@@ -184,21 +193,15 @@ void fold_constants(emo_graph_s &g) {
     g.t_const = tc;
 }
 
-uint32_t fbits(float x) {
-    uint32_t u;
-    std::memcpy(&u, &x, 4);
-    return u;
-}
 
-// Compile a traversal.  fold: only candidate-dependent nodes become steps; backward: every step
-// keeps its own slot (needed for the reverse pass); per_node: slack columns are node ids.
-HostProgram build_program(const emo_graph_s &g, bool fold, bool backward, bool per_node) {
-    HostProgram hp;
+// Topological order of the traversal.  fold: only candidate-dependent nodes become steps.
+// Ready nodes are taken by (key, id) with key = pack id for packs and -1 for fixed nodes, so
+// packs are visited in increasing pack id whenever the pack numbering is consistent with the
+// precedence edges.
+Schedule make_schedule(const emo_graph_s &g, bool fold) {
+    Schedule sc;
     const int32_t V = g.V;
     auto included = [&](int32_t v) { return !fold || g.dyn[v]; };
-    // Kahn over included nodes; ready nodes are taken by (key, id) with key = pack id for packs
-    // and -1 for fixed nodes, so packs are visited in increasing pack id whenever the pack
-    // numbering is consistent with the precedence edges.
     std::vector<int32_t> indeg(V, 0);
     for (int32_t v = 0; v < V; ++v) {
         if (!included(v)) continue;
@@ -210,92 +213,138 @@ HostProgram build_program(const emo_graph_s &g, bool fold, bool backward, bool p
     auto key = [&](int32_t v) -> int64_t { return g.pack[v] >= 0 ? g.pack[v] : -1; };
     for (int32_t v = 0; v < V; ++v)
         if (included(v) && indeg[v] == 0) ready.push({key(v), v});
-    std::vector<int32_t> seq;
     while (!ready.empty()) {
         int32_t v = ready.top().second;
         ready.pop();
-        seq.push_back(v);
+        sc.seq.push_back(v);
         for (int32_t j = g.succ_off[v]; j < g.succ_off[v + 1]; ++j) {
             int32_t u = g.succ[j];
             if (included(u) && --indeg[u] == 0) ready.push({key(u), u});
         }
     }
-    const int32_t n = static_cast<int32_t>(seq.size());
-    hp.seq = seq;
+    const int32_t n = static_cast<int32_t>(sc.seq.size());
     std::vector<int32_t> pos(V, -1);
-    for (int32_t i = 0; i < n; ++i) pos[seq[i]] = i;
-
-    // last step that reads each node's finish time
-    std::vector<int32_t> last_use(V, -1);
-    for (int32_t i = 0; i < n; ++i) {
-        int32_t v = seq[i];
-        for (int32_t j = g.pred_off[v]; j < g.pred_off[v + 1]; ++j) {
-            int32_t k = g.pred[j];
-            if (included(k)) last_use[k] = std::max(last_use[k], i);
-        }
-    }
-    std::vector<int32_t> slot(V, -1);
-    std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> free_slots;
-    int32_t next_slot = 0;
+    for (int32_t i = 0; i < n; ++i) pos[sc.seq[i]] = i;
+    sc.in.resize(n);
+    sc.out.resize(n);
+    sc.cst.assign(n, 0.f);
     int32_t last_pack = -1;
-    hp.op.resize(n);
-    hp.in_range.resize(n);
-    hp.out_col.resize(n, -1);
     for (int32_t i = 0; i < n; ++i) {
-        int32_t v = seq[i];
-        float cst = 0.f;
-        int32_t begin = static_cast<int32_t>(hp.ins.size());
-        std::vector<int32_t> released;
+        const int32_t v = sc.seq[i];
         for (int32_t j = g.pred_off[v]; j < g.pred_off[v + 1]; ++j) {
-            int32_t k = g.pred[j];
-            if (included(k)) {
-                hp.ins.push_back(backward ? pos[k] : slot[k]);
-                if (!backward && last_use[k] == i) released.push_back(slot[k]);
-            } else {
-                cst = std::max(cst, g.const_eft[k]);
-            }
+            const int32_t k = g.pred[j];
+            if (included(k)) sc.in[i].push_back(pos[k]);
+            else sc.cst[i] = std::max(sc.cst[i], g.const_eft[k]);
         }
-        hp.in_range[i] = make_int2(begin, static_cast<int32_t>(hp.ins.size()));
-        for (int32_t s : released) free_slots.push(s);
-        int32_t out = -1;
-        if (backward) {
-            out = i;
-        } else if (last_use[v] >= 0) {
-            if (!free_slots.empty()) {
-                out = free_slots.top();
-                free_slots.pop();
-            } else {
-                out = next_slot++;
-            }
-            slot[v] = out;
-        }
-        emo::Op op;
-        op.pack = g.pack[v];
-        op.cst = fbits(cst);
-        op.dur = fbits(g.pack[v] >= 0 ? 0.f : g.dur[v]);
-        op.out = out;
-        hp.op[i] = op;
-        if (per_node) hp.out_col[i] = v;
-        else hp.out_col[i] = g.pack[v];
+        for (int32_t j = g.succ_off[v]; j < g.succ_off[v + 1]; ++j)
+            if (included(g.succ[j])) sc.out[i].push_back(pos[g.succ[j]]);
         if (g.pack[v] >= 0) {
-            if (g.pack[v] < last_pack) hp.pack_monotone = false;
+            if (g.pack[v] < last_pack) sc.monotone = false;
             last_pack = g.pack[v];
         }
     }
-    hp.n_slots = backward ? n : next_slot;
-    hp.t_const = fold ? g.t_const : 0.f;
-    if (backward) {
-        hp.succ_range.resize(n);
-        for (int32_t i = 0; i < n; ++i) {
-            int32_t v = seq[i];
-            int32_t begin = static_cast<int32_t>(hp.succs.size());
-            for (int32_t j = g.succ_off[v]; j < g.succ_off[v + 1]; ++j) {
-                int32_t u = g.succ[j];
-                if (included(u)) hp.succs.push_back(pos[u]);
+    return sc;
+}
+
+// Hot (register bank) and cold (device scratch) slot pools; the lowest free index is reused.
+struct SlotPool {
+    std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> hot_free, cold_free;
+    int32_t next_hot = 0, next_cold = 0;
+    uint32_t acquire(bool want_hot) {
+        if (want_hot) {
+            if (!hot_free.empty()) {
+                int32_t h = hot_free.top();
+                hot_free.pop();
+                return static_cast<uint32_t>(h);
             }
-            hp.succ_range[i] = make_int2(begin, static_cast<int32_t>(hp.succs.size()));
+            if (next_hot < emo::kHotSlots) return static_cast<uint32_t>(next_hot++);
         }
+        int32_t c;
+        if (!cold_free.empty()) {
+            c = cold_free.top();
+            cold_free.pop();
+        } else {
+            c = next_cold++;
+        }
+        return emo::kColdRef | static_cast<uint32_t>(c);
     }
+    void release(uint32_t ref) {
+        if (ref & emo::kColdRef) cold_free.push(static_cast<int32_t>(ref & ~emo::kColdRef));
+        else hot_free.push(static_cast<int32_t>(ref));
+    }
+};
+
+uint32_t fbits(float x) {
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    return u;
+}
+
+// Interpreter program for a schedule.  backward: add the reverse pass (slack); per_node: slack
+// columns are node ids, else pack ids.
+HostProgram compile_program(const emo_graph_s &g, const Schedule &sc, bool fold, bool backward,
+                            bool per_node) {
+    HostProgram hp;
+    const int32_t n = static_cast<int32_t>(sc.seq.size());
+    hp.t_const = fold ? g.t_const : 0.f;
+    hp.monotone = sc.monotone;
+    // forward: a finish time stays live until its last reader
+    std::vector<int32_t> last_use(n, -1);
+    for (int32_t i = 0; i < n; ++i)
+        for (int32_t k : sc.in[i]) last_use[k] = std::max(last_use[k], i);
+    std::vector<uint32_t> ref(n, 0);
+    SlotPool pool;
+    hp.fwd.resize(n);
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t v = sc.seq[i];
+        emo::FwdStep st{};
+        st.pack = g.pack[v];
+        st.cst = fbits(sc.cst[i]);
+        st.dur = fbits(g.pack[v] >= 0 ? 0.f : g.dur[v]);
+        st.in_begin = static_cast<int32_t>(hp.ins.size());
+        st.in_count = static_cast<int32_t>(sc.in[i].size());
+        for (int32_t k : sc.in[i]) hp.ins.push_back(ref[k]);
+        for (int32_t k : sc.in[i])
+            if (last_use[k] == i) pool.release(ref[k]);
+        if (sc.out[i].empty()) st.flags |= emo::kStepSink;
+        if (last_use[i] >= 0) {
+            ref[i] = pool.acquire(last_use[i] - i <= kHotSpan);
+            st.flags |= emo::kStepOut;
+            st.out = ref[i];
+        }
+        hp.fwd[i] = st;
+    }
+    hp.n_cold = pool.next_cold;
+    hp.n_hot = pool.next_hot;
+    if (!backward) return hp;
+    // backward: a latest start time stays live until its first predecessor (in forward order)
+    std::vector<int32_t> first_pred(n, -1);
+    for (int32_t i = 0; i < n; ++i)
+        if (!sc.in[i].empty()) first_pred[i] = *std::min_element(sc.in[i].begin(), sc.in[i].end());
+    std::vector<uint32_t> bref(n, 0);
+    SlotPool bpool;
+    hp.bwd.reserve(n);
+    for (int32_t i = n - 1; i >= 0; --i) {
+        const int32_t v = sc.seq[i];
+        emo::BwdStep st{};
+        st.pack = g.pack[v];
+        st.dur = fbits(g.pack[v] >= 0 ? 0.f : g.dur[v]);
+        st.succ_begin = static_cast<int32_t>(hp.succs.size());
+        st.succ_count = static_cast<int32_t>(sc.out[i].size());
+        for (int32_t u : sc.out[i]) hp.succs.push_back(bref[u]);
+        for (int32_t u : sc.out[i])
+            if (first_pred[u] == i) bpool.release(bref[u]);
+        if (first_pred[i] >= 0) {
+            bref[i] = bpool.acquire(i - first_pred[i] <= kHotSpan);
+            st.flags |= emo::kStepOut;
+            st.out = bref[i];
+        }
+        st.col = per_node ? v : g.pack[v];
+        st.fwd = i;
+        hp.bwd.push_back(st);
+    }
+    hp.n_cold_bwd = bpool.next_cold;
+    hp.n_hot_bwd = bpool.next_hot;
     return hp;
 }
 
@@ -315,18 +364,16 @@ emo_status upload(emo_graph_s &g, const std::vector<T> &host, const T **dev) {
 }
 
 emo_status upload_program(emo_graph_s &g, const HostProgram &hp, emo::DevProgram &dp) {
-    dp.n_ops = static_cast<int32_t>(hp.op.size());
-    dp.n_slots = hp.n_slots;
+    dp.n_ops = static_cast<int32_t>(hp.fwd.size());
+    dp.n_cold = hp.n_cold;
+    dp.n_cold_bwd = hp.n_cold_bwd;
     dp.t_const = hp.t_const;
+    dp.monotone = hp.monotone ? 1 : 0;
     emo_status s;
-    if ((s = upload(g, hp.op, &dp.op)) != EMO_OK) return s;
-    if ((s = upload(g, hp.in_range, &dp.in_range)) != EMO_OK) return s;
+    if ((s = upload(g, hp.fwd, &dp.fwd)) != EMO_OK) return s;
     if ((s = upload(g, hp.ins, &dp.ins)) != EMO_OK) return s;
-    if ((s = upload(g, hp.out_col, &dp.out_col)) != EMO_OK) return s;
-    if (!hp.succ_range.empty() || dp.n_ops == 0) {
-        if ((s = upload(g, hp.succ_range, &dp.succ_range)) != EMO_OK) return s;
-        if ((s = upload(g, hp.succs, &dp.succs)) != EMO_OK) return s;
-    }
+    if ((s = upload(g, hp.bwd, &dp.bwd)) != EMO_OK) return s;
+    if ((s = upload(g, hp.succs, &dp.succs)) != EMO_OK) return s;
     return EMO_OK;
 }
 
@@ -341,24 +388,25 @@ void release_device(emo_graph_s *g) {
 
 bool is_pow2(int32_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
-// The specialised kernels' view of the graph: the slack program's steps, with predecessors and
-// successors as step indices.
-emo::JitGraph make_jit_graph(const emo_graph_s &g, const HostProgram &ps) {
+// The specialised kernels' view of the graph: the folded schedule's steps, with predecessors
+// and successors as step indices.
+emo::JitGraph make_jit_graph(const emo_graph_s &g, const Schedule &sc) {
     emo::JitGraph jg;
     jg.P = g.P;
     jg.F = g.F;
     jg.static_power = g.static_power;
-    jg.t_const = ps.t_const;
-    jg.pack_monotone = ps.pack_monotone;
-    const size_t n = ps.op.size();
+    jg.t_const = g.t_const;
+    jg.pack_monotone = sc.monotone;
+    const size_t n = sc.seq.size();
     jg.ops.resize(n);
     for (size_t i = 0; i < n; ++i) {
         emo::JitOp &o = jg.ops[i];
-        o.pack = ps.op[i].pack;
-        std::memcpy(&o.cst, &ps.op[i].cst, 4);
-        std::memcpy(&o.dur, &ps.op[i].dur, 4);
-        o.in.assign(ps.ins.begin() + ps.in_range[i].x, ps.ins.begin() + ps.in_range[i].y);
-        o.out.assign(ps.succs.begin() + ps.succ_range[i].x, ps.succs.begin() + ps.succ_range[i].y);
+        const int32_t v = sc.seq[i];
+        o.pack = g.pack[v];
+        o.cst = sc.cst[i];
+        o.dur = g.pack[v] >= 0 ? 0.f : g.dur[v];
+        o.in = sc.in[i];
+        o.out = sc.out[i];
     }
     return jg;
 }
@@ -526,24 +574,26 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     if (s != EMO_OK) return s;
     fold_constants(*g);
 
-    HostProgram pe = build_program(*g, true, false, false);
-    HostProgram ps = build_program(*g, true, true, false);
-    HostProgram pn = build_program(*g, false, true, true);
+    const Schedule sf = make_schedule(*g, true);
+    const Schedule sa = make_schedule(*g, false);
+    HostProgram pe = compile_program(*g, sf, true, false, false);
+    HostProgram ps = compile_program(*g, sf, true, true, false);
+    HostProgram pn = compile_program(*g, sa, false, true, true);
 
     emo_graph_info &in = g->info;
     in.num_nodes = V; in.num_edges = g->E; in.num_packs = P; in.num_levels = F;
-    in.num_dynamic_nodes = static_cast<int32_t>(pe.op.size());
+    in.num_dynamic_nodes = static_cast<int32_t>(pe.fwd.size());
     in.num_dynamic_edges = static_cast<int32_t>(pe.ins.size());
-    in.eval_slots = pe.n_slots;
+    in.eval_slots = pe.n_hot + pe.n_cold;
     in.const_makespan = g->t_const;
     in.device = device;
-    in.pack_order_monotone = pe.pack_monotone ? 1 : 0;
+    in.pack_order_monotone = sf.monotone ? 1 : 0;
     in.kernel_mode = EMO_KERNELS_AUTO;
-    g->jg = make_jit_graph(*g, ps);
-    const int32_t nops = static_cast<int32_t>(ps.op.size());
+    g->jg = make_jit_graph(*g, sf);
+    const int32_t nops = static_cast<int32_t>(sf.seq.size());
     g->jit_eligible = nops >= 1 && nops <= kJitMaxOps;
     g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;
-    g->jit_slack_staged = ps.pack_monotone && P % 16 == 0;
+    g->jit_slack_staged = sf.monotone && P % 16 == 0;
 
     if (device >= 0) {
         DeviceGuard guard(device);

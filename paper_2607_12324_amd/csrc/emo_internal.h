@@ -14,39 +14,57 @@ namespace emo {
 
 constexpr int kTablePad = 256;   // extra zeroed table entries: any level byte stays in bounds
 
-// One step of a kernel program: a node visited in topological order.
-//   pack     pack id, or -1 for a node of fixed duration
-//   cst      fp32 bits: the latest finish time among the node's candidate-independent
-//            predecessors (0 when it has none); the start time is at least this
-//   dur      fp32 bits: the fixed duration (pack == -1)
-//   out      finish-time slot written by this step, or -1
-struct Op {
-    int32_t pack;
-    uint32_t cst;
-    uint32_t dur;
-    int32_t out;
+// Slot references of the interpreting kernels.  A finish time (forward) or latest start time
+// (backward) that is read again soon lives in a 32-entry register bank of each lane ("hot",
+// indexed wave-uniformly); one that stays live longer lives in device scratch laid out
+// [slot][candidate] ("cold", bit 31 of the reference set).
+constexpr uint32_t kColdRef = 0x80000000u;
+constexpr int kHotSlots = 32;
+constexpr uint32_t kStepSink = 1u;   // forward: the node has no successor
+constexpr uint32_t kStepOut = 2u;    // the step writes its value to `out`
+
+// Forward step (32 bytes, one scalar load): a candidate-dependent node in topological order.
+struct FwdStep {
+    int32_t pack;       // pack id, or -1 for a node of fixed duration
+    uint32_t cst;       // fp32 bits: latest finish among candidate-independent predecessors
+    uint32_t dur;       // fp32 bits: the fixed duration (pack == -1)
+    uint32_t flags;     // kStepSink | kStepOut
+    uint32_t out;       // slot reference of the finish time
+    int32_t in_begin;   // predecessor references: ins[in_begin, in_begin + in_count)
+    int32_t in_count;
+    int32_t pad;
 };
 
-// A compiled traversal.  Forward programs list candidate-dependent nodes in a topological
-// order; every predecessor that is itself candidate-dependent is read from a slot.
+// Backward step (32 bytes), in reverse order of the forward steps.
+struct BwdStep {
+    int32_t pack;       // pack id, or -1
+    uint32_t dur;       // fp32 bits: the fixed duration (pack == -1)
+    uint32_t flags;     // kStepOut: predecessors read this node's latest start time
+    uint32_t out;       // slot reference of the latest start time
+    int32_t succ_begin; // successor references: succs[succ_begin, succ_begin + succ_count)
+    int32_t succ_count; // 0 for a sink: its latest finish is the makespan
+    int32_t col;        // slack output column, -1 for none
+    int32_t fwd;        // index of the node's forward step (its finish time is kept there)
+};
+
+// A compiled traversal for the interpreting kernels.
 struct DevProgram {
     int32_t n_ops = 0;
-    int32_t n_slots = 0;
-    float t_const = 0.f;           // makespan floor from candidate-independent nodes
-    const Op *op = nullptr;        // [n_ops]
-    const int2 *in_range = nullptr;   // [n_ops] {begin, end} into ins
-    const int32_t *ins = nullptr;     // slot indices of candidate-dependent predecessors
-    // backward (slack) programs only: slot of step i is i
-    const int2 *succ_range = nullptr; // [n_ops] {begin, end} into succs
-    const int32_t *succs = nullptr;   // step indices of successors
-    const int32_t *out_col = nullptr; // [n_ops] column of the slack output, -1 for none
+    int32_t n_cold = 0;          // cold forward slots
+    int32_t n_cold_bwd = 0;      // cold backward slots
+    float t_const = 0.f;         // makespan floor from candidate-independent nodes
+    int32_t monotone = 1;        // packs visited in increasing id
+    const FwdStep *fwd = nullptr;
+    const uint32_t *ins = nullptr;
+    const BwdStep *bwd = nullptr;     // slack programs only
+    const uint32_t *succs = nullptr;
 };
 
 struct DevGraph {
     int32_t V = 0, P = 0, F = 1;
     float static_power = 0.f;
-    const float2 *tab = nullptr;   // [P*F] interleaved (time, energy)
-    DevProgram eval;               // forward, slots reused (live set only)
+    const float2 *tab = nullptr;   // [P*F + kTablePad] interleaved (time, energy)
+    DevProgram eval;               // forward over candidate-dependent nodes
     DevProgram slack_pack;         // forward + backward over candidate-dependent nodes
     DevProgram slack_node;         // forward + backward over every node
 };

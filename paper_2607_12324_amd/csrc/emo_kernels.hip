@@ -1,19 +1,26 @@
-// HIP kernels for gfx950: batched what-if evaluation of per-pack frequency policies.
+// Precompiled HIP kernels for gfx950: batched what-if evaluation of per-pack frequency
+// policies by interpreting a program compiled from the graph (used for graphs too large to
+// specialise, for per-node slack and for inputs the specialised kernels cannot take).
 //
-// Layout: one candidate policy per lane.  Every lane of a wave walks the same compiled program
-// (the graph is shared by all candidates), so the program, its predecessor lists and the table
-// base offsets are wave-uniform and come through scalar loads; only the level bytes, the table
-// entries they select and the finish times differ per lane.
+// Layout: one candidate policy per lane.  Every lane of a wave walks the same program (the
+// graph is shared by all candidates), so steps, predecessor lists and slot references are
+// wave-uniform and come through scalar loads; only level bytes, the table entries they select
+// and finish times differ per lane.
 //
-// Per step (one node in topological order, Eq. 1 and Alg. 1):
+// Per forward step (one node in topological order, Eq. 1 and Alg. 1):
 //   EST = max(cst, finish times of candidate-dependent predecessors)
 //   EFT = EST + dur,  dur = table time at the pack's level (Eq. 3) or the fixed duration
-// The makespan is the running max (Eq. 2); pack energies are summed in fp32 blocks of 64 packs
-// that are added into an fp64 total, and the static term static_power * T closes Eq. 2.
+// The makespan is the max over sinks (Eq. 2); pack energies are summed in fp32 blocks of 64
+// packs added into an fp64 total, and the static term static_power * T closes Eq. 2.  The
+// backward pass (slack) walks the steps in reverse: LFT = min over successors of their latest
+// start (T for a sink), slack = LFT - EFT, latest start = LFT - dur.
 //
-// Finish-time slots live in LDS (slot k of lane L at [k][L] in the wave's region, conflict
-// free) when they fit, otherwise in device scratch laid out [slot][candidate] so that a wave's
-// access to one slot is one contiguous 256-byte segment.
+// Storage per lane:
+//   hot    32-entry register bank (uniform dynamic index) for values read again soon;
+//   cold   device scratch [slot][candidate] for values that stay live long;
+//   keep   device scratch [step][candidate]: every finish time, for the backward pass;
+//   levels the current 128-byte line of the candidate's level row, in registers.
+// Scratch layouts put one wave's access to a slot in one contiguous 256-byte segment.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -27,18 +34,68 @@ constexpr int kBlock = EMO_BLOCK;
 constexpr int kWave = EMO_WAVE;
 constexpr int kWavesPerBlock = EMO_WAVES_PER_BLOCK;
 constexpr int kEnergyBlock = 64;
-constexpr size_t kLdsBudget = 60 * 1024;   // dynamic LDS, leaves room for static LDS under 64 KB
+constexpr int kStage = 32;            // packs per staged slack segment (one 128-byte line)
+constexpr size_t kLdsBudget = 60 * 1024;
 
-struct Slots {
-    float *lds;        // this wave's LDS region, or nullptr
-    float *glob;       // device scratch [slot][Bpad], or nullptr
-    int64_t stride;    // Bpad
-    int64_t col;       // this lane's column in the scratch
-    int lane;
-    __device__ __forceinline__ float &at(int k) const {
-        return lds ? lds[k * kWave + lane] : glob[static_cast<int64_t>(k) * stride + col];
-    }
+typedef float f32x32 __attribute__((ext_vector_type(32)));
+typedef unsigned int u32x32 __attribute__((ext_vector_type(32)));
+
+__device__ __forceinline__ uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ int32_t uni(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// The candidate's level row, read one 128-byte line (8 x 16 bytes) at a time into a register
+// bank `w` (kept as a plain local of the calling pass so that it stays in VGPRs).
+struct Row {
+    const uint8_t *row;
+    int P;
+    bool vec;       // rows are 16-byte aligned: line loads; otherwise byte loads
 };
+
+__device__ __forceinline__ void load_line(const Row &r, u32x32 &w, int gidx) {
+    const uint4 *src = reinterpret_cast<const uint4 *>(r.row) + gidx * 8;
+    const int nvec = min(8, (r.P - gidx * 128 + 15) / 16);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        if (k < nvec) {
+            const uint4 v = src[k];
+            w[4 * k + 0] = v.x;
+            w[4 * k + 1] = v.y;
+            w[4 * k + 2] = v.z;
+            w[4 * k + 3] = v.w;
+        }
+    }
+}
+
+__device__ __forceinline__ unsigned level_at(const Row &r, u32x32 &w, int &group, int p) {
+    if (!r.vec) return r.row[p];
+    const int gidx = p >> 7;
+    if (gidx != group) {
+        load_line(r, w, gidx);
+        group = gidx;
+    }
+    const unsigned word = w[(p >> 2) & 31];
+    return (word >> ((p & 3) << 3)) & 0xffu;
+}
+
+struct Scratch {
+    float *cold;        // [n_cold][bpad]
+    float *keep;        // [n_ops][bpad] (slack) or nullptr
+    float *cold_bwd;    // [n_cold_bwd][bpad]
+    int64_t bpad;
+    int64_t col;        // this lane's column
+};
+
+__device__ __forceinline__ float slot_get(const f32x32 &hot, const float *cold, int64_t bpad,
+                                          int64_t col, uint32_t ref) {
+    if (ref & kColdRef) return cold[static_cast<int64_t>(ref & ~kColdRef) * bpad + col];
+    return hot[ref];
+}
+
+__device__ __forceinline__ void slot_set(f32x32 &hot, float *cold, int64_t bpad, int64_t col,
+                                         uint32_t ref, float v) {
+    if (ref & kColdRef) cold[static_cast<int64_t>(ref & ~kColdRef) * bpad + col] = v;
+    else hot[ref] = v;
+}
 
 struct Fwd {
     float T;
@@ -46,29 +103,32 @@ struct Fwd {
     bool bad;
 };
 
-__device__ __forceinline__ float2 table_at(const float2 *tab_lds, const float2 *tab, int idx) {
-    return tab_lds ? tab_lds[idx] : tab[idx];
-}
-
-// Forward pass of one candidate (row = its level bytes).
-__device__ Fwd forward(const DevProgram &pr, const float2 *tab_lds, const float2 *tab, int F,
-                       float static_power, const uint8_t *row, const Slots &sl) {
+template <bool TAB_LDS, bool KEEP>
+__device__ __forceinline__ Fwd run_forward(const DevProgram &pr, const float2 *tab, int F, float static_power,
+                           const Row &row, f32x32 &hot, const Scratch &sc) {
+    u32x32 lw;
+    int lgroup = -1;
     float T = pr.t_const;
     double eacc = 0.0;
     float eblk = 0.f;
     int nblk = 0;
     bool bad = false;
-    for (int i = 0; i < pr.n_ops; ++i) {
-        const Op op = pr.op[i];
-        const int2 r = pr.in_range[i];
-        float est = __uint_as_float(op.cst);
-        for (int j = r.x; j < r.y; ++j) est = fmaxf(est, sl.at(pr.ins[j]));
+    const int n = pr.n_ops;
+    for (int i = 0; i < n; ++i) {
+        const FwdStep st = pr.fwd[i];
+        const uint32_t flags = uni(st.flags);
+        const int32_t pack = uni(st.pack);
+        const int32_t nin = uni(st.in_count);
+        const int32_t ib = uni(st.in_begin);
+        float est = __uint_as_float(uni(st.cst));
+        for (int j = 0; j < nin; ++j)
+            est = fmaxf(est, slot_get(hot, sc.cold, sc.bpad, sc.col, uni(pr.ins[ib + j])));
         float dur;
-        if (op.pack >= 0) {
-            unsigned l = row[op.pack];
-            bad |= (l >= static_cast<unsigned>(F));
+        if (pack >= 0) {
+            unsigned l = level_at(row, lw, lgroup, pack);
+            bad |= l >= static_cast<unsigned>(F);
             l = l < static_cast<unsigned>(F) ? l : 0u;
-            const float2 te = table_at(tab_lds, tab, op.pack * F + static_cast<int>(l));
+            const float2 te = tab[pack * F + static_cast<int>(l)];
             dur = te.x;
             eblk += te.y;
             if (++nblk == kEnergyBlock) {
@@ -77,11 +137,12 @@ __device__ Fwd forward(const DevProgram &pr, const float2 *tab_lds, const float2
                 nblk = 0;
             }
         } else {
-            dur = __uint_as_float(op.dur);
+            dur = __uint_as_float(uni(st.dur));
         }
         const float eft = est + dur;
-        if (op.out >= 0) sl.at(op.out) = eft;
-        T = fmaxf(T, eft);
+        if (flags & kStepOut) slot_set(hot, sc.cold, sc.bpad, sc.col, uni(st.out), eft);
+        if (flags & kStepSink) T = fmaxf(T, eft);
+        if (KEEP) sc.keep[static_cast<int64_t>(i) * sc.bpad + sc.col] = eft;
     }
     eacc += static_cast<double>(eblk);
     Fwd f;
@@ -95,115 +156,147 @@ __device__ Fwd forward(const DevProgram &pr, const float2 *tab_lds, const float2
     return f;
 }
 
+// Writes the slack of packs [p0, p0 + kStage) of the wave's 64 candidates, staged in LDS as
+// stg[pack - p0][lane] (stride 65 floats), with 16-byte stores: each candidate's segment is one
+// 128-byte line.
+__device__ __forceinline__ void flush_stage(const float *stg, float *__restrict__ S, int64_t cols,
+                                            int64_t wbase, int64_t B, int p0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int lane = threadIdx.x % kWave;
+    constexpr int per_row = kStage / 4;
+#pragma unroll
+    for (int m = 0; m < per_row; ++m) {
+        const int j = lane + kWave * m;
+        const int r = j / per_row, part = j % per_row;
+        float4 v;
+        v.x = stg[(4 * part + 0) * 65 + r];
+        v.y = stg[(4 * part + 1) * 65 + r];
+        v.z = stg[(4 * part + 2) * 65 + r];
+        v.w = stg[(4 * part + 3) * 65 + r];
+        const int64_t row = wbase + r;
+        if (row < B) *reinterpret_cast<float4 *>(S + row * cols + p0 + 4 * part) = v;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <bool STAGED>
+__device__ __forceinline__ void run_backward(const DevProgram &pr, const float2 *tab, int F, float T, bool bad,
+                             const Row &row, f32x32 &hot, const Scratch &sc, float *__restrict__ S,
+                             int64_t cols, int64_t cand, bool active, float *stg, int64_t wbase,
+                             int64_t B) {
+    u32x32 lw;
+    int lgroup = -1;
+    const int n = pr.n_ops;
+    const float inf = __builtin_inff();
+    const float nan = __builtin_nanf("");
+    const int lane = threadIdx.x % kWave;
+    float eft_next = n > 0 ? sc.keep[static_cast<int64_t>(uni(pr.bwd[0].fwd)) * sc.bpad + sc.col] : 0.f;
+    for (int r = 0; r < n; ++r) {
+        const BwdStep st = pr.bwd[r];
+        const float eft = eft_next;
+        if (r + 1 < n)   // the next step's finish time is fetched one step ahead
+            eft_next = sc.keep[static_cast<int64_t>(uni(pr.bwd[r + 1].fwd)) * sc.bpad + sc.col];
+        const uint32_t flags = uni(st.flags);
+        const int32_t pack = uni(st.pack);
+        const int32_t ns = uni(st.succ_count);
+        const int32_t sb = uni(st.succ_begin);
+        const int32_t col = uni(st.col);
+        float lft = T;
+        if (ns > 0) {
+            lft = inf;
+            for (int j = 0; j < ns; ++j)
+                lft = fminf(lft, slot_get(hot, sc.cold_bwd, sc.bpad, sc.col, uni(pr.succs[sb + j])));
+        }
+        float dur;
+        if (pack >= 0) {
+            unsigned l = level_at(row, lw, lgroup, pack);
+            l = l < static_cast<unsigned>(F) ? l : 0u;
+            dur = tab[pack * F + static_cast<int>(l)].x;
+        } else {
+            dur = __uint_as_float(uni(st.dur));
+        }
+        if (flags & kStepOut) slot_set(hot, sc.cold_bwd, sc.bpad, sc.col, uni(st.out), lft - dur);
+        if (col >= 0) {
+            const float v = bad ? nan : lft - eft;
+            if (STAGED) {
+                stg[(col & (kStage - 1)) * 65 + lane] = v;
+                if ((col & (kStage - 1)) == 0) flush_stage(stg, S, cols, wbase, B, col);
+            } else if (active) {
+                S[cand * cols + col] = v;
+            }
+        }
+    }
+}
+
 // Stage the (time, energy) table into LDS when it fits.
-__device__ const float2 *stage_table(const DevGraph &g, float2 *smem_tab, bool use_lds) {
-    if (!use_lds) return nullptr;
-    const int n = g.P * g.F;
-    for (int i = threadIdx.x; i < n; i += blockDim.x) smem_tab[i] = g.tab[i];
+__device__ const float2 *stage_table(const DevGraph &g, float2 *smem) {
+    const int n = g.P * g.F + kTablePad;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) smem[i] = g.tab[i];
     __syncthreads();
-    return smem_tab;
+    return smem;
 }
 
-struct LaunchShape {
-    bool tab_lds;
-    bool slot_lds;
-    size_t tab_bytes;
-    size_t slot_bytes;   // per block
-    size_t lds_bytes;
-};
-
-LaunchShape shape_for(const DevGraph &g, int n_slots) {
-    LaunchShape s;
-    s.tab_bytes = static_cast<size_t>(g.P) * g.F * sizeof(float2);
-    s.tab_lds = s.tab_bytes <= 32 * 1024;
-    size_t tb = s.tab_lds ? (s.tab_bytes + 15) / 16 * 16 : 0;
-    size_t sb = static_cast<size_t>(n_slots) * kWave * sizeof(float) * kWavesPerBlock;
-    s.slot_lds = tb + sb <= kLdsBudget;
-    s.slot_bytes = s.slot_lds ? sb : 0;
-    s.lds_bytes = tb + s.slot_bytes;
-    return s;
-}
-
-struct Ctx {
-    const float2 *tab_lds;
-    Slots sl;
-    int64_t c;        // candidate of this lane (clamped to B-1 for idle lanes)
+struct LaneCtx {
+    int64_t gid, cand, wbase;
     bool active;
 };
 
-__device__ Ctx make_ctx(const DevGraph &g, int n_slots, bool tab_lds, bool slot_lds,
-                        float *gslots, int64_t bpad, int64_t B) {
-    extern __shared__ float4 smem4[];
-    char *smem = reinterpret_cast<char *>(smem4);
-    const size_t tab_bytes = static_cast<size_t>(g.P) * g.F * sizeof(float2);
-    const size_t tb = tab_lds ? (tab_bytes + 15) / 16 * 16 : 0;
-    Ctx x;
-    x.tab_lds = stage_table(g, reinterpret_cast<float2 *>(smem), tab_lds);
-    const int lane = threadIdx.x % kWave;
-    const int wave = threadIdx.x / kWave;
-    const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    x.active = gid < B;
-    x.c = x.active ? gid : B - 1;
-    x.sl.lane = lane;
-    x.sl.col = gid;
-    x.sl.stride = bpad;
-    x.sl.lds = slot_lds ? reinterpret_cast<float *>(smem + tb) + static_cast<size_t>(wave) * n_slots * kWave : nullptr;
-    x.sl.glob = slot_lds ? nullptr : gslots;
+__device__ __forceinline__ LaneCtx lane_ctx(int64_t B) {
+    LaneCtx x;
+    x.gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    x.active = x.gid < B;
+    x.cand = x.active ? x.gid : B - 1;
+    x.wbase = static_cast<int64_t>(blockIdx.x) * kBlock + (threadIdx.x / kWave) * kWave;
     return x;
 }
 
 // Forward pass; makespan/energy outputs, the mask and the selection partials are each optional.
+template <bool TAB_LDS>
 __global__ void __launch_bounds__(kBlock)
 forward_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ T_out,
                float *__restrict__ E_out, float target, uint32_t *__restrict__ mask,
-               EmoPartial *part, bool tab_lds, bool slot_lds, float *gslots, int64_t bpad) {
-    Ctx x = make_ctx(g, g.eval.n_slots, tab_lds, slot_lds, gslots, bpad, B);
-    Fwd f = forward(g.eval, x.tab_lds, g.tab, g.F, g.static_power, levels + x.c * g.P, x.sl);
+               EmoPartial *part, float *cold, int64_t bpad, bool vec) {
+    extern __shared__ float4 smem4[];
+    const float2 *tab = TAB_LDS ? stage_table(g, reinterpret_cast<float2 *>(smem4)) : g.tab;
+    const LaneCtx x = lane_ctx(B);
+    const Row row{levels + x.cand * g.P, g.P, vec};
+    f32x32 hot;
+    Scratch sc{cold, nullptr, nullptr, bpad, x.gid};
+    const Fwd f = run_forward<TAB_LDS, false>(g.eval, tab, g.F, g.static_power, row, hot, sc);
     if (x.active) {
-        if (T_out) T_out[x.c] = f.T;
-        if (E_out) E_out[x.c] = f.E;
+        if (T_out) T_out[x.cand] = f.T;
+        if (E_out) E_out[x.cand] = f.E;
     }
-    if (mask || part) emo_select_block(x.active, f.T, f.E, x.c, B, target, mask, part);
+    if (mask || part) emo_select_block(x.active, f.T, f.E, x.cand, B, target, mask, part);
 }
 
+// Forward + backward (slack) pass with the same optional outputs.
+template <bool TAB_LDS, bool STAGED>
 __global__ void __launch_bounds__(kBlock)
 slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict__ levels, int64_t B,
-             float *__restrict__ slack, float *__restrict__ T_out, float *__restrict__ E_out,
-             float target, uint32_t *__restrict__ mask, EmoPartial *part,
-             bool tab_lds, bool slot_lds, float *gslots, int64_t bpad) {
-    Ctx x = make_ctx(g, pr.n_slots, tab_lds, slot_lds, gslots, bpad, B);
-    const uint8_t *row = levels + x.c * g.P;
-    Fwd f = forward(pr, x.tab_lds, g.tab, g.F, g.static_power, row, x.sl);
+             float *__restrict__ S, float *__restrict__ T_out, float *__restrict__ E_out,
+             float target, uint32_t *__restrict__ mask, EmoPartial *part, float *cold, float *keep,
+             float *cold_bwd, int64_t bpad, bool vec) {
+    extern __shared__ float4 smem4[];
+    const float2 *tab = TAB_LDS ? stage_table(g, reinterpret_cast<float2 *>(smem4)) : g.tab;
+    __shared__ float stg_all[STAGED ? kWavesPerBlock : 1][STAGED ? kStage * 65 : 1];
+    const LaneCtx x = lane_ctx(B);
+    const Row row{levels + x.cand * g.P, g.P, vec};
+    f32x32 hot;
+    Scratch sc{cold, keep, cold_bwd, bpad, x.gid};
+    const Fwd f = run_forward<TAB_LDS, true>(pr, tab, g.F, g.static_power, row, hot, sc);
     if (x.active) {
-        if (T_out) T_out[x.c] = f.T;
-        if (E_out) E_out[x.c] = f.E;
+        if (T_out) T_out[x.cand] = f.T;
+        if (E_out) E_out[x.cand] = f.E;
     }
-    // backward: slot i holds EFT of step i, replaced by its latest start time LST
-    const float T = f.T;
-    const float inf = __builtin_inff();
-    float *out_row = slack + x.c * static_cast<int64_t>(cols);
-    for (int i = pr.n_ops - 1; i >= 0; --i) {
-        const Op op = pr.op[i];
-        const int2 sr = pr.succ_range[i];
-        float lft = T;
-        if (sr.y > sr.x) {
-            lft = inf;
-            for (int j = sr.x; j < sr.y; ++j) lft = fminf(lft, x.sl.at(pr.succs[j]));
-        }
-        float dur;
-        if (op.pack >= 0) {
-            unsigned l = row[op.pack];
-            l = l < static_cast<unsigned>(g.F) ? l : 0u;
-            dur = table_at(x.tab_lds, g.tab, op.pack * g.F + static_cast<int>(l)).x;
-        } else {
-            dur = __uint_as_float(op.dur);
-        }
-        const float eft = x.sl.at(i);
-        x.sl.at(i) = lft - dur;
-        const int col = pr.out_col[i];
-        if (x.active && col >= 0) out_row[col] = f.bad ? __builtin_nanf("") : lft - eft;
-    }
-    if (mask || part) emo_select_block(x.active, f.T, f.E, x.c, B, target, mask, part);
+    float *stg = STAGED ? stg_all[threadIdx.x / kWave] : nullptr;
+    run_backward<STAGED>(pr, tab, g.F, f.bad ? 0.f : f.T, f.bad, row, hot, sc, S, cols, x.cand,
+                         x.active, stg, x.wbase, B);
+    if (mask || part) emo_select_block(x.active, f.T, f.E, x.cand, B, target, mask, part);
 }
 
 // ---------------------------------------------------------------- selection (Eq. 4)
@@ -235,29 +328,41 @@ select_results_kernel(const float *__restrict__ T, const float *__restrict__ E, 
 
 int64_t grid_for(int64_t B) { return (B + kBlock - 1) / kBlock; }
 
-// Device scratch for finish-time slots that do not fit in LDS.
-hipError_t scratch(size_t bytes, hipStream_t s, float **p) {
-    *p = nullptr;
-    if (bytes == 0) return hipSuccess;
-    return hipMallocAsync(reinterpret_cast<void **>(p), bytes, s);
+size_t table_bytes(const DevGraph &g) {
+    return (static_cast<size_t>(g.P) * g.F + kTablePad) * sizeof(float2);
+}
+
+bool vec_levels(const DevGraph &g, const uint8_t *levels) {
+    return g.P % 16 == 0 && reinterpret_cast<uintptr_t>(levels) % 16 == 0;
 }
 
 }  // namespace
 
+int64_t forward_blocks(int64_t B) { return grid_for(B); }
+
 hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
                           float target, uint32_t *mask, void *part, hipStream_t s) {
-    LaunchShape sh = shape_for(g, g.eval.n_slots);
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
-    float *gs = nullptr;
-    hipError_t e = scratch(sh.slot_lds ? 0 : static_cast<size_t>(g.eval.n_slots) * bpad * 4, s, &gs);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(forward_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBlock), sh.lds_bytes, s,
-                       g, levels, B, T, E, target, mask, static_cast<EmoPartial *>(part), sh.tab_lds,
-                       sh.slot_lds, gs, bpad);
-    e = hipGetLastError();
-    if (gs) {
-        hipError_t e2 = hipFreeAsync(gs, s);
+    float *cold = nullptr;
+    if (g.eval.n_cold > 0) {
+        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&cold),
+                                      static_cast<size_t>(g.eval.n_cold) * bpad * sizeof(float), s);
+        if (e != hipSuccess) return e;
+    }
+    const size_t tb = table_bytes(g);
+    const bool tab_lds = tb <= kLdsBudget;
+    const bool vec = vec_levels(g, levels);
+    EmoPartial *pp = static_cast<EmoPartial *>(part);
+    if (tab_lds)
+        hipLaunchKernelGGL(forward_kernel<true>, dim3(static_cast<unsigned>(grid)), dim3(kBlock), tb, s,
+                           g, levels, B, T, E, target, mask, pp, cold, bpad, vec);
+    else
+        hipLaunchKernelGGL(forward_kernel<false>, dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, s,
+                           g, levels, B, T, E, target, mask, pp, cold, bpad, vec);
+    hipError_t e = hipGetLastError();
+    if (cold) {
+        hipError_t e2 = hipFreeAsync(cold, s);
         if (e == hipSuccess) e = e2;
     }
     return e;
@@ -266,24 +371,42 @@ hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, f
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
                         float target, uint32_t *mask, void *part, hipStream_t s) {
-    LaunchShape sh = shape_for(g, prog.n_slots);
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
-    float *gs = nullptr;
-    hipError_t e = scratch(sh.slot_lds ? 0 : static_cast<size_t>(prog.n_slots) * bpad * 4, s, &gs);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(slack_kernel, dim3(static_cast<unsigned>(grid)), dim3(kBlock), sh.lds_bytes, s,
-                       g, prog, out_cols, levels, B, slack, T, E, target, mask,
-                       static_cast<EmoPartial *>(part), sh.tab_lds, sh.slot_lds, gs, bpad);
-    e = hipGetLastError();
-    if (gs) {
-        hipError_t e2 = hipFreeAsync(gs, s);
+    const size_t n_cold = static_cast<size_t>(prog.n_cold), n_keep = static_cast<size_t>(prog.n_ops),
+                 n_cold_b = static_cast<size_t>(prog.n_cold_bwd);
+    float *buf = nullptr;
+    const size_t total = (n_cold + n_keep + n_cold_b) * static_cast<size_t>(bpad);
+    if (total > 0) {
+        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&buf), total * sizeof(float), s);
+        if (e != hipSuccess) return e;
+    }
+    float *cold = buf;
+    float *keep = buf ? buf + n_cold * bpad : nullptr;
+    float *cold_b = buf ? keep + n_keep * bpad : nullptr;
+    // staged output needs packs visited in increasing id and whole 32-pack segments
+    const bool staged = out_cols == g.P && prog.monotone && g.P % kStage == 0 &&
+                        reinterpret_cast<uintptr_t>(slack) % 16 == 0;
+    const size_t stage_bytes = staged ? static_cast<size_t>(kWavesPerBlock) * kStage * 65 * sizeof(float) : 0;
+    const size_t tb = table_bytes(g);
+    const bool tab_lds = tb + stage_bytes <= kLdsBudget;
+    const bool vec = vec_levels(g, levels);
+    EmoPartial *pp = static_cast<EmoPartial *>(part);
+    const dim3 gd(static_cast<unsigned>(grid)), bd(kBlock);
+    const size_t dyn = tab_lds ? tb : 0;
+#define EMO_SLACK_ARGS g, prog, out_cols, levels, B, slack, T, E, target, mask, pp, cold, keep, cold_b, bpad, vec
+    if (tab_lds && staged) hipLaunchKernelGGL((slack_kernel<true, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+    else if (tab_lds) hipLaunchKernelGGL((slack_kernel<true, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+    else if (staged) hipLaunchKernelGGL((slack_kernel<false, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+    else hipLaunchKernelGGL((slack_kernel<false, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+#undef EMO_SLACK_ARGS
+    hipError_t e = hipGetLastError();
+    if (buf) {
+        hipError_t e2 = hipFreeAsync(buf, s);
         if (e == hipSuccess) e = e2;
     }
     return e;
 }
-
-int64_t forward_blocks(int64_t B) { return grid_for(B); }
 
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s) {
     hipLaunchKernelGGL(empty_result, dim3(1), dim3(1), 0, s, res);
