@@ -41,6 +41,22 @@ typedef float f32x32 __attribute__((ext_vector_type(32)));
 typedef unsigned int u32x32 __attribute__((ext_vector_type(32)));
 
 __device__ __forceinline__ uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Program records and edge lists are never written while a kernel runs.  Reading them through
+// the constant address space lets the compiler use scalar loads: a vector load there would be
+// followed by a wait that also covers every store still in flight.
+#define EMO_CONST_AS __attribute__((address_space(4)))
+template <class T>
+__device__ __forceinline__ T ld_prog(const T *p, int64_t i) {
+    static_assert(sizeof(T) % 4 == 0, "program records are made of 32-bit words");
+    const EMO_CONST_AS uint32_t *q = (const EMO_CONST_AS uint32_t *)(p + i);
+    uint32_t w[sizeof(T) / 4];
+#pragma unroll
+    for (int k = 0; k < static_cast<int>(sizeof(T) / 4); ++k) w[k] = q[k];
+    T v;
+    __builtin_memcpy(&v, w, sizeof(T));
+    return v;
+}
 __device__ __forceinline__ int32_t uni(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // The candidate's level row, read one 128-byte line (8 x 16 bytes) at a time into a register
@@ -77,6 +93,68 @@ __device__ __forceinline__ unsigned level_at(const Row &r, u32x32 &w, int &group
     return (word >> ((p & 3) << 3)) & 0xffu;
 }
 
+// Table access.  kTabGlobal: straight from device memory; kTabLds: the whole table staged in LDS
+// at kernel start; kTabWindow: windows of 2^wlog packs' rows staged into a double-buffered LDS
+// area by the workgroup, one barrier per window, the next window prefetched into registers
+// while the current one is in use.  Windows need the program to visit packs in increasing id
+// (decreasing in the backward pass); every wave of the workgroup walks the same program, so all
+// of them reach each window change at the same step.
+enum TabMode { kTabGlobal = 0, kTabLds = 1, kTabWindow = 2 };
+constexpr int kWindowBytes = 8192;
+constexpr int kWindowEntries = kWindowBytes / 8;   // float2 entries per LDS half
+static_assert(kWindowBytes == 2 * 16 * kBlock, "two 16-byte pieces of a window per thread");
+
+template <int MODE>
+struct Tab {
+    const float2 *tab;     // global table, or the whole LDS copy (kTabLds)
+    float2 *buf;           // kTabWindow: LDS [2][window entries]
+    int F;
+    int wlog;              // packs per window = 1 << wlog
+    int went;              // table entries per window
+    int64_t n_entries;     // valid entries of the global table
+    int cur;               // window in use
+    float4 pre0, pre1;     // this thread's two pieces of the next window
+
+    // Loads window w's rows into registers.  Indices past the table are clamped to its last
+    // piece: those LDS entries belong to packs beyond the last one and are never read.
+    __device__ __forceinline__ void fetch(int w) {
+        const float4 *src = reinterpret_cast<const float4 *>(tab);
+        const int64_t last = n_entries / 2 - 1;
+        const int64_t base = static_cast<int64_t>(w < 0 ? 0 : w) * went / 2;
+        const int64_t i0 = base + threadIdx.x, i1 = i0 + kBlock;
+        pre0 = src[i0 < last ? i0 : last];
+        pre1 = src[i1 < last ? i1 : last];
+    }
+    __device__ __forceinline__ void commit(int w) {
+        float4 *dst = reinterpret_cast<float4 *>(buf + (w & 1) * kWindowEntries);
+        dst[threadIdx.x] = pre0;
+        dst[threadIdx.x + kBlock] = pre1;
+    }
+    // Makes window w current; dir is +1 in the forward pass, -1 in the backward pass.
+    __device__ __forceinline__ void enter(int w, int dir) {
+        if (w == cur + dir) {
+            commit(w);
+        } else {   // first window of a pass (or a jump): stage synchronously
+            __syncthreads();
+            fetch(w);
+            commit(w);
+        }
+        __syncthreads();
+        cur = w;
+        fetch(w + dir);
+    }
+    // The backward pass walks windows downward: refetch the one below the current window.
+    __device__ __forceinline__ void turn() {
+        if (MODE == kTabWindow) fetch(cur - 1);
+    }
+    __device__ __forceinline__ float2 get(int pack, int l, int dir) {
+        if (MODE != kTabWindow) return tab[pack * F + l];
+        const int w = pack >> wlog;
+        if (w != cur) enter(w, dir);
+        return buf[(w & 1) * kWindowEntries + (pack - (w << wlog)) * F + l];
+    }
+};
+
 struct Scratch {
     float *cold;        // [n_cold][bpad]
     float *keep;        // [n_ops][bpad] (slack) or nullptr
@@ -103,8 +181,8 @@ struct Fwd {
     bool bad;
 };
 
-template <bool TAB_LDS, bool KEEP>
-__device__ __forceinline__ Fwd run_forward(const DevProgram &pr, const float2 *tab, int F, float static_power,
+template <int MODE, bool KEEP>
+__device__ __forceinline__ Fwd run_forward(const DevProgram &pr, Tab<MODE> &tab, int F, float static_power,
                            const Row &row, f32x32 &hot, const Scratch &sc) {
     u32x32 lw;
     int lgroup = -1;
@@ -115,20 +193,20 @@ __device__ __forceinline__ Fwd run_forward(const DevProgram &pr, const float2 *t
     bool bad = false;
     const int n = pr.n_ops;
     for (int i = 0; i < n; ++i) {
-        const FwdStep st = pr.fwd[i];
+        const FwdStep st = ld_prog(pr.fwd, i);
         const uint32_t flags = uni(st.flags);
         const int32_t pack = uni(st.pack);
         const int32_t nin = uni(st.in_count);
         const int32_t ib = uni(st.in_begin);
         float est = __uint_as_float(uni(st.cst));
         for (int j = 0; j < nin; ++j)
-            est = fmaxf(est, slot_get(hot, sc.cold, sc.bpad, sc.col, uni(pr.ins[ib + j])));
+            est = fmaxf(est, slot_get(hot, sc.cold, sc.bpad, sc.col, uni(ld_prog(pr.ins, ib + j))));
         float dur;
         if (pack >= 0) {
             unsigned l = level_at(row, lw, lgroup, pack);
             bad |= l >= static_cast<unsigned>(F);
             l = l < static_cast<unsigned>(F) ? l : 0u;
-            const float2 te = tab[pack * F + static_cast<int>(l)];
+            const float2 te = tab.get(pack, static_cast<int>(l), 1);
             dur = te.x;
             eblk += te.y;
             if (++nblk == kEnergyBlock) {
@@ -183,23 +261,24 @@ __device__ __forceinline__ void flush_stage(const float *stg, float *__restrict_
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <bool STAGED>
-__device__ __forceinline__ void run_backward(const DevProgram &pr, const float2 *tab, int F, float T, bool bad,
+template <int MODE, bool STAGED>
+__device__ __forceinline__ void run_backward(const DevProgram &pr, Tab<MODE> &tab, int F, float T, bool bad,
                              const Row &row, f32x32 &hot, const Scratch &sc, float *__restrict__ S,
                              int64_t cols, int64_t cand, bool active, float *stg, int64_t wbase,
                              int64_t B) {
     u32x32 lw;
     int lgroup = -1;
+    tab.turn();
     const int n = pr.n_ops;
     const float inf = __builtin_inff();
     const float nan = __builtin_nanf("");
     const int lane = threadIdx.x % kWave;
-    float eft_next = n > 0 ? sc.keep[static_cast<int64_t>(uni(pr.bwd[0].fwd)) * sc.bpad + sc.col] : 0.f;
+    float eft_next = n > 0 ? sc.keep[static_cast<int64_t>(uni(ld_prog(pr.bwd, 0).fwd)) * sc.bpad + sc.col] : 0.f;
     for (int r = 0; r < n; ++r) {
-        const BwdStep st = pr.bwd[r];
+        const BwdStep st = ld_prog(pr.bwd, r);
         const float eft = eft_next;
         if (r + 1 < n)   // the next step's finish time is fetched one step ahead
-            eft_next = sc.keep[static_cast<int64_t>(uni(pr.bwd[r + 1].fwd)) * sc.bpad + sc.col];
+            eft_next = sc.keep[static_cast<int64_t>(uni(ld_prog(pr.bwd, r + 1).fwd)) * sc.bpad + sc.col];
         const uint32_t flags = uni(st.flags);
         const int32_t pack = uni(st.pack);
         const int32_t ns = uni(st.succ_count);
@@ -209,13 +288,13 @@ __device__ __forceinline__ void run_backward(const DevProgram &pr, const float2 
         if (ns > 0) {
             lft = inf;
             for (int j = 0; j < ns; ++j)
-                lft = fminf(lft, slot_get(hot, sc.cold_bwd, sc.bpad, sc.col, uni(pr.succs[sb + j])));
+                lft = fminf(lft, slot_get(hot, sc.cold_bwd, sc.bpad, sc.col, uni(ld_prog(pr.succs, sb + j))));
         }
         float dur;
         if (pack >= 0) {
             unsigned l = level_at(row, lw, lgroup, pack);
             l = l < static_cast<unsigned>(F) ? l : 0u;
-            dur = tab[pack * F + static_cast<int>(l)].x;
+            dur = tab.get(pack, static_cast<int>(l), -1).x;
         } else {
             dur = __uint_as_float(uni(st.dur));
         }
@@ -232,12 +311,26 @@ __device__ __forceinline__ void run_backward(const DevProgram &pr, const float2 
     }
 }
 
-// Stage the (time, energy) table into LDS when it fits.
-__device__ const float2 *stage_table(const DevGraph &g, float2 *smem) {
-    const int n = g.P * g.F + kTablePad;
-    for (int i = threadIdx.x; i < n; i += blockDim.x) smem[i] = g.tab[i];
-    __syncthreads();
-    return smem;
+// Sets up table access for a kernel (stages the whole table when MODE == kTabLds).
+template <int MODE>
+__device__ __forceinline__ Tab<MODE> make_tab(const DevGraph &g, float4 *smem, int wlog) {
+    Tab<MODE> t;
+    t.F = g.F;
+    t.wlog = wlog;
+    t.went = (1 << wlog) * g.F;
+    t.n_entries = static_cast<int64_t>(g.P) * g.F + kTablePad;
+    t.cur = -2;
+    t.buf = nullptr;
+    t.tab = g.tab;
+    if (MODE == kTabLds) {
+        float2 *lds = reinterpret_cast<float2 *>(smem);
+        for (int64_t i = threadIdx.x; i < t.n_entries; i += blockDim.x) lds[i] = g.tab[i];
+        __syncthreads();
+        t.tab = lds;
+    } else if (MODE == kTabWindow) {
+        t.buf = reinterpret_cast<float2 *>(smem);
+    }
+    return t;
 }
 
 struct LaneCtx {
@@ -255,18 +348,18 @@ __device__ __forceinline__ LaneCtx lane_ctx(int64_t B) {
 }
 
 // Forward pass; makespan/energy outputs, the mask and the selection partials are each optional.
-template <bool TAB_LDS>
+template <int MODE>
 __global__ void __launch_bounds__(kBlock)
 forward_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ T_out,
                float *__restrict__ E_out, float target, uint32_t *__restrict__ mask,
-               EmoPartial *part, float *cold, int64_t bpad, bool vec) {
+               EmoPartial *part, float *cold, int64_t bpad, bool vec, int wlog) {
     extern __shared__ float4 smem4[];
-    const float2 *tab = TAB_LDS ? stage_table(g, reinterpret_cast<float2 *>(smem4)) : g.tab;
+    Tab<MODE> tab = make_tab<MODE>(g, smem4, wlog);
     const LaneCtx x = lane_ctx(B);
     const Row row{levels + x.cand * g.P, g.P, vec};
     f32x32 hot;
     Scratch sc{cold, nullptr, nullptr, bpad, x.gid};
-    const Fwd f = run_forward<TAB_LDS, false>(g.eval, tab, g.F, g.static_power, row, hot, sc);
+    const Fwd f = run_forward<MODE, false>(g.eval, tab, g.F, g.static_power, row, hot, sc);
     if (x.active) {
         if (T_out) T_out[x.cand] = f.T;
         if (E_out) E_out[x.cand] = f.E;
@@ -275,27 +368,27 @@ forward_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float 
 }
 
 // Forward + backward (slack) pass with the same optional outputs.
-template <bool TAB_LDS, bool STAGED>
+template <int MODE, bool STAGED>
 __global__ void __launch_bounds__(kBlock)
 slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict__ levels, int64_t B,
              float *__restrict__ S, float *__restrict__ T_out, float *__restrict__ E_out,
              float target, uint32_t *__restrict__ mask, EmoPartial *part, float *cold, float *keep,
-             float *cold_bwd, int64_t bpad, bool vec) {
+             float *cold_bwd, int64_t bpad, bool vec, int wlog) {
     extern __shared__ float4 smem4[];
-    const float2 *tab = TAB_LDS ? stage_table(g, reinterpret_cast<float2 *>(smem4)) : g.tab;
+    Tab<MODE> tab = make_tab<MODE>(g, smem4, wlog);
     __shared__ float stg_all[STAGED ? kWavesPerBlock : 1][STAGED ? kStage * 65 : 1];
     const LaneCtx x = lane_ctx(B);
     const Row row{levels + x.cand * g.P, g.P, vec};
     f32x32 hot;
     Scratch sc{cold, keep, cold_bwd, bpad, x.gid};
-    const Fwd f = run_forward<TAB_LDS, true>(pr, tab, g.F, g.static_power, row, hot, sc);
+    const Fwd f = run_forward<MODE, true>(pr, tab, g.F, g.static_power, row, hot, sc);
     if (x.active) {
         if (T_out) T_out[x.cand] = f.T;
         if (E_out) E_out[x.cand] = f.E;
     }
     float *stg = STAGED ? stg_all[threadIdx.x / kWave] : nullptr;
-    run_backward<STAGED>(pr, tab, g.F, f.bad ? 0.f : f.T, f.bad, row, hot, sc, S, cols, x.cand,
-                         x.active, stg, x.wbase, B);
+    run_backward<MODE, STAGED>(pr, tab, g.F, f.bad ? 0.f : f.T, f.bad, row, hot, sc, S, cols, x.cand,
+                               x.active, stg, x.wbase, B);
     if (mask || part) emo_select_block(x.active, f.T, f.E, x.cand, B, target, mask, part);
 }
 
@@ -336,6 +429,30 @@ bool vec_levels(const DevGraph &g, const uint8_t *levels) {
     return g.P % 16 == 0 && reinterpret_cast<uintptr_t>(levels) % 16 == 0;
 }
 
+// Packs per table window (a power of two) so that one window of rows fills kWindowBytes.
+int window_log(const DevGraph &g) {
+    int wlog = 0;
+    while ((static_cast<size_t>(2) << wlog) * g.F * sizeof(float2) <= static_cast<size_t>(kWindowBytes)) ++wlog;
+    return wlog;
+}
+
+// Table mode for a launch with `other_lds` bytes of LDS already in use.
+int table_mode(const DevGraph &g, const DevProgram &prog, size_t other_lds, size_t *dyn) {
+    const size_t tb = table_bytes(g);
+    if (tb + other_lds <= kLdsBudget) {
+        *dyn = tb;
+        return kTabLds;
+    }
+    const size_t wb = 2 * static_cast<size_t>(kWindowBytes);
+    // a window holds at least two packs' rows (so its start is 16-byte aligned)
+    if (prog.monotone && window_log(g) >= 1 && wb + other_lds <= kLdsBudget) {
+        *dyn = wb;
+        return kTabWindow;
+    }
+    *dyn = 0;
+    return kTabGlobal;
+}
+
 }  // namespace
 
 int64_t forward_blocks(int64_t B) { return grid_for(B); }
@@ -350,16 +467,17 @@ hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, f
                                       static_cast<size_t>(g.eval.n_cold) * bpad * sizeof(float), s);
         if (e != hipSuccess) return e;
     }
-    const size_t tb = table_bytes(g);
-    const bool tab_lds = tb <= kLdsBudget;
+    size_t dyn = 0;
+    const int mode = table_mode(g, g.eval, 0, &dyn);
     const bool vec = vec_levels(g, levels);
+    const int wlog = window_log(g);
     EmoPartial *pp = static_cast<EmoPartial *>(part);
-    if (tab_lds)
-        hipLaunchKernelGGL(forward_kernel<true>, dim3(static_cast<unsigned>(grid)), dim3(kBlock), tb, s,
-                           g, levels, B, T, E, target, mask, pp, cold, bpad, vec);
-    else
-        hipLaunchKernelGGL(forward_kernel<false>, dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, s,
-                           g, levels, B, T, E, target, mask, pp, cold, bpad, vec);
+    const dim3 gd(static_cast<unsigned>(grid)), bd(kBlock);
+#define EMO_FWD_ARGS g, levels, B, T, E, target, mask, pp, cold, bpad, vec, wlog
+    if (mode == kTabLds) hipLaunchKernelGGL(forward_kernel<kTabLds>, gd, bd, dyn, s, EMO_FWD_ARGS);
+    else if (mode == kTabWindow) hipLaunchKernelGGL(forward_kernel<kTabWindow>, gd, bd, dyn, s, EMO_FWD_ARGS);
+    else hipLaunchKernelGGL(forward_kernel<kTabGlobal>, gd, bd, dyn, s, EMO_FWD_ARGS);
+#undef EMO_FWD_ARGS
     hipError_t e = hipGetLastError();
     if (cold) {
         hipError_t e2 = hipFreeAsync(cold, s);
@@ -388,17 +506,19 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
     const bool staged = out_cols == g.P && prog.monotone && g.P % kStage == 0 &&
                         reinterpret_cast<uintptr_t>(slack) % 16 == 0;
     const size_t stage_bytes = staged ? static_cast<size_t>(kWavesPerBlock) * kStage * 65 * sizeof(float) : 0;
-    const size_t tb = table_bytes(g);
-    const bool tab_lds = tb + stage_bytes <= kLdsBudget;
+    size_t dyn = 0;
+    const int mode = table_mode(g, prog, stage_bytes, &dyn);
     const bool vec = vec_levels(g, levels);
+    const int wlog = window_log(g);
     EmoPartial *pp = static_cast<EmoPartial *>(part);
     const dim3 gd(static_cast<unsigned>(grid)), bd(kBlock);
-    const size_t dyn = tab_lds ? tb : 0;
-#define EMO_SLACK_ARGS g, prog, out_cols, levels, B, slack, T, E, target, mask, pp, cold, keep, cold_b, bpad, vec
-    if (tab_lds && staged) hipLaunchKernelGGL((slack_kernel<true, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
-    else if (tab_lds) hipLaunchKernelGGL((slack_kernel<true, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
-    else if (staged) hipLaunchKernelGGL((slack_kernel<false, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
-    else hipLaunchKernelGGL((slack_kernel<false, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+#define EMO_SLACK_ARGS g, prog, out_cols, levels, B, slack, T, E, target, mask, pp, cold, keep, cold_b, bpad, vec, wlog
+    if (mode == kTabLds && staged) hipLaunchKernelGGL((slack_kernel<kTabLds, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+    else if (mode == kTabLds) hipLaunchKernelGGL((slack_kernel<kTabLds, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+    else if (mode == kTabWindow && staged) hipLaunchKernelGGL((slack_kernel<kTabWindow, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+    else if (mode == kTabWindow) hipLaunchKernelGGL((slack_kernel<kTabWindow, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+    else if (staged) hipLaunchKernelGGL((slack_kernel<kTabGlobal, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
+    else hipLaunchKernelGGL((slack_kernel<kTabGlobal, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
 #undef EMO_SLACK_ARGS
     hipError_t e = hipGetLastError();
     if (buf) {

@@ -136,6 +136,21 @@ def test_random_dags_off_grid(torch, emo, seed):
                     what=f"offgrid seed={seed} i={i}", mode=mode)
 
 
+@pytest.mark.parametrize("F,P", [(16, 700), (200, 64), (5, 1800), (256, 40)])
+def test_interpreter_table_windows(torch, emo, F, P):
+    """Tables too large for LDS with packs in increasing topological order: the interpreting
+    kernels stage windows of table rows (and stream the rest when windows cannot apply)."""
+    rng = np.random.default_rng(F * 1000 + P)
+    V = int(P * 1.5)
+    g = synth.random_dag(rng, V, 2.5 / V, P / V, F, shuffle_ids=False, shuffle_packs=False)
+    assert g.num_packs * F * 8 > 60 * 1024 or F == 256
+    rows = pins.random_rows(rng, g, 700)
+    gh = emo.EmoGraph(g, device=0, kernel_mode=1)
+    assert gh.info()["pack_order_monotone"] == 1
+    T_or, _ = oracle.eval_batch(g, rows)
+    run_all(torch, emo, g, rows, [float(np.median(T_or))], what=f"windows F={F} P={P}", mode=1)
+
+
 def test_large_slot_count_uses_device_scratch(torch, emo):
     """A wide antichain of packs feeding one sink keeps many finish times live at once."""
     rng = np.random.default_rng(5)
