@@ -88,6 +88,9 @@ typedef struct {
                                      bit 1: a specialised slack kernel is compiled,
                                      bit 2: specialisation was tried and failed */
     float compile_seconds;        /* time spent compiling specialised kernels */
+    int32_t num_implied_edges;    /* merged edges u -> v that the kernels skip because another
+                                     path leads from u to v (they never decide a maximum or a
+                                     minimum; results are unchanged) */
 } emo_graph_info;
 
 /* Which kernels evaluate a graph.

@@ -170,6 +170,82 @@ emo_status topo_sort(emo_graph_s &g) {
     return EMO_OK;
 }
 
+// Drops edges implied by longer paths: u -> v goes when another path leads from u to v (found
+// by a search over the merged graph that only visits nodes placed before the last other
+// predecessor of v, within a visit budget; an edge not proven implied stays).  Durations are
+// >= 0 and rounding is monotone, so finish times do not decrease along a path and latest start
+// times do not increase against it, also in fp32: such an edge never decides the maximum of
+// Eq. 1 nor the minimum of the backward pass, and every EFT, LFT and slack is unchanged, bit
+// for bit.  Fewer edges mean fewer operations and shorter live ranges in the kernels.  The
+// removable edges are decided on the merged graph, so reachability is preserved (the result
+// lies between the graph and its transitive reduction).  Returns the number of dropped edges.
+int32_t prune_implied_edges(emo_graph_s &g) {
+    const int32_t V = g.V;
+    std::vector<int32_t> pos(V);
+    for (int32_t i = 0; i < V; ++i) pos[g.order[i]] = i;
+    std::vector<int32_t> stamp(V, -1), target(V, -1), stack;
+    std::vector<char> drop(g.src.size(), 0);
+    // merged edge behind predecessor slot j (build_csr fills the slots in edge order)
+    std::vector<int32_t> edge_of(g.pred.size());
+    {
+        std::vector<int32_t> fill(g.pred_off.begin(), g.pred_off.end() - 1);
+        for (size_t e = 0; e < g.src.size(); ++e) edge_of[fill[g.dst[e]]++] = static_cast<int32_t>(e);
+    }
+    int64_t budget = 64 * (static_cast<int64_t>(V) + static_cast<int64_t>(g.src.size())) + 65536;
+    constexpr int32_t kQueryVisits = 4096;
+    int32_t query = 0, dropped = 0;
+    std::vector<int32_t> preds;
+    for (int32_t v = 0; v < V && budget > 0; ++v) {
+        const int32_t b = g.pred_off[v], e = g.pred_off[v + 1];
+        if (e - b < 2) continue;
+        int32_t top = -1, second = -1;   // the two largest predecessor positions
+        for (int32_t j = b; j < e; ++j) {
+            const int32_t p = pos[g.pred[j]];
+            target[g.pred[j]] = v;
+            if (p > top) { second = top; top = p; }
+            else if (p > second) second = p;
+        }
+        for (int32_t j = b; j < e && budget > 0; ++j) {
+            const int32_t u = g.pred[j];
+            const int32_t lim = pos[u] == top ? second : top;
+            if (lim <= pos[u]) continue;   // no other predecessor comes after u
+            ++query;
+            bool found = false;
+            int32_t visits = 0;
+            stack.assign(1, u);
+            stamp[u] = query;
+            while (!stack.empty() && !found && visits < kQueryVisits) {
+                const int32_t x = stack.back();
+                stack.pop_back();
+                ++visits;
+                for (int32_t k = g.succ_off[x]; k < g.succ_off[x + 1]; ++k) {
+                    const int32_t y = g.succ[k];
+                    if (pos[y] > lim || stamp[y] == query) continue;
+                    // y is another predecessor of v: u reaches v by a path of two or more edges
+                    if (target[y] == v) { found = true; break; }
+                    stamp[y] = query;
+                    stack.push_back(y);
+                }
+            }
+            budget -= visits;
+            if (found) {
+                drop[edge_of[j]] = 1;
+                ++dropped;
+            }
+        }
+    }
+    if (dropped == 0) return 0;
+    std::vector<int32_t> src, dst;
+    for (size_t i = 0; i < g.src.size(); ++i)
+        if (!drop[i]) {
+            src.push_back(g.src[i]);
+            dst.push_back(g.dst[i]);
+        }
+    build_csr(V, src, dst, g.pred_off, g.pred);
+    build_csr(V, dst, src, g.succ_off, g.succ);
+    return dropped;
+}
+
 // Marks candidate-dependent nodes and computes the fp32 finish times of the others.
 void fold_constants(emo_graph_s &g) {
     const int32_t V = g.V;
@@ -572,6 +648,7 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     build_csr(V, g->dst, g->src, g->succ_off, g->succ);
     emo_status s = topo_sort(*g);
     if (s != EMO_OK) return s;
+    const int32_t implied = prune_implied_edges(*g);
     fold_constants(*g);
 
     const Schedule sf = make_schedule(*g, true);
@@ -582,6 +659,7 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
 
     emo_graph_info &in = g->info;
     in.num_nodes = V; in.num_edges = g->E; in.num_packs = P; in.num_levels = F;
+    in.num_implied_edges = implied;
     in.num_dynamic_nodes = static_cast<int32_t>(pe.fwd.size());
     in.num_dynamic_edges = static_cast<int32_t>(pe.ins.size());
     in.eval_slots = pe.n_hot + pe.n_cold;

@@ -41,7 +41,8 @@ class GraphInfo(ctypes.Structure):
                 ("eval_slots", ctypes.c_int32), ("max_depth", ctypes.c_int32),
                 ("const_makespan", ctypes.c_float), ("device", ctypes.c_int32),
                 ("pack_order_monotone", ctypes.c_int32), ("kernel_mode", ctypes.c_int32),
-                ("specialized", ctypes.c_int32), ("compile_seconds", ctypes.c_float)]
+                ("specialized", ctypes.c_int32), ("compile_seconds", ctypes.c_float),
+                ("num_implied_edges", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

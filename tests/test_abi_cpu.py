@@ -116,6 +116,52 @@ def test_duplicate_edges_are_merged(emo):
     assert _load(emo, g2).info()["num_edges"] == g.num_edges
 
 
+def _implied_edges(g) -> int:
+    """Full transitive closure (Python integers as bit sets, filled in reverse topological
+    order): counts merged edges u -> v such that another successor w of u reaches v."""
+    V = g.num_nodes
+    edges = sorted(set(zip(g.edge_src.tolist(), g.edge_dst.tolist())))
+    succ = [[] for _ in range(V)]
+    indeg = [0] * V
+    for u, v in edges:
+        succ[u].append(v)
+        indeg[v] += 1
+    order = [v for v in range(V) if indeg[v] == 0]
+    for v in order:
+        for w in succ[v]:
+            indeg[w] -= 1
+            if indeg[w] == 0:
+                order.append(w)
+    reach = [0] * V          # nodes reachable by one or more edges
+    for u in reversed(order):
+        r = 0
+        for w in succ[u]:
+            r |= (1 << w) | reach[w]
+        reach[u] = r
+    return sum(1 for u, v in edges if any(w != v and (reach[w] >> v) & 1 for w in succ[u]))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_implied_edges_match_brute_force(emo, seed):
+    """The loader skips exactly the edges implied by longer paths (transitive reduction) on
+    graphs small enough for its search budget."""
+    rng = np.random.default_rng(700 + seed)
+    total = 0
+    for i in range(12):
+        V = int(rng.integers(2, 70))
+        g = synth.random_dag(rng, V, float(rng.uniform(0.03, 0.4)), 0.6, 3)
+        want = _implied_edges(g)
+        assert _load(emo, g).info()["num_implied_edges"] == want
+        total += want
+    assert total > 0
+
+
+def test_implied_edges_on_workloads(emo):
+    """Cross-stream edges that span an all-stream synchronisation node are implied."""
+    g = synth.config_graph(4)
+    assert _load(emo, g).info()["num_implied_edges"] == _implied_edges(g)
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_topo_order_matches_oracle_on_random_dags(emo, oracle_lib, seed):
     rng = np.random.default_rng(100 + seed)
