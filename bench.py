@@ -191,8 +191,12 @@ def main():
     algo_bytes = B * (P + 8 + (4 * P if spec.slack else 0)) + (B + 7) // 8
     achieved = algo_bytes / (main_ms / 1e3) / 1e9
     src_hash = kernel_source_hash()
-    kname = ("emo_sp_slack" if spec.slack else "emo_sp_select") if info["specialized"] & 1 else \
-        ("slack_kernel" if spec.slack else "forward_kernel")
+    if info["last_kernels"] == 2:      # segmented kernels: the timed unit is the whole chain
+        kname = "emo_chain"
+    elif info["last_kernels"] == 1:
+        kname = "emo_sp_slack" if spec.slack else "emo_sp_select"
+    else:
+        kname = "slack_kernel" if spec.slack else "forward_kernel"
     traffic = measured_traffic(spec.name, kname, src_hash)
     out = {
         "metric": METRIC,

@@ -85,9 +85,12 @@ typedef struct {
     int32_t pack_order_monotone;  /* 1 if the kernels visit packs in increasing pack id */
     int32_t kernel_mode;          /* emo_kernel_mode in effect */
     int32_t specialized;          /* bit 0: specialised eval/select kernels are compiled,
-                                     bit 1: a specialised slack kernel is compiled,
-                                     bit 2: specialisation was tried and failed */
+                                     bit 1: specialised slack kernels are compiled,
+                                     bit 2: specialisation was tried and failed,
+                                     bit 3: segmented kernels are compiled */
     float compile_seconds;        /* time spent compiling specialised kernels */
+    int32_t last_kernels;         /* kernels of the last batch call: 0 interpreted, 1 one
+                                     specialised kernel, 2 segmented specialised kernels */
     int32_t num_implied_edges;    /* merged edges u -> v that the kernels skip because another
                                      path leads from u to v (they never decide a maximum or a
                                      minimum; results are unchanged) */
@@ -213,8 +216,16 @@ emo_status emo_graph_set_timing_events(emo_graph_t g, void *begin_event, void *e
 /* Diagnostics: the HIP source of the kernels specialised to `g` (the text EMO_KERNELS_AUTO
  * compiles on first use), NUL-terminated.  With buf == NULL, *len receives the size needed
  * including the NUL; otherwise at most *len bytes are written.  Works on host-only graphs.
- * EMO_ERR_UNSUPPORTED when the graph is too large to specialise. */
+ * EMO_ERR_UNSUPPORTED when the graph is too large for one specialised kernel. */
 emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len);
+
+/* Diagnostics: the HIP source of the segmented specialised kernels of `g`, used for graphs too
+ * large for one kernel (eval/select) or to keep every finish time in registers (slack): one
+ * forward kernel per segment of consecutive steps, launched in order, then one backward kernel
+ * per segment in reverse order, which recomputes finish times from checkpointed values instead
+ * of reading stored ones.  Same buffer convention as emo_graph_specialized_source.
+ * EMO_ERR_UNSUPPORTED when the graph uses no segmented kernels. */
+emo_status emo_graph_segmented_source(emo_graph_t g, char *buf, int64_t *len);
 
 /* Static string naming a status code. */
 const char *emo_status_string(emo_status s);

@@ -72,8 +72,17 @@ struct HostProgram {
 // A value read again within this many steps is kept in the register bank when a slot is free.
 constexpr int32_t kHotSpan = 96;
 
-constexpr int32_t kJitMaxOps = 2048;      // larger graphs compile too slowly to specialise
+constexpr int32_t kJitMaxOps = 2048;      // larger graphs compile too slowly as one kernel
 constexpr int32_t kJitMaxSlackOps = 160;  // every finish time stays in a VGPR
+// Segmented kernels (larger graphs): steps per segment kernel and per recompute sub-segment,
+// and the largest graph compiled this way (compile time grows with the step count).
+constexpr int32_t kChainSegOps = 256;
+constexpr int32_t kChainSubOps = 64;
+constexpr int32_t kChainMaxOps = 8192;
+// ... and only for graphs of small cut width: the finish times live at once in the forward pass
+// are held in registers (wider graphs keep the interpreting kernels, which spill cold values to
+// device scratch by design).
+constexpr int32_t kChainMaxLive = 48;
 constexpr size_t kJitTableLds = 64 * 1024;
 constexpr size_t kJitTableLdsSlack = 40 * 1024;
 
@@ -119,6 +128,13 @@ struct emo_graph_s {
     int jit_state = 0;                       // 0 not tried, 1 compiled, -1 failed
     emo::JitModule jm;
     std::string jit_log;
+    // segmented kernels: forward kernels for eval/select when the graph is too large for one
+    // kernel, backward kernels for slack when it is too large to keep every finish time
+    bool chain_eval = false;
+    bool chain_slack = false;
+    int chain_state = 0;                     // 0 not tried, 1 compiled, -1 failed
+    emo::JitModule jc;
+    hipMemPool_t pool = nullptr;             // per-call scratch (kept between calls)
     // profiling hook (hipEvent_t handles owned by the caller)
     hipEvent_t ev_begin = nullptr;
     hipEvent_t ev_end = nullptr;
@@ -457,7 +473,10 @@ void release_device(emo_graph_s *g) {
     if (g->device >= 0) {
         DeviceGuard guard(g->device);
         emo::jit_unload(&g->jm);
+        emo::jit_unload(&g->jc);
         for (void *p : g->allocations) (void)hipFree(p);
+        if (g->pool) (void)hipMemPoolDestroy(g->pool);
+        g->pool = nullptr;
     }
     g->allocations.clear();
 }
@@ -520,25 +539,70 @@ int ensure_jit(emo_graph_s *g) {
     m.block = block;
     g->jm = m;
     g->jit_state = 1;
-    g->info.specialized = 1 | (m.slack ? 2 : 0);
-    g->info.compile_seconds = static_cast<float>(m.compile_seconds);
+    g->info.specialized |= 1 | (m.slack ? 2 : 0);
+    g->info.compile_seconds += static_cast<float>(m.compile_seconds);
+    return 1;
+}
+
+emo::ChainPlan chain_plan(const emo_graph_s &g) {
+    emo::ChainPlan cp = emo::jit_chain_plan(g.jg, g.chain_slack, kChainSegOps, kChainSubOps);
+    cp.block = 256;
+    return cp;
+}
+
+// Generates and compiles the segmented kernels once; returns 1 when they are ready.
+int ensure_chain(emo_graph_s *g) {
+    std::lock_guard<std::mutex> lock(g->jit_mu);
+    if (g->chain_state != 0) return g->chain_state;
+    const emo::ChainPlan cp = chain_plan(*g);
+    const std::string src = emo::jit_generate_chain(g->jg, cp);
+    DeviceGuard guard(g->device);
+    emo::JitModule m;
+    std::string log;
+    if (emo::jit_compile_chain(src, cp, &m, &log) != 0) {
+        g->jit_log = log;
+        g->chain_state = -1;
+        g->info.specialized |= 4;
+        return -1;
+    }
+    g->jc = m;
+    g->chain_state = 1;
+    g->info.specialized |= 8 | (g->chain_eval ? 1 : 0) | (g->chain_slack ? 2 : 0);
+    g->info.compile_seconds += static_cast<float>(m.compile_seconds);
     return 1;
 }
 
 bool aligned(const void *p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
 
-// Whether a batch call uses the specialised kernels; may compile them.
-// Returns EMO_OK and sets *use, or an error in EMO_KERNELS_SPECIALIZED mode.
-emo_status want_jit(emo_graph_s *g, const uint8_t *levels, bool *use) {
-    *use = false;
-    if (g->kernel_mode == EMO_KERNELS_INTERPRETED || !g->jit_eligible) return EMO_OK;
-    if (!aligned(levels, static_cast<size_t>(emo::jit_level_width(g->P)))) return EMO_OK;
-    if (ensure_jit(g) != 1) {
+// Which kernels a batch call uses.
+enum class Path { kInterpreted = 0, kSingle = 1, kChain = 2 };
+
+// Chooses the kernels of a batch call, compiling specialised kernels on first use.  Returns
+// EMO_OK and sets *path, or an error in EMO_KERNELS_SPECIALIZED mode.
+emo_status choose_path(emo_graph_s *g, const uint8_t *levels, const float *slack, bool per_node,
+                       Path *path) {
+    *path = Path::kInterpreted;
+    if (g->kernel_mode == EMO_KERNELS_INTERPRETED) return EMO_OK;
+    if (slack && per_node) return EMO_OK;   // per-node slack: interpreted kernels only
+    if (!aligned(levels, static_cast<size_t>(emo::jit_level_width(g->jg)))) return EMO_OK;
+    bool single = false, chain = false;
+    if (slack) {
+        single = g->jit_slack_eligible;
+        chain = !single && g->chain_slack;
+    } else {
+        single = g->jit_eligible;
+        chain = !single && g->chain_eval;
+    }
+    if (!single && !chain) return EMO_OK;
+    const int st = single ? ensure_jit(g) : ensure_chain(g);
+    if (st != 1) {
         if (g->kernel_mode == EMO_KERNELS_SPECIALIZED)
             return fail(EMO_ERR_DEVICE, "specialised kernels failed to compile: %.400s", g->jit_log.c_str());
         return EMO_OK;
     }
-    *use = true;
+    if (single && slack && (!g->jm.slack || (g->jit_slack_staged && !aligned(slack, 16)))) return EMO_OK;
+    if (chain && slack && g->jc.plan.staged && !aligned(slack, 16)) return EMO_OK;
+    *path = single ? Path::kSingle : Path::kChain;
     return EMO_OK;
 }
 
@@ -672,12 +736,24 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     g->jit_eligible = nops >= 1 && nops <= kJitMaxOps;
     g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;
     g->jit_slack_staged = sf.monotone && P % 16 == 0;
+    const bool narrow = pe.n_hot + pe.n_cold <= kChainMaxLive;
+    g->chain_eval = narrow && nops > kJitMaxOps && nops <= kChainMaxOps;
+    g->chain_slack = narrow && nops > kJitMaxSlackOps && nops <= kChainMaxOps;
 
     if (device >= 0) {
         DeviceGuard guard(device);
         std::vector<float2> tab(static_cast<size_t>(P) * F + emo::kTablePad, make_float2(0.f, 0.f));
         for (size_t i = 0; i < static_cast<size_t>(P) * F; ++i)
             tab[i] = make_float2(pack_time[i], pack_energy[i]);
+        hipMemPoolProps props{};
+        props.allocType = hipMemAllocationTypePinned;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = device;
+        hipError_t perr = hipMemPoolCreate(&g->pool, &props);
+        if (perr != hipSuccess) return device_fail(perr, "hipMemPoolCreate");
+        uint64_t keep = UINT64_MAX;   // keep freed scratch for the next call
+        perr = hipMemPoolSetAttribute(g->pool, hipMemPoolAttrReleaseThreshold, &keep);
+        if (perr != hipSuccess) return device_fail(perr, "hipMemPoolSetAttribute");
         g->dg.V = V; g->dg.P = P; g->dg.F = F; g->dg.static_power = static_power;
         if ((s = upload(*g, tab, &g->dg.tab)) != EMO_OK) return s;
         if ((s = upload_program(*g, pe, g->dg.eval)) != EMO_OK) return s;
@@ -719,9 +795,26 @@ emo_status emo_graph_set_timing_events(emo_graph_t g, void *begin_event, void *e
 
 emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len) {
     if (!g || !len) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
-    if (!g->jit_eligible) return fail(EMO_ERR_UNSUPPORTED, "graph too large to specialise");
+    if (!g->jit_eligible) return fail(EMO_ERR_UNSUPPORTED, "graph too large for one specialised kernel");
     int block = 256;
     std::string src = jit_source(*g, &block);
+    const int64_t need = static_cast<int64_t>(src.size()) + 1;
+    if (!buf) {
+        *len = need;
+        return ok();
+    }
+    if (*len < need) return fail(EMO_ERR_INVALID_ARGUMENT, "buffer of %lld bytes, %lld needed",
+                                 (long long)*len, (long long)need);
+    std::memcpy(buf, src.c_str(), static_cast<size_t>(need));
+    *len = need;
+    return ok();
+}
+
+emo_status emo_graph_segmented_source(emo_graph_t g, char *buf, int64_t *len) {
+    if (!g || !len) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
+    if (!g->chain_eval && !g->chain_slack)
+        return fail(EMO_ERR_UNSUPPORTED, "the graph uses no segmented kernels");
+    const std::string src = emo::jit_generate_chain(g->jg, chain_plan(*g));
     const int64_t need = static_cast<int64_t>(src.size()) + 1;
     if (!buf) {
         *len = need;
@@ -765,43 +858,51 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     }
     if (!makespan && !energy && !slack && !mask && !result) return ok();
     if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
-    bool jit = false;
-    if (!slack || (!per_node && g->jit_slack_eligible)) {
-        if ((s = want_jit(g, levels, &jit)) != EMO_OK) return s;
-        if (slack) jit = jit && g->jm.slack && (!g->jit_slack_staged || aligned(slack, 16));
-    }
+    Path path = Path::kInterpreted;
+    if ((s = choose_path(g, levels, slack, per_node != 0, &path)) != EMO_OK) return s;
     DeviceGuard guard(g->device);
     // one selection partial record per block of the evaluating kernel
-    const int64_t nblocks = jit ? emo::jit_blocks(g->jm, B) : emo::forward_blocks(B);
-    void *part = nullptr;
-    if (result) {
-        hipError_t ea = hipMallocAsync(&part, static_cast<size_t>(nblocks) * emo::kPartialBytes, st);
-        if (ea != hipSuccess) return fail(EMO_ERR_OUT_OF_MEMORY, "hipMallocAsync: %s", hipGetErrorString(ea));
+    const int64_t nblocks = path == Path::kSingle  ? emo::jit_blocks(g->jm, B)
+                            : path == Path::kChain ? emo::jit_chain_blocks(g->jc, B)
+                                                   : emo::forward_blocks(B);
+    size_t part_bytes = result ? static_cast<size_t>(nblocks) * emo::kPartialBytes : 0;
+    part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
+    size_t scratch_bytes = part_bytes;
+    if (path == Path::kChain)
+        scratch_bytes += emo::chain_scratch_bytes(g->jc.plan, nblocks * g->jc.plan.block);
+    void *scratch = nullptr;
+    if (scratch_bytes) {
+        hipError_t ea = hipMallocFromPoolAsync(&scratch, scratch_bytes, g->pool, st);
+        if (ea != hipSuccess) return fail(EMO_ERR_OUT_OF_MEMORY, "scratch of %zu bytes: %s", scratch_bytes, hipGetErrorString(ea));
     }
+    void *part = result ? scratch : nullptr;
+    void *chain_scratch = static_cast<char *>(scratch) + part_bytes;
+    g->info.last_kernels = static_cast<int32_t>(path);
     hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
-    if (e != hipSuccess) {
-        if (part) (void)hipFreeAsync(part, st);
-        return after_launch(e, "hipEventRecord");
-    }
-    if (slack) {
-        if (jit) {
-            e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy, target,
-                                      mask, part, st);
+    if (e == hipSuccess) {
+        if (path == Path::kChain) {
+            e = emo::jit_launch_chain(g->jc, levels, B, g->dg.tab, chain_scratch, slack, makespan,
+                                      energy, target, mask, part, st);
+        } else if (slack) {
+            if (path == Path::kSingle) {
+                e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy,
+                                          target, mask, part, st);
+            } else {
+                const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
+                e = emo::launch_slack(g->dg, prog, per_node ? g->V : g->P, levels, B, slack,
+                                      makespan, energy, target, mask, part, st);
+            }
+        } else if (path == Path::kSingle) {
+            e = emo::jit_launch_forward(g->jm, levels, B, g->dg.tab, makespan, energy, target,
+                                        mask, part, st);
         } else {
-            const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
-            e = emo::launch_slack(g->dg, prog, per_node ? g->V : g->P, levels, B, slack, makespan,
-                                  energy, target, mask, part, st);
+            e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, part, st);
         }
-    } else if (jit) {
-        e = emo::jit_launch_forward(g->jm, levels, B, g->dg.tab, makespan, energy, target, mask,
-                                    part, st);
-    } else {
-        e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, part, st);
     }
     if (e == hipSuccess && g->ev_end) e = hipEventRecord(g->ev_end, st);
-    if (result) {
-        if (e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
-        hipError_t ef = hipFreeAsync(part, st);
+    if (result && e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
+    if (scratch) {
+        hipError_t ef = hipFreeAsync(scratch, st);
         if (e == hipSuccess) e = ef;
     }
     return after_launch(e, "evaluation");

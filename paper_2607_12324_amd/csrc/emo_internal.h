@@ -107,18 +107,65 @@ struct JitGraph {
     std::vector<JitOp> ops;
 };
 
+// Level words are read a line at a time only when packs are visited in increasing id; in any
+// other order a word would stay live from its first to its last use (register pressure), so each
+// level byte is then loaded on its own.
+inline int jit_level_width(const JitGraph &g) {
+    if (!g.pack_monotone) return 1;
+    return g.P % 16 == 0 ? 16 : (g.P % 4 == 0 ? 4 : 1);
+}
+
+// Segmented specialised kernels, for graphs too large for one straight-line kernel: the steps
+// are cut into segments, each with a forward kernel and (for slack) a backward kernel; the
+// forward kernels run in order, then the backward kernels in reverse order, on one stream.
+// Values crossing a kernel boundary go through device scratch rows [row][bp] (bp = the padded
+// grid size).  A backward kernel does not read stored finish times: it recomputes them one
+// sub-segment at a time from the checkpointed inputs of that sub-segment.
+struct ChainPlan {
+    std::vector<int32_t> seg;       // segment boundaries in steps: seg[0] = 0 < ... < seg[m] = n
+    std::vector<int32_t> sub;       // recompute sub-segment boundaries (a refinement of seg)
+    std::vector<int32_t> ck_row;    // checkpoint row of f_i, or -1
+    std::vector<char> ck_always;    // that row is also read by a later forward kernel
+    std::vector<int32_t> bk_row;    // row of s_i (latest start) read by an earlier segment, or -1
+    int32_t n_ck = 0, n_bk = 0;
+    bool slack = false;
+    bool staged = false;            // slack written through LDS in 16-pack chunks
+    int block = 256;
+    int segments() const { return static_cast<int>(seg.size()) - 1; }
+};
+
+// Scratch layout of one chained evaluation (floats unless noted), each [rows][bp]:
+//   ck [n_ck], bk [n_bk], Tc (makespan so far) [1], Ebc (open fp32 energy block) [1],
+//   Edc (fp64 energy sum) [1, doubles]
+size_t chain_scratch_bytes(const ChainPlan &cp, int64_t bp);
+
 struct JitModule {
     hipModule_t module = nullptr;
     hipFunction_t select = nullptr;  // forward pass with optional outputs and selection
     hipFunction_t slack = nullptr;   // only for graphs small enough to keep every finish time
     double compile_seconds = 0.0;
     int block = 256;
+    // segmented kernels
+    bool chain = false;
+    ChainPlan plan;
+    std::vector<hipFunction_t> cf, cb;   // forward kernel of each segment, backward kernel
 };
 
 // Bytes per level load in generated kernels (16, 4 or 1): the alignment they need.
-inline int jit_level_width(int32_t P) { return P % 16 == 0 ? 16 : (P % 4 == 0 ? 4 : 1); }
 
 std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int block);
+// Segments of about seg_ops steps (cut where the pack steps so far are a multiple of 64) and
+// recompute sub-segments of at most sub_ops steps.
+ChainPlan jit_chain_plan(const JitGraph &g, bool with_slack, int seg_ops, int sub_ops);
+std::string jit_generate_chain(const JitGraph &g, const ChainPlan &cp);
+int jit_compile_chain(const std::string &src, const ChainPlan &cp, JitModule *out, std::string *log);
+// Blocks of the segmented kernels' grid (one selection partial each).
+int64_t jit_chain_blocks(const JitModule &m, int64_t B);
+// Forward kernels (and, with S, the backward kernels) of a chained evaluation.  scratch holds
+// chain_scratch_bytes(plan, jit_chain_blocks * block) bytes.
+hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B,
+                            const float2 *tab, void *scratch, float *S, float *T, float *E,
+                            float target, uint32_t *mask, void *part, hipStream_t s);
 // 0 on success; otherwise *log holds the compiler's or loader's message.
 int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log);
 void jit_unload(JitModule *m);

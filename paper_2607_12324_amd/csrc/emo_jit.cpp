@@ -56,6 +56,10 @@ struct LevelPlan {
     int P, F;
     int width;            // 16: uint4 words, 4: u32 words, 1: bytes
     bool pow2;
+    std::string pfx = "L";        // name prefix of the level words
+    bool checks = true;           // record invalid level bytes in `bad`
+    long long base_pack = 0;      // pack whose table row starts at entry 0 of `tab`
+    long long tab_end = 0;        // table entries readable from entry 0
     std::vector<char> loaded, released;
     std::ostringstream *o;
     // Level words are loaded a whole 128-byte line of the row at a time (all of a group's
@@ -68,7 +72,7 @@ struct LevelPlan {
     int nwords() const { return (P + width - 1) / width; }
 
     void check(const std::string &w) {
-        if (F >= 256) return;
+        if (F >= 256 || !checks) return;
         if (pow2) {
             *o << "  bad |= " << w << ";\n";
         } else if (F <= 128) {
@@ -82,31 +86,58 @@ struct LevelPlan {
         }
     }
 
-    void begin() {
-        if (width == 16) *o << "  const uint4 *rowp = (const uint4 *)row;\n";
-        else if (width == 4) *o << "  const unsigned int *rowp = (const unsigned int *)row;\n";
+    // declare_row: declare `rowp` (the row as words); preload: load the first group now.
+    void begin(bool declare_row = true, bool preload = true) {
+        if (declare_row) *o << row_decl(width);
         loaded.assign(nwords() + 1, 0);
         released.assign(nwords() + 1, 0);
-        if (width == 1) return;
+        if (width == 1 || !preload) return;
         load_group(0);
+    }
+
+    static std::string row_decl(int width) {
+        // global address space: the pointer keeps it through the empty asm statements that
+        // order the loads (a generic pointer there would turn them into flat loads, which also
+        // count against the LDS wait counter)
+        if (width == 16) return "  const EMO_GLOBAL emo_u32x4 *rowp = (const EMO_GLOBAL emo_u32x4 *)row;\n";
+        if (width == 4) return "  const EMO_GLOBAL unsigned int *rowp = (const EMO_GLOBAL unsigned int *)row;\n";
+        return "  const EMO_GLOBAL u8 *rowb = (const EMO_GLOBAL u8 *)row;\n";
     }
 
     void load(int q) {
         if (q >= nwords() || loaded[q]) return;
         loaded[q] = 1;
-        *o << "  " << (width == 16 ? "uint4" : "unsigned int") << " L" << q << " = rowp[" << q << "];\n";
+        *o << "  " << (width == 16 ? "emo_u32x4" : "unsigned int") << " " << pfx << q << " = rowp[" << q << "];\n";
     }
 
     void load_group(int gidx) {
         for (int q = gidx * group_words(); q < (gidx + 1) * group_words(); ++q) load(q);
     }
 
-    bool needs_release(int p) const { return width != 1 && !released[p / width]; }
+    // Byte loads (width 1) are released kByteBatch at a time.
+    static constexpr int kByteBatch = 16;
+    int bytes_loaded = 0;
+
+    bool needs_release(int p) const {
+        if (width == 1) return bytes_loaded % kByteBatch == 0;
+        return !released[p / width];
+    }
 
     // Releases chunk q.  `ride` names values computed before this point (the energy partial
     // sum and the finish times still needed later) that pass through the same barrier, so the
     // arithmetic of the previous chunk completes before this chunk's table reads start.
     void release(int q, const std::vector<std::string> &ride) {
+        if (width == 1) {   // the next batch of byte loads reads through a new row pointer
+            std::vector<std::string> ops = {"rowb"};
+            ops.insert(ops.end(), ride.begin(), ride.end());
+            for (size_t b = 0; b < ops.size(); b += 24) {
+                *o << "  __asm__ __volatile__(\"\" :";
+                for (size_t k = b; k < ops.size() && k < b + 24; ++k)
+                    *o << (k == b ? " " : ", ") << "\"+v\"(" << ops[k] << ")";
+                *o << ");\n";
+            }
+            return;
+        }
         const int gidx = q / group_words();
         if (!loaded[q] || (q % group_words() == 0 && (gidx + 1) * group_words() < nwords() &&
                            !loaded[(gidx + 1) * group_words()])) {
@@ -114,10 +145,10 @@ struct LevelPlan {
             load_group(gidx);
             load_group(gidx + 1);
         }
-        std::string w = "L" + std::to_string(q);
+        std::string w = pfx + std::to_string(q);
         std::vector<std::string> ops;
         if (width == 16) {
-            for (int k = 0; k < 4; ++k) ops.push_back(w + "." + comp(k));
+            ops.push_back(w);
         } else {
             ops.push_back(w);
         }
@@ -137,26 +168,59 @@ struct LevelPlan {
         released[q] = 1;
     }
 
+    // Passes every loaded word through an empty asm statement, so that later uses of the
+    // level bytes are computed again from the words (not kept from earlier uses).
+    void launder() {
+        if (width == 1) {
+            *o << "  __asm__ __volatile__(\"\" : \"+v\"(rowb));\n";
+            return;
+        }
+        std::vector<std::string> ops;
+        for (int q = 0; q < nwords(); ++q)
+            if (loaded[q] && released[q]) ops.push_back(pfx + std::to_string(q));
+        for (size_t b = 0; b < ops.size(); b += 16) {
+            *o << "  __asm__ __volatile__(\"\" :";
+            for (size_t k = b; k < ops.size() && k < b + 16; ++k)
+                *o << (k == b ? " " : ", ") << "\"+v\"(" << ops[k] << ")";
+            *o << ");\n";
+        }
+    }
+
+    // Byte loads only: loads pack p's level byte again (after launder(), which gives the row
+    // pointer a new value, so the load is not merged with the first one) and returns its
+    // expression.  Keeps the byte out of a register between the two uses.
+    std::string reload_byte(int p) {
+        const std::string b = pfx + "r" + std::to_string(p);
+        *o << "  const unsigned int " << b << " = rowb[" << p << "];\n";
+        if (pow2 && F < 256 && !raw_ok(p)) return "(" + b + " & " + std::to_string(F - 1) + "u)";
+        return b;
+    }
+
     // Returns the expression of pack p's level byte (emitting loads and checks as needed).
     std::string byte_of(int p) {
         std::ostringstream e;
         if (width == 1) {
-            *o << "  const unsigned int B" << p << " = row[" << p << "];\n";
-            if (F < 256) *o << "  bad |= (B" << p << " >= " << F << "u) ? 0x80808080u : 0u;\n";
-            if (pow2 && F < 256 && !raw_ok(p)) e << "(B" << p << " & " << (F - 1) << "u)";
-            else e << "B" << p;
+            const std::string b = pfx + "b" + std::to_string(p);
+            *o << "  const unsigned int " << b << " = rowb[" << p << "];\n";
+            ++bytes_loaded;
+            if (F < 256 && checks) *o << "  bad |= (" << b << " >= " << F << "u) ? 0x80808080u : 0u;\n";
+            if (pow2 && F < 256 && !raw_ok(p)) e << "(" << b << " & " << (F - 1) << "u)";
+            else e << b;
             return e.str();
         }
         const int q = p / width;
-        std::string w = "L" + std::to_string(q);
+        std::string w = pfx + std::to_string(q);
         if (width == 16) w += std::string(".") + comp((p % 16) / 4);
         const unsigned m = (pow2 && F < 256 && !raw_ok(p)) ? static_cast<unsigned>(F - 1) : 0xffu;
         e << "((" << w << " >> " << 8 * (p % 4) << ") & " << m << "u)";
         return e.str();
     }
 
-    // Whether any byte value at pack p indexes inside the unpadded table.
-    bool raw_ok(int p) const { return !pow2 || static_cast<long long>(p) * F + 255 < static_cast<long long>(P) * F; }
+    // Whether any byte value at pack p indexes inside the readable table.
+    bool raw_ok(int p) const { return !pow2 || (p - base_pack) * F + 255 < tab_end; }
+
+    // Table entry of pack p's row.
+    long long row_entry(int p) const { return (p - base_pack) * F; }
 
     // Bits of `bad` that mark an invalid level.
     std::string bad_bits() const {
@@ -187,28 +251,47 @@ std::string est_expr(const JitGraph &g, int i, const char *prefix) {
     return e;
 }
 
-// Forward pass: declares f<i> (finish time) for every step, and T, E, bad; records the
-// expression of each pack step's level byte in *level_expr.
-void emit_forward(std::ostringstream &o, const JitGraph &g, std::vector<std::string> *level_expr) {
+// Options of a forward walk over the steps [a, b).
+struct RangeOpts {
+    int a = 0, b = 0;
+    bool accumulate = true;                        // makespan T and energy (eb, ed) as well
+    int npk0 = 0;                                  // pack steps before a (energy block phase)
+    const std::vector<int> *ck_row = nullptr;      // store f_i to checkpoint row ck_row[i] >= 0
+    const std::vector<char> *ck_always = nullptr;  // the row is read by a later forward kernel
+    std::string pfx = "L";
+    long long base_pack = 0, tab_end = 0;          // table window (LevelPlan)
+    bool declare_row = true, preload = true;
+    bool checks = true;                            // record invalid level bytes in `bad`
+};
+
+// Forward walk over steps [a, b) (Eq. 1): declares f<i> for each of them (values of earlier
+// steps must be in scope as f<k>); with accumulate, also updates T, eb, ed and bad, which must
+// be declared.  Records the expression of each pack step's level byte in *level_expr.
+LevelPlan emit_forward_range(std::ostringstream &o, const JitGraph &g, const RangeOpts &r,
+                             std::vector<std::string> *level_expr) {
     LevelPlan lp;
     lp.P = g.P;
     lp.F = g.F;
-    lp.width = jit_level_width(g.P);
+    lp.width = jit_level_width(g);
     lp.pow2 = is_pow2(g.F);
+    lp.pfx = r.pfx;
+    lp.base_pack = r.base_pack;
+    lp.tab_end = r.tab_end;
+    lp.checks = r.checks;
     lp.o = &o;
-    o << "  unsigned int bad = 0u;\n  float eb = 0.f;\n  double ed = 0.0;\n";
-    lp.begin();
-    o << "  float T = " << flit(g.t_const) << ";\n";
-    int npk = 0;
+    lp.begin(r.declare_row, r.preload);
+    int npk = r.npk0;
     const int n = static_cast<int>(g.ops.size());
     std::vector<int> last_use(n, -1);
     for (int i = 0; i < n; ++i)
         for (int k : g.ops[i].in) last_use[k] = std::max(last_use[k], i);
-    int since = 0;   // first step not yet passed through a barrier
-    for (int i = 0; i < n; ++i) {
+    int since = r.a;   // first step not yet passed through a barrier
+    for (int i = r.a; i < r.b; ++i) {
         const JitOp &op = g.ops[i];
         if (op.pack >= 0 && lp.needs_release(op.pack)) {
-            std::vector<std::string> ride = {"eb", "ed", "bad"};
+            std::vector<std::string> ride;
+            if (r.accumulate) ride = {"eb", "ed", "bad"};
+            else ride = {"bad"};
             for (int j = since; j < i; ++j)
                 if (last_use[j] >= i) ride.push_back("f" + std::to_string(j));
             lp.release(op.pack / lp.width, ride);
@@ -217,20 +300,47 @@ void emit_forward(std::ostringstream &o, const JitGraph &g, std::vector<std::str
         if (op.pack >= 0) {
             std::string b = lp.byte_of(op.pack);
             if (level_expr) (*level_expr)[i] = b;
-            o << "  const float2 te" << i << " = tab[" << static_cast<long long>(op.pack) * g.F
-              << " + " << b << "];\n";
+            o << "  const float2 te" << i << " = tab[" << lp.row_entry(op.pack) << " + " << b << "];\n";
             o << "  float f" << i << " = " << est_expr(g, i, "f") << " + te" << i << ".x;\n";
-            o << "  eb += te" << i << ".y;\n";
-            if (++npk % 64 == 0) o << "  ed += (double)eb;\n  eb = 0.f;\n";
+            if (r.accumulate) {
+                o << "  eb += te" << i << ".y;\n";
+                if (++npk % 64 == 0) o << "  ed += (double)eb;\n  eb = 0.f;\n";
+            }
         } else {
             o << "  float f" << i << " = " << est_expr(g, i, "f") << " + " << flit(op.dur) << ";\n";
         }
-        if (op.out.empty()) o << "  T = fmaxf(T, f" << i << ");\n";
+        if (r.accumulate && op.out.empty()) o << "  T = fmaxf(T, f" << i << ");\n";
+        if (r.ck_row && (*r.ck_row)[i] >= 0) {
+            o << "  " << ((*r.ck_always)[i] ? "" : "if (full) ") << "EMO_AT(ck, " << (*r.ck_row)[i]
+              << ") = f" << i << ";\n";
+        }
     }
+    return lp;
+}
+
+// Completes the energy (Eq. 2: table energies plus static power times makespan) and marks a
+// candidate with an invalid level byte: declares E and isbad.  nan_carry: an earlier kernel
+// marks an invalid level by a NaN energy partial sum.
+void emit_forward_finish(std::ostringstream &o, const JitGraph &g, const LevelPlan &lp,
+                         bool nan_carry = false) {
     o << "  ed += (double)eb;\n";
     o << "  float E = (float)(ed + (double)" << flit(g.static_power) << " * (double)T);\n";
-    o << "  const bool isbad = (bad & " << lp.bad_bits() << ") != 0u;\n";
+    o << "  const bool isbad = (bad & " << lp.bad_bits() << ") != 0u" << (nan_carry ? " || ed != ed" : "")
+      << ";\n";
     o << "  if (isbad) { T = __builtin_nanf(\"\"); E = __builtin_nanf(\"\"); }\n";
+}
+
+// Forward pass of the whole graph: declares f<i> (finish time) for every step, and T, E, bad,
+// isbad; records the expression of each pack step's level byte in *level_expr.
+LevelPlan emit_forward(std::ostringstream &o, const JitGraph &g, std::vector<std::string> *level_expr) {
+    o << "  unsigned int bad = 0u;\n  float eb = 0.f;\n  double ed = 0.0;\n";
+    o << "  float T = " << flit(g.t_const) << ";\n";
+    RangeOpts r;
+    r.b = static_cast<int>(g.ops.size());
+    r.tab_end = static_cast<long long>(g.P) * g.F;
+    LevelPlan lp = emit_forward_range(o, g, r, level_expr);
+    emit_forward_finish(o, g, lp);
+    return lp;
 }
 
 // Slack output staging: packs [p0, p0 + kc) of the wave's 64 candidates are collected in LDS
@@ -282,8 +392,44 @@ void emit_backward(std::ostringstream &o, const JitGraph &g, bool staged,
     }
 }
 
+// Device routine that writes the slack of packs [p0, p0 + EMO_KC) of the wave's 64 candidates
+// from the LDS staging area (rows of P floats per candidate).
+std::string flush_source(int P) {
+    return std::string(R"(
+// Writes the slack of packs [p0, p0 + EMO_KC) of the wave's 64 candidates, staged in LDS.
+__device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_bad,
+                                          float *__restrict__ S, long long wbase, long long B,
+                                          int p0) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int lane = threadIdx.x % EMO_WAVE;
+  constexpr int per_row = EMO_KC / 4;          // 16-byte pieces per candidate segment
+#pragma unroll
+  for (int m = 0; m < per_row; ++m) {
+    const int j = lane + EMO_WAVE * m;
+    const int r = j / per_row, part = j % per_row;
+    float4 v;
+    v.x = stg[(4 * part + 0) * 65 + r];
+    v.y = stg[(4 * part + 1) * 65 + r];
+    v.z = stg[(4 * part + 2) * 65 + r];
+    v.w = stg[(4 * part + 3) * 65 + r];
+    if (stg_bad[r]) { v.x = EMO_NAN; v.y = EMO_NAN; v.z = EMO_NAN; v.w = EMO_NAN; }
+    const long long row = wbase + r;
+    if (row < B) *(float4 *)(S + row * )" + std::to_string(P) + R"(LL + p0 + 4 * part) = v;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+)");
+}
+
 const char *kPrelude = R"(
 typedef unsigned char u8;
+#define EMO_AT(buf, r) (*(__typeof__(&(buf)[0]))((const char *)((buf) + (long long)(r) * bp) + o4))
+typedef unsigned int emo_u32x4 __attribute__((ext_vector_type(4)));
+#define EMO_GLOBAL __attribute__((address_space(1)))
 #define EMO_NAN __builtin_nanf("")
 )";
 
@@ -334,34 +480,7 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
         if (staged) {
             const int kc = stage_chunk(g.P);
             o << "#define EMO_KC " << kc << "\n";
-            o << R"(
-// Writes the slack of packs [p0, p0 + EMO_KC) of the wave's 64 candidates, staged in LDS.
-__device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_bad,
-                                          float *__restrict__ S, long long wbase, long long B,
-                                          int p0) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  const int lane = threadIdx.x % EMO_WAVE;
-  constexpr int per_row = EMO_KC / 4;          // 16-byte pieces per candidate segment
-#pragma unroll
-  for (int m = 0; m < per_row; ++m) {
-    const int j = lane + EMO_WAVE * m;
-    const int r = j / per_row, part = j % per_row;
-    float4 v;
-    v.x = stg[(4 * part + 0) * 65 + r];
-    v.y = stg[(4 * part + 1) * 65 + r];
-    v.z = stg[(4 * part + 2) * 65 + r];
-    v.w = stg[(4 * part + 3) * 65 + r];
-    if (stg_bad[r]) { v.x = EMO_NAN; v.y = EMO_NAN; v.z = EMO_NAN; v.w = EMO_NAN; }
-    const long long row = wbase + r;
-    if (row < B) *(float4 *)(S + row * )" << g.P << R"(LL + p0 + 4 * part) = v;
-  }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-)";
+            o << flush_source(g.P);
         }
         o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
              "emo_sp_slack(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
@@ -380,9 +499,10 @@ __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_ba
         }
         o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
         std::vector<std::string> level_expr(g.ops.size());
-        emit_forward(o, g, &level_expr);
+        LevelPlan lp = emit_forward(o, g, &level_expr);
         o << "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n";
         if (staged) o << "  stg_bad[lane] = isbad ? 1u : 0u;\n";
+        lp.launder();
         emit_backward(o, g, staged, level_expr);
         o << "  if (mask || part) emo_select_block(active, T, E, cand, B, target, mask, part);\n";
         o << "}\n";
@@ -390,7 +510,292 @@ __device__ __forceinline__ void emo_flush(float *stg, const unsigned int *stg_ba
     return o.str();
 }
 
-int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log) {
+// ------------------------------------------------------------------ segmented kernels
+
+ChainPlan jit_chain_plan(const JitGraph &g, bool with_slack, int seg_ops, int sub_ops) {
+    ChainPlan cp;
+    cp.slack = with_slack;
+    const int n = static_cast<int>(g.ops.size());
+    cp.seg.push_back(0);
+    int npk = 0, start = 0;
+    for (int i = 0; i < n; ++i) {
+        if (g.ops[i].pack >= 0) ++npk;
+        // segments end where the pack steps so far are a multiple of 64: energy blocks and
+        // 16-pack slack chunks never straddle two kernels
+        if (i + 1 < n && i + 1 - start >= seg_ops && n - (i + 1) >= seg_ops / 2 && npk % 64 == 0) {
+            cp.seg.push_back(i + 1);
+            start = i + 1;
+        }
+    }
+    cp.seg.push_back(n);
+    std::vector<int> seg_of(n), sub_of(n);
+    for (int j = 0; j + 1 < static_cast<int>(cp.seg.size()); ++j) {
+        for (int c = cp.seg[j]; c < cp.seg[j + 1]; c += sub_ops) cp.sub.push_back(c);
+        for (int i = cp.seg[j]; i < cp.seg[j + 1]; ++i) seg_of[i] = j;
+    }
+    cp.sub.push_back(n);
+    for (int r = 0; r + 1 < static_cast<int>(cp.sub.size()); ++r)
+        for (int i = cp.sub[r]; i < cp.sub[r + 1]; ++i) sub_of[i] = r;
+    cp.ck_row.assign(n, -1);
+    cp.ck_always.assign(n, 0);
+    cp.bk_row.assign(n, -1);
+    for (int i = 0; i < n; ++i) {
+        bool later_seg = false, other_sub = false;
+        for (int k : g.ops[i].out) {
+            later_seg |= seg_of[k] != seg_of[i];
+            other_sub |= sub_of[k] != sub_of[i];
+        }
+        if (later_seg || (with_slack && other_sub)) {
+            cp.ck_row[i] = cp.n_ck++;
+            cp.ck_always[i] = later_seg;
+        }
+        if (with_slack) {
+            bool earlier = false;
+            for (int k : g.ops[i].in) earlier |= seg_of[k] != seg_of[i];
+            if (earlier) cp.bk_row[i] = cp.n_bk++;
+        }
+    }
+    cp.staged = with_slack && g.pack_monotone && g.P % 16 == 0;
+    return cp;
+}
+
+namespace {
+
+constexpr int kChainStage = 16;                        // slack staging chunk (packs)
+constexpr size_t kChainLdsForward = 48 * 1024;         // table window budget, forward kernels
+constexpr size_t kChainLdsBackward = 48 * 1024;        // table window budget, backward kernels
+
+// Table window of one kernel: the rows of the packs its steps visit, staged in LDS when they
+// fit, else the whole table in device memory.
+struct TabWindow {
+    bool lds = false;
+    long long base_pack = 0, entries = 0, tab_end = 0;
+};
+
+TabWindow chain_window(const JitGraph &g, int a, int b, size_t budget) {
+    int lo = g.P, hi = -1;
+    for (int i = a; i < b; ++i)
+        if (g.ops[i].pack >= 0) {
+            lo = std::min(lo, g.ops[i].pack);
+            hi = std::max(hi, g.ops[i].pack);
+        }
+    TabWindow w;
+    w.tab_end = static_cast<long long>(g.P) * g.F;
+    if (hi < 0) return w;
+    const long long rows = static_cast<long long>(hi - lo + 1) * g.F;
+    const long long ent = rows + (is_pow2(g.F) ? 0 : kTablePad);
+    if (static_cast<size_t>(ent) * 8 > budget) return w;
+    w.lds = true;
+    w.base_pack = lo;
+    w.entries = ent;
+    w.tab_end = rows;
+    return w;
+}
+
+void emit_table(std::ostringstream &o, const JitGraph &g, const TabWindow &w) {
+    if (!w.lds) {
+        o << "  const float2 *__restrict__ tab = tabg;\n";
+        return;
+    }
+    o << "  __shared__ float2 tab[" << w.entries << "];\n"
+      << "  for (int i_ = threadIdx.x; i_ < " << w.entries << "; i_ += EMO_BLOCK) tab[i_] = tabg["
+      << w.base_pack * g.F << "LL + i_];\n"
+      << "  __syncthreads();\n";
+}
+
+// Lane setup of a segmented kernel.  Scratch row r is addressed as a uniform base
+// (buf + r * bp) plus the lane's 32-bit byte offset o4 (bp * 4 < 2^32), which the compiler
+// folds into one load or store with a scalar base.
+const char *kChainLanes =
+    "  const unsigned int g32 = blockIdx.x * EMO_BLOCK + threadIdx.x;\n"
+    "  const unsigned int o4 = g32 * 4u;\n"
+    "  const long long gid = g32;\n"
+    "  const long long bp = (long long)gridDim.x * EMO_BLOCK;\n"
+    "  const bool active = gid < B;\n"
+    "  const long long cand = active ? gid : B - 1;\n"
+    "  (void)active; (void)bp;\n";
+
+// Steps before `a` whose finish times steps [a, b) read.
+std::vector<int> inputs_before(const JitGraph &g, int a, int b) {
+    std::vector<int> v;
+    for (int i = a; i < b; ++i)
+        for (int k : g.ops[i].in)
+            if (k < a) v.push_back(k);
+    std::sort(v.begin(), v.end());
+    v.erase(std::unique(v.begin(), v.end()), v.end());
+    return v;
+}
+
+void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPlan &cp, int j) {
+    const int a = cp.seg[j], b = cp.seg[j + 1];
+    const bool last = j + 1 == cp.segments();
+    int npk0 = 0, npk1 = 0;
+    for (int i = 0; i < b; ++i)
+        if (g.ops[i].pack >= 0) (i < a ? npk0 : npk1)++;
+    npk1 += npk0;
+    const TabWindow w = chain_window(g, a, b, kChainLdsForward);
+    o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
+      << "emo_cf" << j << "(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
+         "    float *__restrict__ ck, float *__restrict__ Tc, double *__restrict__ Edc,\n"
+         "    float *__restrict__ Ebc, int full, float *__restrict__ To, float *__restrict__ Eo,\n"
+         "    float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n";
+    emit_table(o, g, w);
+    o << kChainLanes;
+    o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
+    o << "  unsigned int bad = 0u;\n  (void)full;\n";
+    if (j == 0) {
+        o << "  float T = " << flit(g.t_const) << ";\n  float eb = 0.f;\n  double ed = 0.0;\n";
+    } else {
+        o << "  float T = Tc[g32];\n  double ed = Edc[g32];\n";
+        o << "  float eb = " << (npk0 % 64 ? "Ebc[g32]" : "0.f") << ";\n";
+    }
+    for (int k : inputs_before(g, a, b))
+        o << "  const float f" << k << " = EMO_AT(ck, " << cp.ck_row[k] << ");\n";
+    RangeOpts r;
+    r.a = a;
+    r.b = b;
+    r.npk0 = npk0;
+    r.ck_row = &cp.ck_row;
+    r.ck_always = &cp.ck_always;
+    r.base_pack = w.base_pack;
+    r.tab_end = w.tab_end;
+    r.preload = false;
+    LevelPlan lp = emit_forward_range(o, g, r, nullptr);
+    if (!last) {
+        o << "  if ((bad & " << lp.bad_bits() << ") != 0u) ed = (double)EMO_NAN;\n";
+        o << "  Tc[g32] = T;\n  Edc[g32] = ed;\n";
+        if (npk1 % 64) o << "  Ebc[g32] = eb;\n";
+    } else {
+        emit_forward_finish(o, g, lp, j > 0);
+        o << "  Tc[g32] = T;\n"
+             "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n"
+             "  if (mask || part) emo_select_block(active, T, E, cand, B, target, mask, part);\n";
+    }
+    o << "}\n\n";
+}
+
+void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPlan &cp, int j) {
+    const int a = cp.seg[j], b = cp.seg[j + 1];
+    const TabWindow w = chain_window(g, a, b, kChainLdsBackward);
+    o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
+      << "emo_cb" << j << "(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
+         "    const float *__restrict__ ck, const float *__restrict__ Tc, float *__restrict__ bk,\n"
+         "    float *__restrict__ S) {\n";
+    emit_table(o, g, w);
+    o << kChainLanes;
+    o << "  const int lane = threadIdx.x % EMO_WAVE;\n"
+         "  const int wave = threadIdx.x / EMO_WAVE;\n"
+         "  const long long wbase = (long long)blockIdx.x * EMO_BLOCK + wave * EMO_WAVE;\n"
+         "  (void)lane; (void)wbase;\n";
+    if (cp.staged) {
+        o << "  __shared__ float stg_all[EMO_WAVES_PER_BLOCK][EMO_KC * 65];\n"
+             "  __shared__ unsigned int bad_all[EMO_WAVES_PER_BLOCK][EMO_WAVE];\n"
+             "  float *stg = stg_all[wave];\n"
+             "  unsigned int *stg_bad = bad_all[wave];\n";
+    }
+    o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
+    o << LevelPlan::row_decl(jit_level_width(g));
+    o << "  const float T = Tc[g32];\n  const bool isbad = T != T;\n"
+         "  const float Tb = isbad ? 0.f : T;\n";
+    if (cp.staged) o << "  stg_bad[lane] = isbad ? 1u : 0u;\n";
+    o << "  unsigned int zb = 0u;\n  __asm__ __volatile__(\"\" : \"+v\"(zb));\n";
+    o << "  unsigned int bad = 0u;\n";
+    // latest start times of later segments' steps that this segment's steps precede
+    std::vector<int> later;
+    for (int i = a; i < b; ++i)
+        for (int u : g.ops[i].out)
+            if (u >= b) later.push_back(u);
+    std::sort(later.begin(), later.end());
+    later.erase(std::unique(later.begin(), later.end()), later.end());
+    for (int u : later) o << "  const float s" << u << " = EMO_AT(bk, " << cp.bk_row[u] << ");\n";
+    for (int i = a; i < b; ++i)
+        if (!g.ops[i].in.empty()) o << "  float s" << i << ";\n";
+    // sub-segments from last to first: recompute their finish times, then walk them backwards
+    int r_first = 0;
+    while (cp.sub[r_first] < a) ++r_first;
+    int r_last = r_first;
+    while (cp.sub[r_last + 1] < b) ++r_last;
+    std::vector<std::string> level_expr(g.ops.size());
+    for (int r = r_last; r >= r_first; --r) {
+        const int c = cp.sub[r], d = cp.sub[r + 1];
+        o << "  {\n";
+        for (int k : inputs_before(g, c, d))
+            o << "  const float f" << k << " = EMO_AT(ck, " << cp.ck_row[k] << ");\n";
+        RangeOpts ro;
+        ro.a = c;
+        ro.b = d;
+        ro.accumulate = false;
+        ro.base_pack = w.base_pack;
+        ro.tab_end = w.tab_end;
+        ro.declare_row = false;
+        ro.preload = false;
+        ro.checks = false;
+        LevelPlan lp = emit_forward_range(o, g, ro, &level_expr);
+        lp.launder();
+        for (int i = d - 1; i >= c; --i) {
+            const JitOp &op = g.ops[i];
+            // table reads index through zb, which passes through an empty asm every 16 steps:
+            // the reads of later steps cannot be hoisted (each would hold a VGPR meanwhile)
+            if ((d - 1 - i) % 16 == 0) o << "  __asm__ __volatile__(\"\" : \"+v\"(zb));\n";
+            std::string lft;
+            if (op.out.empty()) {
+                lft = "Tb";
+            } else {
+                bool have = false;
+                for (int k : op.out) {
+                    std::string v = "s" + std::to_string(k);
+                    lft = have ? "fminf(" + lft + ", " + v + ")" : v;
+                    have = true;
+                }
+            }
+            o << "  const float lf" << i << " = " << lft << ";\n";
+            std::string dur = flit(op.dur);
+            if (op.pack >= 0) {
+                const std::string lv = lp.width == 1 ? lp.reload_byte(op.pack) : level_expr[i];
+                o << "  const float t" << i << " = tab[zb + " << lp.row_entry(op.pack) << " + "
+                  << lv << "].x;\n";
+                dur = "t" + std::to_string(i);
+            }
+            if (!op.in.empty()) {
+                o << "  s" << i << " = lf" << i << " - " << dur << ";\n";
+                if (cp.bk_row[i] >= 0) o << "  EMO_AT(bk, " << cp.bk_row[i] << ") = s" << i << ";\n";
+            }
+            if (op.pack >= 0) {
+                const int p = op.pack;
+                if (cp.staged) {
+                    o << "  stg[" << (p % kChainStage) * 65 << " + lane] = lf" << i << " - f" << i << ";\n";
+                    if (p % kChainStage == 0) o << "  emo_flush(stg, stg_bad, S, wbase, B, " << p << ");\n";
+                } else {
+                    o << "  if (active) S[cand * " << g.P << "LL + " << p
+                      << "] = isbad ? EMO_NAN : lf" << i << " - f" << i << ";\n";
+                }
+            }
+        }
+        o << "  }\n";
+    }
+    o << "}\n\n";
+}
+
+}  // namespace
+
+std::string jit_generate_chain(const JitGraph &g, const ChainPlan &cp) {
+    std::ostringstream o;
+    o << "#define EMO_BLOCK " << cp.block << "\n" << kPrelude << kEmoSelectSource << "\n";
+    if (cp.staged) o << "#define EMO_KC " << kChainStage << "\n" << flush_source(g.P);
+    for (int j = 0; j < cp.segments(); ++j) emit_chain_forward(o, g, cp, j);
+    if (cp.slack)
+        for (int j = 0; j < cp.segments(); ++j) emit_chain_backward(o, g, cp, j);
+    return o.str();
+}
+
+size_t chain_scratch_bytes(const ChainPlan &cp, int64_t bp) {
+    return static_cast<size_t>(bp) * (4 * static_cast<size_t>(cp.n_ck + cp.n_bk + 2) + 8);
+}
+
+namespace {
+
+// Compiles `src` for gfx950 and loads it as a module.  0 on success, 1 compile error, 2 load error.
+int compile_module(const std::string &src, hipModule_t *module, double *seconds, std::string *log) {
     hiprtcProgram prog;
     if (hiprtcCreateProgram(&prog, src.c_str(), "emo_specialised.hip", 0, nullptr, nullptr) !=
         HIPRTC_SUCCESS) {
@@ -401,8 +806,7 @@ int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::st
                           "-Xclang", "-packed-fp32-ops"};
     auto t0 = std::chrono::steady_clock::now();
     hiprtcResult r = hiprtcCompileProgram(prog, sizeof(opts) / sizeof(opts[0]), opts);
-    out->compile_seconds =
-        std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    *seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
     size_t ls = 0;
     hiprtcGetProgramLogSize(prog, &ls);
     if (ls > 1) {
@@ -420,17 +824,52 @@ int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::st
     std::string code(cs, '\0');
     hiprtcGetCode(prog, &code[0]);
     hiprtcDestroyProgram(&prog);
-    hipError_t e = hipModuleLoadData(&out->module, code.data());
+    hipError_t e = hipModuleLoadData(module, code.data());
     if (e != hipSuccess) {
         (void)hipGetLastError();
         *log = std::string("hipModuleLoadData: ") + hipGetErrorString(e);
-        out->module = nullptr;
+        *module = nullptr;
         return 2;
     }
-    if (hipModuleGetFunction(&out->select, out->module, "emo_sp_select") != hipSuccess ||
-        (with_slack && hipModuleGetFunction(&out->slack, out->module, "emo_sp_slack") != hipSuccess)) {
-        (void)hipGetLastError();   // clear the runtime's sticky error
+    return 0;
+}
+
+bool get_function(hipModule_t m, const std::string &name, hipFunction_t *f) {
+    if (hipModuleGetFunction(f, m, name.c_str()) == hipSuccess) return true;
+    (void)hipGetLastError();   // clear the runtime's sticky error
+    return false;
+}
+
+}  // namespace
+
+int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log) {
+    int rc = compile_module(src, &out->module, &out->compile_seconds, log);
+    if (rc != 0) return rc;
+    if (!get_function(out->module, "emo_sp_select", &out->select) ||
+        (with_slack && !get_function(out->module, "emo_sp_slack", &out->slack))) {
         *log = "specialised kernels missing from the module";
+        (void)hipModuleUnload(out->module);
+        *out = JitModule();
+        return 2;
+    }
+    return 0;
+}
+
+int jit_compile_chain(const std::string &src, const ChainPlan &cp, JitModule *out, std::string *log) {
+    int rc = compile_module(src, &out->module, &out->compile_seconds, log);
+    if (rc != 0) return rc;
+    out->chain = true;
+    out->plan = cp;
+    out->block = cp.block;
+    out->cf.assign(cp.segments(), nullptr);
+    out->cb.assign(cp.slack ? cp.segments() : 0, nullptr);
+    bool okf = true;
+    for (int j = 0; j < cp.segments(); ++j) {
+        okf = okf && get_function(out->module, "emo_cf" + std::to_string(j), &out->cf[j]);
+        if (cp.slack) okf = okf && get_function(out->module, "emo_cb" + std::to_string(j), &out->cb[j]);
+    }
+    if (!okf) {
+        *log = "segmented kernels missing from the module";
         (void)hipModuleUnload(out->module);
         *out = JitModule();
         return 2;
@@ -455,6 +894,42 @@ hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t
     long long b = B;
     void *args[] = {&levels, &b, &tab, &T, &E, &target, &mask, &part};
     return hipModuleLaunchKernel(m.select, grid_of(B, m.block), 1, 1, m.block, 1, 1, 0, s, args, nullptr);
+}
+
+int64_t jit_chain_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.plan.block); }
+
+hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B,
+                            const float2 *tab, void *scratch, float *S, float *T, float *E,
+                            float target, uint32_t *mask, void *part, hipStream_t s) {
+    const ChainPlan &cp = m.plan;
+    const unsigned grid = grid_of(B, cp.block);
+    const int64_t bp = static_cast<int64_t>(grid) * cp.block;
+    float *ck = static_cast<float *>(scratch);
+    float *bk = ck + static_cast<size_t>(cp.n_ck) * bp;
+    float *Tc = bk + static_cast<size_t>(cp.n_bk) * bp;
+    float *Ebc = Tc + bp;
+    double *Edc = reinterpret_cast<double *>(Ebc + bp);   // 8-byte aligned: bp is a multiple of 64
+    long long b = B;
+    int full = S ? 1 : 0;
+    const int m_seg = cp.segments();
+    for (int j = 0; j < m_seg; ++j) {
+        const bool last = j + 1 == m_seg;
+        float *To = last ? T : nullptr;
+        float *Eo = last ? E : nullptr;
+        uint32_t *mk = last ? mask : nullptr;
+        void *pt = last ? part : nullptr;
+        void *args[] = {&levels, &b, &tab, &ck, &Tc, &Edc, &Ebc, &full, &To, &Eo, &target, &mk, &pt};
+        hipError_t e = hipModuleLaunchKernel(m.cf[j], grid, 1, 1, cp.block, 1, 1, 0, s, args, nullptr);
+        if (e != hipSuccess) return e;
+    }
+    if (!S) return hipSuccess;
+    for (int j = m_seg - 1; j >= 0; --j) {
+        const float *ckc = ck, *Tcc = Tc;
+        void *args[] = {&levels, &b, &tab, &ckc, &Tcc, &bk, &S};
+        hipError_t e = hipModuleLaunchKernel(m.cb[j], grid, 1, 1, cp.block, 1, 1, 0, s, args, nullptr);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,

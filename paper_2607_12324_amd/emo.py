@@ -24,7 +24,8 @@ ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_kernel_mode", "emo_graph_topo_order",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
                 "emo_select_from_results",
-                "emo_graph_set_timing_events", "emo_graph_specialized_source", "emo_status_string",
+                "emo_graph_set_timing_events", "emo_graph_specialized_source",
+                "emo_graph_segmented_source", "emo_status_string",
                 "emo_last_error")
 
 
@@ -42,7 +43,7 @@ class GraphInfo(ctypes.Structure):
                 ("const_makespan", ctypes.c_float), ("device", ctypes.c_int32),
                 ("pack_order_monotone", ctypes.c_int32), ("kernel_mode", ctypes.c_int32),
                 ("specialized", ctypes.c_int32), ("compile_seconds", ctypes.c_float),
-                ("num_implied_edges", ctypes.c_int32)]
+                ("last_kernels", ctypes.c_int32), ("num_implied_edges", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -69,6 +70,7 @@ def _load_library():
         "emo_evaluate": [P, P, i64, P, P, P, i32, f32, P, P, P],
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
         "emo_graph_specialized_source": [P, P, P],
+        "emo_graph_segmented_source": [P, P, P],
         "emo_graph_set_timing_events": [P, P, P],
     }
     for name, args in sig.items():
@@ -184,10 +186,16 @@ class EmoGraph:
         _check(lib.emo_graph_set_timing_events(self._h, hb, he))
 
     def specialized_source(self) -> str:
+        return self._source(lib.emo_graph_specialized_source)
+
+    def segmented_source(self) -> str:
+        return self._source(lib.emo_graph_segmented_source)
+
+    def _source(self, fn) -> str:
         n = ctypes.c_int64(0)
-        _check(lib.emo_graph_specialized_source(self._h, None, ctypes.byref(n)))
+        _check(fn(self._h, None, ctypes.byref(n)))
         buf = ctypes.create_string_buffer(n.value)
-        _check(lib.emo_graph_specialized_source(self._h, buf, ctypes.byref(n)))
+        _check(fn(self._h, buf, ctypes.byref(n)))
         return buf.value.decode()
 
     def topo_order(self):

@@ -238,6 +238,27 @@ def _packed_graph(seed, name, P=4096, S=8, F=16, sync_every=256, cross_p=0.03) -
     return _finish(b, name, sdur, t, e)
 
 
+def packed_graph(seed: int, P: int, S: int, F: int, sync_every: int = 256,
+                 cross_p: float = 0.03, shuffle_pack_ids: bool = False) -> Graph:
+    """A graph shaped like the large packed workload at another size: P packs on S streams with
+    periodic all-stream synchronisation nodes and random cross-stream edges.  With
+    shuffle_pack_ids the pack numbering is a random permutation (tables permuted with it)."""
+    g = _packed_graph(seed, f"packed-{P}p-{S}s-F{F}", P=P, S=S, F=F, sync_every=sync_every,
+                      cross_p=cross_p)
+    if not shuffle_pack_ids:
+        return g
+    perm = np.random.default_rng(seed + 1).permutation(P)     # old id -> new id
+    node_pack = g.node_pack.copy()
+    m = node_pack >= 0
+    node_pack[m] = perm[node_pack[m]]
+    t = np.empty_like(g.pack_time)
+    e = np.empty_like(g.pack_energy)
+    t[perm] = g.pack_time
+    e[perm] = g.pack_energy
+    return dataclasses.replace(g, name=g.name + "-shuffled", node_pack=node_pack.astype(np.int32),
+                               pack_time=t, pack_energy=e)
+
+
 def config_graph(k: int) -> Graph:
     """The execution graph and tables of benchmark workload `k` (1..5)."""
     spec = CONFIGS[k]

@@ -151,6 +151,54 @@ def test_interpreter_table_windows(torch, emo, F, P):
     run_all(torch, emo, g, rows, [float(np.median(T_or))], what=f"windows F={F} P={P}", mode=1)
 
 
+SEGMENTED_CASES = {
+    # name: (packs, streams, levels, shuffled pack ids)
+    "staged-F16": (1024, 8, 16, False),      # slack written through LDS, table windows in LDS
+    "ragged-F16": (1000, 6, 16, False),      # pack count not a multiple of 16: direct stores
+    "shuffled-F8": (700, 4, 8, True),        # packs out of order: byte loads, direct stores
+    "monotone-F5": (896, 8, 5, False),       # level count not a power of two
+    "wide-F16": (2400, 8, 16, False),        # eval/select also segmented (> 2048 steps)
+}
+
+
+@pytest.mark.parametrize("case", list(SEGMENTED_CASES))
+def test_segmented_kernels(torch, emo, case):
+    """Graphs too large to keep every finish time in registers (slack) or for one kernel
+    (eval/select, the wide case): the chained segment kernels, with finish times recomputed per
+    sub-segment in the backward kernels, against the oracle on every row, including rows with an
+    invalid level byte and a batch that ends inside a workgroup."""
+    P, S_, F, shuffled = SEGMENTED_CASES[case]
+    g = synth.packed_graph(P + F, P, S_, F, sync_every=128, cross_p=0.05, shuffle_pack_ids=shuffled)
+    rng = np.random.default_rng(P * F)
+    rows = pins.random_rows(rng, g, 1000 - 23)
+    rows[7, g.num_packs // 2] = F              # invalid levels: NaN results, never feasible
+    rows[300, -1] = 255
+    print(f"[case] segmented {case}: V={g.num_nodes} P={g.num_packs} B={len(rows)}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    lv = dev(torch, rows)
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    T, E = gh.eval_policies(lv)
+    S = gh.slack(lv)
+    torch.cuda.synchronize()
+    info = gh.info()
+    assert info["specialized"] & 8 and info["last_kernels"] == 2, info   # segmented kernels ran
+    ok = ~np.isnan(T_or)
+    assert np.isnan(host(T)[7]) and np.isnan(host(T)[300]) and not ok[7] and not ok[300]
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, case)
+    Sh = host(S)
+    assert np.all(np.isnan(Sh[~ok]))
+    S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in np.nonzero(ok)[0]])
+    parity.assert_slack(Sh[ok], S_or, T_or[ok], True, case + " pack slack")
+    # the same through the fused entry point, and the interpreted kernels bit for bit
+    tgt = float(np.float32(np.median(T_or[ok])))
+    run_all(torch, emo, g, rows, [tgt], per_node=False, what="segmented " + case)
+    gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+    Ti, Ei = gi.eval_policies(lv)
+    Si = gi.slack(lv)
+    for a, b in ((T, Ti), (E, Ei), (S, Si)):
+        assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), case
+
+
 def test_large_slot_count_uses_device_scratch(torch, emo):
     """A wide antichain of packs feeding one sink keeps many finish times live at once."""
     rng = np.random.default_rng(5)
@@ -258,9 +306,11 @@ def test_workload_full_batch(torch, emo, k):
     lv = dev(torch, rows)
     T, E = gh.eval_policies(lv)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, spec.name)
+    # one specialised kernel up to 2048 steps, segmented kernels for the 4096-pack graph, the
+    # interpreting kernels for the 65536-kernel graph
     inf = gh.info()
-    assert bool(inf["specialized"] & 1) == (k <= 3), inf
-    if k <= 3:
+    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 2, 5: 0}[k], inf
+    if k <= 4:
         # the interpreting kernels on the same batch: bit-identical
         gi = emo.EmoGraph(g, device=0, kernel_mode=1)
         Ti, Ei = gi.eval_policies(lv)
@@ -281,9 +331,18 @@ def test_workload_full_batch(torch, emo, k):
                                 tgt, True, f"{spec.name} select_from_results@{r}")
     pick = synth.sample_rows(B, 24)
     S = gh.slack(lv)
+    # slack: one kernel while every finish time fits in registers, then segmented kernels
+    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 2, 5: 0}[k], gh.info()
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in pick])
     idx = torch.from_numpy(pick).cuda()
     parity.assert_slack(host(S.index_select(0, idx)), S_or, T_or[pick], True, spec.name + " slack")
+    if k in (3, 4):
+        # the segmented backward kernels against the interpreting kernels on a leading slice
+        gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+        nb = min(B, 8192)
+        Si = gi.slack(lv[:nb])
+        assert torch.equal(Si.view(torch.int32), S[:nb].view(torch.int32)), spec.name
+        gi.close()
     del S
     # per-node slack over a leading slice
     nb = min(B, 512)

@@ -65,6 +65,8 @@ def check_code_object(path, expect):
                          check=True).stdout
     assert not re.search(r"v_pk_(add|mul|fma)_f32", asm), "packed fp32 arithmetic in specialised kernels"
     assert "scratch_" not in asm
+    # level words and scratch rows are global loads (a flat load would also hold up LDS waits)
+    assert "flat_load" not in asm and "flat_store" not in asm
     return notes, asm
 
 
@@ -81,12 +83,33 @@ def test_workload_kernels_compile_without_spills(emo, hiprtc, tmp_path, k):
     assert valu < 6.5 * g.num_packs + 200, valu
 
 
-def test_large_graph_is_not_specialised(emo):
+def test_large_graph_is_not_one_kernel(emo):
     g = synth.config_graph(4)
     gh = emo.EmoGraph(g, device=-1)
     with pytest.raises(emo.EmoError) as ei:
         gh.specialized_source()
     assert ei.value.status == 5
+    small = emo.EmoGraph(synth.config_graph(2), device=-1)
+    with pytest.raises(emo.EmoError) as ei:
+        small.segmented_source()
+    assert ei.value.status == 5
+
+
+@pytest.mark.parametrize("which", ["packed-4096p", "shuffled-F5"])
+def test_segmented_kernels_compile(emo, hiprtc, tmp_path, which):
+    """The chained segment kernels of a large graph (LDS table windows, staged slack) and of a
+    graph with shuffled pack ids and five levels (device table, direct slack stores): every
+    forward and backward kernel compiles without spills or scratch, within 128 VGPRs."""
+    if which == "packed-4096p":
+        g = synth.config_graph(4)
+    else:
+        g = synth.packed_graph(77, 700, 4, 5, sync_every=128, cross_p=0.05, shuffle_pack_ids=True)
+    src = emo.EmoGraph(g, device=-1).segmented_source()
+    m = len(re.findall(r"\bemo_cf(\d+)\(", src))
+    assert m >= 2 and len(re.findall(r"\bemo_cb(\d+)\(", src)) == m
+    path = compile_source(hiprtc, src, tmp_path)
+    notes, _ = check_code_object(path, [f"emo_cf{j}" for j in range(m)] + [f"emo_cb{j}" for j in range(m)])
+    assert max(v for v, _ in notes.values()) <= 128, notes
 
 
 @pytest.mark.parametrize("seed", range(3))
