@@ -32,7 +32,10 @@
  * GPU the graph was loaded on (e.g. a torch CUDA tensor's data_ptr()).  The caller owns every
  * buffer.  Batch calls are asynchronous on `stream` (a hipStream_t; NULL means the default
  * stream): the caller keeps inputs and outputs alive until the stream has completed.  Scratch
- * device memory, when a call needs it, is taken with hipMallocAsync on the same stream.
+ * device memory is kept by each graph handle (and, for emo_select_from_results, per device)
+ * and reused: it grows with hipMalloc when a call needs more (waiting for the calls still
+ * using it) and is freed with the handle, so steady-state calls allocate nothing and never
+ * block the host.
  *
  * Errors: every entry point returns an emo_status.  Argument errors that the host can detect
  * (sizes, null pointers, indices, non-finite or negative values, cycles, misaligned buffers)
@@ -40,7 +43,10 @@
  * the last failure on the calling thread.  A level byte >= F in a candidate is not an error:
  * that candidate's makespan, energy and slack are NaN and it is never feasible.
  *
- * Thread safety: a loaded graph is immutable; concurrent calls on different streams are safe.
+ * Thread safety: a loaded graph is immutable; calls on one handle from several threads or
+ * streams are safe.  They share the handle's scratch, so the device runs them one after the
+ * other: a call on a different stream than the previous one first waits (on the device) for
+ * that call's kernels.
  */
 #ifndef EMO_H
 #define EMO_H

@@ -100,6 +100,59 @@ struct DeviceGuard {
     }
 };
 
+// Device scratch reused across batch calls (selection partials, checkpoint rows, cold slots):
+// allocated on first need, grown (never shrunk) on demand, freed with its owner.  Calls that
+// share an arena are ordered on the device: a call on another stream than the previous one
+// first waits for the event recorded after that call's kernels, and growing waits for it on
+// the host before the old buffer is freed.  Steady-state calls allocate and free nothing, so
+// the host never blocks and keeps launching ahead of the device.
+struct Arena {
+    std::mutex mu;
+    void *ptr = nullptr;
+    size_t bytes = 0;
+    hipEvent_t done = nullptr;   // recorded after the last call's kernels
+    hipStream_t last = nullptr;
+    bool used = false;
+};
+
+// With a.mu held and the arena's device current: at least `bytes` of scratch for a call on s.
+hipError_t arena_acquire(Arena &a, size_t bytes, hipStream_t s, void **out) {
+    hipError_t e = hipSuccess;
+    if (!a.done && (e = hipEventCreateWithFlags(&a.done, hipEventDisableTiming)) != hipSuccess) return e;
+    if (bytes > a.bytes) {
+        if (a.used && (e = hipEventSynchronize(a.done)) != hipSuccess) return e;
+        const size_t want = std::max(bytes, a.bytes + a.bytes / 4);
+        if (a.ptr) (void)hipFree(a.ptr);
+        a.ptr = nullptr;
+        a.bytes = 0;
+        if ((e = hipMalloc(&a.ptr, want)) != hipSuccess) {
+            a.ptr = nullptr;
+            return e;
+        }
+        a.bytes = want;
+    } else if (a.used && a.last != s) {
+        if ((e = hipStreamWaitEvent(s, a.done, 0)) != hipSuccess) return e;
+    }
+    *out = a.ptr;
+    return hipSuccess;
+}
+
+// With a.mu held: marks the end of the call's kernels on s.
+hipError_t arena_release(Arena &a, hipStream_t s) {
+    a.used = true;
+    a.last = s;
+    return hipEventRecord(a.done, s);
+}
+
+void arena_free(Arena &a) {
+    if (a.done) (void)hipEventDestroy(a.done);
+    if (a.ptr) (void)hipFree(a.ptr);
+    a.done = nullptr;
+    a.ptr = nullptr;
+    a.bytes = 0;
+    a.used = false;
+}
+
 }  // namespace
 
 struct emo_graph_s {
@@ -134,7 +187,7 @@ struct emo_graph_s {
     bool chain_slack = false;
     int chain_state = 0;                     // 0 not tried, 1 compiled, -1 failed
     emo::JitModule jc;
-    hipMemPool_t pool = nullptr;             // per-call scratch (kept between calls)
+    Arena arena;                             // per-call scratch, kept between calls
     // profiling hook (hipEvent_t handles owned by the caller)
     hipEvent_t ev_begin = nullptr;
     hipEvent_t ev_end = nullptr;
@@ -475,8 +528,7 @@ void release_device(emo_graph_s *g) {
         emo::jit_unload(&g->jm);
         emo::jit_unload(&g->jc);
         for (void *p : g->allocations) (void)hipFree(p);
-        if (g->pool) (void)hipMemPoolDestroy(g->pool);
-        g->pool = nullptr;
+        arena_free(g->arena);
     }
     g->allocations.clear();
 }
@@ -545,9 +597,7 @@ int ensure_jit(emo_graph_s *g) {
 }
 
 emo::ChainPlan chain_plan(const emo_graph_s &g) {
-    emo::ChainPlan cp = emo::jit_chain_plan(g.jg, g.chain_slack, kChainSegOps, kChainSubOps);
-    cp.block = 256;
-    return cp;
+    return emo::jit_chain_plan(g.jg, g.chain_slack, kChainSegOps, kChainSubOps);
 }
 
 // Generates and compiles the segmented kernels once; returns 1 when they are ready.
@@ -745,17 +795,11 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
         std::vector<float2> tab(static_cast<size_t>(P) * F + emo::kTablePad, make_float2(0.f, 0.f));
         for (size_t i = 0; i < static_cast<size_t>(P) * F; ++i)
             tab[i] = make_float2(pack_time[i], pack_energy[i]);
-        hipMemPoolProps props{};
-        props.allocType = hipMemAllocationTypePinned;
-        props.location.type = hipMemLocationTypeDevice;
-        props.location.id = device;
-        hipError_t perr = hipMemPoolCreate(&g->pool, &props);
-        if (perr != hipSuccess) return device_fail(perr, "hipMemPoolCreate");
-        uint64_t keep = UINT64_MAX;   // keep freed scratch for the next call
-        perr = hipMemPoolSetAttribute(g->pool, hipMemPoolAttrReleaseThreshold, &keep);
-        if (perr != hipSuccess) return device_fail(perr, "hipMemPoolSetAttribute");
         g->dg.V = V; g->dg.P = P; g->dg.F = F; g->dg.static_power = static_power;
         if ((s = upload(*g, tab, &g->dg.tab)) != EMO_OK) return s;
+        std::vector<float> tabt(tab.size());
+        for (size_t i = 0; i < tab.size(); ++i) tabt[i] = tab[i].x;
+        if ((s = upload(*g, tabt, &g->dg.tabt)) != EMO_OK) return s;
         if ((s = upload_program(*g, pe, g->dg.eval)) != EMO_OK) return s;
         if ((s = upload_program(*g, ps, g->dg.slack_pack)) != EMO_OK) return s;
         if ((s = upload_program(*g, pn, g->dg.slack_node)) != EMO_OK) return s;
@@ -838,6 +882,14 @@ emo_status emo_graph_topo_order(emo_graph_t g, int32_t *order, int32_t *depth) {
 
 namespace {
 
+constexpr int kMaxDevices = 64;
+
+// Scratch of calls that have no graph handle, one arena per device.
+Arena &device_arena(int dev) {
+    static Arena arenas[kMaxDevices];
+    return arenas[dev];
+}
+
 // The hot path for every batch entry point: forward pass, optional backward slack pass,
 // optional feasibility mask and selection, in one kernel launch (plus the initialisation of the
 // selection accumulator).
@@ -865,45 +917,51 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     const int64_t nblocks = path == Path::kSingle  ? emo::jit_blocks(g->jm, B)
                             : path == Path::kChain ? emo::jit_chain_blocks(g->jc, B)
                                                    : emo::forward_blocks(B);
+    const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
     size_t part_bytes = result ? static_cast<size_t>(nblocks) * emo::kPartialBytes : 0;
     part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
-    size_t scratch_bytes = part_bytes;
-    if (path == Path::kChain)
-        scratch_bytes += emo::chain_scratch_bytes(g->jc.plan, nblocks * g->jc.plan.block);
+    size_t work_bytes = 0;
+    if (path == Path::kChain) work_bytes = emo::chain_scratch_bytes(g->jc.plan, B);
+    else if (path == Path::kInterpreted)
+        work_bytes = slack ? emo::slack_scratch_bytes(prog, B) : emo::forward_scratch_bytes(g->dg.eval, B);
+    std::lock_guard<std::mutex> lock(g->arena.mu);
     void *scratch = nullptr;
-    if (scratch_bytes) {
-        hipError_t ea = hipMallocFromPoolAsync(&scratch, scratch_bytes, g->pool, st);
-        if (ea != hipSuccess) return fail(EMO_ERR_OUT_OF_MEMORY, "scratch of %zu bytes: %s", scratch_bytes, hipGetErrorString(ea));
+    if (part_bytes + work_bytes > 0) {
+        hipError_t ea = arena_acquire(g->arena, part_bytes + work_bytes, st, &scratch);
+        if (ea != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(EMO_ERR_OUT_OF_MEMORY, "scratch of %zu bytes: %s", part_bytes + work_bytes,
+                        hipGetErrorString(ea));
+        }
     }
     void *part = result ? scratch : nullptr;
-    void *chain_scratch = static_cast<char *>(scratch) + part_bytes;
+    void *work = scratch ? static_cast<char *>(scratch) + part_bytes : nullptr;
     g->info.last_kernels = static_cast<int32_t>(path);
     hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
     if (e == hipSuccess) {
         if (path == Path::kChain) {
-            e = emo::jit_launch_chain(g->jc, levels, B, g->dg.tab, chain_scratch, slack, makespan,
+            e = emo::jit_launch_chain(g->jc, levels, B, g->dg.tab, g->dg.tabt, work, slack, makespan,
                                       energy, target, mask, part, st);
         } else if (slack) {
             if (path == Path::kSingle) {
                 e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy,
                                           target, mask, part, st);
             } else {
-                const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
                 e = emo::launch_slack(g->dg, prog, per_node ? g->V : g->P, levels, B, slack,
-                                      makespan, energy, target, mask, part, st);
+                                      makespan, energy, target, mask, part, work, st);
             }
         } else if (path == Path::kSingle) {
             e = emo::jit_launch_forward(g->jm, levels, B, g->dg.tab, makespan, energy, target,
                                         mask, part, st);
         } else {
-            e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, part, st);
+            e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, part, work, st);
         }
     }
     if (e == hipSuccess && g->ev_end) e = hipEventRecord(g->ev_end, st);
     if (result && e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
     if (scratch) {
-        hipError_t ef = hipFreeAsync(scratch, st);
-        if (e == hipSuccess) e = ef;
+        hipError_t er = arena_release(g->arena, st);
+        if (e == hipSuccess) e = er;
     }
     return after_launch(e, "evaluation");
 }
@@ -950,13 +1008,23 @@ emo_status emo_select_from_results(const float *makespan, const float *energy, i
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (B == 0) return after_launch(emo::launch_empty_result(result, st), "emo_select_from_results");
     const int64_t nblocks = emo::forward_blocks(B);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return fail(EMO_ERR_DEVICE, "no usable current device (%d)", dev);
+    // selection partials live in a per-device arena (kept until the process ends)
+    Arena &a = device_arena(dev);
+    std::lock_guard<std::mutex> lock(a.mu);
     void *part = nullptr;
-    hipError_t e = hipMallocAsync(&part, static_cast<size_t>(nblocks) * emo::kPartialBytes, st);
-    if (e != hipSuccess) return fail(EMO_ERR_OUT_OF_MEMORY, "hipMallocAsync: %s", hipGetErrorString(e));
+    e = arena_acquire(a, static_cast<size_t>(nblocks) * emo::kPartialBytes, st, &part);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(EMO_ERR_OUT_OF_MEMORY, "scratch: %s", hipGetErrorString(e));
+    }
     e = emo::launch_select_results(makespan, energy, B, latency_target, feasible_mask, part, st);
     if (e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
-    hipError_t ef = hipFreeAsync(part, st);
-    if (e == hipSuccess) e = ef;
+    hipError_t er = arena_release(a, st);
+    if (e == hipSuccess) e = er;
     return after_launch(e, "emo_select_from_results");
 }
 

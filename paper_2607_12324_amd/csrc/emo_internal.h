@@ -64,6 +64,7 @@ struct DevGraph {
     int32_t V = 0, P = 0, F = 1;
     float static_power = 0.f;
     const float2 *tab = nullptr;   // [P*F + kTablePad] interleaved (time, energy)
+    const float *tabt = nullptr;   // [P*F + kTablePad] times only (backward passes)
     DevProgram eval;               // forward over candidate-dependent nodes
     DevProgram slack_pack;         // forward + backward over candidate-dependent nodes
     DevProgram slack_node;         // forward + backward over every node
@@ -75,11 +76,16 @@ constexpr size_t kPartialBytes = 16;
 
 // Interpreting kernels.  T, E, mask, part may each be NULL; `part` receives one selection
 // partial record per block (forward_blocks(B) of them).
+// Device scratch (bytes) the interpreting kernels need for B candidates: cold slots, and for
+// slack the forward finish times kept for the backward pass.  The caller passes that much
+// (256-byte aligned) as `scratch`.
+size_t forward_scratch_bytes(const DevProgram &prog, int64_t B);
+size_t slack_scratch_bytes(const DevProgram &prog, int64_t B);
 hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
-                          float target, uint32_t *mask, void *part, hipStream_t s);
+                          float target, uint32_t *mask, void *part, void *scratch, hipStream_t s);
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
-                        float target, uint32_t *mask, void *part, hipStream_t s);
+                        float target, uint32_t *mask, void *part, void *scratch, hipStream_t s);
 int64_t forward_blocks(int64_t B);
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s);
 hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selection *res,
@@ -129,15 +135,18 @@ struct ChainPlan {
     std::vector<int32_t> bk_row;    // row of s_i (latest start) read by an earlier segment, or -1
     int32_t n_ck = 0, n_bk = 0;
     bool slack = false;
-    bool staged = false;            // slack written through LDS in 16-pack chunks
-    int block = 256;
+    bool staged = false;            // slack written through LDS as 128-byte lines (16-byte stores)
+    int block = 256;                // workgroup of the forward kernels
+    int bblock = 512;               // workgroup of the backward kernels
     int segments() const { return static_cast<int>(seg.size()) - 1; }
 };
 
-// Scratch layout of one chained evaluation (floats unless noted), each [rows][bp]:
+// Scratch layout of one chained evaluation (floats unless noted), each [rows][bp] with the
+// pitch bp = chain_pitch(B):
 //   ck [n_ck], bk [n_bk], Tc (makespan so far) [1], Ebc (open fp32 energy block) [1],
 //   Edc (fp64 energy sum) [1, doubles]
-size_t chain_scratch_bytes(const ChainPlan &cp, int64_t bp);
+inline int64_t chain_pitch(int64_t B) { return (B + 63) / 64 * 64; }
+size_t chain_scratch_bytes(const ChainPlan &cp, int64_t B);
 
 struct JitModule {
     hipModule_t module = nullptr;
@@ -164,8 +173,9 @@ int64_t jit_chain_blocks(const JitModule &m, int64_t B);
 // Forward kernels (and, with S, the backward kernels) of a chained evaluation.  scratch holds
 // chain_scratch_bytes(plan, jit_chain_blocks * block) bytes.
 hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B,
-                            const float2 *tab, void *scratch, float *S, float *T, float *E,
-                            float target, uint32_t *mask, void *part, hipStream_t s);
+                            const float2 *tab, const float *tabt, void *scratch, float *S,
+                            float *T, float *E, float target, uint32_t *mask, void *part,
+                            hipStream_t s);
 // 0 on success; otherwise *log holds the compiler's or loader's message.
 int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log);
 void jit_unload(JitModule *m);

@@ -262,6 +262,7 @@ struct RangeOpts {
     long long base_pack = 0, tab_end = 0;          // table window (LevelPlan)
     bool declare_row = true, preload = true;
     bool checks = true;                            // record invalid level bytes in `bad`
+    bool time_only = false;                        // `tab` holds times only (floats)
 };
 
 // Forward walk over steps [a, b) (Eq. 1): declares f<i> for each of them (values of earlier
@@ -300,8 +301,13 @@ LevelPlan emit_forward_range(std::ostringstream &o, const JitGraph &g, const Ran
         if (op.pack >= 0) {
             std::string b = lp.byte_of(op.pack);
             if (level_expr) (*level_expr)[i] = b;
-            o << "  const float2 te" << i << " = tab[" << lp.row_entry(op.pack) << " + " << b << "];\n";
-            o << "  float f" << i << " = " << est_expr(g, i, "f") << " + te" << i << ".x;\n";
+            if (r.time_only) {
+                o << "  float f" << i << " = " << est_expr(g, i, "f") << " + tab[" << lp.row_entry(op.pack)
+                  << " + " << b << "];\n";
+            } else {
+                o << "  const float2 te" << i << " = tab[" << lp.row_entry(op.pack) << " + " << b << "];\n";
+                o << "  float f" << i << " = " << est_expr(g, i, "f") << " + te" << i << ".x;\n";
+            }
             if (r.accumulate) {
                 o << "  eb += te" << i << ".y;\n";
                 if (++npk % 64 == 0) o << "  ed += (double)eb;\n  eb = 0.f;\n";
@@ -512,26 +518,43 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
 
 // ------------------------------------------------------------------ segmented kernels
 
+namespace {
+constexpr int kChainSegPacks = 256;        // packs per segment kernel at most (table window)
+}  // namespace
+
 ChainPlan jit_chain_plan(const JitGraph &g, bool with_slack, int seg_ops, int sub_ops) {
     ChainPlan cp;
     cp.slack = with_slack;
     const int n = static_cast<int>(g.ops.size());
+    std::vector<int> npk_before(n + 1, 0);
+    for (int i = 0; i < n; ++i) npk_before[i + 1] = npk_before[i] + (g.ops[i].pack >= 0 ? 1 : 0);
+    // Segments end where the pack steps so far are a multiple of 64 (energy blocks and slack
+    // chunks never straddle two kernels), after seg_ops steps or kChainSegPacks packs (the
+    // table window of a kernel); a short tail joins the last segment when the packs allow.
     cp.seg.push_back(0);
-    int npk = 0, start = 0;
-    for (int i = 0; i < n; ++i) {
-        if (g.ops[i].pack >= 0) ++npk;
-        // segments end where the pack steps so far are a multiple of 64: energy blocks and
-        // 16-pack slack chunks never straddle two kernels
-        if (i + 1 < n && i + 1 - start >= seg_ops && n - (i + 1) >= seg_ops / 2 && npk % 64 == 0) {
-            cp.seg.push_back(i + 1);
-            start = i + 1;
-        }
+    for (int i = 0, start = 0; i + 1 < n; ++i) {
+        const int c = i + 1;
+        if (npk_before[c] % 64 != 0) continue;
+        const int packs = npk_before[c] - npk_before[start];
+        if (c - start < seg_ops && packs < kChainSegPacks) continue;
+        const int rest_ops = n - c, rest_packs = npk_before[n] - npk_before[c];
+        if (rest_ops < seg_ops / 4 && packs + rest_packs <= kChainSegPacks) continue;
+        cp.seg.push_back(c);
+        start = c;
     }
     cp.seg.push_back(n);
     std::vector<int> seg_of(n), sub_of(n);
     for (int j = 0; j + 1 < static_cast<int>(cp.seg.size()); ++j) {
-        for (int c = cp.seg[j]; c < cp.seg[j + 1]; c += sub_ops) cp.sub.push_back(c);
-        for (int i = cp.seg[j]; i < cp.seg[j + 1]; ++i) seg_of[i] = j;
+        // sub-segments of at least sub_ops steps, cut where the pack steps so far are a multiple
+        // of 32, so that a 32-pack slack chunk never waits across two of them
+        const int a = cp.seg[j], b = cp.seg[j + 1];
+        cp.sub.push_back(a);
+        for (int c = a + 1, start = a; c < b; ++c)
+            if (c - start >= sub_ops && npk_before[c] % 32 == 0) {
+                cp.sub.push_back(c);
+                start = c;
+            }
+        for (int i = a; i < b; ++i) seg_of[i] = j;
     }
     cp.sub.push_back(n);
     for (int r = 0; r + 1 < static_cast<int>(cp.sub.size()); ++r)
@@ -555,15 +578,16 @@ ChainPlan jit_chain_plan(const JitGraph &g, bool with_slack, int seg_ops, int su
             if (earlier) cp.bk_row[i] = cp.n_bk++;
         }
     }
-    cp.staged = with_slack && g.pack_monotone && g.P % 16 == 0;
+    cp.staged = with_slack && g.pack_monotone && g.P % 32 == 0;
+    cp.block = 256;
+    cp.bblock = 512;
     return cp;
 }
 
 namespace {
 
-constexpr int kChainStage = 16;                        // slack staging chunk (packs)
 constexpr size_t kChainLdsForward = 48 * 1024;         // table window budget, forward kernels
-constexpr size_t kChainLdsBackward = 48 * 1024;        // table window budget, backward kernels
+constexpr size_t kChainLdsBackward = 16 * 1024;        // times window budget, backward kernels
 
 // Table window of one kernel: the rows of the packs its steps visit, staged in LDS when they
 // fit, else the whole table in device memory.
@@ -572,7 +596,7 @@ struct TabWindow {
     long long base_pack = 0, entries = 0, tab_end = 0;
 };
 
-TabWindow chain_window(const JitGraph &g, int a, int b, size_t budget) {
+TabWindow chain_window(const JitGraph &g, int a, int b, size_t budget, size_t entry_bytes) {
     int lo = g.P, hi = -1;
     for (int i = a; i < b; ++i)
         if (g.ops[i].pack >= 0) {
@@ -584,7 +608,7 @@ TabWindow chain_window(const JitGraph &g, int a, int b, size_t budget) {
     if (hi < 0) return w;
     const long long rows = static_cast<long long>(hi - lo + 1) * g.F;
     const long long ent = rows + (is_pow2(g.F) ? 0 : kTablePad);
-    if (static_cast<size_t>(ent) * 8 > budget) return w;
+    if (static_cast<size_t>(ent) * entry_bytes > budget) return w;
     w.lds = true;
     w.base_pack = lo;
     w.entries = ent;
@@ -592,12 +616,12 @@ TabWindow chain_window(const JitGraph &g, int a, int b, size_t budget) {
     return w;
 }
 
-void emit_table(std::ostringstream &o, const JitGraph &g, const TabWindow &w) {
+void emit_table(std::ostringstream &o, const JitGraph &g, const TabWindow &w, const char *type) {
     if (!w.lds) {
-        o << "  const float2 *__restrict__ tab = tabg;\n";
+        o << "  const " << type << " *__restrict__ tab = tabg;\n";
         return;
     }
-    o << "  __shared__ float2 tab[" << w.entries << "];\n"
+    o << "  __shared__ " << type << " tab[" << w.entries << "];\n"
       << "  for (int i_ = threadIdx.x; i_ < " << w.entries << "; i_ += EMO_BLOCK) tab[i_] = tabg["
       << w.base_pack * g.F << "LL + i_];\n"
       << "  __syncthreads();\n";
@@ -606,14 +630,18 @@ void emit_table(std::ostringstream &o, const JitGraph &g, const TabWindow &w) {
 // Lane setup of a segmented kernel.  Scratch row r is addressed as a uniform base
 // (buf + r * bp) plus the lane's 32-bit byte offset o4 (bp * 4 < 2^32), which the compiler
 // folds into one load or store with a scalar base.
-const char *kChainLanes =
-    "  const unsigned int g32 = blockIdx.x * EMO_BLOCK + threadIdx.x;\n"
-    "  const unsigned int o4 = g32 * 4u;\n"
-    "  const long long gid = g32;\n"
-    "  const long long bp = (long long)gridDim.x * EMO_BLOCK;\n"
-    "  const bool active = gid < B;\n"
-    "  const long long cand = active ? gid : B - 1;\n"
-    "  (void)active; (void)bp;\n";
+// Lanes past the batch evaluate the last candidate (cand = B - 1) again and use its scratch
+// slot: they compute and store exactly its values, so no store needs a branch.
+std::string chain_lanes(int block) {
+    std::ostringstream o;
+    o << "  const unsigned int g32 = blockIdx.x * " << block << "u + threadIdx.x;\n"
+         "  const long long gid = g32;\n"
+         "  const bool active = gid < B;\n"
+         "  const long long cand = active ? gid : B - 1;\n"
+         "  const unsigned int o4 = (unsigned int)cand * 4u;\n"
+         "  (void)active;\n";
+    return o.str();
+}
 
 // Steps before `a` whose finish times steps [a, b) read.
 std::vector<int> inputs_before(const JitGraph &g, int a, int b) {
@@ -633,21 +661,21 @@ void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPla
     for (int i = 0; i < b; ++i)
         if (g.ops[i].pack >= 0) (i < a ? npk0 : npk1)++;
     npk1 += npk0;
-    const TabWindow w = chain_window(g, a, b, kChainLdsForward);
+    const TabWindow w = chain_window(g, a, b, kChainLdsForward, sizeof(float) * 2);
     o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
-      << "emo_cf" << j << "(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
-         "    float *__restrict__ ck, float *__restrict__ Tc, double *__restrict__ Edc,\n"
-         "    float *__restrict__ Ebc, int full, float *__restrict__ To, float *__restrict__ Eo,\n"
-         "    float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n";
-    emit_table(o, g, w);
-    o << kChainLanes;
+      << "emo_cf" << j << "(const u8 *__restrict__ lv, long long B, long long bp,\n"
+         "    const float2 *__restrict__ tabg, float *__restrict__ ck, float *__restrict__ Tc,\n"
+         "    double *__restrict__ Edc, float *__restrict__ Ebc, int full, float *__restrict__ To,\n"
+         "    float *__restrict__ Eo, float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n";
+    emit_table(o, g, w, "float2");
+    o << chain_lanes(cp.block);
     o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
     o << "  unsigned int bad = 0u;\n  (void)full;\n";
     if (j == 0) {
         o << "  float T = " << flit(g.t_const) << ";\n  float eb = 0.f;\n  double ed = 0.0;\n";
     } else {
-        o << "  float T = Tc[g32];\n  double ed = Edc[g32];\n";
-        o << "  float eb = " << (npk0 % 64 ? "Ebc[g32]" : "0.f") << ";\n";
+        o << "  float T = Tc[cand];\n  double ed = Edc[cand];\n";
+        o << "  float eb = " << (npk0 % 64 ? "Ebc[cand]" : "0.f") << ";\n";
     }
     for (int k : inputs_before(g, a, b))
         o << "  const float f" << k << " = EMO_AT(ck, " << cp.ck_row[k] << ");\n";
@@ -663,41 +691,85 @@ void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPla
     LevelPlan lp = emit_forward_range(o, g, r, nullptr);
     if (!last) {
         o << "  if ((bad & " << lp.bad_bits() << ") != 0u) ed = (double)EMO_NAN;\n";
-        o << "  Tc[g32] = T;\n  Edc[g32] = ed;\n";
-        if (npk1 % 64) o << "  Ebc[g32] = eb;\n";
+        o << "  Tc[cand] = T;\n  Edc[cand] = ed;\n";
+        if (npk1 % 64) o << "  Ebc[cand] = eb;\n";
     } else {
         emit_forward_finish(o, g, lp, j > 0);
-        o << "  Tc[g32] = T;\n"
+        o << "  Tc[cand] = T;\n"
              "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n"
              "  if (mask || part) emo_select_block(active, T, E, cand, B, target, mask, part);\n";
     }
     o << "}\n\n";
 }
 
+// Slack staging of the backward kernels: the slack of packs [p0, p0 + 32) of the wave's 64
+// candidates is collected in LDS as an unpadded 32 x 64 tile (8 KB), element (k, r) at
+// k * 64 + (r ^ (8 * (k / 4))), then written with 16-byte stores in which 8 lanes cover one
+// candidate's 128-byte line.  The XOR keeps both sides free of bank conflicts: a lane writes
+// its column (k fixed), and a read of piece b (packs 4b..4b+3) by 64 lanes touches 8 rows
+// r = 8m..8m+7 of 8 different swizzles.  Values of a bad candidate are already NaN.
+std::string chain_flush_source(int P) {
+    std::ostringstream o;
+    o << R"(
+__device__ __forceinline__ void emo_cflush(const float *stg, float *__restrict__ S,
+                                           long long wbase, long long B, int p0) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int lane = threadIdx.x % EMO_WAVE;
+  const int b = lane % 8;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const int r = 8 * m + lane / 8;
+    const int sw = r ^ (8 * b);
+    float4 v;
+    v.x = stg[(4 * b + 0) * 64 + sw];
+    v.y = stg[(4 * b + 1) * 64 + sw];
+    v.z = stg[(4 * b + 2) * 64 + sw];
+    v.w = stg[(4 * b + 3) * 64 + sw];
+    long long row = wbase + r;
+    row = row < B ? row : B - 1;   // lanes past the batch hold candidate B - 1's values
+    *(float4 *)(S + row * )" << P << R"(LL + p0 + 4 * b) = v;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+)";
+    return o.str();
+}
+
 void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPlan &cp, int j) {
     const int a = cp.seg[j], b = cp.seg[j + 1];
-    const TabWindow w = chain_window(g, a, b, kChainLdsBackward);
-    o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
-      << "emo_cb" << j << "(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
-         "    const float *__restrict__ ck, const float *__restrict__ Tc, float *__restrict__ bk,\n"
-         "    float *__restrict__ S) {\n";
-    emit_table(o, g, w);
-    o << kChainLanes;
+    const TabWindow w = chain_window(g, a, b, kChainLdsBackward, sizeof(float));
+    // 4 waves per SIMD: two workgroups of 8 waves share a CU's LDS (staging + times window)
+    o << "extern \"C\" __global__ void __launch_bounds__(" << cp.bblock
+      << ") __attribute__((amdgpu_waves_per_eu(4)))\n"
+      << "emo_cb" << j << "(const u8 *__restrict__ lv, long long B, long long bp,\n"
+         "    const float *__restrict__ tabg, const float *__restrict__ ck,\n"
+         "    const float *__restrict__ Tc, float *__restrict__ bk, float *__restrict__ S) {\n";
+    if (w.lds) {
+        o << "  __shared__ float tab[" << w.entries << "];\n"
+          << "  for (int i_ = threadIdx.x; i_ < " << w.entries << "; i_ += " << cp.bblock << ") tab[i_] = tabg["
+          << w.base_pack * g.F << "LL + i_];\n"
+          << "  __syncthreads();\n";
+    } else {
+        o << "  const float *__restrict__ tab = tabg;\n";
+    }
+    o << chain_lanes(cp.bblock);
     o << "  const int lane = threadIdx.x % EMO_WAVE;\n"
          "  const int wave = threadIdx.x / EMO_WAVE;\n"
-         "  const long long wbase = (long long)blockIdx.x * EMO_BLOCK + wave * EMO_WAVE;\n"
+         "  const long long wbase = (long long)blockIdx.x * " << cp.bblock << " + wave * EMO_WAVE;\n"
          "  (void)lane; (void)wbase;\n";
     if (cp.staged) {
-        o << "  __shared__ float stg_all[EMO_WAVES_PER_BLOCK][EMO_KC * 65];\n"
-             "  __shared__ unsigned int bad_all[EMO_WAVES_PER_BLOCK][EMO_WAVE];\n"
-             "  float *stg = stg_all[wave];\n"
-             "  unsigned int *stg_bad = bad_all[wave];\n";
+        o << "  __shared__ float stg_all[" << cp.bblock / 64 << "][32 * 64];\n"
+             "  float *stg = stg_all[wave];\n";
     }
     o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
+    o << "  float *__restrict__ srow = S + cand * " << g.P << "LL;\n  (void)srow;\n";
     o << LevelPlan::row_decl(jit_level_width(g));
-    o << "  const float T = Tc[g32];\n  const bool isbad = T != T;\n"
+    o << "  const float T = Tc[cand];\n  const bool isbad = T != T;\n"
          "  const float Tb = isbad ? 0.f : T;\n";
-    if (cp.staged) o << "  stg_bad[lane] = isbad ? 1u : 0u;\n";
     o << "  unsigned int zb = 0u;\n  __asm__ __volatile__(\"\" : \"+v\"(zb));\n";
     o << "  unsigned int bad = 0u;\n";
     // latest start times of later segments' steps that this segment's steps precede
@@ -730,13 +802,26 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
         ro.declare_row = false;
         ro.preload = false;
         ro.checks = false;
+        ro.time_only = true;
         LevelPlan lp = emit_forward_range(o, g, ro, &level_expr);
         lp.launder();
         for (int i = d - 1; i >= c; --i) {
             const JitOp &op = g.ops[i];
-            // table reads index through zb, which passes through an empty asm every 16 steps:
-            // the reads of later steps cannot be hoisted (each would hold a VGPR meanwhile)
-            if ((d - 1 - i) % 16 == 0) o << "  __asm__ __volatile__(\"\" : \"+v\"(zb));\n";
+            // table reads index through zb, and level bytes are extracted from words, that pass
+            // through an empty asm every 16 steps: neither can be hoisted (each would hold a VGPR
+            // from there on)
+            if ((d - 1 - i) % 16 == 0) {
+                std::vector<std::string> ops = {"zb"};
+                if (lp.width > 1)
+                    for (int k = i; k > i - 16 && k >= c; --k)
+                        if (g.ops[k].pack >= 0) {
+                            const std::string wd = lp.pfx + std::to_string(g.ops[k].pack / lp.width);
+                            if (std::find(ops.begin(), ops.end(), wd) == ops.end()) ops.push_back(wd);
+                        }
+                o << "  __asm__ __volatile__(\"\" :";
+                for (size_t k = 0; k < ops.size(); ++k) o << (k ? ", " : " ") << "\"+v\"(" << ops[k] << ")";
+                o << ");\n";
+            }
             std::string lft;
             if (op.out.empty()) {
                 lft = "Tb";
@@ -753,7 +838,7 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
             if (op.pack >= 0) {
                 const std::string lv = lp.width == 1 ? lp.reload_byte(op.pack) : level_expr[i];
                 o << "  const float t" << i << " = tab[zb + " << lp.row_entry(op.pack) << " + "
-                  << lv << "].x;\n";
+                  << lv << "];\n";
                 dur = "t" + std::to_string(i);
             }
             if (!op.in.empty()) {
@@ -762,12 +847,13 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
             }
             if (op.pack >= 0) {
                 const int p = op.pack;
+                const std::string v = "isbad ? EMO_NAN : lf" + std::to_string(i) + " - f" + std::to_string(i);
                 if (cp.staged) {
-                    o << "  stg[" << (p % kChainStage) * 65 << " + lane] = lf" << i << " - f" << i << ";\n";
-                    if (p % kChainStage == 0) o << "  emo_flush(stg, stg_bad, S, wbase, B, " << p << ");\n";
+                    const int k = p % 32;
+                    o << "  stg[" << k * 64 << " + (lane ^ " << 8 * (k / 4) << ")] = " << v << ";\n";
+                    if (k == 0) o << "  emo_cflush(stg, S, wbase, B, " << p << ");\n";
                 } else {
-                    o << "  if (active) S[cand * " << g.P << "LL + " << p
-                      << "] = isbad ? EMO_NAN : lf" << i << " - f" << i << ";\n";
+                    o << "  srow[" << p << "] = " << v << ";\n";
                 }
             }
         }
@@ -781,15 +867,16 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
 std::string jit_generate_chain(const JitGraph &g, const ChainPlan &cp) {
     std::ostringstream o;
     o << "#define EMO_BLOCK " << cp.block << "\n" << kPrelude << kEmoSelectSource << "\n";
-    if (cp.staged) o << "#define EMO_KC " << kChainStage << "\n" << flush_source(g.P);
+    if (cp.staged) o << chain_flush_source(g.P);
     for (int j = 0; j < cp.segments(); ++j) emit_chain_forward(o, g, cp, j);
     if (cp.slack)
         for (int j = 0; j < cp.segments(); ++j) emit_chain_backward(o, g, cp, j);
     return o.str();
 }
 
-size_t chain_scratch_bytes(const ChainPlan &cp, int64_t bp) {
-    return static_cast<size_t>(bp) * (4 * static_cast<size_t>(cp.n_ck + cp.n_bk + 2) + 8);
+size_t chain_scratch_bytes(const ChainPlan &cp, int64_t B) {
+    const size_t bp = static_cast<size_t>(chain_pitch(B));
+    return bp * (4 * static_cast<size_t>(cp.n_ck + cp.n_bk + 2) + 8);
 }
 
 namespace {
@@ -899,11 +986,13 @@ hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t
 int64_t jit_chain_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.plan.block); }
 
 hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B,
-                            const float2 *tab, void *scratch, float *S, float *T, float *E,
-                            float target, uint32_t *mask, void *part, hipStream_t s) {
+                            const float2 *tab, const float *tabt, void *scratch, float *S,
+                            float *T, float *E, float target, uint32_t *mask, void *part,
+                            hipStream_t s) {
     const ChainPlan &cp = m.plan;
     const unsigned grid = grid_of(B, cp.block);
-    const int64_t bp = static_cast<int64_t>(grid) * cp.block;
+    const unsigned bgrid = grid_of(B, cp.bblock);
+    long long bp = chain_pitch(B);
     float *ck = static_cast<float *>(scratch);
     float *bk = ck + static_cast<size_t>(cp.n_ck) * bp;
     float *Tc = bk + static_cast<size_t>(cp.n_bk) * bp;
@@ -918,15 +1007,15 @@ hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B
         float *Eo = last ? E : nullptr;
         uint32_t *mk = last ? mask : nullptr;
         void *pt = last ? part : nullptr;
-        void *args[] = {&levels, &b, &tab, &ck, &Tc, &Edc, &Ebc, &full, &To, &Eo, &target, &mk, &pt};
+        void *args[] = {&levels, &b, &bp, &tab, &ck, &Tc, &Edc, &Ebc, &full, &To, &Eo, &target, &mk, &pt};
         hipError_t e = hipModuleLaunchKernel(m.cf[j], grid, 1, 1, cp.block, 1, 1, 0, s, args, nullptr);
         if (e != hipSuccess) return e;
     }
     if (!S) return hipSuccess;
     for (int j = m_seg - 1; j >= 0; --j) {
         const float *ckc = ck, *Tcc = Tc;
-        void *args[] = {&levels, &b, &tab, &ckc, &Tcc, &bk, &S};
-        hipError_t e = hipModuleLaunchKernel(m.cb[j], grid, 1, 1, cp.block, 1, 1, 0, s, args, nullptr);
+        void *args[] = {&levels, &b, &bp, &tabt, &ckc, &Tcc, &bk, &S};
+        hipError_t e = hipModuleLaunchKernel(m.cb[j], bgrid, 1, 1, cp.bblock, 1, 1, 0, s, args, nullptr);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

@@ -457,16 +457,21 @@ int table_mode(const DevGraph &g, const DevProgram &prog, size_t other_lds, size
 
 int64_t forward_blocks(int64_t B) { return grid_for(B); }
 
+size_t forward_scratch_bytes(const DevProgram &prog, int64_t B) {
+    return static_cast<size_t>(prog.n_cold) * static_cast<size_t>(grid_for(B) * kBlock) * sizeof(float);
+}
+
+size_t slack_scratch_bytes(const DevProgram &prog, int64_t B) {
+    const size_t rows = static_cast<size_t>(prog.n_cold) + static_cast<size_t>(prog.n_ops) +
+                        static_cast<size_t>(prog.n_cold_bwd);
+    return rows * static_cast<size_t>(grid_for(B) * kBlock) * sizeof(float);
+}
+
 hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
-                          float target, uint32_t *mask, void *part, hipStream_t s) {
+                          float target, uint32_t *mask, void *part, void *scratch, hipStream_t s) {
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
-    float *cold = nullptr;
-    if (g.eval.n_cold > 0) {
-        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&cold),
-                                      static_cast<size_t>(g.eval.n_cold) * bpad * sizeof(float), s);
-        if (e != hipSuccess) return e;
-    }
+    float *cold = g.eval.n_cold > 0 ? static_cast<float *>(scratch) : nullptr;
     size_t dyn = 0;
     const int mode = table_mode(g, g.eval, 0, &dyn);
     const bool vec = vec_levels(g, levels);
@@ -478,27 +483,18 @@ hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, f
     else if (mode == kTabWindow) hipLaunchKernelGGL(forward_kernel<kTabWindow>, gd, bd, dyn, s, EMO_FWD_ARGS);
     else hipLaunchKernelGGL(forward_kernel<kTabGlobal>, gd, bd, dyn, s, EMO_FWD_ARGS);
 #undef EMO_FWD_ARGS
-    hipError_t e = hipGetLastError();
-    if (cold) {
-        hipError_t e2 = hipFreeAsync(cold, s);
-        if (e == hipSuccess) e = e2;
-    }
-    return e;
+    return hipGetLastError();
 }
 
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
-                        float target, uint32_t *mask, void *part, hipStream_t s) {
+                        float target, uint32_t *mask, void *part, void *scratch, hipStream_t s) {
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
     const size_t n_cold = static_cast<size_t>(prog.n_cold), n_keep = static_cast<size_t>(prog.n_ops),
                  n_cold_b = static_cast<size_t>(prog.n_cold_bwd);
-    float *buf = nullptr;
     const size_t total = (n_cold + n_keep + n_cold_b) * static_cast<size_t>(bpad);
-    if (total > 0) {
-        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&buf), total * sizeof(float), s);
-        if (e != hipSuccess) return e;
-    }
+    float *buf = total > 0 ? static_cast<float *>(scratch) : nullptr;
     float *cold = buf;
     float *keep = buf ? buf + n_cold * bpad : nullptr;
     float *cold_b = buf ? keep + n_keep * bpad : nullptr;
@@ -520,12 +516,7 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
     else if (staged) hipLaunchKernelGGL((slack_kernel<kTabGlobal, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
     else hipLaunchKernelGGL((slack_kernel<kTabGlobal, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
 #undef EMO_SLACK_ARGS
-    hipError_t e = hipGetLastError();
-    if (buf) {
-        hipError_t e2 = hipFreeAsync(buf, s);
-        if (e == hipSuccess) e = e2;
-    }
-    return e;
+    return hipGetLastError();
 }
 
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s) {

@@ -199,6 +199,42 @@ def test_segmented_kernels(torch, emo, case):
         assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), case
 
 
+@pytest.mark.parametrize("mode", [0, 1], ids=["auto", "interpreted"])
+def test_scratch_reuse_across_streams(torch, emo, mode):
+    """One handle used from two streams with batches that grow and shrink: the calls share the
+    handle's scratch and must still give exactly the single-stream results."""
+    g = synth.packed_graph(9, 1024, 8, 16, sync_every=128, cross_p=0.05)
+    rng = np.random.default_rng(11)
+    sizes = [300, 2000, 64, 4096, 1000, 4096]
+    rows = [pins.random_rows(rng, g, n) for n in sizes]
+    print(f"[case] scratch reuse mode={mode}: sizes={sizes}", flush=True)
+    gh = emo.EmoGraph(g, device=0, kernel_mode=mode)
+    lvs = [dev(torch, r) for r in rows]
+    ref = []
+    for lv in lvs:   # reference: one stream, synchronised after each call
+        S = gh.slack(lv)
+        T, E = gh.eval_policies(lv)
+        torch.cuda.synchronize()
+        ref.append((host(S).copy(), host(T).copy(), host(E).copy()))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = []
+    for i, lv in enumerate(lvs):   # alternate streams without host synchronisation
+        st = streams[i % 2]
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            S = torch.empty((lv.shape[0], g.num_packs), dtype=torch.float32, device="cuda")
+            gh.slack(lv, out=S, stream=st)
+            T, E = gh.eval_policies(lv, stream=st)
+        outs.append((S, T, E))
+    torch.cuda.synchronize()
+    for (S, T, E), (Sr, Tr, Er) in zip(outs, ref):
+        assert np.array_equal(host(S).view(np.uint32), Sr.view(np.uint32))
+        assert np.array_equal(host(T).view(np.uint32), Tr.view(np.uint32))
+        assert np.array_equal(host(E).view(np.uint32), Er.view(np.uint32))
+    T_or, E_or = oracle.eval_batch(g, rows[3], nthreads=8)
+    parity.assert_eval(ref[3][1], ref[3][2], T_or, E_or, True, "scratch reuse")
+
+
 def test_large_slot_count_uses_device_scratch(torch, emo):
     """A wide antichain of packs feeding one sink keeps many finish times live at once."""
     rng = np.random.default_rng(5)

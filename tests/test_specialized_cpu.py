@@ -55,16 +55,36 @@ def kernel_notes(path):
     return dict(zip(names, zip(vgprs, spills)))
 
 
-def check_code_object(path, expect):
+def kernel_bodies(asm: str) -> dict:
+    out, name = {}, None
+    for line in asm.splitlines():
+        m = re.match(r"^[0-9a-f]+ <(\w+)>:", line)
+        if m:
+            name = m.group(1)
+            out[name] = []
+        elif name:
+            out[name].append(line)
+    return out
+
+
+def check_code_object(path, expect, spill_ok=()):
+    """spill_ok: kernels held to 128 VGPRs (4 waves per SIMD) that may keep a few long-lived
+    values in scratch (at most 1 in 100 instructions)."""
     notes = kernel_notes(path)
     for k in expect:
         assert k in notes, (k, notes)
-    for name, (vgpr, spill) in notes.items():
-        assert spill == 0, f"{name} spills {spill} VGPRs"
     asm = subprocess.run([OBJDUMP, "-d", "--mcpu=gfx950", path], capture_output=True, text=True,
                          check=True).stdout
+    bodies = kernel_bodies(asm)
+    for name, (vgpr, spill) in notes.items():
+        if any(name.startswith(p) for p in spill_ok):
+            assert vgpr <= 128, (name, vgpr)
+            n_scr = sum("scratch_" in l for l in bodies[name])
+            assert n_scr <= len(bodies[name]) // 100, f"{name}: {n_scr} scratch accesses"
+        else:
+            assert spill == 0, f"{name} spills {spill} VGPRs"
+            assert not any("scratch_" in l for l in bodies[name]), name
     assert not re.search(r"v_pk_(add|mul|fma)_f32", asm), "packed fp32 arithmetic in specialised kernels"
-    assert "scratch_" not in asm
     # level words and scratch rows are global loads (a flat load would also hold up LDS waits)
     assert "flat_load" not in asm and "flat_store" not in asm
     return notes, asm
@@ -108,7 +128,8 @@ def test_segmented_kernels_compile(emo, hiprtc, tmp_path, which):
     m = len(re.findall(r"\bemo_cf(\d+)\(", src))
     assert m >= 2 and len(re.findall(r"\bemo_cb(\d+)\(", src)) == m
     path = compile_source(hiprtc, src, tmp_path)
-    notes, _ = check_code_object(path, [f"emo_cf{j}" for j in range(m)] + [f"emo_cb{j}" for j in range(m)])
+    notes, _ = check_code_object(path, [f"emo_cf{j}" for j in range(m)] + [f"emo_cb{j}" for j in range(m)],
+                                 spill_ok=("emo_cb",))
     assert max(v for v, _ in notes.values()) <= 128, notes
 
 
