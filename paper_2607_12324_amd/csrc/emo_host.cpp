@@ -589,6 +589,8 @@ int ensure_jit(emo_graph_s *g) {
         return -1;
     }
     m.block = block;
+    // persistent workgroups pay off when each one copies a large table into LDS
+    if (jit_table_bytes(*g) > 16 * 1024) emo::jit_set_caps(&m);
     g->jm = m;
     g->jit_state = 1;
     g->info.specialized |= 1 | (m.slack ? 2 : 0);

@@ -154,6 +154,9 @@ struct JitModule {
     hipFunction_t slack = nullptr;   // only for graphs small enough to keep every finish time
     double compile_seconds = 0.0;
     int block = 256;
+    // resident workgroups of the one-kernel select / slack kernels on the device (their grid,
+    // at most one workgroup per group of `block` candidates, so each loads the table once)
+    int64_t select_cap = 0, slack_cap = 0;
     // segmented kernels
     bool chain = false;
     ChainPlan plan;
@@ -179,8 +182,11 @@ hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B
 // 0 on success; otherwise *log holds the compiler's or loader's message.
 int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log);
 void jit_unload(JitModule *m);
-// Blocks of the specialised kernels' grid for B candidates (one selection partial each).
+// Candidate groups of the one-kernel specialised kernels for B candidates (one selection
+// partial each).
 int64_t jit_blocks(const JitModule &m, int64_t B);
+// Sets select_cap / slack_cap from the occupancy of the compiled kernels (current device).
+void jit_set_caps(JitModule *m);
 // Forward pass; T, E, mask, part may each be NULL.
 hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,
                               const float2 *tab, float *T, float *E, float target, uint32_t *mask,

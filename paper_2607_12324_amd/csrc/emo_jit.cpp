@@ -454,8 +454,12 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
     } else {
         o << "#define EMO_TABLE_DECL const float2 *__restrict__ tab = tabg;\n";
     }
+    // Persistent workgroups: each loads the table once and walks groups of EMO_BLOCK
+    // candidates grp = blockIdx.x, blockIdx.x + gridDim.x, ...
+    o << "#define EMO_GROUP_LOOP \\\n"
+         "  for (long long grp = blockIdx.x; grp * EMO_BLOCK < B; grp += gridDim.x)\n";
     o << "#define EMO_LANE_SETUP \\\n"
-         "  const long long gid = (long long)blockIdx.x * EMO_BLOCK + threadIdx.x; \\\n"
+         "  const long long gid = grp * EMO_BLOCK + threadIdx.x; \\\n"
          "  const bool active = gid < B; \\\n"
          "  long long cand = active ? gid : B - 1; \\\n"
          "  (void)active;\n";
@@ -474,12 +478,12 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
          "emo_sp_select(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
          "              float *__restrict__ To, float *__restrict__ Eo,\n"
          "              float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n"
-         "  EMO_TABLE_DECL\n  EMO_LANE_SETUP\n"
+         "  EMO_TABLE_DECL\n  EMO_GROUP_LOOP {\n  EMO_LANE_SETUP\n"
          "  const EmoFwd r = emo_forward(lv + cand * "
       << g.P << "LL, tab);\n"
          "  if (active) { if (To) To[cand] = r.T; if (Eo) Eo[cand] = r.E; }\n"
-         "  if (mask || part) emo_select_block(active, r.T, r.E, cand, B, target, mask, part);\n"
-         "}\n";
+         "  if (mask || part) emo_select_block(grp, active, r.T, r.E, cand, B, target, mask, part);\n"
+         "  }\n}\n";
 
     if (with_slack) {
         const bool staged = g.pack_monotone && g.P % 16 == 0;
@@ -492,17 +496,19 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
              "emo_sp_slack(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
              "             float *__restrict__ S, float *__restrict__ To, float *__restrict__ Eo,\n"
              "             float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n"
-             "  EMO_TABLE_DECL\n  EMO_LANE_SETUP\n"
+             "  EMO_TABLE_DECL\n"
              "  const int lane = threadIdx.x % EMO_WAVE;\n"
              "  const int wave = threadIdx.x / EMO_WAVE;\n"
-             "  const long long wbase = (long long)blockIdx.x * EMO_BLOCK + wave * EMO_WAVE;\n"
-             "  (void)lane; (void)wbase;\n";
+             "  (void)lane;\n";
         if (staged) {
             o << "  __shared__ float stg_all[EMO_WAVES_PER_BLOCK][EMO_KC * 65];\n"
                  "  __shared__ unsigned int bad_all[EMO_WAVES_PER_BLOCK][EMO_WAVE];\n"
                  "  float *stg = stg_all[wave];\n"
                  "  unsigned int *stg_bad = bad_all[wave];\n";
         }
+        o << "  EMO_GROUP_LOOP {\n  EMO_LANE_SETUP\n"
+             "  const long long wbase = grp * EMO_BLOCK + wave * EMO_WAVE;\n"
+             "  (void)wbase;\n";
         o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
         std::vector<std::string> level_expr(g.ops.size());
         LevelPlan lp = emit_forward(o, g, &level_expr);
@@ -510,8 +516,8 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
         if (staged) o << "  stg_bad[lane] = isbad ? 1u : 0u;\n";
         lp.launder();
         emit_backward(o, g, staged, level_expr);
-        o << "  if (mask || part) emo_select_block(active, T, E, cand, B, target, mask, part);\n";
-        o << "}\n";
+        o << "  if (mask || part) emo_select_block(grp, active, T, E, cand, B, target, mask, part);\n";
+        o << "  }\n}\n";
     }
     return o.str();
 }
@@ -697,7 +703,7 @@ void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPla
         emit_forward_finish(o, g, lp, j > 0);
         o << "  Tc[cand] = T;\n"
              "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n"
-             "  if (mask || part) emo_select_block(active, T, E, cand, B, target, mask, part);\n";
+             "  if (mask || part) emo_select_block(blockIdx.x, active, T, E, cand, B, target, mask, part);\n";
     }
     o << "}\n\n";
 }
@@ -975,12 +981,36 @@ unsigned grid_of(int64_t B, int block) { return static_cast<unsigned>((B + block
 
 int64_t jit_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.block); }
 
+namespace {
+int64_t resident_blocks(hipFunction_t f, int block) {
+    int dev = 0, ncu = 0, nb = 0;
+    if (!f || hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&nb, f, block, 0) != hipSuccess || nb < 1) {
+        (void)hipGetLastError();
+        return 0;   // unknown: one workgroup per group
+    }
+    return static_cast<int64_t>(nb) * ncu;
+}
+
+unsigned capped_grid(int64_t B, int block, int64_t cap) {
+    const int64_t groups = (B + block - 1) / block;
+    return static_cast<unsigned>(cap > 0 ? std::min(groups, cap) : groups);
+}
+}  // namespace
+
+void jit_set_caps(JitModule *m) {
+    m->select_cap = resident_blocks(m->select, m->block);
+    m->slack_cap = resident_blocks(m->slack, m->block);
+}
+
 hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,
                               const float2 *tab, float *T, float *E, float target, uint32_t *mask,
                               void *part, hipStream_t s) {
     long long b = B;
     void *args[] = {&levels, &b, &tab, &T, &E, &target, &mask, &part};
-    return hipModuleLaunchKernel(m.select, grid_of(B, m.block), 1, 1, m.block, 1, 1, 0, s, args, nullptr);
+    return hipModuleLaunchKernel(m.select, capped_grid(B, m.block, m.select_cap), 1, 1, m.block, 1, 1, 0,
+                                 s, args, nullptr);
 }
 
 int64_t jit_chain_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.plan.block); }
@@ -1026,7 +1056,8 @@ hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B
                             void *part, hipStream_t s) {
     long long b = B;
     void *args[] = {&levels, &b, &tab, &S, &T, &E, &target, &mask, &part};
-    return hipModuleLaunchKernel(m.slack, grid_of(B, m.block), 1, 1, m.block, 1, 1, 0, s, args, nullptr);
+    return hipModuleLaunchKernel(m.slack, capped_grid(B, m.block, m.slack_cap), 1, 1, m.block, 1, 1, 0,
+                                 s, args, nullptr);
 }
 
 }  // namespace emo

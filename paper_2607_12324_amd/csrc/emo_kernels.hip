@@ -364,7 +364,7 @@ forward_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float 
         if (T_out) T_out[x.cand] = f.T;
         if (E_out) E_out[x.cand] = f.E;
     }
-    if (mask || part) emo_select_block(x.active, f.T, f.E, x.cand, B, target, mask, part);
+    if (mask || part) emo_select_block(blockIdx.x, x.active, f.T, f.E, x.cand, B, target, mask, part);
 }
 
 // Forward + backward (slack) pass with the same optional outputs.
@@ -389,7 +389,7 @@ slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict_
     float *stg = STAGED ? stg_all[threadIdx.x / kWave] : nullptr;
     run_backward<MODE, STAGED>(pr, tab, g.F, f.bad ? 0.f : f.T, f.bad, row, hot, sc, S, cols, x.cand,
                                x.active, stg, x.wbase, B);
-    if (mask || part) emo_select_block(x.active, f.T, f.E, x.cand, B, target, mask, part);
+    if (mask || part) emo_select_block(blockIdx.x, x.active, f.T, f.E, x.cand, B, target, mask, part);
 }
 
 // ---------------------------------------------------------------- selection (Eq. 4)
@@ -416,7 +416,7 @@ select_results_kernel(const float *__restrict__ T, const float *__restrict__ E, 
     const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const bool active = gid < B;
     const int64_t c = active ? gid : B - 1;
-    emo_select_block(active, T[c], E[c], c, B, target, mask, part);
+    emo_select_block(blockIdx.x, active, T[c], E[c], c, B, target, mask, part);
 }
 
 int64_t grid_for(int64_t B) { return (B + kBlock - 1) / kBlock; }

@@ -5,9 +5,9 @@
 // includes no headers and uses only HIP built-ins.
 //
 // Two stages, with no atomics (thousands of blocks updating one address would serialise):
-//   1. every block of the evaluating kernel writes the mask bits of its candidates and one
-//      partial record: its least key, its number of feasible candidates and the makespan of the
-//      candidate holding that key;
+//   1. for every group of EMO_BLOCK consecutive candidates, the workgroup that evaluates it
+//      writes the mask bits of its candidates and one partial record: its least key, its number
+//      of feasible candidates and the makespan of the candidate holding that key;
 //   2. one block reduces the partial records and writes the emo_selection record.
 // The key of a feasible candidate c is (fp32 bits of its energy) << 32 | c.  Energies are
 // >= 0, so the bit pattern orders like the value and equal energies order by index; an
@@ -45,10 +45,11 @@ __device__ __forceinline__ void emo_wave_min_key(unsigned long long *key, float 
     }
 }
 
-// Stage 1.  Must be called by every thread of the block.  `part` (one record per block) and
-// `mask` may be NULL.
-__device__ void emo_select_block(bool active, float T, float E, long long c, long long B,
-                                 float target, unsigned int *mask, EmoPartial *part) {
+// Stage 1 for the workgroup's current group of EMO_BLOCK consecutive candidates (group index
+// `group`, candidates group * EMO_BLOCK + threadIdx.x).  Must be called by every thread of the
+// workgroup.  `part` (one record per group) and `mask` may be NULL.
+__device__ void emo_select_block(long long group, bool active, float T, float E, long long c,
+                                 long long B, float target, unsigned int *mask, EmoPartial *part) {
     __shared__ unsigned long long s_key[EMO_WAVES_PER_BLOCK];
     __shared__ float s_T[EMO_WAVES_PER_BLOCK];
     __shared__ unsigned int s_cnt[EMO_WAVES_PER_BLOCK];
@@ -56,7 +57,7 @@ __device__ void emo_select_block(bool active, float T, float E, long long c, lon
     const unsigned long long bal = __ballot(feas);
     const int lane = threadIdx.x % EMO_WAVE;
     const int wave = threadIdx.x / EMO_WAVE;
-    const long long wbase = (long long)blockIdx.x * EMO_BLOCK + wave * EMO_WAVE;
+    const long long wbase = group * EMO_BLOCK + wave * EMO_WAVE;
     if (mask && lane == 0 && wbase < B) {
         const long long nwords = (B + 31) / 32;
         const long long w = wbase / 32;
@@ -87,7 +88,7 @@ __device__ void emo_select_block(bool active, float T, float E, long long c, lon
             }
             p.count += s_cnt[w];
         }
-        part[blockIdx.x] = p;
+        part[group] = p;
     }
 }
 
