@@ -31,7 +31,8 @@ HBM_PEAK_GBS = 8000.0
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for name in ("emo_kernels.hip", "emo_internal.h", "emo_host.cpp", "emo_jit.cpp", "emo_select.h"):
+    for name in ("emo_kernels.hip", "emo_chains.hip", "emo_internal.h", "emo_host.cpp", "emo_jit.cpp",
+                 "emo_select.h"):
         with open(os.path.join(ROOT, "paper_2607_12324_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -193,6 +194,8 @@ def main():
     src_hash = kernel_source_hash()
     if info["last_kernels"] == 2:      # segmented kernels: the timed unit is the whole chain
         kname = "emo_chain"
+    elif info["last_kernels"] == 3:
+        kname = "chains_kernel"
     elif info["last_kernels"] == 1:
         kname = "emo_sp_slack" if spec.slack else "emo_sp_select"
     else:

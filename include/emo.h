@@ -96,7 +96,11 @@ typedef struct {
                                      bit 3: segmented kernels are compiled */
     float compile_seconds;        /* time spent compiling specialised kernels */
     int32_t last_kernels;         /* kernels of the last batch call: 0 interpreted, 1 one
-                                     specialised kernel, 2 segmented specialised kernels */
+                                     specialised kernel, 2 segmented specialised kernels,
+                                     3 chain lanes (one lane per chain and candidate) */
+    int32_t chain_lanes;          /* lanes per candidate of the chain-lane kernels, 0 when the
+                                     candidate-dependent nodes do not form at most 64 disjoint
+                                     chains */
     int32_t num_implied_edges;    /* merged edges u -> v that the kernels skip because another
                                      path leads from u to v (they never decide a maximum or a
                                      minimum; results are unchanged) */

@@ -187,6 +187,7 @@ struct emo_graph_s {
     bool chain_slack = false;
     int chain_state = 0;                     // 0 not tried, 1 compiled, -1 failed
     emo::JitModule jc;
+    emo::DevChains chains;                   // chain-lane program (lanes == 0: not chains)
     Arena arena;                             // per-call scratch, kept between calls
     // profiling hook (hipEvent_t handles owned by the caller)
     hipEvent_t ev_begin = nullptr;
@@ -535,6 +536,56 @@ void release_device(emo_graph_s *g) {
 
 bool is_pow2(int32_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
+// Chain-lane program of a folded schedule whose steps form disjoint chains (at most one
+// candidate-dependent predecessor and successor each) and at most 64 of them: steps[k][lane]
+// is the k-th step of chain `lane`, padded with steps that leave a finish time unchanged.
+// Returns false when the schedule does not have that shape.
+bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::ChainStep> *steps,
+                  std::vector<int32_t> *pos, emo::DevChains *dc) {
+    const int32_t n = static_cast<int32_t>(sc.seq.size());
+    if (n == 0) return false;
+    std::vector<int32_t> heads;
+    for (int32_t i = 0; i < n; ++i) {
+        if (sc.in[i].size() > 1 || sc.out[i].size() > 1) return false;
+        if (sc.in[i].empty()) heads.push_back(i);
+    }
+    const int32_t C = static_cast<int32_t>(heads.size());
+    if (C < 1 || C > 64) return false;
+    std::vector<std::vector<int32_t>> chains(C);
+    size_t longest = 0;
+    for (int32_t c = 0; c < C; ++c) {
+        for (int32_t i = heads[c];; i = sc.out[i][0]) {
+            chains[c].push_back(i);
+            if (sc.out[i].empty()) break;
+        }
+        longest = std::max(longest, chains[c].size());
+    }
+    int32_t lanes = 1, lane_log = 0;
+    while (lanes < C) {
+        lanes <<= 1;
+        ++lane_log;
+    }
+    const int32_t len = static_cast<int32_t>((longest + emo::kChainStepBlock - 1) / emo::kChainStepBlock *
+                                             emo::kChainStepBlock);
+    steps->assign(static_cast<size_t>(len) * lanes, emo::ChainStep{-1, 0.f, 0.f, 0});
+    pos->assign(static_cast<size_t>(g.P), 0);
+    for (int32_t c = 0; c < C; ++c)
+        for (size_t k = 0; k < chains[c].size(); ++k) {
+            const int32_t i = chains[c][k];
+            const int32_t v = sc.seq[i];
+            emo::ChainStep &st = (*steps)[k * lanes + c];
+            st.pack = g.pack[v];
+            st.cst = sc.cst[i];
+            st.dur = g.pack[v] >= 0 ? 0.f : g.dur[v];
+            if (g.pack[v] >= 0) (*pos)[g.pack[v]] = static_cast<int32_t>(k * lanes + c);
+        }
+    dc->lanes = lanes;
+    dc->lane_log = lane_log;
+    dc->len = len;
+    dc->t_const = g.t_const;
+    return true;
+}
+
 // The specialised kernels' view of the graph: the folded schedule's steps, with predecessors
 // and successors as step indices.
 emo::JitGraph make_jit_graph(const emo_graph_s &g, const Schedule &sc) {
@@ -627,7 +678,7 @@ int ensure_chain(emo_graph_s *g) {
 bool aligned(const void *p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
 
 // Which kernels a batch call uses.
-enum class Path { kInterpreted = 0, kSingle = 1, kChain = 2 };
+enum class Path { kInterpreted = 0, kSingle = 1, kChain = 2, kChainLanes = 3 };
 
 // Chooses the kernels of a batch call, compiling specialised kernels on first use.  Returns
 // EMO_OK and sets *path, or an error in EMO_KERNELS_SPECIALIZED mode.
@@ -636,6 +687,13 @@ emo_status choose_path(emo_graph_s *g, const uint8_t *levels, const float *slack
     *path = Path::kInterpreted;
     if (g->kernel_mode == EMO_KERNELS_INTERPRETED) return EMO_OK;
     if (slack && per_node) return EMO_OK;   // per-node slack: interpreted kernels only
+    // disjoint chains too long for the segmented kernels: one lane per chain
+    const bool chain_lanes = g->chains.lanes > 0 && !(slack ? g->jit_slack_eligible || g->chain_slack
+                                                            : g->jit_eligible || g->chain_eval);
+    if (chain_lanes) {
+        *path = Path::kChainLanes;
+        return EMO_OK;
+    }
     if (!aligned(levels, static_cast<size_t>(emo::jit_level_width(g->jg)))) return EMO_OK;
     bool single = false, chain = false;
     if (slack) {
@@ -784,6 +842,11 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     in.pack_order_monotone = sf.monotone ? 1 : 0;
     in.kernel_mode = EMO_KERNELS_AUTO;
     g->jg = make_jit_graph(*g, sf);
+    std::vector<emo::ChainStep> csteps;
+    std::vector<int32_t> cpos;
+    emo::DevChains dc;
+    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc);
+    in.chain_lanes = chains_ok ? dc.lanes : 0;
     const int32_t nops = static_cast<int32_t>(sf.seq.size());
     g->jit_eligible = nops >= 1 && nops <= kJitMaxOps;
     g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;
@@ -805,6 +868,11 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
         if ((s = upload_program(*g, pe, g->dg.eval)) != EMO_OK) return s;
         if ((s = upload_program(*g, ps, g->dg.slack_pack)) != EMO_OK) return s;
         if ((s = upload_program(*g, pn, g->dg.slack_node)) != EMO_OK) return s;
+        if (chains_ok) {
+            if ((s = upload(*g, csteps, &dc.steps)) != EMO_OK) return s;
+            if ((s = upload(*g, cpos, &dc.pos)) != EMO_OK) return s;
+            g->chains = dc;
+        }
     }
     *out = holder.release();
     return ok();
@@ -918,12 +986,13 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     // one selection partial record per block of the evaluating kernel
     const int64_t nblocks = path == Path::kSingle  ? emo::jit_blocks(g->jm, B)
                             : path == Path::kChain ? emo::jit_chain_blocks(g->jc, B)
-                                                   : emo::forward_blocks(B);
+                                                   : emo::forward_blocks(B);   // also chain lanes
     const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
     size_t part_bytes = result ? static_cast<size_t>(nblocks) * emo::kPartialBytes : 0;
     part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
     size_t work_bytes = 0;
     if (path == Path::kChain) work_bytes = emo::chain_scratch_bytes(g->jc.plan, B);
+    else if (path == Path::kChainLanes) work_bytes = emo::chains_scratch_bytes(g->dg, g->chains, B, slack != nullptr);
     else if (path == Path::kInterpreted)
         work_bytes = slack ? emo::slack_scratch_bytes(prog, B) : emo::forward_scratch_bytes(g->dg.eval, B);
     std::lock_guard<std::mutex> lock(g->arena.mu);
@@ -944,6 +1013,9 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
         if (path == Path::kChain) {
             e = emo::jit_launch_chain(g->jc, levels, B, g->dg.tab, g->dg.tabt, work, slack, makespan,
                                       energy, target, mask, part, st);
+        } else if (path == Path::kChainLanes) {
+            e = emo::launch_chains(g->dg, g->chains, levels, B, makespan, energy, slack, target, mask,
+                                   part, work, st);
         } else if (slack) {
             if (path == Path::kSingle) {
                 e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy,

@@ -94,6 +94,34 @@ hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selectio
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
                                  uint32_t *mask, void *part, hipStream_t s);
 
+// ---------------------------------------------------------------- chain-lane kernels
+
+// Graphs whose candidate-dependent steps form disjoint chains (at most one candidate-dependent
+// predecessor and successor each): one lane per chain and candidate.
+constexpr int kChainStepBlock = 8;    // steps per unrolled block (and per backward checkpoint)
+struct ChainStep {                    // 16 bytes
+    int32_t pack;                     // pack id, or -1 (fixed node or padding)
+    float cst;                        // latest finish among candidate-independent predecessors
+    float dur;                        // fixed duration (pack == -1); 0 for padding
+    int32_t pad;
+};
+struct DevChains {
+    int32_t lanes = 0;                // lanes per candidate: a power of two in [1, 64]
+    int32_t lane_log = 0;
+    int32_t len = 0;                  // steps per chain, padded to a multiple of kChainStepBlock
+    float t_const = 0.f;              // makespan floor from candidate-independent nodes
+    const ChainStep *steps = nullptr; // [len][lanes]
+    const int32_t *pos = nullptr;     // [P]: step * lanes + chain of each pack
+};
+// Scratch of launch_chains: backward checkpoints and chain-ordered slack (slack only), and
+// makespan/energy buffers.
+size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, int64_t B, bool slack);
+// Makespan/energy (and per-pack slack when `slack`); the selection stage 1 runs from the stored
+// makespans and energies (forward_blocks(B) partial records in `part`).
+hipError_t launch_chains(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
+                         float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
+                         void *scratch, hipStream_t s);
+
 // ---------------------------------------------------------------- graph-specialised kernels
 
 // One candidate-dependent node of the graph in traversal order.

@@ -259,6 +259,14 @@ def packed_graph(seed: int, P: int, S: int, F: int, sync_every: int = 256,
                                pack_time=t, pack_energy=e)
 
 
+def stream_graph(seed: int, P: int, S: int, F: int, median_us: float = 8.0,
+                 sigma: float = 1.2) -> Graph:
+    """A graph shaped like the unpacked per-kernel workload at another size: P kernels on S
+    streams, each launched by a node of one host launch chain, no cross-stream edges."""
+    return _launch_graph(seed, f"streams-{P}k-{S}s-F{F}", P=P, S=S, F=F, packs_per_host=1,
+                         cross_p=0.0, n_cross_exact=None, median_us=median_us, sigma=sigma)
+
+
 def config_graph(k: int) -> Graph:
     """The execution graph and tables of benchmark workload `k` (1..5)."""
     spec = CONFIGS[k]

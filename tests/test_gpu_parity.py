@@ -199,6 +199,51 @@ def test_segmented_kernels(torch, emo, case):
         assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), case
 
 
+CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-streams": (8500, 33, 8),
+               "64-streams": (8300, 64, 5)}
+
+
+@pytest.mark.parametrize("case", list(CHAIN_CASES))
+def test_chain_lanes(torch, emo, case):
+    """Graphs whose candidate-dependent kernels form disjoint stream chains, too long for the
+    specialised kernels: one lane per chain and candidate, against the oracle on every row and
+    against the interpreting kernels (makespan and slack bit for bit), with invalid levels and a
+    batch that ends inside a workgroup."""
+    P, S_, F = CHAIN_CASES[case]
+    g = synth.stream_graph(P + S_, P, S_, F)
+    rng = np.random.default_rng(P + S_ + F)
+    rows = pins.random_rows(rng, g, 777)
+    rows[5, g.num_packs // 3] = F
+    rows[600, 0] = 255
+    print(f"[case] chain lanes {case}: V={g.num_nodes} P={g.num_packs} B={len(rows)}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    lanes = 1
+    while lanes < S_:
+        lanes *= 2
+    assert gh.info()["chain_lanes"] == lanes
+    lv = dev(torch, rows)
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    T, E = gh.eval_policies(lv)
+    assert gh.info()["last_kernels"] == 3
+    S = gh.slack(lv)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == 3
+    ok = ~np.isnan(T_or)
+    assert not ok[5] and not ok[600]
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, case)
+    Sh = host(S)
+    assert np.all(np.isnan(Sh[~ok]))
+    S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in np.nonzero(ok)[0]])
+    parity.assert_slack(Sh[ok], S_or, T_or[ok], True, case + " pack slack")
+    tgt = float(np.float32(np.median(T_or[ok])))
+    run_all(torch, emo, g, rows, [tgt], per_node=False, what="chain lanes " + case)
+    gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+    Ti, _ = gi.eval_policies(lv)
+    Si = gi.slack(lv)
+    assert np.array_equal(host(T).view(np.uint32), host(Ti).view(np.uint32)), case
+    assert np.array_equal(Sh.view(np.uint32), host(Si).view(np.uint32)), case
+
+
 @pytest.mark.parametrize("mode", [0, 1], ids=["auto", "interpreted"])
 def test_scratch_reuse_across_streams(torch, emo, mode):
     """One handle used from two streams with batches that grow and shrink: the calls share the
@@ -342,10 +387,10 @@ def test_workload_full_batch(torch, emo, k):
     lv = dev(torch, rows)
     T, E = gh.eval_policies(lv)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, spec.name)
-    # one specialised kernel up to 2048 steps, segmented kernels for the 4096-pack graph, the
-    # interpreting kernels for the 65536-kernel graph
+    # one specialised kernel up to 2048 steps, segmented kernels for the 4096-pack graph, chain
+    # lanes for the 65536-kernel graph (16 stream chains)
     inf = gh.info()
-    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 2, 5: 0}[k], inf
+    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 2, 5: 3}[k], inf
     if k <= 4:
         # the interpreting kernels on the same batch: bit-identical
         gi = emo.EmoGraph(g, device=0, kernel_mode=1)
@@ -368,12 +413,12 @@ def test_workload_full_batch(torch, emo, k):
     pick = synth.sample_rows(B, 24)
     S = gh.slack(lv)
     # slack: one kernel while every finish time fits in registers, then segmented kernels
-    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 2, 5: 0}[k], gh.info()
+    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 2, 5: 3}[k], gh.info()
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in pick])
     idx = torch.from_numpy(pick).cuda()
     parity.assert_slack(host(S.index_select(0, idx)), S_or, T_or[pick], True, spec.name + " slack")
-    if k in (3, 4):
-        # the segmented backward kernels against the interpreting kernels on a leading slice
+    if k in (3, 4, 5):
+        # segmented / chain-lane slack against the interpreting kernels on a leading slice
         gi = emo.EmoGraph(g, device=0, kernel_mode=1)
         nb = min(B, 8192)
         Si = gi.slack(lv[:nb])
