@@ -162,6 +162,16 @@ def test_implied_edges_on_workloads(emo):
     assert _load(emo, g).info()["num_implied_edges"] == _implied_edges(g)
 
 
+def test_chain_detection(emo):
+    """Chain lanes: the candidate-dependent nodes must form at most 64 disjoint chains."""
+    expect = {1: 0, 2: 1, 3: 0, 4: 0, 5: 16}   # 2 cross edges / 1 stream / cross edges / syncs / 16 streams
+    for k, lanes in expect.items():
+        assert _load(emo, synth.config_graph(k)).info()["chain_lanes"] == lanes, k
+    for S, lanes in ((1, 1), (3, 4), (17, 32), (64, 64), (65, 0)):
+        g = synth.stream_graph(5, 20 * S, S, 4)
+        assert _load(emo, g).info()["chain_lanes"] == lanes, S
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_topo_order_matches_oracle_on_random_dags(emo, oracle_lib, seed):
     rng = np.random.default_rng(100 + seed)

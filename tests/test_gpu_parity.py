@@ -200,7 +200,11 @@ def test_segmented_kernels(torch, emo, case):
 
 
 CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-streams": (8500, 33, 8),
-               "64-streams": (8300, 64, 5)}
+               "64-streams": (8300, 64, 5),
+               # a block's table rows exceed the LDS stage: every lane reads the table itself
+               "64-streams-F16": (8300, 64, 16),
+               # pack count not a multiple of 4: slack stored directly in pack order
+               "odd-packs": (8301, 7, 8)}
 
 
 @pytest.mark.parametrize("case", list(CHAIN_CASES))
@@ -242,6 +246,54 @@ def test_chain_lanes(torch, emo, case):
     Si = gi.slack(lv)
     assert np.array_equal(host(T).view(np.uint32), host(Ti).view(np.uint32)), case
     assert np.array_equal(Sh.view(np.uint32), host(Si).view(np.uint32)), case
+
+
+def test_chain_lanes_with_fixed_nodes(torch, emo):
+    """Chains that mix packs with fixed-duration nodes (which depend on the candidate through the
+    pack before them), constant floors from a host node, and chains of different lengths."""
+    rng = np.random.default_rng(42)
+    lengths = [3100, 2900, 3400]
+    src, dst, pack, dur = [], [], [], []
+    h0 = 0   # a host node: candidate-independent floor for some chain nodes
+    pack.append(-1)
+    dur.append(5.0)
+    P = 0
+    for L in lengths:
+        prev = None
+        for k in range(L):
+            v = len(pack)
+            if k % 3 == 2:
+                pack.append(-1)
+                dur.append(float(synth.quantize(rng.uniform(0.5, 6.0))))
+            else:
+                pack.append(P)
+                P += 1
+                dur.append(0.0)
+            if prev is not None:
+                src.append(prev)
+                dst.append(v)
+            if k % 50 == 0:
+                src.append(h0)
+                dst.append(v)
+            prev = v
+    V = len(pack)
+    F = 8
+    t = np.sort(synth.quantize(rng.uniform(1.0, 30.0, (P, F))), axis=1)[:, ::-1].copy()
+    e = (0.7 * t * rng.uniform(0.2, 1.0, (P, F))).astype(np.float32)
+    g = synth.Graph("chains-with-fixed", V, np.asarray(src, np.int32), np.asarray(dst, np.int32),
+                    np.asarray(pack, np.int32), np.asarray(dur, np.float32), P, F, t, e, 0.3)
+    rows = pins.random_rows(rng, g, 300)
+    print(f"[case] chain lanes with fixed nodes: V={V} P={P}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    assert gh.info()["chain_lanes"] == 4
+    lv = dev(torch, rows)
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    T, E = gh.eval_policies(lv)
+    S = gh.slack(lv)
+    assert gh.info()["last_kernels"] == 3
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, "chains with fixed nodes")
+    S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(len(rows))])
+    parity.assert_slack(host(S), S_or, T_or, True, "chains with fixed nodes: pack slack")
 
 
 @pytest.mark.parametrize("mode", [0, 1], ids=["auto", "interpreted"])
