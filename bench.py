@@ -27,6 +27,7 @@ if ROOT not in sys.path:
 
 METRIC = "candidate policies evaluated/sec (timing+energy+select); % of VALU/HBM roofline"
 HBM_PEAK_GBS = 8000.0
+VALU_PEAK_TOPS = 39.3   # 256 CUs x 64 fp32 lanes x 2.4 GHz, one op per lane per clock (no packed math)
 
 
 def kernel_source_hash() -> str:
@@ -191,6 +192,11 @@ def main():
     # algorithmic bytes of the main launch: level bytes in; makespan, energy, slack and mask out
     algo_bytes = B * (P + 8 + (4 * P if spec.slack else 0)) + (B + 7) // 8
     achieved = algo_bytes / (main_ms / 1e3) / 1e9
+    # algorithmic VALU work on the folded graph: one max per candidate-dependent edge, one add
+    # per pack for the finish time and one for the energy, two for the makespan/energy close;
+    # the backward pass (min per edge, subtractions per node) doubles it
+    ops_per_cand = (info["num_dynamic_edges"] + 2 * P + 2) * (2 if spec.slack else 1)
+    valu_tops = B * ops_per_cand / (main_ms / 1e3) / 1e12
     src_hash = kernel_source_hash()
     if info["last_kernels"] == 2:      # segmented kernels: the timed unit is the whole chain
         kname = "emo_chain"
@@ -222,7 +228,10 @@ def main():
         "roofline": {"bound": "hbm", "kernel": kname, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes_per_launch": algo_bytes,
-                     "launch_ms": main_ms},
+                     "launch_ms": main_ms,
+                     "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Tops/s",
+                              "frac": valu_tops / VALU_PEAK_TOPS,
+                              "algorithmic_ops_per_candidate": ops_per_cand}},
         "wall_s": wall,
         "selected": [{"target": t, "index": x.index, "energy": x.energy, "makespan": x.makespan,
                       "num_feasible": x.num_feasible} for t, x in zip(targets, sels)],
