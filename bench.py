@@ -202,6 +202,8 @@ def main():
         kname = "emo_chain"
     elif info["last_kernels"] == 3:
         kname = "chains_kernel"
+    elif info["last_kernels"] == 4:
+        kname = "chains_windowed"
     elif info["last_kernels"] == 1:
         kname = "emo_sp_slack" if spec.slack else "emo_sp_select"
     else:

@@ -97,13 +97,19 @@ typedef struct {
     float compile_seconds;        /* time spent compiling specialised kernels */
     int32_t last_kernels;         /* kernels of the last batch call: 0 interpreted, 1 one
                                      specialised kernel, 2 segmented specialised kernels,
-                                     3 chain lanes (one lane per chain and candidate) */
+                                     3 chain lanes (one lane per chain and candidate),
+                                     4 windowed chain lanes (a wave per chain, 64 candidates;
+                                     pack windows staged in LDS) */
     int32_t chain_lanes;          /* lanes per candidate of the chain-lane kernels, 0 when the
                                      candidate-dependent nodes do not form at most 64 disjoint
                                      chains */
     int32_t num_implied_edges;    /* merged edges u -> v that the kernels skip because another
                                      path leads from u to v (they never decide a maximum or a
                                      minimum; results are unchanged) */
+    int32_t chain_window;         /* packs per window of the windowed chain-lane kernel, 0 when
+                                     it does not apply (more than 16 chains, a chain that goes
+                                     back to an earlier window, P not a multiple of 16); calls
+                                     use it when levels and slack are 16-byte aligned */
 } emo_graph_info;
 
 /* Which kernels evaluate a graph.

@@ -349,6 +349,401 @@ gather_slack(const float *__restrict__ tmp, const int32_t *__restrict__ pos, int
     *reinterpret_cast<float4 *>(S + cand * P + p) = v;
 }
 
+// ---------------------------------------------------------------- windowed variant
+//
+// The lane-per-chain kernels above read each candidate's level bytes at the packs its chains
+// are at; when the chains drift thousands of pack ids apart (streams launched in random order),
+// every 8-step block of a wave touches up to 64 different cache lines, and slack has to be
+// written in chain order and gathered.  The windowed kernel cuts the pack ids into windows of
+// W packs instead and turns the layout around: a wave is 64 candidates on ONE chain (so the
+// step records are the same for the whole wave and are read as scalars), and a workgroup is
+// G groups of 64 candidates x nc chains.  Per window the workgroup copies, with 16-byte loads,
+//   - the G*64 candidates' level bytes of the window (levels are checked against F there),
+//   - the window's table rows (time and energy; times only in the backward pass),
+// into LDS, prefetched into registers during the previous window.  Each wave then walks its
+// chain's steps inside the window (the count varies per chain; waves wait at the window's
+// barrier).  The backward pass recomputes the window's finish times from the checkpoint
+// taken at the window's start into an LDS tile [candidate][column], turns them into slack in
+// place while walking the steps in reverse, and the workgroup writes the tile out in pack
+// order with 16-byte stores.
+//
+// Column W of every level row is 0 and row W of the table is zero, so a fixed node (column W)
+// reads a zero time and energy and adds its own duration; its tile entry is column W's pad.
+// Energies are summed per chain in fp32 over each window, added into fp64, and the chains'
+// sums are added in chain order.
+constexpr int kWinPre = 4;                         // 16-byte prefetch pieces per thread and buffer
+constexpr size_t kWinLds = 150 * 1024;
+constexpr int kWinMaxWaves = 16;
+
+__host__ __device__ inline uint32_t round16u(uint32_t x) { return (x + 15u) & ~15u; }
+
+struct WinLayout {
+    uint32_t lvl_pitch;    // bytes per candidate row of a level buffer (W + 4)
+    uint32_t lvl_buf;      // bytes of one level buffer
+    uint32_t off_bad;      // u32 [NC]: candidate has a level >= F
+    uint32_t off_tfin;     // f32 [NC]: makespan (NaN when bad)
+    uint32_t off_x;        // phase region: tables (forward, backward), chain sums, slack tile
+    uint32_t tab_elems;    // entries of one table buffer ((W + 1) * F)
+    uint32_t off_tile;     // f32 [NC][W + 1] (backward)
+    uint32_t total;
+};
+
+__host__ __device__ inline WinLayout win_layout(int W, int NC, int F, int nwaves) {
+    WinLayout L;
+    L.lvl_pitch = static_cast<uint32_t>(W) + 4u;
+    L.lvl_buf = round16u(static_cast<uint32_t>(NC) * L.lvl_pitch);
+    L.off_bad = 2u * L.lvl_buf;
+    L.off_tfin = L.off_bad + 4u * static_cast<uint32_t>(NC);
+    L.off_x = round16u(L.off_tfin + 4u * static_cast<uint32_t>(NC));
+    L.tab_elems = static_cast<uint32_t>(W + 1) * static_cast<uint32_t>(F);
+    const uint32_t fwd = 2u * L.tab_elems * 8u;
+    const uint32_t comb = 64u * 8u * kWinMaxWaves + static_cast<uint32_t>(nwaves) * 64u * 4u;
+    L.off_tile = L.off_x + round16u(2u * L.tab_elems * 4u);
+    const uint32_t bwd = L.off_tile - L.off_x + static_cast<uint32_t>(NC) * static_cast<uint32_t>(W + 1) * 4u;
+    uint32_t m = fwd > comb ? fwd : comb;
+    m = m > bwd ? m : bwd;
+    L.total = L.off_x + m;
+    return L;
+}
+
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Replaces the level bytes >= F of a word by 0 and reports them (F <= 128: a byte b < 128 gets
+// bit 7 from (b + 128 - F) exactly when b >= F, and a byte >= 128 has it already).
+__device__ __forceinline__ uint32_t clean_levels(uint32_t x, uint32_t addf, uint32_t &bad) {
+    const uint32_t hi = (((x & 0x7f7f7f7fu) + addf) | x) & 0x80808080u;
+    bad |= hi;
+    return x & ~((hi >> 7) * 0xffu);
+}
+
+struct WinArgs {
+    int W, wlog, nc, NC, F;
+    WinLayout L;
+};
+
+// Level pieces of window w into registers: piece q is bytes [16k, 16k + 16) of candidate r.
+__device__ __forceinline__ void win_load_levels(const WinArgs &a, const uint8_t *__restrict__ levels,
+                                                int64_t base, int64_t B, int32_t P, int w,
+                                                uint4 (&pre)[kWinPre]) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int per_row = a.W >> 4;
+    const int n = a.NC * per_row;
+#pragma unroll
+    for (int i = 0; i < kWinPre; ++i) {
+        const int q = t + i * nt;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (q < n) {
+            const int r = q / per_row, k = q - r * per_row;
+            const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 16 * k;
+            int64_t row = base + r;
+            row = row < B ? row : B - 1;
+            if (col < P) v = *reinterpret_cast<const uint4 *>(levels + row * P + col);
+        }
+        pre[i] = v;
+    }
+}
+
+__device__ __forceinline__ void win_store_levels(const WinArgs &a, uint8_t *lvl, uint32_t *bad,
+                                                 uint32_t addf, const uint4 (&pre)[kWinPre]) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int per_row = a.W >> 4;
+    const int n = a.NC * per_row;
+#pragma unroll
+    for (int i = 0; i < kWinPre; ++i) {
+        const int q = t + i * nt;
+        if (q < n) {
+            const int r = q / per_row, k = q - r * per_row;
+            uint32_t b = 0u;
+            uint32_t *d = reinterpret_cast<uint32_t *>(lvl + r * a.L.lvl_pitch + 16 * k);
+            d[0] = clean_levels(pre[i].x, addf, b);
+            d[1] = clean_levels(pre[i].y, addf, b);
+            d[2] = clean_levels(pre[i].z, addf, b);
+            d[3] = clean_levels(pre[i].w, addf, b);
+            if (bad && b) bad[r] = 1u;
+        }
+    }
+}
+
+// Table pieces of window w: 16 bytes of the window's rows (W * F entries of `esize` bytes).
+__device__ __forceinline__ void win_load_table(const WinArgs &a, const void *__restrict__ tab, int esize,
+                                               int32_t P, int w, uint4 (&pre)[kWinPre]) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int n = (a.W * a.F * esize) >> 4;
+    const int64_t wb = (static_cast<int64_t>(w) << a.wlog) * a.F * esize;   // byte offset
+    const int64_t end = static_cast<int64_t>(P) * a.F * esize;
+    const char *src = static_cast<const char *>(tab);
+#pragma unroll
+    for (int i = 0; i < kWinPre; ++i) {
+        const int q = t + i * nt;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (q < n && wb + 16 * q < end) v = *reinterpret_cast<const uint4 *>(src + wb + 16 * q);
+        pre[i] = v;
+    }
+}
+
+__device__ __forceinline__ void win_store_table(const WinArgs &a, void *dst, int esize,
+                                                const uint4 (&pre)[kWinPre]) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int n = (a.W * a.F * esize) >> 4;
+#pragma unroll
+    for (int i = 0; i < kWinPre; ++i) {
+        const int q = t + i * nt;
+        if (q < n) reinterpret_cast<uint4 *>(dst)[q] = pre[i];
+    }
+}
+
+// One window's steps of the wave's chain, four at a time: the records (scalars), then the
+// level bytes, then the table entries of the four steps are requested before the finish times
+// are advanced, so the memory round trips overlap.
+constexpr int kWinUnroll = 4;
+
+// max of two non-negative finite floats: their bit patterns order like unsigned integers, and
+// the integer max needs none of the NaN-quieting that the compiler adds to fmaxf on operands
+// loaded from memory.  Finish times and start floors here are always >= 0 and finite.
+__device__ __forceinline__ float fmax_nonneg(float a, float b) {
+    const unsigned x = __float_as_uint(a), y = __float_as_uint(b);
+    return __uint_as_float(x > y ? x : y);
+}
+
+template <bool SLACK, bool FIXED>
+__global__ void __launch_bounds__(kChainBlockThreads)
+chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restrict__ ws,
+                const int32_t *__restrict__ wbeg, const uint8_t *__restrict__ levels, int64_t B,
+                float *__restrict__ To, float *__restrict__ Eo, float *__restrict__ S,
+                float *__restrict__ ck, int64_t pitch) {
+    extern __shared__ float4 smem[];
+    char *lds = reinterpret_cast<char *>(smem);
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int grp = wv / a.nc, ch = wv - grp * a.nc;
+    const int lane = t & 63;
+    const int cl = grp * 64 + lane;                               // candidate within the workgroup
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * a.NC;
+    const int64_t gc = base + cl;                                 // checkpoint column
+    const int W = a.W, F = a.F, nc = a.nc, nwin = c.nwin;
+    const int32_t P = g.P;
+    const WinLayout &L = a.L;
+    uint8_t *lvl0 = reinterpret_cast<uint8_t *>(lds);             // [2][NC][W + 4] bytes
+    uint32_t *bad = reinterpret_cast<uint32_t *>(lds + L.off_bad);
+    float *tfin = reinterpret_cast<float *>(lds + L.off_tfin);
+    float2 *tab2 = reinterpret_cast<float2 *>(lds + L.off_x);     // forward: [2][W + 1][F]
+    float *tabt = reinterpret_cast<float *>(lds + L.off_x);       // backward: [2][W + 1][F]
+    float *tile = reinterpret_cast<float *>(lds + L.off_tile);    // backward: [NC][W + 1]
+    const uint32_t addf = (0x80u - static_cast<uint32_t>(F)) * 0x01010101u;
+
+    // ------------------------------------------------------------------ forward
+    for (int i = t; i < a.NC; i += nt) {
+        bad[i] = 0u;
+        *reinterpret_cast<uint32_t *>(lvl0 + i * L.lvl_pitch + W) = 0u;
+        *reinterpret_cast<uint32_t *>(lvl0 + L.lvl_buf + i * L.lvl_pitch + W) = 0u;
+    }
+    for (int i = t; i < F; i += nt) {
+        tab2[W * F + i] = make_float2(0.f, 0.f);
+        tab2[L.tab_elems + W * F + i] = make_float2(0.f, 0.f);
+    }
+    uint4 pl[kWinPre], pt[kWinPre];
+    win_load_levels(a, levels, base, B, P, 0, pl);
+    win_load_table(a, g.tab, 8, P, 0, pt);
+    lds_barrier();
+    win_store_levels(a, lvl0, bad, addf, pl);
+    win_store_table(a, tab2, 8, pt);
+    lds_barrier();
+    float f = 0.f;
+    double ed = 0.0;
+    for (int w = 0; w < nwin; ++w) {
+        const int buf = w & 1;
+        const bool more = w + 1 < nwin;
+        if (more) {
+            win_load_levels(a, levels, base, B, P, w + 1, pl);
+            win_load_table(a, g.tab, 8, P, w + 1, pt);
+        }
+        if (SLACK) ck[(static_cast<int64_t>(w) * nc + ch) * pitch + gc] = f;
+        const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
+        const float2 *tb = tab2 + buf * L.tab_elems;
+        const int k0 = wbeg[w * nc + ch], k1 = wbeg[(w + 1) * nc + ch];
+        float eb = 0.f;
+        int k = k0;
+        for (; k + kWinUnroll <= k1; k += kWinUnroll) {
+            ChainWinStep r[kWinUnroll];
+            unsigned l[kWinUnroll];
+            float2 te[kWinUnroll];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) r[i] = ws[k + i];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) l[i] = lrow[r[i].col];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) te[i] = tb[r[i].col * F + static_cast<int>(l[i])];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) {
+                f = fmax_nonneg(f, r[i].cst) + te[i].x;
+                if (FIXED) f += r[i].dur;
+                eb += te[i].y;
+            }
+        }
+        for (; k < k1; ++k) {
+            const ChainWinStep r = ws[k];
+            const float2 te = tb[r.col * F + static_cast<int>(lrow[r.col])];
+            f = fmax_nonneg(f, r.cst) + te.x;
+            if (FIXED) f += r.dur;
+            eb += te.y;
+        }
+        ed += static_cast<double>(eb);
+        if (more) {
+            win_store_levels(a, lvl0 + (buf ^ 1) * L.lvl_buf, bad, addf, pl);
+            win_store_table(a, tab2 + (buf ^ 1) * L.tab_elems, 8, pt);
+        }
+        lds_barrier();
+    }
+    // chains' makespans and energies -> the candidate's (chain order)
+    double *esum = reinterpret_cast<double *>(lds + L.off_x);
+    float *tsum = reinterpret_cast<float *>(lds + L.off_x + 8 * 64 * kWinMaxWaves);
+    esum[wv * 64 + lane] = ed;
+    tsum[wv * 64 + lane] = f;
+    lds_barrier();
+    if (ch == 0) {
+        float T = c.t_const;
+        double e = 0.0;
+        for (int j = 0; j < nc; ++j) {
+            T = fmaxf(T, tsum[(grp * nc + j) * 64 + lane]);
+            e += esum[(grp * nc + j) * 64 + lane];
+        }
+        float E = static_cast<float>(e + static_cast<double>(g.static_power) * static_cast<double>(T));
+        if (bad[cl]) {
+            T = __builtin_nanf("");
+            E = __builtin_nanf("");
+        }
+        tfin[cl] = T;
+        if (gc < B) {
+            To[gc] = T;
+            Eo[gc] = E;
+        }
+    }
+    if (!SLACK) return;
+    lds_barrier();
+
+    // ------------------------------------------------------------------ backward
+    for (int i = t; i < F; i += nt) {
+        tabt[W * F + i] = 0.f;
+        tabt[L.tab_elems + W * F + i] = 0.f;
+    }
+    const int top = nwin - 1;
+    win_load_levels(a, levels, base, B, P, top, pl);
+    win_load_table(a, g.tabt, 4, P, top, pt);
+    float fck = ck[(static_cast<int64_t>(top) * nc + ch) * pitch + gc];
+    float lft = tfin[cl];                                   // NaN for a candidate with bad levels
+    win_store_levels(a, lvl0 + (top & 1) * L.lvl_buf, nullptr, addf, pl);
+    win_store_table(a, tabt + (top & 1) * L.tab_elems, 4, pt);
+    lds_barrier();
+    asm volatile("" : "+v"(fck));   // (see the end of the loop)
+    float *trow = tile + cl * (W + 1);
+    const int per_row = W >> 2;                             // float4 pieces per tile row
+    for (int w = top; w >= 0; --w) {
+        const int buf = w & 1;
+        const bool more = w >= 1;
+        float fnext = 0.f;
+        if (more) {
+            win_load_levels(a, levels, base, B, P, w - 1, pl);
+            win_load_table(a, g.tabt, 4, P, w - 1, pt);
+            fnext = ck[(static_cast<int64_t>(w - 1) * nc + ch) * pitch + gc];
+        }
+        const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
+        const float *tb = tabt + buf * L.tab_elems;
+        const int k0 = wbeg[w * nc + ch], k1 = wbeg[(w + 1) * nc + ch];
+        // finish times of the window's steps, from the checkpoint, into the tile
+        float fb = fck;
+        int k = k0;
+        for (; k + kWinUnroll <= k1; k += kWinUnroll) {
+            ChainWinStep r[kWinUnroll];
+            unsigned l[kWinUnroll];
+            float tt[kWinUnroll];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) r[i] = ws[k + i];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) l[i] = lrow[r[i].col];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) tt[i] = tb[r[i].col * F + static_cast<int>(l[i])];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) {
+                fb = fmax_nonneg(fb, r[i].cst) + tt[i];
+                if (FIXED) fb += r[i].dur;
+                trow[r[i].col] = fb;
+            }
+        }
+        for (; k < k1; ++k) {
+            const ChainWinStep r = ws[k];
+            fb = fmax_nonneg(fb, r.cst) + tb[r.col * F + static_cast<int>(lrow[r.col])];
+            if (FIXED) fb += r.dur;
+            trow[r.col] = fb;
+        }
+        // slack = latest finish - finish, walking the steps in reverse (the chain's columns are
+        // distinct, except fixed nodes' pad column, which is never stored)
+        k = k1;
+        for (; k - kWinUnroll >= k0; k -= kWinUnroll) {
+            ChainWinStep r[kWinUnroll];
+            unsigned l[kWinUnroll];
+            float tt[kWinUnroll], ef[kWinUnroll];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) r[i] = ws[k - 1 - i];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) l[i] = lrow[r[i].col];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) tt[i] = tb[r[i].col * F + static_cast<int>(l[i])];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) ef[i] = trow[r[i].col];
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) {
+                if (FIXED) tt[i] += r[i].dur;
+                ef[i] = lft - ef[i];
+                lft = lft - tt[i];
+            }
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) trow[r[i].col] = ef[i];
+        }
+        for (; k > k0; --k) {
+            const ChainWinStep r = ws[k - 1];
+            float tt = tb[r.col * F + static_cast<int>(lrow[r.col])];
+            if (FIXED) tt += r.dur;
+            trow[r.col] = lft - trow[r.col];
+            lft = lft - tt;
+        }
+        if (more) {
+            win_store_levels(a, lvl0 + (buf ^ 1) * L.lvl_buf, nullptr, addf, pl);
+            win_store_table(a, tabt + (buf ^ 1) * L.tab_elems, 4, pt);
+        }
+        lds_barrier();
+        // slack tile -> pack order; a wave covers 4 candidates x 16 pieces when rows are long
+        // enough (conflict-free LDS reads with the odd row pitch), else whole rows
+        const int n = a.NC * per_row;
+        for (int q = t; q < n; q += nt) {
+            int r, kk;
+            if (per_row >= 16) {
+                const int j = q & 63, blk = q >> 6, nkb = per_row >> 4;
+                const int rg = blk / nkb, kb = blk - rg * nkb;
+                r = rg * 4 + (j >> 4);
+                kk = kb * 16 + (j & 15);
+            } else {
+                r = q / per_row;
+                kk = q - r * per_row;
+            }
+            const float *src = tile + r * (W + 1) + 4 * kk;
+            const float4 v = make_float4(src[0], src[1], src[2], src[3]);
+            const int64_t row = base + r;
+            const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 4 * kk;
+            if (row < B && col < P) *reinterpret_cast<float4 *>(S + row * P + col) = v;
+        }
+        lds_barrier();
+        // take the checkpoint here, where its load (issued at the window's start) has landed;
+        // left to the next window's first use, the wait would also cover that window's
+        // prefetch loads
+        asm volatile("" : "+v"(fnext));
+        fck = fnext;
+    }
+}
+
 int64_t chain_grid(const DevChains &c, int64_t B) {
     return ((B << c.lane_log) + kChainBlockThreads - 1) / kChainBlockThreads;
 }
@@ -364,7 +759,42 @@ bool staged_ok(const DevGraph &g, const DevChains &c) {
 size_t round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 }  // namespace
 
-size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, int64_t B, bool slack) {
+bool chain_window_shape(int32_t nc, int32_t F, int32_t P, int32_t *win, int32_t *groups) {
+    if (nc < 1 || nc > kWinMaxWaves || F < 1 || F > 128 || P < 1 || P % 16 != 0) return false;
+    const int G = kWinMaxWaves / nc;
+    const int NC = 64 * G, nthreads = 64 * G * nc;
+    for (int W = 256; W >= 16; W >>= 1) {
+        const WinLayout L = win_layout(W, NC, F, G * nc);
+        const int lvl_pieces = NC * (W / 16), tab_pieces = W * F * 8 / 16;
+        if (L.total <= kWinLds && lvl_pieces <= kWinPre * nthreads && tab_pieces <= kWinPre * nthreads) {
+            *win = W;
+            *groups = G;
+            return true;
+        }
+    }
+    return false;
+}
+
+bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
+    return c.win > 0 && reinterpret_cast<uintptr_t>(levels) % 16 == 0 &&
+           reinterpret_cast<uintptr_t>(slack) % 16 == 0;
+}
+
+namespace {
+int64_t win_grid(const DevChains &c, int64_t B) {
+    const int64_t NC = 64 * static_cast<int64_t>(c.groups);
+    return (B + NC - 1) / NC;
+}
+}  // namespace
+
+size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
+                            const float *slack_ptr) {
+    const bool slack = slack_ptr != nullptr;
+    if (chains_windowed_ok(c, levels, slack_ptr)) {
+        const size_t pitch = static_cast<size_t>(win_grid(c, B)) * 64 * c.groups;
+        const size_t ck = slack ? round256(static_cast<size_t>(c.nwin) * c.nc * pitch * sizeof(float)) : 0;
+        return ck + 2 * round256(static_cast<size_t>(B) * sizeof(float));
+    }
     const size_t lanes = static_cast<size_t>(chain_grid(c, B)) * kChainBlockThreads;
     const size_t ck = slack ? round256(static_cast<size_t>(c.len / K) * lanes * sizeof(float)) : 0;
     const size_t tmp = slack && staged_ok(g, c) && g.P % 4 == 0
@@ -373,9 +803,59 @@ size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, int64_t B, bo
     return ck + tmp + 2 * round256(static_cast<size_t>(B) * sizeof(float));
 }
 
+namespace {
+template <bool SLACK, bool FIXED>
+hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, const DevGraph &g,
+                                  const DevChains &c, const WinArgs &a, const uint8_t *levels, int64_t B,
+                                  float *T, float *E, float *S, float *ck, int64_t pitch) {
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kWinLds));
+    if (attr != hipSuccess) return attr;
+    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED>), gd, bd, lds, s, g, c, a, c.wsteps, c.wbeg, levels, B,
+                       T, E, S, ck, pitch);
+    return hipGetLastError();
+}
+
+hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
+                           float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
+                           void *scratch, hipStream_t s) {
+    WinArgs a;
+    a.W = c.win;
+    a.wlog = 0;
+    while ((1 << a.wlog) < a.W) ++a.wlog;
+    a.nc = c.nc;
+    a.NC = 64 * c.groups;
+    a.F = g.F;
+    a.L = win_layout(a.W, a.NC, a.F, c.groups * c.nc);
+    const int64_t grid = win_grid(c, B);
+    const int64_t pitch = grid * a.NC;
+    char *p = static_cast<char *>(scratch);
+    float *ck = nullptr;
+    if (slack) {
+        ck = reinterpret_cast<float *>(p);
+        p += round256(static_cast<size_t>(c.nwin) * c.nc * pitch * sizeof(float));
+    }
+    const size_t vec = round256(static_cast<size_t>(B) * sizeof(float));
+    float *Ts = T ? T : reinterpret_cast<float *>(p);
+    float *Es = E ? E : reinterpret_cast<float *>(p + vec);
+    const dim3 gd(static_cast<unsigned>(grid)), bd(static_cast<unsigned>(64 * c.groups * c.nc));
+    const size_t lds = a.L.total;
+    hipError_t e;
+    if (slack) e = c.fixed ? launch_windowed_kernel<true, true>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch)
+                           : launch_windowed_kernel<true, false>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch);
+    else e = c.fixed ? launch_windowed_kernel<false, true>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch)
+                     : launch_windowed_kernel<false, false>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch);
+    if (e == hipSuccess && (mask || part)) e = launch_select_results(Ts, Es, B, target, mask, part, s);
+    return e;
+}
+}  // namespace
+
 hipError_t launch_chains(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
                          float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
                          void *scratch, hipStream_t s) {
+    if (chains_windowed_ok(c, levels, slack)) return launch_windowed(g, c, levels, B, T, E, slack, target,
+                                                                     mask, part, scratch, s);
     const int64_t grid = chain_grid(c, B);
     const int64_t pitch = grid * kChainBlockThreads;
     const bool st = staged_ok(g, c);

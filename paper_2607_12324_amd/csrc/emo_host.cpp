@@ -540,8 +540,55 @@ bool is_pow2(int32_t x) { return x > 0 && (x & (x - 1)) == 0; }
 // candidate-dependent predecessor and successor each) and at most 64 of them: steps[k][lane]
 // is the k-th step of chain `lane`, padded with steps that leave a finish time unchanged.
 // Returns false when the schedule does not have that shape.
+// Windowed layout of the chains (see DevChains): steps grouped by the window of their pack
+// (a fixed node stays in the window of the chain's previous pack, window 0 before the first).
+// Returns false when some chain goes back to an earlier window or no window width fits.
+bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
+                         const std::vector<std::vector<int32_t>> &chains,
+                         std::vector<emo::ChainWinStep> *wsteps, std::vector<int32_t> *wbeg,
+                         emo::DevChains *dc) {
+    const int32_t nc = static_cast<int32_t>(chains.size());
+    int32_t W = 0, G = 0;
+    if (!emo::chain_window_shape(nc, g.F, g.P, &W, &G)) return false;
+    const int32_t nwin = (g.P + W - 1) / W;
+    wsteps->clear();
+    wbeg->assign(static_cast<size_t>(nwin + 1) * nc, 0);
+    int32_t fixed = 0;
+    for (int32_t c = 0; c < nc; ++c) {
+        int32_t w = 0;
+        // wbeg[x*nc + c] = first step of chain c in a window >= x
+        int32_t next_win = 0;
+        for (int32_t i : chains[c]) {
+            const int32_t v = sc.seq[i];
+            const int32_t p = g.pack[v];
+            if (p >= 0) {
+                if (p / W < w) return false;
+                w = p / W;
+            }
+            while (next_win <= w) (*wbeg)[static_cast<size_t>(next_win++) * nc + c] =
+                static_cast<int32_t>(wsteps->size());
+            emo::ChainWinStep st;
+            st.col = p >= 0 ? p - w * W : W;
+            st.cst = sc.cst[i];
+            st.dur = p >= 0 ? 0.f : g.dur[v];
+            st.pad = 0;
+            if (p < 0) fixed = 1;
+            wsteps->push_back(st);
+        }
+        while (next_win <= nwin) (*wbeg)[static_cast<size_t>(next_win++) * nc + c] =
+            static_cast<int32_t>(wsteps->size());
+    }
+    dc->nc = nc;
+    dc->win = W;
+    dc->nwin = nwin;
+    dc->groups = G;
+    dc->fixed = fixed;
+    return true;
+}
+
 bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::ChainStep> *steps,
-                  std::vector<int32_t> *pos, emo::DevChains *dc) {
+                  std::vector<int32_t> *pos, emo::DevChains *dc,
+                  std::vector<emo::ChainWinStep> *wsteps, std::vector<int32_t> *wbeg) {
     const int32_t n = static_cast<int32_t>(sc.seq.size());
     if (n == 0) return false;
     std::vector<int32_t> heads;
@@ -583,6 +630,11 @@ bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::Cha
     dc->lane_log = lane_log;
     dc->len = len;
     dc->t_const = g.t_const;
+    if (!build_chain_windows(g, sc, chains, wsteps, wbeg, dc)) {
+        dc->win = 0;
+        wsteps->clear();
+        wbeg->clear();
+    }
     return true;
 }
 
@@ -844,9 +896,12 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     g->jg = make_jit_graph(*g, sf);
     std::vector<emo::ChainStep> csteps;
     std::vector<int32_t> cpos;
+    std::vector<emo::ChainWinStep> cwsteps;
+    std::vector<int32_t> cwbeg;
     emo::DevChains dc;
-    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc);
+    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc, &cwsteps, &cwbeg);
     in.chain_lanes = chains_ok ? dc.lanes : 0;
+    in.chain_window = chains_ok ? dc.win : 0;
     const int32_t nops = static_cast<int32_t>(sf.seq.size());
     g->jit_eligible = nops >= 1 && nops <= kJitMaxOps;
     g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;
@@ -871,6 +926,10 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
         if (chains_ok) {
             if ((s = upload(*g, csteps, &dc.steps)) != EMO_OK) return s;
             if ((s = upload(*g, cpos, &dc.pos)) != EMO_OK) return s;
+            if (dc.win > 0) {
+                if ((s = upload(*g, cwsteps, &dc.wsteps)) != EMO_OK) return s;
+                if ((s = upload(*g, cwbeg, &dc.wbeg)) != EMO_OK) return s;
+            }
             g->chains = dc;
         }
     }
@@ -992,7 +1051,7 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
     size_t work_bytes = 0;
     if (path == Path::kChain) work_bytes = emo::chain_scratch_bytes(g->jc.plan, B);
-    else if (path == Path::kChainLanes) work_bytes = emo::chains_scratch_bytes(g->dg, g->chains, B, slack != nullptr);
+    else if (path == Path::kChainLanes) work_bytes = emo::chains_scratch_bytes(g->dg, g->chains, levels, B, slack);
     else if (path == Path::kInterpreted)
         work_bytes = slack ? emo::slack_scratch_bytes(prog, B) : emo::forward_scratch_bytes(g->dg.eval, B);
     std::lock_guard<std::mutex> lock(g->arena.mu);
@@ -1007,7 +1066,9 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     }
     void *part = result ? scratch : nullptr;
     void *work = scratch ? static_cast<char *>(scratch) + part_bytes : nullptr;
-    g->info.last_kernels = static_cast<int32_t>(path);
+    g->info.last_kernels = path == Path::kChainLanes && emo::chains_windowed_ok(g->chains, levels, slack)
+                               ? 4
+                               : static_cast<int32_t>(path);
     hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
     if (e == hipSuccess) {
         if (path == Path::kChain) {

@@ -172,6 +172,31 @@ def test_chain_detection(emo):
         assert _load(emo, g).info()["chain_lanes"] == lanes, S
 
 
+def test_chain_windows(emo):
+    """Window width of the windowed chain kernel: the widest of 256, 128, ..., 16 packs whose
+    LDS working set fits (two level windows of 16 // chains groups of 64 candidates, two table
+    windows, the slack tile); none with more than 16 chains, more than 128 levels, a pack count
+    that is not a multiple of 16, or a chain that goes back to an earlier window."""
+    expect = {1: 0, 2: 16, 3: 0, 4: 0, 5: 256}
+    for k, win in expect.items():
+        assert _load(emo, synth.config_graph(k)).info()["chain_window"] == win, k
+    for (P, S, F), win in (((8192, 16, 16), 256), ((4096, 3, 8), 64), ((8192, 9, 32), 128),
+                           ((10000, 1, 16), 16), ((9008, 5, 16), 64), ((8304, 7, 8), 128),
+                           ((4096, 2, 64), 32), ((4096, 16, 128), 64), ((9000, 5, 16), 0),
+                           ((8192, 17, 4), 0), ((4096, 2, 200), 0)):
+        g = synth.stream_graph(7, P, S, F)
+        assert _load(emo, g).info()["chain_window"] == win, (P, S, F)
+    # one chain over 48 packs: in pack order it has windows 0, 1, 2; visiting packs 32..47
+    # before 16..31 it goes back from window 2 to window 1
+    for order, win in ((list(range(48)), 16), (list(range(16)) + list(range(32, 48)) + list(range(16, 32)), 0)):
+        rng = np.random.default_rng(3)
+        t = synth.quantize(rng.uniform(1.0, 9.0, (48, 2))).astype(np.float32)
+        g = synth.Graph("one-chain", 48, np.arange(47, dtype=np.int32), np.arange(1, 48, dtype=np.int32),
+                        np.asarray(order, np.int32), np.zeros(48, np.float32), 48, 2, t, 0.5 * t, 0.1)
+        inf = _load(emo, g).info()
+        assert inf["chain_lanes"] == 1 and inf["chain_window"] == win, order[:20]
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_topo_order_matches_oracle_on_random_dags(emo, oracle_lib, seed):
     rng = np.random.default_rng(100 + seed)

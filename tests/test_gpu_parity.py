@@ -204,7 +204,21 @@ CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-strea
                # a block's table rows exceed the LDS stage: every lane reads the table itself
                "64-streams-F16": (8300, 64, 16),
                # pack count not a multiple of 4: slack stored directly in pack order
-               "odd-packs": (8301, 7, 8)}
+               "odd-packs": (8301, 7, 8),
+               # windowed kernel: 16 chains (one workgroup of 64 candidates), 3 chains (5 groups
+               # of 64 candidates), 9 chains with 32 levels (narrower windows); more than 8192
+               # steps, so that the segmented kernels do not apply
+               "16-streams": (8208, 16, 16), "3-streams-F8": (8224, 3, 8), "9-streams-F32": (8208, 9, 32)}
+# packs per window of the windowed kernel (0: lane-per-chain kernels only)
+CHAIN_WINDOW = {"1-stream": 16, "16-streams": 256, "3-streams-F8": 64, "9-streams-F32": 128}
+
+
+def misaligned(torch, rows):
+    """The rows in device memory at an address that is not 16-byte aligned."""
+    buf = torch.empty(rows.size + 16, dtype=torch.uint8, device="cuda")
+    v = buf[1:1 + rows.size].view(rows.shape)
+    v.copy_(torch.from_numpy(np.ascontiguousarray(rows)).to("cuda"))
+    return v
 
 
 @pytest.mark.parametrize("case", list(CHAIN_CASES))
@@ -219,21 +233,25 @@ def test_chain_lanes(torch, emo, case):
     rows = pins.random_rows(rng, g, 777)
     rows[5, g.num_packs // 3] = F
     rows[600, 0] = 255
+    rows[7, g.num_packs - 1] = 128
     print(f"[case] chain lanes {case}: V={g.num_nodes} P={g.num_packs} B={len(rows)}", flush=True)
     gh = emo.EmoGraph(g, device=0)
     lanes = 1
     while lanes < S_:
         lanes *= 2
+    win = CHAIN_WINDOW.get(case, 0)
     assert gh.info()["chain_lanes"] == lanes
+    assert gh.info()["chain_window"] == win
+    kind = 4 if win else 3
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
-    assert gh.info()["last_kernels"] == 3
+    assert gh.info()["last_kernels"] == kind
     S = gh.slack(lv)
     torch.cuda.synchronize()
-    assert gh.info()["last_kernels"] == 3
+    assert gh.info()["last_kernels"] == kind
     ok = ~np.isnan(T_or)
-    assert not ok[5] and not ok[600]
+    assert not ok[5] and not ok[600] and not ok[7]
     parity.assert_eval(host(T), host(E), T_or, E_or, True, case)
     Sh = host(S)
     assert np.all(np.isnan(Sh[~ok]))
@@ -246,13 +264,26 @@ def test_chain_lanes(torch, emo, case):
     Si = gi.slack(lv)
     assert np.array_equal(host(T).view(np.uint32), host(Ti).view(np.uint32)), case
     assert np.array_equal(Sh.view(np.uint32), host(Si).view(np.uint32)), case
+    if win:
+        # the same candidates through the lane-per-chain kernel (unaligned levels): makespans
+        # and slack bit for bit, energies (summed in another order) to the bound
+        lm = misaligned(torch, rows)
+        Tm, Em = gh.eval_policies(lm)
+        Sm = gh.slack(lm)
+        torch.cuda.synchronize()
+        assert gh.info()["last_kernels"] == 3
+        assert np.array_equal(host(T).view(np.uint32), host(Tm).view(np.uint32)), case
+        assert np.array_equal(Sh.view(np.uint32), host(Sm).view(np.uint32)), case
+        parity.assert_eval(host(Tm), host(Em), T_or, E_or, True, case + " lane-per-chain")
 
 
-def test_chain_lanes_with_fixed_nodes(torch, emo):
+@pytest.mark.parametrize("lengths", [[3100, 2900, 3400], [3100, 2900, 3406]],
+                         ids=["lane-per-chain", "windowed"])
+def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
     """Chains that mix packs with fixed-duration nodes (which depend on the candidate through the
-    pack before them), constant floors from a host node, and chains of different lengths."""
+    pack before them), constant floors from a host node, and chains of different lengths (6268
+    packs: lane-per-chain kernel; 6272 packs: windowed kernel)."""
     rng = np.random.default_rng(42)
-    lengths = [3100, 2900, 3400]
     src, dst, pack, dur = [], [], [], []
     h0 = 0   # a host node: candidate-independent floor for some chain nodes
     pack.append(-1)
@@ -286,11 +317,13 @@ def test_chain_lanes_with_fixed_nodes(torch, emo):
     print(f"[case] chain lanes with fixed nodes: V={V} P={P}", flush=True)
     gh = emo.EmoGraph(g, device=0)
     assert gh.info()["chain_lanes"] == 4
+    windowed = P % 16 == 0
+    assert gh.info()["chain_window"] == (64 if windowed else 0)
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
     S = gh.slack(lv)
-    assert gh.info()["last_kernels"] == 3
+    assert gh.info()["last_kernels"] == (4 if windowed else 3)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, "chains with fixed nodes")
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(len(rows))])
     parity.assert_slack(host(S), S_or, T_or, True, "chains with fixed nodes: pack slack")
@@ -442,7 +475,7 @@ def test_workload_full_batch(torch, emo, k):
     # one specialised kernel up to 2048 steps, segmented kernels for the 4096-pack graph, chain
     # lanes for the 65536-kernel graph (16 stream chains)
     inf = gh.info()
-    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 2, 5: 3}[k], inf
+    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 2, 5: 4}[k], inf
     if k <= 4:
         # the interpreting kernels on the same batch: bit-identical
         gi = emo.EmoGraph(g, device=0, kernel_mode=1)
@@ -465,7 +498,7 @@ def test_workload_full_batch(torch, emo, k):
     pick = synth.sample_rows(B, 24)
     S = gh.slack(lv)
     # slack: one kernel while every finish time fits in registers, then segmented kernels
-    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 2, 5: 3}[k], gh.info()
+    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 2, 5: 4}[k], gh.info()
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in pick])
     idx = torch.from_numpy(pick).cuda()
     parity.assert_slack(host(S.index_select(0, idx)), S_or, T_or[pick], True, spec.name + " slack")
