@@ -355,23 +355,23 @@ gather_slack(const float *__restrict__ tmp, const int32_t *__restrict__ pos, int
 // are at; when the chains drift thousands of pack ids apart (streams launched in random order),
 // every 8-step block of a wave touches up to 64 different cache lines, and slack has to be
 // written in chain order and gathered.  The windowed kernel cuts the pack ids into windows of
-// W packs instead and turns the layout around: a wave is 64 candidates on ONE chain (so the
-// step records are the same for the whole wave and are read as scalars), and a workgroup is
-// G groups of 64 candidates x nc chains.  Per window the workgroup copies, with 16-byte loads,
-//   - the G*64 candidates' level bytes of the window (levels are checked against F there),
+// W packs instead and turns the layout around: a wave is 64 candidates on ONE chain, and a
+// workgroup is G groups of 64 candidates x nc chains.  Per window the workgroup copies into
+// LDS, with 16-byte loads issued two windows ahead into registers:
+//   - the G*64 candidates' level bytes of the window (checked against F on the way),
 //   - the window's table rows (time and energy; times only in the backward pass),
-// into LDS, prefetched into registers during the previous window.  Each wave then walks its
-// chain's steps inside the window (the count varies per chain; waves wait at the window's
-// barrier).  The backward pass recomputes the window's finish times from the checkpoint
-// taken at the window's start into an LDS tile [candidate][column], turns them into slack in
-// place while walking the steps in reverse, and the workgroup writes the tile out in pack
-// order with 16-byte stores.
+//   - the window's step block: where each chain's steps start, and the step records.
+// Each wave then walks its chain's steps inside the window (the count varies per chain; waves
+// meet at the window's barrier).  The backward pass recomputes the window's finish times from
+// the checkpoint taken at the window's start into an LDS tile [candidate][column], turns them
+// into slack in place while walking the steps in reverse, and the workgroup writes the tile out
+// in pack order with 16-byte stores.
 //
 // Column W of every level row is 0 and row W of the table is zero, so a fixed node (column W)
 // reads a zero time and energy and adds its own duration; its tile entry is column W's pad.
 // Energies are summed per chain in fp32 over each window, added into fp64, and the chains'
 // sums are added in chain order.
-constexpr int kWinPre = 4;                         // 16-byte prefetch pieces per thread and buffer
+constexpr int kWinPre = 4;                         // 16-byte prefetch pieces per thread and window
 constexpr size_t kWinLds = 150 * 1024;
 constexpr int kWinMaxWaves = 16;
 
@@ -382,19 +382,21 @@ struct WinLayout {
     uint32_t lvl_buf;      // bytes of one level buffer
     uint32_t off_bad;      // u32 [NC]: candidate has a level >= F
     uint32_t off_tfin;     // f32 [NC]: makespan (NaN when bad)
+    uint32_t off_blk;      // [2] step blocks
     uint32_t off_x;        // phase region: tables (forward, backward), chain sums, slack tile
     uint32_t tab_elems;    // entries of one table buffer ((W + 1) * F)
     uint32_t off_tile;     // f32 [NC][W + 1] (backward)
     uint32_t total;
 };
 
-__host__ __device__ inline WinLayout win_layout(int W, int NC, int F, int nwaves) {
+__host__ __device__ inline WinLayout win_layout(int W, int NC, int F, int nwaves, int blk_bytes) {
     WinLayout L;
     L.lvl_pitch = static_cast<uint32_t>(W) + 4u;
     L.lvl_buf = round16u(static_cast<uint32_t>(NC) * L.lvl_pitch);
     L.off_bad = 2u * L.lvl_buf;
     L.off_tfin = L.off_bad + 4u * static_cast<uint32_t>(NC);
-    L.off_x = round16u(L.off_tfin + 4u * static_cast<uint32_t>(NC));
+    L.off_blk = round16u(L.off_tfin + 4u * static_cast<uint32_t>(NC));
+    L.off_x = L.off_blk + 2u * static_cast<uint32_t>(blk_bytes);
     L.tab_elems = static_cast<uint32_t>(W + 1) * static_cast<uint32_t>(F);
     const uint32_t fwd = 2u * L.tab_elems * 8u;
     const uint32_t comb = 64u * 8u * kWinMaxWaves + static_cast<uint32_t>(nwaves) * 64u * 4u;
@@ -420,87 +422,6 @@ __device__ __forceinline__ uint32_t clean_levels(uint32_t x, uint32_t addf, uint
     return x & ~((hi >> 7) * 0xffu);
 }
 
-struct WinArgs {
-    int W, wlog, nc, NC, F;
-    WinLayout L;
-};
-
-// Level pieces of window w into registers: piece q is bytes [16k, 16k + 16) of candidate r.
-__device__ __forceinline__ void win_load_levels(const WinArgs &a, const uint8_t *__restrict__ levels,
-                                                int64_t base, int64_t B, int32_t P, int w,
-                                                uint4 (&pre)[kWinPre]) {
-    const int t = threadIdx.x, nt = blockDim.x;
-    const int per_row = a.W >> 4;
-    const int n = a.NC * per_row;
-#pragma unroll
-    for (int i = 0; i < kWinPre; ++i) {
-        const int q = t + i * nt;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (q < n) {
-            const int r = q / per_row, k = q - r * per_row;
-            const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 16 * k;
-            int64_t row = base + r;
-            row = row < B ? row : B - 1;
-            if (col < P) v = *reinterpret_cast<const uint4 *>(levels + row * P + col);
-        }
-        pre[i] = v;
-    }
-}
-
-__device__ __forceinline__ void win_store_levels(const WinArgs &a, uint8_t *lvl, uint32_t *bad,
-                                                 uint32_t addf, const uint4 (&pre)[kWinPre]) {
-    const int t = threadIdx.x, nt = blockDim.x;
-    const int per_row = a.W >> 4;
-    const int n = a.NC * per_row;
-#pragma unroll
-    for (int i = 0; i < kWinPre; ++i) {
-        const int q = t + i * nt;
-        if (q < n) {
-            const int r = q / per_row, k = q - r * per_row;
-            uint32_t b = 0u;
-            uint32_t *d = reinterpret_cast<uint32_t *>(lvl + r * a.L.lvl_pitch + 16 * k);
-            d[0] = clean_levels(pre[i].x, addf, b);
-            d[1] = clean_levels(pre[i].y, addf, b);
-            d[2] = clean_levels(pre[i].z, addf, b);
-            d[3] = clean_levels(pre[i].w, addf, b);
-            if (bad && b) bad[r] = 1u;
-        }
-    }
-}
-
-// Table pieces of window w: 16 bytes of the window's rows (W * F entries of `esize` bytes).
-__device__ __forceinline__ void win_load_table(const WinArgs &a, const void *__restrict__ tab, int esize,
-                                               int32_t P, int w, uint4 (&pre)[kWinPre]) {
-    const int t = threadIdx.x, nt = blockDim.x;
-    const int n = (a.W * a.F * esize) >> 4;
-    const int64_t wb = (static_cast<int64_t>(w) << a.wlog) * a.F * esize;   // byte offset
-    const int64_t end = static_cast<int64_t>(P) * a.F * esize;
-    const char *src = static_cast<const char *>(tab);
-#pragma unroll
-    for (int i = 0; i < kWinPre; ++i) {
-        const int q = t + i * nt;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (q < n && wb + 16 * q < end) v = *reinterpret_cast<const uint4 *>(src + wb + 16 * q);
-        pre[i] = v;
-    }
-}
-
-__device__ __forceinline__ void win_store_table(const WinArgs &a, void *dst, int esize,
-                                                const uint4 (&pre)[kWinPre]) {
-    const int t = threadIdx.x, nt = blockDim.x;
-    const int n = (a.W * a.F * esize) >> 4;
-#pragma unroll
-    for (int i = 0; i < kWinPre; ++i) {
-        const int q = t + i * nt;
-        if (q < n) reinterpret_cast<uint4 *>(dst)[q] = pre[i];
-    }
-}
-
-// One window's steps of the wave's chain, four at a time: the records (scalars), then the
-// level bytes, then the table entries of the four steps are requested before the finish times
-// are advanced, so the memory round trips overlap.
-constexpr int kWinUnroll = 4;
-
 // max of two non-negative finite floats: their bit patterns order like unsigned integers, and
 // the integer max needs none of the NaN-quieting that the compiler adds to fmaxf on operands
 // loaded from memory.  Finish times and start floors here are always >= 0 and finite.
@@ -509,12 +430,141 @@ __device__ __forceinline__ float fmax_nonneg(float a, float b) {
     return __uint_as_float(x > y ? x : y);
 }
 
+struct WinArgs {
+    int W, wlog, nc, NC, F;
+    int blk_bytes, hdr_words;
+    int slots_lvl, slots_tab8, slots_tab4, slots_blk;   // prefetch slots per category
+    WinLayout L;
+};
+
+// Prefetch slots of each category for nt threads; false when they exceed kWinPre.
+__host__ __device__ inline bool win_slots(int W, int NC, int F, int blk_bytes, int nt, int *sl, int *st8,
+                                          int *st4, int *sb) {
+    *sl = (NC * (W / 16) + nt - 1) / nt;
+    *st8 = (W * F / 2 + nt - 1) / nt;
+    *st4 = (W * F / 4 + nt - 1) / nt;
+    *sb = (blk_bytes / 16 + nt - 1) / nt;
+    return *sl + *st8 + *sb <= kWinPre;
+}
+
+// One window's copy in flight: the thread's pieces (16 bytes each), slot by slot: the first
+// slots hold level rows, the next table rows, the next the step block (how many of each is the
+// same for every thread, so the category of a slot is uniform); which of them read as zero
+// (level columns past P, table rows past the last pack, pieces past the end); and the wave's
+// checkpoint (backward pass).
+struct WinSet {
+    uint4 v[kWinPre];
+    uint32_t zero;
+    float ck;
+};
+
+// Issues exactly kWinPre loads for window w (a piece past the end reads a valid address and is
+// zeroed when stored; unused slots read the first block piece), with the addresses as scalar
+// bases plus 32-bit lane offsets, so that the compiler counts them and waits at a commit for
+// the older window's loads only.  esize: bytes per table entry (8 forward, 4 backward).
+__device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__restrict__ levels,
+                                         const void *__restrict__ tab, int esize,
+                                         const uint4 *__restrict__ blocks, int64_t base, int64_t B,
+                                         int32_t P, int w, WinSet &s) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int rlog = a.wlog - 4;                                   // pieces per level row: W / 16
+    const int n_lvl = a.NC << rlog;
+    const int n_tab = (a.W * a.F * esize) >> 4;
+    const int n_blk = a.blk_bytes >> 4;
+    const int s_lvl = a.slots_lvl, s_tab = esize == 8 ? a.slots_tab8 : a.slots_tab4;
+    const int64_t wcol = static_cast<int64_t>(w) << a.wlog;
+    const uint8_t *lbase = levels + base * P + wcol;               // window's first column, row base
+    const int64_t tab_off = wcol * a.F * esize;                    // bytes
+    const uint32_t tab_left = static_cast<uint32_t>(static_cast<int64_t>(P) * a.F * esize - tab_off);
+    const char *tbase = static_cast<const char *>(tab) + tab_off;
+    const char *bbase = reinterpret_cast<const char *>(blocks + static_cast<int64_t>(w) * n_blk);
+    const int64_t rows_left = B - base;                             // rows of this workgroup in range
+    const int64_t cols_left = P - wcol;
+    uint32_t zero = 0u;
+#pragma unroll
+    for (int i = 0; i < kWinPre; ++i) {
+        const char *src;
+        uint32_t off;
+        bool z;
+        if (i < s_lvl) {
+            const int q = t + i * nt;
+            const int r = q >> rlog, k = q - (r << rlog);
+            const int rr = r < rows_left ? r : static_cast<int>(rows_left - 1);
+            z = q >= n_lvl || 16 * k >= cols_left;
+            off = z ? 0u : static_cast<uint32_t>(rr) * static_cast<uint32_t>(P) + 16u * static_cast<uint32_t>(k);
+            src = reinterpret_cast<const char *>(lbase);
+        } else if (i < s_lvl + s_tab) {
+            const int q = t + (i - s_lvl) * nt;
+            z = q >= n_tab || 16u * static_cast<uint32_t>(q) >= tab_left;
+            off = z ? 0u : 16u * static_cast<uint32_t>(q);
+            src = tbase;
+        } else {
+            const int q = t + (i - s_lvl - s_tab) * nt;
+            z = q >= n_blk || i >= s_lvl + s_tab + a.slots_blk;
+            off = z ? 0u : 16u * static_cast<uint32_t>(q);
+            src = bbase;
+        }
+        zero |= z ? 1u << i : 0u;
+        s.v[i] = *reinterpret_cast<const uint4 *>(src + off);
+    }
+    s.zero = zero;
+}
+
+// Copies window w's pieces into LDS buffer `buf` (level bytes >= F become 0 and mark their
+// candidate in `bad` when it is given).
+__device__ __forceinline__ void win_store(const WinArgs &a, char *lds, int buf, void *tabbuf, int esize,
+                                          uint32_t *bad, uint32_t addf, const WinSet &s) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int rlog = a.wlog - 4;
+    const int n_lvl = a.NC << rlog;
+    const int n_tab = (a.W * a.F * esize) >> 4;
+    const int n_blk = a.blk_bytes >> 4;
+    const int s_lvl = a.slots_lvl, s_tab = esize == 8 ? a.slots_tab8 : a.slots_tab4;
+    uint8_t *lvl = reinterpret_cast<uint8_t *>(lds) + buf * a.L.lvl_buf;
+    uint4 *blk = reinterpret_cast<uint4 *>(lds + a.L.off_blk + buf * a.blk_bytes);
+#pragma unroll
+    for (int i = 0; i < kWinPre; ++i) {
+        uint4 v = s.v[i];
+        if ((s.zero >> i) & 1u) v = make_uint4(0u, 0u, 0u, 0u);
+        if (i < s_lvl) {
+            const int q = t + i * nt;
+            if (q < n_lvl) {
+                const int r = q >> rlog, k = q - (r << rlog);
+                uint32_t b = 0u;
+                uint32_t *d = reinterpret_cast<uint32_t *>(lvl + r * a.L.lvl_pitch + 16 * k);
+                d[0] = clean_levels(v.x, addf, b);
+                d[1] = clean_levels(v.y, addf, b);
+                d[2] = clean_levels(v.z, addf, b);
+                d[3] = clean_levels(v.w, addf, b);
+                if (bad && b) bad[r] = 1u;
+            }
+        } else if (i < s_lvl + s_tab) {
+            const int q = t + (i - s_lvl) * nt;
+            if (q < n_tab) reinterpret_cast<uint4 *>(tabbuf)[q] = v;
+        } else if (i < s_lvl + s_tab + a.slots_blk) {
+            const int q = t + (i - s_lvl - s_tab) * nt;
+            if (q < n_blk) blk[q] = v;
+        }
+    }
+}
+
+// The wave's step range [k0, k1) in the window's block (scalars).
+__device__ __forceinline__ void win_range(const WinArgs &a, const char *lds, int buf, int ch, int &k0, int &k1) {
+    const int32_t *hdr = reinterpret_cast<const int32_t *>(lds + a.L.off_blk + buf * a.blk_bytes);
+    k0 = __builtin_amdgcn_readfirstlane(hdr[ch]);
+    k1 = __builtin_amdgcn_readfirstlane(hdr[ch + 1]);
+}
+
+// The windows' steps are walked four at a time: the records, then the level bytes, then the
+// table entries of the four steps are requested before the finish times advance, so the LDS
+// round trips overlap.
+constexpr int kWinUnroll = 4;
+
 template <bool SLACK, bool FIXED>
 __global__ void __launch_bounds__(kChainBlockThreads)
-chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restrict__ ws,
-                const int32_t *__restrict__ wbeg, const uint8_t *__restrict__ levels, int64_t B,
-                float *__restrict__ To, float *__restrict__ Eo, float *__restrict__ S,
-                float *__restrict__ ck, int64_t pitch) {
+chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ blocks,
+                const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ To,
+                float *__restrict__ Eo, float *__restrict__ S, float *__restrict__ ck, int64_t pitch) {
     extern __shared__ float4 smem[];
     char *lds = reinterpret_cast<char *>(smem);
     const int t = threadIdx.x, nt = blockDim.x;
@@ -534,6 +584,9 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restri
     float *tabt = reinterpret_cast<float *>(lds + L.off_x);       // backward: [2][W + 1][F]
     float *tile = reinterpret_cast<float *>(lds + L.off_tile);    // backward: [NC][W + 1]
     const uint32_t addf = (0x80u - static_cast<uint32_t>(F)) * 0x01010101u;
+    auto recs = [&](int buf) {
+        return reinterpret_cast<const ChainWinStep *>(lds + L.off_blk + buf * a.blk_bytes + 4 * a.hdr_words);
+    };
 
     // ------------------------------------------------------------------ forward
     for (int i = t; i < a.NC; i += nt) {
@@ -545,26 +598,24 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restri
         tab2[W * F + i] = make_float2(0.f, 0.f);
         tab2[L.tab_elems + W * F + i] = make_float2(0.f, 0.f);
     }
-    uint4 pl[kWinPre], pt[kWinPre];
-    win_load_levels(a, levels, base, B, P, 0, pl);
-    win_load_table(a, g.tab, 8, P, 0, pt);
+    WinSet s0, s1;
+    win_load(a, levels, g.tab, 8, blocks, base, B, P, 0, s0);
+    win_load(a, levels, g.tab, 8, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
     lds_barrier();
-    win_store_levels(a, lvl0, bad, addf, pl);
-    win_store_table(a, tab2, 8, pt);
+    win_store(a, lds, 0, tab2, 8, bad, addf, s0);
     lds_barrier();
     float f = 0.f;
     double ed = 0.0;
-    for (int w = 0; w < nwin; ++w) {
+    // window w from buffer w & 1; `ld` takes window w + 2, `cm` holds window w + 1
+    auto forward_window = [&](int w, WinSet &ld, WinSet &cm) {
         const int buf = w & 1;
-        const bool more = w + 1 < nwin;
-        if (more) {
-            win_load_levels(a, levels, base, B, P, w + 1, pl);
-            win_load_table(a, g.tab, 8, P, w + 1, pt);
-        }
+        win_load(a, levels, g.tab, 8, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
         if (SLACK) ck[(static_cast<int64_t>(w) * nc + ch) * pitch + gc] = f;
         const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
-        const float2 *tb = tab2 + buf * L.tab_elems;
-        const int k0 = wbeg[w * nc + ch], k1 = wbeg[(w + 1) * nc + ch];
+        const char *tb = reinterpret_cast<const char *>(tab2 + buf * L.tab_elems);
+        const ChainWinStep *rs = recs(buf);
+        int k0, k1;
+        win_range(a, lds, buf, ch, k0, k1);
         float eb = 0.f;
         int k = k0;
         for (; k + kWinUnroll <= k1; k += kWinUnroll) {
@@ -572,11 +623,12 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restri
             unsigned l[kWinUnroll];
             float2 te[kWinUnroll];
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) r[i] = ws[k + i];
+            for (int i = 0; i < kWinUnroll; ++i) r[i] = rs[k + i];
 #pragma unroll
             for (int i = 0; i < kWinUnroll; ++i) l[i] = lrow[r[i].col];
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) te[i] = tb[r[i].col * F + static_cast<int>(l[i])];
+            for (int i = 0; i < kWinUnroll; ++i)
+                te[i] = *reinterpret_cast<const float2 *>(tb + ((r[i].tf + static_cast<int>(l[i])) << 3));
 #pragma unroll
             for (int i = 0; i < kWinUnroll; ++i) {
                 f = fmax_nonneg(f, r[i].cst) + te[i].x;
@@ -585,18 +637,19 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restri
             }
         }
         for (; k < k1; ++k) {
-            const ChainWinStep r = ws[k];
-            const float2 te = tb[r.col * F + static_cast<int>(lrow[r.col])];
+            const ChainWinStep r = rs[k];
+            const float2 te = *reinterpret_cast<const float2 *>(tb + ((r.tf + static_cast<int>(lrow[r.col])) << 3));
             f = fmax_nonneg(f, r.cst) + te.x;
             if (FIXED) f += r.dur;
             eb += te.y;
         }
         ed += static_cast<double>(eb);
-        if (more) {
-            win_store_levels(a, lvl0 + (buf ^ 1) * L.lvl_buf, bad, addf, pl);
-            win_store_table(a, tab2 + (buf ^ 1) * L.tab_elems, 8, pt);
-        }
+        if (w + 1 < nwin) win_store(a, lds, buf ^ 1, tab2 + (buf ^ 1) * L.tab_elems, 8, bad, addf, cm);
         lds_barrier();
+    };
+    for (int w = 0; w < nwin; w += 2) {
+        forward_window(w, s0, s1);
+        if (w + 1 < nwin) forward_window(w + 1, s1, s0);
     }
     // chains' makespans and energies -> the candidate's (chain order)
     double *esum = reinterpret_cast<double *>(lds + L.off_x);
@@ -631,72 +684,74 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restri
         tabt[L.tab_elems + W * F + i] = 0.f;
     }
     const int top = nwin - 1;
-    win_load_levels(a, levels, base, B, P, top, pl);
-    win_load_table(a, g.tabt, 4, P, top, pt);
-    float fck = ck[(static_cast<int64_t>(top) * nc + ch) * pitch + gc];
+    auto ck_at = [&](int w) { return ck[(static_cast<int64_t>(w) * nc + ch) * pitch + gc]; };
+    win_load(a, levels, g.tabt, 4, blocks, base, B, P, top, s0);
+    s0.ck = ck_at(top);
+    win_load(a, levels, g.tabt, 4, blocks, base, B, P, top >= 1 ? top - 1 : 0, s1);
+    s1.ck = ck_at(top >= 1 ? top - 1 : 0);
     float lft = tfin[cl];                                   // NaN for a candidate with bad levels
-    win_store_levels(a, lvl0 + (top & 1) * L.lvl_buf, nullptr, addf, pl);
-    win_store_table(a, tabt + (top & 1) * L.tab_elems, 4, pt);
+    win_store(a, lds, top & 1, tabt + (top & 1) * L.tab_elems, 4, nullptr, addf, s0);
+    float fck = s0.ck;
     lds_barrier();
-    asm volatile("" : "+v"(fck));   // (see the end of the loop)
+    // the checkpoint is taken where its load has landed: left to its first use in the next
+    // window, the wait would also cover that window's prefetch loads
+    asm volatile("" : "+v"(fck));
     float *trow = tile + cl * (W + 1);
     const int per_row = W >> 2;                             // float4 pieces per tile row
-    for (int w = top; w >= 0; --w) {
+    // window w from buffer w & 1; `ld` takes window w - 2, `cm` holds window w - 1
+    auto backward_window = [&](int w, WinSet &ld, WinSet &cm) {
         const int buf = w & 1;
-        const bool more = w >= 1;
-        float fnext = 0.f;
-        if (more) {
-            win_load_levels(a, levels, base, B, P, w - 1, pl);
-            win_load_table(a, g.tabt, 4, P, w - 1, pt);
-            fnext = ck[(static_cast<int64_t>(w - 1) * nc + ch) * pitch + gc];
-        }
+        win_load(a, levels, g.tabt, 4, blocks, base, B, P, w >= 2 ? w - 2 : 0, ld);
+        ld.ck = ck_at(w >= 2 ? w - 2 : 0);
         const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
-        const float *tb = tabt + buf * L.tab_elems;
-        const int k0 = wbeg[w * nc + ch], k1 = wbeg[(w + 1) * nc + ch];
-        // finish times of the window's steps, from the checkpoint, into the tile
+        const char *tb = reinterpret_cast<const char *>(tabt + buf * L.tab_elems);
+        const ChainWinStep *rs = recs(buf);
+        int k0, k1;
+        win_range(a, lds, buf, ch, k0, k1);
+        // finish times of the window's steps, from the checkpoint, into the tile (a group's times
+        // are read before its finish times are written)
+        auto time_of = [&](const ChainWinStep &r) {
+            float tt = *reinterpret_cast<const float *>(tb + ((r.tf + static_cast<int>(lrow[r.col])) << 2));
+            if (FIXED) tt += r.dur;
+            return tt;
+        };
         float fb = fck;
         int k = k0;
         for (; k + kWinUnroll <= k1; k += kWinUnroll) {
             ChainWinStep r[kWinUnroll];
-            unsigned l[kWinUnroll];
-            float tt[kWinUnroll];
+            float tt[kWinUnroll], fi[kWinUnroll];
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) r[i] = ws[k + i];
+            for (int i = 0; i < kWinUnroll; ++i) r[i] = rs[k + i];
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) l[i] = lrow[r[i].col];
-#pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) tt[i] = tb[r[i].col * F + static_cast<int>(l[i])];
+            for (int i = 0; i < kWinUnroll; ++i) tt[i] = time_of(r[i]);
 #pragma unroll
             for (int i = 0; i < kWinUnroll; ++i) {
                 fb = fmax_nonneg(fb, r[i].cst) + tt[i];
-                if (FIXED) fb += r[i].dur;
-                trow[r[i].col] = fb;
+                fi[i] = fb;
             }
+#pragma unroll
+            for (int i = 0; i < kWinUnroll; ++i) trow[r[i].col] = fi[i];
         }
         for (; k < k1; ++k) {
-            const ChainWinStep r = ws[k];
-            fb = fmax_nonneg(fb, r.cst) + tb[r.col * F + static_cast<int>(lrow[r.col])];
-            if (FIXED) fb += r.dur;
+            const ChainWinStep r = rs[k];
+            fb = fmax_nonneg(fb, r.cst) + time_of(r);
             trow[r.col] = fb;
         }
         // slack = latest finish - finish, walking the steps in reverse (the chain's columns are
-        // distinct, except fixed nodes' pad column, which is never stored)
+        // distinct, except fixed nodes' pad column, which is never stored): a group's finish
+        // times are read before its slack is written
         k = k1;
         for (; k - kWinUnroll >= k0; k -= kWinUnroll) {
             ChainWinStep r[kWinUnroll];
-            unsigned l[kWinUnroll];
             float tt[kWinUnroll], ef[kWinUnroll];
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) r[i] = ws[k - 1 - i];
+            for (int i = 0; i < kWinUnroll; ++i) r[i] = rs[k - 1 - i];
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) l[i] = lrow[r[i].col];
-#pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) tt[i] = tb[r[i].col * F + static_cast<int>(l[i])];
+            for (int i = 0; i < kWinUnroll; ++i) tt[i] = time_of(r[i]);
 #pragma unroll
             for (int i = 0; i < kWinUnroll; ++i) ef[i] = trow[r[i].col];
 #pragma unroll
             for (int i = 0; i < kWinUnroll; ++i) {
-                if (FIXED) tt[i] += r[i].dur;
                 ef[i] = lft - ef[i];
                 lft = lft - tt[i];
             }
@@ -704,15 +759,15 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restri
             for (int i = 0; i < kWinUnroll; ++i) trow[r[i].col] = ef[i];
         }
         for (; k > k0; --k) {
-            const ChainWinStep r = ws[k - 1];
-            float tt = tb[r.col * F + static_cast<int>(lrow[r.col])];
-            if (FIXED) tt += r.dur;
+            const ChainWinStep r = rs[k - 1];
+            const float tt = time_of(r);
             trow[r.col] = lft - trow[r.col];
             lft = lft - tt;
         }
-        if (more) {
-            win_store_levels(a, lvl0 + (buf ^ 1) * L.lvl_buf, nullptr, addf, pl);
-            win_store_table(a, tabt + (buf ^ 1) * L.tab_elems, 4, pt);
+        float fnext = 0.f;
+        if (w >= 1) {
+            win_store(a, lds, buf ^ 1, tabt + (buf ^ 1) * L.tab_elems, 4, nullptr, addf, cm);
+            fnext = cm.ck;
         }
         lds_barrier();
         // slack tile -> pack order; a wave covers 4 candidates x 16 pieces when rows are long
@@ -736,11 +791,12 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const ChainWinStep *__restri
             if (row < B && col < P) *reinterpret_cast<float4 *>(S + row * P + col) = v;
         }
         lds_barrier();
-        // take the checkpoint here, where its load (issued at the window's start) has landed;
-        // left to the next window's first use, the wait would also cover that window's
-        // prefetch loads
         asm volatile("" : "+v"(fnext));
         fck = fnext;
+    };
+    for (int w = top; w >= 0; w -= 2) {
+        backward_window(w, s0, s1);
+        if (w >= 1) backward_window(w - 1, s1, s0);
     }
 }
 
@@ -759,20 +815,16 @@ bool staged_ok(const DevGraph &g, const DevChains &c) {
 size_t round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 }  // namespace
 
-bool chain_window_shape(int32_t nc, int32_t F, int32_t P, int32_t *win, int32_t *groups) {
-    if (nc < 1 || nc > kWinMaxWaves || F < 1 || F > 128 || P < 1 || P % 16 != 0) return false;
+bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int32_t *groups) {
+    if (nc < 1 || nc > kWinMaxWaves || F < 1 || F > 128 || W < 16 || W > 256 || blk_bytes % 16 != 0)
+        return false;
     const int G = kWinMaxWaves / nc;
     const int NC = 64 * G, nthreads = 64 * G * nc;
-    for (int W = 256; W >= 16; W >>= 1) {
-        const WinLayout L = win_layout(W, NC, F, G * nc);
-        const int lvl_pieces = NC * (W / 16), tab_pieces = W * F * 8 / 16;
-        if (L.total <= kWinLds && lvl_pieces <= kWinPre * nthreads && tab_pieces <= kWinPre * nthreads) {
-            *win = W;
-            *groups = G;
-            return true;
-        }
-    }
-    return false;
+    const WinLayout L = win_layout(W, NC, F, G * nc, blk_bytes);
+    int sl, st8, st4, sb;
+    if (L.total > kWinLds || !win_slots(W, NC, F, blk_bytes, nthreads, &sl, &st8, &st4, &sb)) return false;
+    *groups = G;
+    return true;
 }
 
 bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
@@ -812,8 +864,8 @@ hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, c
         reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED>),
         hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kWinLds));
     if (attr != hipSuccess) return attr;
-    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED>), gd, bd, lds, s, g, c, a, c.wsteps, c.wbeg, levels, B,
-                       T, E, S, ck, pitch);
+    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED>), gd, bd, lds, s, g, c, a, c.blocks, levels, B, T, E,
+                       S, ck, pitch);
     return hipGetLastError();
 }
 
@@ -827,7 +879,11 @@ hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t 
     a.nc = c.nc;
     a.NC = 64 * c.groups;
     a.F = g.F;
-    a.L = win_layout(a.W, a.NC, a.F, c.groups * c.nc);
+    a.blk_bytes = c.blk_bytes;
+    a.hdr_words = c.hdr_words;
+    win_slots(a.W, a.NC, a.F, a.blk_bytes, 64 * c.groups * c.nc, &a.slots_lvl, &a.slots_tab8, &a.slots_tab4,
+              &a.slots_blk);
+    a.L = win_layout(a.W, a.NC, a.F, c.groups * c.nc, c.blk_bytes);
     const int64_t grid = win_grid(c, B);
     const int64_t pitch = grid * a.NC;
     char *p = static_cast<char *>(scratch);

@@ -540,55 +540,84 @@ bool is_pow2(int32_t x) { return x > 0 && (x & (x - 1)) == 0; }
 // candidate-dependent predecessor and successor each) and at most 64 of them: steps[k][lane]
 // is the k-th step of chain `lane`, padded with steps that leave a finish time unchanged.
 // Returns false when the schedule does not have that shape.
-// Windowed layout of the chains (see DevChains): steps grouped by the window of their pack
-// (a fixed node stays in the window of the chain's previous pack, window 0 before the first).
+// Windowed layout of the chains (see DevChains): steps grouped by the window of their pack (a
+// fixed node stays in the window of the chain's previous pack, window 0 before the first), one
+// block per window.  Takes the widest window (256, 128, ... 16 packs) whose working set fits.
 // Returns false when some chain goes back to an earlier window or no window width fits.
 bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
                          const std::vector<std::vector<int32_t>> &chains,
-                         std::vector<emo::ChainWinStep> *wsteps, std::vector<int32_t> *wbeg,
-                         emo::DevChains *dc) {
+                         std::vector<uint4> *blocks, emo::DevChains *dc) {
     const int32_t nc = static_cast<int32_t>(chains.size());
-    int32_t W = 0, G = 0;
-    if (!emo::chain_window_shape(nc, g.F, g.P, &W, &G)) return false;
-    const int32_t nwin = (g.P + W - 1) / W;
-    wsteps->clear();
-    wbeg->assign(static_cast<size_t>(nwin + 1) * nc, 0);
-    int32_t fixed = 0;
-    for (int32_t c = 0; c < nc; ++c) {
-        int32_t w = 0;
-        // wbeg[x*nc + c] = first step of chain c in a window >= x
-        int32_t next_win = 0;
-        for (int32_t i : chains[c]) {
-            const int32_t v = sc.seq[i];
-            const int32_t p = g.pack[v];
-            if (p >= 0) {
-                if (p / W < w) return false;
-                w = p / W;
+    // (level offsets within a workgroup's rows are 32-bit: at most 1024 rows of P bytes)
+    if (nc < 1 || nc > 16 || g.P < 16 || g.P % 16 != 0 || g.P >= (1 << 21)) return false;
+    const int32_t hdr_words = (nc + 1 + 3) / 4 * 4;
+    for (int32_t W = 256; W >= 16; W >>= 1) {
+        const int32_t nwin = (g.P + W - 1) / W;
+        // window of every step; per-window record counts
+        std::vector<std::vector<int32_t>> win(nc);
+        std::vector<int32_t> count(nwin, 0);
+        bool monotone = true;
+        int32_t fixed = 0;
+        for (int32_t c = 0; c < nc && monotone; ++c) {
+            int32_t w = 0;
+            for (int32_t i : chains[c]) {
+                const int32_t p = g.pack[sc.seq[i]];
+                if (p >= 0) {
+                    if (p / W < w) {
+                        monotone = false;
+                        break;
+                    }
+                    w = p / W;
+                } else {
+                    fixed = 1;
+                }
+                win[c].push_back(w);
+                ++count[w];
             }
-            while (next_win <= w) (*wbeg)[static_cast<size_t>(next_win++) * nc + c] =
-                static_cast<int32_t>(wsteps->size());
-            emo::ChainWinStep st;
-            st.col = p >= 0 ? p - w * W : W;
-            st.cst = sc.cst[i];
-            st.dur = p >= 0 ? 0.f : g.dur[v];
-            st.pad = 0;
-            if (p < 0) fixed = 1;
-            wsteps->push_back(st);
         }
-        while (next_win <= nwin) (*wbeg)[static_cast<size_t>(next_win++) * nc + c] =
-            static_cast<int32_t>(wsteps->size());
+        if (!monotone) return false;   // narrower windows would not be monotone either
+        const int32_t rec_max = *std::max_element(count.begin(), count.end());
+        const int32_t blk_bytes = 4 * hdr_words + 16 * rec_max;
+        int32_t G = 0;
+        if (!emo::chain_window_fits(nc, g.F, W, blk_bytes, &G)) continue;
+        const size_t words = static_cast<size_t>(blk_bytes) / 4;
+        std::vector<uint32_t> buf(static_cast<size_t>(nwin) * words, 0u);
+        std::vector<int32_t> fill(nwin, 0);   // records written per window
+        // chain after chain: chain c's records of window w follow those of chains < c
+        for (int32_t c = 0; c < nc; ++c) {
+            for (int32_t w = 0; w < nwin; ++w) buf[static_cast<size_t>(w) * words + c] = static_cast<uint32_t>(fill[w]);
+            for (size_t k = 0; k < chains[c].size(); ++k) {
+                const int32_t i = chains[c][k];
+                const int32_t v = sc.seq[i];
+                const int32_t p = g.pack[v];
+                const int32_t w = win[c][k];
+                emo::ChainWinStep st;
+                st.col = p >= 0 ? p - w * W : W;
+                st.cst = sc.cst[i];
+                st.dur = p >= 0 ? 0.f : g.dur[v];
+                st.tf = st.col * g.F;
+                std::memcpy(&buf[static_cast<size_t>(w) * words + hdr_words + 4 * static_cast<size_t>(fill[w])],
+                            &st, sizeof(st));
+                ++fill[w];
+            }
+        }
+        for (int32_t w = 0; w < nwin; ++w) buf[static_cast<size_t>(w) * words + nc] = static_cast<uint32_t>(fill[w]);
+        blocks->assign(buf.size() / 4, make_uint4(0u, 0u, 0u, 0u));
+        std::memcpy(blocks->data(), buf.data(), buf.size() * sizeof(uint32_t));
+        dc->nc = nc;
+        dc->win = W;
+        dc->nwin = nwin;
+        dc->groups = G;
+        dc->fixed = fixed;
+        dc->hdr_words = hdr_words;
+        dc->blk_bytes = blk_bytes;
+        return true;
     }
-    dc->nc = nc;
-    dc->win = W;
-    dc->nwin = nwin;
-    dc->groups = G;
-    dc->fixed = fixed;
-    return true;
+    return false;
 }
 
 bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::ChainStep> *steps,
-                  std::vector<int32_t> *pos, emo::DevChains *dc,
-                  std::vector<emo::ChainWinStep> *wsteps, std::vector<int32_t> *wbeg) {
+                  std::vector<int32_t> *pos, emo::DevChains *dc, std::vector<uint4> *blocks) {
     const int32_t n = static_cast<int32_t>(sc.seq.size());
     if (n == 0) return false;
     std::vector<int32_t> heads;
@@ -630,10 +659,9 @@ bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::Cha
     dc->lane_log = lane_log;
     dc->len = len;
     dc->t_const = g.t_const;
-    if (!build_chain_windows(g, sc, chains, wsteps, wbeg, dc)) {
+    if (!build_chain_windows(g, sc, chains, blocks, dc)) {
         dc->win = 0;
-        wsteps->clear();
-        wbeg->clear();
+        blocks->clear();
     }
     return true;
 }
@@ -896,10 +924,9 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     g->jg = make_jit_graph(*g, sf);
     std::vector<emo::ChainStep> csteps;
     std::vector<int32_t> cpos;
-    std::vector<emo::ChainWinStep> cwsteps;
-    std::vector<int32_t> cwbeg;
+    std::vector<uint4> cblocks;
     emo::DevChains dc;
-    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc, &cwsteps, &cwbeg);
+    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc, &cblocks);
     in.chain_lanes = chains_ok ? dc.lanes : 0;
     in.chain_window = chains_ok ? dc.win : 0;
     const int32_t nops = static_cast<int32_t>(sf.seq.size());
@@ -926,10 +953,7 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
         if (chains_ok) {
             if ((s = upload(*g, csteps, &dc.steps)) != EMO_OK) return s;
             if ((s = upload(*g, cpos, &dc.pos)) != EMO_OK) return s;
-            if (dc.win > 0) {
-                if ((s = upload(*g, cwsteps, &dc.wsteps)) != EMO_OK) return s;
-                if ((s = upload(*g, cwbeg, &dc.wbeg)) != EMO_OK) return s;
-            }
+            if (dc.win > 0 && (s = upload(*g, cblocks, &dc.blocks)) != EMO_OK) return s;
             g->chains = dc;
         }
     }

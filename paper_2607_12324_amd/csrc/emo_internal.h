@@ -105,12 +105,13 @@ struct ChainStep {                    // 16 bytes
     float dur;                        // fixed duration (pack == -1); 0 for padding
     int32_t pad;
 };
-// Step of the windowed layout: the chain's steps in pack window w (packs [w*win, (w+1)*win)).
+// Step record of the windowed layout: the chain's steps in pack window w (packs
+// [w*win, (w+1)*win)).
 struct ChainWinStep {                 // 16 bytes
     int32_t col;                      // pack id - w*win, or win for a fixed node
     float cst;                        // latest finish among candidate-independent predecessors
     float dur;                        // fixed duration; 0 for a pack
-    int32_t pad;
+    int32_t tf;                       // col * F: the step's first table entry in the window
 };
 struct DevChains {
     int32_t lanes = 0;                // lanes per candidate: a power of two in [1, 64]
@@ -119,19 +120,21 @@ struct DevChains {
     float t_const = 0.f;              // makespan floor from candidate-independent nodes
     const ChainStep *steps = nullptr; // [len][lanes]
     const int32_t *pos = nullptr;     // [P]: step * lanes + chain of each pack
-    // windowed layout (win > 0): chain c's steps in window w are wsteps[wbeg[w*nc + c] ..
-    // wbeg[(w+1)*nc + c]); it exists when every chain visits the windows in increasing order
+    // windowed layout (win > 0): one block of blk_bytes per window: hdr_words int32 (chain c's
+    // steps are records hdr[c] .. hdr[c+1]-1), then the window's ChainWinStep records, chain
+    // after chain; it exists when every chain visits the windows in increasing order
     int32_t nc = 0;                   // chains
     int32_t win = 0;                  // packs per window, a power of two in [16, 256]
     int32_t nwin = 0;
     int32_t groups = 0;               // groups of 64 candidates per workgroup
     int32_t fixed = 0;                // 1 if some step is a fixed node
-    const ChainWinStep *wsteps = nullptr;
-    const int32_t *wbeg = nullptr;    // [(nwin + 1)][nc]
+    int32_t hdr_words = 0;            // nc + 1 rounded up to a multiple of 4
+    int32_t blk_bytes = 0;
+    const uint4 *blocks = nullptr;    // [nwin][blk_bytes / 16]
 };
-// Window width and candidate groups per workgroup of the windowed kernel for a graph of `nc`
-// chains, P packs and F levels; false when it does not apply.
-bool chain_window_shape(int32_t nc, int32_t F, int32_t P, int32_t *win, int32_t *groups);
+// Whether the windowed kernel's LDS working set and prefetch fit for `nc` chains, F levels,
+// windows of W packs and step blocks of blk_bytes; sets the candidate groups per workgroup.
+bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int32_t *groups);
 // Whether a call runs the windowed kernel (the layout exists and the buffers are 16-byte
 // aligned).
 bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *slack);

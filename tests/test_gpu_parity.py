@@ -210,7 +210,7 @@ CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-strea
                # steps, so that the segmented kernels do not apply
                "16-streams": (8208, 16, 16), "3-streams-F8": (8224, 3, 8), "9-streams-F32": (8208, 9, 32)}
 # packs per window of the windowed kernel (0: lane-per-chain kernels only)
-CHAIN_WINDOW = {"1-stream": 16, "16-streams": 256, "3-streams-F8": 64, "9-streams-F32": 128}
+CHAIN_WINDOW = {"1-stream": 16, "16-streams": 256, "3-streams-F8": 64, "9-streams-F32": 64}
 
 
 def misaligned(torch, rows):
