@@ -555,10 +555,34 @@ __device__ __forceinline__ void win_range(const WinArgs &a, const char *lds, int
     k1 = __builtin_amdgcn_readfirstlane(hdr[ch + 1]);
 }
 
-// The windows' steps are walked four at a time: the records, then the level bytes, then the
-// table entries of the four steps are requested before the finish times advance, so the LDS
-// round trips overlap.
-constexpr int kWinUnroll = 4;
+// Keeps the LDS reads issued before it from being moved down to their first use (the compiler
+// would otherwise sink the next groups' reads and serialise the round trips again).
+__device__ __forceinline__ void win_issue_point() { asm volatile("" ::: "memory"); }
+
+// Four consecutive steps of the wave's chain: their records (column and table offset, start
+// floor, fixed duration) and, once read, the candidate's level bytes at their columns.  A chain's
+// steps in a window come in whole groups (padded with no-op steps), and every block has 8 no-op
+// steps on both sides, so reading up to two groups beyond a chain's range stays in the block.
+template <bool FIXED>
+struct WinGroup {
+    uint32_t ct[4];
+    float cst[4];
+    float dur[4];
+    unsigned lv[4];
+    __device__ __forceinline__ void read(const ChainWinStep *rs, int k) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint2 v = *reinterpret_cast<const uint2 *>(rs + k + i);
+            ct[i] = v.x;
+            cst[i] = __uint_as_float(v.y);
+            if (FIXED) dur[i] = rs[k + i].dur;
+        }
+    }
+    __device__ __forceinline__ void levels(const uint8_t *lrow) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) lv[i] = lrow[ct[i] & 0xffffu];
+    }
+};
 
 template <bool SLACK, bool FIXED>
 __global__ void __launch_bounds__(kChainBlockThreads)
@@ -617,31 +641,34 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
         int k0, k1;
         win_range(a, lds, buf, ch, k0, k1);
         float eb = 0.f;
-        int k = k0;
-        for (; k + kWinUnroll <= k1; k += kWinUnroll) {
-            ChainWinStep r[kWinUnroll];
-            unsigned l[kWinUnroll];
-            float2 te[kWinUnroll];
+        const int ng = (k1 - k0) >> 2;
+        // group g of 4 steps: its table entries are read while the next group's level bytes and
+        // the records of the group after it are in flight
+        auto stage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int g) {
+            float2 te[4];
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) r[i] = rs[k + i];
+            for (int i = 0; i < 4; ++i)
+                te[i] = *reinterpret_cast<const float2 *>(tb + (((A.ct[i] >> 16) + A.lv[i]) << 3));
+            Bn.levels(lrow);
+            C.read(rs, k0 + 4 * (g + 2));
+            win_issue_point();
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) l[i] = lrow[r[i].col];
-#pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i)
-                te[i] = *reinterpret_cast<const float2 *>(tb + ((r[i].tf + static_cast<int>(l[i])) << 3));
-#pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) {
-                f = fmax_nonneg(f, r[i].cst) + te[i].x;
-                if (FIXED) f += r[i].dur;
+            for (int i = 0; i < 4; ++i) {
+                f = fmax_nonneg(f, A.cst[i]) + te[i].x;
+                if (FIXED) f += A.dur[i];
                 eb += te[i].y;
             }
-        }
-        for (; k < k1; ++k) {
-            const ChainWinStep r = rs[k];
-            const float2 te = *reinterpret_cast<const float2 *>(tb + ((r.tf + static_cast<int>(lrow[r.col])) << 3));
-            f = fmax_nonneg(f, r.cst) + te.x;
-            if (FIXED) f += r.dur;
-            eb += te.y;
+        };
+        WinGroup<FIXED> G0, G1, G2;
+        G0.read(rs, k0);
+        G1.read(rs, k0 + 4);
+        G0.levels(lrow);
+        for (int g = 0; g < ng; g += 3) {
+            stage(G0, G1, G2, g);
+            if (g + 1 >= ng) break;
+            stage(G1, G2, G0, g + 1);
+            if (g + 2 >= ng) break;
+            stage(G2, G0, G1, g + 2);
         }
         ed += static_cast<double>(eb);
         if (w + 1 < nwin) win_store(a, lds, buf ^ 1, tab2 + (buf ^ 1) * L.tab_elems, 8, bad, addf, cm);
@@ -708,61 +735,70 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
         const ChainWinStep *rs = recs(buf);
         int k0, k1;
         win_range(a, lds, buf, ch, k0, k1);
-        // finish times of the window's steps, from the checkpoint, into the tile (a group's times
-        // are read before its finish times are written)
-        auto time_of = [&](const ChainWinStep &r) {
-            float tt = *reinterpret_cast<const float *>(tb + ((r.tf + static_cast<int>(lrow[r.col])) << 2));
-            if (FIXED) tt += r.dur;
-            return tt;
+        const int ng = (k1 - k0) >> 2;
+        auto times = [&](const WinGroup<FIXED> &A, float (&tt)[4]) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                tt[i] = *reinterpret_cast<const float *>(tb + (((A.ct[i] >> 16) + A.lv[i]) << 2));
+                if (FIXED) tt[i] += A.dur[i];
+            }
         };
+        // finish times of the window's steps, from the checkpoint, into the tile; pipelined like
+        // the forward pass
         float fb = fck;
-        int k = k0;
-        for (; k + kWinUnroll <= k1; k += kWinUnroll) {
-            ChainWinStep r[kWinUnroll];
-            float tt[kWinUnroll], fi[kWinUnroll];
+        auto fstage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int g) {
+            float tt[4], fi[4];
+            times(A, tt);
+            Bn.levels(lrow);
+            C.read(rs, k0 + 4 * (g + 2));
+            win_issue_point();
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) r[i] = rs[k + i];
-#pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) tt[i] = time_of(r[i]);
-#pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) {
-                fb = fmax_nonneg(fb, r[i].cst) + tt[i];
+            for (int i = 0; i < 4; ++i) {
+                fb = fmax_nonneg(fb, A.cst[i]) + tt[i];
                 fi[i] = fb;
             }
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) trow[r[i].col] = fi[i];
+            for (int i = 0; i < 4; ++i) trow[A.ct[i] & 0xffffu] = fi[i];
+        };
+        WinGroup<FIXED> G0, G1, G2;
+        G0.read(rs, k0);
+        G1.read(rs, k0 + 4);
+        G0.levels(lrow);
+        for (int g = 0; g < ng; g += 3) {
+            fstage(G0, G1, G2, g);
+            if (g + 1 >= ng) break;
+            fstage(G1, G2, G0, g + 1);
+            if (g + 2 >= ng) break;
+            fstage(G2, G0, G1, g + 2);
         }
-        for (; k < k1; ++k) {
-            const ChainWinStep r = rs[k];
-            fb = fmax_nonneg(fb, r.cst) + time_of(r);
-            trow[r.col] = fb;
-        }
-        // slack = latest finish - finish, walking the steps in reverse (the chain's columns are
-        // distinct, except fixed nodes' pad column, which is never stored): a group's finish
-        // times are read before its slack is written
-        k = k1;
-        for (; k - kWinUnroll >= k0; k -= kWinUnroll) {
-            ChainWinStep r[kWinUnroll];
-            float tt[kWinUnroll], ef[kWinUnroll];
+        // slack = latest finish - finish, walking the groups and their steps in reverse (the
+        // chain's columns are distinct, except the pad column of fixed nodes and no-op steps,
+        // which is never stored): a group's finish times are read before its slack is written
+        auto bstage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int g) {
+            float tt[4], ef[4];
+            times(A, tt);
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) r[i] = rs[k - 1 - i];
+            for (int i = 0; i < 4; ++i) ef[i] = trow[A.ct[i] & 0xffffu];
+            Bn.levels(lrow);
+            C.read(rs, k0 + 4 * (g - 2));
+            win_issue_point();
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) tt[i] = time_of(r[i]);
-#pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) ef[i] = trow[r[i].col];
-#pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) {
+            for (int i = 3; i >= 0; --i) {
                 ef[i] = lft - ef[i];
                 lft = lft - tt[i];
             }
 #pragma unroll
-            for (int i = 0; i < kWinUnroll; ++i) trow[r[i].col] = ef[i];
-        }
-        for (; k > k0; --k) {
-            const ChainWinStep r = rs[k - 1];
-            const float tt = time_of(r);
-            trow[r.col] = lft - trow[r.col];
-            lft = lft - tt;
+            for (int i = 0; i < 4; ++i) trow[A.ct[i] & 0xffffu] = ef[i];
+        };
+        G0.read(rs, k0 + 4 * (ng - 1));
+        G1.read(rs, k0 + 4 * (ng - 2));
+        G0.levels(lrow);
+        for (int g = ng - 1; g >= 0; g -= 3) {
+            bstage(G0, G1, G2, g);
+            if (g - 1 < 0) break;
+            bstage(G1, G2, G0, g - 1);
+            if (g - 2 < 0) break;
+            bstage(G2, G0, G1, g - 2);
         }
         float fnext = 0.f;
         if (w >= 1) {

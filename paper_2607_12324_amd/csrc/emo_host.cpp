@@ -553,9 +553,8 @@ bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
     const int32_t hdr_words = (nc + 1 + 3) / 4 * 4;
     for (int32_t W = 256; W >= 16; W >>= 1) {
         const int32_t nwin = (g.P + W - 1) / W;
-        // window of every step; per-window record counts
+        // window of every step
         std::vector<std::vector<int32_t>> win(nc);
-        std::vector<int32_t> count(nwin, 0);
         bool monotone = true;
         int32_t fixed = 0;
         for (int32_t c = 0; c < nc && monotone; ++c) {
@@ -572,18 +571,36 @@ bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
                     fixed = 1;
                 }
                 win[c].push_back(w);
-                ++count[w];
             }
         }
         if (!monotone) return false;   // narrower windows would not be monotone either
-        const int32_t rec_max = *std::max_element(count.begin(), count.end());
+        // records per window: 8 no-op steps on each side (reads run up to two groups of 4 past
+        // a chain's range) and each chain's steps padded to a multiple of 4
+        std::vector<int32_t> per(static_cast<size_t>(nwin) * nc, 0);
+        for (int32_t c = 0; c < nc; ++c)
+            for (int32_t w : win[c]) ++per[static_cast<size_t>(w) * nc + c];
+        int32_t rec_max = 0;
+        for (int32_t w = 0; w < nwin; ++w) {
+            int32_t n = 16;
+            for (int32_t c = 0; c < nc; ++c) n += (per[static_cast<size_t>(w) * nc + c] + 3) / 4 * 4;
+            rec_max = std::max(rec_max, n);
+        }
         const int32_t blk_bytes = 4 * hdr_words + 16 * rec_max;
         int32_t G = 0;
         if (!emo::chain_window_fits(nc, g.F, W, blk_bytes, &G)) continue;
         const size_t words = static_cast<size_t>(blk_bytes) / 4;
+        emo::ChainWinStep noop;
+        noop.ct = static_cast<uint32_t>(W) | (static_cast<uint32_t>(W * g.F) << 16);
+        noop.cst = 0.f;
+        noop.dur = 0.f;
+        noop.pad = 0u;
         std::vector<uint32_t> buf(static_cast<size_t>(nwin) * words, 0u);
-        std::vector<int32_t> fill(nwin, 0);   // records written per window
+        for (int32_t w = 0; w < nwin; ++w)
+            for (int32_t r = 0; r < rec_max; ++r)
+                std::memcpy(&buf[static_cast<size_t>(w) * words + hdr_words + 4 * static_cast<size_t>(r)], &noop,
+                            sizeof(noop));
         // chain after chain: chain c's records of window w follow those of chains < c
+        std::vector<int32_t> fill(nwin, 8);   // next record per window
         for (int32_t c = 0; c < nc; ++c) {
             for (int32_t w = 0; w < nwin; ++w) buf[static_cast<size_t>(w) * words + c] = static_cast<uint32_t>(fill[w]);
             for (size_t k = 0; k < chains[c].size(); ++k) {
@@ -591,15 +608,17 @@ bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
                 const int32_t v = sc.seq[i];
                 const int32_t p = g.pack[v];
                 const int32_t w = win[c][k];
+                const uint32_t col = static_cast<uint32_t>(p >= 0 ? p - w * W : W);
                 emo::ChainWinStep st;
-                st.col = p >= 0 ? p - w * W : W;
+                st.ct = col | ((col * static_cast<uint32_t>(g.F)) << 16);
                 st.cst = sc.cst[i];
                 st.dur = p >= 0 ? 0.f : g.dur[v];
-                st.tf = st.col * g.F;
+                st.pad = 0u;
                 std::memcpy(&buf[static_cast<size_t>(w) * words + hdr_words + 4 * static_cast<size_t>(fill[w])],
                             &st, sizeof(st));
                 ++fill[w];
             }
+            for (int32_t w = 0; w < nwin; ++w) fill[w] = (fill[w] + 3) / 4 * 4;
         }
         for (int32_t w = 0; w < nwin; ++w) buf[static_cast<size_t>(w) * words + nc] = static_cast<uint32_t>(fill[w]);
         blocks->assign(buf.size() / 4, make_uint4(0u, 0u, 0u, 0u));

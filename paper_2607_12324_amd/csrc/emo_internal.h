@@ -108,10 +108,11 @@ struct ChainStep {                    // 16 bytes
 // Step record of the windowed layout: the chain's steps in pack window w (packs
 // [w*win, (w+1)*win)).
 struct ChainWinStep {                 // 16 bytes
-    int32_t col;                      // pack id - w*win, or win for a fixed node
+    uint32_t ct;                      // col | (col * F) << 16, col = pack id - w*win, or win for
+                                      // a fixed node (or a no-op step)
     float cst;                        // latest finish among candidate-independent predecessors
     float dur;                        // fixed duration; 0 for a pack
-    int32_t tf;                       // col * F: the step's first table entry in the window
+    uint32_t pad;
 };
 struct DevChains {
     int32_t lanes = 0;                // lanes per candidate: a power of two in [1, 64]
@@ -121,8 +122,9 @@ struct DevChains {
     const ChainStep *steps = nullptr; // [len][lanes]
     const int32_t *pos = nullptr;     // [P]: step * lanes + chain of each pack
     // windowed layout (win > 0): one block of blk_bytes per window: hdr_words int32 (chain c's
-    // steps are records hdr[c] .. hdr[c+1]-1), then the window's ChainWinStep records, chain
-    // after chain; it exists when every chain visits the windows in increasing order
+    // steps are records hdr[c] .. hdr[c+1]-1), then the window's ChainWinStep records: 8 no-op
+    // steps, each chain's steps padded with no-op steps to a multiple of 4, chain after chain,
+    // 8 no-op steps; it exists when every chain visits the windows in increasing order
     int32_t nc = 0;                   // chains
     int32_t win = 0;                  // packs per window, a power of two in [16, 256]
     int32_t nwin = 0;
