@@ -30,10 +30,17 @@ HBM_PEAK_GBS = 8000.0
 VALU_PEAK_TOPS = 39.3   # 256 CUs x 64 fp32 lanes x 2.4 GHz, one op per lane per clock (no packed math)
 
 
-def kernel_source_hash() -> str:
+# sources that make the kernels of each kind (last_kernels): graph preparation and the
+# selection code are common to all of them
+KIND_SOURCES = {0: ("emo_kernels.hip",), 1: ("emo_jit.cpp",), 2: ("emo_jit.cpp",),
+                3: ("emo_chains.hip", "emo_kernels.hip"), 4: ("emo_chains.hip", "emo_kernels.hip")}
+
+
+def kernel_source_hash(kind: int) -> str:
+    """Hash of the sources that generate the kernels of `kind`, so that a committed counter
+    summary goes stale only when the kernel it measured can have changed."""
     h = hashlib.sha256()
-    for name in ("emo_kernels.hip", "emo_chains.hip", "emo_internal.h", "emo_host.cpp", "emo_jit.cpp",
-                 "emo_select.h"):
+    for name in KIND_SOURCES[kind] + ("emo_internal.h", "emo_host.cpp", "emo_select.h"):
         with open(os.path.join(ROOT, "paper_2607_12324_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -197,7 +204,7 @@ def main():
     # the backward pass (min per edge, subtractions per node) doubles it
     ops_per_cand = (info["num_dynamic_edges"] + 2 * P + 2) * (2 if spec.slack else 1)
     valu_tops = B * ops_per_cand / (main_ms / 1e3) / 1e12
-    src_hash = kernel_source_hash()
+    src_hash = kernel_source_hash(info["last_kernels"])
     if info["last_kernels"] == 2:      # segmented kernels: the timed unit is the whole chain
         kname = "emo_chain"
     elif info["last_kernels"] == 3:
