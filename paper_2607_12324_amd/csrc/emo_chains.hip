@@ -398,7 +398,9 @@ __host__ __device__ inline WinLayout win_layout(int W, int NC, int F, int nwaves
     L.off_blk = round16u(L.off_tfin + 4u * static_cast<uint32_t>(NC));
     L.off_x = L.off_blk + 2u * static_cast<uint32_t>(blk_bytes);
     L.tab_elems = static_cast<uint32_t>(W + 1) * static_cast<uint32_t>(F);
-    const uint32_t fwd = 2u * L.tab_elems * 8u;
+    // (256 spare float2 entries: a lookup with an invalid level byte reads at most 255 entries
+    // past a table buffer; the backward tables are followed by the slack tile)
+    const uint32_t fwd = (2u * L.tab_elems + 256u) * 8u;
     const uint32_t comb = 64u * 8u * kWinMaxWaves + static_cast<uint32_t>(nwaves) * 64u * 4u;
     L.off_tile = L.off_x + round16u(2u * L.tab_elems * 4u);
     const uint32_t bwd = L.off_tile - L.off_x + static_cast<uint32_t>(NC) * static_cast<uint32_t>(W + 1) * 4u;
@@ -414,12 +416,10 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Replaces the level bytes >= F of a word by 0 and reports them (F <= 128: a byte b < 128 gets
-// bit 7 from (b + 128 - F) exactly when b >= F, and a byte >= 128 has it already).
-__device__ __forceinline__ uint32_t clean_levels(uint32_t x, uint32_t addf, uint32_t &bad) {
-    const uint32_t hi = (((x & 0x7f7f7f7fu) + addf) | x) & 0x80808080u;
-    bad |= hi;
-    return x & ~((hi >> 7) * 0xffu);
+// Bit 7 of every byte of a word that holds a level >= F (F <= 128: a byte b < 128 gets bit 7
+// from (b + 128 - F) exactly when b >= F, and a byte >= 128 has it already).
+__device__ __forceinline__ uint32_t bad_levels(uint32_t x, uint32_t addf) {
+    return (((x & 0x7f7f7f7fu) + addf) | x) & 0x80808080u;
 }
 
 // max of two non-negative finite floats: their bit patterns order like unsigned integers, and
@@ -510,8 +510,11 @@ __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__rest
     s.zero = zero;
 }
 
-// Copies window w's pieces into LDS buffer `buf` (level bytes >= F become 0 and mark their
-// candidate in `bad` when it is given).
+// Copies window w's pieces into LDS buffer `buf`; a level byte >= F marks its candidate in `bad`
+// when it is given (the forward pass).  Such a byte is not cleared: the candidate's makespan,
+// energy and slack become NaN whatever its lookups read, and a lookup at column c <= W with
+// level l <= 255 stays inside the workgroup's LDS (at most 255 entries past the window's table,
+// which the layout leaves room for).
 __device__ __forceinline__ void win_store(const WinArgs &a, char *lds, int buf, void *tabbuf, int esize,
                                           uint32_t *bad, uint32_t addf, const WinSet &s) {
     const int t = threadIdx.x, nt = blockDim.x;
@@ -530,13 +533,14 @@ __device__ __forceinline__ void win_store(const WinArgs &a, char *lds, int buf, 
             const int q = t + i * nt;
             if (q < n_lvl) {
                 const int r = q >> rlog, k = q - (r << rlog);
-                uint32_t b = 0u;
                 uint32_t *d = reinterpret_cast<uint32_t *>(lvl + r * a.L.lvl_pitch + 16 * k);
-                d[0] = clean_levels(v.x, addf, b);
-                d[1] = clean_levels(v.y, addf, b);
-                d[2] = clean_levels(v.z, addf, b);
-                d[3] = clean_levels(v.w, addf, b);
-                if (bad && b) bad[r] = 1u;
+                d[0] = v.x;
+                d[1] = v.y;
+                d[2] = v.z;
+                d[3] = v.w;
+                if (bad && (bad_levels(v.x, addf) | bad_levels(v.y, addf) | bad_levels(v.z, addf) |
+                            bad_levels(v.w, addf)))
+                    bad[r] = 1u;
             }
         } else if (i < s_lvl + s_tab) {
             const int q = t + (i - s_lvl) * nt;
