@@ -23,6 +23,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "emo_internal.h"
 
 namespace emo {
@@ -900,10 +902,18 @@ template <bool SLACK, bool FIXED>
 hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, const DevGraph &g,
                                   const DevChains &c, const WinArgs &a, const uint8_t *levels, int64_t B,
                                   float *T, float *E, float *S, float *ck, int64_t pitch) {
-    static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kWinLds));
-    if (attr != hipSuccess) return attr;
+    // the dynamic LDS limit is raised once per device (the caller made the graph's device current)
+    static std::atomic<uint64_t> done{0};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
+    if (!bit || !(done.load(std::memory_order_acquire) & bit)) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kWinLds));
+        if (e != hipSuccess) return e;
+        done.fetch_or(bit, std::memory_order_acq_rel);
+    }
     hipLaunchKernelGGL((chains_windowed<SLACK, FIXED>), gd, bd, lds, s, g, c, a, c.blocks, levels, B, T, E,
                        S, ck, pitch);
     return hipGetLastError();
