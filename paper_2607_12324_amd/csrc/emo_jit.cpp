@@ -435,6 +435,7 @@ const char *kPrelude = R"(
 typedef unsigned char u8;
 #define EMO_AT(buf, r) (*(__typeof__(&(buf)[0]))((const char *)((buf) + (long long)(r) * bp) + o4))
 typedef unsigned int emo_u32x4 __attribute__((ext_vector_type(4)));
+typedef float emo_f32x4 __attribute__((ext_vector_type(4)));
 #define EMO_GLOBAL __attribute__((address_space(1)))
 #define EMO_NAN __builtin_nanf("")
 )";
@@ -728,14 +729,16 @@ __device__ __forceinline__ void emo_cflush(const float *stg, float *__restrict__
   for (int m = 0; m < 8; ++m) {
     const int r = 8 * m + lane / 8;
     const int sw = r ^ (8 * b);
-    float4 v;
+    emo_f32x4 v;
     v.x = stg[(4 * b + 0) * 64 + sw];
     v.y = stg[(4 * b + 1) * 64 + sw];
     v.z = stg[(4 * b + 2) * 64 + sw];
     v.w = stg[(4 * b + 3) * 64 + sw];
     long long row = wbase + r;
     row = row < B ? row : B - 1;   // lanes past the batch hold candidate B - 1's values
-    *(float4 *)(S + row * )" << P << R"(LL + p0 + 4 * b) = v;
+    // streaming store: slack is never read back here, and leaving it out of L2 keeps the
+    // checkpoint rows that the backward kernels read several times there
+    __builtin_nontemporal_store(v, (emo_f32x4 *)(S + row * )" << P << R"(LL + p0 + 4 * b));
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();

@@ -277,6 +277,32 @@ def test_chain_lanes(torch, emo, case):
         parity.assert_eval(host(Tm), host(Em), T_or, E_or, True, case + " lane-per-chain")
 
 
+def test_chain_windows_small_batches(torch, emo):
+    """Windowed kernel with batches smaller than a workgroup's 64 candidates and one past it
+    (lanes past the batch repeat the last row and store nothing), repeated calls bit for bit."""
+    g = synth.stream_graph(77, 8208, 16, 16)
+    rng = np.random.default_rng(77)
+    gh = emo.EmoGraph(g, device=0)
+    assert gh.info()["chain_window"] == 256
+    for B in (1, 3, 64, 65):
+        rows = pins.random_rows(rng, g, B)
+        print(f"[case] windowed chains B={B}", flush=True)
+        lv = dev(torch, rows)
+        T, E = gh.eval_policies(lv)
+        S = gh.slack(lv)
+        torch.cuda.synchronize()
+        assert gh.info()["last_kernels"] == 4
+        T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+        parity.assert_eval(host(T), host(E), T_or, E_or, True, f"windowed B={B}")
+        S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(B)])
+        parity.assert_slack(host(S), S_or, T_or, True, f"windowed B={B} pack slack")
+        T2, E2 = gh.eval_policies(lv)
+        S2 = gh.slack(lv)
+        assert np.array_equal(host(T).view(np.uint32), host(T2).view(np.uint32))
+        assert np.array_equal(host(E).view(np.uint32), host(E2).view(np.uint32))
+        assert np.array_equal(host(S).view(np.uint32), host(S2).view(np.uint32))
+
+
 @pytest.mark.parametrize("lengths", [[3100, 2900, 3400], [3100, 2900, 3406]],
                          ids=["lane-per-chain", "windowed"])
 def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
