@@ -277,6 +277,26 @@ def test_chain_lanes(torch, emo, case):
         parity.assert_eval(host(Tm), host(Em), T_or, E_or, True, case + " lane-per-chain")
 
 
+def test_one_kernel_ragged_batches(torch, emo):
+    """512-pack graph in one kernel: batches that leave the last workgroup partly or wholly past
+    the batch, with an invalid level among the rows, against the oracle, and the selection."""
+    g = synth.config_graph(3)
+    gh = emo.EmoGraph(g, device=0)
+    for B in (1, 65, 777, 1025, 3000):
+        rows = synth.config_policies(3, g, 5000 + B, B)
+        if B > 2:
+            rows[B // 2, 7] = 200   # an invalid level
+        print(f"[case] one kernel B={B}", flush=True)
+        T, E = gh.eval_policies(dev(torch, rows))
+        torch.cuda.synchronize()
+        assert gh.info()["last_kernels"] == 1
+        T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+        assert np.isnan(host(T)[B // 2]) == (B > 2)
+        parity.assert_eval(host(T), host(E), T_or, E_or, True, f"one kernel B={B}")
+        tgt = float(np.float32(1.05 * float(np.nanmin(T_or))))
+        run_all(torch, emo, g, rows, [tgt], per_node=False, what=f"one kernel B={B}")
+
+
 def test_chain_windows_small_batches(torch, emo):
     """Windowed kernel with batches smaller than a workgroup's 64 candidates and one past it
     (lanes past the batch repeat the last row and store nothing), repeated calls bit for bit."""
