@@ -93,13 +93,15 @@ typedef struct {
     int32_t specialized;          /* bit 0: specialised eval/select kernels are compiled,
                                      bit 1: specialised slack kernels are compiled,
                                      bit 2: specialisation was tried and failed,
-                                     bit 3: segmented kernels are compiled */
+                                     bit 3: segmented kernels are compiled,
+                                     bit 4: cut-segment kernels are compiled */
     float compile_seconds;        /* time spent compiling specialised kernels */
     int32_t last_kernels;         /* kernels of the last batch call: 0 interpreted, 1 one
                                      specialised kernel, 2 segmented specialised kernels,
                                      3 chain lanes (one lane per chain and candidate),
                                      4 windowed chain lanes (a wave per chain, 64 candidates;
-                                     pack windows staged in LDS) */
+                                     pack windows staged in LDS), 5 cut segments (the
+                                     segments between cut nodes evaluated in parallel) */
     int32_t chain_lanes;          /* lanes per candidate of the chain-lane kernels, 0 when the
                                      candidate-dependent nodes do not form at most 64 disjoint
                                      chains */
@@ -110,6 +112,22 @@ typedef struct {
                                      it does not apply (more than 16 chains, a chain that goes
                                      back to an earlier window, P not a multiple of 16); calls
                                      use it when levels and slack are 16-byte aligned */
+    int32_t cut_segments;         /* segments of the cut-segment kernels, 0 when they do not
+                                     apply.  A cut node is one that every other node precedes
+                                     or follows (an all-stream synchronisation): no path
+                                     bypasses it, so its slack is zero and, measured from the
+                                     finish time of the cut before them, the finish times and
+                                     slack of the nodes between two cuts depend on those
+                                     nodes' levels only (Eq. 1; slack as in Sec. III-A:
+                                     time off the critical path).  The kernels cut the graph there, in segments of
+                                     at most 256 packs, when packs are visited in increasing
+                                     id, segments start at multiples of 32 packs, and every
+                                     time value is a multiple of one power of two u with the
+                                     sum of all nodes' largest durations below 2^24 u (every
+                                     sum is then exact in fp32 in any order).  Batch calls of
+                                     graphs too large for one specialised kernel use them
+                                     when levels (and slack) are 16-byte aligned and fewer
+                                     than 2^30 candidates are evaluated. */
 } emo_graph_info;
 
 /* Which kernels evaluate a graph.
@@ -127,7 +145,7 @@ typedef enum {
 } emo_kernel_mode;
 
 /*
- * Load an execution graph and its pack tables (Sec. IV-C; Alg. 1 REQUIRE line).
+ * Load an execution graph and its pack tables (Sec. IV-C; the inputs of Alg. 1).
  *   num_nodes, num_edges  V >= 0, E >= 0.
  *   edge_src, edge_dst    host int32 [E]: node edge_src[i] finishes before edge_dst[i] starts.
  *                         Duplicates are merged.  A self-loop or cycle gives EMO_ERR_CYCLE.
@@ -242,6 +260,13 @@ emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len);
  * of reading stored ones.  Same buffer convention as emo_graph_specialized_source.
  * EMO_ERR_UNSUPPORTED when the graph uses no segmented kernels. */
 emo_status emo_graph_segmented_source(emo_graph_t g, char *buf, int64_t *len);
+
+/* Diagnostics: the HIP source of the cut-segment kernels of `g` (see cut_segments in
+ * emo_graph_info): one kernel whose grid row y evaluates segment y for a group of candidates
+ * (forward only, and forward with slack), and the kernel that adds up the segments' makespans
+ * and energy blocks and completes the selection.  Same buffer convention as
+ * emo_graph_specialized_source.  EMO_ERR_UNSUPPORTED when the graph has no cut segments. */
+emo_status emo_graph_cut_source(emo_graph_t g, char *buf, int64_t *len);
 
 /* Static string naming a status code. */
 const char *emo_status_string(emo_status s);

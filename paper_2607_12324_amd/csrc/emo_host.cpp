@@ -10,6 +10,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -79,6 +80,9 @@ constexpr int32_t kJitMaxSlackOps = 160;  // every finish time stays in a VGPR
 constexpr int32_t kChainSegOps = 256;
 constexpr int32_t kChainSubOps = 64;
 constexpr int32_t kChainMaxOps = 8192;
+// Cut-segment kernels: packs per segment at most, packs per recompute sub-segment.
+constexpr int32_t kCutMaxPacks = 256;
+constexpr int32_t kCutSubPacks = 32;
 // ... and only for graphs of small cut width: the finish times live at once in the forward pass
 // are held in registers (wider graphs keep the interpreting kernels, which spill cold values to
 // device scratch by design).
@@ -188,6 +192,11 @@ struct emo_graph_s {
     int chain_state = 0;                     // 0 not tried, 1 compiled, -1 failed
     emo::JitModule jc;
     emo::DevChains chains;                   // chain-lane program (lanes == 0: not chains)
+    // cut-segment kernels
+    emo::CutPlan cut_plan;
+    bool cut_ok = false;
+    int cut_state = 0;                       // 0 not tried, 1 compiled, -1 failed
+    emo::JitModule jk;
     Arena arena;                             // per-call scratch, kept between calls
     // profiling hook (hipEvent_t handles owned by the caller)
     hipEvent_t ev_begin = nullptr;
@@ -528,6 +537,7 @@ void release_device(emo_graph_s *g) {
         DeviceGuard guard(g->device);
         emo::jit_unload(&g->jm);
         emo::jit_unload(&g->jc);
+        emo::jit_unload(&g->jk);
         for (void *p : g->allocations) (void)hipFree(p);
         arena_free(g->arena);
     }
@@ -708,6 +718,70 @@ emo::JitGraph make_jit_graph(const emo_graph_s &g, const Schedule &sc) {
     return jg;
 }
 
+// Steps that are cut nodes: nodes that every other node precedes or follows.  At position i of
+// a topological order that holds exactly when no edge jumps over position i, no node before it
+// is a sink and no node after it is a source.  Returns their step indices in increasing order.
+std::vector<int32_t> cut_steps(const emo_graph_s &g, const Schedule &sf) {
+    const int32_t V = g.V;
+    std::vector<int32_t> pos(V), jump(static_cast<size_t>(V) + 1, 0), step(V, -1);
+    for (int32_t i = 0; i < V; ++i) pos[g.order[i]] = i;
+    for (int32_t u = 0; u < V; ++u)
+        for (int32_t k = g.succ_off[u]; k < g.succ_off[u + 1]; ++k) {
+            const int32_t a = pos[u], b = pos[g.succ[k]];
+            if (b > a + 1) {
+                jump[a + 1]++;
+                jump[b]--;
+            }
+        }
+    for (size_t i = 0; i < sf.seq.size(); ++i) step[sf.seq[i]] = static_cast<int32_t>(i);
+    std::vector<char> source_after(static_cast<size_t>(V) + 1, 0);
+    for (int32_t i = V - 1; i >= 0; --i) {
+        const int32_t v = g.order[i];
+        source_after[i] = source_after[i + 1] || g.pred_off[v] == g.pred_off[v + 1];
+    }
+    std::vector<int32_t> cuts;
+    bool sink_before = false;
+    int32_t over = 0;
+    for (int32_t i = 0; i < V; ++i) {
+        over += jump[i];
+        const int32_t v = g.order[i];
+        if (over == 0 && !sink_before && !source_after[i + 1] && step[v] >= 0) cuts.push_back(step[v]);
+        sink_before = sink_before || g.succ_off[v] == g.succ_off[v + 1];
+    }
+    std::sort(cuts.begin(), cuts.end());
+    return cuts;
+}
+
+// Whether every sum and difference of durations along paths is an exact fp32 number, whatever
+// the order of the additions: all time values (table times and fixed durations) are multiples
+// of one power of two u, and the sum over all nodes of their largest duration is below 2^24 u.
+bool exact_time_sums(const emo_graph_s &g, const float *pack_time) {
+    int emin = INT_MAX;
+    double total = 0.0;
+    auto visit = [&](float x) {
+        if (x <= 0.f) return;
+        int e = 0;
+        const float m = std::frexp(x, &e);
+        const uint32_t M = static_cast<uint32_t>(std::ldexp(m, 24));
+        emin = std::min(emin, e - 24 + __builtin_ctz(M));
+    };
+    for (int32_t v = 0; v < g.V; ++v) {
+        if (g.pack[v] >= 0) {
+            float mx = 0.f;
+            for (int32_t f = 0; f < g.F; ++f) {
+                const float x = pack_time[static_cast<size_t>(g.pack[v]) * g.F + f];
+                visit(x);
+                mx = std::max(mx, x);
+            }
+            total += mx;
+        } else {
+            visit(g.dur[v]);
+            total += g.dur[v];
+        }
+    }
+    return emin == INT_MAX || total < std::ldexp(1.0, 24 + emin);
+}
+
 size_t jit_table_bytes(const emo_graph_s &g) {
     return (static_cast<size_t>(g.P) * g.F + (is_pow2(g.F) ? 0 : emo::kTablePad)) * sizeof(float2);
 }
@@ -774,15 +848,37 @@ int ensure_chain(emo_graph_s *g) {
     return 1;
 }
 
+// Generates and compiles the cut-segment kernels once; returns 1 when they are ready.
+int ensure_cut(emo_graph_s *g) {
+    std::lock_guard<std::mutex> lock(g->jit_mu);
+    if (g->cut_state != 0) return g->cut_state;
+    const std::string src = emo::jit_generate_cut(g->jg, g->cut_plan);
+    DeviceGuard guard(g->device);
+    emo::JitModule m;
+    std::string log;
+    if (emo::jit_compile_cut(src, g->cut_plan, &m, &log) != 0) {
+        g->jit_log = log;
+        g->cut_state = -1;
+        g->info.specialized |= 4;
+        return -1;
+    }
+    g->jk = m;
+    g->cut_state = 1;
+    g->info.specialized |= 16;
+    g->info.compile_seconds += static_cast<float>(m.compile_seconds);
+    return 1;
+}
+
 bool aligned(const void *p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
 
-// Which kernels a batch call uses.
-enum class Path { kInterpreted = 0, kSingle = 1, kChain = 2, kChainLanes = 3 };
+// Which kernels a batch call uses (the value of emo_graph_info.last_kernels, except that the
+// windowed form of the chain lanes reports 4).
+enum class Path { kInterpreted = 0, kSingle = 1, kChain = 2, kChainLanes = 3, kCut = 5 };
 
 // Chooses the kernels of a batch call, compiling specialised kernels on first use.  Returns
 // EMO_OK and sets *path, or an error in EMO_KERNELS_SPECIALIZED mode.
 emo_status choose_path(emo_graph_s *g, const uint8_t *levels, const float *slack, bool per_node,
-                       Path *path) {
+                       int64_t B, Path *path) {
     *path = Path::kInterpreted;
     if (g->kernel_mode == EMO_KERNELS_INTERPRETED) return EMO_OK;
     if (slack && per_node) return EMO_OK;   // per-node slack: interpreted kernels only
@@ -792,6 +888,17 @@ emo_status choose_path(emo_graph_s *g, const uint8_t *levels, const float *slack
     if (chain_lanes) {
         *path = Path::kChainLanes;
         return EMO_OK;
+    }
+    // graphs with cut nodes, too large for one kernel: the segments between cuts in parallel
+    const bool single_ok = slack ? g->jit_slack_eligible : g->jit_eligible;
+    if (!single_ok && g->cut_ok && B < (int64_t(1) << 30) && aligned(levels, 16) &&
+        (!slack || aligned(slack, 16))) {
+        if (ensure_cut(g) == 1) {
+            *path = Path::kCut;
+            return EMO_OK;
+        }
+        if (g->kernel_mode == EMO_KERNELS_SPECIALIZED)
+            return fail(EMO_ERR_DEVICE, "cut-segment kernels failed to compile: %.400s", g->jit_log.c_str());
     }
     if (!aligned(levels, static_cast<size_t>(emo::jit_level_width(g->jg)))) return EMO_OK;
     bool single = false, chain = false;
@@ -955,6 +1062,9 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     const bool narrow = pe.n_hot + pe.n_cold <= kChainMaxLive;
     g->chain_eval = narrow && nops > kJitMaxOps && nops <= kChainMaxOps;
     g->chain_slack = narrow && nops > kJitMaxSlackOps && nops <= kChainMaxOps;
+    g->cut_plan = emo::jit_cut_plan(g->jg, cut_steps(*g, sf), kCutMaxPacks, kCutSubPacks);
+    g->cut_ok = g->cut_plan.segments() >= 2 && nops <= kChainMaxOps && exact_time_sums(*g, pack_time);
+    in.cut_segments = g->cut_ok ? g->cut_plan.segments() : 0;
 
     if (device >= 0) {
         DeviceGuard guard(device);
@@ -1043,6 +1153,22 @@ emo_status emo_graph_segmented_source(emo_graph_t g, char *buf, int64_t *len) {
     return ok();
 }
 
+emo_status emo_graph_cut_source(emo_graph_t g, char *buf, int64_t *len) {
+    if (!g || !len) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
+    if (!g->cut_ok) return fail(EMO_ERR_UNSUPPORTED, "the graph has no cut segments");
+    const std::string src = emo::jit_generate_cut(g->jg, g->cut_plan);
+    const int64_t need = static_cast<int64_t>(src.size()) + 1;
+    if (!buf) {
+        *len = need;
+        return ok();
+    }
+    if (*len < need) return fail(EMO_ERR_INVALID_ARGUMENT, "buffer of %lld bytes, %lld needed",
+                                 (long long)*len, (long long)need);
+    std::memcpy(buf, src.c_str(), static_cast<size_t>(need));
+    *len = need;
+    return ok();
+}
+
 emo_status emo_graph_topo_order(emo_graph_t g, int32_t *order, int32_t *depth) {
     if (!g || (!order && g->V > 0)) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
     if (g->V > 0) std::memcpy(order, g->order.data(), sizeof(int32_t) * g->V);
@@ -1083,17 +1209,19 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     if (!makespan && !energy && !slack && !mask && !result) return ok();
     if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
     Path path = Path::kInterpreted;
-    if ((s = choose_path(g, levels, slack, per_node != 0, &path)) != EMO_OK) return s;
+    if ((s = choose_path(g, levels, slack, per_node != 0, B, &path)) != EMO_OK) return s;
     DeviceGuard guard(g->device);
     // one selection partial record per block of the evaluating kernel
     const int64_t nblocks = path == Path::kSingle  ? emo::jit_blocks(g->jm, B)
                             : path == Path::kChain ? emo::jit_chain_blocks(g->jc, B)
+                            : path == Path::kCut   ? emo::jit_cut_blocks(g->jk, B)
                                                    : emo::forward_blocks(B);   // also chain lanes
     const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
     size_t part_bytes = result ? static_cast<size_t>(nblocks) * emo::kPartialBytes : 0;
     part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
     size_t work_bytes = 0;
     if (path == Path::kChain) work_bytes = emo::chain_scratch_bytes(g->jc.plan, B);
+    else if (path == Path::kCut) work_bytes = emo::cut_scratch_bytes(g->jk.cut_plan, B);
     else if (path == Path::kChainLanes) work_bytes = emo::chains_scratch_bytes(g->dg, g->chains, levels, B, slack);
     else if (path == Path::kInterpreted)
         work_bytes = slack ? emo::slack_scratch_bytes(prog, B) : emo::forward_scratch_bytes(g->dg.eval, B);
@@ -1114,7 +1242,10 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
                                : static_cast<int32_t>(path);
     hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
     if (e == hipSuccess) {
-        if (path == Path::kChain) {
+        if (path == Path::kCut) {
+            e = emo::jit_launch_cut(g->jk, levels, B, g->dg.tab, work, slack, makespan, energy, target,
+                                    mask, part, st);
+        } else if (path == Path::kChain) {
             e = emo::jit_launch_chain(g->jc, levels, B, g->dg.tab, g->dg.tabt, work, slack, makespan,
                                       energy, target, mask, part, st);
         } else if (path == Path::kChainLanes) {

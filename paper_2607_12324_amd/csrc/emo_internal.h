@@ -204,6 +204,36 @@ struct ChainPlan {
 inline int64_t chain_pitch(int64_t B) { return (B + 63) / 64 * 64; }
 size_t chain_scratch_bytes(const ChainPlan &cp, int64_t B);
 
+// Cut-segment kernels, for graphs with cut steps: steps that every other node of the graph
+// precedes or follows (an all-stream synchronisation, for instance).  No path bypasses a cut,
+// so a cut step is on every longest path and has zero slack; measured from the finish time of
+// the cut before it, the finish times, latest start times and slack of the steps between two
+// cuts depend on those steps' levels only.  With every duration a multiple of one power of two
+// u and the sum of all nodes' largest durations below 2^24 u, each of these values is an exact
+// fp32 number however the additions are ordered, so the segments are evaluated independently
+// and in parallel (one kernel, one grid row per segment), each writing its local makespan and
+// its energy blocks; a last kernel adds them up in order (makespan, energy, selection) and
+// overwrites the slack rows of candidates with an invalid level with NaN.  A segment kernel
+// takes a few segments (grid rows); compile time grows faster than linearly with the code of
+// one kernel, so the segments are spread over several kernels.
+struct CutPlan {
+    std::vector<int32_t> seg;       // segment boundaries in steps: seg[0] = 0 < ... < seg[m] = n;
+                                    // every segment but possibly the last ends with a cut step
+    bool closed_last = true;        // the last segment ends with a cut step as well
+    std::vector<int32_t> sub;       // recompute sub-segments of the slack kernel (refine seg)
+    std::vector<int32_t> blk0;      // first energy block row of each segment; blk0[m] = rows
+    std::vector<char> ck;           // f_i is read by a later sub-segment of its segment
+    int block = 512;                // workgroup of the segment kernels and the finishing kernel
+    int per_kernel = 4;             // segments per segment kernel (grid rows); the kernels of
+                                    // consecutive groups of segments run one after another
+    int segments() const { return static_cast<int>(seg.size()) - 1; }
+    int kernels() const { return (segments() + per_kernel - 1) / per_kernel; }
+};
+
+// Scratch of a cut-segment evaluation, each [rows][bp] floats with bp = chain_pitch(B):
+//   D (local makespan of each segment, NaN for an invalid level) [m], energy blocks [blk0[m]]
+size_t cut_scratch_bytes(const CutPlan &cp, int64_t B);
+
 struct JitModule {
     hipModule_t module = nullptr;
     hipFunction_t select = nullptr;  // forward pass with optional outputs and selection
@@ -217,6 +247,12 @@ struct JitModule {
     bool chain = false;
     ChainPlan plan;
     std::vector<hipFunction_t> cf, cb;   // forward kernel of each segment, backward kernel
+    // cut-segment kernels
+    bool cut = false;
+    CutPlan cut_plan;
+    std::vector<hipFunction_t> kf;       // segment kernels, forward only (one per group)
+    std::vector<hipFunction_t> ks;       // segment kernels, forward and slack
+    hipFunction_t kfin = nullptr;        // makespan, energy, selection, NaN rows
 };
 
 // Bytes per level load in generated kernels (16, 4 or 1): the alignment they need.
@@ -235,6 +271,19 @@ hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B
                             const float2 *tab, const float *tabt, void *scratch, float *S,
                             float *T, float *E, float target, uint32_t *mask, void *part,
                             hipStream_t s);
+// Plan of the cut-segment kernels over the cut steps `cuts` (increasing step indices): segments
+// of whole cut-to-cut pieces with at most max_packs packs each, recompute sub-segments of
+// sub_packs packs.  Returns an empty plan (no segments) when a piece is larger.
+CutPlan jit_cut_plan(const JitGraph &g, const std::vector<int32_t> &cuts, int max_packs, int sub_packs);
+std::string jit_generate_cut(const JitGraph &g, const CutPlan &cp);
+int jit_compile_cut(const std::string &src, const CutPlan &cp, JitModule *out, std::string *log);
+// Selection partial records of a cut-segment evaluation.
+int64_t jit_cut_blocks(const JitModule &m, int64_t B);
+// Segment kernel (forward only, or with slack S) and the finishing kernel.  scratch holds
+// cut_scratch_bytes(plan, B) bytes.
+hipError_t jit_launch_cut(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
+                          void *scratch, float *S, float *T, float *E, float target, uint32_t *mask,
+                          void *part, hipStream_t s);
 // 0 on success; otherwise *log holds the compiler's or loader's message.
 int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log);
 void jit_unload(JitModule *m);

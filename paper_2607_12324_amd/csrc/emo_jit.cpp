@@ -262,7 +262,11 @@ struct RangeOpts {
     long long base_pack = 0, tab_end = 0;          // table window (LevelPlan)
     bool declare_row = true, preload = true;
     bool checks = true;                            // record invalid level bytes in `bad`
-    bool time_only = false;                        // `tab` holds times only (floats)
+    bool time_only = false;                        // read times only: tab[..] + tsel
+    std::string tsel;                              // "" (times table) or ".x" ((t, e) table)
+    const std::vector<char> *ck_copy = nullptr;    // copy f_i to c<i> where set
+    int blk_row0 = -1;                             // >= 0: store each energy block (64 packs
+                                                   // from npk0) to row blk_row0 + q of Ebg
 };
 
 // Forward walk over steps [a, b) (Eq. 1): declares f<i> for each of them (values of earlier
@@ -291,7 +295,8 @@ LevelPlan emit_forward_range(std::ostringstream &o, const JitGraph &g, const Ran
         const JitOp &op = g.ops[i];
         if (op.pack >= 0 && lp.needs_release(op.pack)) {
             std::vector<std::string> ride;
-            if (r.accumulate) ride = {"eb", "ed", "bad"};
+            if (r.accumulate) ride = r.blk_row0 >= 0 ? std::vector<std::string>{"eb", "bad"}
+                                                     : std::vector<std::string>{"eb", "ed", "bad"};
             else ride = {"bad"};
             for (int j = since; j < i; ++j)
                 if (last_use[j] >= i) ride.push_back("f" + std::to_string(j));
@@ -303,19 +308,25 @@ LevelPlan emit_forward_range(std::ostringstream &o, const JitGraph &g, const Ran
             if (level_expr) (*level_expr)[i] = b;
             if (r.time_only) {
                 o << "  float f" << i << " = " << est_expr(g, i, "f") << " + tab[" << lp.row_entry(op.pack)
-                  << " + " << b << "];\n";
+                  << " + " << b << "]" << r.tsel << ";\n";
             } else {
                 o << "  const float2 te" << i << " = tab[" << lp.row_entry(op.pack) << " + " << b << "];\n";
                 o << "  float f" << i << " = " << est_expr(g, i, "f") << " + te" << i << ".x;\n";
             }
             if (r.accumulate) {
                 o << "  eb += te" << i << ".y;\n";
-                if (++npk % 64 == 0) o << "  ed += (double)eb;\n  eb = 0.f;\n";
+                if (++npk % 64 == 0) {
+                    if (r.blk_row0 >= 0)
+                        o << "  EMO_AT(Ebg, " << r.blk_row0 + (npk - r.npk0) / 64 - 1 << ") = eb;\n  eb = 0.f;\n";
+                    else
+                        o << "  ed += (double)eb;\n  eb = 0.f;\n";
+                }
             }
         } else {
             o << "  float f" << i << " = " << est_expr(g, i, "f") << " + " << flit(op.dur) << ";\n";
         }
         if (r.accumulate && op.out.empty()) o << "  T = fmaxf(T, f" << i << ");\n";
+        if (r.ck_copy && (*r.ck_copy)[i]) o << "  c" << i << " = f" << i << ";\n";
         if (r.ck_row && (*r.ck_row)[i] >= 0) {
             o << "  " << ((*r.ck_always)[i] ? "" : "if (full) ") << "EMO_AT(ck, " << (*r.ck_row)[i]
               << ") = f" << i << ";\n";
@@ -888,6 +899,307 @@ size_t chain_scratch_bytes(const ChainPlan &cp, int64_t B) {
     return bp * (4 * static_cast<size_t>(cp.n_ck + cp.n_bk + 2) + 8);
 }
 
+// ------------------------------------------------------------------ cut-segment kernels
+
+namespace {
+constexpr size_t kCutTableLds = 32 * 1024;   // (t, e) table window of one segment in LDS
+
+int packs_in(const JitGraph &g, int a, int b) {
+    int n = 0;
+    for (int i = a; i < b; ++i) n += g.ops[i].pack >= 0 ? 1 : 0;
+    return n;
+}
+}  // namespace
+
+CutPlan jit_cut_plan(const JitGraph &g, const std::vector<int32_t> &cuts, int max_packs, int sub_packs) {
+    CutPlan cp;
+    const int n = static_cast<int>(g.ops.size());
+    if (cuts.empty() || !g.pack_monotone || g.P % 32 != 0) return cp;
+    // a segment's (t, e) table rows stay within the LDS window (whole slack tiles of 32 packs)
+    const long long fit = (static_cast<long long>(kCutTableLds / (sizeof(float) * 2)) -
+                           (is_pow2(g.F) ? 0 : kTablePad)) / g.F / 32 * 32;
+    max_packs = static_cast<int>(std::min<long long>(max_packs, fit));
+    if (max_packs < 32) return cp;
+    std::vector<int> npk_before(n + 1, 0);
+    for (int i = 0; i < n; ++i) npk_before[i + 1] = npk_before[i] + (g.ops[i].pack >= 0 ? 1 : 0);
+    // pieces between consecutive cuts (each ends with its cut), then the steps after the last;
+    // only cuts after a multiple of 32 packs can end a segment (whole slack tiles)
+    std::vector<int> ends;
+    for (int c : cuts)
+        if (npk_before[c + 1] % 32 == 0) ends.push_back(c + 1);
+    cp.closed_last = !ends.empty() && ends.back() == n;
+    if (!cp.closed_last) ends.push_back(n);
+    // segments: as many whole pieces as max_packs allows
+    std::vector<int32_t> seg = {0};
+    int last_end = -1;
+    for (int e : ends) {
+        if (npk_before[e] - npk_before[seg.back()] <= max_packs) {
+            last_end = e;
+            continue;
+        }
+        if (last_end <= seg.back()) return CutPlan();   // one piece alone is too large
+        seg.push_back(last_end);
+        if (npk_before[e] - npk_before[last_end] > max_packs) return CutPlan();
+        last_end = e;
+    }
+    seg.push_back(last_end);
+    const int m = static_cast<int>(seg.size()) - 1;
+    if (m < 2) return CutPlan();
+    for (int j = 0; j < m; ++j) {
+        const int a = seg[j], b = seg[j + 1];
+        const bool closed = j + 1 < m || cp.closed_last;
+        // no edge leaves a segment except from its final cut, and every edge into it comes from
+        // the cut before it (the property the cuts were found by; checked again here)
+        for (int i = a; i < b; ++i) {
+            for (int k : g.ops[i].out)
+                if (k >= b && !(closed && i == b - 1)) return CutPlan();
+            for (int k : g.ops[i].in)
+                if (k < a && k != a - 1) return CutPlan();
+            if (j > 0 && g.ops[i].cst != 0.f) return CutPlan();
+        }
+        // slack tiles of 32 packs never straddle two segments; the table window fits in LDS
+        int lo = g.P, hi = -1;
+        for (int i = a; i < b; ++i)
+            if (g.ops[i].pack >= 0) {
+                lo = std::min(lo, g.ops[i].pack);
+                hi = std::max(hi, g.ops[i].pack);
+            }
+        if (hi < 0 || lo % 32 != 0 || (hi + 1) % 32 != 0) return CutPlan();
+        const size_t ent = static_cast<size_t>(hi - lo + 1) * g.F + (is_pow2(g.F) ? 0 : kTablePad);
+        if (ent * sizeof(float) * 2 > kCutTableLds) return CutPlan();
+    }
+    cp.seg = seg;
+    // energy blocks of 64 packs counted from each segment's start
+    int rows = 0;
+    for (int j = 0; j < m; ++j) {
+        cp.blk0.push_back(rows);
+        rows += (packs_in(g, seg[j], seg[j + 1]) + 63) / 64;
+    }
+    cp.blk0.push_back(rows);
+    // recompute sub-segments of sub_packs packs (a multiple of 32: whole slack tiles)
+    std::vector<int> sub_of(n);
+    for (int j = 0; j < m; ++j) {
+        const int a = seg[j], b = seg[j + 1];
+        cp.sub.push_back(a);
+        for (int c = a + 1, start = a; c < b; ++c)
+            if (npk_before[c] - npk_before[start] >= sub_packs && (npk_before[c] - npk_before[a]) % 32 == 0) {
+                cp.sub.push_back(c);
+                start = c;
+            }
+    }
+    cp.sub.push_back(n);
+    for (size_t r = 0; r + 1 < cp.sub.size(); ++r)
+        for (int i = cp.sub[r]; i < cp.sub[r + 1]; ++i) sub_of[i] = static_cast<int>(r);
+    cp.ck.assign(n, 0);
+    for (int j = 0; j < m; ++j)
+        for (int i = seg[j]; i < seg[j + 1]; ++i)
+            for (int k : g.ops[i].out)
+                if (k < seg[j + 1] && sub_of[k] != sub_of[i]) cp.ck[i] = 1;
+    return cp;
+}
+
+size_t cut_scratch_bytes(const CutPlan &cp, int64_t B) {
+    const size_t bp = static_cast<size_t>(chain_pitch(B));
+    return bp * 4 * static_cast<size_t>(cp.segments() + cp.blk0.back());
+}
+
+namespace {
+
+TabWindow cut_window(const JitGraph &g, const CutPlan &cp, int j) {
+    return chain_window(g, cp.seg[j], cp.seg[j + 1], kCutTableLds, sizeof(float) * 2);
+}
+
+// Whether step i's latest start time is read: some predecessor lies in its own segment.
+bool reads_start(const JitGraph &g, int i, int a) {
+    for (int k : g.ops[i].in)
+        if (k >= a) return true;
+    return false;
+}
+
+// Backward pass of segment j (slack): the sub-segments from last to first, each recomputing its
+// finish times from the checkpoint copies c<k> (or 0 for the cut before the segment) and level
+// words loaded again, then walking its steps backwards.  Latest finish times are local: the
+// segment's makespan Db for its final cut and for sinks.
+void emit_cut_backward(std::ostringstream &o, const JitGraph &g, const CutPlan &cp, int j,
+                       const TabWindow &w) {
+    const int a = cp.seg[j], b = cp.seg[j + 1];
+    const bool closed = j + 1 < cp.segments() || cp.closed_last;
+    o << "  {\n";
+    o << "  const bool isbad = D != D;\n  const float Db = isbad ? 0.f : D;\n";
+    o << "  unsigned int zb = 0u;\n  __asm__ __volatile__(\"\" : \"+v\"(zb));\n";
+    o << "  unsigned int bad = 0u;\n  (void)bad;\n";
+    o << LevelPlan::row_decl(jit_level_width(g));
+    for (int i = a; i < b; ++i)
+        if (reads_start(g, i, a)) o << "  float s" << i << ";\n";
+    int r_first = 0;
+    while (cp.sub[r_first] < a) ++r_first;
+    int r_last = r_first;
+    while (cp.sub[r_last + 1] < b) ++r_last;
+    std::vector<std::string> level_expr(g.ops.size());
+    for (int r = r_last; r >= r_first; --r) {
+        const int c = cp.sub[r], d = cp.sub[r + 1];
+        o << "  {\n";
+        for (int k : inputs_before(g, c, d)) {
+            if (k < a) o << "  const float f" << k << " = 0.f;\n";
+            else o << "  const float f" << k << " = c" << k << ";\n";
+        }
+        RangeOpts ro;
+        ro.a = c;
+        ro.b = d;
+        ro.accumulate = false;
+        ro.base_pack = w.base_pack;
+        ro.tab_end = w.tab_end;
+        ro.declare_row = false;
+        ro.preload = false;
+        ro.checks = false;
+        ro.time_only = true;
+        ro.tsel = ".x";
+        LevelPlan lp = emit_forward_range(o, g, ro, &level_expr);
+        lp.launder();
+        for (int i = d - 1; i >= c; --i) {
+            const JitOp &op = g.ops[i];
+            if ((d - 1 - i) % 16 == 0) {
+                std::vector<std::string> ops = {"zb"};
+                for (int k = i; k > i - 16 && k >= c; --k)
+                    if (g.ops[k].pack >= 0) {
+                        const std::string wd = lp.pfx + std::to_string(g.ops[k].pack / lp.width);
+                        if (std::find(ops.begin(), ops.end(), wd) == ops.end()) ops.push_back(wd);
+                    }
+                o << "  __asm__ __volatile__(\"\" :";
+                for (size_t k = 0; k < ops.size(); ++k) o << (k ? ", " : " ") << "\"+v\"(" << ops[k] << ")";
+                o << ");\n";
+            }
+            std::string lft;
+            if (op.out.empty() || (closed && i == b - 1)) {
+                lft = "Db";
+            } else {
+                bool have = false;
+                for (int k : op.out) {
+                    std::string v = "s" + std::to_string(k);
+                    lft = have ? "fminf(" + lft + ", " + v + ")" : v;
+                    have = true;
+                }
+            }
+            o << "  const float lf" << i << " = " << lft << ";\n";
+            std::string dur = flit(op.dur);
+            if (op.pack >= 0) {
+                o << "  const float t" << i << " = tab[zb + " << lp.row_entry(op.pack) << " + "
+                  << level_expr[i] << "].x;\n";
+                dur = "t" + std::to_string(i);
+            }
+            if (reads_start(g, i, a)) o << "  s" << i << " = lf" << i << " - " << dur << ";\n";
+            if (op.pack >= 0) {
+                const int k = op.pack % 32;
+                o << "  stg[" << k * 64 << " + (lane ^ " << 8 * (k / 4) << ")] = isbad ? EMO_NAN : lf" << i
+                  << " - f" << i << ";\n";
+                if (k == 0) o << "  emo_cflush(stg, S, wbase, B, " << op.pack << ");\n";
+            }
+        }
+        o << "  }\n";
+    }
+    o << "  }\n";
+}
+
+// Segment j of the segment kernel: its table window, the forward pass from the local origin
+// (its local makespan D and energy blocks stored), and with slack the backward pass.
+void emit_cut_segment(std::ostringstream &o, const JitGraph &g, const CutPlan &cp, int j, bool slack) {
+    const int a = cp.seg[j], b = cp.seg[j + 1];
+    const bool closed = j + 1 < cp.segments() || cp.closed_last;
+    const TabWindow w = cut_window(g, cp, j);
+    o << "  case " << j << ": {\n";
+    o << "  for (int i_ = threadIdx.x; i_ < " << w.entries << "; i_ += EMO_BLOCK) tab[i_] = tabg["
+      << w.base_pack * g.F << "LL + i_];\n  __syncthreads();\n";
+    o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
+    if (slack)
+        for (int i = a; i < b; ++i)
+            if (cp.ck[i]) o << "  float c" << i << ";\n";
+    o << "  float D;\n  {\n";
+    o << "  unsigned int bad = 0u;\n  float eb = 0.f;\n  float T = 0.f;\n";
+    if (j > 0) o << "  const float f" << a - 1 << " = 0.f;\n";
+    RangeOpts r;
+    r.a = a;
+    r.b = b;
+    r.npk0 = 0;
+    r.blk_row0 = cp.blk0[j];
+    r.base_pack = w.base_pack;
+    r.tab_end = w.tab_end;
+    r.preload = false;
+    r.ck_copy = slack ? &cp.ck : nullptr;
+    LevelPlan lp = emit_forward_range(o, g, r, nullptr);
+    const int npk = packs_in(g, a, b);
+    if (npk % 64) o << "  EMO_AT(Ebg, " << cp.blk0[j] + npk / 64 << ") = eb;\n";
+    o << "  D = " << (closed ? "f" + std::to_string(b - 1) : std::string("T")) << ";\n";
+    o << "  if ((bad & " << lp.bad_bits() << ") != 0u) D = EMO_NAN;\n";
+    o << "  EMO_AT(Dg, " << j << ") = D;\n  }\n";
+    if (slack) emit_cut_backward(o, g, cp, j, w);
+    o << "  } break;\n";
+}
+
+}  // namespace
+
+std::string jit_generate_cut(const JitGraph &g, const CutPlan &cp) {
+    std::ostringstream o;
+    o << "#define EMO_BLOCK " << cp.block << "\n" << kPrelude << kEmoSelectSource << "\n";
+    o << chain_flush_source(g.P);
+    long long entries = 0;   // the largest window, so that every segment kernel has one LDS layout
+    for (int j = 0; j < cp.segments(); ++j) entries = std::max(entries, cut_window(g, cp, j).entries);
+    for (int slack = 0; slack < 2; ++slack)
+      for (int kk = 0; kk < cp.kernels(); ++kk) {
+        const int j0 = kk * cp.per_kernel, j1 = std::min(cp.segments(), j0 + cp.per_kernel);
+        o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
+          << (slack ? "emo_ks" : "emo_kf") << kk
+          << "(const u8 *__restrict__ lv, long long B, long long bp,\n"
+             "    const float2 *__restrict__ tabg, float *__restrict__ Dg, float *__restrict__ Ebg,\n"
+             "    float *__restrict__ S) {\n";
+        // the table first, at LDS address 0: every table read keeps its row offset as an
+        // immediate (16 bits), which a table placed after the 64 KB of slack tiles would not
+        if (slack)
+            o << "  __shared__ struct { float2 t[" << entries << "]; float s[EMO_BLOCK / 64][32 * 64]; } emo_sh;\n"
+                 "  float2 *tab = emo_sh.t;\n"
+                 "  float *stg = emo_sh.s[threadIdx.x / EMO_WAVE];\n";
+        else
+            o << "  __shared__ float2 tab[" << entries << "];\n";
+        o << chain_lanes(cp.block);
+        o << "  const int lane = threadIdx.x % EMO_WAVE;\n"
+             "  const long long wbase = (long long)blockIdx.x * EMO_BLOCK + (threadIdx.x / EMO_WAVE) * EMO_WAVE;\n"
+             "  (void)lane; (void)wbase; (void)S;\n";
+        o << "  switch (blockIdx.y + " << j0 << ") {\n";
+        for (int j = j0; j < j1; ++j) emit_cut_segment(o, g, cp, j, slack != 0);
+        o << "  default: break;\n  }\n}\n\n";
+      }
+    // finishing kernel: makespan = the segments' local makespans added in order, energy = the
+    // blocks added in order into fp64 plus static power times makespan (Eq. 2); an invalid level
+    // in any segment (NaN D) makes the candidate's makespan, energy and slack row NaN
+    o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
+         "emo_kfin(long long B, long long bp, const float *__restrict__ Dg, const float *__restrict__ Ebg,\n"
+         "    float *__restrict__ S, float *__restrict__ To, float *__restrict__ Eo, float target,\n"
+         "    unsigned int *__restrict__ mask, EmoPartial *part) {\n";
+    o << chain_lanes(cp.block);
+    o << "  float T = EMO_AT(Dg, 0);\n";
+    for (int j = 1; j < cp.segments(); ++j) o << "  T = T + EMO_AT(Dg, " << j << ");\n";
+    o << "  const bool isbad = T != T;\n";
+    o << "  T = fmaxf(T, " << flit(g.t_const) << ");\n";
+    o << "  double ed = 0.0;\n";
+    for (int q = 0; q < cp.blk0.back(); ++q) o << "  ed += (double)EMO_AT(Ebg, " << q << ");\n";
+    o << "  float E = (float)(ed + (double)" << flit(g.static_power) << " * (double)T);\n";
+    o << "  if (isbad) { T = EMO_NAN; E = EMO_NAN; }\n";
+    o << "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n";
+    o << "  if (S) {\n"
+         "    const int lane = threadIdx.x % EMO_WAVE;\n"
+         "    const long long wbase = (long long)blockIdx.x * EMO_BLOCK + (threadIdx.x / EMO_WAVE) * EMO_WAVE;\n"
+         "    unsigned long long bm = __ballot(active && isbad);\n"
+         "    while (bm) {\n"
+         "      const int r = __ffsll((long long)bm) - 1;\n"
+         "      bm &= bm - 1ull;\n"
+         "      float *__restrict__ srow = S + (wbase + r) * " << g.P << "LL;\n"
+         "      for (int c = 4 * lane; c < " << g.P << "; c += 4 * EMO_WAVE) *(emo_f32x4 *)(srow + c) = (emo_f32x4)(EMO_NAN);\n"
+         "    }\n"
+         "  }\n";
+    o << "  if (mask || part) emo_select_block(blockIdx.x, active, T, E, cand, B, target, mask, part);\n";
+    o << "}\n";
+    return o.str();
+}
+
 namespace {
 
 // Compiles `src` for gfx950 and loads it as a module.  0 on success, 1 compile error, 2 load error.
@@ -966,6 +1278,27 @@ int jit_compile_chain(const std::string &src, const ChainPlan &cp, JitModule *ou
     }
     if (!okf) {
         *log = "segmented kernels missing from the module";
+        (void)hipModuleUnload(out->module);
+        *out = JitModule();
+        return 2;
+    }
+    return 0;
+}
+
+int jit_compile_cut(const std::string &src, const CutPlan &cp, JitModule *out, std::string *log) {
+    int rc = compile_module(src, &out->module, &out->compile_seconds, log);
+    if (rc != 0) return rc;
+    out->cut = true;
+    out->cut_plan = cp;
+    out->block = cp.block;
+    out->kf.assign(cp.kernels(), nullptr);
+    out->ks.assign(cp.kernels(), nullptr);
+    bool okf = get_function(out->module, "emo_kfin", &out->kfin);
+    for (int k = 0; k < cp.kernels(); ++k)
+        okf = okf && get_function(out->module, "emo_kf" + std::to_string(k), &out->kf[k]) &&
+              get_function(out->module, "emo_ks" + std::to_string(k), &out->ks[k]);
+    if (!okf) {
+        *log = "cut-segment kernels missing from the module";
         (void)hipModuleUnload(out->module);
         *out = JitModule();
         return 2;
@@ -1052,6 +1385,29 @@ hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+int64_t jit_cut_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.cut_plan.block); }
+
+hipError_t jit_launch_cut(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
+                          void *scratch, float *S, float *T, float *E, float target, uint32_t *mask,
+                          void *part, hipStream_t s) {
+    const CutPlan &cp = m.cut_plan;
+    const unsigned grid = grid_of(B, cp.block);
+    long long bp = chain_pitch(B);
+    float *Dg = static_cast<float *>(scratch);
+    float *Ebg = Dg + static_cast<size_t>(cp.segments()) * bp;
+    long long b = B;
+    void *args[] = {&levels, &b, &bp, &tab, &Dg, &Ebg, &S};
+    for (int k = 0; k < cp.kernels(); ++k) {
+        const int rows = std::min(cp.per_kernel, cp.segments() - k * cp.per_kernel);
+        hipError_t e = hipModuleLaunchKernel(S ? m.ks[k] : m.kf[k], grid, static_cast<unsigned>(rows), 1,
+                                             cp.block, 1, 1, 0, s, args, nullptr);
+        if (e != hipSuccess) return e;
+    }
+    const float *Dc = Dg, *Ec = Ebg;
+    void *fargs[] = {&b, &bp, &Dc, &Ec, &S, &T, &E, &target, &mask, &part};
+    return hipModuleLaunchKernel(m.kfin, grid, 1, 1, cp.block, 1, 1, 0, s, fargs, nullptr);
 }
 
 hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,

@@ -25,7 +25,7 @@ ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
                 "emo_select_from_results",
                 "emo_graph_set_timing_events", "emo_graph_specialized_source",
-                "emo_graph_segmented_source", "emo_status_string",
+                "emo_graph_segmented_source", "emo_graph_cut_source", "emo_status_string",
                 "emo_last_error")
 
 
@@ -44,7 +44,8 @@ class GraphInfo(ctypes.Structure):
                 ("pack_order_monotone", ctypes.c_int32), ("kernel_mode", ctypes.c_int32),
                 ("specialized", ctypes.c_int32), ("compile_seconds", ctypes.c_float),
                 ("last_kernels", ctypes.c_int32), ("chain_lanes", ctypes.c_int32),
-                ("num_implied_edges", ctypes.c_int32), ("chain_window", ctypes.c_int32)]
+                ("num_implied_edges", ctypes.c_int32), ("chain_window", ctypes.c_int32),
+                ("cut_segments", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -72,6 +73,7 @@ def _load_library():
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
         "emo_graph_specialized_source": [P, P, P],
         "emo_graph_segmented_source": [P, P, P],
+        "emo_graph_cut_source": [P, P, P],
         "emo_graph_set_timing_events": [P, P, P],
     }
     for name, args in sig.items():
@@ -191,6 +193,9 @@ class EmoGraph:
 
     def segmented_source(self) -> str:
         return self._source(lib.emo_graph_segmented_source)
+
+    def cut_source(self) -> str:
+        return self._source(lib.emo_graph_cut_source)
 
     def _source(self, fn) -> str:
         n = ctypes.c_int64(0)

@@ -198,6 +198,142 @@ def test_chain_windows(emo):
         assert inf["chain_lanes"] == 1 and inf["chain_window"] == win, order[:20]
 
 
+def _cut_nodes(V, src, dst):
+    """Nodes that every other node reaches or is reached from (the definition of a cut),
+    by full reachability (Python integers as bit sets)."""
+    succ = [[] for _ in range(V)]
+    indeg = [0] * V
+    for u, v in set(zip(src.tolist(), dst.tolist())):
+        succ[u].append(v)
+        indeg[v] += 1
+    order = [v for v in range(V) if indeg[v] == 0]
+    for v in order:
+        for w in succ[v]:
+            indeg[w] -= 1
+            if indeg[w] == 0:
+                order.append(w)
+    down = [0] * V
+    for u in reversed(order):
+        for w in succ[u]:
+            down[u] |= (1 << w) | down[w]
+    up = [0] * V
+    for v in range(V):
+        r = down[v]
+        while r:
+            w = (r & -r).bit_length() - 1
+            up[w] |= 1 << v
+            r &= r - 1
+    full = (1 << V) - 1
+    return [c for c in range(V) if (down[c] | up[c] | (1 << c)) == full], up
+
+
+def _expected_cut_segments(g, max_packs):
+    """Segments of the cut-segment kernels from the definition: segment ends are cuts after a
+    multiple of 32 packs (and the end of the graph); whole pieces are taken greedily while a
+    segment holds at most max_packs packs; 0 when a piece is larger or there is one segment."""
+    if g.num_packs % 32:
+        return 0
+    cuts, up = _cut_nodes(g.num_nodes, g.edge_src, g.edge_dst)
+    packs = {int(v) for v in np.nonzero(g.node_pack >= 0)[0]}
+    ends = set()
+    for c in cuts:
+        n = sum(1 for v in packs if (up[c] >> v) & 1) + (1 if c in packs else 0)
+        if n % 32 == 0 and n > 0:
+            ends.add(n)
+    ends.add(g.num_packs)
+    seg, last = [0], None
+    for e in sorted(ends):
+        if e - seg[-1] <= max_packs:
+            last = e
+            continue
+        if last is None or last <= seg[-1] or e - last > max_packs:
+            return 0
+        seg.append(last)
+        last = e
+    seg.append(last)
+    return len(seg) - 1 if len(seg) > 2 else 0
+
+
+def _block_graph(rng, nblk, bypass_p, F=16):
+    """Blocks of 32 packs (random edges from earlier to later packs of the block), each closed by
+    a synchronisation node that waits for the block's sinks and starts the next block's sources;
+    with probability bypass_p a fixed node runs from a pack of the previous block to a pack of
+    the next one beside the synchronisation, which then is no cut."""
+    src, dst, pack, dur = [], [], [], []
+
+    def node(p=-1, d=0.0):
+        pack.append(p)
+        dur.append(d)
+        return len(pack) - 1
+
+    prev_sync, prev_ids = None, None
+    for b in range(nblk):
+        ids = [node(32 * b + i) for i in range(32)]
+        has_in, has_out = [False] * 32, [False] * 32
+        for i in range(1, 32):
+            for _ in range(int(rng.integers(0, 3))):
+                j = int(rng.integers(0, i))
+                src.append(ids[j]); dst.append(ids[i])
+                has_in[i] = has_out[j] = True
+        if prev_sync is not None:
+            for i in range(32):
+                if not has_in[i]:
+                    src.append(prev_sync); dst.append(ids[i])
+            if rng.random() < bypass_p:
+                x = node(-1, 0.5)
+                src += [prev_ids[int(rng.integers(0, 32))], x]
+                dst += [x, ids[int(rng.integers(0, 32))]]
+        s = node(-1, float(synth.quantize(rng.uniform(1.0, 5.0))))
+        for i in range(32):
+            if not has_out[i]:
+                src.append(ids[i]); dst.append(s)
+        prev_sync, prev_ids = s, ids
+    P = 32 * nblk
+    t = synth.quantize(rng.uniform(1.0, 9.0, (P, F))).astype(np.float32)
+    return synth.Graph(f"blocks-{nblk}", len(pack), np.asarray(src, np.int32), np.asarray(dst, np.int32),
+                       np.asarray(pack, np.int32), np.asarray(dur, np.float32), P, F, t,
+                       (0.5 * t).astype(np.float32), 0.25)
+
+
+def test_cut_segments(emo):
+    """Segments of the cut-segment kernels on the workloads and on packed graphs with periodic
+    all-stream synchronisations: at most 256 packs (and 32 KB of (time, energy) table rows) per
+    segment, ends after a multiple of 32 packs, packs visited in increasing id."""
+    expect = {1: 0, 2: 0, 3: 0, 4: 16, 5: 0}
+    for k, m in expect.items():
+        assert _load(emo, synth.config_graph(k)).info()["cut_segments"] == m, k
+    for (P, S, F, se), m in (((1024, 8, 16, 256), 4), ((2048, 4, 8, 128), 8), ((1056, 8, 16, 256), 5),
+                             ((960, 6, 5, 96), 5), ((1024, 4, 32, 128), 8), ((1024, 4, 32, 256), 0),
+                             ((1000, 4, 16, 100), 0), ((1024, 4, 200, 128), 0), ((2048, 8, 16, 64), 8)):
+        g = synth.packed_graph(11, P, S, F, sync_every=se, cross_p=0.05)
+        assert _load(emo, g).info()["cut_segments"] == m, (P, S, F, se)
+    g = synth.packed_graph(11, 1024, 8, 16, sync_every=256, cross_p=0.05, shuffle_pack_ids=True)
+    assert _load(emo, g).info()["cut_segments"] == 0
+    # times off a common dyadic grid with a sum of largest durations of 2^24 grid units or more
+    g = synth.packed_graph(11, 1024, 8, 16, sync_every=256, cross_p=0.05)
+    assert _load(emo, _mod(g, pack_time=(g.pack_time * 64.0).astype(np.float32))).info()["cut_segments"] == 0
+    t = g.pack_time.copy()
+    t[5, 3] += np.float32(2.0 ** -12)   # grid 2^-12: the sum bound becomes 4096 us
+    assert _load(emo, _mod(g, pack_time=t)).info()["cut_segments"] == 0
+    assert _load(emo, _mod(g, pack_time=(g.pack_time * 8.0).astype(np.float32))).info()["cut_segments"] == 4
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_cut_segments_match_definition(emo, seed):
+    """Cut detection (a linear scan of one topological order) against the definition by full
+    reachability, through the segment count, on block graphs where some synchronisations are
+    bypassed and some packs are cuts as well."""
+    rng = np.random.default_rng(900 + seed)
+    seen = set()
+    for i in range(8):
+        F = int(rng.choice([16, 32, 64]))   # at most 256, 128 or 64 packs per segment
+        g = _block_graph(rng, int(rng.integers(2, 20)), float(rng.uniform(0.0, 0.5)), F)
+        want = _expected_cut_segments(g, 4096 // F)
+        assert _load(emo, g).info()["cut_segments"] == want, (seed, i, g.num_packs)
+        seen.add(want > 0)
+    assert seen == {True, False} or seed > 0
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_topo_order_matches_oracle_on_random_dags(emo, oracle_lib, seed):
     rng = np.random.default_rng(100 + seed)

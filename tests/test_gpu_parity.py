@@ -1,4 +1,6 @@
 """HIP path against the oracle, through the C ABI (needs an MI355X)."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -151,6 +153,35 @@ def test_interpreter_table_windows(torch, emo, F, P):
     run_all(torch, emo, g, rows, [float(np.median(T_or))], what=f"windows F={F} P={P}", mode=1)
 
 
+def without_cuts(g):
+    """The same graph plus a zero-duration source node into the node of the last pack: no node
+    before that pack is a cut any more (the new node is neither before nor after it), so the
+    cut-segment kernels do not apply."""
+    v = int(np.nonzero(g.node_pack == g.num_packs - 1)[0][0])
+    V = g.num_nodes
+    return dataclasses.replace(
+        g, name=g.name + "-nocut", num_nodes=V + 1,
+        edge_src=np.append(g.edge_src, np.int32(V)).astype(np.int32),
+        edge_dst=np.append(g.edge_dst, np.int32(v)).astype(np.int32),
+        node_pack=np.append(g.node_pack, np.int32(-1)).astype(np.int32),
+        node_duration=np.append(g.node_duration, np.float32(0)).astype(np.float32),
+        node_stream=None if g.node_stream is None else np.append(g.node_stream, np.int32(-1)).astype(np.int32))
+
+
+def with_host_source(g, dur=7.5):
+    """The same graph plus a fixed-duration node before every source (a candidate-independent
+    start-time floor for the first packs)."""
+    V = g.num_nodes
+    srcs = np.setdiff1d(np.arange(V), g.edge_dst).astype(np.int32)
+    return dataclasses.replace(
+        g, name=g.name + "-host", num_nodes=V + 1,
+        edge_src=np.concatenate([g.edge_src, np.full(len(srcs), V, np.int32)]),
+        edge_dst=np.concatenate([g.edge_dst, srcs]),
+        node_pack=np.append(g.node_pack, np.int32(-1)).astype(np.int32),
+        node_duration=np.append(g.node_duration, np.float32(dur)).astype(np.float32),
+        node_stream=None if g.node_stream is None else np.append(g.node_stream, np.int32(-1)).astype(np.int32))
+
+
 SEGMENTED_CASES = {
     # name: (packs, streams, levels, shuffled pack ids)
     "staged-F16": (1024, 8, 16, False),      # slack written through LDS, table windows in LDS
@@ -168,13 +199,15 @@ def test_segmented_kernels(torch, emo, case):
     sub-segment in the backward kernels, against the oracle on every row, including rows with an
     invalid level byte and a batch that ends inside a workgroup."""
     P, S_, F, shuffled = SEGMENTED_CASES[case]
-    g = synth.packed_graph(P + F, P, S_, F, sync_every=128, cross_p=0.05, shuffle_pack_ids=shuffled)
+    g = without_cuts(synth.packed_graph(P + F, P, S_, F, sync_every=128, cross_p=0.05,
+                                        shuffle_pack_ids=shuffled))
     rng = np.random.default_rng(P * F)
     rows = pins.random_rows(rng, g, 1000 - 23)
     rows[7, g.num_packs // 2] = F              # invalid levels: NaN results, never feasible
     rows[300, -1] = 255
     print(f"[case] segmented {case}: V={g.num_nodes} P={g.num_packs} B={len(rows)}", flush=True)
     gh = emo.EmoGraph(g, device=0)
+    assert gh.info()["cut_segments"] == 0
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
@@ -197,6 +230,86 @@ def test_segmented_kernels(torch, emo, case):
     Si = gi.slack(lv)
     for a, b in ((T, Ti), (E, Ei), (S, Si)):
         assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), case
+
+
+CUT_CASES = {
+    # name: (packs, streams, levels, packs between synchronisations, segments)
+    "sync-256-F16": (1024, 8, 16, 256, 4),   # 256-pack segments, as in the 4096-pack workload
+    "sync-128-F8": (2048, 4, 8, 128, 8),     # pieces of 128 packs, two per segment
+    "open-end-F16": (1056, 8, 16, 256, 5),   # 32 packs after the last synchronisation
+    "sync-96-F5": (960, 6, 5, 96, 5),        # level count not a power of two; 192-pack segments
+    "sync-128-F32": (1024, 4, 32, 128, 8),   # 32 levels: 128 packs fill the table window
+    "host-source": (1024, 8, 16, 256, 4),    # a fixed node before every source
+}
+
+
+@pytest.mark.parametrize("case", list(CUT_CASES))
+def test_cut_segment_kernels(torch, emo, case):
+    """Graphs with all-stream synchronisations: the segments between them evaluated on their own
+    (finish times from the segment's start, exact on the time grid), against the oracle on every
+    row, with rows holding invalid level bytes (two in one wave: the last kernel rewrites their
+    slack rows with NaN), a batch that ends inside a workgroup, and the interpreted kernels bit
+    for bit."""
+    P, S_, F, se, m = CUT_CASES[case]
+    g = synth.packed_graph(P + F + se, P, S_, F, sync_every=se, cross_p=0.05)
+    if case == "host-source":
+        g = with_host_source(g)
+    rng = np.random.default_rng(P + se)
+    rows = pins.random_rows(rng, g, 1000 - 23)
+    rows[7, P // 2] = F
+    rows[300, -1] = 255
+    rows[301, 0] = F
+    print(f"[case] cut segments {case}: V={g.num_nodes} P={P} B={len(rows)}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    assert gh.info()["cut_segments"] == m
+    lv = dev(torch, rows)
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    T, E = gh.eval_policies(lv)
+    S = gh.slack(lv)
+    torch.cuda.synchronize()
+    info = gh.info()
+    assert info["specialized"] & 16 and info["last_kernels"] == 5, info
+    ok = ~np.isnan(T_or)
+    assert not ok[[7, 300, 301]].any()
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, case)
+    Sh = host(S)
+    assert np.all(np.isnan(Sh[~ok]))
+    S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in np.nonzero(ok)[0]])
+    parity.assert_slack(Sh[ok], S_or, T_or[ok], True, case + " pack slack")
+    tgt = float(np.float32(np.median(T_or[ok])))
+    run_all(torch, emo, g, rows, [tgt], per_node=False, what="cut " + case)
+    gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+    Ti, Ei = gi.eval_policies(lv)
+    Si = gi.slack(lv)
+    for a, b in ((T, Ti), (E, Ei), (S, Si)):
+        assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), case
+
+
+def test_cut_segments_small_batches(torch, emo):
+    """Cut-segment kernels with batches smaller than a workgroup and one past it (lanes past the
+    batch repeat the last row and store nothing), repeated calls bit for bit."""
+    g = synth.packed_graph(5, 1024, 8, 16, sync_every=256, cross_p=0.05)
+    rng = np.random.default_rng(5)
+    gh = emo.EmoGraph(g, device=0)
+    gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+    for B in (1, 3, 512, 513):
+        rows = pins.random_rows(rng, g, B)
+        print(f"[case] cut segments B={B}", flush=True)
+        lv = dev(torch, rows)
+        T, E = gh.eval_policies(lv)
+        S = gh.slack(lv)
+        torch.cuda.synchronize()
+        assert gh.info()["last_kernels"] == 5
+        T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+        parity.assert_eval(host(T), host(E), T_or, E_or, True, f"cut B={B}")
+        S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(B)])
+        parity.assert_slack(host(S), S_or, T_or, True, f"cut B={B} pack slack")
+        T2, E2 = gh.eval_policies(lv)
+        S2 = gh.slack(lv)
+        Ti, Ei = gi.eval_policies(lv)
+        Si = gi.slack(lv)
+        for a, b in ((T, T2), (E, E2), (S, S2), (T, Ti), (E, Ei), (S, Si)):
+            assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), B
 
 
 CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-streams": (8500, 33, 8),
@@ -518,10 +631,10 @@ def test_workload_full_batch(torch, emo, k):
     lv = dev(torch, rows)
     T, E = gh.eval_policies(lv)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, spec.name)
-    # one specialised kernel up to 2048 steps, segmented kernels for the 4096-pack graph, chain
-    # lanes for the 65536-kernel graph (16 stream chains)
+    # one specialised kernel up to 2048 steps, cut-segment kernels for the 4096-pack graph (16
+    # synchronisations), chain lanes for the 65536-kernel graph (16 stream chains)
     inf = gh.info()
-    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 2, 5: 4}[k], inf
+    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 5, 5: 4}[k], inf
     if k <= 4:
         # the interpreting kernels on the same batch: bit-identical
         gi = emo.EmoGraph(g, device=0, kernel_mode=1)
@@ -544,7 +657,8 @@ def test_workload_full_batch(torch, emo, k):
     pick = synth.sample_rows(B, 24)
     S = gh.slack(lv)
     # slack: one kernel while every finish time fits in registers, then segmented kernels
-    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 2, 5: 4}[k], gh.info()
+    # (cut segments for the 4096-pack graph)
+    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 5, 5: 4}[k], gh.info()
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in pick])
     idx = torch.from_numpy(pick).cuda()
     parity.assert_slack(host(S.index_select(0, idx)), S_or, T_or[pick], True, spec.name + " slack")
