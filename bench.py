@@ -33,7 +33,8 @@ VALU_PEAK_TOPS = 39.3   # 256 CUs x 64 fp32 lanes x 2.4 GHz, one op per lane per
 # sources that make the kernels of each kind (last_kernels): graph preparation and the
 # selection code are common to all of them
 KIND_SOURCES = {0: ("emo_kernels.hip",), 1: ("emo_jit.cpp",), 2: ("emo_jit.cpp",),
-                3: ("emo_chains.hip", "emo_kernels.hip"), 4: ("emo_chains.hip", "emo_kernels.hip")}
+                3: ("emo_chains.hip", "emo_kernels.hip"), 4: ("emo_chains.hip", "emo_kernels.hip"),
+                5: ("emo_jit.cpp",)}
 
 
 def kernel_source_hash(kind: int) -> str:
@@ -211,6 +212,8 @@ def main():
         kname = "chains_kernel"
     elif info["last_kernels"] == 4:
         kname = "chains_windowed"
+    elif info["last_kernels"] == 5:    # cut-segment kernels and their last kernel, as one unit
+        kname = "emo_cut"
     elif info["last_kernels"] == 1:
         kname = "emo_sp_slack" if spec.slack else "emo_sp_select"
     else:

@@ -262,9 +262,10 @@ emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len);
 emo_status emo_graph_segmented_source(emo_graph_t g, char *buf, int64_t *len);
 
 /* Diagnostics: the HIP source of the cut-segment kernels of `g` (see cut_segments in
- * emo_graph_info): one kernel whose grid row y evaluates segment y for a group of candidates
- * (forward only, and forward with slack), and the kernel that adds up the segments' makespans
- * and energy blocks and completes the selection.  Same buffer convention as
+ * emo_graph_info): segment kernels whose grid row y evaluates one segment for a group of
+ * candidates (four segments per kernel; forward only, and forward with slack), launched one
+ * after another, and the kernel that adds up the segments' makespans and energy blocks and
+ * completes the selection.  Same buffer convention as
  * emo_graph_specialized_source.  EMO_ERR_UNSUPPORTED when the graph has no cut segments. */
 emo_status emo_graph_cut_source(emo_graph_t g, char *buf, int64_t *len);
 
