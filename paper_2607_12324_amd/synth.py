@@ -267,6 +267,47 @@ def stream_graph(seed: int, P: int, S: int, F: int, median_us: float = 8.0,
                          cross_p=0.0, n_cross_exact=None, median_us=median_us, sigma=sigma)
 
 
+def block_graph(rng, nblk: int, bypass_p: float, F: int = 16) -> Graph:
+    """Blocks of 32 packs (random edges from earlier to later packs of the block), each closed by
+    a synchronisation node that waits for the block's sinks and starts the next block's sources;
+    with probability bypass_p a fixed node runs from a pack of the previous block to a pack of
+    the next one beside the synchronisation, which then is no cut."""
+    src, dst, pack, dur = [], [], [], []
+
+    def node(p=-1, d=0.0):
+        pack.append(p)
+        dur.append(d)
+        return len(pack) - 1
+
+    prev_sync, prev_ids = None, None
+    for b in range(nblk):
+        ids = [node(32 * b + i) for i in range(32)]
+        has_in, has_out = [False] * 32, [False] * 32
+        for i in range(1, 32):
+            for _ in range(int(rng.integers(0, 3))):
+                j = int(rng.integers(0, i))
+                src.append(ids[j]); dst.append(ids[i])
+                has_in[i] = has_out[j] = True
+        if prev_sync is not None:
+            for i in range(32):
+                if not has_in[i]:
+                    src.append(prev_sync); dst.append(ids[i])
+            if rng.random() < bypass_p:
+                x = node(-1, 0.5)
+                src += [prev_ids[int(rng.integers(0, 32))], x]
+                dst += [x, ids[int(rng.integers(0, 32))]]
+        s = node(-1, float(quantize(rng.uniform(1.0, 5.0))))
+        for i in range(32):
+            if not has_out[i]:
+                src.append(ids[i]); dst.append(s)
+        prev_sync, prev_ids = s, ids
+    P = 32 * nblk
+    t = quantize(rng.uniform(1.0, 9.0, (P, F))).astype(np.float32)
+    return Graph(f"blocks-{nblk}", len(pack), np.asarray(src, np.int32), np.asarray(dst, np.int32),
+                       np.asarray(pack, np.int32), np.asarray(dur, np.float32), P, F, t,
+                       (0.5 * t).astype(np.float32), 0.25)
+
+
 def config_graph(k: int) -> Graph:
     """The execution graph and tables of benchmark workload `k` (1..5)."""
     spec = CONFIGS[k]

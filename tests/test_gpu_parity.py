@@ -312,6 +312,71 @@ def test_cut_segments_small_batches(torch, emo):
             assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), B
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_cut_segments_on_block_graphs(torch, emo, seed):
+    """Random block graphs: synchronisations (some bypassed by a fixed node), packs that are cuts
+    themselves, 16, 32 or 64 levels (segments of at most 256, 128 or 64 packs).  Slack runs on the
+    cut-segment kernels wherever the graph has cut segments; every call matches the oracle and
+    the interpreted kernels bit for bit."""
+    grng = np.random.default_rng(950 + seed)
+    rrng = np.random.default_rng(960 + seed)
+    ran = 0
+    for i in range(4):
+        F = int(grng.choice([16, 32, 64]))
+        g = synth.block_graph(grng, int(grng.integers(6, 20)), float(grng.uniform(0.0, 0.4)), F)
+        rows = pins.random_rows(rrng, g, 300)
+        gh = emo.EmoGraph(g, device=0)
+        m = gh.info()["cut_segments"]
+        print(f"[case] block graph seed={seed} #{i}: P={g.num_packs} F={F} segments={m}", flush=True)
+        lv = dev(torch, rows)
+        T, E = gh.eval_policies(lv)
+        S = gh.slack(lv)
+        torch.cuda.synchronize()
+        if m:
+            assert gh.info()["last_kernels"] == 5
+            ran += 1
+        T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+        parity.assert_eval(host(T), host(E), T_or, E_or, True, f"block graph {seed}/{i}")
+        S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(len(rows))])
+        parity.assert_slack(host(S), S_or, T_or, True, f"block graph {seed}/{i} pack slack")
+        gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+        Ti, Ei = gi.eval_policies(lv)
+        Si = gi.slack(lv)
+        for a, b in ((T, Ti), (E, Ei), (S, Si)):
+            assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), (seed, i)
+    assert ran >= 3
+
+
+def test_cut_segments_unaligned_buffers(torch, emo):
+    """A graph with cut segments and level rows or a slack buffer that are not 16-byte aligned:
+    the call takes other kernels (the cut-segment kernels load levels and store slack in 16-byte
+    pieces) and the results stay those of the oracle and of the aligned call, bit for bit."""
+    g = synth.packed_graph(6, 1024, 8, 16, sync_every=256, cross_p=0.05)
+    rng = np.random.default_rng(6)
+    rows = pins.random_rows(rng, g, 700)
+    print("[case] cut segments, unaligned buffers", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    lv = dev(torch, rows)
+    T, E = gh.eval_policies(lv)
+    S = gh.slack(lv)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == 5
+    lm = misaligned(torch, rows)
+    Tm, Em = gh.eval_policies(lm)
+    Sm = gh.slack(lm)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] != 5
+    sbuf = torch.empty(rows.shape[0] * g.num_packs + 4, dtype=torch.float32, device="cuda")
+    Su = sbuf[1:1 + rows.shape[0] * g.num_packs].view(rows.shape[0], g.num_packs)
+    gh.slack(lv, out=Su)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] != 5
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, "cut aligned")
+    for a, b in ((T, Tm), (E, Em), (S, Sm), (S, Su)):
+        assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32))
+
+
 CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-streams": (8500, 33, 8),
                "64-streams": (8300, 64, 5),
                # a block's table rows exceed the LDS stage: every lane reads the table itself
