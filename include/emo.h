@@ -247,6 +247,33 @@ emo_status emo_select_from_results(const float *makespan, const float *energy,
  * concurrently on another thread. */
 emo_status emo_graph_set_timing_events(emo_graph_t g, void *begin_event, void *end_event);
 
+/*
+ * Near-optimal policy search (Alg. 2, Sec. IV-F) with one frequency interval per pack, on the
+ * device.  Dynamic programming over the packs in `pack_order`: dp[0] holds the all-maximum
+ * policy P_0 (level F-1 everywhere); stage i sets pack order[i] to every level f in every
+ * stored policy, evaluates those policies with the batch evaluator (Alg. 1), drops the ones
+ * whose makespan exceeds latency_target, and keeps for each makespan bucket
+ * floor(makespan / quantum) the one of least energy (among equal energies the first in the
+ * order (stored policy by increasing bucket, level f increasing)).  The result is the least
+ * energy over the last stage's policies (among equal energies the lowest bucket).  Makespans
+ * and energies are the evaluator's fp32 values; buckets are computed in double precision.
+ *   latency_target   T_max, finite (the constraint of Eq. 4).
+ *   quantum          bucket width, finite and > 0 (the paper discretises time at e.g. 1 ms).
+ *   pack_order       host int32 [P], a permutation of the pack ids, or NULL for 0..P-1.
+ *   max_states       the most buckets the search may keep: from one below the bucket of the
+ *                    least possible makespan (every pack at its fastest level) to the bucket of
+ *                    latency_target; a larger range is EMO_ERR_INVALID_ARGUMENT (choose a
+ *                    coarser quantum).  Device scratch grows with max_states x F x P bytes.
+ *   best_levels      device uint8 [P]: the policy found; left unchanged when none is found.
+ *   result           device emo_selection, 8-byte aligned: index = floor(makespan / quantum) of
+ *                    the policy found, or -1 (energy and makespan NaN) when no policy meets
+ *                    the target; num_feasible = the policies stored after the last stage.
+ * One call runs P + 1 evaluations of at most max_states x F candidates each, asynchronously on
+ * `stream`.  Not to be called concurrently with itself on the same graph.
+ */
+emo_status emo_dp_search(emo_graph_t g, float latency_target, float quantum, const int32_t *pack_order,
+                         int32_t max_states, uint8_t *best_levels, emo_selection *result, void *stream);
+
 /* Diagnostics: the HIP source of the kernels specialised to `g` (the text EMO_KERNELS_AUTO
  * compiles on first use), NUL-terminated.  With buf == NULL, *len receives the size needed
  * including the NUL; otherwise at most *len bytes are written.  Works on host-only graphs.

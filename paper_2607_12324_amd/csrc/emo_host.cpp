@@ -171,6 +171,7 @@ struct emo_graph_s {
     std::vector<int32_t> kahn;               // a topological order (Kahn, FIFO)
     std::vector<char> dyn;                   // depends on the candidate
     std::vector<float> const_eft;            // finish time of candidate-independent nodes
+    std::vector<float> tmin;                 // each pack's least time over its levels
     float t_const = 0.f;
     emo_graph_info info{};
     std::vector<void *> allocations;         // device memory owned by the handle
@@ -198,6 +199,8 @@ struct emo_graph_s {
     int cut_state = 0;                       // 0 not tried, 1 compiled, -1 failed
     emo::JitModule jk;
     Arena arena;                             // per-call scratch, kept between calls
+    Arena dp_arena;                          // scratch of the policy search (whose evaluations
+                                             // use `arena`)
     // profiling hook (hipEvent_t handles owned by the caller)
     hipEvent_t ev_begin = nullptr;
     hipEvent_t ev_end = nullptr;
@@ -540,6 +543,7 @@ void release_device(emo_graph_s *g) {
         emo::jit_unload(&g->jk);
         for (void *p : g->allocations) (void)hipFree(p);
         arena_free(g->arena);
+        arena_free(g->dp_arena);
     }
     g->allocations.clear();
 }
@@ -1008,6 +1012,12 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     g->V = V; g->P = P; g->F = F; g->static_power = static_power; g->device = device;
     g->pack.assign(node_pack, node_pack + V);
     g->dur.assign(node_duration, node_duration + V);
+    g->tmin.assign(P, 0.f);
+    for (int32_t p = 0; p < P; ++p) {
+        float m = pack_time[static_cast<size_t>(p) * F];
+        for (int32_t f = 1; f < F; ++f) m = std::min(m, pack_time[static_cast<size_t>(p) * F + f]);
+        g->tmin[p] = m;
+    }
     for (int32_t v = 0; v < V; ++v)
         if (g->pack[v] >= 0) g->dur[v] = 0.f;
     // merge duplicate edges
@@ -1335,6 +1345,130 @@ emo_status emo_select_from_results(const float *makespan, const float *energy, i
     hipError_t er = arena_release(a, st);
     if (e == hipSuccess) e = er;
     return after_launch(e, "emo_select_from_results");
+}
+
+}  // extern "C"
+
+namespace {
+
+// A lower bound of every policy's makespan: the longest path with each pack at its least time
+// over the levels (fp64).
+double least_makespan(const emo_graph_s &g) {
+    std::vector<double> eft(static_cast<size_t>(g.V), 0.0);
+    double T = 0.0;
+    for (int32_t v : g.order) {
+        double est = 0.0;
+        for (int32_t j = g.pred_off[v]; j < g.pred_off[v + 1]; ++j) est = std::max(est, eft[g.pred[j]]);
+        eft[v] = est + (g.pack[v] >= 0 ? static_cast<double>(g.tmin[g.pack[v]]) : static_cast<double>(g.dur[v]));
+        T = std::max(T, eft[v]);
+    }
+    return T;
+}
+
+// Device scratch of one search, carved from one arena block (256-byte aligned pieces).
+struct DPBuffers {
+    uint8_t *rows, *state[2];
+    unsigned long long *keys[2];
+    float *Tst[2], *T, *E;
+};
+
+size_t dp_layout(int64_t S, int64_t R, int32_t P, DPBuffers *b, char *base) {
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char *p = base ? base + off : nullptr;
+        off += (bytes + 255) & ~static_cast<size_t>(255);
+        return p;
+    };
+    const size_t pb = static_cast<size_t>(P > 0 ? P : 1);
+    b->rows = reinterpret_cast<uint8_t *>(take(static_cast<size_t>(R) * pb));
+    for (int i = 0; i < 2; ++i) {
+        b->state[i] = reinterpret_cast<uint8_t *>(take(static_cast<size_t>(S) * pb));
+        b->keys[i] = reinterpret_cast<unsigned long long *>(take(static_cast<size_t>(S) * 8));
+        b->Tst[i] = reinterpret_cast<float *>(take(static_cast<size_t>(S) * 4));
+    }
+    b->T = reinterpret_cast<float *>(take(static_cast<size_t>(R) * 4));
+    b->E = reinterpret_cast<float *>(take(static_cast<size_t>(R) * 4));
+    return off;
+}
+
+}  // namespace
+
+extern "C" {
+
+emo_status emo_dp_search(emo_graph_t g, float latency_target, float quantum, const int32_t *pack_order,
+                         int32_t max_states, uint8_t *best_levels, emo_selection *result, void *stream) {
+    emo_status s = check_batch(g, 1);
+    if (s != EMO_OK) return s;
+    if (!result || reinterpret_cast<uintptr_t>(result) % 8)
+        return fail(EMO_ERR_INVALID_ARGUMENT, "result is NULL or not 8-byte aligned");
+    const int32_t P = g->P, F = g->F;
+    if (P > 0 && !best_levels) return fail(EMO_ERR_INVALID_ARGUMENT, "best_levels is NULL");
+    if (!std::isfinite(latency_target)) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target must be finite");
+    if (!std::isfinite(quantum) || !(quantum > 0.f))
+        return fail(EMO_ERR_INVALID_ARGUMENT, "quantum must be finite and > 0");
+    if (max_states < 1) return fail(EMO_ERR_INVALID_ARGUMENT, "max_states must be >= 1");
+    std::vector<int32_t> order(static_cast<size_t>(P));
+    if (pack_order) {
+        std::vector<char> seen(static_cast<size_t>(P), 0);
+        for (int32_t i = 0; i < P; ++i) {
+            const int32_t p = pack_order[i];
+            if (p < 0 || p >= P || seen[p]++)
+                return fail(EMO_ERR_INVALID_ARGUMENT, "pack_order is not a permutation of the pack ids (entry %d: %d)",
+                            i, p);
+            order[i] = p;
+        }
+    } else {
+        for (int32_t i = 0; i < P; ++i) order[i] = i;
+    }
+    // makespan buckets floor(t / q) from one below the least possible makespan's to the target's
+    const double q = quantum;
+    const int64_t bmin = std::max<int64_t>(0, static_cast<int64_t>(std::floor(least_makespan(*g) / q)) - 1);
+    const int64_t btop = static_cast<int64_t>(std::floor(static_cast<double>(latency_target) / q));
+    const int64_t NB = std::max<int64_t>(0, btop - bmin + 1);
+    if (NB > max_states)
+        return fail(EMO_ERR_INVALID_ARGUMENT,
+                    "%lld makespan buckets of %g between the least makespan and the target, more than max_states (%d)",
+                    (long long)NB, q, max_states);
+    const int64_t S = std::max<int64_t>(NB, 1);
+    const int64_t R = S * F;
+    if (R > (int64_t(1) << 31)) return fail(EMO_ERR_INVALID_ARGUMENT, "too many candidates per stage");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    DeviceGuard guard(g->device);
+    DPBuffers b{};
+    const size_t bytes = dp_layout(S, R, P, &b, nullptr);
+    std::lock_guard<std::mutex> lock(g->dp_arena.mu);
+    void *base = nullptr;
+    hipError_t e = arena_acquire(g->dp_arena, bytes, st, &base);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(EMO_ERR_OUT_OF_MEMORY, "scratch of %zu bytes: %s", bytes, hipGetErrorString(e));
+    }
+    dp_layout(S, R, P, &b, static_cast<char *>(base));
+    // dp[0] = {P_0}
+    e = emo::dp_launch_default_row(b.rows, P, F, st);
+    if (e == hipSuccess) s = evaluate(g, b.rows, 1, b.T, b.E, nullptr, 0, 0.f, nullptr, nullptr, st);
+    if (e == hipSuccess && s == EMO_OK)
+        e = emo::dp_launch_init_state(b.rows, P, b.T, b.E, b.state[0], b.keys[0], b.Tst[0], st);
+    int64_t cur = 1;
+    int a = 0;
+    // one stage per interval (pack): every stored policy with each level at that pack
+    for (int32_t i = 0; i < P && NB > 0 && e == hipSuccess && s == EMO_OK; ++i) {
+        const int64_t B = cur * F;
+        e = emo::dp_launch_expand(b.state[a], cur, P, F, order[i], b.rows, st);
+        if (e != hipSuccess) break;
+        s = evaluate(g, b.rows, B, b.T, b.E, nullptr, 0, 0.f, nullptr, nullptr, st);
+        if (s != EMO_OK) break;
+        e = emo::dp_launch_select(b.T, b.E, b.keys[a], B, F, latency_target, q, bmin, NB, b.keys[1 - a], st);
+        if (e == hipSuccess) e = emo::dp_launch_gather(b.rows, b.T, b.keys[1 - a], NB, P, b.state[1 - a], b.Tst[1 - a], st);
+        a = 1 - a;
+        cur = NB;
+    }
+    if (e == hipSuccess && s == EMO_OK)
+        e = emo::dp_launch_final(b.state[a], b.keys[a], b.Tst[a], cur, P, latency_target, q, best_levels, result, st);
+    hipError_t er = arena_release(g->dp_arena, st);
+    if (s != EMO_OK) return s;
+    if (e == hipSuccess) e = er;
+    return after_launch(e, "emo_dp_search");
 }
 
 }  // extern "C"

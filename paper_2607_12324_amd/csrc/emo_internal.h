@@ -150,6 +150,29 @@ hipError_t launch_chains(const DevGraph &g, const DevChains &c, const uint8_t *l
                          float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
                          void *scratch, hipStream_t s);
 
+// ---------------------------------------------------------------- policy search (Alg. 2)
+
+// Kernels of emo_dp_search (one frequency interval per pack).  A stage: dp_launch_expand turns
+// the S stored states ([S][P] level rows) into S*F candidate rows with level f at pack p, the
+// batch evaluator computes their makespans and energies, dp_launch_select keeps for each of the
+// NB buckets (floor(makespan / q) - bmin) the least key (fp32 energy bits << 32 | candidate) of
+// the candidates that come from a stored state (src_keys != empty) and meet tmax, and
+// dp_launch_gather copies each bucket's winning row (and makespan) into the next states.
+hipError_t dp_launch_default_row(uint8_t *row, int32_t P, int32_t F, hipStream_t s);
+hipError_t dp_launch_init_state(const uint8_t *row, int32_t P, const float *T, const float *E,
+                                uint8_t *state, unsigned long long *key, float *Tst, hipStream_t s);
+hipError_t dp_launch_expand(const uint8_t *states, int64_t S, int32_t P, int32_t F, int32_t p,
+                            uint8_t *rows, hipStream_t s);
+hipError_t dp_launch_select(const float *T, const float *E, const unsigned long long *src_keys,
+                            int64_t B, int32_t F, float tmax, double q, int64_t bmin, int64_t NB,
+                            unsigned long long *keys, hipStream_t s);
+hipError_t dp_launch_gather(const uint8_t *rows, const float *T, const unsigned long long *keys,
+                            int64_t NB, int32_t P, uint8_t *dst, float *Tst, hipStream_t s);
+// The least-energy stored state with makespan <= tmax (ties: lowest bucket) to best and res.
+hipError_t dp_launch_final(const uint8_t *states, const unsigned long long *keys, const float *Tst,
+                           int64_t S, int32_t P, float tmax, double q, uint8_t *best,
+                           emo_selection *res, hipStream_t s);
+
 // ---------------------------------------------------------------- graph-specialised kernels
 
 // One candidate-dependent node of the graph in traversal order.

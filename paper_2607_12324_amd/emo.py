@@ -23,7 +23,7 @@ STATUS_NAMES = {0: "EMO_OK", 1: "EMO_ERR_INVALID_ARGUMENT", 2: "EMO_ERR_CYCLE",
 ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_kernel_mode", "emo_graph_topo_order",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
-                "emo_select_from_results",
+                "emo_select_from_results", "emo_dp_search",
                 "emo_graph_set_timing_events", "emo_graph_specialized_source",
                 "emo_graph_segmented_source", "emo_graph_cut_source", "emo_status_string",
                 "emo_last_error")
@@ -71,6 +71,7 @@ def _load_library():
         "emo_select_policy": [P, P, i64, f32, P, P, P],
         "emo_evaluate": [P, P, i64, P, P, P, i32, f32, P, P, P],
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
+        "emo_dp_search": [P, f32, f32, P, i32, P, P, P],
         "emo_graph_specialized_source": [P, P, P],
         "emo_graph_segmented_source": [P, P, P],
         "emo_graph_cut_source": [P, P, P],
@@ -264,6 +265,26 @@ class EmoGraph:
                                      _dptr(mask, torch.int32, (B + 31) // 32, "mask"),
                                      _dptr(result, torch.int64, 3, "result"), _stream(stream)))
         return result, mask
+
+
+    def dp_search(self, latency_target: float, quantum: float, pack_order=None,
+                  max_states: int = 4096, best_levels=None, result=None, stream=None):
+        """Policy search of Alg. 2 with one frequency interval per pack (emo_dp_search): returns
+        the device tensors (levels [P] uint8, result [3] int64 as an emo_selection)."""
+        import torch
+        dev = f"cuda:{self.device}"
+        if best_levels is None:
+            best_levels = torch.empty(max(self.num_packs, 1), dtype=torch.uint8, device=dev)
+        if result is None:
+            result = torch.empty(3, dtype=torch.int64, device=dev)
+        order = None if pack_order is None else _np(pack_order, np.int32)
+        if order is not None and order.size != self.num_packs:
+            raise ValueError(f"pack_order must hold {self.num_packs} pack ids")
+        _check(lib.emo_dp_search(self._h, float(latency_target), float(quantum),
+                                 None if order is None else _nptr(order), int(max_states),
+                                 _dptr(best_levels, torch.uint8, self.num_packs, "best_levels"),
+                                 _dptr(result, torch.int64, 3, "result"), _stream(stream)))
+        return best_levels[: self.num_packs], result
 
 
 def select_from_results(makespan, energy, latency_target: float, mask=None, result=None,

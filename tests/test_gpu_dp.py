@@ -1,0 +1,134 @@
+"""Policy search (Alg. 2, one frequency interval per pack) on the GPU through the C ABI, against
+the search oracle (needs an MI355X).  Graphs whose energies lie on a dyadic grid keep every
+makespan and energy exact in fp32, so both sides take every decision on the same numbers."""
+import dataclasses
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import pins
+from oracle import dp
+from paper_2607_12324_amd import synth
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    return t
+
+
+@pytest.fixture(scope="module")
+def emo(torch):
+    from paper_2607_12324_amd import emo as mod
+    return mod
+
+
+def run(emo, gh, tgt, q, order=None, max_states=4096):
+    lv, res = gh.dp_search(tgt, q, order, max_states=max_states)
+    sel = emo.parse_selection(res)
+    return lv.cpu().numpy(), sel
+
+
+def check(emo, g, gh, tgt, q, order=None, what=""):
+    r = dp.dp_search(g, tgt, q, order)
+    lv, sel = run(emo, gh, tgt, q, order)
+    assert sel.num_feasible == r.num_states, what
+    if r.levels is None:
+        assert sel.index == -1 and math.isnan(sel.energy) and math.isnan(sel.makespan), what
+        return r
+    assert np.array_equal(lv, r.levels), what
+    assert sel.energy == r.energy and sel.makespan == r.makespan, what
+    assert sel.index == math.floor(r.makespan / float(np.float32(q))), what
+    return r
+
+
+def test_dp_handworked(torch, emo):
+    g = pins.graph_from_golden(pins.load_golden())
+    gh = emo.EmoGraph(g, device=0)
+    with open(os.path.join(HERE, "golden", "handworked_dp.json")) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
+        print(f"[case] dp hand-worked {case['latency_target']} {case['quantum']} {case['pack_order']}", flush=True)
+        lv, sel = run(emo, gh, case["latency_target"], case["quantum"], case["pack_order"])
+        assert sel.num_feasible == case["num_states"], case
+        if case["levels"] is None:
+            assert sel.index == -1, case
+        else:
+            assert list(lv) == case["levels"], case
+            assert sel.energy == case["energy"] and sel.makespan == case["makespan"], case
+
+
+def dyadic(g, rng, step=2.0 ** -6):
+    """The same graph with energies rounded to multiples of `step` and a dyadic static power."""
+    e = (np.round(g.pack_energy / step) * step).astype(np.float32)
+    return dataclasses.replace(g, pack_energy=e, static_power=float(rng.choice([0.0, 0.25, 0.5])))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_dp_matches_oracle_on_random_dags(torch, emo, seed):
+    rng = np.random.default_rng(800 + seed)
+    found = 0
+    for i in range(8):
+        g = dyadic(synth.random_dag(rng, int(rng.integers(4, 14)), float(rng.uniform(0.15, 0.5)), 0.75,
+                                    int(rng.integers(2, 6))), rng)
+        if g.num_packs == 0:
+            continue
+        gh = emo.EmoGraph(g, device=0)
+        T0 = float(dp.eval_batch(g, np.full((1, g.num_packs), g.num_levels - 1, np.uint8))[0][0])
+        for tr in (0.9, 1.1, 1.4):
+            tgt = float(np.float32(T0 * tr))
+            q = float(rng.choice([0.25, 0.75, 1.0, 3.0]))
+            order = rng.permutation(g.num_packs) if rng.random() < 0.5 else None
+            print(f"[case] dp random seed={seed} #{i} P={g.num_packs} F={g.num_levels} target={tgt} q={q}", flush=True)
+            r = check(emo, g, gh, tgt, q, order, f"{seed}/{i}/{tr}")
+            found += r.levels is not None
+        gh.close()
+    assert found > 0
+
+
+def test_dp_on_inference_graph(torch, emo):
+    """The 64-pack inference graph (energies rounded to 2^-10) with about a hundred buckets:
+    64 stages of up to ~800 candidates, against the oracle."""
+    rng = np.random.default_rng(2)
+    g = dyadic(synth.config_graph(2), rng, 2.0 ** -10)
+    g = dataclasses.replace(g, static_power=0.25)
+    gh = emo.EmoGraph(g, device=0)
+    T0 = float(dp.eval_batch(g, np.full((1, g.num_packs), g.num_levels - 1, np.uint8))[0][0])
+    tgt = float(np.float32(1.05 * T0))
+    q = 2.0 ** math.floor(math.log2(0.05 * T0 / 100))
+    print(f"[case] dp inference graph T0={T0} target={tgt} q={q}", flush=True)
+    r = check(emo, g, gh, tgt, q, None, "inference graph")
+    assert r.levels is not None and r.num_states > 10
+
+
+def test_dp_without_packs_and_argument_errors(torch, emo):
+    z = np.zeros(0, np.int32)
+    g = synth.Graph("fixed-only", 2, np.asarray([0], np.int32), np.asarray([1], np.int32),
+                    np.asarray([-1, -1], np.int32), np.asarray([3.0, 4.5], np.float32), 0, 2,
+                    np.zeros((0, 2), np.float32), np.zeros((0, 2), np.float32), 0.5)
+    gh = emo.EmoGraph(g, device=0)
+    lv, sel = run(emo, gh, 8.0, 1.0)
+    assert sel.index == 7 and sel.makespan == 7.5 and sel.energy == 3.75 and sel.num_feasible == 1
+    lv, sel = run(emo, gh, 7.0, 1.0)
+    assert sel.index == -1 and sel.num_feasible == 0
+    del z
+    g = pins.graph_from_golden(pins.load_golden())
+    gh = emo.EmoGraph(g, device=0)
+    for kw, status in ((dict(latency_target=float("nan"), quantum=1.0), 1),
+                       (dict(latency_target=20.0, quantum=0.0), 1),
+                       (dict(latency_target=20.0, quantum=1.0, pack_order=[0, 0, 1]), 1),
+                       (dict(latency_target=20.0, quantum=2.0 ** -10, max_states=8), 1)):
+        with pytest.raises(emo.EmoError) as ei:
+            gh.dp_search(**kw)
+        assert ei.value.status == status, kw
+    # the same search twice: the scratch is reused and the result repeats exactly
+    a = run(emo, gh, 20.0, 1.0)
+    b = run(emo, gh, 20.0, 1.0)
+    assert np.array_equal(a[0], b[0]) and a[1] == b[1]
