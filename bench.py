@@ -97,6 +97,75 @@ def cpu_baseline(k: int, budget_s: float = 12.0):
                       f"({what} x{len(spec.targets)} target(s), fp64 C, 1 thread)"}
 
 
+def run_dp(args, emo, synth, np, torch):
+    """Policy search (Alg. 2, one frequency interval per pack) on workload k's graph and tables:
+    target 1.05 T0, buckets of 0.05 T0 / dp_buckets.  `value` = searches per second; the CPU
+    baseline runs the search oracle (the fp64 C predictor under Python control, one thread) on
+    the same search, whole when it takes seconds, else its first stages scaled to all stages."""
+    k = args.workload
+    g = synth.config_graph(k)
+    P, F = g.num_packs, g.num_levels
+    gh = emo.EmoGraph(g, device=0)
+    top = torch.full((1, P), F - 1, dtype=torch.uint8, device="cuda")
+    fast = torch.from_numpy(np.argmin(g.pack_time, axis=1).astype(np.uint8)[None, :]).cuda()
+    T0 = float(gh.eval_policies(top)[0].item())
+    Tl = float(gh.eval_policies(fast)[0].item())
+    tgt = float(np.float32(1.05 * T0))
+    q = float(np.float32(0.05 * T0 / args.dp_buckets))
+    nb = int(np.floor(tgt / q)) - max(0, int(np.floor(Tl / q)) - 1) + 1
+    cands = 1 + F + max(P - 1, 0) * nb * F
+    lv, res = gh.dp_search(tgt, q)
+    for _ in range(max(args.warmup - 1, 0)):
+        gh.dp_search(tgt, q, best_levels=lv, result=res)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    a.record()
+    for _ in range(args.steps):
+        gh.dp_search(tgt, q, best_levels=lv, result=res)
+    b.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms = a.elapsed_time(b) / args.steps
+    sel = emo.parse_selection(res)
+    E0 = float(gh.eval_policies(top)[1].item())
+    out = {
+        "metric": "policy search (Alg. 2, one interval per pack): searches/sec",
+        "value": 1e3 / ms, "unit": "searches/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": synth.CONFIGS[k].name, "packs": P, "levels": F, "stages": P,
+                   "buckets": nb, "quantum": q, "target_ratio": 1.05,
+                   "candidates_per_search": cands, "step": "emo_dp_search"},
+        "per_stage_us": 1e3 * ms / max(P, 1),
+        "candidates_evaluated_per_s": cands / (ms / 1e3),
+        "roofline": None,
+        "roofline_note": "launch-bound: a stage evaluates at most buckets x levels candidates "
+                         "(a few MB) in one evaluation kernel plus two small kernels",
+        "result": {"energy": sel.energy, "makespan": sel.makespan, "bucket": sel.index,
+                   "states": sel.num_feasible, "all_max_energy": E0, "T0": T0},
+        "wall_s": wall,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import dp as odp   # the CPU baseline leg only
+        stages = P if P * nb * F <= 1 << 20 else max(1, (1 << 20) // (nb * F))
+        t = time.perf_counter()
+        r = odp.dp_search(g, tgt, q, max_stages=stages)
+        dt = time.perf_counter() - t
+        whole = stages == P
+        out["cpu_baseline"] = {"value": stages / (dt * P), "unit": "searches/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": (f"the whole search ({r.evaluated} candidate evaluations in {dt:.2f} s"
+                                          if whole else
+                                          f"the first {stages} of {P} stages ({r.evaluated} candidate "
+                                          f"evaluations in {dt:.2f} s), scaled to {P} stages")
+                                         + "; fp64 C predictor, Python control, 1 thread)",
+                               "result": ({"energy": r.energy, "makespan": r.makespan,
+                                           "states": r.num_states} if whole else None)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -105,12 +174,17 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="benchmark workload 1..5 (default 2)")
     ap.add_argument("--copies", type=int, default=5, help="rotated copies of the level batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dp", action="store_true",
+                    help="time the policy search of Alg. 2 (emo_dp_search) on the workload's graph "
+                         "instead of the evaluation step")
+    ap.add_argument("--dp-buckets", type=int, default=64,
+                    help="makespan buckets of the search between T0 and 1.05 T0 (default 64)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB, --steps times (the reference "
                          "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build evaluates candidate policies on a single "
+        print("bench.py runs on one GPU only: the library evaluates candidate policies on a single "
               "MI355X (candidates would shard across GPUs with one MIN all-reduce of the "
               "selection key; that path is not built).", file=sys.stderr)
         sys.exit(2)
@@ -128,6 +202,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "launches": args.steps}))
+        return
+
+    if args.dp:
+        run_dp(args, emo, synth, np, torch)
         return
 
     k = args.workload

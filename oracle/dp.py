@@ -35,14 +35,17 @@ class DPResult:
     energy: float               # fp32 value, NaN when none
     makespan: float             # fp32 value, NaN when none
     num_states: int             # states stored after the last stage (with makespan <= T_max)
+    evaluated: int = 0          # candidate policies evaluated (P_0 included)
 
 
 def _f32(x) -> np.float32:
     return np.float32(x)
 
 
-def dp_search(g, latency_target: float, quantum: float, pack_order=None) -> DPResult:
-    """Alg. 2 over the packs of `g` in `pack_order` (default: pack ids in increasing order)."""
+def dp_search(g, latency_target: float, quantum: float, pack_order=None,
+              max_stages: int | None = None) -> DPResult:
+    """Alg. 2 over the packs of `g` in `pack_order` (default: pack ids in increasing order).
+    max_stages stops after that many stages (for timing a bounded sample)."""
     P, F = int(g.num_packs), int(g.num_levels)
     order = list(range(P)) if pack_order is None else [int(x) for x in pack_order]
     if sorted(order) != list(range(P)):
@@ -56,8 +59,9 @@ def dp_search(g, latency_target: float, quantum: float, pack_order=None) -> DPRe
     p0 = np.full(P, F - 1, dtype=np.uint8)
     T0, E0 = eval_batch(g, p0[None, :])
     states = [(math.floor(float(_f32(T0[0])) / q), _f32(E0[0]), _f32(T0[0]), p0)]
+    evaluated = 1
 
-    for p in order:
+    for p in order[:max_stages]:
         # P' = P with frequency f in interval p, for every stored state and every f
         cands = []
         for (_, _, _, lv) in states:
@@ -68,6 +72,7 @@ def dp_search(g, latency_target: float, quantum: float, pack_order=None) -> DPRe
         if not cands:          # no state left: every later stage is empty too
             break
         Tc, Ec = eval_batch(g, np.stack(cands))
+        evaluated += len(cands)
         nxt = {}
         for c, lv2 in enumerate(cands):
             t, e = _f32(Tc[c]), _f32(Ec[c])
@@ -84,8 +89,8 @@ def dp_search(g, latency_target: float, quantum: float, pack_order=None) -> DPRe
             best = (b, e, t, lv)
     n = sum(1 for s in states if s[2] <= t_max)
     if best is None:
-        return DPResult(None, float("nan"), float("nan"), n)
-    return DPResult(best[3].copy(), float(best[1]), float(best[2]), n)
+        return DPResult(None, float("nan"), float("nan"), n, evaluated)
+    return DPResult(best[3].copy(), float(best[1]), float(best[2]), n, evaluated)
 
 
 def exhaustive_best(g, latency_target: float):

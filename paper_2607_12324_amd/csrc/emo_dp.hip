@@ -1,12 +1,15 @@
 // Device kernels of the policy search (Alg. 2, Sec. IV-F) with one frequency interval per pack.
 //
 // A stage of the dynamic program sets the level of one pack p in every stored policy: the
-// stored states (one per makespan bucket, a level row each) are expanded into S x F candidate
-// rows, the candidates are evaluated by the batch evaluator (Alg. 1), and each bucket keeps the
-// candidate with the least key (fp32 energy bits << 32 | candidate index): the least energy,
+// stored states (one per makespan bucket) are S x F candidate rows (each stored policy with
+// every level f at p), the candidates are evaluated by the batch evaluator (Alg. 1), each
+// bucket keeps the candidate with the least key (fp32 energy bits << 32 | candidate index): the least energy,
 // and among equal energies the first candidate in the order (state, level), as a sequential
-// "replace when strictly lower" walk over the states in bucket order would keep.
+// "replace when strictly lower" walk over the states in bucket order would keep; the winners are
+// then written out directly as the next stage's candidate rows.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "emo_internal.h"
 
@@ -26,36 +29,32 @@ __global__ void dp_default_row(uint8_t *__restrict__ row, int32_t P, uint8_t top
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < P; i += gridDim.x * blockDim.x) row[i] = top;
 }
 
-// dp[0] = {P_0}: one state holding row 0 with P_0's makespan and energy (kept whatever the
-// makespan: the initialisation of Alg. 2 does not test the constraint).
-__global__ void dp_init_state(const uint8_t *__restrict__ row, int32_t P, const float *__restrict__ T,
-                              const float *__restrict__ E, uint8_t *__restrict__ state,
-                              unsigned long long *__restrict__ key, float *__restrict__ Tst) {
-    for (int32_t i = threadIdx.x; i < P; i += blockDim.x) state[i] = row[i];
-    if (threadIdx.x == 0) {
-        key[0] = (static_cast<unsigned long long>(__float_as_uint(E[0])) << 32);
-        Tst[0] = T[0];
-    }
-}
-
-// rows[s * F + f] = state s with level f at pack p.  States that hold no policy are expanded
-// as well (their rows are evaluated and then ignored), so the grid does not depend on them.
-__global__ void dp_expand(const uint8_t *__restrict__ states, int64_t S, int32_t P, int32_t F,
-                          int32_t p, uint8_t *__restrict__ rows) {
-    const int64_t n = S * F * P;
+// dp[0] = {P_0}: row0 (P_0, evaluated: T[0], E[0]) is the only stored policy.  Without packs it
+// is the final state (state, key, Tst); otherwise it is expanded into the F candidate rows of
+// the first stage (level f at pack p), its key marks it stored, and the first stage's output
+// keys are cleared.  (dp[0] keeps P_0 whatever its makespan: the initialisation of Alg. 2 does
+// not test the constraint.)
+__global__ void dp_seed(const uint8_t *__restrict__ row0, int32_t P, int32_t F, int32_t p,
+                        const float *__restrict__ T, const float *__restrict__ E,
+                        uint8_t *__restrict__ rows, uint8_t *__restrict__ state,
+                        unsigned long long *__restrict__ key, float *__restrict__ Tst,
+                        unsigned long long *__restrict__ out_keys, int64_t NB) {
+    const int64_t n = p >= 0 ? static_cast<int64_t>(F) * P : 0;
     for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
          i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int64_t r = i / P;
-        const int32_t col = static_cast<int32_t>(i - r * P);
-        const int64_t s = r / F;
-        rows[i] = col == p ? static_cast<uint8_t>(r - s * F) : states[s * P + col];
+        const int32_t f = static_cast<int32_t>(i / P), col = static_cast<int32_t>(i - static_cast<int64_t>(f) * P);
+        rows[i] = col == p ? static_cast<uint8_t>(f) : row0[col];
     }
-}
-
-__global__ void dp_clear_keys(unsigned long long *__restrict__ keys, int64_t n) {
-    for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
+    for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < P;
          i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-        keys[i] = kEmptyKey;
+        state[i] = row0[i];
+    for (int64_t b = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; b < NB;
+         b += static_cast<int64_t>(gridDim.x) * blockDim.x)
+        out_keys[b] = kEmptyKey;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        key[0] = static_cast<unsigned long long>(__float_as_uint(E[0])) << 32;
+        Tst[0] = T[0];
+    }
 }
 
 // Candidate c (from state c / F) with makespan T[c] <= tmax proposes itself for bucket
@@ -77,22 +76,37 @@ __global__ void dp_bucket(const float *__restrict__ T, const float *__restrict__
     }
 }
 
-// dst[b] = the winning candidate row of bucket b, Tst[b] its makespan.
-__global__ void dp_gather(const uint8_t *__restrict__ rows, const float *__restrict__ T,
-                          const unsigned long long *__restrict__ keys, int64_t NB, int32_t P,
-                          uint8_t *__restrict__ dst, float *__restrict__ Tst) {
-    const int64_t n = NB * P;
+// After the bucket step of a stage: the winning candidate of each bucket b becomes stored
+// policy b.  With a next pack p_next >= 0 it is expanded at once into that stage's candidate
+// rows next_rows[b * F + f] (level f at p_next); after the last stage it is copied to state[b]
+// with its makespan Tst[b].  Also clears done_keys (the keys of this stage's source states, no
+// longer read), which the next stage's bucket step fills.
+__global__ void dp_advance(const uint8_t *__restrict__ rows, const float *__restrict__ T,
+                           const unsigned long long *__restrict__ keys, int64_t NB, int32_t P,
+                           int32_t F, int32_t p_next, uint8_t *__restrict__ next_rows,
+                           uint8_t *__restrict__ state, float *__restrict__ Tst,
+                           unsigned long long *__restrict__ done_keys) {
+    const int64_t per = p_next >= 0 ? static_cast<int64_t>(F) * P : P;   // bytes per bucket
+    const int64_t n = NB * per;
     for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
          i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int64_t b = i / P;
+        const int64_t b = i / per;
         const unsigned long long k = keys[b];
         if (k == kEmptyKey) continue;
-        dst[i] = rows[static_cast<int64_t>(k & 0xffffffffull) * P + (i - b * P)];
+        const int64_t c = static_cast<int64_t>(k & 0xffffffffull);
+        const int64_t j = i - b * per;
+        if (p_next >= 0) {
+            const int32_t f = static_cast<int32_t>(j / P), col = static_cast<int32_t>(j - static_cast<int64_t>(f) * P);
+            next_rows[i] = col == p_next ? static_cast<uint8_t>(f) : rows[c * P + col];
+        } else {
+            state[i] = rows[c * P + j];
+        }
     }
     for (int64_t b = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; b < NB;
          b += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const unsigned long long k = keys[b];
         if (k != kEmptyKey) Tst[b] = T[k & 0xffffffffull];
+        done_keys[b] = kEmptyKey;
     }
 }
 
@@ -153,29 +167,27 @@ hipError_t dp_launch_default_row(uint8_t *row, int32_t P, int32_t F, hipStream_t
     return hipGetLastError();
 }
 
-hipError_t dp_launch_init_state(const uint8_t *row, int32_t P, const float *T, const float *E,
-                                uint8_t *state, unsigned long long *key, float *Tst, hipStream_t s) {
-    dp_init_state<<<1, kThreads, 0, s>>>(row, P, T, E, state, key, Tst);
+hipError_t dp_launch_seed(const uint8_t *row0, int32_t P, int32_t F, int32_t p, const float *T,
+                          const float *E, uint8_t *rows, uint8_t *state, unsigned long long *key,
+                          float *Tst, unsigned long long *out_keys, int64_t NB, hipStream_t s) {
+    const int64_t n = std::max<int64_t>(std::max<int64_t>(static_cast<int64_t>(F) * P, NB), 1);
+    dp_seed<<<blocks_for(n), kThreads, 0, s>>>(row0, P, F, p, T, E, rows, state, key, Tst, out_keys, NB);
     return hipGetLastError();
 }
 
-hipError_t dp_launch_expand(const uint8_t *states, int64_t S, int32_t P, int32_t F, int32_t p,
-                            uint8_t *rows, hipStream_t s) {
-    dp_expand<<<blocks_for(S * F * P), kThreads, 0, s>>>(states, S, P, F, p, rows);
-    return hipGetLastError();
-}
-
-hipError_t dp_launch_select(const float *T, const float *E, const unsigned long long *src_keys,
+hipError_t dp_launch_bucket(const float *T, const float *E, const unsigned long long *src_keys,
                             int64_t B, int32_t F, float tmax, double q, int64_t bmin, int64_t NB,
                             unsigned long long *keys, hipStream_t s) {
-    dp_clear_keys<<<blocks_for(NB), kThreads, 0, s>>>(keys, NB);
     dp_bucket<<<blocks_for(B), kThreads, 0, s>>>(T, E, src_keys, B, F, tmax, q, bmin, NB, keys);
     return hipGetLastError();
 }
 
-hipError_t dp_launch_gather(const uint8_t *rows, const float *T, const unsigned long long *keys,
-                            int64_t NB, int32_t P, uint8_t *dst, float *Tst, hipStream_t s) {
-    dp_gather<<<blocks_for(NB * (P > 0 ? P : 1)), kThreads, 0, s>>>(rows, T, keys, NB, P, dst, Tst);
+hipError_t dp_launch_advance(const uint8_t *rows, const float *T, const unsigned long long *keys,
+                             int64_t NB, int32_t P, int32_t F, int32_t p_next, uint8_t *next_rows,
+                             uint8_t *state, float *Tst, unsigned long long *done_keys, hipStream_t s) {
+    const int64_t per = p_next >= 0 ? static_cast<int64_t>(F) * P : P;
+    dp_advance<<<blocks_for(std::max<int64_t>(NB * per, NB)), kThreads, 0, s>>>(
+        rows, T, keys, NB, P, F, p_next, next_rows, state, Tst, done_keys);
     return hipGetLastError();
 }
 

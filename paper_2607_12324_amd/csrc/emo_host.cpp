@@ -1365,11 +1365,13 @@ double least_makespan(const emo_graph_s &g) {
     return T;
 }
 
-// Device scratch of one search, carved from one arena block (256-byte aligned pieces).
+// Device scratch of one search, carved from one arena block (256-byte aligned pieces): two
+// candidate row buffers (this stage's and the next), the stored states after the last stage,
+// two key buffers (a stage's source states and its buckets), makespans and energies.
 struct DPBuffers {
-    uint8_t *rows, *state[2];
+    uint8_t *rows[2], *state;
     unsigned long long *keys[2];
-    float *Tst[2], *T, *E;
+    float *Tst, *T, *E;
 };
 
 size_t dp_layout(int64_t S, int64_t R, int32_t P, DPBuffers *b, char *base) {
@@ -1380,12 +1382,12 @@ size_t dp_layout(int64_t S, int64_t R, int32_t P, DPBuffers *b, char *base) {
         return p;
     };
     const size_t pb = static_cast<size_t>(P > 0 ? P : 1);
-    b->rows = reinterpret_cast<uint8_t *>(take(static_cast<size_t>(R) * pb));
     for (int i = 0; i < 2; ++i) {
-        b->state[i] = reinterpret_cast<uint8_t *>(take(static_cast<size_t>(S) * pb));
+        b->rows[i] = reinterpret_cast<uint8_t *>(take(static_cast<size_t>(R) * pb));
         b->keys[i] = reinterpret_cast<unsigned long long *>(take(static_cast<size_t>(S) * 8));
-        b->Tst[i] = reinterpret_cast<float *>(take(static_cast<size_t>(S) * 4));
     }
+    b->state = reinterpret_cast<uint8_t *>(take(static_cast<size_t>(S) * pb));
+    b->Tst = reinterpret_cast<float *>(take(static_cast<size_t>(S) * 4));
     b->T = reinterpret_cast<float *>(take(static_cast<size_t>(R) * 4));
     b->E = reinterpret_cast<float *>(take(static_cast<size_t>(R) * 4));
     return off;
@@ -1444,27 +1446,30 @@ emo_status emo_dp_search(emo_graph_t g, float latency_target, float quantum, con
         return fail(EMO_ERR_OUT_OF_MEMORY, "scratch of %zu bytes: %s", bytes, hipGetErrorString(e));
     }
     dp_layout(S, R, P, &b, static_cast<char *>(base));
-    // dp[0] = {P_0}
-    e = emo::dp_launch_default_row(b.rows, P, F, st);
-    if (e == hipSuccess) s = evaluate(g, b.rows, 1, b.T, b.E, nullptr, 0, 0.f, nullptr, nullptr, st);
+    // dp[0] = {P_0}, expanded into the first stage's candidates (row buffer 1 holds P_0)
+    e = emo::dp_launch_default_row(b.rows[1], P, F, st);
+    if (e == hipSuccess) s = evaluate(g, b.rows[1], 1, b.T, b.E, nullptr, 0, 0.f, nullptr, nullptr, st);
     if (e == hipSuccess && s == EMO_OK)
-        e = emo::dp_launch_init_state(b.rows, P, b.T, b.E, b.state[0], b.keys[0], b.Tst[0], st);
+        e = emo::dp_launch_seed(b.rows[1], P, F, P > 0 ? order[0] : -1, b.T, b.E, b.rows[0], b.state,
+                                b.keys[0], b.Tst, b.keys[1], NB, st);
     int64_t cur = 1;
-    int a = 0;
-    // one stage per interval (pack): every stored policy with each level at that pack
+    int kfin = 0;
+    // stage i sets pack order[i]: its candidates are in rows[i % 2], its source keys in
+    // keys[i % 2], its buckets go to keys[1 - i % 2]
     for (int32_t i = 0; i < P && NB > 0 && e == hipSuccess && s == EMO_OK; ++i) {
+        const int x = i % 2;
         const int64_t B = cur * F;
-        e = emo::dp_launch_expand(b.state[a], cur, P, F, order[i], b.rows, st);
-        if (e != hipSuccess) break;
-        s = evaluate(g, b.rows, B, b.T, b.E, nullptr, 0, 0.f, nullptr, nullptr, st);
+        s = evaluate(g, b.rows[x], B, b.T, b.E, nullptr, 0, 0.f, nullptr, nullptr, st);
         if (s != EMO_OK) break;
-        e = emo::dp_launch_select(b.T, b.E, b.keys[a], B, F, latency_target, q, bmin, NB, b.keys[1 - a], st);
-        if (e == hipSuccess) e = emo::dp_launch_gather(b.rows, b.T, b.keys[1 - a], NB, P, b.state[1 - a], b.Tst[1 - a], st);
-        a = 1 - a;
+        e = emo::dp_launch_bucket(b.T, b.E, b.keys[x], B, F, latency_target, q, bmin, NB, b.keys[1 - x], st);
+        if (e == hipSuccess)
+            e = emo::dp_launch_advance(b.rows[x], b.T, b.keys[1 - x], NB, P, F, i + 1 < P ? order[i + 1] : -1,
+                                       b.rows[1 - x], b.state, b.Tst, b.keys[x], st);
+        kfin = 1 - x;
         cur = NB;
     }
     if (e == hipSuccess && s == EMO_OK)
-        e = emo::dp_launch_final(b.state[a], b.keys[a], b.Tst[a], cur, P, latency_target, q, best_levels, result, st);
+        e = emo::dp_launch_final(b.state, b.keys[kfin], b.Tst, cur, P, latency_target, q, best_levels, result, st);
     hipError_t er = arena_release(g->dp_arena, st);
     if (s != EMO_OK) return s;
     if (e == hipSuccess) e = er;

@@ -152,22 +152,24 @@ hipError_t launch_chains(const DevGraph &g, const DevChains &c, const uint8_t *l
 
 // ---------------------------------------------------------------- policy search (Alg. 2)
 
-// Kernels of emo_dp_search (one frequency interval per pack).  A stage: dp_launch_expand turns
-// the S stored states ([S][P] level rows) into S*F candidate rows with level f at pack p, the
-// batch evaluator computes their makespans and energies, dp_launch_select keeps for each of the
-// NB buckets (floor(makespan / q) - bmin) the least key (fp32 energy bits << 32 | candidate) of
-// the candidates that come from a stored state (src_keys != empty) and meet tmax, and
-// dp_launch_gather copies each bucket's winning row (and makespan) into the next states.
+// Kernels of emo_dp_search (one frequency interval per pack).  dp_launch_seed stores P_0 (row0,
+// evaluated) and expands it into the first stage's F candidate rows.  A stage: the batch
+// evaluator computes the makespans and energies of its S*F candidate rows, dp_launch_bucket
+// keeps for each of the NB buckets (floor(makespan / q) - bmin) the least key (fp32 energy
+// bits << 32 | candidate) among the candidates that come from a stored state (src_keys not
+// empty) and meet tmax, and dp_launch_advance writes each bucket's winner as the next stage's
+// candidate rows (level f at p_next), or after the last stage as a stored state with its
+// makespan, and clears the stage's source keys for the next bucket step.
 hipError_t dp_launch_default_row(uint8_t *row, int32_t P, int32_t F, hipStream_t s);
-hipError_t dp_launch_init_state(const uint8_t *row, int32_t P, const float *T, const float *E,
-                                uint8_t *state, unsigned long long *key, float *Tst, hipStream_t s);
-hipError_t dp_launch_expand(const uint8_t *states, int64_t S, int32_t P, int32_t F, int32_t p,
-                            uint8_t *rows, hipStream_t s);
-hipError_t dp_launch_select(const float *T, const float *E, const unsigned long long *src_keys,
+hipError_t dp_launch_seed(const uint8_t *row0, int32_t P, int32_t F, int32_t p, const float *T,
+                          const float *E, uint8_t *rows, uint8_t *state, unsigned long long *key,
+                          float *Tst, unsigned long long *out_keys, int64_t NB, hipStream_t s);
+hipError_t dp_launch_bucket(const float *T, const float *E, const unsigned long long *src_keys,
                             int64_t B, int32_t F, float tmax, double q, int64_t bmin, int64_t NB,
                             unsigned long long *keys, hipStream_t s);
-hipError_t dp_launch_gather(const uint8_t *rows, const float *T, const unsigned long long *keys,
-                            int64_t NB, int32_t P, uint8_t *dst, float *Tst, hipStream_t s);
+hipError_t dp_launch_advance(const uint8_t *rows, const float *T, const unsigned long long *keys,
+                             int64_t NB, int32_t P, int32_t F, int32_t p_next, uint8_t *next_rows,
+                             uint8_t *state, float *Tst, unsigned long long *done_keys, hipStream_t s);
 // The least-energy stored state with makespan <= tmax (ties: lowest bucket) to best and res.
 hipError_t dp_launch_final(const uint8_t *states, const unsigned long long *keys, const float *Tst,
                            int64_t S, int32_t P, float tmax, double q, uint8_t *best,
