@@ -33,9 +33,12 @@
  * buffer.  Batch calls are asynchronous on `stream` (a hipStream_t; NULL means the default
  * stream): the caller keeps inputs and outputs alive until the stream has completed.  Scratch
  * device memory is kept by each graph handle (and, for emo_select_from_results, per device)
- * and reused: it grows with hipMalloc when a call needs more (waiting for the calls still
- * using it) and is freed with the handle, so steady-state calls allocate nothing and never
- * block the host.
+ * and reused: one buffer for each of the first eight streams that call (calls on one stream
+ * are ordered by that stream) and one shared by calls from further streams.  It grows with
+ * hipMalloc when a call needs more (waiting for the calls still using it) and is freed with
+ * the handle, so steady-state calls allocate nothing and never block the host.  Since a
+ * stream's buffer is found again by the stream's handle, a stream must have completed the
+ * calls made on it before it is destroyed (a new stream may receive the same handle).
  *
  * Errors: every entry point returns an emo_status.  Argument errors that the host can detect
  * (sizes, null pointers, indices, non-finite or negative values, cycles, misaligned buffers)
@@ -44,9 +47,10 @@
  * that candidate's makespan, energy and slack are NaN and it is never feasible.
  *
  * Thread safety: a loaded graph is immutable; calls on one handle from several threads or
- * streams are safe.  They share the handle's scratch, so the device runs them one after the
- * other: a call on a different stream than the previous one first waits (on the device) for
- * that call's kernels.
+ * streams are safe.  Calls from the first eight streams use a scratch buffer per stream; calls
+ * from further streams share one, so the device runs those one after the other: such a call on
+ * a different stream than the previous one first waits (on the device) for that call's
+ * kernels.
  */
 #ifndef EMO_H
 #define EMO_H

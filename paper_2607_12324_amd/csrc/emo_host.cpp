@@ -105,27 +105,76 @@ struct DeviceGuard {
 };
 
 // Device scratch reused across batch calls (selection partials, checkpoint rows, cold slots):
-// allocated on first need, grown (never shrunk) on demand, freed with its owner.  Calls that
-// share an arena are ordered on the device: a call on another stream than the previous one
-// first waits for the event recorded after that call's kernels, and growing waits for it on
-// the host before the old buffer is freed.  Steady-state calls allocate and free nothing, so
-// the host never blocks and keeps launching ahead of the device.
+// allocated on first need, grown (never shrunk) on demand, freed with its owner.  Each of the
+// first kStreamSlots streams that call gets a buffer of its own: calls on one stream are
+// ordered by the stream, so they reuse it with no event and no host wait (an event record per
+// call cost about 4 us of device time between kernels), and growing waits for that stream,
+// which is live since it is the caller's.  Calls from further streams share one buffer: a call
+// on another stream than the previous one first waits for the event recorded after that
+// call's kernels, and growing waits for it on the host before the old buffer is freed.
+// Steady-state calls allocate and free nothing, so the host keeps launching ahead of the
+// device.
+constexpr int kStreamSlots = 8;
+
 struct Arena {
+    struct Slot {
+        hipStream_t s = nullptr;
+        void *ptr = nullptr;
+        size_t bytes = 0;
+    };
     std::mutex mu;
+    Slot slots[kStreamSlots];
+    int nslots = 0;
+    // the shared buffer of calls from further streams
     void *ptr = nullptr;
     size_t bytes = 0;
-    hipEvent_t done = nullptr;   // recorded after the last call's kernels
+    hipEvent_t done = nullptr;   // recorded after the last shared call's kernels
     hipStream_t last = nullptr;
     bool used = false;
+    bool shared_call = false;    // the current call uses the shared buffer
 };
+
+size_t grown(size_t need, size_t have) { return std::max(need, have + have / 4); }
 
 // With a.mu held and the arena's device current: at least `bytes` of scratch for a call on s.
 hipError_t arena_acquire(Arena &a, size_t bytes, hipStream_t s, void **out) {
     hipError_t e = hipSuccess;
+    a.shared_call = false;
+    for (int i = 0; i < a.nslots; ++i) {
+        Arena::Slot &sl = a.slots[i];
+        if (sl.s != s) continue;
+        if (bytes > sl.bytes) {
+            if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;   // earlier calls on s
+            const size_t want = grown(bytes, sl.bytes);
+            (void)hipFree(sl.ptr);
+            sl.ptr = nullptr;
+            sl.bytes = 0;
+            if ((e = hipMalloc(&sl.ptr, want)) != hipSuccess) {
+                sl.ptr = nullptr;
+                return e;
+            }
+            sl.bytes = want;
+        }
+        *out = sl.ptr;
+        return hipSuccess;
+    }
+    if (a.nslots < kStreamSlots) {
+        Arena::Slot &sl = a.slots[a.nslots];
+        if ((e = hipMalloc(&sl.ptr, bytes)) != hipSuccess) {
+            sl.ptr = nullptr;
+            return e;
+        }
+        sl.s = s;
+        sl.bytes = bytes;
+        ++a.nslots;
+        *out = sl.ptr;
+        return hipSuccess;
+    }
+    a.shared_call = true;
     if (!a.done && (e = hipEventCreateWithFlags(&a.done, hipEventDisableTiming)) != hipSuccess) return e;
     if (bytes > a.bytes) {
         if (a.used && (e = hipEventSynchronize(a.done)) != hipSuccess) return e;
-        const size_t want = std::max(bytes, a.bytes + a.bytes / 4);
+        const size_t want = grown(bytes, a.bytes);
         if (a.ptr) (void)hipFree(a.ptr);
         a.ptr = nullptr;
         a.bytes = 0;
@@ -141,14 +190,18 @@ hipError_t arena_acquire(Arena &a, size_t bytes, hipStream_t s, void **out) {
     return hipSuccess;
 }
 
-// With a.mu held: marks the end of the call's kernels on s.
+// With a.mu held: marks the end of the call's kernels on s (shared buffer only).
 hipError_t arena_release(Arena &a, hipStream_t s) {
+    if (!a.shared_call) return hipSuccess;
     a.used = true;
     a.last = s;
     return hipEventRecord(a.done, s);
 }
 
 void arena_free(Arena &a) {
+    for (int i = 0; i < a.nslots; ++i)
+        if (a.slots[i].ptr) (void)hipFree(a.slots[i].ptr);
+    a.nslots = 0;
     if (a.done) (void)hipEventDestroy(a.done);
     if (a.ptr) (void)hipFree(a.ptr);
     a.done = nullptr;

@@ -589,6 +589,47 @@ def test_scratch_reuse_across_streams(torch, emo, mode):
     parity.assert_eval(ref[3][1], ref[3][2], T_or, E_or, True, "scratch reuse")
 
 
+def test_scratch_with_many_streams(torch, emo):
+    """Calls from twelve streams without host synchronisation: the first eight streams get a
+    scratch buffer each, the others share one ordered by an event; growing batches make every
+    kind of buffer grow while earlier calls may still be running.  Every result equals the
+    single-stream one bit for bit."""
+    g = synth.packed_graph(9, 1024, 8, 16, sync_every=128, cross_p=0.05)
+    rng = np.random.default_rng(12)
+    sizes = [64, 300, 1000, 2000, 4096, 128, 3000, 700, 4096, 50, 2500, 4096] * 2
+    rows = [pins.random_rows(rng, g, n) for n in sizes[:12]]
+    print(f"[case] scratch with 12 streams", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    lvs = [dev(torch, r) for r in rows]
+    ref = []
+    for lv in lvs:
+        S = gh.slack(lv)
+        T, E = gh.eval_policies(lv)
+        torch.cuda.synchronize()
+        ref.append((host(S).copy(), host(T).copy(), host(E).copy()))
+    gh2 = emo.EmoGraph(g, device=0)
+    streams = [torch.cuda.Stream() for _ in range(12)]
+    outs = []
+    for i, n in enumerate(sizes):
+        st = streams[i % 12]
+        lv = lvs[i % 12]
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            S = torch.empty((lv.shape[0], g.num_packs), dtype=torch.float32, device="cuda")
+            gh2.slack(lv, out=S, stream=st)
+            T, E = gh2.eval_policies(lv, stream=st)
+            res, _ = emo.select_from_results(T, E, 1e9, stream=st)
+        outs.append((i % 12, S, T, E, res))
+    torch.cuda.synchronize()
+    for j, S, T, E, res in outs:
+        Sr, Tr, Er = ref[j]
+        assert np.array_equal(host(S).view(np.uint32), Sr.view(np.uint32)), j
+        assert np.array_equal(host(T).view(np.uint32), Tr.view(np.uint32)), j
+        assert np.array_equal(host(E).view(np.uint32), Er.view(np.uint32)), j
+        sel = emo.parse_selection(res)
+        assert sel.num_feasible == len(Tr) and sel.index == int(np.argmin(Er)), j
+
+
 def test_large_slot_count_uses_device_scratch(torch, emo):
     """A wide antichain of packs feeding one sink keeps many finish times live at once."""
     rng = np.random.default_rng(5)
