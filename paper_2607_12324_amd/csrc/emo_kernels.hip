@@ -405,9 +405,71 @@ __global__ void empty_result(emo_selection *res) {
     r->num_feasible = 0;
 }
 
-__global__ void __launch_bounds__(kBlock)
+// Stage 2 of the selection: one workgroup of kFinThreads reduces the n partial records into the
+// emo_selection record.  It is latency-bound, so each thread keeps four independent loads in
+// flight and a round covers 4 * kFinThreads records (all of them up to 4M candidates).
+constexpr int kFinThreads = 1024;
+constexpr int kFinWaves = kFinThreads / kWave;
+
+__global__ void __launch_bounds__(kFinThreads)
 select_finalize_kernel(const EmoPartial *__restrict__ part, int64_t n, emo_selection *res) {
-    emo_select_finalize(part, n, res);
+    __shared__ unsigned long long s_key[kFinWaves];
+    __shared__ float s_T[kFinWaves];
+    __shared__ unsigned long long s_cnt[kFinWaves];
+    unsigned long long key = ~0ull;
+    float T = 0.f;
+    unsigned long long cnt = 0;
+    for (int64_t base = threadIdx.x; base < n; base += 4 * kFinThreads) {
+        EmoPartial p[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int64_t i = base + k * kFinThreads;
+            if (i < n) {
+                p[k] = part[i];
+            } else {
+                p[k].key = ~0ull;
+                p[k].count = 0;
+                p[k].makespan = 0.f;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            cnt += p[k].count;
+            if (p[k].key < key) {
+                key = p[k].key;
+                T = p[k].makespan;
+            }
+        }
+    }
+    emo_wave_min_key(&key, &T);
+    for (int off = kWave / 2; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    if (lane == 0) {
+        s_key[wave] = key;
+        s_T[wave] = T;
+        s_cnt[wave] = cnt;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int w = 1; w < kFinWaves; ++w) {
+        if (s_key[w] < key) {
+            key = s_key[w];
+            T = s_T[w];
+        }
+        cnt += s_cnt[w];
+    }
+    EmoSel *r = reinterpret_cast<EmoSel *>(res);
+    if (key == ~0ull) {
+        r->index = -1;
+        r->energy = __builtin_nanf("");
+        r->makespan = __builtin_nanf("");
+    } else {
+        r->index = static_cast<int64_t>(key & 0xffffffffull);
+        r->energy = __uint_as_float(static_cast<unsigned int>(key >> 32));
+        r->makespan = T;
+    }
+    r->num_feasible = static_cast<int64_t>(cnt);
 }
 
 __global__ void __launch_bounds__(kBlock)
@@ -526,7 +588,7 @@ hipError_t launch_empty_result(emo_selection *res, hipStream_t s) {
 
 hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selection *res,
                                   hipStream_t s) {
-    hipLaunchKernelGGL(select_finalize_kernel, dim3(1), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(select_finalize_kernel, dim3(1), dim3(kFinThreads), 0, s,
                        static_cast<const EmoPartial *>(part), nparts, res);
     return hipGetLastError();
 }

@@ -8,7 +8,8 @@
 //   1. for every group of EMO_BLOCK consecutive candidates, the workgroup that evaluates it
 //      writes the mask bits of its candidates and one partial record: its least key, its number
 //      of feasible candidates and the makespan of the candidate holding that key;
-//   2. one block reduces the partial records and writes the emo_selection record.
+//   2. one workgroup reduces the partial records and writes the emo_selection record (a kernel
+//      of the precompiled library, launched after the evaluating kernel).
 // The key of a feasible candidate c is (fp32 bits of its energy) << 32 | c.  Energies are
 // >= 0, so the bit pattern orders like the value and equal energies order by index; an
 // infeasible candidate has the key ~0.
@@ -90,67 +91,4 @@ __device__ void emo_select_block(long long group, bool active, float T, float E,
         }
         part[group] = p;
     }
-}
-
-// Stage 2, run by one block of EMO_BLOCK threads: reduces n partial records into the
-// emo_selection record `res`.
-__device__ void emo_select_finalize(const EmoPartial *part, long long n, void *res) {
-    __shared__ unsigned long long s_key[EMO_WAVES_PER_BLOCK];
-    __shared__ float s_T[EMO_WAVES_PER_BLOCK];
-    __shared__ unsigned long long s_cnt[EMO_WAVES_PER_BLOCK];
-    unsigned long long key = ~0ull;
-    float T = 0.f;
-    unsigned long long cnt = 0;
-    // four independent loads in flight per thread: the single workgroup is latency-bound
-    for (long long base = threadIdx.x; base < n; base += 4 * EMO_BLOCK) {
-        EmoPartial p[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const long long i = base + k * EMO_BLOCK;
-            if (i < n) {
-                p[k] = part[i];
-            } else {
-                p[k].key = ~0ull;
-                p[k].count = 0;
-                p[k].makespan = 0.f;
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            cnt += p[k].count;
-            if (p[k].key < key) {
-                key = p[k].key;
-                T = p[k].makespan;
-            }
-        }
-    }
-    emo_wave_min_key(&key, &T);
-    for (int off = EMO_WAVE / 2; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, EMO_WAVE);
-    const int lane = threadIdx.x % EMO_WAVE;
-    const int wave = threadIdx.x / EMO_WAVE;
-    if (lane == 0) {
-        s_key[wave] = key;
-        s_T[wave] = T;
-        s_cnt[wave] = cnt;
-    }
-    __syncthreads();
-    if (threadIdx.x != 0) return;
-    for (int w = 1; w < EMO_WAVES_PER_BLOCK; ++w) {
-        if (s_key[w] < key) {
-            key = s_key[w];
-            T = s_T[w];
-        }
-        cnt += s_cnt[w];
-    }
-    EmoSel *r = (EmoSel *)res;
-    if (key == ~0ull) {
-        r->index = -1;
-        r->energy = __builtin_nanf("");
-        r->makespan = __builtin_nanf("");
-    } else {
-        r->index = (long long)(key & 0xffffffffull);
-        r->energy = __uint_as_float((unsigned int)(key >> 32));
-        r->makespan = T;
-    }
-    r->num_feasible = (long long)cnt;
 }

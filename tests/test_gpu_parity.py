@@ -718,6 +718,32 @@ def test_determinism(torch, emo, mode):
     assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
 
 
+@pytest.mark.parametrize("mode", [0, 1], ids=["auto", "interpreted"])
+def test_selection_across_calls(torch, emo, mode):
+    """Calls that select, calls that do not (which reuse the same scratch buffer for other data)
+    and selections from stored results, with batches that shrink and grow, on one stream: every
+    selection matches the oracle's."""
+    rng = np.random.default_rng(4242 + mode)
+    g = synth.random_dag(rng, 180, 3.0 / 180, 0.6, 9)
+    rows = pins.random_rows(rng, g, 70001)
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    gh = emo.EmoGraph(g, device=0, kernel_mode=mode)
+    lv = dev(torch, rows)
+    tq = [float(np.float32(np.quantile(T_or, q))) for q in (0.05, 0.5, 1.0)]
+    for n, tgt in ((70001, tq[0]), (513, tq[1]), (70001, tq[2]), (1, tq[2]), (40000, tq[0]), (256, tq[1])):
+        print(f"[case] across calls mode={mode} B={n} target={tgt}", flush=True)
+        res, mask = gh.select_policy(lv[:n], tgt)
+        parity.assert_selection(emo.parse_selection(res), emo.unpack_mask(mask, n), T_or[:n], E_or[:n],
+                                tgt, True, f"select B={n}")
+        T, E = gh.eval_policies(lv[:n])                        # no selection: scratch reused
+        S = gh.slack(lv[:min(n, 3000)])
+        del S
+        res2, mask2 = emo.select_from_results(T, E, tgt)
+        parity.assert_selection(emo.parse_selection(res2), emo.unpack_mask(mask2, n), T_or[:n], E_or[:n],
+                                tgt, True, f"select_from_results B={n}")
+    gh.close()
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_workload_full_batch(torch, emo, k):
     """Every candidate of workload k: makespan/energy of all rows, masks and selection for each
