@@ -1278,7 +1278,8 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     const int64_t nblocks = path == Path::kSingle  ? emo::jit_blocks(g->jm, B)
                             : path == Path::kChain ? emo::jit_chain_blocks(g->jc, B)
                             : path == Path::kCut   ? emo::jit_cut_blocks(g->jk, B)
-                                                   : emo::forward_blocks(B);   // also chain lanes
+                            : path == Path::kChainLanes ? emo::select_results_blocks(B)
+                                                   : emo::forward_blocks(B);
     const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
     size_t part_bytes = result ? static_cast<size_t>(nblocks) * emo::kPartialBytes : 0;
     part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
@@ -1379,7 +1380,7 @@ emo_status emo_select_from_results(const float *makespan, const float *energy, i
     if (std::isnan(latency_target)) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (B == 0) return after_launch(emo::launch_empty_result(result, st), "emo_select_from_results");
-    const int64_t nblocks = emo::forward_blocks(B);
+    const int64_t nblocks = emo::select_results_blocks(B);
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess || dev < 0 || dev >= kMaxDevices)

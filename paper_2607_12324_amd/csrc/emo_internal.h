@@ -90,7 +90,9 @@ int64_t forward_blocks(int64_t B);
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s);
 hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selection *res,
                                   hipStream_t s);
-// Stage 1 of a selection from stored makespans and energies (forward_blocks(B) partials).
+// Stage 1 of a selection from stored makespans and energies (select_results_blocks(B)
+// partials: one per 1024 candidates).
+int64_t select_results_blocks(int64_t B);
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
                                  uint32_t *mask, void *part, hipStream_t s);
 
@@ -145,7 +147,7 @@ bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *
 size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
                             const float *slack);
 // Makespan/energy (and per-pack slack when `slack`); the selection stage 1 runs from the stored
-// makespans and energies (forward_blocks(B) partial records in `part`).
+// makespans and energies (select_results_blocks(B) partial records in `part`).
 hipError_t launch_chains(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
                          float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
                          void *scratch, hipStream_t s);

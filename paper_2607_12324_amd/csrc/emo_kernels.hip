@@ -472,13 +472,82 @@ select_finalize_kernel(const EmoPartial *__restrict__ part, int64_t n, emo_selec
     r->num_feasible = static_cast<int64_t>(cnt);
 }
 
+// Selection from stored makespans and energies: each lane takes kSelPer consecutive candidates
+// (16-byte loads when both arrays are 16-byte aligned), so a workgroup covers kSelGroup
+// candidates and writes one partial record for them.  A wave covers 8 mask words: the lanes
+// 8j .. 8j+7 hold the 32 candidates of word j, four bits each.
+constexpr int kSelPer = 4;
+constexpr int64_t kSelGroup = static_cast<int64_t>(kBlock) * kSelPer;
+
 __global__ void __launch_bounds__(kBlock)
 select_results_kernel(const float *__restrict__ T, const float *__restrict__ E, int64_t B,
-                      float target, uint32_t *__restrict__ mask, EmoPartial *part) {
-    const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    const bool active = gid < B;
-    const int64_t c = active ? gid : B - 1;
-    emo_select_block(blockIdx.x, active, T[c], E[c], c, B, target, mask, part);
+                      float target, uint32_t *__restrict__ mask, EmoPartial *part, bool vec) {
+    __shared__ unsigned long long s_key[kWavesPerBlock];
+    __shared__ float s_T[kWavesPerBlock];
+    __shared__ unsigned int s_cnt[kWavesPerBlock];
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kSelGroup + static_cast<int64_t>(threadIdx.x) * kSelPer;
+    float t[kSelPer], e[kSelPer];
+    if (vec && c0 + kSelPer <= B) {
+        const float4 tv = *reinterpret_cast<const float4 *>(T + c0);
+        const float4 ev = *reinterpret_cast<const float4 *>(E + c0);
+        t[0] = tv.x; t[1] = tv.y; t[2] = tv.z; t[3] = tv.w;
+        e[0] = ev.x; e[1] = ev.y; e[2] = ev.z; e[3] = ev.w;
+    } else {
+#pragma unroll
+        for (int k = 0; k < kSelPer; ++k) {
+            const bool in = c0 + k < B;
+            t[k] = in ? T[c0 + k] : 0.f;
+            e[k] = in ? E[c0 + k] : 0.f;
+        }
+    }
+    unsigned int nib = 0u;
+    unsigned long long key = ~0ull;
+    float kT = 0.f;
+#pragma unroll
+    for (int k = 0; k < kSelPer; ++k) {
+        const bool feas = c0 + k < B && t[k] <= target;   // false for NaN
+        nib |= feas ? 1u << k : 0u;
+        const unsigned long long kk = feas ? (static_cast<unsigned long long>(__float_as_uint(e[k])) << 32) |
+                                                 static_cast<unsigned long long>(c0 + k)
+                                           : ~0ull;
+        if (kk < key) {
+            key = kk;
+            kT = t[k];
+        }
+    }
+    if (mask) {
+        unsigned int w = nib << (kSelPer * (lane & 7));
+        w |= __shfl_xor(w, 1, kWave);
+        w |= __shfl_xor(w, 2, kWave);
+        w |= __shfl_xor(w, 4, kWave);
+        const int64_t word = c0 / 32;
+        if ((lane & 7) == 0 && word * 32 < B) mask[word] = w;
+    }
+    emo_wave_min_key(&key, &kT);
+    unsigned int cnt = static_cast<unsigned int>(__popc(nib));
+    for (int off = kWave / 2; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+    if (!part) return;
+    if (lane == 0) {
+        s_key[wave] = key;
+        s_T[wave] = kT;
+        s_cnt[wave] = cnt;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    EmoPartial p;
+    p.key = s_key[0];
+    p.makespan = s_T[0];
+    p.count = s_cnt[0];
+    for (int w = 1; w < kWavesPerBlock; ++w) {
+        if (s_key[w] < p.key) {
+            p.key = s_key[w];
+            p.makespan = s_T[w];
+        }
+        p.count += s_cnt[w];
+    }
+    part[blockIdx.x] = p;
 }
 
 int64_t grid_for(int64_t B) { return (B + kBlock - 1) / kBlock; }
@@ -518,6 +587,8 @@ int table_mode(const DevGraph &g, const DevProgram &prog, size_t other_lds, size
 }  // namespace
 
 int64_t forward_blocks(int64_t B) { return grid_for(B); }
+
+int64_t select_results_blocks(int64_t B) { return (B + kSelGroup - 1) / kSelGroup; }
 
 size_t forward_scratch_bytes(const DevProgram &prog, int64_t B) {
     return static_cast<size_t>(prog.n_cold) * static_cast<size_t>(grid_for(B) * kBlock) * sizeof(float);
@@ -595,8 +666,9 @@ hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selectio
 
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
                                  uint32_t *mask, void *part, hipStream_t s) {
-    hipLaunchKernelGGL(select_results_kernel, dim3(static_cast<unsigned>(grid_for(B))), dim3(kBlock), 0, s,
-                       T, E, B, target, mask, static_cast<EmoPartial *>(part));
+    const bool vec = (reinterpret_cast<uintptr_t>(T) | reinterpret_cast<uintptr_t>(E)) % 16 == 0;
+    hipLaunchKernelGGL(select_results_kernel, dim3(static_cast<unsigned>(select_results_blocks(B))), dim3(kBlock),
+                       0, s, T, E, B, target, mask, static_cast<EmoPartial *>(part), vec);
     return hipGetLastError();
 }
 
