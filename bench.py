@@ -166,6 +166,103 @@ def run_dp(args, emo, synth, np, torch):
     print(json.dumps(out), flush=True)
 
 
+def run_intervals(args, emo, synth, np, torch):
+    """Time-interval policies (emo_eval_intervals) on workload k's graph: the workload's batch
+    size, K intervals over [0, 1.05 T0) (change points on the time grid), idle power rising with
+    the level's frequency, uniform random levels; one call per step with mask and selection at
+    1.02 T0.  `value` = candidates per second."""
+    k = args.workload
+    spec = synth.CONFIGS[k]
+    g = synth.config_graph(k)
+    F, K, B = g.num_levels, args.intervals, spec.num_candidates
+    gh = emo.EmoGraph(g, device=0)
+    dev = torch.device("cuda", 0)
+    top = torch.full((1, g.num_packs), F - 1, dtype=torch.uint8, device=dev)
+    T0 = float(gh.eval_policies(top)[0].item())
+    pts = [float(synth.quantize(T0 * 1.05 * (i + 1) / K)) for i in range(K - 1)]
+    idle = [float(x) for x in np.round(g.static_power * (0.5 + 0.5 * synth.level_ratios(F)) * 64) / 64]
+    rows = synth.random_policies_parallel(spec.policy_seed, K, F, B, "uniform", workers=8)
+    copies = max(1, args.copies if B * K < (1 << 30) else 1)
+    lv = [torch.from_numpy(rows).to(dev)]
+    for _ in range(copies - 1):
+        lv.append(lv[0].clone())
+    T = torch.empty(B, dtype=torch.float32, device=dev)
+    E = torch.empty(B, dtype=torch.float32, device=dev)
+    m = torch.empty((B + 31) // 32, dtype=torch.int32, device=dev)
+    r = torch.empty(3, dtype=torch.int64, device=dev)
+    tgt = float(np.float32(1.02 * T0))
+    stream = torch.cuda.current_stream()
+
+    def call(i):
+        gh.eval_intervals(lv[i % copies], pts, idle, makespan=T, energy=E, latency_target=tgt, mask=m,
+                          result=r)
+
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+    every = max(1, args.time_every)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(0, args.steps, every)]
+    for a, b in ev:
+        a.record(stream)
+        b.record(stream)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        if i % every == 0:
+            gh.set_timing_events(ev[i // every][0], ev[i // every][1])
+        elif i % every == 1:
+            gh.set_timing_events(None, None)
+        call(i)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    gh.set_timing_events(None, None)
+    ms_step = start.elapsed_time(end) / args.steps
+    main_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    info = gh.info()
+    algo_bytes = B * (K + 8) + (B + 7) // 8
+    achieved = algo_bytes / (main_ms / 1e3) / 1e9
+    # per candidate: the forward work of the per-pack kernel plus, per pack, the binary search
+    # over the change points (one compare and one select per halving step)
+    steps = int(np.ceil(np.log2(K))) if K > 1 else 0
+    ops_per_cand = info["num_dynamic_edges"] + 2 * g.num_packs + 2 + 2 * steps * g.num_packs + 3 * K
+    valu_tops = B * ops_per_cand / (main_ms / 1e3) / 1e12
+    sel = emo.parse_selection(r)
+    out = {
+        "metric": "time-interval policies evaluated/sec (makespan + energy + selection)",
+        "value": B / (ms_step / 1e3), "unit": "policies/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": spec.name, "candidates": B, "intervals": K, "packs": g.num_packs,
+                   "levels": F, "target_ratio": 1.02, "step": "emo_eval_intervals",
+                   "rotated_input_copies": copies},
+        "roofline": {"bound": "hbm", "kernel": "interval_kernel", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes_per_launch": algo_bytes,
+                     "launch_ms": main_ms, "timed_launches": len(ev),
+                     "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Tops/s",
+                              "frac": valu_tops / VALU_PEAK_TOPS,
+                              "algorithmic_ops_per_candidate": ops_per_cand}},
+        "selected": {"index": sel.index, "energy": sel.energy, "makespan": sel.makespan,
+                     "num_feasible": sel.num_feasible},
+        "wall_s": wall,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import intervals as oiv   # the CPU baseline leg only
+        n = 2048
+        t = time.perf_counter()
+        oiv.eval_intervals(g, pts, rows[:n], idle)
+        dt = time.perf_counter() - t
+        out["cpu_baseline"] = {"value": n / dt, "unit": "policies/s", "cores": 1, "kind": "oracle",
+                               "sample": f"the first {n} candidates of the batch in {dt:.2f} s "
+                                         "(pure-Python fp64 interval oracle, 1 thread)"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -180,6 +277,9 @@ def main():
     ap.add_argument("--dp", action="store_true",
                     help="time the policy search of Alg. 2 (emo_dp_search) on the workload's graph "
                          "instead of the evaluation step")
+    ap.add_argument("--intervals", type=int, default=0, metavar="K",
+                    help="time emo_eval_intervals (time-interval policies with K intervals) on the "
+                         "workload's graph and batch size instead of the evaluation step")
     ap.add_argument("--dp-buckets", type=int, default=64,
                     help="makespan buckets of the search between T0 and 1.05 T0 (default 64)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -209,6 +309,9 @@ def main():
 
     if args.dp:
         run_dp(args, emo, synth, np, torch)
+        return
+    if args.intervals:
+        run_intervals(args, emo, synth, np, torch)
         return
 
     k = args.workload

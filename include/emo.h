@@ -224,8 +224,9 @@ emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t num_c
                              emo_selection *result, void *stream);
 
 /*
- * The whole hot path in one pass over the candidates, as one kernel launch (plus a tiny one
- * that initialises the selection accumulator): makespan and energy (Eq. 1-3), slack of every
+ * The whole hot path in one pass over the candidates, as one kernel launch (plus, with
+ * `result`, a one-workgroup kernel that completes the selection): makespan and energy
+ * (Eq. 1-3), slack of every
  * pack or node when `slack` is given, and the feasibility mask and least-energy feasible
  * candidate under `latency_target` (Eq. 4) when `feasible_mask` or `result` is given.
  * Every output is optional (NULL); their layouts are those of emo_eval_policies, emo_slack and
@@ -243,6 +244,35 @@ emo_status emo_evaluate(emo_graph_t g, const uint8_t *levels, int64_t num_candid
 emo_status emo_select_from_results(const float *makespan, const float *energy,
                                    int64_t num_candidates, float latency_target,
                                    uint32_t *feasible_mask, emo_selection *result, void *stream);
+
+/*
+ * Time-interval frequency policies: the general policy form P = {<T_i, F_i>} of the optimisation
+ * problem (Sec. IV-A) as Alg. 1 evaluates it.  The batch shares K = num_intervals intervals
+ * [T_i, T_{i+1}) with T_0 = 0, T_i = change_points[i - 1] and the last interval open-ended; each
+ * candidate gives one level per interval.  A pack runs at the level of the interval that holds
+ * its start time (the largest finish time among its predecessors, 0 for a source; half-open
+ * intervals, so a start equal to a change point takes the later interval), which makes a pack's
+ * level depend on the schedule.  makespan as in Eq. 1-2; energy = the packs' table energies plus
+ * the idle energy of Alg. 1, read as idle_power[F_i] times the wall time interval i covers
+ * inside [0, makespan) (with idle_power[f] = the graph's static_power for every f, one interval
+ * gives the energy of emo_eval_policies with that level on every pack).  The graph's
+ * static_power is not used here.
+ *   levels:        device uint8 [B][K], row-major (16-byte aligned rows with K % 16 == 0 are
+ *                  read as vectors; any layout works).  A byte >= F anywhere in a row makes
+ *                  that candidate's makespan and energy NaN (never feasible).
+ *   num_intervals: K in [1, 256].
+ *   change_points: host float [K - 1] (NULL when K = 1), finite, > 0, strictly increasing;
+ *                  copied at the call (the kernel receives them as arguments).
+ *   idle_power:    host float [F], finite, >= 0 (power units; times are in microseconds).
+ *   makespan, energy: device float [B] or NULL; feasible_mask, result and latency_target as in
+ *                  emo_evaluate.
+ * Asynchronous on `stream`; invalid arguments are reported synchronously and launch nothing.
+ */
+emo_status emo_eval_intervals(emo_graph_t g, const uint8_t *levels, int64_t num_candidates,
+                              int32_t num_intervals, const float *change_points,
+                              const float *idle_power, float *makespan, float *energy,
+                              float latency_target, uint32_t *feasible_mask,
+                              emo_selection *result, void *stream);
 
 /* Profiling hook: while set, batch calls on `g` record `begin_event` on their stream right
  * before the kernel that evaluates the candidates and `end_event` right after it (before the

@@ -1369,6 +1369,71 @@ emo_status emo_evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *
                     feasible_mask, result, stream);
 }
 
+emo_status emo_eval_intervals(emo_graph_t g, const uint8_t *levels, int64_t B, int32_t num_intervals,
+                              const float *change_points, const float *idle_power, float *makespan,
+                              float *energy, float latency_target, uint32_t *feasible_mask,
+                              emo_selection *result, void *stream) {
+    emo_status s = check_batch(g, B);
+    if (s != EMO_OK) return s;
+    if (num_intervals < 1 || num_intervals > emo::kMaxIntervals)
+        return fail(EMO_ERR_INVALID_ARGUMENT, "num_intervals %d outside [1, %d]", num_intervals,
+                    emo::kMaxIntervals);
+    if (num_intervals > 1 && !change_points) return fail(EMO_ERR_INVALID_ARGUMENT, "change_points is NULL");
+    if (!idle_power) return fail(EMO_ERR_INVALID_ARGUMENT, "idle_power is NULL");
+    emo::IvPolicy pol;
+    pol.K = num_intervals;
+    for (int i = 0; i + 1 < num_intervals; ++i) {
+        const float t = change_points[i];
+        if (!std::isfinite(t) || t <= 0.f || (i > 0 && !(t > change_points[i - 1])))
+            return fail(EMO_ERR_INVALID_ARGUMENT,
+                        "change point %d (%g) is not finite, positive and above the previous one", i, (double)t);
+        pol.pts[i] = t;
+    }
+    for (int f = 0; f < emo::kMaxLevels; ++f) pol.idle[f] = 0.f;
+    for (int f = 0; f < g->F; ++f) {
+        if (!finite_nonneg(idle_power[f]))
+            return fail(EMO_ERR_INVALID_ARGUMENT, "idle_power[%d] is negative or not finite", f);
+        pol.idle[f] = idle_power[f];
+    }
+    if (result && reinterpret_cast<uintptr_t>(result) % 8)
+        return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
+    if ((result || feasible_mask) && std::isnan(latency_target))
+        return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    DeviceGuard guard(g->device);
+    if (B == 0) return result ? after_launch(emo::launch_empty_result(result, st), "empty selection") : ok();
+    if (!makespan && !energy && !feasible_mask && !result) return ok();
+    if (!levels) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
+    const int64_t nblocks = emo::forward_blocks(B);
+    size_t part_bytes = result ? static_cast<size_t>(nblocks) * emo::kPartialBytes : 0;
+    part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
+    const size_t work_bytes = emo::forward_scratch_bytes(g->dg.eval, B);
+    std::lock_guard<std::mutex> lock(g->arena.mu);
+    void *scratch = nullptr;
+    if (part_bytes + work_bytes > 0) {
+        hipError_t ea = arena_acquire(g->arena, part_bytes + work_bytes, st, &scratch);
+        if (ea != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(EMO_ERR_OUT_OF_MEMORY, "scratch of %zu bytes: %s", part_bytes + work_bytes,
+                        hipGetErrorString(ea));
+        }
+    }
+    void *part = result ? scratch : nullptr;
+    void *work = scratch ? static_cast<char *>(scratch) + part_bytes : nullptr;
+    g->info.last_kernels = 0;
+    hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
+    if (e == hipSuccess)
+        e = emo::launch_intervals(g->dg, pol, levels, B, makespan, energy, latency_target, feasible_mask,
+                                  part, work, st);
+    if (e == hipSuccess && g->ev_end) e = hipEventRecord(g->ev_end, st);
+    if (result && e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
+    if (scratch) {
+        hipError_t er = arena_release(g->arena, st);
+        if (e == hipSuccess) e = er;
+    }
+    return after_launch(e, "emo_eval_intervals");
+}
+
 emo_status emo_select_from_results(const float *makespan, const float *energy, int64_t B,
                                    float latency_target, uint32_t *feasible_mask,
                                    emo_selection *result, void *stream) {

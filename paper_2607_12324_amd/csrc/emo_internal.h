@@ -87,6 +87,22 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
                         float target, uint32_t *mask, void *part, void *scratch, hipStream_t s);
 int64_t forward_blocks(int64_t B);
+
+// A time-interval policy batch (the policy form of Sec. IV-A; Alg. 1): K intervals [T_i,
+// T_{i+1}) with T_0 = 0 and the last one open-ended; each candidate's row holds K levels.  Passed
+// to the kernel by value (2 KB of kernel arguments).
+constexpr int kMaxIntervals = 256;
+constexpr int kMaxLevels = 256;
+struct IvPolicy {
+    int32_t K = 1;
+    float pts[kMaxIntervals - 1];   // change points T_1 < ... < T_{K-1}
+    float idle[kMaxLevels];         // idle power per level
+};
+// Makespan, energy and the selection stage 1 of B interval policies (forward_blocks(B) partials);
+// scratch as for launch_forward (forward_scratch_bytes(g.eval, B)).
+hipError_t launch_intervals(const DevGraph &g, const IvPolicy &pol, const uint8_t *levels, int64_t B,
+                            float *T, float *E, float target, uint32_t *mask, void *part, void *scratch,
+                            hipStream_t s);
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s);
 hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selection *res,
                                   hipStream_t s);

@@ -392,6 +392,105 @@ slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict_
     if (mask || part) emo_select_block(blockIdx.x, x.active, f.T, f.E, x.cand, B, target, mask, part);
 }
 
+// ---------------------------------------------------------------- time-interval policies
+
+// Forward pass for a time-interval policy (the policy form of Sec. IV-A; Alg. 1): the row holds
+// one level per interval [T_i, T_{i+1}) of the batch's change points (T_0 = 0, the last interval
+// open-ended), a pack runs at the level of the interval that holds its start time, and the
+// energy adds each interval's idle power times the wall time it covers inside [0, makespan).
+// `pts` (K - 1 change points, increasing) and `idle` (F values) are in LDS.
+template <int MODE>
+__device__ __forceinline__ Fwd run_forward_iv(const DevProgram &pr, Tab<MODE> &tab, int F, const Row &row,
+                                              int K, const float *pts, const float *idle, f32x32 &hot,
+                                              const Scratch &sc) {
+    u32x32 lw;
+    int lgroup = -1;
+    bool bad = false;   // any level byte >= F in the row (the idle term reads every interval's)
+    for (int i = 0; i < K; ++i) bad |= level_at(row, lw, lgroup, i) >= static_cast<unsigned>(F);
+    float T = pr.t_const;
+    double eacc = 0.0;
+    float eblk = 0.f;
+    int nblk = 0;
+    const int n = pr.n_ops;
+    for (int i = 0; i < n; ++i) {
+        const FwdStep st = ld_prog(pr.fwd, i);
+        const uint32_t flags = uni(st.flags);
+        const int32_t pack = uni(st.pack);
+        const int32_t nin = uni(st.in_count);
+        const int32_t ib = uni(st.in_begin);
+        float est = __uint_as_float(uni(st.cst));
+        for (int j = 0; j < nin; ++j)
+            est = fmaxf(est, slot_get(hot, sc.cold, sc.bpad, sc.col, uni(ld_prog(pr.ins, ib + j))));
+        float dur;
+        if (pack >= 0) {
+            int lo = 0, hi = K - 1;   // number of change points <= est
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (pts[mid] <= est) lo = mid + 1;
+                else hi = mid;
+            }
+            unsigned l = level_at(row, lw, lgroup, lo);
+            l = l < static_cast<unsigned>(F) ? l : 0u;
+            const float2 te = tab.get(pack, static_cast<int>(l), 1);
+            dur = te.x;
+            eblk += te.y;
+            if (++nblk == kEnergyBlock) {
+                eacc += static_cast<double>(eblk);
+                eblk = 0.f;
+                nblk = 0;
+            }
+        } else {
+            dur = __uint_as_float(uni(st.dur));
+        }
+        const float eft = est + dur;
+        if (flags & kStepOut) slot_set(hot, sc.cold, sc.bpad, sc.col, uni(st.out), eft);
+        if (flags & kStepSink) T = fmaxf(T, eft);
+    }
+    eacc += static_cast<double>(eblk);
+    for (int i = 0; i < K; ++i) {
+        const double lo = i > 0 ? static_cast<double>(pts[i - 1]) : 0.0;
+        const double hi = i < K - 1 ? fmin(static_cast<double>(pts[i]), static_cast<double>(T))
+                                    : static_cast<double>(T);
+        unsigned l = level_at(row, lw, lgroup, i);
+        l = l < static_cast<unsigned>(F) ? l : 0u;
+        if (hi > lo) eacc += static_cast<double>(idle[l]) * (hi - lo);
+    }
+    Fwd f;
+    f.E = static_cast<float>(eacc);
+    f.T = T;
+    f.bad = bad;
+    if (bad) {
+        f.T = __builtin_nanf("");
+        f.E = __builtin_nanf("");
+    }
+    return f;
+}
+
+template <int MODE>
+__global__ void __launch_bounds__(kBlock)
+interval_kernel(DevGraph g, IvPolicy pol, const uint8_t *__restrict__ levels, int64_t B,
+                float *__restrict__ T_out, float *__restrict__ E_out, float target,
+                uint32_t *__restrict__ mask, EmoPartial *part, float *cold, int64_t bpad, bool vec,
+                int wlog) {
+    extern __shared__ float4 smem4[];
+    __shared__ float s_pts[kMaxIntervals];
+    __shared__ float s_idle[kMaxLevels];
+    for (int i = threadIdx.x; i < pol.K - 1; i += kBlock) s_pts[i] = pol.pts[i];
+    for (int i = threadIdx.x; i < g.F; i += kBlock) s_idle[i] = pol.idle[i];
+    __syncthreads();
+    Tab<MODE> tab = make_tab<MODE>(g, smem4, wlog);
+    const LaneCtx x = lane_ctx(B);
+    const Row row{levels + x.cand * pol.K, pol.K, vec};
+    f32x32 hot;
+    Scratch sc{cold, nullptr, nullptr, bpad, x.gid};
+    const Fwd f = run_forward_iv<MODE>(g.eval, tab, g.F, row, pol.K, s_pts, s_idle, hot, sc);
+    if (x.active) {
+        if (T_out) T_out[x.cand] = f.T;
+        if (E_out) E_out[x.cand] = f.E;
+    }
+    if (mask || part) emo_select_block(blockIdx.x, x.active, f.T, f.E, x.cand, B, target, mask, part);
+}
+
 // ---------------------------------------------------------------- selection (Eq. 4)
 
 static_assert(sizeof(EmoSel) == sizeof(emo_selection), "result layout");
@@ -649,6 +748,26 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
     else if (staged) hipLaunchKernelGGL((slack_kernel<kTabGlobal, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
     else hipLaunchKernelGGL((slack_kernel<kTabGlobal, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
 #undef EMO_SLACK_ARGS
+    return hipGetLastError();
+}
+
+hipError_t launch_intervals(const DevGraph &g, const IvPolicy &pol, const uint8_t *levels, int64_t B,
+                            float *T, float *E, float target, uint32_t *mask, void *part, void *scratch,
+                            hipStream_t s) {
+    const int64_t grid = grid_for(B);
+    const int64_t bpad = grid * kBlock;
+    float *cold = g.eval.n_cold > 0 ? static_cast<float *>(scratch) : nullptr;
+    size_t dyn = 0;
+    const int mode = table_mode(g, g.eval, 0, &dyn);
+    const bool vec = pol.K % 16 == 0 && reinterpret_cast<uintptr_t>(levels) % 16 == 0;
+    const int wlog = window_log(g);
+    EmoPartial *pp = static_cast<EmoPartial *>(part);
+    const dim3 gd(static_cast<unsigned>(grid)), bd(kBlock);
+#define EMO_IV_ARGS g, pol, levels, B, T, E, target, mask, pp, cold, bpad, vec, wlog
+    if (mode == kTabLds) hipLaunchKernelGGL(interval_kernel<kTabLds>, gd, bd, dyn, s, EMO_IV_ARGS);
+    else if (mode == kTabWindow) hipLaunchKernelGGL(interval_kernel<kTabWindow>, gd, bd, dyn, s, EMO_IV_ARGS);
+    else hipLaunchKernelGGL(interval_kernel<kTabGlobal>, gd, bd, dyn, s, EMO_IV_ARGS);
+#undef EMO_IV_ARGS
     return hipGetLastError();
 }
 

@@ -23,7 +23,7 @@ STATUS_NAMES = {0: "EMO_OK", 1: "EMO_ERR_INVALID_ARGUMENT", 2: "EMO_ERR_CYCLE",
 ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_kernel_mode", "emo_graph_topo_order",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
-                "emo_select_from_results", "emo_dp_search",
+                "emo_select_from_results", "emo_dp_search", "emo_eval_intervals",
                 "emo_graph_set_timing_events", "emo_graph_specialized_source",
                 "emo_graph_segmented_source", "emo_graph_cut_source", "emo_status_string",
                 "emo_last_error")
@@ -72,6 +72,7 @@ def _load_library():
         "emo_evaluate": [P, P, i64, P, P, P, i32, f32, P, P, P],
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
         "emo_dp_search": [P, f32, f32, P, i32, P, P, P],
+        "emo_eval_intervals": [P, P, i64, i32, P, P, P, P, f32, P, P, P],
         "emo_graph_specialized_source": [P, P, P],
         "emo_graph_segmented_source": [P, P, P],
         "emo_graph_cut_source": [P, P, P],
@@ -266,6 +267,32 @@ class EmoGraph:
                                      _dptr(result, torch.int64, 3, "result"), _stream(stream)))
         return result, mask
 
+
+    def eval_intervals(self, levels, change_points, idle_power, makespan=None, energy=None,
+                       latency_target: float = 0.0, mask=None, result=None, stream=None):
+        """Time-interval policies (emo_eval_intervals): levels [B, K] uint8 with K =
+        len(change_points) + 1; idle_power has one value per level.  Returns (makespan, energy,
+        mask, result); makespan and energy are allocated when not given."""
+        import torch
+        pts = _np(change_points, np.float32).reshape(-1)
+        idle = _np(idle_power, np.float32).reshape(-1)
+        K = int(pts.size) + 1
+        if levels.dim() != 2 or levels.shape[1] != K:
+            raise ValueError(f"levels must be [B, {K}] for {K - 1} change points")
+        if idle.size != self.num_levels:
+            raise ValueError(f"idle_power must hold {self.num_levels} values")
+        B = int(levels.shape[0])
+        if makespan is None:
+            makespan = torch.empty(B, dtype=torch.float32, device=levels.device)
+        if energy is None:
+            energy = torch.empty(B, dtype=torch.float32, device=levels.device)
+        _check(lib.emo_eval_intervals(self._h, _dptr(levels, torch.uint8, name="levels"), B, K,
+                                      _nptr(pts) if pts.size else None, _nptr(idle),
+                                      _dptr(makespan, torch.float32, B, "makespan"),
+                                      _dptr(energy, torch.float32, B, "energy"), float(latency_target),
+                                      _dptr(mask, torch.int32, (B + 31) // 32, "mask"),
+                                      _dptr(result, torch.int64, 3, "result"), _stream(stream)))
+        return makespan, energy, mask, result
 
     def dp_search(self, latency_target: float, quantum: float, pack_order=None,
                   max_states: int = 4096, best_levels=None, result=None, stream=None):
