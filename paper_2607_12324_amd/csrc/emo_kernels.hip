@@ -398,15 +398,38 @@ slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict_
 // one level per interval [T_i, T_{i+1}) of the batch's change points (T_0 = 0, the last interval
 // open-ended), a pack runs at the level of the interval that holds its start time, and the
 // energy adds each interval's idle power times the wall time it covers inside [0, makespan).
-// `pts` (K - 1 change points, increasing) and `idle` (F values) are in LDS.
-template <int MODE>
+// `pts` (K - 1 change points, increasing) and `idle` (F values) are in LDS.  With NREG > 0
+// (K - 1 <= NREG) the change points are also held in registers `rp` (uniform values, padded with
+// +infinity) and a pack's interval is the count of points <= its start, an unrolled sequence of
+// compares with no memory access on the dependency chain; otherwise a binary search over LDS.
+constexpr int kIvRegPoints = 15;
+
+template <int MODE, int NREG>
 __device__ __forceinline__ Fwd run_forward_iv(const DevProgram &pr, Tab<MODE> &tab, int F, const Row &row,
-                                              int K, const float *pts, const float *idle, f32x32 &hot,
-                                              const Scratch &sc) {
+                                              int K, const float *pts, const float *rp, const float *idle,
+                                              f32x32 &hot, const Scratch &sc) {
     u32x32 lw;
     int lgroup = -1;
     bool bad = false;   // any level byte >= F in the row (the idle term reads every interval's)
     for (int i = 0; i < K; ++i) bad |= level_at(row, lw, lgroup, i) >= static_cast<unsigned>(F);
+    // the level of a lane-dependent interval: with NREG > 0 (K <= 16) from the row's four words
+    // by a two-level select; otherwise a byte load from the row (indexing the register bank with
+    // a lane-dependent index would cost a select per word of the bank)
+    unsigned q0 = 0u, q1 = 0u, q2 = 0u, q3 = 0u;
+    if (NREG > 0) {
+        if (row.vec) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(row.row);
+            q0 = v.x; q1 = v.y; q2 = v.z; q3 = v.w;
+        } else {
+            for (int i = 0; i < K; ++i) {
+                const unsigned b = static_cast<unsigned>(row.row[i]) << ((i & 3) * 8);
+                if (i < 4) q0 |= b;
+                else if (i < 8) q1 |= b;
+                else if (i < 12) q2 |= b;
+                else q3 |= b;
+            }
+        }
+    }
     float T = pr.t_const;
     double eacc = 0.0;
     float eblk = 0.f;
@@ -424,12 +447,23 @@ __device__ __forceinline__ Fwd run_forward_iv(const DevProgram &pr, Tab<MODE> &t
         float dur;
         if (pack >= 0) {
             int lo = 0, hi = K - 1;   // number of change points <= est
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (pts[mid] <= est) lo = mid + 1;
-                else hi = mid;
+            if (NREG > 0) {
+#pragma unroll
+                for (int j = 0; j < NREG; ++j) lo += rp[j] <= est ? 1 : 0;
+            } else {
+                while (lo < hi) {
+                    const int mid = (lo + hi) >> 1;
+                    if (pts[mid] <= est) lo = mid + 1;
+                    else hi = mid;
+                }
             }
-            unsigned l = level_at(row, lw, lgroup, lo);
+            unsigned l;
+            if (NREG > 0) {
+                const unsigned wd = lo < 8 ? (lo < 4 ? q0 : q1) : (lo < 12 ? q2 : q3);
+                l = (wd >> ((lo & 3) * 8)) & 0xffu;
+            } else {
+                l = row.row[lo];
+            }
             l = l < static_cast<unsigned>(F) ? l : 0u;
             const float2 te = tab.get(pack, static_cast<int>(l), 1);
             dur = te.x;
@@ -466,7 +500,7 @@ __device__ __forceinline__ Fwd run_forward_iv(const DevProgram &pr, Tab<MODE> &t
     return f;
 }
 
-template <int MODE>
+template <int MODE, int NREG>
 __global__ void __launch_bounds__(kBlock)
 interval_kernel(DevGraph g, IvPolicy pol, const uint8_t *__restrict__ levels, int64_t B,
                 float *__restrict__ T_out, float *__restrict__ E_out, float target,
@@ -483,7 +517,10 @@ interval_kernel(DevGraph g, IvPolicy pol, const uint8_t *__restrict__ levels, in
     const Row row{levels + x.cand * pol.K, pol.K, vec};
     f32x32 hot;
     Scratch sc{cold, nullptr, nullptr, bpad, x.gid};
-    const Fwd f = run_forward_iv<MODE>(g.eval, tab, g.F, row, pol.K, s_pts, s_idle, hot, sc);
+    float rp[NREG > 0 ? NREG : 1];
+#pragma unroll
+    for (int j = 0; j < NREG; ++j) rp[j] = j < pol.K - 1 ? pol.pts[j] : __builtin_inff();
+    const Fwd f = run_forward_iv<MODE, NREG>(g.eval, tab, g.F, row, pol.K, s_pts, rp, s_idle, hot, sc);
     if (x.active) {
         if (T_out) T_out[x.cand] = f.T;
         if (E_out) E_out[x.cand] = f.E;
@@ -764,9 +801,13 @@ hipError_t launch_intervals(const DevGraph &g, const IvPolicy &pol, const uint8_
     EmoPartial *pp = static_cast<EmoPartial *>(part);
     const dim3 gd(static_cast<unsigned>(grid)), bd(kBlock);
 #define EMO_IV_ARGS g, pol, levels, B, T, E, target, mask, pp, cold, bpad, vec, wlog
-    if (mode == kTabLds) hipLaunchKernelGGL(interval_kernel<kTabLds>, gd, bd, dyn, s, EMO_IV_ARGS);
-    else if (mode == kTabWindow) hipLaunchKernelGGL(interval_kernel<kTabWindow>, gd, bd, dyn, s, EMO_IV_ARGS);
-    else hipLaunchKernelGGL(interval_kernel<kTabGlobal>, gd, bd, dyn, s, EMO_IV_ARGS);
+    const bool reg = pol.K - 1 <= kIvRegPoints;
+    if (mode == kTabLds && reg) hipLaunchKernelGGL((interval_kernel<kTabLds, kIvRegPoints>), gd, bd, dyn, s, EMO_IV_ARGS);
+    else if (mode == kTabLds) hipLaunchKernelGGL((interval_kernel<kTabLds, 0>), gd, bd, dyn, s, EMO_IV_ARGS);
+    else if (mode == kTabWindow && reg) hipLaunchKernelGGL((interval_kernel<kTabWindow, kIvRegPoints>), gd, bd, dyn, s, EMO_IV_ARGS);
+    else if (mode == kTabWindow) hipLaunchKernelGGL((interval_kernel<kTabWindow, 0>), gd, bd, dyn, s, EMO_IV_ARGS);
+    else if (reg) hipLaunchKernelGGL((interval_kernel<kTabGlobal, kIvRegPoints>), gd, bd, dyn, s, EMO_IV_ARGS);
+    else hipLaunchKernelGGL((interval_kernel<kTabGlobal, 0>), gd, bd, dyn, s, EMO_IV_ARGS);
 #undef EMO_IV_ARGS
     return hipGetLastError();
 }
