@@ -308,6 +308,66 @@ emo_status emo_graph_set_timing_events(emo_graph_t g, void *begin_event, void *e
 emo_status emo_dp_search(emo_graph_t g, float latency_target, float quantum, const int32_t *pack_order,
                          int32_t max_states, uint8_t *best_levels, emo_selection *result, void *stream);
 
+/*
+ * Dependency-aware greedy kernel packing (Sec. IV-D: the critical predecessor of Eq. 5, the two
+ * dependency-safety rules and the granularity rule), a host-only load-time pass that needs no
+ * GPU.  The input is a graph in emo_load_graph's form whose packs are single GPU compute
+ * kernels, plus the stream of every node.  Completion times are the all-maximum schedule
+ * (level F-1 everywhere, in double precision); the critical predecessor of a node is its
+ * predecessor of latest completion, the first in the canonical topological order among equals,
+ * and the critical successors of u are the nodes whose critical predecessor is u.  Kernels are
+ * visited in the canonical topological order; each stream has one open pack.  Kernel v joins
+ * the open pack of its stream when that pack's last kernel u is a direct predecessor of v and
+ *   rule 1: v and its critical predecessor are on the same stream,
+ *   rule 2: every critical successor of u is on u's stream,
+ *   rule 3: the pack's duration at level F-1 plus v's (summed in double) < max_pack_duration;
+ * otherwise v opens a new pack.  Groups are numbered in the order of their first kernels.
+ *   edges, node_pack, node_duration, tables: host arrays as in emo_load_graph (pack_energy is
+ *                  not needed here); every pack must sit on exactly one node.
+ *   node_stream:   host int32 [V]: the GPU stream of each node, >= 0 for every kernel (pack)
+ *                  node; -1 for host or other nodes that are on no stream.
+ *   max_pack_duration: the granularity bound (the paper uses 5 ms), > 0; +inf disables it.
+ *   pack_group:    host int32 [P] out: the group (new pack) of each input pack.
+ *   num_groups:    host out: the number of groups.
+ * Synchronous.  Invalid arguments give EMO_ERR_INVALID_ARGUMENT, a cycle EMO_ERR_CYCLE, and
+ * leave the outputs unspecified.
+ */
+emo_status emo_pack_kernels(int32_t num_nodes, int32_t num_edges, const int32_t *edge_src,
+                            const int32_t *edge_dst, const int32_t *node_pack,
+                            const float *node_duration, const int32_t *node_stream,
+                            int32_t num_packs, int32_t num_levels, const float *pack_time,
+                            float max_pack_duration, int32_t *pack_group, int32_t *num_groups);
+
+/*
+ * The packed graph of a grouping of the packs (Sec. IV-D: a pack keeps the incoming
+ * dependencies of its first kernel and the outgoing dependencies of its last; the ones in
+ * between are dropped), in emo_load_graph's form, host-only.  A group's members are ordered by
+ * the canonical topological order.  Packed nodes are the non-kernel nodes and one node per
+ * group, numbered by increasing id of the input node standing for them (for a group, its first
+ * kernel).  An input edge a -> b survives as packed_node[a] -> packed_node[b] when a is a
+ * non-kernel node or its group's last kernel, b is a non-kernel node or its group's first
+ * kernel, and the two packed nodes differ; duplicates are merged, edges come out sorted by
+ * (src, dst).  A group's latency and energy at level f are the sums of its members' entries,
+ * accumulated in double in member order and rounded to fp32.
+ *   pack_group, num_groups: as produced by emo_pack_kernels (any grouping in [0, num_groups)
+ *                  with no empty group is accepted).
+ *   packed_node:   host int32 [V] out: the packed node standing for each input node.
+ *   packed_node_pack, packed_node_duration: host [V] capacity, out: the packed graph's
+ *                  node_pack (the group id, or -1) and node_duration (0 for groups).
+ *   packed_src, packed_dst: host int32 [E] capacity, out: the packed graph's edges.
+ *   group_time, group_energy: host float [num_groups * F] out, row-major.
+ *   counts:        host int32 [2] out: packed nodes, packed edges.
+ * Synchronous; errors as in emo_pack_kernels.
+ */
+emo_status emo_contract_packs(int32_t num_nodes, int32_t num_edges, const int32_t *edge_src,
+                              const int32_t *edge_dst, const int32_t *node_pack,
+                              const float *node_duration, int32_t num_packs, int32_t num_levels,
+                              const float *pack_time, const float *pack_energy,
+                              const int32_t *pack_group, int32_t num_groups, int32_t *packed_node,
+                              int32_t *packed_node_pack, float *packed_node_duration,
+                              int32_t *packed_src, int32_t *packed_dst, float *group_time,
+                              float *group_energy, int32_t *counts);
+
 /* Diagnostics: the HIP source of the kernels specialised to `g` (the text EMO_KERNELS_AUTO
  * compiles on first use), NUL-terminated.  With buf == NULL, *len receives the size needed
  * including the NUL; otherwise at most *len bytes are written.  Works on host-only graphs.

@@ -46,6 +46,21 @@ emo_status ok() {
     return EMO_OK;
 }
 
+}  // namespace
+
+namespace emo {
+emo_status report(emo_status s, const char *message) {
+    if (s == EMO_OK) {
+        g_last_error.clear();
+    } else {
+        g_last_error = message;
+    }
+    return s;
+}
+}  // namespace emo
+
+namespace {
+
 emo_status device_fail(hipError_t e, const char *where) {
     return fail(EMO_ERR_DEVICE, "%s: %s", where, hipGetErrorString(e));
 }

@@ -12,6 +12,9 @@
 
 namespace emo {
 
+// Records `message` as the calling thread's last error (clears it for EMO_OK); returns `s`.
+emo_status report(emo_status s, const char *message);
+
 constexpr int kTablePad = 256;   // extra zeroed table entries: any level byte stays in bounds
 
 // Slot references of the interpreting kernels.  A finish time (forward) or latest start time

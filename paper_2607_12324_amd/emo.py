@@ -24,7 +24,8 @@ ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_kernel_mode", "emo_graph_topo_order",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
                 "emo_select_from_results", "emo_dp_search", "emo_eval_intervals",
-                "emo_graph_set_timing_events", "emo_graph_specialized_source",
+                "emo_graph_set_timing_events", "emo_pack_kernels", "emo_contract_packs",
+                "emo_graph_specialized_source",
                 "emo_graph_segmented_source", "emo_graph_cut_source", "emo_status_string",
                 "emo_last_error")
 
@@ -77,6 +78,9 @@ def _load_library():
         "emo_graph_segmented_source": [P, P, P],
         "emo_graph_cut_source": [P, P, P],
         "emo_graph_set_timing_events": [P, P, P],
+        "emo_pack_kernels": [i32, i32, P, P, P, P, P, i32, i32, P, f32, P, P],
+        "emo_contract_packs": [i32, i32, P, P, P, P, i32, i32, P, P, P, i32, P, P, P, P, P, P,
+                               P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -335,3 +339,74 @@ def unpack_mask(mask, B: int) -> np.ndarray:
     words = mask.detach().cpu().numpy().view(np.uint32)[: (B + 31) // 32]
     bits = np.unpackbits(words.view(np.uint8), bitorder="little")
     return bits[:B].astype(bool)
+
+
+@dataclass
+class PackedGraph:
+    """A packed execution graph in the field layout of ``Graph`` (the loader's form)."""
+    name: str
+    num_nodes: int
+    edge_src: np.ndarray
+    edge_dst: np.ndarray
+    node_pack: np.ndarray
+    node_duration: np.ndarray
+    num_packs: int
+    num_levels: int
+    pack_time: np.ndarray
+    pack_energy: np.ndarray
+    static_power: float
+    packed_node: np.ndarray     # [V of the input] packed node standing for each input node
+
+    @property
+    def num_edges(self) -> int:
+        return int(self.edge_src.shape[0])
+
+
+def _graph_arrays(graph):
+    return (_np(graph.edge_src, np.int32), _np(graph.edge_dst, np.int32),
+            _np(graph.node_pack, np.int32), _np(graph.node_duration, np.float32),
+            _np(graph.pack_time, np.float32).reshape(-1),
+            _np(graph.pack_energy, np.float32).reshape(-1))
+
+
+def pack_kernels(graph, node_stream, max_pack_duration: float):
+    """Greedy dependency-aware packing (host pass): (group of each input pack, group count)."""
+    src, dst, pk, dur, pt, _ = _graph_arrays(graph)
+    stream = _np(node_stream, np.int32)
+    if stream.shape[0] != int(graph.num_nodes):
+        raise ValueError("node_stream needs one entry per node")
+    group = np.empty(int(graph.num_packs), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check(lib.emo_pack_kernels(int(graph.num_nodes), int(src.shape[0]), _nptr(src), _nptr(dst),
+                                _nptr(pk), _nptr(dur), _nptr(stream), int(graph.num_packs),
+                                int(graph.num_levels), _nptr(pt), float(max_pack_duration),
+                                _nptr(group), ctypes.byref(n)))
+    return group, int(n.value)
+
+
+def contract_packs(graph, group, num_groups: int) -> PackedGraph:
+    """The packed graph of a grouping of the input packs (host pass)."""
+    src, dst, pk, dur, pt, pe = _graph_arrays(graph)
+    V, E, F = int(graph.num_nodes), int(src.shape[0]), int(graph.num_levels)
+    group = _np(group, np.int32)
+    if group.shape[0] != int(graph.num_packs):
+        raise ValueError("group needs one entry per pack")
+    packed_node = np.empty(V, dtype=np.int32)
+    node_pack = np.empty(V, dtype=np.int32)
+    node_dur = np.empty(V, dtype=np.float32)
+    psrc = np.empty(E, dtype=np.int32)
+    pdst = np.empty(E, dtype=np.int32)
+    gt = np.empty((int(num_groups), F), dtype=np.float32)
+    ge = np.empty((int(num_groups), F), dtype=np.float32)
+    counts = np.zeros(2, dtype=np.int32)
+    _check(lib.emo_contract_packs(V, E, _nptr(src), _nptr(dst), _nptr(pk), _nptr(dur),
+                                  int(graph.num_packs), F, _nptr(pt), _nptr(pe), _nptr(group),
+                                  int(num_groups), _nptr(packed_node), _nptr(node_pack),
+                                  _nptr(node_dur), _nptr(psrc), _nptr(pdst), _nptr(gt), _nptr(ge),
+                                  _nptr(counts)))
+    n, m = int(counts[0]), int(counts[1])
+    return PackedGraph(name=f"{getattr(graph, 'name', 'graph')}-packed", num_nodes=n,
+                       edge_src=psrc[:m].copy(), edge_dst=pdst[:m].copy(),
+                       node_pack=node_pack[:n].copy(), node_duration=node_dur[:n].copy(),
+                       num_packs=int(num_groups), num_levels=F, pack_time=gt, pack_energy=ge,
+                       static_power=float(graph.static_power), packed_node=packed_node)
