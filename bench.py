@@ -166,6 +166,80 @@ def run_dp(args, emo, synth, np, torch):
     print(json.dumps(out), flush=True)
 
 
+def run_pack(args, emo, synth, np, torch):
+    """Dependency-aware greedy packing (emo_pack_kernels + emo_contract_packs, host passes) of
+    workload k's graph with every pack taken as one kernel, bound 5 ms.  `value` = packings per
+    second; beside it the packed graph's evaluation rate (emo_evaluate on the workload's number
+    of candidates) next to the per-kernel graph's, and the packing oracle on the host."""
+    k = args.workload
+    spec = synth.CONFIGS[k]
+    g = synth.config_graph(k)
+    bound = 5000.0
+    times = []
+    for i in range(args.warmup + args.steps):
+        t = time.perf_counter()
+        grp, n = emo.pack_kernels(g, g.node_stream, bound)
+        pg = emo.contract_packs(g, grp, n)
+        if i >= args.warmup:
+            times.append(time.perf_counter() - t)
+    ms = 1e3 * float(np.median(times))
+    F, B = g.num_levels, spec.num_candidates
+
+    def eval_rate(graph, rows):
+        gh = emo.EmoGraph(graph, device=0)
+        lv = torch.from_numpy(rows).cuda()
+        T = torch.empty(B, dtype=torch.float32, device="cuda")
+        E = torch.empty_like(T)
+        for _ in range(3):
+            gh.eval_policies(lv, T, E)
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        reps = 5
+        for _ in range(reps):
+            gh.eval_policies(lv, T, E)
+        b.record()
+        torch.cuda.synchronize()
+        t0 = float(T[0].item())
+        gh.close()
+        return B / (a.elapsed_time(b) / reps / 1e3), t0
+
+    rng = np.random.default_rng(spec.policy_seed)
+    rows = rng.integers(0, F, (B, n)).astype(np.uint8)
+    rows[0] = F - 1
+    kernel_rows = np.ascontiguousarray(rows[:, grp])
+    packed_rate, T0p = eval_rate(pg, rows)
+    unpacked_rate, T0u = eval_rate(g, kernel_rows)
+    out = {
+        "metric": "dependency-aware greedy packing (Sec. IV-D), host pass: packings/sec",
+        "value": 1e3 / ms, "unit": "packings/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": spec.name, "kernels": g.num_packs, "nodes": g.num_nodes,
+                   "edges": g.num_edges, "max_pack_duration_us": bound,
+                   "step": "emo_pack_kernels + emo_contract_packs"},
+        "packed": {"packs": n, "nodes": pg.num_nodes, "edges": pg.num_edges,
+                   "all_max_makespan_packed": T0p, "all_max_makespan_per_kernel": T0u,
+                   "eval_policies_per_s_packed": packed_rate,
+                   "eval_policies_per_s_per_kernel": unpacked_rate, "candidates": B},
+        "roofline": None,
+        "roofline_note": "host pass, O(V + E) once per graph; no device kernel",
+    }
+    if not args.no_cpu_baseline:
+        from oracle import packing as opk   # the CPU baseline leg only
+        t = time.perf_counter()
+        og, on = opk.pack_kernels(g, g.node_stream, bound)
+        opk.contract(g, og, on)
+        dt = time.perf_counter() - t
+        out["cpu_baseline"] = {"value": 1.0 / dt, "unit": "packings/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": "one whole packing and contraction of the same graph "
+                                         "(Python over the fp64 C schedule, 1 thread)",
+                               "same_result": bool(on == n and np.array_equal(og, grp))}
+    print(json.dumps(out), flush=True)
+
+
 def run_intervals(args, emo, synth, np, torch):
     """Time-interval policies (emo_eval_intervals) on workload k's graph: the workload's batch
     size, K intervals over [0, 1.05 T0) (change points on the time grid), idle power rising with
@@ -280,6 +354,8 @@ def main():
     ap.add_argument("--intervals", type=int, default=0, metavar="K",
                     help="time emo_eval_intervals (time-interval policies with K intervals) on the "
                          "workload's graph and batch size instead of the evaluation step")
+    ap.add_argument("--pack", action="store_true",
+                    help="time the packing pass on --workload's graph (each pack one kernel)")
     ap.add_argument("--dp-buckets", type=int, default=64,
                     help="makespan buckets of the search between T0 and 1.05 T0 (default 64)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -312,6 +388,9 @@ def main():
         return
     if args.intervals:
         run_intervals(args, emo, synth, np, torch)
+        return
+    if args.pack:
+        run_pack(args, emo, synth, np, torch)
         return
 
     k = args.workload
