@@ -477,3 +477,35 @@ def random_dag(rng: np.random.Generator, num_nodes: int, edge_prob: float, pack_
                  pack_time=np.ascontiguousarray(t, dtype=np.float32),
                  pack_energy=np.ascontiguousarray(e, dtype=np.float32),
                  static_power=float(np.float32(rng.uniform(0.0, 1.0))))
+
+
+MODEL_METRICS = 16      # metrics per pack (counter groups, read and write split)
+MODEL_BENCHMARKS = 12   # microbenchmarks in the proxy suite
+
+
+@dataclasses.dataclass
+class ModelInputs:
+    """Inputs of the microbenchmark pack model: the metric matrix of the suite (metrics x
+    benchmarks, each metric row scaled to a maximum of 1), the suite's latency and energy at
+    every level, and the metric vector of every pack (a non-negative mix of the suite plus
+    noise)."""
+    metric_matrix: np.ndarray    # float32 [n, m]
+    bench_time: np.ndarray       # float32 [m, F]
+    bench_energy: np.ndarray     # float32 [m, F]
+    pack_metrics: np.ndarray     # float32 [P, n]
+    true_weights: np.ndarray     # float64 [P, m] (the mix before noise)
+
+
+def model_inputs(seed: int, num_packs: int, num_levels: int, n: int = MODEL_METRICS,
+                 m: int = MODEL_BENCHMARKS, noise: float = 0.02) -> ModelInputs:
+    rng = np.random.default_rng(seed)
+    B = rng.lognormal(0.0, 1.0, (n, m)) * (rng.random((n, m)) < 0.6)
+    B[rng.integers(0, n, m), np.arange(m)] += 1.0       # every benchmark touches some metric
+    B /= B.max(axis=1, keepdims=True).clip(min=1e-30)
+    t, _ = pack_tables(rng, m, num_levels, 200.0, 0.5)
+    r = level_ratios(num_levels)
+    e = ((STATIC_POWER + C_DYN * r[None, :] ** 3) * t.astype(np.float64)).astype(np.float32)
+    w = rng.exponential(1.0, (num_packs, m)) * (rng.random((num_packs, m)) < 0.4)
+    w[np.arange(num_packs), rng.integers(0, m, num_packs)] += 0.5
+    b = (w @ B.T) * rng.lognormal(0.0, noise, (num_packs, n))
+    return ModelInputs(B.astype(np.float32), t, e, b.astype(np.float32), w)
