@@ -368,6 +368,31 @@ emo_status emo_contract_packs(int32_t num_nodes, int32_t num_edges, const int32_
                               int32_t *packed_src, int32_t *packed_dst, float *group_time,
                               float *group_energy, int32_t *counts);
 
+/*
+ * Microbenchmark pack model (Sec. IV-E, Eq. 6-7), a host-only load-time pass that needs no GPU.
+ * For every pack p, the non-negative weights x = argmin ||B x - b_p||^2 subject to x >= 0 over
+ * the microbenchmark suite (Eq. 6), then the pack's tables at every level f:
+ *   pack_time[p][f] = sum_i x_i bench_time[i][f],  pack_energy[p][f] = sum_i x_i bench_energy[i][f]
+ * (Eq. 7), accumulated in double in benchmark order and rounded to fp32: the tables
+ * emo_load_graph takes.  The solver is Lawson and Hanson's active-set method with Householder
+ * QR on the passive columns, in double precision.  When B has full column rank the minimiser is
+ * unique; otherwise (fewer metrics than benchmarks) the residual is, and the weights are one
+ * minimiser.
+ *   metric_matrix: host float [n][m] row-major: metric r of benchmark i at the default
+ *                  frequency (n = num_metrics >= 1, m = num_benchmarks in [1, 64]), finite.
+ *   bench_time, bench_energy: host float [m][F], finite, >= 0; F = num_levels in [1, 256].
+ *   pack_metrics:  host float [P][n]: each pack's metric vector b_p at the default frequency.
+ *   weights:       host float [P][m] out, or NULL.
+ *   pack_time, pack_energy: host float [P][F] out.
+ *   num_threads:   host threads to use (packs are independent); <= 0 for all cores.
+ * Synchronous.  EMO_ERR_INVALID_ARGUMENT for bad sizes, NULLs or non-finite inputs;
+ * EMO_ERR_UNSUPPORTED if a pack's iteration does not converge (outputs then unspecified).
+ */
+emo_status emo_pack_model(int32_t num_metrics, int32_t num_benchmarks, const float *metric_matrix,
+                          int32_t num_levels, const float *bench_time, const float *bench_energy,
+                          int32_t num_packs, const float *pack_metrics, float *weights,
+                          float *pack_time, float *pack_energy, int32_t num_threads);
+
 /* Diagnostics: the HIP source of the kernels specialised to `g` (the text EMO_KERNELS_AUTO
  * compiles on first use), NUL-terminated.  With buf == NULL, *len receives the size needed
  * including the NUL; otherwise at most *len bytes are written.  Works on host-only graphs.

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libemo.so")
-SOURCES = ["emo_host.cpp", "emo_jit.cpp", "emo_pack.cpp", "emo_kernels.hip", "emo_chains.hip", "emo_dp.hip"]
+SOURCES = ["emo_host.cpp", "emo_jit.cpp", "emo_pack.cpp", "emo_model.cpp", "emo_kernels.hip", "emo_chains.hip", "emo_dp.hip"]
 ARCH = os.environ.get("EMO_OFFLOAD_ARCH", "gfx950")
 
 HIPCC_FLAGS = [

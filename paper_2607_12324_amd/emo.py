@@ -25,6 +25,7 @@ ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
                 "emo_select_from_results", "emo_dp_search", "emo_eval_intervals",
                 "emo_graph_set_timing_events", "emo_pack_kernels", "emo_contract_packs",
+                "emo_pack_model",
                 "emo_graph_specialized_source",
                 "emo_graph_segmented_source", "emo_graph_cut_source", "emo_status_string",
                 "emo_last_error")
@@ -79,6 +80,7 @@ def _load_library():
         "emo_graph_cut_source": [P, P, P],
         "emo_graph_set_timing_events": [P, P, P],
         "emo_pack_kernels": [i32, i32, P, P, P, P, P, i32, i32, P, f32, P, P],
+        "emo_pack_model": [i32, i32, P, i32, P, P, i32, P, P, P, P, i32],
         "emo_contract_packs": [i32, i32, P, P, P, P, i32, i32, P, P, P, i32, P, P, P, P, P, P,
                                P, P],
     }
@@ -410,3 +412,22 @@ def contract_packs(graph, group, num_groups: int) -> PackedGraph:
                        node_pack=node_pack[:n].copy(), node_duration=node_dur[:n].copy(),
                        num_packs=int(num_groups), num_levels=F, pack_time=gt, pack_energy=ge,
                        static_power=float(graph.static_power), packed_node=packed_node)
+
+
+def pack_model(metric_matrix, bench_time, bench_energy, pack_metrics, num_threads: int = 0):
+    """Microbenchmark pack model (host pass): weights [P, m] and tables [P, F] (Eq. 6-7)."""
+    B = _np(metric_matrix, np.float32)
+    bt = _np(bench_time, np.float32)
+    be = _np(bench_energy, np.float32)
+    b = _np(pack_metrics, np.float32)
+    n, m = B.shape
+    F = bt.shape[1]
+    if bt.shape != (m, F) or be.shape != (m, F) or b.ndim != 2 or b.shape[1] != n:
+        raise ValueError("pack_model: inconsistent shapes")
+    P = b.shape[0]
+    W = np.empty((P, m), dtype=np.float32)
+    T = np.empty((P, F), dtype=np.float32)
+    E = np.empty((P, F), dtype=np.float32)
+    _check(lib.emo_pack_model(n, m, _nptr(B), F, _nptr(bt), _nptr(be), P, _nptr(b), _nptr(W),
+                              _nptr(T), _nptr(E), int(num_threads)))
+    return W, T, E
