@@ -240,6 +240,51 @@ def run_pack(args, emo, synth, np, torch):
     print(json.dumps(out), flush=True)
 
 
+def run_model(args, emo, synth, np, torch):
+    """Microbenchmark pack model (emo_pack_model, host pass, Eq. 6-7) for every pack of workload
+    k: a 16-metric, 12-benchmark suite; `value` = packs modelled per second.  The CPU baseline
+    runs the pack-model oracle on the first packs for about 10 s."""
+    k = args.workload
+    g = synth.config_graph(k)
+    mi = synth.model_inputs(k, g.num_packs, g.num_levels)
+    times = []
+    for i in range(args.warmup + args.steps):
+        t = time.perf_counter()
+        W, T, E = emo.pack_model(mi.metric_matrix, mi.bench_time, mi.bench_energy, mi.pack_metrics)
+        if i >= args.warmup:
+            times.append(time.perf_counter() - t)
+    ms = 1e3 * float(np.median(times))
+    threads = os.cpu_count()
+    out = {
+        "metric": "microbenchmark pack model (Sec. IV-E, NNLS + Eq. 7), host pass: packs/sec",
+        "value": g.num_packs / (ms / 1e3), "unit": "packs/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": synth.CONFIGS[k].name, "packs": g.num_packs,
+                   "levels": g.num_levels, "metrics": int(mi.metric_matrix.shape[0]),
+                   "benchmarks": int(mi.metric_matrix.shape[1]), "host_threads": threads,
+                   "step": "emo_pack_model"},
+        "roofline": None,
+        "roofline_note": "host pass, once per graph; no device kernel",
+    }
+    if not args.no_cpu_baseline:
+        from oracle import pack_model as opm   # the CPU baseline leg only
+        t = time.perf_counter()
+        done = 0
+        same = True
+        while done < g.num_packs and time.perf_counter() - t < 10.0:
+            x, _ = opm.fit_pack(mi.metric_matrix, mi.pack_metrics[done])
+            to, _ = opm.predict(x, mi.bench_time, mi.bench_energy)
+            same &= bool(np.allclose(to, T[done], rtol=1e-6))
+            done += 1
+        dt = time.perf_counter() - t
+        out["cpu_baseline"] = {"value": done / dt, "unit": "packs/s", "cores": 1, "kind": "oracle",
+                               "sample": f"the first {done} packs ({dt:.1f} s; SciPy NNLS certified "
+                                         "by KKT, Eq. 7 in Python, 1 thread)",
+                               "same_tables": same}
+    print(json.dumps(out), flush=True)
+
+
 def run_intervals(args, emo, synth, np, torch):
     """Time-interval policies (emo_eval_intervals) on workload k's graph: the workload's batch
     size, K intervals over [0, 1.05 T0) (change points on the time grid), idle power rising with
@@ -356,6 +401,8 @@ def main():
                          "workload's graph and batch size instead of the evaluation step")
     ap.add_argument("--pack", action="store_true",
                     help="time the packing pass on --workload's graph (each pack one kernel)")
+    ap.add_argument("--model", action="store_true",
+                    help="time the pack model (NNLS, Eq. 7) for every pack of --workload")
     ap.add_argument("--dp-buckets", type=int, default=64,
                     help="makespan buckets of the search between T0 and 1.05 T0 (default 64)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -391,6 +438,9 @@ def main():
         return
     if args.pack:
         run_pack(args, emo, synth, np, torch)
+        return
+    if args.model:
+        run_model(args, emo, synth, np, torch)
         return
 
     k = args.workload

@@ -132,18 +132,28 @@ bool nnls(const double *B, int n, int m, const double *b, double tol, double *x)
                 break;
             }
             // step from x toward s until the first passive weight reaches zero
-            double alpha = 1.0;
+            double alpha = 2.0;
+            int qmin = -1;
             for (int i = 0; i < k; ++i) {
                 const int q = S[i];
-                if (s[q] <= 0.0) alpha = std::min(alpha, x[q] / (x[q] - s[q]));
+                if (s[q] <= 0.0) {
+                    const double a = x[q] / (x[q] - s[q]);
+                    if (a < alpha) {
+                        alpha = a;
+                        qmin = q;
+                    }
+                }
             }
+            if (qmin < 0) return false;
             for (int i = 0; i < m; ++i) {
                 x[i] += alpha * (s[i] - x[i]);
-                if (passive[i] && x[i] <= 0.0) {
+                // the weight that limits the step leaves exactly, whatever the rounding left
+                if (passive[i] && (i == qmin || x[i] <= 0.0)) {
                     passive[i] = false;
                     x[i] = 0.0;
                 }
             }
+            if (inner == m) return false;
         }
         if (added)
             for (int i = 0; i < m; ++i) dependent[i] = false;

@@ -78,3 +78,24 @@ def test_packed_graph(torch, emo, case):
           f"mean makespan gap {float(np.mean((Tu - Tp) / Tu)):.2e}", flush=True)
     hp.close()
     hu.close()
+
+
+def test_model_tables_feed_the_evaluator(torch, emo):
+    """Tables from the pack model (emo_pack_model, Eq. 6-7) on the 512-pack training graph,
+    evaluated through the C ABI against the oracle on the same tables."""
+    print("[case] pack-model tables on training-512p-4s-F16", flush=True)
+    import dataclasses
+    g = synth.config_graph(3)
+    mi = synth.model_inputs(2, g.num_packs, g.num_levels)
+    _, T, E = emo.pack_model(mi.metric_matrix, mi.bench_time, mi.bench_energy, mi.pack_metrics)
+    gm = dataclasses.replace(g, pack_time=T, pack_energy=E)
+    rng = np.random.default_rng(3)
+    rows = rng.integers(0, g.num_levels, (4096, g.num_packs)).astype(np.uint8)
+    rows[0] = g.num_levels - 1
+    h = emo.EmoGraph(gm, device=0)
+    Tg, Eg = (x.cpu().numpy() for x in h.eval_policies(torch.from_numpy(rows).cuda()))
+    sample = np.arange(0, 4096, 97)
+    To, Eo = oracle.eval_batch(gm, rows[sample])
+    assert np.all(np.abs(Tg[sample] - To) <= 1e-5 * To)
+    assert np.all(np.abs(Eg[sample] - Eo) <= 1e-5 * Eo)
+    h.close()

@@ -65,3 +65,17 @@ def test_library_edge_cases_and_errors(emo):
     big = synth.model_inputs(2, 2, 2, m=65)
     with pytest.raises(emo.EmoError, match="INVALID_ARGUMENT"):
         emo.pack_model(big.metric_matrix, big.bench_time, big.bench_energy, big.pack_metrics)
+
+
+def test_library_step_to_boundary_regression(emo):
+    """Packs of the 65,536-pack suite where a weight left at a rounding residue instead of zero
+    after the step to the boundary once stopped the iteration at a non-optimal point."""
+    mi = synth.model_inputs(5, 65536, 16)
+    W, T, E = emo.pack_model(mi.metric_matrix, mi.bench_time, mi.bench_energy, mi.pack_metrics)
+    B = mi.metric_matrix.astype(np.float64)
+    for p in (4868, 15139):
+        b = mi.pack_metrics[p].astype(np.float64)
+        x, res = pm.fit_pack(B, b)
+        to, eo = pm.predict(x, mi.bench_time, mi.bench_energy)
+        assert np.allclose(T[p], to, rtol=1e-6) and np.allclose(E[p], eo, rtol=1e-6)
+        assert np.linalg.norm(B @ W[p].astype(np.float64) - b) <= res * (1 + 1e-6) + 1e-9
