@@ -60,6 +60,9 @@ def _load_library():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() or "
                           "python -m paper_2607_12324_amd.build")
+    # torch first: it carries its own HIP runtime, and libemo must bind to that same runtime
+    # (loaded first, libemo would map the system's as a second runtime, which sees no device)
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     P, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
     sig = {

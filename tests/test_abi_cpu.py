@@ -322,3 +322,17 @@ def test_topo_order_and_analysis_on_workloads(emo, oracle_lib, k):
     if n_host_const:
         host = np.nonzero(g.node_pack < 0)[0]
         assert inf["const_makespan"] == float(np.sum(g.node_duration[host].astype(np.float64)))
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Importing the binding before torch must not map a second HIP runtime: the library has
+    to share torch's, or it sees no device."""
+    import subprocess
+    import sys
+    code = ("from paper_2607_12324_amd import emo\nimport torch\n"
+            "maps = [l.split()[-1] for l in open('/proc/self/maps') if 'amdhip64' in l]\n"
+            "print(len(set(maps)))\n")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip() == "1"
