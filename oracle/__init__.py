@@ -48,6 +48,9 @@ def _bind(path):
     lib.oracle_eval_batch.restype = i32
     lib.oracle_slack.argtypes = [i32, i32, P, P, P, P, i32, i32, P, P, f64, P, P, P, P, P, P, P]
     lib.oracle_slack.restype = i32
+    lib.oracle_slack_batch.argtypes = [i32, i32, P, P, P, P, i32, i32, P, P, f64, P, i64, i32,
+                                       P, P, P, i32]
+    lib.oracle_slack_batch.restype = i32
     lib.oracle_select.argtypes = [P, P, i64, f64, P, P]
     lib.oracle_select.restype = i64
     return lib
@@ -137,7 +140,7 @@ class SlackResult:
     eft: np.ndarray          # [V] completion (earliest finish) times
     lft: np.ndarray          # [V] latest finish times
     slack: np.ndarray        # [V] total float
-    critical_pred: np.ndarray  # [V] Alg. 1 critical predecessor, -1 for none
+    critical_pred: np.ndarray  # [V] critical predecessor (Eq. 5), -1 for none
 
 
 def slack(g, level_row) -> SlackResult:
@@ -164,6 +167,21 @@ def pack_slack(g, level_row) -> np.ndarray:
     m = pk >= 0
     out[pk[m]] = r.slack[m]
     return out
+
+
+def slack_batch(g, levels, per_node: bool = False, nthreads: int = 1):
+    """Makespan, energy ([B] float64) and slack of every row of `levels` ([B, P] uint8): [B, P]
+    by pack id, or [B, V] by node id with per_node.  Rows with a level >= F are NaN."""
+    lib = _load()
+    G = _G(g)
+    lv = _c(levels, np.uint8).reshape(-1, G.P) if G.P > 0 else np.zeros((len(levels), 0), np.uint8)
+    B = int(lv.shape[0])
+    T = np.empty(B, dtype=np.float64)
+    E = np.empty(B, dtype=np.float64)
+    S = np.empty((B, G.V if per_node else G.P), dtype=np.float64)
+    _check(lib.oracle_slack_batch(*G.args(), _ptr(lv), B, int(bool(per_node)), _ptr(T), _ptr(E),
+                                  _ptr(S), int(nthreads)))
+    return T, E, S
 
 
 def select(T, E, target):

@@ -10,26 +10,28 @@
  * Arithmetic: every time and energy is held in double precision (the fp32 inputs convert
  * exactly); no blocking, fusion or reordering beyond the definitions below.
  *
- * Definitions followed (all citations are to the paper):
- *   - completion time C_v = t_v + max over predecessors of C_k            (Eq. 1)
- *     with sources starting at time 0 (the paper leaves comp[pred[v]] undefined for a
- *     node without predecessors; start 0 is the reading taken here);
- *   - makespan T = max_v C_v, energy E = sum_v e_v + E_idle               (Eq. 2)
- *     with E_idle read as static_power * T;
- *   - frequency-dependent cost: a pack's duration and energy come from its latency/energy
- *     tables at the level its policy assigns; other nodes keep their fixed duration and
- *     contribute no energy                                                (Eq. 3, Alg. 1);
- *   - one level per pack (the per-pack form of the policy of Eq. 4);
- *   - the prediction itself is one traversal in topological order that tracks each node's
- *     critical predecessor with a strict "greater than" test               (Alg. 1, Eq. 5);
- *   - slack: total float of the critical-path method, LFT(v) - EFT(v) with
- *     LFT(v) = T for a node without successors, else min over successors (LFT(u) - t_u);
- *     the paper defines slack as the time windows in which a kernel is off the critical path
+ * Each quantity is computed from its defining equation, one equation per function:
+ *   - node cost (Eq. 3): a pack's duration and energy are its latency and energy table entries
+ *     at the level its policy assigns (one level per pack, the per-pack form of the policy of
+ *     Eq. 4); other nodes keep their fixed duration and use no energy;
+ *   - completion time (Eq. 1): C_v = t_v + the largest completion time among v's
+ *     predecessors, 0 for a node without predecessors (the paper leaves that maximum
+ *     undefined; start 0 is the reading taken here).  Evaluated in a topological order so
+ *     that every predecessor is known first;
+ *   - makespan and energy (Eq. 2): T = max over all nodes of C_v, E = sum over all nodes of
+ *     e_v + E_idle, with E_idle read as static_power * T;
+ *   - critical predecessor (Eq. 5): the predecessor of largest completion time; among equal
+ *     ones the first in the canonical topological order (the strict comparison with which the
+ *     paper's predictor keeps the first one it meets);
+ *   - slack: total float of the critical-path method, LFT(v) - C_v with LFT(v) = T for a
+ *     node without successors, else the least latest start LFT(u) - t_u over its successors;
+ *     the paper describes slack as the time in which a kernel is off the critical path
  *     (Sec. I);
  *   - feasibility T <= T_set and the argmin of energy over feasible policies (Eq. 4), ties
  *     broken by the lower candidate index;
  *   - canonical topological order: nodes sorted by (depth, id), depth(v) = 0 for a source
  *     and 1 + max depth of its predecessors otherwise, computed by memoised recursion.
+ * A level byte >= F makes a candidate's makespan, energy and slack NaN (not a policy).
  *
  * Every function is pinned by the CPU tests (brute force over paths, closed forms, a
  * hand-worked example and invariants); none is "parity unpinned".
@@ -46,7 +48,6 @@
 
 typedef struct {
     int V, E, P, F;
-    const int *src, *dst;      /* [E] */
     const int *pack;           /* [V] pack id or -1 */
     const float *dur;          /* [V] fixed durations */
     const float *tt, *te;      /* [P*F] latency / energy tables */
@@ -55,15 +56,17 @@ typedef struct {
     int *pred_off, *pred;      /* CSR of predecessors */
     int *succ_off, *succ;      /* CSR of successors */
     int *order;                /* canonical topological order */
+    int *pos;                  /* position of each node in that order */
     int *depth;
 } ograph;
 
 static void ograph_free(ograph *g) {
     free(g->pred_off); free(g->pred); free(g->succ_off); free(g->succ);
-    free(g->order); free(g->depth);
+    free(g->order); free(g->pos); free(g->depth);
     memset(g, 0, sizeof(*g));
 }
 
+/* adjacency lists adj[off[v] .. off[v+1]) = { from[i] : to[i] == v } */
 static int build_csr(int V, int E, const int *from, const int *to, int **off_out, int **adj_out) {
     int *off = (int *)calloc((size_t)V + 1, sizeof(int));
     int *adj = (int *)malloc(((size_t)E + 1) * sizeof(int));
@@ -133,19 +136,21 @@ static int ograph_init(ograph *g, int V, int E, const int *src, const int *dst, 
     for (int v = 0; v < V && pack; ++v)
         if (pack[v] < -1 || pack[v] >= P) return ORACLE_BAD_ARGUMENT;
     g->V = V; g->E = E; g->P = P; g->F = F;
-    g->src = src; g->dst = dst; g->pack = pack; g->dur = dur; g->tt = tt; g->te = te;
+    g->pack = pack; g->dur = dur; g->tt = tt; g->te = te;
     g->static_power = static_power;
     int rc = build_csr(V, E, src, dst, &g->pred_off, &g->pred);
     if (rc == ORACLE_OK) rc = build_csr(V, E, dst, src, &g->succ_off, &g->succ);
     if (rc != ORACLE_OK) { ograph_free(g); return rc; }
     g->order = (int *)malloc(((size_t)V + 1) * sizeof(int));
+    g->pos = (int *)malloc(((size_t)V + 1) * sizeof(int));
     g->depth = (int *)malloc(((size_t)V + 1) * sizeof(int));
-    if (!g->order || !g->depth) { ograph_free(g); return ORACLE_NO_MEMORY; }
+    if (!g->order || !g->pos || !g->depth) { ograph_free(g); return ORACLE_NO_MEMORY; }
     rc = compute_depths(g);
     if (rc != ORACLE_OK) { ograph_free(g); return rc; }
     for (int v = 0; v < V; ++v) g->order[v] = v;
     g_sort_depth = g->depth;
     qsort(g->order, (size_t)V, sizeof(int), cmp_depth_id);
+    for (int i = 0; i < V; ++i) g->pos[g->order[i]] = i;
     return ORACLE_OK;
 }
 
@@ -160,42 +165,87 @@ int oracle_topo_order(int V, int E, const int *src, const int *dst, int *order, 
     return ORACLE_OK;
 }
 
-/* Duration and energy of node v under the level row `lv` (Eq. 3). Sets *bad on a level
- * outside [0, F). */
-static void node_cost(const ograph *g, const uint8_t *lv, int v, double *d, double *e, int *bad) {
-    int p = g->pack[v];
-    if (p < 0) { *d = (double)g->dur[v]; *e = 0.0; return; }
-    int l = lv[p];
-    if (l >= g->F) { *bad = 1; *d = 0.0; *e = 0.0; return; }
-    *d = (double)g->tt[(size_t)p * g->F + l];
-    *e = (double)g->te[(size_t)p * g->F + l];
+/* Eq. 3: dur[v] and en[v] of every node under the level row `lv`.  Returns 0, or 1 when a
+ * pack's level lies outside [0, F) (the row is then not a policy). */
+static int node_costs(const ograph *g, const uint8_t *lv, double *dur, double *en) {
+    int bad = 0;
+    for (int v = 0; v < g->V; ++v) {
+        int p = g->pack[v];
+        if (p < 0) { dur[v] = (double)g->dur[v]; en[v] = 0.0; continue; }
+        int l = lv[p];
+        if (l >= g->F) { bad = 1; dur[v] = 0.0; en[v] = 0.0; continue; }
+        dur[v] = (double)g->tt[(size_t)p * g->F + l];
+        en[v] = (double)g->te[(size_t)p * g->F + l];
+    }
+    return bad;
 }
 
-/* What-if prediction of one candidate (Alg. 1 with one level per pack):
- * one traversal in topological order; comp[] are completion times, cpred[] critical
- * predecessors (-1: none).  Returns makespan and energy; NaN for both on a bad level. */
-static void predict_one(const ograph *g, const uint8_t *lv, double *comp, int *cpred,
-                        double *T_out, double *E_out) {
-    int bad = 0;
-    double Ea = 0.0;
-    for (int v = 0; v < g->V; ++v) cpred[v] = -1;
+/* Eq. 1: C[v] = dur[v] + max over predecessors k of C[k] (0 without predecessors), taken in
+ * topological order so that every C[k] is final when v is reached. */
+static void completion_times(const ograph *g, const double *dur, double *C) {
     for (int i = 0; i < g->V; ++i) {
         int v = g->order[i];
-        double start = cpred[v] >= 0 ? comp[cpred[v]] : 0.0;
-        double d, e;
-        node_cost(g, lv, v, &d, &e, &bad);
-        comp[v] = start + d;
-        Ea += e;
-        for (int j = g->succ_off[v]; j < g->succ_off[v + 1]; ++j) {
-            int u = g->succ[j];
-            if (cpred[u] < 0 || comp[v] > comp[cpred[u]]) cpred[u] = v;
+        double s = 0.0;
+        for (int j = g->pred_off[v]; j < g->pred_off[v + 1]; ++j) {
+            int k = g->pred[j];
+            if (C[k] > s) s = C[k];
         }
+        C[v] = s + dur[v];
     }
-    double T = 0.0;
-    for (int v = 0; v < g->V; ++v) if (comp[v] > T) T = comp[v];
-    if (bad) { *T_out = NAN; *E_out = NAN; return; }
+}
+
+/* Eq. 2: T = max over nodes of C, E = sum over nodes of e + static_power * T. */
+static void makespan_energy(const ograph *g, const double *C, const double *en, double *T_out,
+                            double *E_out) {
+    double T = 0.0, Ea = 0.0;
+    for (int v = 0; v < g->V; ++v) {
+        if (C[v] > T) T = C[v];
+        Ea += en[v];
+    }
     *T_out = T;
     *E_out = Ea + g->static_power * T;
+}
+
+/* Eq. 5: cpred[v] = the predecessor of largest completion time, the first in the canonical
+ * order among equal ones; -1 for a node without predecessors. */
+static void critical_predecessors(const ograph *g, const double *C, int *cpred) {
+    for (int v = 0; v < g->V; ++v) {
+        int best = -1;
+        for (int j = g->pred_off[v]; j < g->pred_off[v + 1]; ++j) {
+            int k = g->pred[j];
+            if (best < 0 || C[k] > C[best] || (C[k] == C[best] && g->pos[k] < g->pos[best]))
+                best = k;
+        }
+        cpred[v] = best;
+    }
+}
+
+/* Backward pass of the critical-path method: LFT(v) = T without successors, else the least
+ * LFT(u) - dur(u) over successors u, taken in reverse topological order; slack = LFT - C. */
+static void total_float(const ograph *g, const double *dur, const double *C, double T,
+                        double *lft, double *slack) {
+    for (int i = g->V - 1; i >= 0; --i) {
+        int v = g->order[i];
+        double l = T;
+        for (int j = g->succ_off[v]; j < g->succ_off[v + 1]; ++j) {
+            int u = g->succ[j];
+            double lst_u = lft[u] - dur[u];
+            if (j == g->succ_off[v] || lst_u < l) l = lst_u;
+        }
+        lft[v] = l;
+        slack[v] = l - C[v];
+    }
+}
+
+/* One candidate: costs, completion times, makespan and energy; NaN T and E on a bad level.
+ * Returns the bad flag. */
+static int evaluate_one(const ograph *g, const uint8_t *lv, double *dur, double *en, double *C,
+                        double *T, double *En) {
+    int bad = node_costs(g, lv, dur, en);
+    completion_times(g, dur, C);
+    makespan_energy(g, C, en, T, En);
+    if (bad) { *T = NAN; *En = NAN; }
+    return bad;
 }
 
 /* Evaluate B candidates: levels is [B][P] row-major. T and E are [B]. */
@@ -209,24 +259,24 @@ int oracle_eval_batch(int V, int E, const int *src, const int *dst, const int *p
     int failed = 0;
 #pragma omp parallel num_threads(nthreads > 0 ? nthreads : 1)
     {
-        double *comp = (double *)malloc(((size_t)V + 1) * sizeof(double));
-        int *cpred = (int *)malloc(((size_t)V + 1) * sizeof(int));
-        if (!comp || !cpred) {
+        double *buf = (double *)malloc(3 * ((size_t)V + 1) * sizeof(double));
+        if (!buf) {
 #pragma omp atomic write
             failed = 1;
         } else {
+            double *d = buf, *e = buf + V + 1, *C = buf + 2 * ((size_t)V + 1);
 #pragma omp for schedule(static)
             for (int64_t c = 0; c < B; ++c)
-                predict_one(&g, levels + (size_t)c * P, comp, cpred, &T[c], &En[c]);
+                evaluate_one(&g, levels + (size_t)c * P, d, e, C, &T[c], &En[c]);
         }
-        free(comp); free(cpred);
+        free(buf);
     }
     ograph_free(&g);
     return failed ? ORACLE_NO_MEMORY : ORACLE_OK;
 }
 
-/* Forward completion times, backward latest finish times and slack of every node for one
- * candidate, plus the critical-predecessor array of Alg. 1.  All outputs are [V]. */
+/* Completion times, latest finish times, slack and critical predecessors of every node for one
+ * candidate.  All outputs are [V]; a bad level makes lft and slack NaN. */
 int oracle_slack(int V, int E, const int *src, const int *dst, const int *pack, const float *dur,
                  int P, int F, const float *tt, const float *te, double static_power,
                  const uint8_t *lv, double *eft, double *lft, double *slack, int *cpred,
@@ -234,28 +284,55 @@ int oracle_slack(int V, int E, const int *src, const int *dst, const int *pack, 
     ograph g;
     int rc = ograph_init(&g, V, E, src, dst, pack, dur, P, F, tt, te, static_power);
     if (rc != ORACLE_OK) return rc;
-    predict_one(&g, lv, eft, cpred, T_out, E_out);
-    double T = *T_out;
-    int bad = 0;
-    for (int i = V - 1; i >= 0; --i) {
-        int v = g.order[i];
-        double l = T;
-        if (g.succ_off[v + 1] > g.succ_off[v]) {
-            l = INFINITY;
-            for (int j = g.succ_off[v]; j < g.succ_off[v + 1]; ++j) {
-                int u = g.succ[j];
-                double du, eu;
-                node_cost(&g, lv, u, &du, &eu, &bad);
-                double lst_u = lft[u] - du;
-                if (lst_u < l) l = lst_u;
-            }
-        }
-        lft[v] = l;
-        slack[v] = l - eft[v];
-    }
-    if (bad || isnan(T)) for (int v = 0; v < V; ++v) { lft[v] = NAN; slack[v] = NAN; }
+    double *d = (double *)malloc(2 * ((size_t)V + 1) * sizeof(double));
+    if (!d) { ograph_free(&g); return ORACLE_NO_MEMORY; }
+    double *e = d + V + 1;
+    int bad = evaluate_one(&g, lv, d, e, eft, T_out, E_out);
+    critical_predecessors(&g, eft, cpred);
+    total_float(&g, d, eft, *T_out, lft, slack);
+    if (bad) for (int v = 0; v < V; ++v) { lft[v] = NAN; slack[v] = NAN; }
+    free(d);
     ograph_free(&g);
     return ORACLE_OK;
+}
+
+/* Makespan, energy and slack of B candidates (levels [B][P]).  per_node = 0: S is [B][P],
+ * the slack of pack p at S[c*P + p]; per_node = 1: S is [B][V] indexed by node id.  T and E
+ * are [B].  A bad level makes the candidate's T, E and slack row NaN. */
+int oracle_slack_batch(int V, int E, const int *src, const int *dst, const int *pack,
+                       const float *dur, int P, int F, const float *tt, const float *te,
+                       double static_power, const uint8_t *levels, int64_t B, int per_node,
+                       double *T, double *En, double *S, int nthreads) {
+    ograph g;
+    int rc = ograph_init(&g, V, E, src, dst, pack, dur, P, F, tt, te, static_power);
+    if (rc != ORACLE_OK) return rc;
+    int failed = 0;
+    const size_t cols = per_node ? (size_t)V : (size_t)P;
+#pragma omp parallel num_threads(nthreads > 0 ? nthreads : 1)
+    {
+        double *buf = (double *)malloc(5 * ((size_t)V + 1) * sizeof(double));
+        if (!buf) {
+#pragma omp atomic write
+            failed = 1;
+        } else {
+            const size_t n = (size_t)V + 1;
+            double *d = buf, *e = buf + n, *C = buf + 2 * n, *lft = buf + 3 * n, *sl = buf + 4 * n;
+#pragma omp for schedule(static)
+            for (int64_t c = 0; c < B; ++c) {
+                int bad = evaluate_one(&g, levels + (size_t)c * P, d, e, C, &T[c], &En[c]);
+                total_float(&g, d, C, T[c], lft, sl);
+                double *row = S + (size_t)c * cols;
+                for (int v = 0; v < V; ++v) {
+                    double s = bad ? NAN : sl[v];
+                    if (per_node) row[v] = s;
+                    else if (g.pack[v] >= 0) row[g.pack[v]] = s;
+                }
+            }
+        }
+        free(buf);
+    }
+    ograph_free(&g);
+    return failed ? ORACLE_NO_MEMORY : ORACLE_OK;
 }
 
 /* Feasibility (T <= target) and the lowest-energy feasible candidate, lower index on ties.

@@ -370,6 +370,67 @@ def pin_exhaustive_tiny_workload():
     assert idx == int(best), (idx, best)
 
 
+def pin_invalid_level(seed=61):
+    """A level byte >= F is not a policy: that candidate's makespan, energy and every slack
+    value are NaN, it is never feasible and never selected; the other rows are unaffected."""
+    rng = np.random.default_rng(seed)
+    for g in tiny_dags(seed, 20):
+        if g.num_packs == 0:
+            continue
+        rows = random_rows(rng, g, 5)
+        good_T, good_E = oracle.eval_batch(g, rows)
+        bad = rows.copy()
+        bad[1, int(rng.integers(0, g.num_packs))] = g.num_levels + int(rng.integers(0, 256 - g.num_levels))
+        bad[3, -1] = 255
+        T, E = oracle.eval_batch(g, bad)
+        assert np.isnan(T[1]) and np.isnan(E[1]) and np.isnan(T[3]) and np.isnan(E[3])
+        keep = [0, 2, 4]
+        assert np.array_equal(T[keep], good_T[keep]) and np.array_equal(E[keep], good_E[keep])
+        r = oracle.slack(g, bad[1])
+        assert np.isnan(r.makespan) and np.all(np.isnan(r.slack)) and np.all(np.isnan(r.lft))
+        for pn in (False, True):
+            Tb, Eb, Sb = oracle.slack_batch(g, bad, per_node=pn)
+            assert np.all(np.isnan(Sb[[1, 3]])) and not np.any(np.isnan(Sb[keep]))
+            assert np.isnan(Tb[1]) and np.isnan(Eb[3])
+        idx, feas, n = oracle.select(T, E, float("inf"))
+        assert not feas[1] and not feas[3] and n == 3 and idx in keep
+
+
+def pin_critical_pred_ties():
+    """Eq. 5 with equal completion times: the first maximal predecessor in the canonical order
+    (depth, then id), which is not always the lowest id.  Nodes: 0 (1 us) -> 1 (4 us); 2 (5 us);
+    1 and 2 -> 3.  C_1 = C_2 = 5; node 2 has depth 0 and node 1 depth 1, so 2 comes first."""
+    g = synth.Graph("ties", 4, np.array([0, 1, 2], np.int32), np.array([1, 3, 3], np.int32),
+                    np.full(4, -1, np.int32), np.array([1, 4, 5, 2], np.float32), 0, 1,
+                    np.zeros((0, 1), np.float32), np.zeros((0, 1), np.float32), 0.0)
+    r = oracle.slack(g, np.zeros(0, np.uint8))
+    assert r.eft.tolist() == [1.0, 5.0, 5.0, 7.0]
+    assert r.critical_pred.tolist() == [-1, 0, -1, 2], r.critical_pred
+    # with unequal times the later one in the order can win
+    g2 = synth.Graph(**{**g.__dict__, "node_duration": np.array([1, 4.5, 5, 2], np.float32)})
+    assert oracle.slack(g2, np.zeros(0, np.uint8)).critical_pred.tolist() == [-1, 0, -1, 1]
+
+
+def pin_slack_batch(seed=71, count=30):
+    """The batched slack (by pack and by node) against longest paths through each node."""
+    rng = np.random.default_rng(seed + 1)
+    for g in tiny_dags(seed, count):
+        paths = all_paths(g)
+        rows = random_rows(rng, g, 5)
+        T, E, SN = oracle.slack_batch(g, rows, per_node=True, nthreads=2)
+        _, _, SP = oracle.slack_batch(g, rows, per_node=False)
+        for i, row in enumerate(rows):
+            Tb, sb = brute_makespan_and_slack(g, row, paths)
+            assert T[i] == Tb and np.array_equal(SN[i], sb), (g.name, SN[i], sb)
+            for v in range(g.num_nodes):
+                p = int(g.node_pack[v])
+                if p >= 0:
+                    assert SP[i, p] == sb[v], (g.name, p, SP[i, p], sb[v])
+        T1, E1 = oracle.eval_batch(g, rows)
+        assert np.array_equal(T, T1) and np.array_equal(E, E1)
+
+
 ALL_PINS = [pin_handworked, pin_bruteforce_paths, pin_topo_order, pin_cycles, pin_closed_forms,
             pin_all_max_is_longest_path, pin_invariants_tiny, pin_invariants_tiny_workload,
-            pin_exhaustive_selection, pin_select_edge_cases, pin_exhaustive_tiny_workload]
+            pin_exhaustive_selection, pin_select_edge_cases, pin_exhaustive_tiny_workload,
+            pin_invalid_level, pin_critical_pred_ties, pin_slack_batch]

@@ -12,20 +12,25 @@ SRC = os.path.join(os.path.dirname(os.path.abspath(oracle.__file__)), "emo_oracl
 
 MUTANTS = {
     "static_energy_dropped": ("*E_out = Ea + g->static_power * T;", "*E_out = Ea;"),
-    "backward_sign": ("double lst_u = lft[u] - du;", "double lst_u = lft[u] + du;"),
-    "critical_pred_min": ("comp[v] > comp[cpred[u]]", "comp[v] < comp[cpred[u]]"),
+    "backward_sign": ("double lst_u = lft[u] - dur[u];", "double lst_u = lft[u] + dur[u];"),
+    "backward_takes_max": ("if (j == g->succ_off[v] || lst_u < l) l = lst_u;",
+                           "if (j == g->succ_off[v] || lst_u > l) l = lst_u;"),
+    "critical_pred_min": ("C[k] > C[best]", "C[k] < C[best]"),
+    "critical_pred_tie_last": ("g->pos[k] < g->pos[best]", "g->pos[k] > g->pos[best]"),
     "table_transposed": ("(size_t)p * g->F + l", "(size_t)l * g->P + p"),
-    "sink_lft_is_own_eft": ("double l = T;", "double l = eft[v];"),
+    "sink_lft_is_own_eft": ("double l = T;", "double l = C[v];"),
     "feasibility_strict": ("int ok = T[c] <= target;", "int ok = T[c] < target;"),
     "tie_takes_last": ("En[c] < En[best]", "En[c] <= En[best]"),
     "depth_not_incremented": ("int dk = g->depth[g->pred[i]] + 1;", "int dk = g->depth[g->pred[i]];"),
-    "makespan_last_node": ("if (comp[v] > T) T = comp[v];", "T = comp[v];"),
-    "energy_overwritten": ("Ea += e;", "Ea = e;"),
-    "duration_not_added": ("comp[v] = start + d;", "comp[v] = start;"),
-    "start_from_first_pred": ("if (cpred[u] < 0 || comp[v] > comp[cpred[u]]) cpred[u] = v;",
-                              "if (cpred[u] < 0) cpred[u] = v;"),
-    "slack_uses_lft_only": ("slack[v] = l - eft[v];", "slack[v] = l;"),
+    "makespan_last_node": ("if (C[v] > T) T = C[v];", "T = C[v];"),
+    "energy_overwritten": ("Ea += en[v];", "Ea = en[v];"),
+    "duration_not_added": ("C[v] = s + dur[v];", "C[v] = s;"),
+    "start_from_last_pred": ("if (C[k] > s) s = C[k];", "s = C[k];"),
+    "slack_uses_lft_only": ("slack[v] = l - C[v];", "slack[v] = l;"),
     "level_off_by_one": ("int l = lv[p];", "int l = lv[p] > 0 ? lv[p] - 1 : 0;"),
+    "bad_level_ignored": ("if (l >= g->F) { bad = 1;", "if (l >= g->F) { bad = 0;"),
+    "batch_slack_row_shifted": ("else if (g.pack[v] >= 0) row[g.pack[v]] = s;",
+                                "else if (g.pack[v] >= 0) row[(g.pack[v] + 1) % P] = s;"),
 }
 
 
