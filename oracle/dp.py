@@ -1,27 +1,36 @@
 """CPU oracle for the policy search of Alg. 2 -- TEST INFRASTRUCTURE ONLY.
 
-Follows Alg. 2 (Sec. IV-F) step by step, with one frequency interval per pack (the per-pack
-reading of the policy, R1): the intervals [p_i, p_{i+1}) are the packs taken in `pack_order`,
-and the predictor Pred is the oracle's fp64 evaluation of Alg. 1 (``oracle.eval_batch``).
+The search of Sec. IV-F written as a recurrence over makespan buckets, with one frequency
+interval per pack (the per-pack reading of the policy, R1): the change points are the packs
+taken in `pack_order`, and the predictor is the oracle's fp64 evaluation of Eq. 1-3
+(``oracle.eval_batch``).
 
-Readings where the algorithm leaves a choice open (they are the library's as well):
+The state after i change points is a table over discretised end-to-end times: bucket t holds
+the least energy found for a makespan in that bucket and the policy that reaches it.  Sec. IV-F
+builds the table of stage i + 1 from that of stage i only:
 
-* dp[i] is a map from the discretised makespan to one (energy, policy) pair.  The makespan t is
-  discretised as floor(t / quantum), computed in double precision.
+    X_i      = every stored policy (in increasing bucket order) with interval i set to every
+               level f (in increasing order): |dp[i]| x |F| candidates, evaluated by the
+               predictor;
+    dp[i+1]  = for each bucket t, the candidate of X_i with makespan in t and within the
+               latency target of least energy.
+
+dp[0] holds the all-maximum policy P_0.  The answer is the least-energy state of the last table.
+
+Readings where the paper leaves a choice open (they are the library's as well):
+
+* Buckets: floor(t / quantum), computed in double precision.
 * Decisions are taken in fp32, the precision of the library's makespans and energies: the
   predictor's fp64 makespan and energy are rounded to fp32 first, then compared with the fp32
   latency target and with each other.
-* "for each (t, (E, P)) in dp[i]" visits the stored states in increasing bucket order, and "for
-  each f in F" the levels in increasing order.  The update takes a new pair only when its energy
-  is strictly lower, so among equal energies the first candidate in that order stays.
-* dp[0] holds the all-maximum policy P_0 whatever its makespan (the initialisation of Alg. 2
-  does not test the constraint); the stages keep only policies with t <= T_max.
-* The result is the least energy over the final states whose makespan meets T_max; among equal
-  energies the lowest bucket wins.
+* Ties in the per-bucket minimum: the first candidate of X_i in the order above (a later one
+  replaces a stored one only with strictly lower energy).  Ties in the answer: the lowest
+  bucket.
+* dp[0] holds P_0 whatever its makespan (the initialisation does not test the constraint); the
+  later tables hold only policies with t <= T_max.
 """
 from __future__ import annotations
 
-import math
 from dataclasses import dataclass
 
 import numpy as np
@@ -38,59 +47,71 @@ class DPResult:
     evaluated: int = 0          # candidate policies evaluated (P_0 included)
 
 
-def _f32(x) -> np.float32:
-    return np.float32(x)
+@dataclass
+class _Table:
+    """One stage's states, sorted by bucket: bucket [S], energy [S] fp32, makespan [S] fp32,
+    policies [S, P] uint8."""
+    bucket: np.ndarray
+    energy: np.ndarray
+    makespan: np.ndarray
+    policy: np.ndarray
+
+
+def _predict(g, policies, quantum):
+    """fp32 makespans and energies of the policies, and their buckets."""
+    T, E = eval_batch(g, policies)
+    T32, E32 = T.astype(np.float32), E.astype(np.float32)
+    return T32, E32, np.floor(T32.astype(np.float64) / quantum).astype(np.int64)
+
+
+def _expand(table: _Table, interval: int, F: int) -> np.ndarray:
+    """X_i: each stored policy (bucket order) repeated with `interval` set to 0..F-1."""
+    X = np.repeat(table.policy, F, axis=0)
+    X[:, interval] = np.tile(np.arange(F, dtype=np.uint8), table.policy.shape[0])
+    return X
+
+
+def _least_per_bucket(X, T32, E32, bucket, t_max) -> _Table:
+    """dp[i+1]: per bucket, the feasible candidate of least (energy, position in X)."""
+    ok = np.nonzero(T32 <= t_max)[0]
+    order = ok[np.lexsort((ok, E32[ok], bucket[ok]))]       # bucket, then energy, then position
+    first = np.ones(order.size, dtype=bool)
+    first[1:] = bucket[order][1:] != bucket[order][:-1]
+    keep = order[first]
+    return _Table(bucket[keep], E32[keep], T32[keep], X[keep])
 
 
 def dp_search(g, latency_target: float, quantum: float, pack_order=None,
               max_stages: int | None = None) -> DPResult:
-    """Alg. 2 over the packs of `g` in `pack_order` (default: pack ids in increasing order).
+    """The search over the packs of `g` in `pack_order` (default: pack ids in increasing order).
     max_stages stops after that many stages (for timing a bounded sample)."""
     P, F = int(g.num_packs), int(g.num_levels)
     order = list(range(P)) if pack_order is None else [int(x) for x in pack_order]
     if sorted(order) != list(range(P)):
         raise ValueError("pack_order must be a permutation of the pack ids")
-    t_max = _f32(latency_target)
-    q = float(_f32(quantum))
+    t_max = np.float32(latency_target)
+    q = float(np.float32(quantum))
     if not q > 0.0:
         raise ValueError("quantum must be positive")
 
-    # P_0: the default (maximum) frequency in every interval; dp[0] = {t_0: (E_0, P_0)}
-    p0 = np.full(P, F - 1, dtype=np.uint8)
-    T0, E0 = eval_batch(g, p0[None, :])
-    states = [(math.floor(float(_f32(T0[0])) / q), _f32(E0[0]), _f32(T0[0]), p0)]
+    p0 = np.full((1, P), F - 1, dtype=np.uint8)
+    T0, E0, b0 = _predict(g, p0, q)
+    table = _Table(b0, E0, T0, p0)
     evaluated = 1
-
-    for p in order[:max_stages]:
-        # P' = P with frequency f in interval p, for every stored state and every f
-        cands = []
-        for (_, _, _, lv) in states:
-            for f in range(F):
-                lv2 = lv.copy()
-                lv2[p] = f
-                cands.append(lv2)
-        if not cands:          # no state left: every later stage is empty too
+    for interval in order[:max_stages]:
+        if table.policy.shape[0] == 0:       # nothing stored: every later table is empty too
             break
-        Tc, Ec = eval_batch(g, np.stack(cands))
-        evaluated += len(cands)
-        nxt = {}
-        for c, lv2 in enumerate(cands):
-            t, e = _f32(Tc[c]), _f32(Ec[c])
-            if not t <= t_max:
-                continue
-            b = math.floor(float(t) / q)
-            if b not in nxt or e < nxt[b][0]:
-                nxt[b] = (e, t, lv2)
-        states = [(b,) + nxt[b] for b in sorted(nxt)]
+        X = _expand(table, interval, F)
+        T32, E32, bucket = _predict(g, X, q)
+        evaluated += X.shape[0]
+        table = _least_per_bucket(X, T32, E32, bucket, t_max)
 
-    best = None
-    for (b, e, t, lv) in states:
-        if t <= t_max and (best is None or e < best[1]):
-            best = (b, e, t, lv)
-    n = sum(1 for s in states if s[2] <= t_max)
-    if best is None:
-        return DPResult(None, float("nan"), float("nan"), n, evaluated)
-    return DPResult(best[3].copy(), float(best[1]), float(best[2]), n, evaluated)
+    ok = np.nonzero(table.makespan <= t_max)[0]
+    if ok.size == 0:
+        return DPResult(None, float("nan"), float("nan"), 0, evaluated)
+    best = ok[np.lexsort((table.bucket[ok], table.energy[ok]))[0]]   # energy, then bucket
+    return DPResult(table.policy[best].copy(), float(table.energy[best]),
+                    float(table.makespan[best]), int(ok.size), evaluated)
 
 
 def exhaustive_best(g, latency_target: float):
@@ -105,7 +126,7 @@ def exhaustive_best(g, latency_target: float):
         rows[:, p] = (idx // (F ** p)) % F
     T, E = eval_batch(g, rows)
     T32, E32 = T.astype(np.float32), E.astype(np.float32)
-    ok = T32 <= _f32(latency_target)
+    ok = T32 <= np.float32(latency_target)
     if not ok.any():
         return None, float("nan"), float("nan")
     cand = np.nonzero(ok)[0]
