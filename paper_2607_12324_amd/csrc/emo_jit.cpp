@@ -652,7 +652,9 @@ void emit_table(std::ostringstream &o, const JitGraph &g, const TabWindow &w, co
 // (buf + r * bp) plus the lane's 32-bit byte offset o4 (bp * 4 < 2^32), which the compiler
 // folds into one load or store with a scalar base.
 // Lanes past the batch evaluate the last candidate (cand = B - 1) again and use its scratch
-// slot: they compute and store exactly its values, so no store needs a branch.
+// slot.  Stores of values that depend only on the candidate's levels (checkpoint rows, slack)
+// need no branch: those lanes store exactly the owner's values.  Running sums that the next
+// kernel reads back and adds to are stored by the owning lane only.
 std::string chain_lanes(int block) {
     std::ostringstream o;
     o << "  const unsigned int g32 = blockIdx.x * " << block << "u + threadIdx.x;\n"
@@ -712,11 +714,15 @@ void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPla
     LevelPlan lp = emit_forward_range(o, g, r, nullptr);
     if (!last) {
         o << "  if ((bad & " << lp.bad_bits() << ") != 0u) ed = (double)EMO_NAN;\n";
-        o << "  Tc[cand] = T;\n  Edc[cand] = ed;\n";
-        if (npk1 % 64) o << "  Ebc[cand] = eb;\n";
+        // the running makespan and energy are read back and added to by the next kernel: only
+        // the lane that owns the candidate stores them (a lane past the batch repeats candidate
+        // B - 1 in another wave that may run after its owner's store, and would add twice)
+        o << "  if (active) {\n    Tc[cand] = T;\n    Edc[cand] = ed;\n";
+        if (npk1 % 64) o << "    Ebc[cand] = eb;\n";
+        o << "  }\n";
     } else {
         emit_forward_finish(o, g, lp, j > 0);
-        o << "  Tc[cand] = T;\n"
+        o << "  if (active) Tc[cand] = T;\n"
              "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n"
              "  if (mask || part) emo_select_block(blockIdx.x, active, T, E, cand, B, target, mask, part);\n";
     }

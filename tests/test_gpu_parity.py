@@ -232,6 +232,30 @@ def test_segmented_kernels(torch, emo, case):
         assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), case
 
 
+@pytest.mark.parametrize("B", [3 * 256 + 64, 3 * 256 + 1, 5 * 256 + 192])
+def test_segmented_kernels_ragged_last_workgroup(torch, emo, B):
+    """Batches that end one wave (or one lane) into a 256-thread workgroup of the segmented
+    forward kernels: the workgroup's remaining waves hold only lanes past the batch, which
+    repeat candidate B - 1.  Its running makespan and energy, read back and added to by the next
+    kernel, must be stored once; every row, B - 1 included, against the oracle."""
+    g = without_cuts(synth.packed_graph(2400 + 16, 2400, 8, 16, sync_every=128, cross_p=0.05))
+    rng = np.random.default_rng(B)
+    rows = pins.random_rows(rng, g, B)
+    print(f"[case] segmented ragged B={B}: V={g.num_nodes} P={g.num_packs}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    lv = dev(torch, rows)
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    for rep in range(3):
+        T, E = gh.eval_policies(lv)
+        torch.cuda.synchronize()
+        assert gh.info()["last_kernels"] == 2, gh.info()
+        parity.assert_eval(host(T), host(E), T_or, E_or, True, f"segmented ragged B={B} rep={rep}")
+    tgt = float(np.float32(np.median(T_or)))
+    res, mask = gh.select_policy(lv, tgt)
+    parity.assert_selection(emo.parse_selection(res), emo.unpack_mask(mask, B), T_or, E_or, tgt,
+                            True, f"segmented ragged B={B} select")
+
+
 CUT_CASES = {
     # name: (packs, streams, levels, packs between synchronisations, segments)
     "sync-256-F16": (1024, 8, 16, 256, 4),   # 256-pack segments, as in the 4096-pack workload
