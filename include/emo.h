@@ -132,6 +132,11 @@ typedef struct {
                                      graphs too large for one specialised kernel use them
                                      when levels (and slack) are 16-byte aligned and fewer
                                      than 2^30 candidates are evaluated. */
+    int32_t hip_runtime_version;  /* hipRuntimeGetVersion of the HIP runtime the library runs
+                                     on (e.g. 70051831 for 7.0.51831).  The run-time compiler
+                                     of the specialised kernels is the hiprtc of that same
+                                     runtime, so this also names the compiler that builds
+                                     them. */
 } emo_graph_info;
 
 /* Which kernels evaluate a graph.

@@ -1143,6 +1143,8 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     g->cut_plan = emo::jit_cut_plan(g->jg, cut_steps(*g, sf), kCutMaxPacks, kCutSubPacks);
     g->cut_ok = g->cut_plan.segments() >= 2 && nops <= kChainMaxOps && exact_time_sums(*g, pack_time);
     in.cut_segments = g->cut_ok ? g->cut_plan.segments() : 0;
+    int rt = 0;
+    in.hip_runtime_version = hipRuntimeGetVersion(&rt) == hipSuccess ? rt : 0;
 
     if (device >= 0) {
         DeviceGuard guard(device);

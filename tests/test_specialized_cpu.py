@@ -27,6 +27,15 @@ def hiprtc():
     return ctypes.CDLL("libhiprtc.so")
 
 
+def compiler_runtime() -> int:
+    """hipRuntimeGetVersion of the runtime whose hiprtc the tests compile with (the one the
+    library uses: torch's, loaded first)."""
+    rt = ctypes.c_int(0)
+    lib = ctypes.CDLL("libamdhip64.so")
+    assert lib.hipRuntimeGetVersion(ctypes.byref(rt)) == 0
+    return rt.value
+
+
 def compile_source(hiprtc, src: str, tmp_path) -> str:
     prog = ctypes.c_void_p()
     assert hiprtc.hiprtcCreateProgram(ctypes.byref(prog), src.encode(), b"k.hip", 0, None, None) == 0
@@ -80,10 +89,11 @@ def check_code_object(path, expect, spill_ok=()):
         if any(name.startswith(p) for p in spill_ok):
             assert vgpr <= 128, (name, vgpr)
             n_scr = sum("scratch_" in l for l in bodies[name])
-            if len(bodies[name]) // 100 < n_scr <= len(bodies[name]) // 20:
-                pytest.xfail(f"{name}: {n_scr} scratch accesses under torch's bundled hiprtc "
-                             "(ROCm 7.0), the compiler the library uses once torch is loaded "
-                             "first; within 1% under ROCm 7.2's")
+            if (compiler_runtime() < 70200000 and
+                    len(bodies[name]) // 100 < n_scr <= len(bodies[name]) // 20):
+                pytest.xfail(f"{name}: {n_scr} scratch accesses under the hiprtc of HIP runtime "
+                             f"{compiler_runtime()} (ROCm 7.0, torch's bundle); the bound is "
+                             "met under ROCm 7.2's")
             assert n_scr <= len(bodies[name]) // 100, f"{name}: {n_scr} scratch accesses"
         else:
             assert spill == 0, f"{name} spills {spill} VGPRs"
