@@ -429,6 +429,17 @@ def config_policies(k: int, graph: Graph, start: int = 0, count: int | None = No
     return random_policies(spec.policy_seed, graph.num_packs, graph.num_levels, start, count, dist)
 
 
+def bench_policies(k: int, graph: Graph, workers: int = 8) -> np.ndarray:
+    """The whole candidate batch of workload `k` as the benchmark step evaluates it, all-max
+    policy first: the tiny workload's exhaustive space in reverse mixed-radix order, the others'
+    seeded mixture batch."""
+    spec = CONFIGS[k]
+    if spec.exhaustive:
+        return np.ascontiguousarray(config_policies(k, graph)[::-1])
+    return random_policies_parallel(spec.policy_seed, graph.num_packs, graph.num_levels,
+                                    spec.num_candidates, workers=workers)
+
+
 def sample_rows(num_candidates: int, n: int, seed: int = 7) -> np.ndarray:
     """A seeded sample of candidate rows that always includes the first and last rows."""
     rng = np.random.default_rng(seed)
