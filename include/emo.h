@@ -251,6 +251,25 @@ emo_status emo_select_from_results(const float *makespan, const float *energy,
                                    uint32_t *feasible_mask, emo_selection *result, void *stream);
 
 /*
+ * emo_select_from_results without any allocation, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, outputs and results as emo_select_from_results.  Its selection partial
+ * records (16 bytes per 1024 candidates) live in a static 4 MiB device array that each GPU the
+ * library runs on holds until the process ends; the call allocates and frees nothing.  The
+ * first call on a device looks up that device's address of the array (hipGetSymbolAddress).
+ *   num_candidates  0 <= B <= 268,435,456 (2^28, the records the array holds); a larger B is
+ *                   EMO_ERR_INVALID_ARGUMENT and launches nothing.
+ * Every call on one GPU shares that GPU's array (nothing in it needs to start cleared: each
+ * call writes every record it reads).  Calls that overlap on one GPU (on different streams
+ * with no ordering between them, or from several threads) race on it and may return a wrong
+ * selection; calls ordered on one stream are safe.
+ */
+emo_status emo_select_from_results_noalloc(const float *makespan, const float *energy,
+                                           int64_t num_candidates, float latency_target,
+                                           uint32_t *feasible_mask, emo_selection *result,
+                                           void *stream);
+
+/*
  * Time-interval frequency policies: the general policy form P = {<T_i, F_i>} of the optimisation
  * problem (Sec. IV-A) as Alg. 1 evaluates it.  The batch shares K = num_intervals intervals
  * [T_i, T_{i+1}) with T_0 = 0, T_i = change_points[i - 1] and the last interval open-ended; each

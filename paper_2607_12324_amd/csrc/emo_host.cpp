@@ -1483,6 +1483,36 @@ emo_status emo_select_from_results(const float *makespan, const float *energy, i
     return after_launch(e, "emo_select_from_results");
 }
 
+emo_status emo_select_from_results_noalloc(const float *makespan, const float *energy,
+                                           int64_t B, float latency_target,
+                                           uint32_t *feasible_mask, emo_selection *result,
+                                           void *stream) {
+    if (B < 0 || B > emo::noalloc_max_candidates())
+        return fail(EMO_ERR_INVALID_ARGUMENT,
+                    "num_candidates %lld outside [0, %lld], the batch the static scratch covers",
+                    (long long)B, (long long)emo::noalloc_max_candidates());
+    if (!result) return fail(EMO_ERR_INVALID_ARGUMENT, "result is NULL");
+    if (reinterpret_cast<uintptr_t>(result) % 8) return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
+    if (B > 0 && (!makespan || !energy)) return fail(EMO_ERR_INVALID_ARGUMENT, "makespan/energy is NULL");
+    if (std::isnan(latency_target)) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (B == 0) return after_launch(emo::launch_empty_result(result, st), "emo_select_from_results_noalloc");
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= emo::kNoAllocMaxDevices)
+        return fail(EMO_ERR_DEVICE, "no usable current device (%d)", dev);
+    void *part = nullptr;
+    e = emo::noalloc_scratch(dev, &part);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(EMO_ERR_DEVICE, "static scratch of device %d: %s", dev, hipGetErrorString(e));
+    }
+    // every partial record is written before the finalize reads it: nothing needs clearing
+    e = emo::launch_select_results(makespan, energy, B, latency_target, feasible_mask, part, st);
+    if (e == hipSuccess) e = emo::launch_select_finalize(part, emo::select_results_blocks(B), result, st);
+    return after_launch(e, "emo_select_from_results_noalloc");
+}
+
 }  // extern "C"
 
 namespace {

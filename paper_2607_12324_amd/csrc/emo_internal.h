@@ -112,6 +112,11 @@ hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selectio
 // Stage 1 of a selection from stored makespans and energies (select_results_blocks(B)
 // partials: one per 1024 candidates).
 int64_t select_results_blocks(int64_t B);
+// The static selection scratch of emo_select_from_results_noalloc: the largest batch its
+// records cover, and the current device's address of it (looked up once per device).
+constexpr int kNoAllocMaxDevices = 64;
+int64_t noalloc_max_candidates();
+hipError_t noalloc_scratch(int dev, void **out);
 hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
                                  uint32_t *mask, void *part, hipStream_t s);
 

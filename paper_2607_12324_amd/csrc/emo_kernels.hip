@@ -24,8 +24,17 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "emo_internal.h"
 #include "emo_select.h"
+
+// Selection partial records of emo_select_from_results_noalloc, one 16-byte record per group
+// of candidates: a static array each device holds until the process ends.  In host code its
+// name is not a device address; host code reaches it only through the address that
+// hipGetSymbolAddress returns for the current device (emo::noalloc_scratch below).
+constexpr size_t kNoAllocScratchBytes = size_t(4) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 
 namespace emo {
 namespace {
@@ -830,6 +839,26 @@ hipError_t launch_select_results(const float *T, const float *E, int64_t B, floa
     hipLaunchKernelGGL(select_results_kernel, dim3(static_cast<unsigned>(select_results_blocks(B))), dim3(kBlock),
                        0, s, T, E, B, target, mask, static_cast<EmoPartial *>(part), vec);
     return hipGetLastError();
+}
+
+int64_t noalloc_max_candidates() {
+    return static_cast<int64_t>(kNoAllocScratchBytes / kPartialBytes) * kSelGroup;
+}
+
+hipError_t noalloc_scratch(int dev, void **out) {
+    static std::mutex mu;
+    static void *addr[kNoAllocMaxDevices] = {};
+    if (dev < 0 || dev >= kNoAllocMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        // the caller has made `dev` current: this is that device's copy of the array
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
 }
 
 }  // namespace emo

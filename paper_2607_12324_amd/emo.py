@@ -23,7 +23,7 @@ STATUS_NAMES = {0: "EMO_OK", 1: "EMO_ERR_INVALID_ARGUMENT", 2: "EMO_ERR_CYCLE",
 ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_kernel_mode", "emo_graph_topo_order",
                 "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
-                "emo_select_from_results", "emo_dp_search", "emo_eval_intervals",
+                "emo_select_from_results", "emo_select_from_results_noalloc", "emo_dp_search", "emo_eval_intervals",
                 "emo_graph_set_timing_events", "emo_pack_kernels", "emo_contract_packs",
                 "emo_pack_model",
                 "emo_graph_specialized_source",
@@ -76,6 +76,7 @@ def _load_library():
         "emo_select_policy": [P, P, i64, f32, P, P, P],
         "emo_evaluate": [P, P, i64, P, P, P, i32, f32, P, P, P],
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
+        "emo_select_from_results_noalloc": [P, P, i64, f32, P, P, P],
         "emo_dp_search": [P, f32, f32, P, i32, P, P, P],
         "emo_eval_intervals": [P, P, i64, i32, P, P, P, P, f32, P, P, P],
         "emo_graph_specialized_source": [P, P, P],
@@ -336,6 +337,19 @@ def select_from_results(makespan, energy, latency_target: float, mask=None, resu
                                        float(latency_target),
                                        _dptr(mask, torch.int32, (B + 31) // 32, "mask"),
                                        _dptr(result, torch.int64, 3, "result"), _stream(stream)))
+    return result, mask
+
+
+def select_from_results_noalloc(makespan, energy, latency_target: float, mask, result,
+                                stream=None):
+    """emo_select_from_results_noalloc: the same selection with the library's static scratch;
+    the caller passes every output (nothing is allocated here or in the library)."""
+    import torch
+    B = int(makespan.numel())
+    _check(lib.emo_select_from_results_noalloc(
+        _dptr(makespan, torch.float32, B, "makespan"), _dptr(energy, torch.float32, B, "energy"), B,
+        float(latency_target), _dptr(mask, torch.int32, (B + 31) // 32, "mask"),
+        _dptr(result, torch.int64, 3, "result"), _stream(stream)))
     return result, mask
 
 
