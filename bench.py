@@ -1,14 +1,16 @@
 """Benchmark: batched what-if evaluation of DVFS frequency policies on one MI355X.
 
-One step is the whole hot path over one batch of candidate policies.  The default workload is
-the inference-like trace (64 packs on one stream, 64 host launch nodes, 8 frequency levels,
-2^20 candidates); its step is one emo_evaluate launch that computes, for every candidate, the
-forward pass (finish times, makespan, energy), the backward pass (slack of every pack) and the
-feasibility mask and least-energy feasible candidate under the latency target 1.05 x the
-all-max makespan.  Workloads with a second target re-select it from the stored makespans and
-energies (emo_select_from_results); workloads without slack skip the backward pass.
-Inputs are resident in HBM before timing starts; level batches rotate over several copies so
-that the 256 MB last-level cache does not hold them across steps.
+One step is the whole hot path over one batch of candidate policies: one emo_evaluate launch
+that computes, for every candidate, the forward pass (finish times, makespan, energy), the
+backward pass (slack of every pack) when the workload has it, and the feasibility mask and
+least-energy feasible candidate under the first latency target; workloads with a second target
+re-select it from the stored makespans and energies (emo_select_from_results).
+
+By default all five workloads run one after another.  The headline is the largest one that fits
+one GPU, the per-kernel graph of 65,536 kernels and 65,536 host nodes (2^14 candidates,
+forward and backward for every candidate); the other four are reported under "configs".
+Inputs are resident in HBM before timing starts; level batches that fit rotate over several
+copies so that the 256 MB last-level cache does not hold them across steps.
 
 Prints one JSON line.  `value` is candidate policies fully evaluated per second.
 """
@@ -26,6 +28,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "candidate policies evaluated/sec (timing+energy+select); % of VALU/HBM roofline"
+HEADLINE = 5            # the largest workload: 65,536 kernels + 65,536 host nodes, slack
 HBM_PEAK_GBS = 8000.0
 VALU_PEAK_TOPS = 39.3   # 256 CUs x 64 fp32 lanes x 2.4 GHz, one op per lane per clock (no packed math)
 
@@ -65,36 +68,114 @@ def measured_traffic(workload_name: str, kernel: str, src_hash: str):
     return float(fields["hbm_bytes_per_launch"])
 
 
-def cpu_baseline(k: int, budget_s: float = 12.0):
-    """The oracle (plain fp64 C, one thread) on a bounded prefix of the same workload, doing the
-    same work per candidate as the step: makespan and energy, slack of every pack when the
-    workload has it, and the selection for each target."""
+def host_cpu():
+    """Host facts for the CPU baseline: logical CPUs, the CPUs this process may run on, the
+    threads the baseline uses (the box's share: OMP_NUM_THREADS, else the affinity set) and the
+    CPU model."""
+    n_aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or n_aff
+    threads = max(1, min(threads, n_aff))
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity": n_aff, "threads": threads, "model": model}
+
+
+def cpu_baseline(k, g, rows, out, targets, budget_s: float = 20.0):
+    """The oracle (plain fp64 C) on the host: the whole candidate batch (or, beyond the budget,
+    a leading prefix) on all the threads this process may use, doing the step's work per
+    candidate (makespan and energy, slack of every pack when the step has it, the selection
+    for each target), then a bounded one-thread run.  The oracle's outputs are compared with
+    the step's device outputs `out` (parity statistics); only the oracle calls are timed."""
     import numpy as np
 
     import oracle
-    from paper_2607_12324_amd import synth
+    from paper_2607_12324_amd import emo, synth
     oracle.build()
     spec = synth.CONFIGS[k]
-    g = synth.config_graph(k)
-    n = max(16, min(2048, 2_000_000 // max(1, g.num_nodes + g.num_edges)))
-    rows = synth.config_policies(k, g, 0, n)
-    t0 = time.perf_counter()
+    B, P = rows.shape
+    hc = host_cpu()
+    nt = hc["threads"]
+    # pieces of at most 2^27 slack values (1 GiB of fp64) or 2^16 rows
+    step = max(1, min(1 << 16, (1 << 27) // max(1, P))) if spec.slack else 1 << 18
+    T_or = np.empty(B)
+    E_or = np.empty(B)
+    t_oracle = 0.0
     done = 0
-    while True:
-        T, E = oracle.eval_batch(g, rows, nthreads=1)
+    s_max_err, s_bad, s_rows = 0.0, 0, 0
+    while done < B:
+        n = min(step, B - done)
+        blk = rows[done:done + n]
+        t = time.perf_counter()
         if spec.slack:
-            for c in range(n):
-                oracle.pack_slack(g, rows[c])
-        for r in spec.targets:
-            oracle.select(T, E, float(np.float32(r * T[0])))
+            T_b, E_b, S_b = oracle.slack_batch(g, blk, nthreads=nt)
+        else:
+            T_b, E_b = oracle.eval_batch(g, blk, nthreads=nt)
+        t_oracle += time.perf_counter() - t
+        T_or[done:done + n], E_or[done:done + n] = T_b, E_b
+        if spec.slack:
+            S_d = out["S"][done:done + n].cpu().numpy().astype(np.float64)
+            ok = ~np.isnan(S_b)
+            s_bad += int(np.count_nonzero(np.isnan(S_d) != ~ok))
+            err = np.abs(S_d[ok] - S_b[ok]) / np.repeat(np.maximum(T_b, 1e-30), P).reshape(n, P)[ok]
+            s_max_err = max(s_max_err, float(err.max()) if err.size else 0.0)
+            s_rows += n
+            del S_d, S_b
         done += n
-        if time.perf_counter() - t0 >= budget_s:
+        if t_oracle > budget_s:
             break
-    dt = time.perf_counter() - t0
-    what = "eval + pack slack + select" if spec.slack else "eval + select"
-    return {"value": done / dt, "unit": "policies/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {n} candidates of the same batch, repeated {done // n}x for {dt:.1f} s "
-                      f"({what} x{len(spec.targets)} target(s), fp64 C, 1 thread)"}
+    n_or = done
+    t = time.perf_counter()
+    sels = [oracle.select(T_or[:n_or], E_or[:n_or], tgt) for tgt in targets]
+    t_oracle += time.perf_counter() - t
+    # parity of the step's outputs over the rows the oracle evaluated
+    Td = out["T"][:n_or].cpu().numpy().astype(np.float64)
+    Ed = out["E"][:n_or].cpu().numpy().astype(np.float64)
+    parity = {"rows": n_or, "of": B,
+              "makespan_max_rel_err": float(np.max(np.abs(Td - T_or[:n_or]) / T_or[:n_or])),
+              "makespan_mismatches": int(np.count_nonzero(Td != T_or[:n_or])),
+              "energy_max_rel_err": float(np.max(np.abs(Ed - E_or[:n_or]) / E_or[:n_or]))}
+    if spec.slack:
+        parity.update({"slack_rows": s_rows, "slack_max_err_over_makespan": s_max_err,
+                       "slack_nan_mismatches": s_bad})
+    agree = []
+    for tgt, (idx, feas, nf), m, r in zip(targets, sels, out["masks"], out["results"]):
+        if n_or == B:
+            bits = emo.unpack_mask(m, B)
+            sel = emo.parse_selection(r)
+        else:   # a prefix: re-select the device outputs over the same prefix
+            r2, m2 = emo.select_from_results(out["T"][:n_or], out["E"][:n_or], tgt)
+            bits, sel = emo.unpack_mask(m2, n_or), emo.parse_selection(r2)
+        best = E_or[idx] if idx >= 0 else np.nan
+        near = feas & (np.abs(E_or[:n_or] - best) <= 1e-5 * best) if idx >= 0 else feas & False
+        agree.append({"target": tgt, "oracle_index": idx, "index": sel.index,
+                      "agree": bool(sel.index == idx or (idx >= 0 and 0 <= sel.index < n_or and near[sel.index])),
+                      "oracle_feasible": nf, "feasible": sel.num_feasible,
+                      "mask_mismatches": int(np.count_nonzero(bits != feas))})
+    parity["selection"] = agree
+    # one thread on a bounded prefix
+    n1 = max(1, min(B, int(n_or / max(t_oracle, 1e-9) / nt * 2.0)))
+    t = time.perf_counter()
+    if spec.slack:
+        oracle.slack_batch(g, rows[:n1], nthreads=1)
+    else:
+        oracle.eval_batch(g, rows[:n1], nthreads=1)
+    t1 = time.perf_counter() - t
+    what = "makespan + energy + slack of every pack" if spec.slack else "makespan + energy"
+    base = {"value": n_or / t_oracle, "unit": "policies/s", "cores": nt, "kind": "oracle",
+            "sample": (f"{'the whole batch' if n_or == B else f'the first {n_or} of {B} candidates'} "
+                       f"({what}, selection at {len(targets)} target(s); fp64 C) on {nt} threads "
+                       f"in {t_oracle:.2f} s"),
+            "host": hc,
+            "one_thread": {"value": n1 / t1, "unit": "policies/s", "cores": 1,
+                           "sample": f"the first {n1} candidates, {what}, in {t1:.2f} s"}}
+    return base, parity
 
 
 def run_dp(args, emo, synth, np, torch):
@@ -387,7 +468,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2, help="benchmark workload 1..5 (default 2)")
+    ap.add_argument("--workload", type=int, default=0,
+                    help="one benchmark workload 1..5; default 0: all five, the largest "
+                         "(65,536 kernels) as the headline and the others under 'configs'")
     ap.add_argument("--copies", type=int, default=5, help="rotated copies of the level batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--time-every", type=int, default=8,
@@ -430,6 +513,8 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n, "launches": args.steps}))
         return
 
+    if (args.dp or args.intervals or args.pack or args.model) and args.workload == 0:
+        args.workload = 2
     if args.dp:
         run_dp(args, emo, synth, np, torch)
         return
@@ -443,23 +528,57 @@ def main():
         run_model(args, emo, synth, np, torch)
         return
 
-    k = args.workload
+    ks = [1, 2, 3, 4, 5] if args.workload == 0 else [args.workload]
+    head = HEADLINE if args.workload == 0 else args.workload
+    recs = {}
+    t_all = time.perf_counter()
+    for k in ks:
+        recs[k] = run_workload(k, args, emo, synth, np, torch)
+        print(f"# workload {k} done: {recs[k]['ms_per_step']:.4f} ms/step, "
+              f"{recs[k]['value']:.4g} policies/s", file=sys.stderr, flush=True)
+    h = recs[head]
+    out = {
+        "metric": METRIC,
+        "value": h["value"],
+        "unit": "policies/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": h["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": h["config"],
+        "roofline": h["roofline"],
+        "cpu_baseline": h.get("cpu_baseline"),
+        "parity": h.get("parity"),
+        "selected": h["selected"],
+        "compile_seconds": h["compile_seconds"],
+        "hip_runtime_version": h["hip_runtime_version"],
+        "kernel_source_hash": h["kernel_source_hash"],
+        "configs": {synth.CONFIGS[k].name: {x: v for x, v in recs[k].items() if x != "config"} |
+                    {"config": recs[k]["config"]} for k in ks if k != head},
+        "wall_s": time.perf_counter() - t_all,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_workload(k, args, emo, synth, np, torch):
+    """One workload's step timed over args.steps steps (after args.warmup), its roofline, and,
+    unless disabled, the oracle baseline with parity statistics.  Frees its device memory."""
     spec = synth.CONFIGS[k]
     g = synth.config_graph(k)
     B = spec.num_candidates
     P = g.num_packs
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
-    if spec.exhaustive:
-        rows = synth.config_policies(k, g)
-        rows = np.ascontiguousarray(rows[::-1])   # all-max row first
-    else:
-        rows = synth.random_policies_parallel(spec.policy_seed, P, g.num_levels, B, workers=8)
+    rows = synth.bench_policies(k, g)
     copies = max(1, args.copies if B * P < (1 << 30) else 1)
     lv = [torch.from_numpy(rows).to(dev)]
     for _ in range(copies - 1):
         lv.append(lv[0].clone())
-    del rows
     gh = emo.EmoGraph(g, device=0)
     stream = torch.cuda.current_stream()
     T = torch.empty(B, dtype=torch.float32, device=dev)
@@ -467,7 +586,8 @@ def main():
     S = torch.empty((B, P), dtype=torch.float32, device=dev) if spec.slack else None
     masks = [torch.empty((B + 31) // 32, dtype=torch.int32, device=dev) for _ in spec.targets]
     results = [torch.empty(3, dtype=torch.int64, device=dev) for _ in spec.targets]
-    T0, _ = gh.eval_policies(lv[0][:1])
+    t_c = time.perf_counter()
+    T0, _ = gh.eval_policies(lv[0][:1])       # row 0 is the all-max policy
     targets = [float(np.float32(r * float(T0.item()))) for r in spec.targets]
 
     def main_call(x):
@@ -479,37 +599,48 @@ def main():
         for j in range(1, len(targets)):
             emo.select_from_results(T, E, targets[j], mask=masks[j], result=results[j])
 
+    step(0)                                   # compiles the specialised kernels if any
+    torch.cuda.synchronize()
+    first_call_s = time.perf_counter() - t_c
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    every = max(1, args.time_every)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(0, args.steps, every)]
-    for a, b in ev:   # create the underlying HIP events
-        a.record(stream)
-        b.record(stream)
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    start.record(stream)
-    for i in range(args.steps):
-        # the library records the pair right around the kernel that evaluates the candidates
-        if i % every == 0:
-            gh.set_timing_events(ev[i // every][0], ev[i // every][1])
-        elif i % every == 1:
-            gh.set_timing_events(None, None)
-        main_call(lv[i % copies])
-        for j in range(1, len(targets)):
-            emo.select_from_results(T, E, targets[j], mask=masks[j], result=results[j])
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall
-    gh.set_timing_events(None, None)
-    ms_total = start.elapsed_time(end)
-    ms_step = ms_total / args.steps
-    main_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    def timed(copies_used):
+        every = max(1, args.time_every)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(0, args.steps, every)]
+        for a, b in ev:   # create the underlying HIP events
+            a.record(stream)
+            b.record(stream)
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        start.record(stream)
+        for i in range(args.steps):
+            # the library records the pair right around the kernel(s) evaluating the candidates
+            if i % every == 0:
+                gh.set_timing_events(ev[i // every][0], ev[i // every][1])
+            elif i % every == 1:
+                gh.set_timing_events(None, None)
+            main_call(lv[i % copies_used])
+            for j in range(1, len(targets)):
+                emo.select_from_results(T, E, targets[j], mask=masks[j], result=results[j])
+        end.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t_wall
+        gh.set_timing_events(None, None)
+        return (start.elapsed_time(end) / args.steps,
+                float(np.mean([a.elapsed_time(b) for a, b in ev])), len(ev), wall)
+
+    ms_step, main_ms, n_ev, wall = timed(copies)
+    cache = None
+    if copies > 1:
+        # the same step on one resident input copy (a small batch then stays in the 256 MB
+        # last-level cache across steps)
+        ms1, main1, _, _ = timed(1)
+        cache = {"ms_per_step": ms1, "value": B / (ms1 / 1e3), "launch_ms": main1}
     sels = [emo.parse_selection(r) for r in results]
     info = gh.info()
 
@@ -523,32 +654,11 @@ def main():
     ops_per_cand = (info["num_dynamic_edges"] + 2 * P + 2) * (2 if spec.slack else 1)
     valu_tops = B * ops_per_cand / (main_ms / 1e3) / 1e12
     src_hash = kernel_source_hash(info["last_kernels"])
-    if info["last_kernels"] == 2:      # segmented kernels: the timed unit is the whole chain
-        kname = "emo_chain"
-    elif info["last_kernels"] == 3:
-        kname = "chains_kernel"
-    elif info["last_kernels"] == 4:
-        kname = "chains_windowed"
-    elif info["last_kernels"] == 5:    # cut-segment kernels and their last kernel, as one unit
-        kname = "emo_cut"
-    elif info["last_kernels"] == 1:
-        kname = "emo_sp_slack" if spec.slack else "emo_sp_select"
-    else:
-        kname = "slack_kernel" if spec.slack else "forward_kernel"
+    kname = kernel_name(info["last_kernels"], spec.slack)
     traffic = measured_traffic(spec.name, kname, src_hash)
-    out = {
-        "metric": METRIC,
+    rec = {
         "value": value,
-        "unit": "policies/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": ms_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
         "config": {"workload": spec.name, "candidates": B, "nodes": g.num_nodes,
                    "edges": g.num_edges, "packs": P, "levels": g.num_levels,
                    "target_ratios": list(spec.targets), "slack": spec.slack,
@@ -556,21 +666,38 @@ def main():
                    "rotated_input_copies": copies},
         "roofline": {"bound": "hbm", "kernel": kname, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "algorithmic_bytes_per_launch": algo_bytes,
-                     "launch_ms": main_ms, "timed_launches": len(ev),
+                     "traffic": traffic,
+                     "traffic_ratio": None if traffic is None else traffic / algo_bytes,
+                     "algorithmic_bytes_per_launch": algo_bytes,
+                     "launch_ms": main_ms, "timed_launches": n_ev,
                      "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Tops/s",
                               "frac": valu_tops / VALU_PEAK_TOPS,
                               "algorithmic_ops_per_candidate": ops_per_cand}},
-        "wall_s": wall,
+        "cache_resident": cache,
         "selected": [{"target": t, "index": x.index, "energy": x.energy, "makespan": x.makespan,
                       "num_feasible": x.num_feasible} for t, x in zip(targets, sels)],
-        "specialized_kernels": bool(info["specialized"] & 1),
+        "kernels": info["last_kernels"],
+        "compile_seconds": info["compile_seconds"],
+        "first_call_s": first_call_s,
+        "hip_runtime_version": info["hip_runtime_version"],
         "kernel_source_hash": src_hash,
+        "timed_wall_s": wall,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(k)
-    print(json.dumps(out), flush=True)
+        out = {"T": T, "E": E, "S": S, "masks": masks, "results": results}
+        rec["cpu_baseline"], rec["parity"] = cpu_baseline(k, g, rows, out, targets)
+    del lv, S, T, E, rows
+    gh.close()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rec
 
+
+def kernel_name(kind: int, slack: bool) -> str:
+    """The evaluating kernel (or chain of kernels timed as one unit) of a kernel kind."""
+    return {2: "emo_chain", 3: "chains_kernel", 4: "chains_windowed", 5: "emo_cut",
+            1: "emo_sp_slack" if slack else "emo_sp_select"}.get(
+                kind, "slack_kernel" if slack else "forward_kernel")
 
 if __name__ == "__main__":
     main()
