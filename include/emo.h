@@ -105,7 +105,10 @@ typedef struct {
                                      3 chain lanes (one lane per chain and candidate),
                                      4 windowed chain lanes (a wave per chain, 64 candidates;
                                      pack windows staged in LDS), 5 cut segments (the
-                                     segments between cut nodes evaluated in parallel) */
+                                     segments between cut nodes evaluated in parallel),
+                                     6 two-pass chain scan (windowed chain lanes whose slack
+                                     comes from a second forward pass, for chains with exact
+                                     time sums) */
     int32_t chain_lanes;          /* lanes per candidate of the chain-lane kernels, 0 when the
                                      candidate-dependent nodes do not form at most 64 disjoint
                                      chains */
@@ -132,6 +135,13 @@ typedef struct {
                                      graphs too large for one specialised kernel use them
                                      when levels (and slack) are 16-byte aligned and fewer
                                      than 2^30 candidates are evaluated. */
+    int32_t chain_scan_window;    /* packs per window of the two-pass chain scan kernel
+                                     (last_kernels 6), 0 when it does not apply: the
+                                     candidate-dependent nodes must form at most 16 disjoint
+                                     chains visiting the windows in increasing order, P a
+                                     multiple of 16, and every time sum exact as for
+                                     cut_segments; calls use it when levels and slack are
+                                     16-byte aligned */
     int32_t hip_runtime_version;  /* hipRuntimeGetVersion of the HIP runtime the library runs
                                      on (e.g. 70051831 for 7.0.51831).  The run-time compiler
                                      of the specialised kernels is the hiprtc of that same

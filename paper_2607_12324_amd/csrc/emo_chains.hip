@@ -399,7 +399,9 @@ __host__ __device__ inline WinLayout win_layout(int W, int NC, int F, int nwaves
     L.off_tfin = L.off_bad + 4u * static_cast<uint32_t>(NC);
     L.off_blk = round16u(L.off_tfin + 4u * static_cast<uint32_t>(NC));
     L.off_x = L.off_blk + 2u * static_cast<uint32_t>(blk_bytes);
-    L.tab_elems = static_cast<uint32_t>(W + 1) * static_cast<uint32_t>(F);
+    // entries per table buffer, a multiple of 4 so that the second buffer starts 16-byte
+    // aligned for its 16-byte stores (with fp32 or float2 entries)
+    L.tab_elems = (static_cast<uint32_t>(W + 1) * static_cast<uint32_t>(F) + 3u) & ~3u;
     // (256 spare float2 entries: a lookup with an invalid level byte reads at most 255 entries
     // past a table buffer; the backward tables are followed by the slack tile)
     const uint32_t fwd = (2u * L.tab_elems + 256u) * 8u;
@@ -430,6 +432,13 @@ __device__ __forceinline__ uint32_t bad_levels(uint32_t x, uint32_t addf) {
 __device__ __forceinline__ float fmax_nonneg(float a, float b) {
     const unsigned x = __float_as_uint(a), y = __float_as_uint(b);
     return __uint_as_float(x > y ? x : y);
+}
+
+// max(a, b) for a >= 0 and any finite b: non-negative floats order like their bit patterns as
+// signed integers, and negative ones lie below every non-negative pattern.
+__device__ __forceinline__ float fmax_lo(float a, float b) {
+    const int x = __float_as_int(a), y = __float_as_int(b);
+    return __int_as_float(x > y ? x : y);
 }
 
 struct WinArgs {
@@ -590,7 +599,17 @@ struct WinGroup {
     }
 };
 
-template <bool SLACK, bool FIXED>
+// SCAN (graphs whose time sums are exact: every time a multiple of one power of two u and every
+// path below 2^24 u, so every sum and difference below is exact in fp32 in any order): slack
+// comes from a second forward pass instead of the backward one.  Along a chain with durations
+// d_j and start floors cst_j, a step's only successor is the next step, so its latest finish is
+// the makespan minus the durations after it; with Pre_i = d_1 + ... + d_i and Tot = Pre_n,
+//   slack_i = LFT_i - EFT_i = (T - Tot) - (EFT_i - Pre_i),
+// and D_i = EFT_i - Pre_i obeys D_i = max(D_{i-1}, cst_i - Pre_{i-1}), D_0 = 0, because
+// EFT_i = max(EFT_{i-1}, cst_i) + d_i.  The forward pass also sums Tot per chain; the second
+// pass walks the windows again for D and writes slack = K - D, K = T - Tot, through the tile.
+// No finish time is checkpointed or recomputed backwards.
+template <bool SLACK, bool FIXED, bool SCAN>
 __global__ void __launch_bounds__(kChainBlockThreads)
 chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ blocks,
                 const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ To,
@@ -634,13 +653,13 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     lds_barrier();
     win_store(a, lds, 0, tab2, 8, bad, addf, s0);
     lds_barrier();
-    float f = 0.f;
+    float f = 0.f, pre = 0.f;
     double ed = 0.0;
     // window w from buffer w & 1; `ld` takes window w + 2, `cm` holds window w + 1
     auto forward_window = [&](int w, WinSet &ld, WinSet &cm) {
         const int buf = w & 1;
         win_load(a, levels, g.tab, 8, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
-        if (SLACK) ck[(static_cast<int64_t>(w) * nc + ch) * pitch + gc] = f;
+        if (SLACK && !SCAN) ck[(static_cast<int64_t>(w) * nc + ch) * pitch + gc] = f;
         const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
         const char *tb = reinterpret_cast<const char *>(tab2 + buf * L.tab_elems);
         const ChainWinStep *rs = recs(buf);
@@ -663,6 +682,10 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
                 f = fmax_nonneg(f, A.cst[i]) + te[i].x;
                 if (FIXED) f += A.dur[i];
                 eb += te[i].y;
+                if (SLACK && SCAN) {
+                    pre += te[i].x;
+                    if (FIXED) pre += A.dur[i];
+                }
             }
         };
         WinGroup<FIXED> G0, G1, G2;
@@ -711,11 +734,95 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     if (!SLACK) return;
     lds_barrier();
 
-    // ------------------------------------------------------------------ backward
+    const int per_row = W >> 2;                             // float4 pieces per tile row
+    // slack tile of window w -> pack order; a wave covers 4 candidates x 16 pieces when rows
+    // are long enough (conflict-free LDS reads with the odd row pitch), else whole rows
+    auto flush_tile = [&](int w) {
+        const int n = a.NC * per_row;
+        for (int q = t; q < n; q += nt) {
+            int r, kk;
+            if (per_row >= 16) {
+                const int j = q & 63, blk = q >> 6, nkb = per_row >> 4;
+                const int rg = blk / nkb, kb = blk - rg * nkb;
+                r = rg * 4 + (j >> 4);
+                kk = kb * 16 + (j & 15);
+            } else {
+                r = q / per_row;
+                kk = q - r * per_row;
+            }
+            const float *src = tile + r * (W + 1) + 4 * kk;
+            const float4 v = make_float4(src[0], src[1], src[2], src[3]);
+            const int64_t row = base + r;
+            const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 4 * kk;
+            if (row < B && col < P) *reinterpret_cast<float4 *>(S + row * P + col) = v;
+        }
+    };
     for (int i = t; i < F; i += nt) {
         tabt[W * F + i] = 0.f;
         tabt[L.tab_elems + W * F + i] = 0.f;
     }
+
+    if (SCAN) {
+        // ---------------------------------------------------------------- second forward pass
+        const float K = tfin[cl] - pre;                     // NaN for a candidate with bad levels
+        float D = 0.f, p2 = 0.f;
+        win_load(a, levels, g.tabt, 4, blocks, base, B, P, 0, s0);
+        win_load(a, levels, g.tabt, 4, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
+        win_store(a, lds, 0, tabt, 4, nullptr, addf, s0);
+        lds_barrier();
+        float *trow = tile + cl * (W + 1);
+        auto scan_window = [&](int w, WinSet &ld, WinSet &cm) {
+            const int buf = w & 1;
+            win_load(a, levels, g.tabt, 4, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
+            const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
+            const char *tb = reinterpret_cast<const char *>(tabt + buf * L.tab_elems);
+            const ChainWinStep *rs = recs(buf);
+            int k0, k1;
+            win_range(a, lds, buf, ch, k0, k1);
+            const int ng = (k1 - k0) >> 2;
+            // group g of 4 steps, pipelined like the forward pass: its times are read while the
+            // next group's level bytes and the records of the group after it are in flight
+            auto stage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int g) {
+                float tt[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    tt[i] = *reinterpret_cast<const float *>(tb + (((A.ct[i] >> 16) + A.lv[i]) << 2));
+                    if (FIXED) tt[i] += A.dur[i];
+                }
+                Bn.levels(lrow);
+                C.read(rs, k0 + 4 * (g + 2));
+                win_issue_point();
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    D = fmax_lo(D, A.cst[i] - p2);
+                    p2 += tt[i];
+                    trow[A.ct[i] & 0xffffu] = K - D;
+                }
+            };
+            WinGroup<FIXED> G0, G1, G2;
+            G0.read(rs, k0);
+            G1.read(rs, k0 + 4);
+            G0.levels(lrow);
+            for (int g = 0; g < ng; g += 3) {
+                stage(G0, G1, G2, g);
+                if (g + 1 >= ng) break;
+                stage(G1, G2, G0, g + 1);
+                if (g + 2 >= ng) break;
+                stage(G2, G0, G1, g + 2);
+            }
+            if (w + 1 < nwin) win_store(a, lds, buf ^ 1, tabt + (buf ^ 1) * L.tab_elems, 4, nullptr, addf, cm);
+            lds_barrier();
+            flush_tile(w);
+            lds_barrier();
+        };
+        for (int w = 0; w < nwin; w += 2) {
+            scan_window(w, s0, s1);
+            if (w + 1 < nwin) scan_window(w + 1, s1, s0);
+        }
+        return;
+    }
+
+    // ------------------------------------------------------------------ backward
     const int top = nwin - 1;
     auto ck_at = [&](int w) { return ck[(static_cast<int64_t>(w) * nc + ch) * pitch + gc]; };
     win_load(a, levels, g.tabt, 4, blocks, base, B, P, top, s0);
@@ -730,7 +837,6 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     // window, the wait would also cover that window's prefetch loads
     asm volatile("" : "+v"(fck));
     float *trow = tile + cl * (W + 1);
-    const int per_row = W >> 2;                             // float4 pieces per tile row
     // window w from buffer w & 1; `ld` takes window w - 2, `cm` holds window w - 1
     auto backward_window = [&](int w, WinSet &ld, WinSet &cm) {
         const int buf = w & 1;
@@ -812,26 +918,7 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
             fnext = cm.ck;
         }
         lds_barrier();
-        // slack tile -> pack order; a wave covers 4 candidates x 16 pieces when rows are long
-        // enough (conflict-free LDS reads with the odd row pitch), else whole rows
-        const int n = a.NC * per_row;
-        for (int q = t; q < n; q += nt) {
-            int r, kk;
-            if (per_row >= 16) {
-                const int j = q & 63, blk = q >> 6, nkb = per_row >> 4;
-                const int rg = blk / nkb, kb = blk - rg * nkb;
-                r = rg * 4 + (j >> 4);
-                kk = kb * 16 + (j & 15);
-            } else {
-                r = q / per_row;
-                kk = q - r * per_row;
-            }
-            const float *src = tile + r * (W + 1) + 4 * kk;
-            const float4 v = make_float4(src[0], src[1], src[2], src[3]);
-            const int64_t row = base + r;
-            const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 4 * kk;
-            if (row < B && col < P) *reinterpret_cast<float4 *>(S + row * P + col) = v;
-        }
+        flush_tile(w);
         lds_barrier();
         asm volatile("" : "+v"(fnext));
         fck = fnext;
@@ -869,6 +956,10 @@ bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int3
     return true;
 }
 
+bool chains_scan_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
+    return c.exact && chains_windowed_ok(c, levels, slack);
+}
+
 bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
     return c.win > 0 && reinterpret_cast<uintptr_t>(levels) % 16 == 0 &&
            reinterpret_cast<uintptr_t>(slack) % 16 == 0;
@@ -884,6 +975,7 @@ int64_t win_grid(const DevChains &c, int64_t B) {
 size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
                             const float *slack_ptr) {
     const bool slack = slack_ptr != nullptr;
+    if (chains_scan_ok(c, levels, slack_ptr)) return 2 * round256(static_cast<size_t>(B) * sizeof(float));
     if (chains_windowed_ok(c, levels, slack_ptr)) {
         const size_t pitch = static_cast<size_t>(win_grid(c, B)) * 64 * c.groups;
         const size_t ck = slack ? round256(static_cast<size_t>(c.nwin) * c.nc * pitch * sizeof(float)) : 0;
@@ -898,7 +990,7 @@ size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t
 }
 
 namespace {
-template <bool SLACK, bool FIXED>
+template <bool SLACK, bool FIXED, bool SCAN>
 hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, const DevGraph &g,
                                   const DevChains &c, const WinArgs &a, const uint8_t *levels, int64_t B,
                                   float *T, float *E, float *S, float *ck, int64_t pitch) {
@@ -909,12 +1001,12 @@ hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, c
     if (e != hipSuccess) return e;
     const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
     if (!bit || !(done.load(std::memory_order_acquire) & bit)) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED>),
+        e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED, SCAN>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kWinLds));
         if (e != hipSuccess) return e;
         done.fetch_or(bit, std::memory_order_acq_rel);
     }
-    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED>), gd, bd, lds, s, g, c, a, c.blocks, levels, B, T, E,
+    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED, SCAN>), gd, bd, lds, s, g, c, a, c.blocks, levels, B, T, E,
                        S, ck, pitch);
     return hipGetLastError();
 }
@@ -938,7 +1030,8 @@ hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t 
     const int64_t pitch = grid * a.NC;
     char *p = static_cast<char *>(scratch);
     float *ck = nullptr;
-    if (slack) {
+    const bool scan = c.exact != 0;
+    if (slack && !scan) {
         ck = reinterpret_cast<float *>(p);
         p += round256(static_cast<size_t>(c.nwin) * c.nc * pitch * sizeof(float));
     }
@@ -948,10 +1041,14 @@ hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t 
     const dim3 gd(static_cast<unsigned>(grid)), bd(static_cast<unsigned>(64 * c.groups * c.nc));
     const size_t lds = a.L.total;
     hipError_t e;
-    if (slack) e = c.fixed ? launch_windowed_kernel<true, true>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch)
-                           : launch_windowed_kernel<true, false>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch);
-    else e = c.fixed ? launch_windowed_kernel<false, true>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch)
-                     : launch_windowed_kernel<false, false>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch);
+#define EMO_WIN_ARGS gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch
+    if (slack && scan) e = c.fixed ? launch_windowed_kernel<true, true, true>(EMO_WIN_ARGS)
+                                   : launch_windowed_kernel<true, false, true>(EMO_WIN_ARGS);
+    else if (slack) e = c.fixed ? launch_windowed_kernel<true, true, false>(EMO_WIN_ARGS)
+                                : launch_windowed_kernel<true, false, false>(EMO_WIN_ARGS);
+    else e = c.fixed ? launch_windowed_kernel<false, true, false>(EMO_WIN_ARGS)
+                     : launch_windowed_kernel<false, false, false>(EMO_WIN_ARGS);
+#undef EMO_WIN_ARGS
     if (e == hipSuccess && (mask || part)) e = launch_select_results(Ts, Es, B, target, mask, part, s);
     return e;
 }

@@ -718,7 +718,7 @@ bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
 }
 
 bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::ChainStep> *steps,
-                  std::vector<int32_t> *pos, emo::DevChains *dc, std::vector<uint4> *blocks) {
+                  std::vector<int32_t> *pos, emo::DevChains *dc, std::vector<uint4> *blocks, bool exact) {
     const int32_t n = static_cast<int32_t>(sc.seq.size());
     if (n == 0) return false;
     std::vector<int32_t> heads;
@@ -764,6 +764,7 @@ bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::Cha
         dc->win = 0;
         blocks->clear();
     }
+    dc->exact = exact && dc->win > 0 ? 1 : 0;
     return true;
 }
 
@@ -826,10 +827,12 @@ std::vector<int32_t> cut_steps(const emo_graph_s &g, const Schedule &sf) {
 
 // Whether every sum and difference of durations along paths is an exact fp32 number, whatever
 // the order of the additions: all time values (table times and fixed durations) are multiples
-// of one power of two u, and the sum over all nodes of their largest duration is below 2^24 u.
+// of one power of two u, and the longest path with every pack at its largest duration is below
+// 2^24 u.  Every finish time, start floor, partial sum along a path and makespan of any policy
+// is then a multiple of u below 2^24 u (durations only lengthen paths), and so is the
+// difference of two of them.
 bool exact_time_sums(const emo_graph_s &g, const float *pack_time) {
     int emin = INT_MAX;
-    double total = 0.0;
     auto visit = [&](float x) {
         if (x <= 0.f) return;
         int e = 0;
@@ -837,21 +840,27 @@ bool exact_time_sums(const emo_graph_s &g, const float *pack_time) {
         const uint32_t M = static_cast<uint32_t>(std::ldexp(m, 24));
         emin = std::min(emin, e - 24 + __builtin_ctz(M));
     };
-    for (int32_t v = 0; v < g.V; ++v) {
+    std::vector<double> longest(static_cast<size_t>(g.V), 0.0);
+    double T = 0.0;
+    for (int32_t i = 0; i < g.V; ++i) {
+        const int32_t v = g.order[i];
+        double d = 0.0;
         if (g.pack[v] >= 0) {
-            float mx = 0.f;
             for (int32_t f = 0; f < g.F; ++f) {
                 const float x = pack_time[static_cast<size_t>(g.pack[v]) * g.F + f];
                 visit(x);
-                mx = std::max(mx, x);
+                d = std::max(d, static_cast<double>(x));
             }
-            total += mx;
         } else {
             visit(g.dur[v]);
-            total += g.dur[v];
+            d = g.dur[v];
         }
+        double start = 0.0;
+        for (int32_t j = g.pred_off[v]; j < g.pred_off[v + 1]; ++j) start = std::max(start, longest[g.pred[j]]);
+        longest[v] = start + d;
+        T = std::max(T, longest[v]);
     }
-    return emin == INT_MAX || total < std::ldexp(1.0, 24 + emin);
+    return emin == INT_MAX || T < std::ldexp(1.0, 24 + emin);
 }
 
 size_t jit_table_bytes(const emo_graph_s &g) {
@@ -1130,9 +1139,11 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     std::vector<int32_t> cpos;
     std::vector<uint4> cblocks;
     emo::DevChains dc;
-    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc, &cblocks);
+    const bool exact_sums = exact_time_sums(*g, pack_time);
+    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc, &cblocks, exact_sums);
     in.chain_lanes = chains_ok ? dc.lanes : 0;
     in.chain_window = chains_ok ? dc.win : 0;
+    in.chain_scan_window = chains_ok && dc.exact ? dc.win : 0;
     const int32_t nops = static_cast<int32_t>(sf.seq.size());
     g->jit_eligible = nops >= 1 && nops <= kJitMaxOps;
     g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;
@@ -1141,7 +1152,7 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     g->chain_eval = narrow && nops > kJitMaxOps && nops <= kChainMaxOps;
     g->chain_slack = narrow && nops > kJitMaxSlackOps && nops <= kChainMaxOps;
     g->cut_plan = emo::jit_cut_plan(g->jg, cut_steps(*g, sf), kCutMaxPacks, kCutSubPacks);
-    g->cut_ok = g->cut_plan.segments() >= 2 && nops <= kChainMaxOps && exact_time_sums(*g, pack_time);
+    g->cut_ok = g->cut_plan.segments() >= 2 && nops <= kChainMaxOps && exact_sums;
     in.cut_segments = g->cut_ok ? g->cut_plan.segments() : 0;
     int rt = 0;
     in.hip_runtime_version = hipRuntimeGetVersion(&rt) == hipSuccess ? rt : 0;
@@ -1318,9 +1329,11 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     }
     void *part = result ? scratch : nullptr;
     void *work = scratch ? static_cast<char *>(scratch) + part_bytes : nullptr;
-    g->info.last_kernels = path == Path::kChainLanes && emo::chains_windowed_ok(g->chains, levels, slack)
-                               ? 4
-                               : static_cast<int32_t>(path);
+    g->info.last_kernels = path == Path::kChainLanes && emo::chains_scan_ok(g->chains, levels, slack)
+                               ? 6
+                               : path == Path::kChainLanes && emo::chains_windowed_ok(g->chains, levels, slack)
+                                     ? 4
+                                     : static_cast<int32_t>(path);
     hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
     if (e == hipSuccess) {
         if (path == Path::kCut) {

@@ -159,6 +159,9 @@ struct DevChains {
     int32_t hdr_words = 0;            // nc + 1 rounded up to a multiple of 4
     int32_t blk_bytes = 0;
     const uint4 *blocks = nullptr;    // [nwin][blk_bytes / 16]
+    // slack by a second forward pass (chains_windowed with SCAN): the windowed layout exists and
+    // every time sum is exact
+    int32_t exact = 0;
 };
 // Whether the windowed kernel's LDS working set and prefetch fit for `nc` chains, F levels,
 // windows of W packs and step blocks of blk_bytes; sets the candidate groups per workgroup.
@@ -166,6 +169,9 @@ bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int3
 // Whether a call runs the windowed kernel (the layout exists and the buffers are 16-byte
 // aligned).
 bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *slack);
+// Whether a call runs the windowed kernel with slack from a second forward pass (the windowed
+// layout exists, the graph's time sums are exact and the buffers are 16-byte aligned).
+bool chains_scan_ok(const DevChains &c, const uint8_t *levels, const float *slack);
 // Scratch of launch_chains: backward checkpoints and chain-ordered slack (slack only), and
 // makespan/energy buffers.
 size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,

@@ -415,6 +415,42 @@ CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-strea
 CHAIN_WINDOW = {"1-stream": 16, "16-streams": 256, "3-streams-F8": 64, "9-streams-F32": 64}
 
 
+def off_grid(g):
+    """The same graph plus one isolated node of 2^-30 us.  The common power of two of all times
+    drops to 2^-30, so the loader can no longer show that every time sum is exact and the
+    two-pass chain scan gives way to the windowed kernel; every value the chains compute is
+    still on the 2^-4 us grid, so results stay exact."""
+    V = g.num_nodes
+    return dataclasses.replace(
+        g, name=g.name + "-offgrid", num_nodes=V + 1,
+        node_pack=np.append(g.node_pack, np.int32(-1)).astype(np.int32),
+        node_duration=np.append(g.node_duration, np.float32(2.0 ** -30)).astype(np.float32),
+        node_stream=None if g.node_stream is None else np.append(g.node_stream, np.int32(-1)).astype(np.int32))
+
+
+def check_windowed_off_grid(torch, emo, g, rows, win, what):
+    """The windowed kernel on the off-grid copy of `g`: makespan, energy and slack against the
+    oracle, makespan and slack bit for bit against the interpreter."""
+    g2 = off_grid(g)
+    gh = emo.EmoGraph(g2, device=0)
+    assert gh.info()["chain_scan_window"] == 0 and gh.info()["chain_window"] == win
+    lv = dev(torch, rows)
+    T, E = gh.eval_policies(lv)
+    S = gh.slack(lv)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == 4, gh.info()
+    T_or, E_or = oracle.eval_batch(g2, rows, nthreads=8)
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, what + " off grid")
+    ok = ~np.isnan(T_or)
+    _, _, S_or = oracle.slack_batch(g2, rows[ok], nthreads=8)
+    parity.assert_slack(host(S)[ok], S_or, T_or[ok], True, what + " off grid slack")
+    gi = emo.EmoGraph(g2, device=0, kernel_mode=1)
+    Ti, _ = gi.eval_policies(lv)
+    Si = gi.slack(lv)
+    assert np.array_equal(host(T).view(np.uint32), host(Ti).view(np.uint32)), what
+    assert np.array_equal(host(S).view(np.uint32), host(Si).view(np.uint32)), what
+
+
 def misaligned(torch, rows):
     """The rows in device memory at an address that is not 16-byte aligned."""
     buf = torch.empty(rows.size + 16, dtype=torch.uint8, device="cuda")
@@ -444,7 +480,9 @@ def test_chain_lanes(torch, emo, case):
     win = CHAIN_WINDOW.get(case, 0)
     assert gh.info()["chain_lanes"] == lanes
     assert gh.info()["chain_window"] == win
-    kind = 4 if win else 3
+    # on the time grid the two-pass scan kernel takes the windowed layout's place
+    assert gh.info()["chain_scan_window"] == win
+    kind = 6 if win else 3
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
@@ -477,6 +515,7 @@ def test_chain_lanes(torch, emo, case):
         assert np.array_equal(host(T).view(np.uint32), host(Tm).view(np.uint32)), case
         assert np.array_equal(Sh.view(np.uint32), host(Sm).view(np.uint32)), case
         parity.assert_eval(host(Tm), host(Em), T_or, E_or, True, case + " lane-per-chain")
+        check_windowed_off_grid(torch, emo, g, rows, win, "chain lanes " + case)
 
 
 def test_one_kernel_ragged_batches(torch, emo):
@@ -499,21 +538,27 @@ def test_one_kernel_ragged_batches(torch, emo):
         run_all(torch, emo, g, rows, [tgt], per_node=False, what=f"one kernel B={B}")
 
 
-def test_chain_windows_small_batches(torch, emo):
-    """Windowed kernel with batches smaller than a workgroup's 64 candidates and one past it
-    (lanes past the batch repeat the last row and store nothing), repeated calls bit for bit."""
+@pytest.mark.parametrize("grid", ["on", "off"])
+def test_chain_windows_small_batches(torch, emo, grid):
+    """Two-pass scan kernel (on the time grid) and windowed kernel (off it) with batches smaller
+    than a workgroup's 64 candidates and one past it (lanes past the batch repeat the last row
+    and store nothing), repeated calls bit for bit."""
     g = synth.stream_graph(77, 8208, 16, 16)
+    if grid == "off":
+        g = off_grid(g)
     rng = np.random.default_rng(77)
     gh = emo.EmoGraph(g, device=0)
     assert gh.info()["chain_window"] == 256
+    assert gh.info()["chain_scan_window"] == (256 if grid == "on" else 0)
+    scan = grid == "on"
     for B in (1, 3, 64, 65):
         rows = pins.random_rows(rng, g, B)
-        print(f"[case] windowed chains B={B}", flush=True)
+        print(f"[case] windowed chains grid={grid} B={B}", flush=True)
         lv = dev(torch, rows)
         T, E = gh.eval_policies(lv)
         S = gh.slack(lv)
         torch.cuda.synchronize()
-        assert gh.info()["last_kernels"] == 4
+        assert gh.info()["last_kernels"] == (6 if scan else 4)
         T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
         parity.assert_eval(host(T), host(E), T_or, E_or, True, f"windowed B={B}")
         S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(B)])
@@ -567,14 +612,69 @@ def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
     assert gh.info()["chain_lanes"] == 4
     windowed = P % 16 == 0
     assert gh.info()["chain_window"] == (64 if windowed else 0)
+    assert gh.info()["chain_scan_window"] == (64 if windowed else 0)
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
     S = gh.slack(lv)
-    assert gh.info()["last_kernels"] == (4 if windowed else 3)
+    assert gh.info()["last_kernels"] == (6 if windowed else 3)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, "chains with fixed nodes")
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(len(rows))])
     parity.assert_slack(host(S), S_or, T_or, True, "chains with fixed nodes: pack slack")
+    if windowed:
+        check_windowed_off_grid(torch, emo, g, rows, 64, "chains with fixed nodes")
+
+
+def skewed_chains(seed, P, S, F, share):
+    """P kernels on S streams, stream 0 taking `share` of them, each launched by a node of one
+    host launch chain: in a window of the scan kernel one chain holds far more than 64 steps."""
+    rng = np.random.default_rng(seed)
+    stream = np.where(rng.random(P) < share, 0, rng.integers(1, S, P))
+    src, dst, pack, dur = [], [], [], []
+    last = {}
+    prev_h = None
+    for p in range(P):
+        h = len(pack)
+        pack.append(-1)
+        dur.append(float(synth.quantize(rng.uniform(0.5, 3.0))))
+        if prev_h is not None:
+            src.append(prev_h)
+            dst.append(h)
+        prev_h = h
+        k = len(pack)
+        pack.append(p)
+        dur.append(0.0)
+        src.append(h)
+        dst.append(k)
+        if stream[p] in last:
+            src.append(last[stream[p]])
+            dst.append(k)
+        last[stream[p]] = k
+    t = np.sort(synth.quantize(rng.uniform(1.0, 30.0, (P, F))), axis=1)[:, ::-1].copy()
+    e = (0.7 * t * rng.uniform(0.2, 1.0, (P, F))).astype(np.float32)
+    return synth.Graph(f"skewed-{P}k-{S}s", len(pack), np.asarray(src, np.int32), np.asarray(dst, np.int32),
+                       np.asarray(pack, np.int32), np.asarray(dur, np.float32), P, F, t, e, 0.3)
+
+
+def test_chain_scan_long_window_lists(torch, emo):
+    """Two-pass scan kernel where one chain holds about 230 steps of a 256-pack window (records
+    loaded 64 at a time), with an invalid level and a ragged batch, against the oracle."""
+    g = skewed_chains(5, 8448, 16, 16, 0.9)
+    gh = emo.EmoGraph(g, device=0)
+    assert gh.info()["chain_scan_window"] == 256, gh.info()
+    rng = np.random.default_rng(6)
+    rows = pins.random_rows(rng, g, 130)
+    rows[77, 4000] = 16
+    print(f"[case] chain scan, long window lists: V={g.num_nodes} P={g.num_packs}", flush=True)
+    lv = dev(torch, rows)
+    T, E = gh.eval_policies(lv)
+    S = gh.slack(lv)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == 6
+    T_or, E_or, S_or = oracle.slack_batch(g, rows, nthreads=8)
+    assert np.isnan(T_or[77])
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, "skewed chains")
+    parity.assert_slack(host(S), S_or, T_or, True, "skewed chains slack")
 
 
 @pytest.mark.parametrize("mode", [0, 1], ids=["auto", "interpreted"])
@@ -790,7 +890,7 @@ def test_workload_full_batch(torch, emo, k):
     # one specialised kernel up to 2048 steps, cut-segment kernels for the 4096-pack graph (16
     # synchronisations), chain lanes for the 65536-kernel graph (16 stream chains)
     inf = gh.info()
-    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 5, 5: 4}[k], inf
+    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 5, 5: 6}[k], inf
     if k <= 4:
         # the interpreting kernels on the same batch: bit-identical
         gi = emo.EmoGraph(g, device=0, kernel_mode=1)
@@ -814,7 +914,7 @@ def test_workload_full_batch(torch, emo, k):
     S = gh.slack(lv)
     # slack: one kernel while every finish time fits in registers, then segmented kernels
     # (cut segments for the 4096-pack graph)
-    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 5, 5: 4}[k], gh.info()
+    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 5, 5: 6}[k], gh.info()
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in pick])
     idx = torch.from_numpy(pick).cuda()
     parity.assert_slack(host(S.index_select(0, idx)), S_or, T_or[pick], True, spec.name + " slack")
