@@ -434,11 +434,10 @@ __device__ __forceinline__ float fmax_nonneg(float a, float b) {
     return __uint_as_float(x > y ? x : y);
 }
 
-// max(a, b) for a >= 0 and any finite b: non-negative floats order like their bit patterns as
-// signed integers, and negative ones lie below every non-negative pattern.
-__device__ __forceinline__ float fmax_lo(float a, float b) {
-    const int x = __float_as_int(a), y = __float_as_int(b);
-    return __int_as_float(x > y ? x : y);
+// min of two non-negative finite floats (their bit patterns order like unsigned integers)
+__device__ __forceinline__ float fmin_nonneg(float a, float b) {
+    const unsigned x = __float_as_uint(a), y = __float_as_uint(b);
+    return __uint_as_float(x < y ? x : y);
 }
 
 struct WinArgs {
@@ -606,9 +605,10 @@ struct WinGroup {
 // the makespan minus the durations after it; with Pre_i = d_1 + ... + d_i and Tot = Pre_n,
 //   slack_i = LFT_i - EFT_i = (T - Tot) - (EFT_i - Pre_i),
 // and D_i = EFT_i - Pre_i obeys D_i = max(D_{i-1}, cst_i - Pre_{i-1}), D_0 = 0, because
-// EFT_i = max(EFT_{i-1}, cst_i) + d_i.  The forward pass also sums Tot per chain; the second
-// pass walks the windows again for D and writes slack = K - D, K = T - Tot, through the tile.
-// No finish time is checkpointed or recomputed backwards.
+// EFT_i = max(EFT_{i-1}, cst_i) + d_i.  With K = T - Tot, Q_i = K + Pre_i and Z_i = K - D_i:
+//   slack_i = Z_i = min(Z_{i-1}, Q_{i-1} - cst_i),  Q_i = Q_{i-1} + d_i,  Z_0 = Q_0 = K.
+// The forward pass also sums Tot per chain; the second pass walks the windows again for Z and
+// writes it through the slack tile.  No finish time is checkpointed or recomputed backwards.
 template <bool SLACK, bool FIXED, bool SCAN>
 __global__ void __launch_bounds__(kChainBlockThreads)
 chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ blocks,
@@ -734,24 +734,27 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     if (!SLACK) return;
     lds_barrier();
 
-    const int per_row = W >> 2;                             // float4 pieces per tile row
+    const int prlog = a.wlog - 2;                           // float4 pieces per tile row: W / 4
     // slack tile of window w -> pack order; a wave covers 4 candidates x 16 pieces when rows
     // are long enough (conflict-free LDS reads with the odd row pitch), else whole rows
+    // (W is a power of two: shifts, no divisions)
     auto flush_tile = [&](int w) {
-        const int n = a.NC * per_row;
+        const int n = a.NC << prlog;
         for (int q = t; q < n; q += nt) {
             int r, kk;
-            if (per_row >= 16) {
-                const int j = q & 63, blk = q >> 6, nkb = per_row >> 4;
-                const int rg = blk / nkb, kb = blk - rg * nkb;
+            if (prlog >= 4) {
+                const int j = q & 63, blk = q >> 6, kblog = prlog - 4;
+                const int rg = blk >> kblog, kb = blk & ((1 << kblog) - 1);
                 r = rg * 4 + (j >> 4);
                 kk = kb * 16 + (j & 15);
             } else {
-                r = q / per_row;
-                kk = q - r * per_row;
+                r = q >> prlog;
+                kk = q & ((1 << prlog) - 1);
             }
             const float *src = tile + r * (W + 1) + 4 * kk;
-            const float4 v = make_float4(src[0], src[1], src[2], src[3]);
+            float4 v = make_float4(src[0], src[1], src[2], src[3]);
+            if (SCAN && tfin[r] != tfin[r]) v = make_float4(__builtin_nanf(""), __builtin_nanf(""),
+                                                           __builtin_nanf(""), __builtin_nanf(""));
             const int64_t row = base + r;
             const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 4 * kk;
             if (row < B && col < P) *reinterpret_cast<float4 *>(S + row * P + col) = v;
@@ -764,8 +767,12 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
 
     if (SCAN) {
         // ---------------------------------------------------------------- second forward pass
-        const float K = tfin[cl] - pre;                     // NaN for a candidate with bad levels
-        float D = 0.f, p2 = 0.f;
+        // slack_i = K - D_i with K = T - Tot; carried as Q = K + Pre and Z = K - D:
+        //   Z_i = min(Z_{i-1}, Q_{i-1} - cst_i),  Q_i = Q_{i-1} + d_i,  Z_0 = Q_0 = K
+        // (a candidate with a bad level, K = NaN, gets its NaN row from the flush instead)
+        const float Kc = tfin[cl] - pre;
+        const float K = Kc == Kc ? Kc : 0.f;
+        float Z = K, Q = K;
         win_load(a, levels, g.tabt, 4, blocks, base, B, P, 0, s0);
         win_load(a, levels, g.tabt, 4, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
         win_store(a, lds, 0, tabt, 4, nullptr, addf, s0);
@@ -794,9 +801,10 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
                 win_issue_point();
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    D = fmax_lo(D, A.cst[i] - p2);
-                    p2 += tt[i];
-                    trow[A.ct[i] & 0xffffu] = K - D;
+                    // both operands are >= 0: Q_{i-1} - cst_i >= K - D_i = slack_i
+                    Z = fmin_nonneg(Z, Q - A.cst[i]);
+                    Q += tt[i];
+                    trow[A.ct[i] & 0xffffu] = Z;
                 }
             };
             WinGroup<FIXED> G0, G1, G2;
