@@ -93,7 +93,7 @@ constexpr int32_t kJitMaxSlackOps = 160;  // every finish time stays in a VGPR
 // Segmented kernels (larger graphs): steps per segment kernel and per recompute sub-segment,
 // and the largest graph compiled this way (compile time grows with the step count).
 constexpr int32_t kChainSegOps = 256;
-constexpr int32_t kChainSubOps = 64;
+constexpr int32_t kChainSubOps = 32;
 constexpr int32_t kChainMaxOps = 8192;
 // Cut-segment kernels: packs per segment at most, packs per recompute sub-segment.
 constexpr int32_t kCutMaxPacks = 256;
