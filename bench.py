@@ -37,7 +37,8 @@ VALU_PEAK_TOPS = 39.3   # 256 CUs x 64 fp32 lanes x 2.4 GHz, one op per lane per
 # selection code are common to all of them
 KIND_SOURCES = {0: ("emo_kernels.hip",), 1: ("emo_jit.cpp",), 2: ("emo_jit.cpp",),
                 3: ("emo_chains.hip", "emo_kernels.hip"), 4: ("emo_chains.hip", "emo_kernels.hip"),
-                5: ("emo_jit.cpp",), 6: ("emo_chains.hip", "emo_kernels.hip")}
+                5: ("emo_jit.cpp",), 6: ("emo_chains.hip", "emo_kernels.hip"),
+                7: ("emo_jit.cpp",)}
 
 
 def kernel_source_hash(kind: int) -> str:
@@ -439,8 +440,10 @@ def run_intervals(args, emo, synth, np, torch):
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": spec.name, "candidates": B, "intervals": K, "packs": g.num_packs,
                    "levels": F, "target_ratio": 1.02, "step": "emo_eval_intervals",
-                   "rotated_input_copies": copies},
-        "roofline": {"bound": "hbm", "kernel": "interval_kernel", "achieved": achieved,
+                   "rotated_input_copies": copies, "kernels": info["last_kernels"]},
+        "roofline": {"bound": "hbm",
+                     "kernel": "emo_iv" if info["last_kernels"] == 7
+                     else "interval_kernel", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": None, "algorithmic_bytes_per_launch": algo_bytes,
                      "launch_ms": main_ms, "timed_launches": len(ev),

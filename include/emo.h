@@ -108,7 +108,9 @@ typedef struct {
                                      segments between cut nodes evaluated in parallel),
                                      6 two-pass chain scan (windowed chain lanes whose slack
                                      comes from a second forward pass, for chains with exact
-                                     time sums) */
+                                     time sums), 7 time-interval kernel specialised to the
+                                     graph (emo_eval_intervals; 0 there means the interpreting
+                                     kernel) */
     int32_t chain_lanes;          /* lanes per candidate of the chain-lane kernels, 0 when the
                                      candidate-dependent nodes do not form at most 64 disjoint
                                      chains */
@@ -448,6 +450,14 @@ emo_status emo_graph_segmented_source(emo_graph_t g, char *buf, int64_t *len);
  * completes the selection.  Same buffer convention as
  * emo_graph_specialized_source.  EMO_ERR_UNSUPPORTED when the graph has no cut segments. */
 emo_status emo_graph_cut_source(emo_graph_t g, char *buf, int64_t *len);
+
+/* Diagnostics: the HIP source of the time-interval kernel specialised to `g` (what
+ * emo_eval_intervals compiles on first use when the graph is small enough for one specialised
+ * kernel): emo_iv, whose workgroups copy their candidates' rows into LDS with coalesced loads and
+ * find each pack's interval in a bucket table of the change points (in dynamic LDS, with the
+ * rows).  Same buffer convention as emo_graph_specialized_source.  EMO_ERR_UNSUPPORTED when the
+ * graph is too large for one kernel. */
+emo_status emo_graph_interval_source(emo_graph_t g, char *buf, int64_t *len);
 
 /* Static string naming a status code. */
 const char *emo_status_string(emo_status s);

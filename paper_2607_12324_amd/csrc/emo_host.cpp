@@ -266,6 +266,10 @@ struct emo_graph_s {
     bool cut_ok = false;
     int cut_state = 0;                       // 0 not tried, 1 compiled, -1 failed
     emo::JitModule jk;
+    // time-interval kernels specialised to the graph
+    int iv_state = 0;                        // 0 not tried, 1 compiled, -1 failed
+    emo::JitModule jiv;
+    int64_t iv_cap_key = -1, iv_cap = 0;     // resident workgroups for the last (K, M)
     Arena arena;                             // per-call scratch, kept between calls
     Arena dp_arena;                          // scratch of the policy search (whose evaluations
                                              // use `arena`)
@@ -878,6 +882,56 @@ std::string jit_source(const emo_graph_s &g, int *block_out) {
     return emo::jit_generate(g.jg, with_slack, tab_lds, block);
 }
 
+// Generates and compiles the time-interval kernels once; returns 1 when they are ready.
+int ensure_iv(emo_graph_s *g) {
+    std::lock_guard<std::mutex> lock(g->jit_mu);
+    if (g->iv_state != 0) return g->iv_state;
+    const size_t tb = static_cast<size_t>(g->P) * g->F * sizeof(float2);
+    const bool tab_lds = tb <= kJitTableLds;
+    const std::string src = emo::jit_generate_intervals(g->jg, tab_lds, 256);
+    DeviceGuard guard(g->device);
+    emo::JitModule m;
+    std::string log;
+    if (emo::jit_compile_intervals(src, &m, &log) != 0) {
+        g->jit_log = log;
+        g->iv_state = -1;
+        return -1;
+    }
+    m.block = 256;
+    g->jiv = m;
+    g->iv_state = 1;
+    g->info.compile_seconds += static_cast<float>(m.compile_seconds);
+    return 1;
+}
+
+// Bucket table parameters of the time-interval kernels for change points p_0 < ... < p_{K-2}: a
+// scale with distinct floor(fl(p_j * scale)) (the exact fp32 product the kernel forms) and
+// M = the largest such bucket + 2.  False when that needs more than kIvMaxBuckets buckets.
+bool iv_buckets(const float *pts, int K, float *scale_out, int *M_out) {
+    if (K <= 1) {
+        *scale_out = 0.f;
+        *M_out = 1;
+        return true;
+    }
+    double gap = INFINITY;
+    for (int i = 0; i + 2 < K; ++i) gap = std::min(gap, static_cast<double>(pts[i + 1]) - pts[i]);
+    if (K == 2) gap = pts[0];
+    for (double c : {1.01, 1.25, 2.0, 4.0}) {
+        const float s = static_cast<float>(c / gap);
+        if (!(s > 0.f) || !std::isfinite(s)) continue;
+        const float top = pts[K - 2] * s;
+        if (!(top < static_cast<float>(emo::kIvMaxBuckets - 2))) continue;
+        bool distinct = true;
+        for (int i = 0; i + 2 < K && distinct; ++i)
+            distinct = static_cast<int>(pts[i] * s) < static_cast<int>(pts[i + 1] * s);
+        if (!distinct) continue;
+        *scale_out = s;
+        *M_out = static_cast<int>(top) + 2;
+        return true;
+    }
+    return false;
+}
+
 // Generates and compiles the specialised kernels once; returns 1 when they are ready.
 int ensure_jit(emo_graph_s *g) {
     std::lock_guard<std::mutex> lock(g->jit_mu);
@@ -1260,6 +1314,23 @@ emo_status emo_graph_cut_source(emo_graph_t g, char *buf, int64_t *len) {
     return ok();
 }
 
+emo_status emo_graph_interval_source(emo_graph_t g, char *buf, int64_t *len) {
+    if (!g || !len) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
+    if (!g->jit_eligible) return fail(EMO_ERR_UNSUPPORTED, "graph too large for one specialised kernel");
+    const size_t tb = static_cast<size_t>(g->P) * g->F * sizeof(float2);
+    const std::string src = emo::jit_generate_intervals(g->jg, tb <= kJitTableLds, 256);
+    const int64_t need = static_cast<int64_t>(src.size()) + 1;
+    if (!buf) {
+        *len = need;
+        return ok();
+    }
+    if (*len < need) return fail(EMO_ERR_INVALID_ARGUMENT, "buffer of %lld bytes, %lld needed",
+                                 (long long)*len, (long long)need);
+    std::memcpy(buf, src.c_str(), static_cast<size_t>(need));
+    *len = need;
+    return ok();
+}
+
 emo_status emo_graph_topo_order(emo_graph_t g, int32_t *order, int32_t *depth) {
     if (!g || (!order && g->V > 0)) return fail(EMO_ERR_INVALID_ARGUMENT, "NULL argument");
     if (g->V > 0) std::memcpy(order, g->order.data(), sizeof(int32_t) * g->V);
@@ -1434,10 +1505,37 @@ emo_status emo_eval_intervals(emo_graph_t g, const uint8_t *levels, int64_t B, i
     if (B == 0) return result ? after_launch(emo::launch_empty_result(result, st), "empty selection") : ok();
     if (!makespan && !energy && !feasible_mask && !result) return ok();
     if (!levels) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
-    const int64_t nblocks = emo::forward_blocks(B);
+    // straight-line kernels specialised to the graph when it is small enough for one kernel and
+    // the change points fit the bucket table; otherwise the interpreting kernel
+    emo::IvJitArgs iva;
+    bool use_jit = g->kernel_mode != EMO_KERNELS_INTERPRETED && g->jit_eligible &&
+                   iv_buckets(pol.pts, num_intervals, &iva.scale, &iva.M);
+    if (use_jit) {
+        const int st = ensure_iv(g);
+        if (st != 1 && g->kernel_mode == EMO_KERNELS_SPECIALIZED)
+            return fail(EMO_ERR_DEVICE, "time-interval kernel compilation failed: %s", g->jit_log.c_str());
+        // the rows and the bucket table must fit the workgroup's LDS beside the static tables
+        use_jit = st == 1 && g->jiv.iv_static_lds + emo::jit_iv_dyn_lds(g->jiv.block, num_intervals, iva.M) <=
+                                 static_cast<size_t>(g->jiv.iv_max_lds);
+    }
+    int64_t iv_cap = 0;
+    if (use_jit) {
+        iva.K = num_intervals;
+        std::memcpy(iva.pts, pol.pts, sizeof(iva.pts));
+        std::memcpy(iva.idle, pol.idle, sizeof(iva.idle));
+        // persistent workgroups (each builds the bucket table once): as many as are resident
+        const int64_t key = static_cast<int64_t>(num_intervals) << 32 | iva.M;
+        std::lock_guard<std::mutex> lock(g->jit_mu);
+        if (g->iv_cap_key != key) {
+            g->iv_cap = emo::jit_iv_cap(g->jiv, num_intervals, iva.M);
+            g->iv_cap_key = key;
+        }
+        iv_cap = g->iv_cap;
+    }
+    const int64_t nblocks = use_jit ? emo::jit_blocks(g->jiv, B) : emo::forward_blocks(B);
     size_t part_bytes = result ? static_cast<size_t>(nblocks) * emo::kPartialBytes : 0;
     part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
-    const size_t work_bytes = emo::forward_scratch_bytes(g->dg.eval, B);
+    const size_t work_bytes = use_jit ? 0 : emo::forward_scratch_bytes(g->dg.eval, B);
     std::lock_guard<std::mutex> lock(g->arena.mu);
     void *scratch = nullptr;
     if (part_bytes + work_bytes > 0) {
@@ -1450,9 +1548,12 @@ emo_status emo_eval_intervals(emo_graph_t g, const uint8_t *levels, int64_t B, i
     }
     void *part = result ? scratch : nullptr;
     void *work = scratch ? static_cast<char *>(scratch) + part_bytes : nullptr;
-    g->info.last_kernels = 0;
+    g->info.last_kernels = use_jit ? 7 : 0;
     hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
-    if (e == hipSuccess)
+    if (e == hipSuccess && use_jit)
+        e = emo::jit_launch_intervals(g->jiv, levels, B, g->dg.tab, iva, iv_cap, makespan, energy,
+                                      latency_target, feasible_mask, part, st);
+    else if (e == hipSuccess)
         e = emo::launch_intervals(g->dg, pol, levels, B, makespan, energy, latency_target, feasible_mask,
                                   part, work, st);
     if (e == hipSuccess && g->ev_end) e = hipEventRecord(g->ev_end, st);

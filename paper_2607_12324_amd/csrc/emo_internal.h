@@ -94,6 +94,8 @@ int64_t forward_blocks(int64_t B);
 // A time-interval policy batch (the policy form of Sec. IV-A; Alg. 1): K intervals [T_i,
 // T_{i+1}) with T_0 = 0 and the last one open-ended; each candidate's row holds K levels.  Passed
 // to the kernel by value (2 KB of kernel arguments).
+// pack energies are summed in fp32 blocks of this many packs (program order) added into fp64
+constexpr int kEnergyBlock = 64;
 constexpr int kMaxIntervals = 256;
 constexpr int kMaxLevels = 256;
 struct IvPolicy {
@@ -310,6 +312,8 @@ struct JitModule {
     std::vector<hipFunction_t> kf;       // segment kernels, forward only (one per group)
     std::vector<hipFunction_t> ks;       // segment kernels, forward and slack
     hipFunction_t kfin = nullptr;        // makespan, energy, selection, NaN rows
+    // time-interval kernel: its static LDS bytes and the device's per-workgroup limit
+    int iv_static_lds = 0, iv_max_lds = 0;
 };
 
 // Bytes per level load in generated kernels (16, 4 or 1): the alignment they need.
@@ -347,6 +351,26 @@ void jit_unload(JitModule *m);
 // Candidate groups of the one-kernel specialised kernels for B candidates (one selection
 // partial each).
 int64_t jit_blocks(const JitModule &m, int64_t B);
+// Time-interval kernel specialised to the graph (emo_iv, any K): each workgroup copies its
+// candidates' rows to LDS and looks the start times' intervals up in a bucket table; the batch's
+// change points, idle powers and bucket table parameters by value.
+constexpr int kIvMaxBuckets = 4096;
+struct IvJitArgs {
+    int32_t K = 1, M = 1;
+    float scale = 0.f;
+    int32_t pad = 0;
+    float pts[kMaxIntervals - 1];
+    float idle[kMaxLevels];
+};
+std::string jit_generate_intervals(const JitGraph &g, bool tab_lds, int block);
+int jit_compile_intervals(const std::string &src, JitModule *out, std::string *log);
+// Dynamic LDS bytes of emo_iv for K intervals and M buckets (bucket table, then the rows).
+size_t jit_iv_dyn_lds(int block, int K, int M);
+// Resident workgroups of emo_iv on the current device with that dynamic LDS (0: unknown).
+int64_t jit_iv_cap(const JitModule &m, int K, int M);
+hipError_t jit_launch_intervals(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
+                                const IvJitArgs &a, int64_t cap, float *T, float *E, float target,
+                                uint32_t *mask, void *part, hipStream_t s);
 // Sets select_cap / slack_cap from the occupancy of the compiled kernels (current device).
 void jit_set_caps(JitModule *m);
 // Forward pass; T, E, mask, part may each be NULL.

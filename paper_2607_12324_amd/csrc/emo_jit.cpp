@@ -537,6 +537,197 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
     return o.str();
 }
 
+// ------------------------------------------------------------------ time-interval kernels
+//
+// Time-interval policies (the policy form of Sec. IV-A as Alg. 1 evaluates it): a candidate's
+// row holds one level per interval [T_i, T_{i+1}) of the batch's change points, and a pack runs
+// at the level of the interval that holds its start time.  The forward pass is the same
+// straight-line code as emo_sp_select; before each pack's table read, its interval comes from a
+// bucket table built in LDS from the change points: with u(x) = fl(x * scale), bucket
+// b = floor(min(u(est), M - 1)) holds the count of change points whose bucket is below b and the
+// one point whose bucket is b (+inf if none; the host picks scale so that no two points share a
+// bucket).  Since fl(x * scale) is monotone in x, every point of a lower bucket is <= est, every
+// point of a higher one is > est, and the one in bucket b is compared directly: the count of
+// points <= est is exact, as in the interpreting kernel.  Energies and the idle term follow the
+// interpreting kernel's order, so both give bit-identical results.
+
+std::string jit_generate_intervals(const JitGraph &g, bool tab_lds, int block) {
+    std::ostringstream o;
+    o << "#define EMO_BLOCK " << block << "\n" << kPrelude << kEmoSelectSource << "\n";
+    const long long ntab = static_cast<long long>(g.P) * g.F;
+    o << "#define NTAB " << (ntab > 0 ? ntab : 1) << "\n";
+    o << "#define EMO_F " << g.F << "\n";
+    o << "struct EmoIvArgs { int K; int M; float scale; int pad; float pts[" << kMaxIntervals - 1
+      << "]; float idle[" << kMaxLevels << "]; };\n";
+    // a level byte is invalid when it is >= F: SWAR test of the four bytes of a word
+    std::string bad_word;
+    if (g.F >= 256) {
+        bad_word = "0u";
+    } else if (g.F <= 128) {
+        bad_word = "(((w & 0x7f7f7f7fu) + " + std::to_string((128u - g.F) * 0x01010101u) +
+                   "u) | w) & 0x80808080u";
+    } else {
+        bad_word = "(((w & 0x7f7f7f7fu) + " + std::to_string((256u - g.F) * 0x01010101u) +
+                   "u) & w) & 0x80808080u";
+    }
+    o << R"(
+// interval of start time `est`: the number of change points <= est
+__device__ __forceinline__ unsigned int emo_interval(float est, const int2 *bk, float scale, int M) {
+  const int b = (int)fminf(est * scale, (float)(M - 1));
+  const int2 e = bk[b];
+  return (unsigned int)e.x + (est >= __int_as_float(e.y) ? 1u : 0u);
+}
+struct EmoFwd { float T; float E; bool bad; };
+)";
+    // forward body; the lane's row of K level bytes is in LDS at `myrow` (word aligned)
+    o << "__device__ __forceinline__ EmoFwd emo_iv_forward(const u8 *myrow, int K,\n"
+         "    const float2 *__restrict__ tab, const int2 *bk, float scale, int M, const float *pts,\n"
+         "    const double *dur, const float *idle) {\n"
+         "  float T = " << flit(g.t_const) << ";\n"
+         "  double eacc = 0.0;\n  float eblk = 0.f;\n";
+    const int n = static_cast<int>(g.ops.size());
+    std::vector<int> last_use(n, -1);
+    for (int i = 0; i < n; ++i)
+        for (int k : g.ops[i].in) last_use[k] = std::max(last_use[k], i);
+    int npk = 0;
+    for (int i = 0; i < n; ++i) {
+        const JitOp &op = g.ops[i];
+        if (i > 0 && i % 4 == 0) {
+            // the finish times still needed and the running sums pass through an empty asm: the
+            // scheduler cannot interleave far-apart steps (which would keep many values live)
+            std::vector<std::string> live = {"eblk", "T"};
+            for (int j = 0; j < i; ++j)
+                if (last_use[j] >= i) live.push_back("f" + std::to_string(j));
+            for (size_t b = 0; b < live.size(); b += 24) {
+                o << "  __asm__ __volatile__(\"\" :";
+                for (size_t k = b; k < live.size() && k < b + 24; ++k)
+                    o << (k == b ? " " : ", ") << "\"+v\"(" << live[k] << ")";
+                o << ");\n";
+            }
+        }
+        o << "  const float e" << i << " = " << est_expr(g, i, "f") << ";\n";
+        if (op.pack >= 0) {
+            o << "  const unsigned int v" << i << " = emo_interval(e" << i << ", bk, scale, M);\n"
+              << "  unsigned int l" << i << " = myrow[v" << i << "];\n"
+              << "  l" << i << " = l" << i << " < EMO_F ? l" << i << " : 0u;\n"
+              << "  const float2 te" << i << " = tab[" << static_cast<long long>(op.pack) * g.F << " + l" << i
+              << "];\n"
+              << "  float f" << i << " = e" << i << " + te" << i << ".x;\n"
+              << "  eblk += te" << i << ".y;\n";
+            if (++npk % kEnergyBlock == 0) o << "  eacc += (double)eblk;\n  eblk = 0.f;\n";
+        } else {
+            o << "  float f" << i << " = e" << i << " + " << flit(op.dur) << ";\n";
+        }
+        if (op.out.empty()) o << "  T = fmaxf(T, f" << i << ");\n";
+    }
+    o << "  eacc += (double)eblk;\n"
+         "  // invalid levels anywhere in the row, four bytes a word\n"
+         "  const unsigned int *mw = (const unsigned int *)myrow;\n"
+         "  unsigned int bad = 0u;\n"
+         "  for (int j = 0; 4 * j < K; ++j) {\n"
+         "    unsigned int w = mw[j];\n"
+         "    if (4 * j + 4 > K) w &= 0xffffffffu >> (8 * (4 * j + 4 - K));   // bytes past the row\n"
+         "    bad |= " << bad_word << ";\n"
+         "  }\n";
+    o << R"(  // idle energy, interval by interval in increasing order: the whole length of the nf
+  // intervals that end at or before T (nf: the number of change points <= T, the interval of T),
+  // then the part of interval nf below T.  Levels >= F read zeros (their row gives NaN anyway).
+  const int nf = (int)emo_interval(T, bk, scale, M);
+  for (int j = 0; 4 * j < nf; ++j) {
+    const unsigned int w = mw[j];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (4 * j + q < nf) eacc = fma((double)idle[(w >> (8 * q)) & 255u], dur[4 * j + q], eacc);
+  }
+  const double Td = (double)T;
+  const double lo = nf > 0 ? (double)pts[nf - 1] : 0.0;
+  if (Td > lo) eacc = fma((double)idle[myrow[nf]], Td - lo, eacc);
+  EmoFwd r;
+  r.T = T;
+  r.E = (float)eacc;
+  r.bad = bad != 0u;
+  if (r.bad) { r.T = EMO_NAN; r.E = EMO_NAN; }
+  return r;
+}
+)";
+    o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
+         "emo_iv(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg, EmoIvArgs a,\n"
+         "    int copy, float inv_k, float *__restrict__ To, float *__restrict__ Eo, float target,\n"
+         "    unsigned int *__restrict__ mask, EmoPartial *part) {\n";
+    if (tab_lds)
+        o << "  __shared__ float2 tab[NTAB];\n"
+             "  for (int i_ = threadIdx.x; i_ < NTAB; i_ += EMO_BLOCK) tab[i_] = tabg[i_];\n";
+    else
+        o << "  const float2 *__restrict__ tab = tabg;\n";
+    o << R"(  __shared__ float s_pts[256];
+  __shared__ double s_dur[256];      // interval lengths T_{i+1} - T_i (T_0 = 0)
+  __shared__ float s_idle[256];      // zero past F
+  // dynamic: the bucket table (M entries), then the group's rows, SD words a row
+  extern __shared__ __align__(16) unsigned int emo_dyn[];
+  const int K = a.K, M = a.M;
+  const int SD = ((K + 3) >> 2) | 1;        // odd: a word column of the rows is conflict free
+  int2 *s_bk = (int2 *)emo_dyn;
+  unsigned int *s_rows = emo_dyn + 2 * M;
+  const float scale = a.scale;
+  for (int i = threadIdx.x; i < K - 1; i += EMO_BLOCK) s_pts[i] = a.pts[i];
+  for (int i = threadIdx.x; i < K - 1; i += EMO_BLOCK)
+    s_dur[i] = (double)a.pts[i] - (i > 0 ? (double)a.pts[i - 1] : 0.0);
+  for (int i = threadIdx.x; i < 256; i += EMO_BLOCK) s_idle[i] = i < EMO_F ? a.idle[i] : 0.f;
+  __syncthreads();
+  // bucket b: the number of points whose bucket is below b (they are increasing, and so are
+  // their buckets), and the point whose bucket is b, if any
+  for (int b = threadIdx.x; b < M; b += EMO_BLOCK) {
+    int lo = 0, hi = K - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if ((int)(s_pts[mid] * scale) < b) lo = mid + 1; else hi = mid;
+    }
+    const float c = lo < K - 1 && (int)(s_pts[lo] * scale) == b ? s_pts[lo] : __builtin_inff();
+    s_bk[b] = make_int2(lo, __float_as_int(c));
+  }
+  const u8 *my = (const u8 *)(s_rows + threadIdx.x * SD);
+  for (long long grp = blockIdx.x; grp * EMO_BLOCK < B; grp += gridDim.x) {
+    // the group's rows are contiguous: copy them to LDS with coalesced loads of `copy` bytes
+    // (16 when K is a multiple of 16, 4 when of 4, else 1; the batch aligned to match).  Row of
+    // byte x: floor((x + 0.5) / K), exact from the fp32 product for x < 2^16, K <= 256.
+    __syncthreads();   // the previous group's rows are read (and the tables built)
+    {
+      const long long r0 = grp * EMO_BLOCK;
+      const int nb = (int)(B - r0 < EMO_BLOCK ? B - r0 : EMO_BLOCK) * K;
+      const u8 *src = lv + r0 * K;
+      if (copy == 16) {
+        for (int q = threadIdx.x; q < (nb >> 4); q += EMO_BLOCK) {
+          const emo_u32x4 w = ((const emo_u32x4 *)src)[q];
+          const int r = (int)(((float)(q << 4) + 0.5f) * inv_k);
+          unsigned int *d = s_rows + r * SD + (((q << 4) - r * K) >> 2);
+          d[0] = w.x; d[1] = w.y; d[2] = w.z; d[3] = w.w;
+        }
+      } else if (copy == 4) {
+        for (int q = threadIdx.x; q < (nb >> 2); q += EMO_BLOCK) {
+          const unsigned int w = ((const unsigned int *)src)[q];
+          const int r = (int)(((float)(q << 2) + 0.5f) * inv_k);
+          s_rows[r * SD + (((q << 2) - r * K) >> 2)] = w;
+        }
+      } else {
+        for (int q = threadIdx.x; q < nb; q += EMO_BLOCK) {
+          const int r = (int)(((float)q + 0.5f) * inv_k);
+          ((u8 *)s_rows)[((r * SD) << 2) + q - r * K] = src[q];
+        }
+      }
+    }
+    __syncthreads();
+    const long long gid = grp * EMO_BLOCK + threadIdx.x;
+    const bool active = gid < B;
+    const long long cand = active ? gid : B - 1;
+    const EmoFwd r = emo_iv_forward(my, K, tab, s_bk, scale, M, s_pts, s_dur, s_idle);
+    if (active) { if (To) To[cand] = r.T; if (Eo) Eo[cand] = r.E; }
+    if (mask || part) emo_select_block(grp, active, r.T, r.E, cand, B, target, mask, part);
+  }
+}
+)";
+    return o.str();
+}
+
 // ------------------------------------------------------------------ segmented kernels
 
 namespace {
@@ -1349,6 +1540,30 @@ namespace {
 unsigned grid_of(int64_t B, int block) { return static_cast<unsigned>((B + block - 1) / block); }
 }  // namespace
 
+int jit_compile_intervals(const std::string &src, JitModule *out, std::string *log) {
+    int rc = compile_module(src, &out->module, &out->compile_seconds, log);
+    if (rc != 0) return rc;
+    int dev = 0;
+    if (!get_function(out->module, "emo_iv", &out->select) ||
+        hipFuncGetAttribute(&out->iv_static_lds, HIP_FUNC_ATTRIBUTE_SHARED_SIZE_BYTES, out->select) !=
+            hipSuccess ||
+        hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&out->iv_max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+            hipSuccess) {
+        (void)hipGetLastError();
+        *log = "time-interval kernel missing from the module or its attributes unknown";
+        (void)hipModuleUnload(out->module);
+        *out = JitModule();
+        return 2;
+    }
+    return 0;
+}
+
+size_t jit_iv_dyn_lds(int block, int K, int M) {
+    const size_t sd = static_cast<size_t>(((K + 3) >> 2) | 1);
+    return static_cast<size_t>(M) * 8 + static_cast<size_t>(block) * sd * 4;
+}
+
 int64_t jit_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.block); }
 
 namespace {
@@ -1372,6 +1587,33 @@ unsigned capped_grid(int64_t B, int block, int64_t cap) {
 void jit_set_caps(JitModule *m) {
     m->select_cap = resident_blocks(m->select, m->block);
     m->slack_cap = resident_blocks(m->slack, m->block);
+}
+
+hipError_t jit_launch_intervals(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
+                                const IvJitArgs &a, int64_t cap, float *T, float *E, float target,
+                                uint32_t *mask, void *part, hipStream_t s) {
+    long long b = B;
+    IvJitArgs args_v = a;
+    const uintptr_t al = reinterpret_cast<uintptr_t>(levels);
+    int copy = a.K % 16 == 0 && al % 16 == 0 ? 16 : (a.K % 4 == 0 && al % 4 == 0 ? 4 : 1);
+    float inv_k = static_cast<float>(1.0 / a.K);
+    void *args[] = {&levels, &b, &tab, &args_v, &copy, &inv_k, &T, &E, &target, &mask, &part};
+    const unsigned dyn = static_cast<unsigned>(jit_iv_dyn_lds(m.block, a.K, a.M));
+    return hipModuleLaunchKernel(m.select, capped_grid(B, m.block, cap), 1, 1, m.block, 1, 1, dyn, s, args,
+                                 nullptr);
+}
+
+int64_t jit_iv_cap(const JitModule &m, int K, int M) {
+    int dev = 0, ncu = 0, nb = 0;
+    const size_t dyn = jit_iv_dyn_lds(m.block, K, M);
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&nb, m.select, m.block, dyn) != hipSuccess ||
+        nb < 1) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return static_cast<int64_t>(nb) * ncu;
 }
 
 hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,

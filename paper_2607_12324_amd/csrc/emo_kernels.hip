@@ -42,7 +42,6 @@ namespace {
 constexpr int kBlock = EMO_BLOCK;
 constexpr int kWave = EMO_WAVE;
 constexpr int kWavesPerBlock = EMO_WAVES_PER_BLOCK;
-constexpr int kEnergyBlock = 64;
 constexpr int kStage = 32;            // packs per staged slack segment (one 128-byte line)
 constexpr size_t kLdsBudget = 60 * 1024;
 
@@ -490,13 +489,18 @@ __device__ __forceinline__ Fwd run_forward_iv(const DevProgram &pr, Tab<MODE> &t
         if (flags & kStepSink) T = fmaxf(T, eft);
     }
     eacc += static_cast<double>(eblk);
+    // idle energy, interval by interval in increasing order: the whole length of each interval
+    // that ends at or before the makespan, then the part of the next one below it
+    const double Td = static_cast<double>(T);
     for (int i = 0; i < K; ++i) {
         const double lo = i > 0 ? static_cast<double>(pts[i - 1]) : 0.0;
-        const double hi = i < K - 1 ? fmin(static_cast<double>(pts[i]), static_cast<double>(T))
-                                    : static_cast<double>(T);
+        if (!(Td > lo)) break;   // this interval and the later ones start at or after T
+        const bool whole = i < K - 1 && pts[i] <= T;
+        const double d = whole ? static_cast<double>(pts[i]) - lo : Td - lo;
         unsigned l = level_at(row, lw, lgroup, i);
         l = l < static_cast<unsigned>(F) ? l : 0u;
-        if (hi > lo) eacc += static_cast<double>(idle[l]) * (hi - lo);
+        eacc = fma(static_cast<double>(idle[l]), d, eacc);
+        if (!whole) break;
     }
     Fwd f;
     f.E = static_cast<float>(eacc);

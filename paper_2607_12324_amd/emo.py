@@ -27,7 +27,8 @@ ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_timing_events", "emo_pack_kernels", "emo_contract_packs",
                 "emo_pack_model",
                 "emo_graph_specialized_source",
-                "emo_graph_segmented_source", "emo_graph_cut_source", "emo_status_string",
+                "emo_graph_segmented_source", "emo_graph_cut_source", "emo_graph_interval_source",
+                "emo_status_string",
                 "emo_last_error")
 
 
@@ -83,6 +84,7 @@ def _load_library():
         "emo_graph_specialized_source": [P, P, P],
         "emo_graph_segmented_source": [P, P, P],
         "emo_graph_cut_source": [P, P, P],
+        "emo_graph_interval_source": [P, P, P],
         "emo_graph_set_timing_events": [P, P, P],
         "emo_pack_kernels": [i32, i32, P, P, P, P, P, i32, i32, P, f32, P, P],
         "emo_pack_model": [i32, i32, P, i32, P, P, i32, P, P, P, P, i32],
@@ -209,6 +211,9 @@ class EmoGraph:
 
     def cut_source(self) -> str:
         return self._source(lib.emo_graph_cut_source)
+
+    def interval_source(self) -> str:
+        return self._source(lib.emo_graph_interval_source)
 
     def _source(self, fn) -> str:
         n = ctypes.c_int64(0)

@@ -132,3 +132,29 @@ def test_dp_without_packs_and_argument_errors(torch, emo):
     a = run(emo, gh, 20.0, 1.0)
     b = run(emo, gh, 20.0, 1.0)
     assert np.array_equal(a[0], b[0]) and a[1] == b[1]
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_dp_on_workload_tables(torch, emo, k):
+    """The search on the 64- and 512-pack workload graphs with their own (non-dyadic) energies,
+    64 buckets between T0 and 1.05 T0.  Energies in fp32 can tie differently on the two sides
+    and lead the searches through different stored policies, so the result is accepted when it
+    is feasible, evaluates (oracle) to the makespan and energy it reports, and its energy is
+    within 1e-5 of the oracle search's best."""
+    g = synth.config_graph(k)
+    gh = emo.EmoGraph(g, device=0)
+    P, F = g.num_packs, g.num_levels
+    T0 = float(dp.eval_batch(g, np.full((1, P), F - 1, np.uint8))[0][0])
+    tgt = float(np.float32(1.05 * T0))
+    q = float(np.float32(0.05 * T0 / 64))
+    print(f"[case] dp on workload {k} tables: P={P} F={F} target={tgt} q={q}", flush=True)
+    r = dp.dp_search(g, tgt, q)
+    lv, sel = run(emo, gh, tgt, q)
+    assert r.levels is not None and sel.index >= 0
+    assert sel.makespan <= tgt
+    T, E = dp.eval_batch(g, lv[None, :])
+    assert float(np.float32(T[0])) == sel.makespan
+    assert abs(sel.energy - E[0]) <= 1e-5 * E[0]
+    assert abs(sel.energy - r.energy) <= 1e-5 * r.energy, (sel.energy, r.energy)
+    assert sel.index == math.floor(sel.makespan / float(np.float32(q)))
+    print(f"  energy {sel.energy} vs oracle {r.energy}; states {sel.num_feasible} vs {r.num_states}", flush=True)

@@ -52,6 +52,7 @@ def test_intervals_handworked(torch, emo):
         print(f"[case] intervals hand-worked {case['change_points']} {case['levels']}", flush=True)
         lv = dev(torch, np.asarray([case["levels"]], np.uint8))
         T, E, _, _ = gh.eval_intervals(lv, case["change_points"], d["idle_power"])
+        assert gh.info()["last_kernels"] == 7     # the kernel specialised to the graph
         T, E = host(T), host(E)
         if case["makespan"] is None:
             assert np.isnan(T[0]) and np.isnan(E[0]), case
@@ -83,7 +84,16 @@ def test_intervals_match_oracle_on_random_dags(torch, emo, seed):
         gh = emo.EmoGraph(g, device=0)
         lv = dev(torch, rows)
         T, E, _, _ = gh.eval_intervals(lv, pts, idle)
-        check(host(T), host(E), To, Eo, f"seed={seed} K={K}")
+        kind = gh.info()["last_kernels"]
+        assert kind in (0, 7)
+        check(host(T), host(E), To, Eo, f"seed={seed} K={K} kernels={kind}")
+        # the interpreting kernel gives the same bits
+        gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+        Ti, Ei, _, _ = gi.eval_intervals(lv, pts, idle)
+        assert gi.info()["last_kernels"] == 0
+        assert np.array_equal(host(T).view(np.uint32), host(Ti).view(np.uint32))
+        assert np.array_equal(host(E).view(np.uint32), host(Ei).view(np.uint32))
+        gi.close()
         finite = To[~np.isnan(To)]
         tgt = float(np.float32(np.quantile(finite, 0.4))) if finite.size else 1.0
         m = torch.empty(max(1, (B + 31) // 32), dtype=torch.int32, device="cuda")
@@ -155,3 +165,38 @@ def test_intervals_argument_errors(torch, emo):
         gh.eval_intervals(lv1, [12.0], [0.1, 0.1], latency_target=float("nan"), result=r)
     T, E, _, _ = gh.eval_intervals(lv1[:0], [12.0], [0.1, 0.1], result=r)
     assert emo.parse_selection(r).index == -1
+
+
+@pytest.mark.parametrize("K", [1, 16, 17, 256])
+def test_intervals_workload_kernels(torch, emo, K):
+    """The 64-pack graph's specialised time-interval kernel (row in LDS for K <= 16, read from
+    device memory above) on 200,000 candidates with K intervals evenly over [0, 1.05 T0): every
+    row bit for bit against the interpreting kernel, sampled rows against the oracle, invalid
+    levels and a ragged batch included."""
+    g = synth.config_graph(2)
+    B = 200_003
+    T0 = float(oracle.eval_batch(g, np.full((1, g.num_packs), g.num_levels - 1, np.uint8))[0][0])
+    pts = [float(synth.quantize(T0 * 1.05 * (i + 1) / K)) for i in range(K - 1)]
+    idle = [float(x) for x in synth.quantize(0.3 * (0.5 + 0.5 * synth.level_ratios(g.num_levels)))]
+    rows = synth.random_policies(12 + K, K, g.num_levels, 0, B, "uniform")
+    rows[7, K // 2] = 200
+    rows[B - 1, 0] = g.num_levels
+    print(f"[case] interval kernels on the 64-pack graph K={K} B={B}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    lv = dev(torch, rows)
+    tgt = float(np.float32(1.02 * T0))
+    m = torch.empty((B + 31) // 32, dtype=torch.int32, device="cuda")
+    r = torch.empty(3, dtype=torch.int64, device="cuda")
+    T, E, _, _ = gh.eval_intervals(lv, pts, idle, latency_target=tgt, mask=m, result=r)
+    assert gh.info()["last_kernels"] == 7
+    gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+    mi = torch.empty_like(m)
+    ri = torch.empty_like(r)
+    Ti, Ei, _, _ = gi.eval_intervals(lv, pts, idle, latency_target=tgt, mask=mi, result=ri)
+    assert np.array_equal(host(T).view(np.uint32), host(Ti).view(np.uint32))
+    assert np.array_equal(host(E).view(np.uint32), host(Ei).view(np.uint32))
+    assert torch.equal(m, mi) and torch.equal(r, ri)
+    assert np.isnan(host(T)[7]) and np.isnan(host(T)[B - 1])
+    pick = np.concatenate([synth.sample_rows(B, 200), [7]])
+    To, Eo = intervals.eval_intervals(g, pts, rows[pick], idle)
+    check(host(T)[pick], host(E)[pick], To, Eo, f"K={K} sampled rows")

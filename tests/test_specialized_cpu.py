@@ -174,3 +174,14 @@ def test_random_graph_kernels_compile(emo, hiprtc, tmp_path, seed):
         src = emo.EmoGraph(g, device=-1).specialized_source()
         path = compile_source(hiprtc, src, tmp_path)
         check_code_object(path, ["emo_sp_select"])
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_interval_kernels_compile(emo, hiprtc, tmp_path, k):
+    """The time-interval kernel of the small workloads (the 512-pack graph's 64 KB table in LDS,
+    the bucket table and the rows in dynamic LDS) compiles without spills, scratch, packed fp32
+    or flat accesses."""
+    g = synth.config_graph(k)
+    src = emo.EmoGraph(g, device=-1).interval_source()
+    path = compile_source(hiprtc, src, tmp_path)
+    notes, asm = check_code_object(path, ["emo_iv"])
