@@ -38,7 +38,7 @@ VALU_PEAK_TOPS = 39.3   # 256 CUs x 64 fp32 lanes x 2.4 GHz, one op per lane per
 KIND_SOURCES = {0: ("emo_kernels.hip",), 1: ("emo_jit.cpp",), 2: ("emo_jit.cpp",),
                 3: ("emo_chains.hip", "emo_kernels.hip"), 4: ("emo_chains.hip", "emo_kernels.hip"),
                 5: ("emo_jit.cpp",), 6: ("emo_chains.hip", "emo_kernels.hip"),
-                7: ("emo_jit.cpp",)}
+                7: ("emo_jit.cpp",), 8: ("emo_chains.hip",)}
 
 
 def kernel_source_hash(kind: int) -> str:
@@ -698,7 +698,7 @@ def run_workload(k, args, emo, synth, np, torch):
 
 def kernel_name(kind: int, slack: bool) -> str:
     """The evaluating kernel (or chain of kernels timed as one unit) of a kernel kind."""
-    return {2: "emo_chain", 3: "chains_kernel", 4: "chains_windowed", 5: "emo_cut", 6: "chains_scan",
+    return {2: "emo_chain", 3: "chains_kernel", 4: "chains_windowed", 5: "emo_cut", 6: "chains_scan", 8: "chains_scan_full",
             1: "emo_sp_slack" if slack else "emo_sp_select"}.get(
                 kind, "slack_kernel" if slack else "forward_kernel")
 

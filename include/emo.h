@@ -108,9 +108,11 @@ typedef struct {
                                      segments between cut nodes evaluated in parallel),
                                      6 two-pass chain scan (windowed chain lanes whose slack
                                      comes from a second forward pass, for chains with exact
-                                     time sums), 7 time-interval kernel specialised to the
-                                     graph (emo_eval_intervals; 0 there means the interpreting
-                                     kernel) */
+                                     time sums; only calls with slack), 7 time-interval kernel
+                                     specialised to the graph (emo_eval_intervals; 0 there
+                                     means the interpreting kernel), 8 two-pass chain scan
+                                     whose window copies and slack stores follow per-thread
+                                     plans fixed for the call (chain_scan_full) */
     int32_t chain_lanes;          /* lanes per candidate of the chain-lane kernels, 0 when the
                                      candidate-dependent nodes do not form at most 64 disjoint
                                      chains */
@@ -137,13 +139,20 @@ typedef struct {
                                      graphs too large for one specialised kernel use them
                                      when levels (and slack) are 16-byte aligned and fewer
                                      than 2^30 candidates are evaluated. */
-    int32_t chain_scan_window;    /* packs per window of the two-pass chain scan kernel
-                                     (last_kernels 6), 0 when it does not apply: the
+    int32_t chain_scan_window;    /* packs per window of the two-pass chain scan kernels
+                                     (last_kernels 6 and 8), 0 when it does not apply: the
                                      candidate-dependent nodes must form at most 16 disjoint
                                      chains visiting the windows in increasing order, P a
                                      multiple of 16, and every time sum exact as for
                                      cut_segments; calls use it when levels and slack are
                                      16-byte aligned */
+    int32_t chain_scan_full;      /* 1 when slack calls of the two-pass chain scan run the
+                                     kernel with per-thread copy plans (last_kernels 8): every
+                                     window lies wholly inside the graph (P a multiple of
+                                     chain_scan_window), a thread holds at most four 16-byte
+                                     pieces of a window's slack tile (at least
+                                     chain_scan_window / 16 chains) and a workgroup's slack
+                                     rows span less than 4 GiB; 0 otherwise */
     int32_t hip_runtime_version;  /* hipRuntimeGetVersion of the HIP runtime the library runs
                                      on (e.g. 70051831 for 7.0.51831).  The run-time compiler
                                      of the specialised kernels is the hiprtc of that same

@@ -375,6 +375,7 @@ gather_slack(const float *__restrict__ tmp, const int32_t *__restrict__ pos, int
 // sums are added in chain order.
 constexpr int kWinPre = 4;                         // 16-byte prefetch pieces per thread and window
 constexpr size_t kWinLds = 150 * 1024;
+constexpr size_t kWinSpare = 1024;                   // chains_scan_full: 16 spare bytes per lane
 constexpr int kWinMaxWaves = 16;
 
 __host__ __device__ inline uint32_t round16u(uint32_t x) { return (x + 15u) & ~15u; }
@@ -559,6 +560,201 @@ __device__ __forceinline__ void win_store(const WinArgs &a, char *lds, int buf, 
             const int q = t + (i - s_lvl - s_tab) * nt;
             if (q < n_blk) blk[q] = v;
         }
+    }
+}
+
+// Buffer resources of the planned copies: raw buffer accesses with a 32-bit per-lane offset and a
+// uniform offset, and the hardware's range check (an access at or past `bytes` reads zeros and
+// writes nothing).  The fourth word is the CDNA3/CDNA4 raw-buffer configuration.
+typedef unsigned int emo_u4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t win_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
+                                             static_cast<int>(bytes), 0x00020000);
+}
+// An offset past every planned buffer (they all hold less than 2^31 bytes, and a uniform offset
+// stays below 2^31 too): loads there read zeros and stores are dropped.
+constexpr uint32_t kWinNoStore = 0x80000000u;
+
+// The copy of a window wholly inside the graph (its W columns and table rows all exist), with
+// each thread's pieces at offsets fixed for the whole kernel: win_plan computes them once, and a
+// window then costs its loads, its stores and a few scalar operations.  A thread with no piece
+// in a slot loads past the slot's buffer (the range check returns zeros without touching memory)
+// and stores them to its lane's spare 16 bytes at LDS offset `spare` (so every load is waited
+// for and every store made on every path, which keeps the compiler's count of loads in flight
+// exact).
+struct WinPlan {
+    uint32_t src[kWinPre];    // byte offset of the piece in its slot's per-window source
+    uint32_t dst0[kWinPre];   // LDS byte offset of the piece in buffer 0 (or the spare)
+    uint32_t dst1[kWinPre];   // in buffer 1
+    uint32_t has;             // bit i: the thread has a piece in slot i
+};
+
+template <int NT>
+__device__ __forceinline__ WinPlan win_plan(const WinArgs &a, int esize, int64_t rows_left, int32_t P,
+                                            uint32_t spare) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int rlog = a.wlog - 4;
+    const int n_lvl = a.NC << rlog;
+    const int n_tab = (a.W * a.F * esize) >> 4;
+    const int n_blk = a.blk_bytes >> 4;
+    const int s_lvl = 1, s_tab = NT;
+    const uint32_t own = spare + 16u * static_cast<uint32_t>(t & 63);
+    WinPlan p;
+    p.has = 0u;
+#pragma unroll
+    for (int i = 0; i < kWinPre; ++i) {
+        bool ok = false;
+        uint32_t src = 0u, d0 = 0u, stride = 0u;
+        if (i < s_lvl) {
+            const int q = t + i * nt;
+            const int r = q >> rlog, k = q - (r << rlog);
+            const int rr = r < rows_left ? r : static_cast<int>(rows_left - 1);
+            ok = q < n_lvl;
+            src = static_cast<uint32_t>(rr) * static_cast<uint32_t>(P) + 16u * static_cast<uint32_t>(k);
+            d0 = static_cast<uint32_t>(r) * a.L.lvl_pitch + 16u * static_cast<uint32_t>(k);
+            stride = a.L.lvl_buf;
+        } else if (i < s_lvl + s_tab) {
+            const int q = t + (i - s_lvl) * nt;
+            ok = q < n_tab;
+            src = 16u * static_cast<uint32_t>(q);
+            d0 = a.L.off_x + 16u * static_cast<uint32_t>(q);
+            stride = a.L.tab_elems * static_cast<uint32_t>(esize);
+        } else if (i == s_lvl + s_tab) {
+            const int q = t + (i - s_lvl - s_tab) * nt;
+            ok = q < n_blk;
+            src = 16u * static_cast<uint32_t>(q);
+            d0 = a.L.off_blk + 16u * static_cast<uint32_t>(q);
+            stride = static_cast<uint32_t>(a.blk_bytes);
+        }
+        // an absent piece reads past its buffer's end (zeros, with no memory traffic)
+        p.src[i] = ok ? src : kWinNoStore;
+        p.dst0[i] = ok ? d0 : own;   // (slots past those in use: ok is false, the spare slot)
+        p.dst1[i] = ok ? d0 + stride : own;
+        p.has |= ok ? 1u << i : 0u;
+    }
+    return p;
+}
+
+// The per-workgroup buffers of a pass's planned copies: the workgroup's level rows, the pass's
+// table (8-byte entries forward, 4-byte in the second pass) and the step blocks.
+struct WinBufs {
+    __amdgpu_buffer_rsrc_t lvl, tab, blk;
+    int32_t tab_win;   // table bytes per window: W * F * esize
+};
+
+// Issues the loads of window w (wholly inside the graph) from the plan.  The slots are fixed at
+// compile time: slot 0 levels, slots 1 .. NT the table, slot NT + 1 the step block.
+template <int NT>
+__device__ __forceinline__ void win_load_full(const WinArgs &a, const WinPlan &p, const WinBufs &b, int w,
+                                              WinSet &s) {
+    const int so_lvl = w << a.wlog, so_tab = w * b.tab_win, so_blk = w * a.blk_bytes;
+#pragma unroll
+    for (int i = 0; i < NT + 2; ++i) {
+        emo_u4 v;
+        if (i == 0) v = __builtin_amdgcn_raw_buffer_load_b128(b.lvl, p.src[i], so_lvl, 0);
+        else if (i <= NT) v = __builtin_amdgcn_raw_buffer_load_b128(b.tab, p.src[i], so_tab, 0);
+        else v = __builtin_amdgcn_raw_buffer_load_b128(b.blk, p.src[i], so_blk, 0);
+        s.v[i] = make_uint4(v.x, v.y, v.z, v.w);
+    }
+    s.zero = 0u;
+}
+
+// Stores a window loaded by win_load_full<NT> at the plan's destinations `dst` (its dst0 or
+// dst1), with no branches.  In the forward pass (`badbits` given) the thread's level piece with
+// a byte >= F sets bit 0 of *badbits; the caller marks the rows at the end of the pass.  hib: the
+// bits of a byte at or above F when F is a power of two (then one mask test), else 0.
+template <int NT>
+__device__ __forceinline__ void win_store_full(const WinPlan &p, const uint32_t *dst, char *lds,
+                                               uint32_t *badbits, uint32_t addf, uint32_t hib, const WinSet &s) {
+#pragma unroll
+    for (int i = 0; i < NT + 2; ++i) {
+        const uint4 v = s.v[i];
+        if (i == 0) {
+            if (badbits) {
+                const uint32_t b = hib ? (v.x | v.y | v.z | v.w) & hib
+                                       : bad_levels(v.x, addf) | bad_levels(v.y, addf) | bad_levels(v.z, addf) |
+                                             bad_levels(v.w, addf);
+                *badbits |= b && (p.has & 1u) ? 1u : 0u;
+            }
+            // level rows are 4-byte aligned (odd pitch in words)
+            uint32_t *d = reinterpret_cast<uint32_t *>(lds + dst[0]);
+            d[0] = v.x;
+            d[1] = v.y;
+            d[2] = v.z;
+            d[3] = v.w;
+        } else {
+            *reinterpret_cast<uint4 *>(lds + dst[i]) = v;
+        }
+    }
+}
+
+// Marks the rows of the forward pass's level pieces that held a byte >= F (after the pass; the
+// caller's barrier then makes bad[] complete).
+__device__ __forceinline__ void win_mark_bad(const WinArgs &a, uint32_t badbits, uint32_t *bad) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int rlog = a.wlog - 4;
+    (void)nt;
+    if (badbits & 1u) bad[t >> rlog] = 1u;
+}
+
+// The slack tile's flush when every window lies wholly inside the graph, with each thread's (at
+// most four) pieces at LDS and global offsets fixed for the whole kernel: piece j of the thread
+// is float4 piece q = t + j * nt of the tile in the order of the general flush.  Global offsets
+// are bytes from the workgroup's first row at the window's first column (32-bit: NC * P * 4 <
+// 2^32).
+struct FlushPlan {
+    uint32_t src[4];   // LDS byte offset of the piece's first float
+    uint32_t dst[4];   // byte offset in the slack rows
+    uint32_t has;      // bit j: the piece exists and its row is in the batch
+    uint32_t nan;      // bit j: the piece's candidate has an invalid level (its slack row is NaN)
+};
+
+// (after the forward pass: tfin holds the makespans, NaN for a candidate with an invalid level)
+__device__ __forceinline__ FlushPlan flush_plan(const WinArgs &a, int64_t rows_left, int32_t P, const float *tfin) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int W = a.W, prlog = a.wlog - 2;
+    const int n = a.NC << prlog;
+    FlushPlan f;
+    f.has = 0u;
+    f.nan = 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int q = t + j * nt;
+        int r, kk;
+        if (prlog >= 4) {
+            const int jj = q & 63, blk = q >> 6, kblog = prlog - 4;
+            const int rg = blk >> kblog, kb = blk & ((1 << kblog) - 1);
+            r = rg * 4 + (jj >> 4);
+            kk = kb * 16 + (jj & 15);
+        } else {
+            r = q >> prlog;
+            kk = q & ((1 << prlog) - 1);
+        }
+        const bool ok = q < n && r < rows_left;
+        f.src[j] = ok ? a.L.off_tile + 4u * static_cast<uint32_t>(r * (W + 1) + 4 * kk) : a.L.off_tile;
+        f.dst[j] = ok ? 4u * (static_cast<uint32_t>(r) * static_cast<uint32_t>(P) + 4u * static_cast<uint32_t>(kk))
+                      : kWinNoStore;
+        f.has |= ok ? 1u << j : 0u;
+        const float tr = tfin[ok ? r : 0];
+        f.nan |= ok && tr != tr ? 1u << j : 0u;
+    }
+    return f;
+}
+
+// `rows`: the workgroup's slack rows (S from its first row, a range check at the batch's end);
+// pieces a thread does not have and rows past the batch store at kWinNoStore, which the range
+// check drops, so no store needs a lane mask
+__device__ __forceinline__ void flush_full(const FlushPlan &f, __amdgpu_buffer_rsrc_t rows, const char *lds, int w,
+                                           int wlog) {
+    const int so = (w << wlog) * 4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float *src = reinterpret_cast<const float *>(lds + f.src[j]);
+        float4 v = make_float4(src[0], src[1], src[2], src[3]);
+        if ((f.nan >> j) & 1u) v = make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""),
+                                               __builtin_nanf(""));
+        const emo_u4 u = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
+        __builtin_amdgcn_raw_buffer_store_b128(u, rows, f.dst[j], so, 0);
     }
 }
 
@@ -937,6 +1133,214 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     }
 }
 
+// The two-pass chain scan (chains_windowed with SCAN) for the layouts where every window lies
+// wholly inside the graph (P a multiple of W) and a thread holds at most four pieces of the slack
+// tile: every window copy and every flush follows a per-thread plan fixed for the kernel, so the
+// per-window work is the loads, the LDS stores, the flush stores and the barriers, with no bounds
+// checks, category tests or zeroing.  The walk of each window is that of chains_windowed; a
+// candidate with an invalid level gets its NaN row from the flush plan.
+template <bool FIXED, int NT8>
+__global__ void __launch_bounds__(kChainBlockThreads)
+chains_scan_full(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ blocks,
+                 const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ To,
+                 float *__restrict__ Eo, float *__restrict__ S) {
+    extern __shared__ float4 smem[];
+    char *lds = reinterpret_cast<char *>(smem);
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int grp = wv / a.nc, ch = wv - grp * a.nc;
+    const int lane = t & 63;
+    const int cl = grp * 64 + lane;                               // candidate within the workgroup
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * a.NC;
+    const int64_t gc = base + cl;
+    const int W = a.W, F = a.F, nc = a.nc, nwin = c.nwin;
+    const int32_t P = g.P;
+    const WinLayout &L = a.L;
+    const int64_t rows_left = B - base;
+    uint8_t *lvl0 = reinterpret_cast<uint8_t *>(lds);             // [2][NC][W + 4] bytes
+    uint32_t *bad = reinterpret_cast<uint32_t *>(lds + L.off_bad);
+    float *tfin = reinterpret_cast<float *>(lds + L.off_tfin);
+    float2 *tab2 = reinterpret_cast<float2 *>(lds + L.off_x);     // forward: [2][W + 1][F]
+    float *tabt = reinterpret_cast<float *>(lds + L.off_x);       // second pass: [2][W + 1][F]
+    float *tile = reinterpret_cast<float *>(lds + L.off_tile);    // second pass: [NC][W + 1]
+    const uint32_t addf = (0x80u - static_cast<uint32_t>(F)) * 0x01010101u;
+    // the bits of a byte that is >= F when F is a power of two
+    const uint32_t hib = (F & (F - 1)) == 0 ? (0xffu & ~static_cast<uint32_t>(F - 1)) * 0x01010101u : 0u;
+    auto recs = [&](int buf) {
+        return reinterpret_cast<const ChainWinStep *>(lds + L.off_blk + buf * a.blk_bytes + 4 * a.hdr_words);
+    };
+
+    // ------------------------------------------------------------------ forward
+    for (int i = t; i < a.NC; i += nt) {
+        bad[i] = 0u;
+        *reinterpret_cast<uint32_t *>(lvl0 + i * L.lvl_pitch + W) = 0u;
+        *reinterpret_cast<uint32_t *>(lvl0 + L.lvl_buf + i * L.lvl_pitch + W) = 0u;
+    }
+    for (int i = t; i < F; i += nt) {
+        tab2[W * F + i] = make_float2(0.f, 0.f);
+        tab2[L.tab_elems + W * F + i] = make_float2(0.f, 0.f);
+    }
+    const uint32_t spare = L.total;                               // 1 KiB past the layout: spare slots
+    WinPlan plan = win_plan<NT8>(a, 8, rows_left, P, spare);
+    uint32_t badbits = 0u;
+    const int64_t nrows = rows_left < a.NC ? rows_left : a.NC;
+    WinBufs bf;
+    bf.lvl = win_rsrc(levels + base * P, static_cast<uint32_t>(nrows * P));
+    bf.tab = win_rsrc(g.tab, static_cast<uint32_t>(static_cast<int64_t>(P) * F * 8));
+    bf.blk = win_rsrc(blocks, static_cast<uint32_t>(static_cast<int64_t>(nwin) * a.blk_bytes));
+    bf.tab_win = W * F * 8;
+    WinSet s0, s1;
+    win_load_full<NT8>(a, plan, bf, 0, s0);
+    win_load_full<NT8>(a, plan, bf, nwin > 1 ? 1 : 0, s1);
+    lds_barrier();
+    win_store_full<NT8>(plan, plan.dst0, lds, &badbits, addf, hib, s0);
+    lds_barrier();
+    float f = 0.f, pre = 0.f;
+    double ed = 0.0;
+    // window w from buffer buf = w & 1; `ld` takes window w + 2, `cm` holds window w + 1
+    auto forward_window = [&](int w, int buf, WinSet &ld, WinSet &cm) {
+        win_load_full<NT8>(a, plan, bf, w + 2 < nwin ? w + 2 : nwin - 1, ld);
+        const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
+        const char *tb = reinterpret_cast<const char *>(tab2 + buf * L.tab_elems);
+        const ChainWinStep *rs = recs(buf);
+        int k0, k1;
+        win_range(a, lds, buf, ch, k0, k1);
+        float eb = 0.f;
+        const int ng = (k1 - k0) >> 2;
+        auto stage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int gi) {
+            float2 te[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                te[i] = *reinterpret_cast<const float2 *>(tb + (((A.ct[i] >> 16) + A.lv[i]) << 3));
+            Bn.levels(lrow);
+            C.read(rs, k0 + 4 * (gi + 2));
+            win_issue_point();
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                f = fmax_nonneg(f, A.cst[i]) + te[i].x;
+                pre += te[i].x;
+                if (FIXED) {
+                    f += A.dur[i];
+                    pre += A.dur[i];
+                }
+                eb += te[i].y;
+            }
+        };
+        WinGroup<FIXED> G0, G1, G2;
+        G0.read(rs, k0);
+        G1.read(rs, k0 + 4);
+        G0.levels(lrow);
+        for (int gi = 0; gi < ng; gi += 3) {
+            stage(G0, G1, G2, gi);
+            if (gi + 1 >= ng) break;
+            stage(G1, G2, G0, gi + 1);
+            if (gi + 2 >= ng) break;
+            stage(G2, G0, G1, gi + 2);
+        }
+        ed += static_cast<double>(eb);
+        // (after the last window: a copy of it into the idle buffer, which nothing reads)
+        win_store_full<NT8>(plan, buf ? plan.dst0 : plan.dst1, lds, &badbits, addf, hib, cm);
+        lds_barrier();
+    };
+    for (int w = 0; w < nwin; w += 2) {
+        forward_window(w, 0, s0, s1);
+        if (w + 1 < nwin) forward_window(w + 1, 1, s1, s0);
+    }
+    win_mark_bad(a, badbits, bad);
+    // chains' makespans and energies -> the candidate's (chain order)
+    double *esum = reinterpret_cast<double *>(lds + L.off_x);
+    float *tsum = reinterpret_cast<float *>(lds + L.off_x + 8 * 64 * kWinMaxWaves);
+    esum[wv * 64 + lane] = ed;
+    tsum[wv * 64 + lane] = f;
+    lds_barrier();
+    if (ch == 0) {
+        float T = c.t_const;
+        double e = 0.0;
+        for (int j = 0; j < nc; ++j) {
+            T = fmaxf(T, tsum[(grp * nc + j) * 64 + lane]);
+            e += esum[(grp * nc + j) * 64 + lane];
+        }
+        float E = static_cast<float>(e + static_cast<double>(g.static_power) * static_cast<double>(T));
+        if (bad[cl]) {
+            T = __builtin_nanf("");
+            E = __builtin_nanf("");
+        }
+        tfin[cl] = T;
+        if (gc < B) {
+            To[gc] = T;
+            Eo[gc] = E;
+        }
+    }
+    lds_barrier();
+
+    // ---------------------------------------------------------------- second forward pass
+    // slack_i = K - D_i with K = T - Tot, carried as Q = K + Pre and Z = K - D (see
+    // chains_windowed); a candidate with an invalid level (K = NaN) gets NaN from the flush
+    const FlushPlan fp = flush_plan(a, rows_left, P, tfin);
+    const __amdgpu_buffer_rsrc_t srows = win_rsrc(S + base * P, static_cast<uint32_t>(nrows * P * 4));
+    plan = win_plan<1>(a, 4, rows_left, P, spare);
+    bf.tab = win_rsrc(g.tabt, static_cast<uint32_t>(static_cast<int64_t>(P) * F * 4));
+    bf.tab_win = W * F * 4;
+    for (int i = t; i < F; i += nt) {
+        tabt[W * F + i] = 0.f;
+        tabt[L.tab_elems + W * F + i] = 0.f;
+    }
+    const float Kc = tfin[cl] - pre;
+    const float K = Kc == Kc ? Kc : 0.f;
+    float Z = K, Q = K;
+    win_load_full<1>(a, plan, bf, 0, s0);
+    win_load_full<1>(a, plan, bf, nwin > 1 ? 1 : 0, s1);
+    win_store_full<1>(plan, plan.dst0, lds, nullptr, addf, hib, s0);
+    lds_barrier();
+    float *trow = tile + cl * (W + 1);
+    auto scan_window = [&](int w, int buf, WinSet &ld, WinSet &cm) {
+        win_load_full<1>(a, plan, bf, w + 2 < nwin ? w + 2 : nwin - 1, ld);
+        const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
+        const char *tb = reinterpret_cast<const char *>(tabt + buf * L.tab_elems);
+        const ChainWinStep *rs = recs(buf);
+        int k0, k1;
+        win_range(a, lds, buf, ch, k0, k1);
+        const int ng = (k1 - k0) >> 2;
+        auto stage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int gi) {
+            float tt[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                tt[i] = *reinterpret_cast<const float *>(tb + (((A.ct[i] >> 16) + A.lv[i]) << 2));
+                if (FIXED) tt[i] += A.dur[i];
+            }
+            Bn.levels(lrow);
+            C.read(rs, k0 + 4 * (gi + 2));
+            win_issue_point();
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                // both operands are >= 0: Q_{i-1} - cst_i >= K - D_i = slack_i
+                Z = fmin_nonneg(Z, Q - A.cst[i]);
+                Q += tt[i];
+                trow[A.ct[i] & 0xffffu] = Z;
+            }
+        };
+        WinGroup<FIXED> G0, G1, G2;
+        G0.read(rs, k0);
+        G1.read(rs, k0 + 4);
+        G0.levels(lrow);
+        for (int gi = 0; gi < ng; gi += 3) {
+            stage(G0, G1, G2, gi);
+            if (gi + 1 >= ng) break;
+            stage(G1, G2, G0, gi + 1);
+            if (gi + 2 >= ng) break;
+            stage(G2, G0, G1, gi + 2);
+        }
+        win_store_full<1>(plan, buf ? plan.dst0 : plan.dst1, lds, nullptr, addf, hib, cm);
+        lds_barrier();
+        flush_full(fp, srows, lds, w, a.wlog);
+        lds_barrier();
+    };
+    for (int w = 0; w < nwin; w += 2) {
+        scan_window(w, 0, s0, s1);
+        if (w + 1 < nwin) scan_window(w + 1, 1, s1, s0);
+    }
+}
+
 int64_t chain_grid(const DevChains &c, int64_t B) {
     return ((B << c.lane_log) + kChainBlockThreads - 1) / kChainBlockThreads;
 }
@@ -965,7 +1369,11 @@ bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int3
 }
 
 bool chains_scan_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
-    return c.exact && chains_windowed_ok(c, levels, slack);
+    return c.exact && slack && chains_windowed_ok(c, levels, slack);
+}
+
+bool chains_scan_full_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
+    return c.full && chains_scan_ok(c, levels, slack);
 }
 
 bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
@@ -1019,6 +1427,26 @@ hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, c
     return hipGetLastError();
 }
 
+template <bool FIXED, int NT8>
+hipError_t launch_scan_full_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, const DevGraph &g,
+                                   const DevChains &c, const WinArgs &a, const uint8_t *levels, int64_t B,
+                                   float *T, float *E, float *S) {
+    static std::atomic<uint64_t> done{0};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
+    if (!bit || !(done.load(std::memory_order_acquire) & bit)) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chains_scan_full<FIXED, NT8>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kWinLds + kWinSpare));
+        if (e != hipSuccess) return e;
+        done.fetch_or(bit, std::memory_order_acq_rel);
+    }
+    hipLaunchKernelGGL((chains_scan_full<FIXED, NT8>), gd, bd, lds + kWinSpare, s, g, c, a, c.blocks, levels, B, T,
+                       E, S);
+    return hipGetLastError();
+}
+
 hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
                            float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
                            void *scratch, hipStream_t s) {
@@ -1050,7 +1478,15 @@ hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t 
     const size_t lds = a.L.total;
     hipError_t e;
 #define EMO_WIN_ARGS gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch
-    if (slack && scan) e = c.fixed ? launch_windowed_kernel<true, true, true>(EMO_WIN_ARGS)
+    if (slack && scan && c.full) {
+        // one or two 16-byte forward table pieces per thread (c.full guarantees the rest of the
+        // slot layout: one level piece, one block piece, one second-pass table piece)
+        const bool two = a.slots_tab8 == 2;
+        e = c.fixed ? (two ? launch_scan_full_kernel<true, 2>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack)
+                           : launch_scan_full_kernel<true, 1>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack))
+                    : (two ? launch_scan_full_kernel<false, 2>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack)
+                           : launch_scan_full_kernel<false, 1>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack));
+    } else if (slack && scan) e = c.fixed ? launch_windowed_kernel<true, true, true>(EMO_WIN_ARGS)
                                    : launch_windowed_kernel<true, false, true>(EMO_WIN_ARGS);
     else if (slack) e = c.fixed ? launch_windowed_kernel<true, true, false>(EMO_WIN_ARGS)
                                 : launch_windowed_kernel<true, false, false>(EMO_WIN_ARGS);

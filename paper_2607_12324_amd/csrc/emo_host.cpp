@@ -716,6 +716,21 @@ bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
         dc->fixed = fixed;
         dc->hdr_words = hdr_words;
         dc->blk_bytes = blk_bytes;
+        // per-thread plans of chains_scan_full: NC = 64 G candidates, 64 G nc threads and
+        // NC * W / 4 float4 pieces of the slack tile per window
+        // (and the copy slots that kernel is compiled for: one level piece, one or two forward
+        // and one second-pass table pieces and one step-block piece per thread)
+        const int64_t NC = 64 * static_cast<int64_t>(G);
+        const int64_t nthr = 64 * static_cast<int64_t>(G) * nc;
+        const int64_t tab8 = (static_cast<int64_t>(W) * g.F / 2 + nthr - 1) / nthr;
+        const int64_t tab4 = (static_cast<int64_t>(W) * g.F / 4 + nthr - 1) / nthr;
+        const bool slots = NC * (W / 16) <= nthr && (tab8 == 1 || tab8 == 2) && tab4 == 1 && blk_bytes / 16 <= nthr;
+        dc->full = slots && g.P % W == 0 && NC * W / 4 <= 4 * nthr &&
+                           NC * g.P * 4 < (int64_t(1) << 31) &&
+                           static_cast<int64_t>(g.P) * g.F * 8 < (int64_t(1) << 31) &&
+                           static_cast<int64_t>(nwin) * blk_bytes < (int64_t(1) << 31)
+                       ? 1
+                       : 0;
         return true;
     }
     return false;
@@ -1198,6 +1213,7 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     in.chain_lanes = chains_ok ? dc.lanes : 0;
     in.chain_window = chains_ok ? dc.win : 0;
     in.chain_scan_window = chains_ok && dc.exact ? dc.win : 0;
+    in.chain_scan_full = chains_ok && dc.exact && dc.full ? 1 : 0;
     const int32_t nops = static_cast<int32_t>(sf.seq.size());
     g->jit_eligible = nops >= 1 && nops <= kJitMaxOps;
     g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;
@@ -1400,7 +1416,9 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     }
     void *part = result ? scratch : nullptr;
     void *work = scratch ? static_cast<char *>(scratch) + part_bytes : nullptr;
-    g->info.last_kernels = path == Path::kChainLanes && emo::chains_scan_ok(g->chains, levels, slack)
+    g->info.last_kernels = path == Path::kChainLanes && emo::chains_scan_full_ok(g->chains, levels, slack)
+                               ? 8
+                               : path == Path::kChainLanes && emo::chains_scan_ok(g->chains, levels, slack)
                                ? 6
                                : path == Path::kChainLanes && emo::chains_windowed_ok(g->chains, levels, slack)
                                      ? 4

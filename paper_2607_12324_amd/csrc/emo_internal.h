@@ -164,6 +164,10 @@ struct DevChains {
     // slack by a second forward pass (chains_windowed with SCAN): the windowed layout exists and
     // every time sum is exact
     int32_t exact = 0;
+    // every window lies wholly inside the graph (P a multiple of win), a thread of the windowed
+    // kernel holds at most four float4 pieces of the slack tile, and a workgroup's slack rows
+    // span less than 2^32 bytes: the second-pass kernel with per-thread copy plans applies
+    int32_t full = 0;
 };
 // Whether the windowed kernel's LDS working set and prefetch fit for `nc` chains, F levels,
 // windows of W packs and step blocks of blk_bytes; sets the candidate groups per workgroup.
@@ -174,6 +178,8 @@ bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *
 // Whether a call runs the windowed kernel with slack from a second forward pass (the windowed
 // layout exists, the graph's time sums are exact and the buffers are 16-byte aligned).
 bool chains_scan_ok(const DevChains &c, const uint8_t *levels, const float *slack);
+// Whether that call runs the second-pass kernel with per-thread copy plans (chains_scan_full).
+bool chains_scan_full_ok(const DevChains &c, const uint8_t *levels, const float *slack);
 // Scratch of launch_chains: backward checkpoints and chain-ordered slack (slack only), and
 // makespan/energy buffers.
 size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,

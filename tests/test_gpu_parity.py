@@ -482,14 +482,17 @@ def test_chain_lanes(torch, emo, case):
     assert gh.info()["chain_window"] == win
     # on the time grid the two-pass scan kernel takes the windowed layout's place
     assert gh.info()["chain_scan_window"] == win
-    kind = 6 if win else 3
+    # without slack the windowed kernel; with it the two-pass scan (per-thread copy plans when
+    # every window is full and there are enough chains)
+    kind = 4 if win else 3
+    skind = (8 if gh.info()["chain_scan_full"] else 6) if win else 3
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
     assert gh.info()["last_kernels"] == kind
     S = gh.slack(lv)
     torch.cuda.synchronize()
-    assert gh.info()["last_kernels"] == kind
+    assert gh.info()["last_kernels"] == skind
     ok = ~np.isnan(T_or)
     assert not ok[5] and not ok[600] and not ok[7]
     parity.assert_eval(host(T), host(E), T_or, E_or, True, case)
@@ -550,6 +553,7 @@ def test_chain_windows_small_batches(torch, emo, grid):
     gh = emo.EmoGraph(g, device=0)
     assert gh.info()["chain_window"] == 256
     assert gh.info()["chain_scan_window"] == (256 if grid == "on" else 0)
+    assert gh.info()["chain_scan_full"] == 0     # 8208 packs: the last window is partial
     scan = grid == "on"
     for B in (1, 3, 64, 65):
         rows = pins.random_rows(rng, g, B)
@@ -558,7 +562,7 @@ def test_chain_windows_small_batches(torch, emo, grid):
         T, E = gh.eval_policies(lv)
         S = gh.slack(lv)
         torch.cuda.synchronize()
-        assert gh.info()["last_kernels"] == (6 if scan else 4)
+        assert gh.info()["last_kernels"] == (6 if scan else 4)     # (the slack call)
         T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
         parity.assert_eval(host(T), host(E), T_or, E_or, True, f"windowed B={B}")
         S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(B)])
@@ -570,12 +574,13 @@ def test_chain_windows_small_batches(torch, emo, grid):
         assert np.array_equal(host(S).view(np.uint32), host(S2).view(np.uint32))
 
 
-@pytest.mark.parametrize("lengths", [[3100, 2900, 3400], [3100, 2900, 3406]],
-                         ids=["lane-per-chain", "windowed"])
+@pytest.mark.parametrize("lengths", [[3100, 2900, 3400], [3100, 2900, 3406], [768] * 16],
+                         ids=["lane-per-chain", "windowed", "scan-full"])
 def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
     """Chains that mix packs with fixed-duration nodes (which depend on the candidate through the
     pack before them), constant floors from a host node, and chains of different lengths (6268
-    packs: lane-per-chain kernel; 6272 packs: windowed kernel)."""
+    packs: lane-per-chain kernel; 6272 packs: windowed kernels; 16 chains of 512 packs: the
+    two-pass scan with per-thread copy plans, every 256-pack window full)."""
     rng = np.random.default_rng(42)
     src, dst, pack, dur = [], [], [], []
     h0 = 0   # a host node: candidate-independent floor for some chain nodes
@@ -609,20 +614,24 @@ def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
     rows = pins.random_rows(rng, g, 300)
     print(f"[case] chain lanes with fixed nodes: V={V} P={P}", flush=True)
     gh = emo.EmoGraph(g, device=0)
-    assert gh.info()["chain_lanes"] == 4
+    full = len(lengths) == 16
+    assert gh.info()["chain_lanes"] == (16 if full else 4)
     windowed = P % 16 == 0
-    assert gh.info()["chain_window"] == (64 if windowed else 0)
-    assert gh.info()["chain_scan_window"] == (64 if windowed else 0)
+    win = 256 if full else 64
+    assert gh.info()["chain_window"] == (win if windowed else 0)
+    assert gh.info()["chain_scan_window"] == (win if windowed else 0)
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
     S = gh.slack(lv)
-    assert gh.info()["last_kernels"] == (6 if windowed else 3)
+    # (3 chains are too few for the per-thread plans of 64-pack windows)
+    assert gh.info()["chain_scan_full"] == (1 if full else 0)
+    assert gh.info()["last_kernels"] == ((8 if full else 6) if windowed else 3)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, "chains with fixed nodes")
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(len(rows))])
     parity.assert_slack(host(S), S_or, T_or, True, "chains with fixed nodes: pack slack")
     if windowed:
-        check_windowed_off_grid(torch, emo, g, rows, 64, "chains with fixed nodes")
+        check_windowed_off_grid(torch, emo, g, rows, win, "chains with fixed nodes")
 
 
 def skewed_chains(seed, P, S, F, share):
@@ -662,6 +671,7 @@ def test_chain_scan_long_window_lists(torch, emo):
     g = skewed_chains(5, 8448, 16, 16, 0.9)
     gh = emo.EmoGraph(g, device=0)
     assert gh.info()["chain_scan_window"] == 256, gh.info()
+    assert gh.info()["chain_scan_full"] == 1, gh.info()
     rng = np.random.default_rng(6)
     rows = pins.random_rows(rng, g, 130)
     rows[77, 4000] = 16
@@ -670,7 +680,7 @@ def test_chain_scan_long_window_lists(torch, emo):
     T, E = gh.eval_policies(lv)
     S = gh.slack(lv)
     torch.cuda.synchronize()
-    assert gh.info()["last_kernels"] == 6
+    assert gh.info()["last_kernels"] == 8
     T_or, E_or, S_or = oracle.slack_batch(g, rows, nthreads=8)
     assert np.isnan(T_or[77])
     parity.assert_eval(host(T), host(E), T_or, E_or, True, "skewed chains")
@@ -890,7 +900,7 @@ def test_workload_full_batch(torch, emo, k):
     # one specialised kernel up to 2048 steps, cut-segment kernels for the 4096-pack graph (16
     # synchronisations), chain lanes for the 65536-kernel graph (16 stream chains)
     inf = gh.info()
-    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 5, 5: 6}[k], inf
+    assert inf["last_kernels"] == {1: 1, 2: 1, 3: 1, 4: 5, 5: 4}[k], inf
     if k <= 4:
         # the interpreting kernels on the same batch: bit-identical
         gi = emo.EmoGraph(g, device=0, kernel_mode=1)
@@ -914,7 +924,7 @@ def test_workload_full_batch(torch, emo, k):
     S = gh.slack(lv)
     # slack: one kernel while every finish time fits in registers, then segmented kernels
     # (cut segments for the 4096-pack graph)
-    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 5, 5: 6}[k], gh.info()
+    assert gh.info()["last_kernels"] == {1: 1, 2: 1, 3: 2, 4: 5, 5: 8}[k], gh.info()
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in pick])
     idx = torch.from_numpy(pick).cuda()
     parity.assert_slack(host(S.index_select(0, idx)), S_or, T_or[pick], True, spec.name + " slack")
