@@ -81,33 +81,46 @@ __global__ void dp_bucket(const float *__restrict__ T, const float *__restrict__
 // rows next_rows[b * F + f] (level f at p_next); after the last stage it is copied to state[b]
 // with its makespan Tst[b].  Also clears done_keys (the keys of this stage's source states, no
 // longer read), which the next stage's bucket step fills.
+// Grid: x covers a row in pieces (16 bytes when P is a multiple of 16, else single bytes), y the
+// output rows (next_rows or state); row y of the expansion is bucket y / F at level y % F.
 __global__ void dp_advance(const uint8_t *__restrict__ rows, const float *__restrict__ T,
                            const unsigned long long *__restrict__ keys, int64_t NB, int32_t P,
                            int32_t F, int32_t p_next, uint8_t *__restrict__ next_rows,
                            uint8_t *__restrict__ state, float *__restrict__ Tst,
                            unsigned long long *__restrict__ done_keys) {
-    const int64_t per = p_next >= 0 ? static_cast<int64_t>(F) * P : P;   // bytes per bucket
-    const int64_t n = NB * per;
-    for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
-         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int64_t b = i / per;
-        const unsigned long long k = keys[b];
-        if (k == kEmptyKey) continue;
-        const int64_t c = static_cast<int64_t>(k & 0xffffffffull);
-        const int64_t j = i - b * per;
-        if (p_next >= 0) {
-            const int32_t f = static_cast<int32_t>(j / P), col = static_cast<int32_t>(j - static_cast<int64_t>(f) * P);
-            next_rows[i] = col == p_next ? static_cast<uint8_t>(f) : rows[c * P + col];
-        } else {
-            state[i] = rows[c * P + j];
+    const int64_t nrows = p_next >= 0 ? NB * F : NB;
+    const bool vec = P % 16 == 0;
+    const int32_t npiece = vec ? P / 16 : P;
+    const int32_t x = static_cast<int32_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (x < npiece) {
+        for (int64_t y = blockIdx.y; y < nrows; y += gridDim.y) {
+            const int64_t b = p_next >= 0 ? y / F : y;
+            const unsigned long long k = keys[b];
+            if (k == kEmptyKey) continue;
+            const int64_t c = static_cast<int64_t>(k & 0xffffffffull);
+            const uint8_t f = static_cast<uint8_t>(y - b * F);
+            uint8_t *dst = (p_next >= 0 ? next_rows : state) + y * P;
+            const uint8_t *src = rows + c * P;
+            if (vec) {
+                uint4 v = reinterpret_cast<const uint4 *>(src)[x];
+                const int32_t o = p_next - 16 * x;   // the pack's byte within this piece, if any
+                if (p_next >= 0 && o >= 0 && o < 16) {
+                    uint32_t *w = o < 4 ? &v.x : (o < 8 ? &v.y : (o < 12 ? &v.z : &v.w));
+                    const int sh = 8 * (o & 3);
+                    *w = (*w & ~(0xffu << sh)) | (static_cast<uint32_t>(f) << sh);
+                }
+                reinterpret_cast<uint4 *>(dst)[x] = v;
+            } else {
+                dst[x] = x == p_next ? f : src[x];
+            }
         }
     }
-    for (int64_t b = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; b < NB;
-         b += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const unsigned long long k = keys[b];
-        if (k != kEmptyKey) Tst[b] = T[k & 0xffffffffull];
-        done_keys[b] = kEmptyKey;
-    }
+    if (blockIdx.x == 0 && blockIdx.y == 0)
+        for (int64_t b = threadIdx.x; b < NB; b += blockDim.x) {
+            const unsigned long long k = keys[b];
+            if (k != kEmptyKey) Tst[b] = T[k & 0xffffffffull];
+            done_keys[b] = kEmptyKey;
+        }
 }
 
 // The least (energy, bucket) over the stored states whose makespan meets tmax: its level row
@@ -185,9 +198,11 @@ hipError_t dp_launch_bucket(const float *T, const float *E, const unsigned long 
 hipError_t dp_launch_advance(const uint8_t *rows, const float *T, const unsigned long long *keys,
                              int64_t NB, int32_t P, int32_t F, int32_t p_next, uint8_t *next_rows,
                              uint8_t *state, float *Tst, unsigned long long *done_keys, hipStream_t s) {
-    const int64_t per = p_next >= 0 ? static_cast<int64_t>(F) * P : P;
-    dp_advance<<<blocks_for(std::max<int64_t>(NB * per, NB)), kThreads, 0, s>>>(
-        rows, T, keys, NB, P, F, p_next, next_rows, state, Tst, done_keys);
+    const int64_t nrows = p_next >= 0 ? NB * F : NB;
+    const int64_t npiece = P % 16 == 0 ? P / 16 : P;
+    const dim3 grid(static_cast<unsigned>(std::max<int64_t>((npiece + kThreads - 1) / kThreads, 1)),
+                    static_cast<unsigned>(std::min<int64_t>(std::max<int64_t>(nrows, 1), 65535)));
+    dp_advance<<<grid, kThreads, 0, s>>>(rows, T, keys, NB, P, F, p_next, next_rows, state, Tst, done_keys);
     return hipGetLastError();
 }
 

@@ -289,10 +289,13 @@ struct CutPlan {
     std::vector<int32_t> blk0;      // first energy block row of each segment; blk0[m] = rows
     std::vector<char> ck;           // f_i is read by a later sub-segment of its segment
     int block = 512;                // workgroup of the segment kernels and the finishing kernel
-    int per_kernel = 4;             // segments per segment kernel (grid rows); the kernels of
-                                    // consecutive groups of segments run one after another
+    int per_kernel = 4;             // segments per slack segment kernel (grid rows); the kernels
+                                    // of consecutive groups of segments run one after another
+    int per_kernel_fwd = 16;        // segments per forward-only segment kernel (smaller code: more
+                                    // segments per kernel, so that small batches launch fewer)
     int segments() const { return static_cast<int>(seg.size()) - 1; }
     int kernels() const { return (segments() + per_kernel - 1) / per_kernel; }
+    int kernels_fwd() const { return (segments() + per_kernel_fwd - 1) / per_kernel_fwd; }
 };
 
 // Scratch of a cut-segment evaluation, each [rows][bp] floats with bp = chain_pitch(B):

@@ -1369,8 +1369,9 @@ std::string jit_generate_cut(const JitGraph &g, const CutPlan &cp) {
     long long entries = 0;   // the largest window, so that every segment kernel has one LDS layout
     for (int j = 0; j < cp.segments(); ++j) entries = std::max(entries, cut_window(g, cp, j).entries);
     for (int slack = 0; slack < 2; ++slack)
-      for (int kk = 0; kk < cp.kernels(); ++kk) {
-        const int j0 = kk * cp.per_kernel, j1 = std::min(cp.segments(), j0 + cp.per_kernel);
+      for (int kk = 0; kk < (slack ? cp.kernels() : cp.kernels_fwd()); ++kk) {
+        const int per = slack ? cp.per_kernel : cp.per_kernel_fwd;
+        const int j0 = kk * per, j1 = std::min(cp.segments(), j0 + per);
         o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
           << (slack ? "emo_ks" : "emo_kf") << kk
           << "(const u8 *__restrict__ lv, long long B, long long bp,\n"
@@ -1516,12 +1517,13 @@ int jit_compile_cut(const std::string &src, const CutPlan &cp, JitModule *out, s
     out->cut = true;
     out->cut_plan = cp;
     out->block = cp.block;
-    out->kf.assign(cp.kernels(), nullptr);
+    out->kf.assign(cp.kernels_fwd(), nullptr);
     out->ks.assign(cp.kernels(), nullptr);
     bool okf = get_function(out->module, "emo_kfin", &out->kfin);
+    for (int k = 0; k < cp.kernels_fwd(); ++k)
+        okf = okf && get_function(out->module, "emo_kf" + std::to_string(k), &out->kf[k]);
     for (int k = 0; k < cp.kernels(); ++k)
-        okf = okf && get_function(out->module, "emo_kf" + std::to_string(k), &out->kf[k]) &&
-              get_function(out->module, "emo_ks" + std::to_string(k), &out->ks[k]);
+        okf = okf && get_function(out->module, "emo_ks" + std::to_string(k), &out->ks[k]);
     if (!okf) {
         *log = "cut-segment kernels missing from the module";
         (void)hipModuleUnload(out->module);
@@ -1675,8 +1677,10 @@ hipError_t jit_launch_cut(const JitModule &m, const uint8_t *levels, int64_t B, 
     float *Ebg = Dg + static_cast<size_t>(cp.segments()) * bp;
     long long b = B;
     void *args[] = {&levels, &b, &bp, &tab, &Dg, &Ebg, &S};
-    for (int k = 0; k < cp.kernels(); ++k) {
-        const int rows = std::min(cp.per_kernel, cp.segments() - k * cp.per_kernel);
+    const int per = S ? cp.per_kernel : cp.per_kernel_fwd;
+    const int nk = S ? cp.kernels() : cp.kernels_fwd();
+    for (int k = 0; k < nk; ++k) {
+        const int rows = std::min(per, cp.segments() - k * per);
         hipError_t e = hipModuleLaunchKernel(S ? m.ks[k] : m.kf[k], grid, static_cast<unsigned>(rows), 1,
                                              cp.block, 1, 1, 0, s, args, nullptr);
         if (e != hipSuccess) return e;

@@ -133,15 +133,16 @@ def test_large_graph_is_not_one_kernel(emo):
 
 
 def test_cut_segment_kernels_compile(emo, hiprtc, tmp_path):
-    """The cut-segment kernels of the 4096-pack graph (16 segments of 256 packs, four per
-    kernel): every segment kernel, with and without slack, and the last kernel compile without
-    spills, scratch or flat accesses, the slack kernels within 168 VGPRs (three waves per SIMD)."""
+    """The cut-segment kernels of the 4096-pack graph (16 segments of 256 packs: all in one
+    forward-only kernel, four per slack kernel): every segment kernel and the last kernel compile
+    without spills, scratch or flat accesses, the slack kernels within 168 VGPRs (three waves per
+    SIMD)."""
     g = synth.config_graph(4)
     src = emo.EmoGraph(g, device=-1).cut_source()
     k = len(re.findall(r"\bemo_ks(\d+)\(", src))
-    assert k == 4 and len(re.findall(r"\bemo_kf(\d+)\(", src)) == k
+    assert k == 4 and len(re.findall(r"\bemo_kf(\d+)\(", src)) == 1
     path = compile_source(hiprtc, src, tmp_path)
-    names = [f"emo_kf{j}" for j in range(k)] + [f"emo_ks{j}" for j in range(k)] + ["emo_kfin"]
+    names = ["emo_kf0"] + [f"emo_ks{j}" for j in range(k)] + ["emo_kfin"]
     notes, _ = check_code_object(path, names)
     assert max(v for v, _ in notes.values()) <= 168, notes
 
