@@ -3,8 +3,9 @@
 One step is the whole hot path over one batch of candidate policies: one emo_evaluate launch
 that computes, for every candidate, the forward pass (finish times, makespan, energy), the
 backward pass (slack of every pack) when the workload has it, and the feasibility mask and
-least-energy feasible candidate under the first latency target; workloads with a second target
-re-select it from the stored makespans and energies (emo_select_from_results).
+least-energy feasible candidate under the latency target; workloads with two targets take both
+from that one launch (emo_evaluate_targets: every target's mask bits and selection records from
+the evaluating kernel, one finalize launch for all of them).
 
 By default all five workloads run one after another.  The headline is the largest one that fits
 one GPU, the per-kernel graph of 65,536 kernels and 65,536 host nodes (2^14 candidates,
@@ -588,19 +589,22 @@ def run_workload(k, args, emo, synth, np, torch):
     E = torch.empty(B, dtype=torch.float32, device=dev)
     S = torch.empty((B, P), dtype=torch.float32, device=dev) if spec.slack else None
     masks = [torch.empty((B + 31) // 32, dtype=torch.int32, device=dev) for _ in spec.targets]
-    results = [torch.empty(3, dtype=torch.int64, device=dev) for _ in spec.targets]
+    res_all = torch.empty((len(spec.targets), 3), dtype=torch.int64, device=dev)
+    results = [res_all[j] for j in range(len(spec.targets))]
     t_c = time.perf_counter()
     T0, _ = gh.eval_policies(lv[0][:1])       # row 0 is the all-max policy
     targets = [float(np.float32(r * float(T0.item()))) for r in spec.targets]
 
     def main_call(x):
-        gh.evaluate(x, makespan=T, energy=E, slack=S, latency_target=targets[0], mask=masks[0],
-                    result=results[0])
+        if len(targets) == 1:
+            gh.evaluate(x, makespan=T, energy=E, slack=S, latency_target=targets[0], mask=masks[0],
+                        result=results[0])
+        else:
+            # every target's mask and selection records from the one evaluating launch
+            gh.evaluate_targets(x, targets, makespan=T, energy=E, slack=S, masks=masks, results=res_all)
 
     def step(i):
         main_call(lv[i % copies])
-        for j in range(1, len(targets)):
-            emo.select_from_results(T, E, targets[j], mask=masks[j], result=results[j])
 
     step(0)                                   # compiles the specialised kernels if any
     torch.cuda.synchronize()
@@ -628,8 +632,6 @@ def run_workload(k, args, emo, synth, np, torch):
             elif i % every == 1:
                 gh.set_timing_events(None, None)
             main_call(lv[i % copies_used])
-            for j in range(1, len(targets)):
-                emo.select_from_results(T, E, targets[j], mask=masks[j], result=results[j])
         end.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t_wall
@@ -649,7 +651,7 @@ def run_workload(k, args, emo, synth, np, torch):
 
     value = B / (ms_step / 1e3)
     # algorithmic bytes of the main launch: level bytes in; makespan, energy, slack and mask out
-    algo_bytes = B * (P + 8 + (4 * P if spec.slack else 0)) + (B + 7) // 8
+    algo_bytes = B * (P + 8 + (4 * P if spec.slack else 0)) + len(targets) * ((B + 7) // 8)
     achieved = algo_bytes / (main_ms / 1e3) / 1e9
     # algorithmic VALU work on the folded graph: one max per candidate-dependent edge, one add
     # per pack for the finish time and one for the energy, two for the makespan/energy close;
@@ -665,7 +667,7 @@ def run_workload(k, args, emo, synth, np, torch):
         "config": {"workload": spec.name, "candidates": B, "nodes": g.num_nodes,
                    "edges": g.num_edges, "packs": P, "levels": g.num_levels,
                    "target_ratios": list(spec.targets), "slack": spec.slack,
-                   "step": "emo_evaluate" + (" + emo_select_from_results" * (len(targets) - 1)),
+                   "step": "emo_evaluate" if len(targets) == 1 else f"emo_evaluate_targets ({len(targets)} targets)",
                    "rotated_input_copies": copies},
         "roofline": {"bound": "hbm", "kernel": kname, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,

@@ -264,6 +264,27 @@ emo_status emo_evaluate(emo_graph_t g, const uint8_t *levels, int64_t num_candid
                         void *stream);
 
 /*
+ * emo_evaluate with several latency targets in the same pass (Eq. 4 once per target over one
+ * evaluation of the batch, e.g. the operating points of a latency sweep): the evaluating kernel
+ * writes every target's mask bits and selection partial records, and one finalize launch with a
+ * workgroup per target completes every selection.  Each target's mask and result are those
+ * emo_evaluate gives for that target alone, bit for bit.
+ *   num_targets      1 <= n <= 8.
+ *   latency_targets  host float [n], none NaN (checked when a mask or the results are given).
+ *   feasible_masks   host array of n device pointers (each device uint32 [ceil(B/32)] or NULL),
+ *                    or NULL for no masks.
+ *   results          device emo_selection [n], 8-byte aligned, or NULL: results[k] is target k's
+ *                    selection.
+ * makespan, energy, slack and per_node as in emo_evaluate.  The scratch for the partial records
+ * (n x 16 bytes per evaluating workgroup) comes from the graph's stream-ordered arena.
+ */
+emo_status emo_evaluate_targets(emo_graph_t g, const uint8_t *levels, int64_t num_candidates,
+                                float *makespan, float *energy, float *slack, int32_t per_node,
+                                int32_t num_targets, const float *latency_targets,
+                                uint32_t *const *feasible_masks, emo_selection *results,
+                                void *stream);
+
+/*
  * The same selection from makespans and energies already computed (e.g. a second latency
  * target over one evaluation).  makespan, energy: device float [B].
  */

@@ -1448,8 +1448,8 @@ hipError_t launch_scan_full_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, 
 }
 
 hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
-                           float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
-                           void *scratch, hipStream_t s) {
+                           float *T, float *E, float *slack, const SelTargets &tg, void *scratch,
+                           hipStream_t s) {
     WinArgs a;
     a.W = c.win;
     a.wlog = 0;
@@ -1493,16 +1493,15 @@ hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t 
     else e = c.fixed ? launch_windowed_kernel<false, true, false>(EMO_WIN_ARGS)
                      : launch_windowed_kernel<false, false, false>(EMO_WIN_ARGS);
 #undef EMO_WIN_ARGS
-    if (e == hipSuccess && (mask || part)) e = launch_select_results(Ts, Es, B, target, mask, part, s);
+    if (e == hipSuccess && tg.n) e = launch_select_results(Ts, Es, B, tg, s);
     return e;
 }
 }  // namespace
 
 hipError_t launch_chains(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
-                         float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
-                         void *scratch, hipStream_t s) {
-    if (chains_windowed_ok(c, levels, slack)) return launch_windowed(g, c, levels, B, T, E, slack, target,
-                                                                     mask, part, scratch, s);
+                         float *T, float *E, float *slack, const SelTargets &tg, void *scratch,
+                         hipStream_t s) {
+    if (chains_windowed_ok(c, levels, slack)) return launch_windowed(g, c, levels, B, T, E, slack, tg, scratch, s);
     const int64_t grid = chain_grid(c, B);
     const int64_t pitch = grid * kChainBlockThreads;
     const bool st = staged_ok(g, c);
@@ -1530,7 +1529,7 @@ hipError_t launch_chains(const DevGraph &g, const DevChains &c, const uint8_t *l
                            dim3(kGatherThreads), 0, s, tmp, c.pos, B, g.P, srow, slack);
         e = hipGetLastError();
     }
-    if (e == hipSuccess && (mask || part)) e = launch_select_results(Ts, Es, B, target, mask, part, s);
+    if (e == hipSuccess && tg.n) e = launch_select_results(Ts, Es, B, tg, s);
     return e;
 }
 

@@ -1366,25 +1366,47 @@ Arena &device_arena(int dev) {
     return arenas[dev];
 }
 
-// The hot path for every batch entry point: forward pass, optional backward slack pass,
-// optional feasibility mask and selection, in one kernel launch (plus the initialisation of the
-// selection accumulator).
+// Checks nt latency targets with their optional masks and results (nt == 0: none) and fills
+// tg's targets and masks; tg.n stays 0 when no target has a mask or a result.
+emo_status check_targets(int32_t nt, const float *targets, uint32_t *const *masks,
+                         emo_selection *results, emo::SelTargets *tg) {
+    if (nt < 0 || nt > emo::kMaxTargets)
+        return fail(EMO_ERR_INVALID_ARGUMENT, "num_targets %d outside [0, %d]", nt, emo::kMaxTargets);
+    if (results && reinterpret_cast<uintptr_t>(results) % 8)
+        return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
+    bool any = results != nullptr;
+    for (int32_t k = 0; k < nt && masks; ++k) any = any || masks[k];
+    if (!any || nt == 0) return ok();
+    if (!targets) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_targets is NULL");
+    for (int32_t k = 0; k < nt; ++k) {
+        if (std::isnan(targets[k])) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target %d is NaN", k);
+        tg->t[k] = targets[k];
+        tg->mask[k] = masks ? masks[k] : nullptr;
+    }
+    tg->n = nt;
+    return ok();
+}
+
+// The hot path for every batch entry point: forward pass, optional backward slack pass, and for
+// each of nt latency targets an optional feasibility mask and selection, in one evaluating
+// kernel launch (the selection's stage 1 inside it) plus one finalize launch for all targets.
 emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
-                    float *energy, float *slack, int32_t per_node, float target, uint32_t *mask,
-                    emo_selection *result, void *stream) {
+                    float *energy, float *slack, int32_t per_node, int32_t nt, const float *targets,
+                    uint32_t *const *masks, emo_selection *results, void *stream) {
     emo_status s = check_batch(g, B);
     if (s != EMO_OK) return s;
-    if (result && reinterpret_cast<uintptr_t>(result) % 8)
-        return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
-    if ((result || mask) && std::isnan(target))
-        return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
+    emo::SelTargets tg;
+    if ((s = check_targets(nt, targets, masks, results, &tg)) != EMO_OK) return s;
+    if (!tg.n) results = nullptr;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (B == 0) {
-        if (!result) return ok();
+        if (!results) return ok();
         DeviceGuard guard(g->device);
-        return after_launch(emo::launch_empty_result(result, st), "empty selection");
+        hipError_t e = hipSuccess;
+        for (int32_t k = 0; k < tg.n && e == hipSuccess; ++k) e = emo::launch_empty_result(results + k, st);
+        return after_launch(e, "empty selection");
     }
-    if (!makespan && !energy && !slack && !mask && !result) return ok();
+    if (!makespan && !energy && !slack && !tg.n) return ok();
     if (!levels && g->P > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
     Path path = Path::kInterpreted;
     if ((s = choose_path(g, levels, slack, per_node != 0, B, &path)) != EMO_OK) return s;
@@ -1396,7 +1418,7 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
                             : path == Path::kChainLanes ? emo::select_results_blocks(B)
                                                    : emo::forward_blocks(B);
     const emo::DevProgram &prog = per_node ? g->dg.slack_node : g->dg.slack_pack;
-    size_t part_bytes = result ? static_cast<size_t>(nblocks) * emo::kPartialBytes : 0;
+    size_t part_bytes = results ? static_cast<size_t>(tg.n) * nblocks * emo::kPartialBytes : 0;
     part_bytes = (part_bytes + 255) & ~static_cast<size_t>(255);
     size_t work_bytes = 0;
     if (path == Path::kChain) work_bytes = emo::chain_scratch_bytes(g->jc.plan, B);
@@ -1414,7 +1436,8 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
                         hipGetErrorString(ea));
         }
     }
-    void *part = result ? scratch : nullptr;
+    tg.part = results ? scratch : nullptr;
+    tg.nparts = nblocks;
     void *work = scratch ? static_cast<char *>(scratch) + part_bytes : nullptr;
     g->info.last_kernels = path == Path::kChainLanes && emo::chains_scan_full_ok(g->chains, levels, slack)
                                ? 8
@@ -1426,31 +1449,27 @@ emo_status evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *make
     hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
     if (e == hipSuccess) {
         if (path == Path::kCut) {
-            e = emo::jit_launch_cut(g->jk, levels, B, g->dg.tab, work, slack, makespan, energy, target,
-                                    mask, part, st);
+            e = emo::jit_launch_cut(g->jk, levels, B, g->dg.tab, work, slack, makespan, energy, tg, st);
         } else if (path == Path::kChain) {
             e = emo::jit_launch_chain(g->jc, levels, B, g->dg.tab, g->dg.tabt, work, slack, makespan,
-                                      energy, target, mask, part, st);
+                                      energy, tg, st);
         } else if (path == Path::kChainLanes) {
-            e = emo::launch_chains(g->dg, g->chains, levels, B, makespan, energy, slack, target, mask,
-                                   part, work, st);
+            e = emo::launch_chains(g->dg, g->chains, levels, B, makespan, energy, slack, tg, work, st);
         } else if (slack) {
             if (path == Path::kSingle) {
-                e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy,
-                                          target, mask, part, st);
+                e = emo::jit_launch_slack(g->jm, levels, B, g->dg.tab, slack, makespan, energy, tg, st);
             } else {
                 e = emo::launch_slack(g->dg, prog, per_node ? g->V : g->P, levels, B, slack,
-                                      makespan, energy, target, mask, part, work, st);
+                                      makespan, energy, tg, work, st);
             }
         } else if (path == Path::kSingle) {
-            e = emo::jit_launch_forward(g->jm, levels, B, g->dg.tab, makespan, energy, target,
-                                        mask, part, st);
+            e = emo::jit_launch_forward(g->jm, levels, B, g->dg.tab, makespan, energy, tg, st);
         } else {
-            e = emo::launch_forward(g->dg, levels, B, makespan, energy, target, mask, part, work, st);
+            e = emo::launch_forward(g->dg, levels, B, makespan, energy, tg, work, st);
         }
     }
     if (e == hipSuccess && g->ev_end) e = hipEventRecord(g->ev_end, st);
-    if (result && e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
+    if (results && e == hipSuccess) e = emo::launch_select_finalize(tg, results, st);
     if (scratch) {
         hipError_t er = arena_release(g->arena, st);
         if (e == hipSuccess) e = er;
@@ -1464,28 +1483,39 @@ extern "C" {
 
 emo_status emo_eval_policies(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
                              float *energy, void *stream) {
-    return evaluate(g, levels, B, makespan, energy, nullptr, 0, 0.f, nullptr, nullptr, stream);
+    return evaluate(g, levels, B, makespan, energy, nullptr, 0, 0, nullptr, nullptr, nullptr, stream);
 }
 
 emo_status emo_slack(emo_graph_t g, const uint8_t *levels, int64_t B, float *slack,
                      int32_t per_node, float *makespan, float *energy, void *stream) {
     if (!slack && B > 0) return fail(EMO_ERR_INVALID_ARGUMENT, "slack is NULL");
-    return evaluate(g, levels, B, makespan, energy, slack, per_node, 0.f, nullptr, nullptr, stream);
+    return evaluate(g, levels, B, makespan, energy, slack, per_node, 0, nullptr, nullptr, nullptr, stream);
 }
 
 emo_status emo_select_policy(emo_graph_t g, const uint8_t *levels, int64_t B,
                              float latency_target, uint32_t *feasible_mask,
                              emo_selection *result, void *stream) {
     if (!result) return fail(EMO_ERR_INVALID_ARGUMENT, "result is NULL");
-    return evaluate(g, levels, B, nullptr, nullptr, nullptr, 0, latency_target, feasible_mask,
+    return evaluate(g, levels, B, nullptr, nullptr, nullptr, 0, 1, &latency_target, &feasible_mask,
                     result, stream);
 }
 
 emo_status emo_evaluate(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
                         float *energy, float *slack, int32_t per_node, float latency_target,
                         uint32_t *feasible_mask, emo_selection *result, void *stream) {
-    return evaluate(g, levels, B, makespan, energy, slack, per_node, latency_target,
-                    feasible_mask, result, stream);
+    return evaluate(g, levels, B, makespan, energy, slack, per_node, 1, &latency_target,
+                    &feasible_mask, result, stream);
+}
+
+emo_status emo_evaluate_targets(emo_graph_t g, const uint8_t *levels, int64_t B, float *makespan,
+                                float *energy, float *slack, int32_t per_node, int32_t num_targets,
+                                const float *latency_targets, uint32_t *const *feasible_masks,
+                                emo_selection *results, void *stream) {
+    if (num_targets < 1 || num_targets > emo::kMaxTargets)
+        return fail(EMO_ERR_INVALID_ARGUMENT, "num_targets %d outside [1, %d]", num_targets, emo::kMaxTargets);
+    if (!latency_targets) return fail(EMO_ERR_INVALID_ARGUMENT, "latency_targets is NULL");
+    return evaluate(g, levels, B, makespan, energy, slack, per_node, num_targets, latency_targets,
+                    feasible_masks, results, stream);
 }
 
 emo_status emo_eval_intervals(emo_graph_t g, const uint8_t *levels, int64_t B, int32_t num_intervals,
@@ -1514,14 +1544,12 @@ emo_status emo_eval_intervals(emo_graph_t g, const uint8_t *levels, int64_t B, i
             return fail(EMO_ERR_INVALID_ARGUMENT, "idle_power[%d] is negative or not finite", f);
         pol.idle[f] = idle_power[f];
     }
-    if (result && reinterpret_cast<uintptr_t>(result) % 8)
-        return fail(EMO_ERR_INVALID_ARGUMENT, "result is not 8-byte aligned");
-    if ((result || feasible_mask) && std::isnan(latency_target))
-        return fail(EMO_ERR_INVALID_ARGUMENT, "latency_target is NaN");
+    emo::SelTargets tg;
+    if ((s = check_targets(1, &latency_target, &feasible_mask, result, &tg)) != EMO_OK) return s;
     hipStream_t st = static_cast<hipStream_t>(stream);
     DeviceGuard guard(g->device);
     if (B == 0) return result ? after_launch(emo::launch_empty_result(result, st), "empty selection") : ok();
-    if (!makespan && !energy && !feasible_mask && !result) return ok();
+    if (!makespan && !energy && !tg.n) return ok();
     if (!levels) return fail(EMO_ERR_INVALID_ARGUMENT, "levels is NULL");
     // straight-line kernels specialised to the graph when it is small enough for one kernel and
     // the change points fit the bucket table; otherwise the interpreting kernel
@@ -1564,18 +1592,17 @@ emo_status emo_eval_intervals(emo_graph_t g, const uint8_t *levels, int64_t B, i
                         hipGetErrorString(ea));
         }
     }
-    void *part = result ? scratch : nullptr;
+    tg.part = result ? scratch : nullptr;
+    tg.nparts = nblocks;
     void *work = scratch ? static_cast<char *>(scratch) + part_bytes : nullptr;
     g->info.last_kernels = use_jit ? 7 : 0;
     hipError_t e = g->ev_begin ? hipEventRecord(g->ev_begin, st) : hipSuccess;
     if (e == hipSuccess && use_jit)
-        e = emo::jit_launch_intervals(g->jiv, levels, B, g->dg.tab, iva, iv_cap, makespan, energy,
-                                      latency_target, feasible_mask, part, st);
+        e = emo::jit_launch_intervals(g->jiv, levels, B, g->dg.tab, iva, iv_cap, makespan, energy, tg, st);
     else if (e == hipSuccess)
-        e = emo::launch_intervals(g->dg, pol, levels, B, makespan, energy, latency_target, feasible_mask,
-                                  part, work, st);
+        e = emo::launch_intervals(g->dg, pol, levels, B, makespan, energy, tg, work, st);
     if (e == hipSuccess && g->ev_end) e = hipEventRecord(g->ev_end, st);
-    if (result && e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
+    if (result && e == hipSuccess) e = emo::launch_select_finalize(tg, result, st);
     if (scratch) {
         hipError_t er = arena_release(g->arena, st);
         if (e == hipSuccess) e = er;
@@ -1608,8 +1635,9 @@ emo_status emo_select_from_results(const float *makespan, const float *energy, i
         (void)hipGetLastError();
         return fail(EMO_ERR_OUT_OF_MEMORY, "scratch: %s", hipGetErrorString(e));
     }
-    e = emo::launch_select_results(makespan, energy, B, latency_target, feasible_mask, part, st);
-    if (e == hipSuccess) e = emo::launch_select_finalize(part, nblocks, result, st);
+    const emo::SelTargets tg = emo::one_target(latency_target, feasible_mask, part, nblocks);
+    e = emo::launch_select_results(makespan, energy, B, tg, st);
+    if (e == hipSuccess) e = emo::launch_select_finalize(tg, result, st);
     hipError_t er = arena_release(a, st);
     if (e == hipSuccess) e = er;
     return after_launch(e, "emo_select_from_results");
@@ -1640,8 +1668,9 @@ emo_status emo_select_from_results_noalloc(const float *makespan, const float *e
         return fail(EMO_ERR_DEVICE, "static scratch of device %d: %s", dev, hipGetErrorString(e));
     }
     // every partial record is written before the finalize reads it: nothing needs clearing
-    e = emo::launch_select_results(makespan, energy, B, latency_target, feasible_mask, part, st);
-    if (e == hipSuccess) e = emo::launch_select_finalize(part, emo::select_results_blocks(B), result, st);
+    const emo::SelTargets tg = emo::one_target(latency_target, feasible_mask, part, emo::select_results_blocks(B));
+    e = emo::launch_select_results(makespan, energy, B, tg, st);
+    if (e == hipSuccess) e = emo::launch_select_finalize(tg, result, st);
     return after_launch(e, "emo_select_from_results_noalloc");
 }
 
@@ -1746,7 +1775,7 @@ emo_status emo_dp_search(emo_graph_t g, float latency_target, float quantum, con
     dp_layout(S, R, P, &b, static_cast<char *>(base));
     // dp[0] = {P_0}, expanded into the first stage's candidates (row buffer 1 holds P_0)
     e = emo::dp_launch_default_row(b.rows[1], P, F, st);
-    if (e == hipSuccess) s = evaluate(g, b.rows[1], 1, b.T, b.E, nullptr, 0, 0.f, nullptr, nullptr, st);
+    if (e == hipSuccess) s = evaluate(g, b.rows[1], 1, b.T, b.E, nullptr, 0, 0, nullptr, nullptr, nullptr, st);
     if (e == hipSuccess && s == EMO_OK)
         e = emo::dp_launch_seed(b.rows[1], P, F, P > 0 ? order[0] : -1, b.T, b.E, b.rows[0], b.state,
                                 b.keys[0], b.Tst, b.keys[1], NB, st);
@@ -1757,7 +1786,7 @@ emo_status emo_dp_search(emo_graph_t g, float latency_target, float quantum, con
     for (int32_t i = 0; i < P && NB > 0 && e == hipSuccess && s == EMO_OK; ++i) {
         const int x = i % 2;
         const int64_t B = cur * F;
-        s = evaluate(g, b.rows[x], B, b.T, b.E, nullptr, 0, 0.f, nullptr, nullptr, st);
+        s = evaluate(g, b.rows[x], B, b.T, b.E, nullptr, 0, 0, nullptr, nullptr, nullptr, st);
         if (s != EMO_OK) break;
         e = emo::dp_launch_bucket(b.T, b.E, b.keys[x], B, F, latency_target, q, bmin, NB, b.keys[1 - x], st);
         if (e == hipSuccess)

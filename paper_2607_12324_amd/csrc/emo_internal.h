@@ -77,6 +77,33 @@ struct DevGraph {
 // launch_select_finalize (16 bytes each: least key, feasible count, makespan).
 constexpr size_t kPartialBytes = 16;
 
+// The latency targets of one evaluation, passed to the kernels by value (the layout of the
+// kernels' EmoTargets): target k's feasibility mask to mask[k] (when not NULL) and its partial
+// records to part + k * nparts * kPartialBytes (all targets, when part is not NULL).  n = 0: no
+// mask and no selection.
+constexpr int kMaxTargets = 8;
+struct SelTargets {
+    int32_t n = 0;
+    int32_t pad = 0;
+    int64_t nparts = 0;
+    void *part = nullptr;
+    float t[kMaxTargets] = {};
+    uint32_t *mask[kMaxTargets] = {};
+};
+static_assert(sizeof(SelTargets) == 120, "kernel argument layout of the targets");
+// One target (the single-target entry points): none when neither mask nor part is given.
+inline SelTargets one_target(float target, uint32_t *mask, void *part, int64_t nparts) {
+    SelTargets tg;
+    if (mask || part) {
+        tg.n = 1;
+        tg.t[0] = target;
+        tg.mask[0] = mask;
+        tg.part = part;
+        tg.nparts = nparts;
+    }
+    return tg;
+}
+
 // Interpreting kernels.  T, E, mask, part may each be NULL; `part` receives one selection
 // partial record per block (forward_blocks(B) of them).
 // Device scratch (bytes) the interpreting kernels need for B candidates: cold slots, and for
@@ -85,10 +112,10 @@ constexpr size_t kPartialBytes = 16;
 size_t forward_scratch_bytes(const DevProgram &prog, int64_t B);
 size_t slack_scratch_bytes(const DevProgram &prog, int64_t B);
 hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
-                          float target, uint32_t *mask, void *part, void *scratch, hipStream_t s);
+                          const SelTargets &tg, void *scratch, hipStream_t s);
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
-                        float target, uint32_t *mask, void *part, void *scratch, hipStream_t s);
+                        const SelTargets &tg, void *scratch, hipStream_t s);
 int64_t forward_blocks(int64_t B);
 
 // A time-interval policy batch (the policy form of Sec. IV-A; Alg. 1): K intervals [T_i,
@@ -106,11 +133,10 @@ struct IvPolicy {
 // Makespan, energy and the selection stage 1 of B interval policies (forward_blocks(B) partials);
 // scratch as for launch_forward (forward_scratch_bytes(g.eval, B)).
 hipError_t launch_intervals(const DevGraph &g, const IvPolicy &pol, const uint8_t *levels, int64_t B,
-                            float *T, float *E, float target, uint32_t *mask, void *part, void *scratch,
-                            hipStream_t s);
+                            float *T, float *E, const SelTargets &tg, void *scratch, hipStream_t s);
 hipError_t launch_empty_result(emo_selection *res, hipStream_t s);
-hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selection *res,
-                                  hipStream_t s);
+// Stage 2 for every target of tg with part: results[k] from target k's records.
+hipError_t launch_select_finalize(const SelTargets &tg, emo_selection *results, hipStream_t s);
 // Stage 1 of a selection from stored makespans and energies (select_results_blocks(B)
 // partials: one per 1024 candidates).
 int64_t select_results_blocks(int64_t B);
@@ -119,8 +145,9 @@ int64_t select_results_blocks(int64_t B);
 constexpr int kNoAllocMaxDevices = 64;
 int64_t noalloc_max_candidates();
 hipError_t noalloc_scratch(int dev, void **out);
-hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
-                                 uint32_t *mask, void *part, hipStream_t s);
+// (tg.nparts must be select_results_blocks(B))
+hipError_t launch_select_results(const float *T, const float *E, int64_t B, const SelTargets &tg,
+                                 hipStream_t s);
 
 // ---------------------------------------------------------------- chain-lane kernels
 
@@ -187,8 +214,8 @@ size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t
 // Makespan/energy (and per-pack slack when `slack`); the selection stage 1 runs from the stored
 // makespans and energies (select_results_blocks(B) partial records in `part`).
 hipError_t launch_chains(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
-                         float *T, float *E, float *slack, float target, uint32_t *mask, void *part,
-                         void *scratch, hipStream_t s);
+                         float *T, float *E, float *slack, const SelTargets &tg, void *scratch,
+                         hipStream_t s);
 
 // ---------------------------------------------------------------- policy search (Alg. 2)
 
@@ -339,8 +366,7 @@ int64_t jit_chain_blocks(const JitModule &m, int64_t B);
 // chain_scratch_bytes(plan, jit_chain_blocks * block) bytes.
 hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B,
                             const float2 *tab, const float *tabt, void *scratch, float *S,
-                            float *T, float *E, float target, uint32_t *mask, void *part,
-                            hipStream_t s);
+                            float *T, float *E, const SelTargets &tg, hipStream_t s);
 // Plan of the cut-segment kernels over the cut steps `cuts` (increasing step indices): segments
 // of whole cut-to-cut pieces with at most max_packs packs each, recompute sub-segments of
 // sub_packs packs.  Returns an empty plan (no segments) when a piece is larger.
@@ -352,8 +378,7 @@ int64_t jit_cut_blocks(const JitModule &m, int64_t B);
 // Segment kernel (forward only, or with slack S) and the finishing kernel.  scratch holds
 // cut_scratch_bytes(plan, B) bytes.
 hipError_t jit_launch_cut(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                          void *scratch, float *S, float *T, float *E, float target, uint32_t *mask,
-                          void *part, hipStream_t s);
+                          void *scratch, float *S, float *T, float *E, const SelTargets &tg, hipStream_t s);
 // 0 on success; otherwise *log holds the compiler's or loader's message.
 int jit_compile(const std::string &src, bool with_slack, JitModule *out, std::string *log);
 void jit_unload(JitModule *m);
@@ -378,17 +403,15 @@ size_t jit_iv_dyn_lds(int block, int K, int M);
 // Resident workgroups of emo_iv on the current device with that dynamic LDS (0: unknown).
 int64_t jit_iv_cap(const JitModule &m, int K, int M);
 hipError_t jit_launch_intervals(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                                const IvJitArgs &a, int64_t cap, float *T, float *E, float target,
-                                uint32_t *mask, void *part, hipStream_t s);
+                                const IvJitArgs &a, int64_t cap, float *T, float *E, const SelTargets &tg,
+                                hipStream_t s);
 // Sets select_cap / slack_cap from the occupancy of the compiled kernels (current device).
 void jit_set_caps(JitModule *m);
 // Forward pass; T, E, mask, part may each be NULL.
 hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,
-                              const float2 *tab, float *T, float *E, float target, uint32_t *mask,
-                              void *part, hipStream_t s);
+                              const float2 *tab, float *T, float *E, const SelTargets &tg, hipStream_t s);
 // Forward + backward slack pass with the same optional outputs.
 hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                            float *S, float *T, float *E, float target, uint32_t *mask,
-                            void *part, hipStream_t s);
+                            float *S, float *T, float *E, const SelTargets &tg, hipStream_t s);
 
 }  // namespace emo

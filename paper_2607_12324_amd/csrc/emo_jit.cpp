@@ -492,12 +492,12 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
     o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
          "emo_sp_select(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
          "              float *__restrict__ To, float *__restrict__ Eo,\n"
-         "              float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n"
+         "              EmoTargets tg) {\n"
          "  EMO_TABLE_DECL\n  EMO_GROUP_LOOP {\n  EMO_LANE_SETUP\n"
          "  const EmoFwd r = emo_forward(lv + cand * "
       << g.P << "LL, tab);\n"
          "  if (active) { if (To) To[cand] = r.T; if (Eo) Eo[cand] = r.E; }\n"
-         "  if (mask || part) emo_select_block(grp, active, r.T, r.E, cand, B, target, mask, part);\n"
+         "  if (tg.n) emo_select_all(grp, active, r.T, r.E, cand, B, tg);\n"
          "  }\n}\n";
 
     if (with_slack) {
@@ -510,7 +510,7 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
         o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
              "emo_sp_slack(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg,\n"
              "             float *__restrict__ S, float *__restrict__ To, float *__restrict__ Eo,\n"
-             "             float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n"
+             "             EmoTargets tg) {\n"
              "  EMO_TABLE_DECL\n"
              "  const int lane = threadIdx.x % EMO_WAVE;\n"
              "  const int wave = threadIdx.x / EMO_WAVE;\n"
@@ -531,7 +531,7 @@ std::string jit_generate(const JitGraph &g, bool with_slack, bool tab_lds, int b
         if (staged) o << "  stg_bad[lane] = isbad ? 1u : 0u;\n";
         lp.launder();
         emit_backward(o, g, staged, level_expr);
-        o << "  if (mask || part) emo_select_block(grp, active, T, E, cand, B, target, mask, part);\n";
+        o << "  if (tg.n) emo_select_all(grp, active, T, E, cand, B, tg);\n";
         o << "  }\n}\n";
     }
     return o.str();
@@ -652,8 +652,7 @@ struct EmoFwd { float T; float E; bool bad; };
 )";
     o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
          "emo_iv(const u8 *__restrict__ lv, long long B, const float2 *__restrict__ tabg, EmoIvArgs a,\n"
-         "    int copy, float inv_k, float *__restrict__ To, float *__restrict__ Eo, float target,\n"
-         "    unsigned int *__restrict__ mask, EmoPartial *part) {\n";
+         "    int copy, float inv_k, float *__restrict__ To, float *__restrict__ Eo, EmoTargets tg) {\n";
     if (tab_lds)
         o << "  __shared__ float2 tab[NTAB];\n"
              "  for (int i_ = threadIdx.x; i_ < NTAB; i_ += EMO_BLOCK) tab[i_] = tabg[i_];\n";
@@ -721,7 +720,7 @@ struct EmoFwd { float T; float E; bool bad; };
     const long long cand = active ? gid : B - 1;
     const EmoFwd r = emo_iv_forward(my, K, tab, s_bk, scale, M, s_pts, s_dur, s_idle);
     if (active) { if (To) To[cand] = r.T; if (Eo) Eo[cand] = r.E; }
-    if (mask || part) emo_select_block(grp, active, r.T, r.E, cand, B, target, mask, part);
+    if (tg.n) emo_select_all(grp, active, r.T, r.E, cand, B, tg);
   }
 }
 )";
@@ -880,7 +879,7 @@ void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPla
       << "emo_cf" << j << "(const u8 *__restrict__ lv, long long B, long long bp,\n"
          "    const float2 *__restrict__ tabg, float *__restrict__ ck, float *__restrict__ Tc,\n"
          "    double *__restrict__ Edc, float *__restrict__ Ebc, int full, float *__restrict__ To,\n"
-         "    float *__restrict__ Eo, float target, unsigned int *__restrict__ mask, EmoPartial *part) {\n";
+         "    float *__restrict__ Eo, EmoTargets tg) {\n";
     emit_table(o, g, w, "float2");
     o << chain_lanes(cp.block);
     o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
@@ -915,7 +914,7 @@ void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPla
         emit_forward_finish(o, g, lp, j > 0);
         o << "  if (active) Tc[cand] = T;\n"
              "  if (active) { if (To) To[cand] = T; if (Eo) Eo[cand] = E; }\n"
-             "  if (mask || part) emo_select_block(blockIdx.x, active, T, E, cand, B, target, mask, part);\n";
+             "  if (tg.n) emo_select_all(blockIdx.x, active, T, E, cand, B, tg);\n";
     }
     o << "}\n\n";
 }
@@ -1398,8 +1397,7 @@ std::string jit_generate_cut(const JitGraph &g, const CutPlan &cp) {
     // in any segment (NaN D) makes the candidate's makespan, energy and slack row NaN
     o << "extern \"C\" __global__ void __launch_bounds__(EMO_BLOCK)\n"
          "emo_kfin(long long B, long long bp, const float *__restrict__ Dg, const float *__restrict__ Ebg,\n"
-         "    float *__restrict__ S, float *__restrict__ To, float *__restrict__ Eo, float target,\n"
-         "    unsigned int *__restrict__ mask, EmoPartial *part) {\n";
+         "    float *__restrict__ S, float *__restrict__ To, float *__restrict__ Eo, EmoTargets tg) {\n";
     o << chain_lanes(cp.block);
     o << "  float T = EMO_AT(Dg, 0);\n";
     for (int j = 1; j < cp.segments(); ++j) o << "  T = T + EMO_AT(Dg, " << j << ");\n";
@@ -1421,7 +1419,7 @@ std::string jit_generate_cut(const JitGraph &g, const CutPlan &cp) {
          "      for (int c = 4 * lane; c < " << g.P << "; c += 4 * EMO_WAVE) *(emo_f32x4 *)(srow + c) = (emo_f32x4)(EMO_NAN);\n"
          "    }\n"
          "  }\n";
-    o << "  if (mask || part) emo_select_block(blockIdx.x, active, T, E, cand, B, target, mask, part);\n";
+    o << "  if (tg.n) emo_select_all(blockIdx.x, active, T, E, cand, B, tg);\n";
     o << "}\n";
     return o.str();
 }
@@ -1592,14 +1590,15 @@ void jit_set_caps(JitModule *m) {
 }
 
 hipError_t jit_launch_intervals(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                                const IvJitArgs &a, int64_t cap, float *T, float *E, float target,
-                                uint32_t *mask, void *part, hipStream_t s) {
+                                const IvJitArgs &a, int64_t cap, float *T, float *E, const SelTargets &tg,
+                                hipStream_t s) {
+    SelTargets dt = tg;
     long long b = B;
     IvJitArgs args_v = a;
     const uintptr_t al = reinterpret_cast<uintptr_t>(levels);
     int copy = a.K % 16 == 0 && al % 16 == 0 ? 16 : (a.K % 4 == 0 && al % 4 == 0 ? 4 : 1);
     float inv_k = static_cast<float>(1.0 / a.K);
-    void *args[] = {&levels, &b, &tab, &args_v, &copy, &inv_k, &T, &E, &target, &mask, &part};
+    void *args[] = {&levels, &b, &tab, &args_v, &copy, &inv_k, &T, &E, &dt};
     const unsigned dyn = static_cast<unsigned>(jit_iv_dyn_lds(m.block, a.K, a.M));
     return hipModuleLaunchKernel(m.select, capped_grid(B, m.block, cap), 1, 1, m.block, 1, 1, dyn, s, args,
                                  nullptr);
@@ -1619,10 +1618,10 @@ int64_t jit_iv_cap(const JitModule &m, int K, int M) {
 }
 
 hipError_t jit_launch_forward(const JitModule &m, const uint8_t *levels, int64_t B,
-                              const float2 *tab, float *T, float *E, float target, uint32_t *mask,
-                              void *part, hipStream_t s) {
+                              const float2 *tab, float *T, float *E, const SelTargets &tg, hipStream_t s) {
     long long b = B;
-    void *args[] = {&levels, &b, &tab, &T, &E, &target, &mask, &part};
+    SelTargets dt = tg;
+    void *args[] = {&levels, &b, &tab, &T, &E, &dt};
     return hipModuleLaunchKernel(m.select, capped_grid(B, m.block, m.select_cap), 1, 1, m.block, 1, 1, 0,
                                  s, args, nullptr);
 }
@@ -1631,8 +1630,7 @@ int64_t jit_chain_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.pl
 
 hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B,
                             const float2 *tab, const float *tabt, void *scratch, float *S,
-                            float *T, float *E, float target, uint32_t *mask, void *part,
-                            hipStream_t s) {
+                            float *T, float *E, const SelTargets &tg, hipStream_t s) {
     const ChainPlan &cp = m.plan;
     const unsigned grid = grid_of(B, cp.block);
     const unsigned bgrid = grid_of(B, cp.bblock);
@@ -1649,9 +1647,8 @@ hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B
         const bool last = j + 1 == m_seg;
         float *To = last ? T : nullptr;
         float *Eo = last ? E : nullptr;
-        uint32_t *mk = last ? mask : nullptr;
-        void *pt = last ? part : nullptr;
-        void *args[] = {&levels, &b, &bp, &tab, &ck, &Tc, &Edc, &Ebc, &full, &To, &Eo, &target, &mk, &pt};
+        SelTargets dt = last ? tg : SelTargets();
+        void *args[] = {&levels, &b, &bp, &tab, &ck, &Tc, &Edc, &Ebc, &full, &To, &Eo, &dt};
         hipError_t e = hipModuleLaunchKernel(m.cf[j], grid, 1, 1, cp.block, 1, 1, 0, s, args, nullptr);
         if (e != hipSuccess) return e;
     }
@@ -1668,8 +1665,7 @@ hipError_t jit_launch_chain(const JitModule &m, const uint8_t *levels, int64_t B
 int64_t jit_cut_blocks(const JitModule &m, int64_t B) { return grid_of(B, m.cut_plan.block); }
 
 hipError_t jit_launch_cut(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                          void *scratch, float *S, float *T, float *E, float target, uint32_t *mask,
-                          void *part, hipStream_t s) {
+                          void *scratch, float *S, float *T, float *E, const SelTargets &tg, hipStream_t s) {
     const CutPlan &cp = m.cut_plan;
     const unsigned grid = grid_of(B, cp.block);
     long long bp = chain_pitch(B);
@@ -1686,15 +1682,16 @@ hipError_t jit_launch_cut(const JitModule &m, const uint8_t *levels, int64_t B, 
         if (e != hipSuccess) return e;
     }
     const float *Dc = Dg, *Ec = Ebg;
-    void *fargs[] = {&b, &bp, &Dc, &Ec, &S, &T, &E, &target, &mask, &part};
+    SelTargets dt = tg;
+    void *fargs[] = {&b, &bp, &Dc, &Ec, &S, &T, &E, &dt};
     return hipModuleLaunchKernel(m.kfin, grid, 1, 1, cp.block, 1, 1, 0, s, fargs, nullptr);
 }
 
 hipError_t jit_launch_slack(const JitModule &m, const uint8_t *levels, int64_t B, const float2 *tab,
-                            float *S, float *T, float *E, float target, uint32_t *mask,
-                            void *part, hipStream_t s) {
+                            float *S, float *T, float *E, const SelTargets &tg, hipStream_t s) {
     long long b = B;
-    void *args[] = {&levels, &b, &tab, &S, &T, &E, &target, &mask, &part};
+    SelTargets dt = tg;
+    void *args[] = {&levels, &b, &tab, &S, &T, &E, &dt};
     return hipModuleLaunchKernel(m.slack, capped_grid(B, m.block, m.slack_cap), 1, 1, m.block, 1, 1, 0,
                                  s, args, nullptr);
 }

@@ -22,8 +22,10 @@
 //   levels the current 128-byte line of the candidate's level row, in registers.
 // Scratch layouts put one wave's access to a slot in one contiguous 256-byte segment.
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
+#include <cstring>
 #include <mutex>
 
 #include "emo_internal.h"
@@ -359,8 +361,7 @@ __device__ __forceinline__ LaneCtx lane_ctx(int64_t B) {
 template <int MODE>
 __global__ void __launch_bounds__(kBlock)
 forward_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ T_out,
-               float *__restrict__ E_out, float target, uint32_t *__restrict__ mask,
-               EmoPartial *part, float *cold, int64_t bpad, bool vec, int wlog) {
+               float *__restrict__ E_out, EmoTargets tg, float *cold, int64_t bpad, bool vec, int wlog) {
     extern __shared__ float4 smem4[];
     Tab<MODE> tab = make_tab<MODE>(g, smem4, wlog);
     const LaneCtx x = lane_ctx(B);
@@ -372,7 +373,7 @@ forward_kernel(DevGraph g, const uint8_t *__restrict__ levels, int64_t B, float 
         if (T_out) T_out[x.cand] = f.T;
         if (E_out) E_out[x.cand] = f.E;
     }
-    if (mask || part) emo_select_block(blockIdx.x, x.active, f.T, f.E, x.cand, B, target, mask, part);
+    if (tg.n) emo_select_all(blockIdx.x, x.active, f.T, f.E, x.cand, B, tg);
 }
 
 // Forward + backward (slack) pass with the same optional outputs.
@@ -380,8 +381,7 @@ template <int MODE, bool STAGED>
 __global__ void __launch_bounds__(kBlock)
 slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict__ levels, int64_t B,
              float *__restrict__ S, float *__restrict__ T_out, float *__restrict__ E_out,
-             float target, uint32_t *__restrict__ mask, EmoPartial *part, float *cold, float *keep,
-             float *cold_bwd, int64_t bpad, bool vec, int wlog) {
+             EmoTargets tg, float *cold, float *keep, float *cold_bwd, int64_t bpad, bool vec, int wlog) {
     extern __shared__ float4 smem4[];
     Tab<MODE> tab = make_tab<MODE>(g, smem4, wlog);
     __shared__ float stg_all[STAGED ? kWavesPerBlock : 1][STAGED ? kStage * 65 : 1];
@@ -397,7 +397,7 @@ slack_kernel(DevGraph g, DevProgram pr, int32_t cols, const uint8_t *__restrict_
     float *stg = STAGED ? stg_all[threadIdx.x / kWave] : nullptr;
     run_backward<MODE, STAGED>(pr, tab, g.F, f.bad ? 0.f : f.T, f.bad, row, hot, sc, S, cols, x.cand,
                                x.active, stg, x.wbase, B);
-    if (mask || part) emo_select_block(blockIdx.x, x.active, f.T, f.E, x.cand, B, target, mask, part);
+    if (tg.n) emo_select_all(blockIdx.x, x.active, f.T, f.E, x.cand, B, tg);
 }
 
 // ---------------------------------------------------------------- time-interval policies
@@ -516,8 +516,8 @@ __device__ __forceinline__ Fwd run_forward_iv(const DevProgram &pr, Tab<MODE> &t
 template <int MODE, int NREG>
 __global__ void __launch_bounds__(kBlock)
 interval_kernel(DevGraph g, IvPolicy pol, const uint8_t *__restrict__ levels, int64_t B,
-                float *__restrict__ T_out, float *__restrict__ E_out, float target,
-                uint32_t *__restrict__ mask, EmoPartial *part, float *cold, int64_t bpad, bool vec,
+                float *__restrict__ T_out, float *__restrict__ E_out, EmoTargets tg, float *cold,
+                int64_t bpad, bool vec,
                 int wlog) {
     extern __shared__ float4 smem4[];
     __shared__ float s_pts[kMaxIntervals];
@@ -538,7 +538,7 @@ interval_kernel(DevGraph g, IvPolicy pol, const uint8_t *__restrict__ levels, in
         if (T_out) T_out[x.cand] = f.T;
         if (E_out) E_out[x.cand] = f.E;
     }
-    if (mask || part) emo_select_block(blockIdx.x, x.active, f.T, f.E, x.cand, B, target, mask, part);
+    if (tg.n) emo_select_all(blockIdx.x, x.active, f.T, f.E, x.cand, B, tg);
 }
 
 // ---------------------------------------------------------------- selection (Eq. 4)
@@ -561,7 +561,10 @@ constexpr int kFinThreads = 1024;
 constexpr int kFinWaves = kFinThreads / kWave;
 
 __global__ void __launch_bounds__(kFinThreads)
-select_finalize_kernel(const EmoPartial *__restrict__ part, int64_t n, emo_selection *res) {
+select_finalize_kernel(const EmoPartial *__restrict__ parts, int64_t n, emo_selection *results) {
+    // workgroup k: target k's records
+    const EmoPartial *__restrict__ part = parts + static_cast<int64_t>(blockIdx.x) * n;
+    emo_selection *res = results + blockIdx.x;
     __shared__ unsigned long long s_key[kFinWaves];
     __shared__ float s_T[kFinWaves];
     __shared__ unsigned long long s_cnt[kFinWaves];
@@ -629,8 +632,8 @@ constexpr int kSelPer = 4;
 constexpr int64_t kSelGroup = static_cast<int64_t>(kBlock) * kSelPer;
 
 __global__ void __launch_bounds__(kBlock)
-select_results_kernel(const float *__restrict__ T, const float *__restrict__ E, int64_t B,
-                      float target, uint32_t *__restrict__ mask, EmoPartial *part, bool vec) {
+select_results_kernel(const float *__restrict__ T, const float *__restrict__ E, int64_t B, EmoTargets tg,
+                      bool vec) {
     __shared__ unsigned long long s_key[kWavesPerBlock];
     __shared__ float s_T[kWavesPerBlock];
     __shared__ unsigned int s_cnt[kWavesPerBlock];
@@ -651,52 +654,60 @@ select_results_kernel(const float *__restrict__ T, const float *__restrict__ E, 
             e[k] = in ? E[c0 + k] : 0.f;
         }
     }
-    unsigned int nib = 0u;
-    unsigned long long key = ~0ull;
-    float kT = 0.f;
+    // the targets one after another from the same loaded makespans and energies
+    for (int j = 0; j < tg.n; ++j) {
+        const float target = tg.t[j];
+        unsigned int *mask = tg.mask[j];
+        EmoPartial *part = tg.part ? tg.part + j * tg.nparts : nullptr;
+        unsigned int nib = 0u;
+        unsigned long long key = ~0ull;
+        float kT = 0.f;
 #pragma unroll
-    for (int k = 0; k < kSelPer; ++k) {
-        const bool feas = c0 + k < B && t[k] <= target;   // false for NaN
-        nib |= feas ? 1u << k : 0u;
-        const unsigned long long kk = feas ? (static_cast<unsigned long long>(__float_as_uint(e[k])) << 32) |
-                                                 static_cast<unsigned long long>(c0 + k)
-                                           : ~0ull;
-        if (kk < key) {
-            key = kk;
-            kT = t[k];
+        for (int k = 0; k < kSelPer; ++k) {
+            const bool feas = c0 + k < B && t[k] <= target;   // false for NaN
+            nib |= feas ? 1u << k : 0u;
+            const unsigned long long kk = feas ? (static_cast<unsigned long long>(__float_as_uint(e[k])) << 32) |
+                                                     static_cast<unsigned long long>(c0 + k)
+                                               : ~0ull;
+            if (kk < key) {
+                key = kk;
+                kT = t[k];
+            }
+        }
+        if (mask) {
+            unsigned int w = nib << (kSelPer * (lane & 7));
+            w |= __shfl_xor(w, 1, kWave);
+            w |= __shfl_xor(w, 2, kWave);
+            w |= __shfl_xor(w, 4, kWave);
+            const int64_t word = c0 / 32;
+            if ((lane & 7) == 0 && word * 32 < B) mask[word] = w;
+        }
+        if (!part) continue;
+        emo_wave_min_key(&key, &kT);
+        unsigned int cnt = static_cast<unsigned int>(__popc(nib));
+        for (int off = kWave / 2; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+        if (j > 0) __syncthreads();   // the previous target's records have been read
+        if (lane == 0) {
+            s_key[wave] = key;
+            s_T[wave] = kT;
+            s_cnt[wave] = cnt;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            EmoPartial p;
+            p.key = s_key[0];
+            p.makespan = s_T[0];
+            p.count = s_cnt[0];
+            for (int w = 1; w < kWavesPerBlock; ++w) {
+                if (s_key[w] < p.key) {
+                    p.key = s_key[w];
+                    p.makespan = s_T[w];
+                }
+                p.count += s_cnt[w];
+            }
+            part[blockIdx.x] = p;
         }
     }
-    if (mask) {
-        unsigned int w = nib << (kSelPer * (lane & 7));
-        w |= __shfl_xor(w, 1, kWave);
-        w |= __shfl_xor(w, 2, kWave);
-        w |= __shfl_xor(w, 4, kWave);
-        const int64_t word = c0 / 32;
-        if ((lane & 7) == 0 && word * 32 < B) mask[word] = w;
-    }
-    emo_wave_min_key(&key, &kT);
-    unsigned int cnt = static_cast<unsigned int>(__popc(nib));
-    for (int off = kWave / 2; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
-    if (!part) return;
-    if (lane == 0) {
-        s_key[wave] = key;
-        s_T[wave] = kT;
-        s_cnt[wave] = cnt;
-    }
-    __syncthreads();
-    if (threadIdx.x != 0) return;
-    EmoPartial p;
-    p.key = s_key[0];
-    p.makespan = s_T[0];
-    p.count = s_cnt[0];
-    for (int w = 1; w < kWavesPerBlock; ++w) {
-        if (s_key[w] < p.key) {
-            p.key = s_key[w];
-            p.makespan = s_T[w];
-        }
-        p.count += s_cnt[w];
-    }
-    part[blockIdx.x] = p;
 }
 
 int64_t grid_for(int64_t B) { return (B + kBlock - 1) / kBlock; }
@@ -749,8 +760,18 @@ size_t slack_scratch_bytes(const DevProgram &prog, int64_t B) {
     return rows * static_cast<size_t>(grid_for(B) * kBlock) * sizeof(float);
 }
 
+static_assert(sizeof(EmoTargets) == sizeof(SelTargets) && offsetof(EmoTargets, part) == offsetof(SelTargets, part) &&
+                  offsetof(EmoTargets, t) == offsetof(SelTargets, t) &&
+                  offsetof(EmoTargets, mask) == offsetof(SelTargets, mask),
+              "the targets' kernel argument layout");
+EmoTargets dev_targets(const SelTargets &tg) {
+    EmoTargets d;
+    std::memcpy(&d, &tg, sizeof(d));
+    return d;
+}
+
 hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, float *T, float *E,
-                          float target, uint32_t *mask, void *part, void *scratch, hipStream_t s) {
+                          const SelTargets &tg, void *scratch, hipStream_t s) {
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
     float *cold = g.eval.n_cold > 0 ? static_cast<float *>(scratch) : nullptr;
@@ -758,9 +779,9 @@ hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, f
     const int mode = table_mode(g, g.eval, 0, &dyn);
     const bool vec = vec_levels(g, levels);
     const int wlog = window_log(g);
-    EmoPartial *pp = static_cast<EmoPartial *>(part);
+    const EmoTargets dt = dev_targets(tg);
     const dim3 gd(static_cast<unsigned>(grid)), bd(kBlock);
-#define EMO_FWD_ARGS g, levels, B, T, E, target, mask, pp, cold, bpad, vec, wlog
+#define EMO_FWD_ARGS g, levels, B, T, E, dt, cold, bpad, vec, wlog
     if (mode == kTabLds) hipLaunchKernelGGL(forward_kernel<kTabLds>, gd, bd, dyn, s, EMO_FWD_ARGS);
     else if (mode == kTabWindow) hipLaunchKernelGGL(forward_kernel<kTabWindow>, gd, bd, dyn, s, EMO_FWD_ARGS);
     else hipLaunchKernelGGL(forward_kernel<kTabGlobal>, gd, bd, dyn, s, EMO_FWD_ARGS);
@@ -770,7 +791,7 @@ hipError_t launch_forward(const DevGraph &g, const uint8_t *levels, int64_t B, f
 
 hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_cols,
                         const uint8_t *levels, int64_t B, float *slack, float *T, float *E,
-                        float target, uint32_t *mask, void *part, void *scratch, hipStream_t s) {
+                        const SelTargets &tg, void *scratch, hipStream_t s) {
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
     const size_t n_cold = static_cast<size_t>(prog.n_cold), n_keep = static_cast<size_t>(prog.n_ops),
@@ -788,9 +809,9 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
     const int mode = table_mode(g, prog, stage_bytes, &dyn);
     const bool vec = vec_levels(g, levels);
     const int wlog = window_log(g);
-    EmoPartial *pp = static_cast<EmoPartial *>(part);
+    const EmoTargets dt = dev_targets(tg);
     const dim3 gd(static_cast<unsigned>(grid)), bd(kBlock);
-#define EMO_SLACK_ARGS g, prog, out_cols, levels, B, slack, T, E, target, mask, pp, cold, keep, cold_b, bpad, vec, wlog
+#define EMO_SLACK_ARGS g, prog, out_cols, levels, B, slack, T, E, dt, cold, keep, cold_b, bpad, vec, wlog
     if (mode == kTabLds && staged) hipLaunchKernelGGL((slack_kernel<kTabLds, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
     else if (mode == kTabLds) hipLaunchKernelGGL((slack_kernel<kTabLds, false>), gd, bd, dyn, s, EMO_SLACK_ARGS);
     else if (mode == kTabWindow && staged) hipLaunchKernelGGL((slack_kernel<kTabWindow, true>), gd, bd, dyn, s, EMO_SLACK_ARGS);
@@ -802,8 +823,7 @@ hipError_t launch_slack(const DevGraph &g, const DevProgram &prog, int32_t out_c
 }
 
 hipError_t launch_intervals(const DevGraph &g, const IvPolicy &pol, const uint8_t *levels, int64_t B,
-                            float *T, float *E, float target, uint32_t *mask, void *part, void *scratch,
-                            hipStream_t s) {
+                            float *T, float *E, const SelTargets &tg, void *scratch, hipStream_t s) {
     const int64_t grid = grid_for(B);
     const int64_t bpad = grid * kBlock;
     float *cold = g.eval.n_cold > 0 ? static_cast<float *>(scratch) : nullptr;
@@ -811,9 +831,9 @@ hipError_t launch_intervals(const DevGraph &g, const IvPolicy &pol, const uint8_
     const int mode = table_mode(g, g.eval, 0, &dyn);
     const bool vec = pol.K % 16 == 0 && reinterpret_cast<uintptr_t>(levels) % 16 == 0;
     const int wlog = window_log(g);
-    EmoPartial *pp = static_cast<EmoPartial *>(part);
+    const EmoTargets dt = dev_targets(tg);
     const dim3 gd(static_cast<unsigned>(grid)), bd(kBlock);
-#define EMO_IV_ARGS g, pol, levels, B, T, E, target, mask, pp, cold, bpad, vec, wlog
+#define EMO_IV_ARGS g, pol, levels, B, T, E, dt, cold, bpad, vec, wlog
     const bool reg = pol.K - 1 <= kIvRegPoints;
     if (mode == kTabLds && reg) hipLaunchKernelGGL((interval_kernel<kTabLds, kIvRegPoints>), gd, bd, dyn, s, EMO_IV_ARGS);
     else if (mode == kTabLds) hipLaunchKernelGGL((interval_kernel<kTabLds, 0>), gd, bd, dyn, s, EMO_IV_ARGS);
@@ -830,18 +850,19 @@ hipError_t launch_empty_result(emo_selection *res, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_select_finalize(const void *part, int64_t nparts, emo_selection *res,
-                                  hipStream_t s) {
-    hipLaunchKernelGGL(select_finalize_kernel, dim3(1), dim3(kFinThreads), 0, s,
-                       static_cast<const EmoPartial *>(part), nparts, res);
+hipError_t launch_select_finalize(const SelTargets &tg, emo_selection *results, hipStream_t s) {
+    if (tg.n < 1 || !tg.part) return hipSuccess;
+    hipLaunchKernelGGL(select_finalize_kernel, dim3(static_cast<unsigned>(tg.n)), dim3(kFinThreads), 0, s,
+                       static_cast<const EmoPartial *>(tg.part), tg.nparts, results);
     return hipGetLastError();
 }
 
-hipError_t launch_select_results(const float *T, const float *E, int64_t B, float target,
-                                 uint32_t *mask, void *part, hipStream_t s) {
+hipError_t launch_select_results(const float *T, const float *E, int64_t B, const SelTargets &tg,
+                                 hipStream_t s) {
+    if (tg.n < 1) return hipSuccess;
     const bool vec = (reinterpret_cast<uintptr_t>(T) | reinterpret_cast<uintptr_t>(E)) % 16 == 0;
     hipLaunchKernelGGL(select_results_kernel, dim3(static_cast<unsigned>(select_results_blocks(B))), dim3(kBlock),
-                       0, s, T, E, B, target, mask, static_cast<EmoPartial *>(part), vec);
+                       0, s, T, E, B, dev_targets(tg), vec);
     return hipGetLastError();
 }
 

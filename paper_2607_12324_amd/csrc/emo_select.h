@@ -34,6 +34,12 @@ struct EmoSel {
     long long num_feasible;
 };
 
+// Mask words and partial records are stored through global (address space 1) pointers: a
+// pointer taken from the targets' argument array with a run-time index is otherwise generic,
+// and its flat stores would also count against the LDS wait counter.
+#define EMO_SEL_GLOBAL(T, p) ((__attribute__((address_space(1))) T *)(p))
+typedef unsigned int emo_sel_u4 __attribute__((ext_vector_type(4)));
+
 // Least key over the wave, carrying the makespan of its candidate.
 __device__ __forceinline__ void emo_wave_min_key(unsigned long long *key, float *T) {
     for (int off = EMO_WAVE / 2; off > 0; off >>= 1) {
@@ -62,8 +68,8 @@ __device__ void emo_select_block(long long group, bool active, float T, float E,
     if (mask && lane == 0 && wbase < B) {
         const long long nwords = (B + 31) / 32;
         const long long w = wbase / 32;
-        mask[w] = (unsigned int)bal;
-        if (w + 1 < nwords) mask[w + 1] = (unsigned int)(bal >> 32);
+        EMO_SEL_GLOBAL(unsigned int, mask)[w] = (unsigned int)bal;
+        if (w + 1 < nwords) EMO_SEL_GLOBAL(unsigned int, mask)[w + 1] = (unsigned int)(bal >> 32);
     }
     if (!part) return;
     unsigned long long key = feas ? (((unsigned long long)__float_as_uint(E)) << 32) |
@@ -89,6 +95,35 @@ __device__ void emo_select_block(long long group, bool active, float T, float E,
             }
             p.count += s_cnt[w];
         }
-        part[group] = p;
+        // one 16-byte store in the record's layout: key (low word first), count, makespan
+        const emo_sel_u4 v = {(unsigned int)p.key, (unsigned int)(p.key >> 32), p.count,
+                              __float_as_uint(p.makespan)};
+        *EMO_SEL_GLOBAL(emo_sel_u4, part + group) = v;
     }
 }
+
+// The latency targets of one evaluation (Eq. 4 at each of them): the feasibility mask of target
+// k goes to mask[k] (when not NULL) and its per-group partial records to part + k * nparts (all
+// targets, when part is not NULL).  n = 0: no mask and no selection.
+#define EMO_MAX_TARGETS 8
+struct EmoTargets {
+    int n;
+    int pad;
+    long long nparts;
+    EmoPartial *part;
+    float t[EMO_MAX_TARGETS];
+    unsigned int *mask[EMO_MAX_TARGETS];
+};
+
+// Stage 1 for every target of `tg` (see emo_select_block; called by every thread of the
+// workgroup, the targets one after another).
+__device__ void emo_select_all(long long group, bool active, float T, float E, long long c,
+                               long long B, const EmoTargets &tg) {
+    for (int k = 0; k < tg.n; ++k) {
+        // the previous target's records in LDS have been read before they are overwritten
+        if (k > 0 && tg.part) __syncthreads();
+        emo_select_block(group, active, T, E, c, B, tg.t[k], tg.mask[k],
+                         tg.part ? tg.part + k * tg.nparts : (EmoPartial *)0);
+    }
+}
+

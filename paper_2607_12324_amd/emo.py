@@ -22,7 +22,7 @@ STATUS_NAMES = {0: "EMO_OK", 1: "EMO_ERR_INVALID_ARGUMENT", 2: "EMO_ERR_CYCLE",
 
 ENTRY_POINTS = ("emo_load_graph", "emo_free_graph", "emo_graph_get_info",
                 "emo_graph_set_kernel_mode", "emo_graph_topo_order",
-                "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate",
+                "emo_eval_policies", "emo_slack", "emo_select_policy", "emo_evaluate", "emo_evaluate_targets",
                 "emo_select_from_results", "emo_select_from_results_noalloc", "emo_dp_search", "emo_eval_intervals",
                 "emo_graph_set_timing_events", "emo_pack_kernels", "emo_contract_packs",
                 "emo_pack_model",
@@ -77,6 +77,7 @@ def _load_library():
         "emo_slack": [P, P, i64, P, i32, P, P, P],
         "emo_select_policy": [P, P, i64, f32, P, P, P],
         "emo_evaluate": [P, P, i64, P, P, P, i32, f32, P, P, P],
+        "emo_evaluate_targets": [P, P, i64, P, P, P, i32, i32, P, P, P, P],
         "emo_select_from_results": [P, P, i64, f32, P, P, P],
         "emo_select_from_results_noalloc": [P, P, i64, f32, P, P, P],
         "emo_dp_search": [P, f32, f32, P, i32, P, P, P],
@@ -269,6 +270,29 @@ class EmoGraph:
                                 float(latency_target), _dptr(mask, torch.int32, (B + 31) // 32, "mask"),
                                 _dptr(result, torch.int64, 3, "result"), _stream(stream)))
         return makespan, energy, slack, mask, result
+
+    def evaluate_targets(self, levels, latency_targets, makespan=None, energy=None, slack=None,
+                         per_node: bool = False, masks=None, results=None, stream=None):
+        """emo_evaluate with several latency targets in one pass (emo_evaluate_targets).
+        masks: None or a list of one int32 tensor (or None) per target; results: None or an
+        int64 [n, 3] tensor (one emo_selection per target)."""
+        import torch
+        lv, B = self._levels(levels)
+        cols = self.num_nodes if per_node else self.num_packs
+        tg = np.ascontiguousarray(np.asarray(latency_targets, dtype=np.float32).reshape(-1))
+        n = int(tg.size)
+        mk = None
+        if masks is not None:
+            if len(masks) != n:
+                raise ValueError(f"masks must hold {n} entries")
+            mk = (ctypes.c_void_p * n)(*[_dptr(m, torch.int32, (B + 31) // 32, "mask") for m in masks])
+        _check(lib.emo_evaluate_targets(self._h, lv, B, _dptr(makespan, torch.float32, B, "makespan"),
+                                        _dptr(energy, torch.float32, B, "energy"),
+                                        _dptr(slack, torch.float32, B * cols, "slack"),
+                                        int(bool(per_node)), n, _nptr(tg) if n else None,
+                                        ctypes.cast(mk, ctypes.c_void_p) if mk is not None else None,
+                                        _dptr(results, torch.int64, 3 * n, "results"), _stream(stream)))
+        return makespan, energy, slack, masks, results
 
     def select_policy(self, levels, latency_target: float, mask=None, result=None, stream=None,
                       want_mask: bool = True):

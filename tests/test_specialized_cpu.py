@@ -111,10 +111,11 @@ def test_workload_kernels_compile_without_spills(emo, hiprtc, tmp_path, k):
     path = compile_source(hiprtc, src, tmp_path)
     expect = ["emo_sp_select"] + (["emo_sp_slack"] if g.num_packs <= 160 else [])
     notes, asm = check_code_object(path, expect)
-    # the forward pass is straight-line: roughly five vector instructions per pack
+    # the forward pass is straight-line: roughly five vector instructions per pack, plus a
+    # fixed amount for the group loop and the selection loop over the latency targets
     body = asm.split("<emo_sp_select>:")[1].split("s_endpgm")[0]
     valu = len(re.findall(r"^\s+v_", body, flags=re.M))
-    assert valu < 6.5 * g.num_packs + 200, valu
+    assert valu < 6.5 * g.num_packs + 300, valu
 
 
 def test_large_graph_is_not_one_kernel(emo):
