@@ -331,8 +331,10 @@ LevelPlan emit_forward_range(std::ostringstream &o, const JitGraph &g, const Ran
         if (r.accumulate && op.out.empty()) o << "  T = fmaxf(T, f" << i << ");\n";
         if (r.ck_copy && (*r.ck_copy)[i]) o << "  c" << i << " = f" << i << ";\n";
         if (r.ck_row && (*r.ck_row)[i] >= 0) {
-            o << "  " << ((*r.ck_always)[i] ? "" : "if (full) ") << "EMO_AT(ck, " << (*r.ck_row)[i]
-              << ") = f" << i << ";\n";
+            if ((*r.ck_always)[i])
+                o << "  EMO_AT(ck, " << (*r.ck_row)[i] << ") = f" << i << ";\n";
+            else
+                o << "  EMO_CKST(" << (*r.ck_row)[i] << ", f" << i << ");\n";
         }
     }
     return lp;
@@ -827,15 +829,44 @@ TabWindow chain_window(const JitGraph &g, int a, int b, size_t budget, size_t en
     return w;
 }
 
-void emit_table(std::ostringstream &o, const JitGraph &g, const TabWindow &w, const char *type) {
+// Copy of `entries` table elements of `elem_bytes` bytes from tabg + base into the LDS array
+// tab by `block` threads: every 16-byte piece a thread copies is requested before the first is
+// stored, so the copy costs one round trip to the L2 instead of one per piece (a strided loop
+// waits for each load before the next).  Needs tabg + base 16-byte aligned (the device tables
+// are, from their allocation); otherwise a plain unrolled loop.  No barrier.
+std::string table_copy(long long entries, long long base, int elem_bytes, int block) {
+    std::ostringstream o;
+    const long long bytes = entries * elem_bytes;
+    if ((base * elem_bytes) % 16 != 0 || bytes % 16 != 0) {
+        o << "  #pragma unroll\n"
+             "  for (int i_ = threadIdx.x; i_ < " << entries << "; i_ += " << block << ") tab[i_] = tabg["
+          << base << "LL + i_];\n";
+        return o.str();
+    }
+    const long long pieces = bytes / 16;
+    const long long rounds = pieces / block, rest = pieces % block;
+    o << "  {\n"
+         "  const EMO_GLOBAL emo_u32x4 *src_ = (const EMO_GLOBAL emo_u32x4 *)(tabg + " << base << "LL);\n"
+         "  emo_u32x4 *dst_ = (emo_u32x4 *)tab;\n";
+    for (long long k = 0; k < rounds; ++k)
+        o << "  const emo_u32x4 tc" << k << " = src_[threadIdx.x + " << k * block << "];\n";
+    if (rest)
+        o << "  const emo_u32x4 tcr = threadIdx.x < " << rest << " ? src_[threadIdx.x + " << rounds * block
+          << "] : (emo_u32x4)(0u);\n";
+    for (long long k = 0; k < rounds; ++k) o << "  dst_[threadIdx.x + " << k * block << "] = tc" << k << ";\n";
+    if (rest) o << "  if (threadIdx.x < " << rest << ") dst_[threadIdx.x + " << rounds * block << "] = tcr;\n";
+    o << "  }\n";
+    return o.str();
+}
+
+void emit_table(std::ostringstream &o, const JitGraph &g, const TabWindow &w, const char *type,
+                int elem_bytes, int block) {
     if (!w.lds) {
         o << "  const " << type << " *__restrict__ tab = tabg;\n";
         return;
     }
     o << "  __shared__ " << type << " tab[" << w.entries << "];\n"
-      << "  for (int i_ = threadIdx.x; i_ < " << w.entries << "; i_ += EMO_BLOCK) tab[i_] = tabg["
-      << w.base_pack * g.F << "LL + i_];\n"
-      << "  __syncthreads();\n";
+      << table_copy(w.entries, w.base_pack * g.F, elem_bytes, block) << "  __syncthreads();\n";
 }
 
 // Lane setup of a segmented kernel.  Scratch row r is addressed as a uniform base
@@ -880,10 +911,16 @@ void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPla
          "    const float2 *__restrict__ tabg, float *__restrict__ ck, float *__restrict__ Tc,\n"
          "    double *__restrict__ Edc, float *__restrict__ Ebc, int full, float *__restrict__ To,\n"
          "    float *__restrict__ Eo, EmoTargets tg) {\n";
-    emit_table(o, g, w, "float2");
+    emit_table(o, g, w, "float2", 8, cp.block);
     o << chain_lanes(cp.block);
     o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
-    o << "  unsigned int bad = 0u;\n  (void)full;\n";
+    // checkpoints only the backward kernels read: stored through a buffer resource whose range
+    // is empty without slack (the hardware drops those stores), so no branch splits the code
+    o << "  unsigned int bad = 0u;\n"
+         "  const int ckn = full ? (int)(unsigned int)(bp * 4) : 0;\n"
+         "  (void)ckn;\n"
+         "#define EMO_CKST(r, v) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), "
+         "__builtin_amdgcn_make_buffer_rsrc((void *)(ck + (long long)(r) * bp), (short)0, ckn, 0x00020000), o4, 0, 0)\n";
     if (j == 0) {
         o << "  float T = " << flit(g.t_const) << ";\n  float eb = 0.f;\n  double ed = 0.0;\n";
     } else {
@@ -969,9 +1006,7 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
          "    const float *__restrict__ Tc, float *__restrict__ bk, float *__restrict__ S) {\n";
     if (w.lds) {
         o << "  __shared__ float tab[" << w.entries << "];\n"
-          << "  for (int i_ = threadIdx.x; i_ < " << w.entries << "; i_ += " << cp.bblock << ") tab[i_] = tabg["
-          << w.base_pack * g.F << "LL + i_];\n"
-          << "  __syncthreads();\n";
+          << table_copy(w.entries, w.base_pack * g.F, 4, cp.bblock) << "  __syncthreads();\n";
     } else {
         o << "  const float *__restrict__ tab = tabg;\n";
     }
@@ -1001,17 +1036,48 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
     for (int u : later) o << "  const float s" << u << " = EMO_AT(bk, " << cp.bk_row[u] << ");\n";
     for (int i = a; i < b; ++i)
         if (!g.ops[i].in.empty()) o << "  float s" << i << ";\n";
-    // sub-segments from last to first: recompute their finish times, then walk them backwards
+    // sub-segments from last to first: recompute their finish times, then walk them backwards.
+    // The checkpoints and level words of the next sub-segment are requested during this one's
+    // walk, before its slack stores: on this GPU a wait for a load also waits for every store
+    // issued before it, so loads issued after the stores would stall on their completion.
     int r_first = 0;
     while (cp.sub[r_first] < a) ++r_first;
     int r_last = r_first;
     while (cp.sub[r_last + 1] < b) ++r_last;
+    const int width = jit_level_width(g);
+    auto word_range = [&](int c, int d, int *lo, int *hi) {
+        *lo = g.P;
+        *hi = 0;
+        for (int i = c; i < d; ++i)
+            if (g.ops[i].pack >= 0) {
+                *lo = std::min(*lo, g.ops[i].pack / width);
+                *hi = std::max(*hi, g.ops[i].pack / width + 1);
+            }
+        if (*lo >= *hi) *lo = *hi = 0;
+    };
+    for (int r = r_first; r < r_last; ++r) {
+        for (int k : inputs_before(g, cp.sub[r], cp.sub[r + 1])) o << "  float pf" << r << "_" << k << ";\n";
+        int lo, hi;
+        word_range(cp.sub[r], cp.sub[r + 1], &lo, &hi);
+        for (int q = lo; q < hi && width > 1; ++q)
+            o << "  " << (width == 16 ? "emo_u32x4" : "unsigned int") << " P" << r << "L" << q << ";\n";
+    }
+    auto prefetch = [&](int r) {
+        for (int k : inputs_before(g, cp.sub[r], cp.sub[r + 1]))
+            o << "  pf" << r << "_" << k << " = EMO_AT(ck, " << cp.ck_row[k] << ");\n";
+        int lo, hi;
+        word_range(cp.sub[r], cp.sub[r + 1], &lo, &hi);
+        for (int q = lo; q < hi && width > 1; ++q) o << "  P" << r << "L" << q << " = rowp[" << q << "];\n";
+    };
     std::vector<std::string> level_expr(g.ops.size());
     for (int r = r_last; r >= r_first; --r) {
         const int c = cp.sub[r], d = cp.sub[r + 1];
+        const bool fetched = r < r_last;
         o << "  {\n";
-        for (int k : inputs_before(g, c, d))
-            o << "  const float f" << k << " = EMO_AT(ck, " << cp.ck_row[k] << ");\n";
+        for (int k : inputs_before(g, c, d)) {
+            if (fetched) o << "  const float f" << k << " = pf" << r << "_" << k << ";\n";
+            else o << "  const float f" << k << " = EMO_AT(ck, " << cp.ck_row[k] << ");\n";
+        }
         RangeOpts ro;
         ro.a = c;
         ro.b = d;
@@ -1022,8 +1088,17 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
         ro.preload = false;
         ro.checks = false;
         ro.time_only = true;
+        if (fetched && width > 1) {
+            ro.pfx = "P" + std::to_string(r) + "L";
+            word_range(c, d, &ro.pre_lo, &ro.pre_hi);
+        }
         LevelPlan lp = emit_forward_range(o, g, ro, &level_expr);
         lp.launder();
+        bool prefetched = r == r_first;
+        if (!cp.staged && !prefetched) {
+            prefetch(r - 1);
+            prefetched = true;
+        }
         for (int i = d - 1; i >= c; --i) {
             const JitOp &op = g.ops[i];
             // table reads index through zb, and level bytes are extracted from words, that pass
@@ -1070,12 +1145,17 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
                 if (cp.staged) {
                     const int k = p % 32;
                     o << "  stg[" << k * 64 << " + (lane ^ " << 8 * (k / 4) << ")] = " << v << ";\n";
+                    if (k == 0 && !prefetched) {
+                        prefetch(r - 1);
+                        prefetched = true;
+                    }
                     if (k == 0) o << "  emo_cflush(stg, S, wbase, B, " << p << ");\n";
                 } else {
                     o << "  srow[" << p << "] = " << v << ";\n";
                 }
             }
         }
+        if (!prefetched) prefetch(r - 1);
         o << "  }\n";
     }
     o << "}\n\n";
@@ -1315,8 +1395,7 @@ void emit_cut_segment(std::ostringstream &o, const JitGraph &g, const CutPlan &c
     const int q_lo = plo / width, q_hi = phi / width + 1;
     o << "  case " << j << ": {\n";
     if (slack) {
-        o << "  for (int i_ = threadIdx.x; i_ < " << w.entries << "; i_ += EMO_BLOCK) tab[i_] = tabg["
-          << w.base_pack * g.F << "LL + i_];\n  __syncthreads();\n";
+        o << table_copy(w.entries, w.base_pack * g.F, 8, cp.block) << "  __syncthreads();\n";
         o << "  {\n";
         o << "  const u8 *__restrict__ row = lv + cand * " << g.P << "LL;\n";
     } else {
@@ -1328,8 +1407,7 @@ void emit_cut_segment(std::ostringstream &o, const JitGraph &g, const CutPlan &c
         o << LevelPlan::row_decl(width);
         for (int q = q_lo; q < q_hi; ++q)
             o << "  " << (width == 16 ? "emo_u32x4" : "unsigned int") << " L" << q << " = rowp[" << q << "];\n";
-        o << "  for (int i_ = threadIdx.x; i_ < " << w.entries << "; i_ += EMO_BLOCK) tab[i_] = tabg["
-          << w.base_pack * g.F << "LL + i_];\n  __syncthreads();\n";
+        o << table_copy(w.entries, w.base_pack * g.F, 8, cp.block) << "  __syncthreads();\n";
     }
     if (slack)
         for (int i = a; i < b; ++i)
