@@ -647,7 +647,11 @@ struct WinBufs {
 template <int NT>
 __device__ __forceinline__ void win_load_full(const WinArgs &a, const WinPlan &p, const WinBufs &b, int w,
                                               WinSet &s) {
-    const int so_lvl = w << a.wlog, so_tab = w * b.tab_win, so_blk = w * a.blk_bytes;
+    // the window offsets are uniform; readfirstlane says so to the compiler (an offset it takes
+    // for divergent becomes a loop over the distinct values around each load)
+    const int so_lvl = __builtin_amdgcn_readfirstlane(w << a.wlog);
+    const int so_tab = __builtin_amdgcn_readfirstlane(w * b.tab_win);
+    const int so_blk = __builtin_amdgcn_readfirstlane(w * a.blk_bytes);
 #pragma unroll
     for (int i = 0; i < NT + 2; ++i) {
         emo_u4 v;
