@@ -898,6 +898,18 @@ std::vector<int> inputs_before(const JitGraph &g, int a, int b) {
     return v;
 }
 
+// Level words [*lo, *hi) holding the packs of steps [c, d) (empty when there are none).
+void sub_words(const JitGraph &g, int c, int d, int width, int *lo, int *hi) {
+    *lo = g.P;
+    *hi = 0;
+    for (int i = c; i < d; ++i)
+        if (g.ops[i].pack >= 0) {
+            *lo = std::min(*lo, g.ops[i].pack / width);
+            *hi = std::max(*hi, g.ops[i].pack / width + 1);
+        }
+    if (*lo >= *hi) *lo = *hi = 0;
+}
+
 void emit_chain_forward(std::ostringstream &o, const JitGraph &g, const ChainPlan &cp, int j) {
     const int a = cp.seg[j], b = cp.seg[j + 1];
     const bool last = j + 1 == cp.segments();
@@ -1045,20 +1057,10 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
     int r_last = r_first;
     while (cp.sub[r_last + 1] < b) ++r_last;
     const int width = jit_level_width(g);
-    auto word_range = [&](int c, int d, int *lo, int *hi) {
-        *lo = g.P;
-        *hi = 0;
-        for (int i = c; i < d; ++i)
-            if (g.ops[i].pack >= 0) {
-                *lo = std::min(*lo, g.ops[i].pack / width);
-                *hi = std::max(*hi, g.ops[i].pack / width + 1);
-            }
-        if (*lo >= *hi) *lo = *hi = 0;
-    };
     for (int r = r_first; r < r_last; ++r) {
         for (int k : inputs_before(g, cp.sub[r], cp.sub[r + 1])) o << "  float pf" << r << "_" << k << ";\n";
         int lo, hi;
-        word_range(cp.sub[r], cp.sub[r + 1], &lo, &hi);
+        sub_words(g, cp.sub[r], cp.sub[r + 1], width, &lo, &hi);
         for (int q = lo; q < hi && width > 1; ++q)
             o << "  " << (width == 16 ? "emo_u32x4" : "unsigned int") << " P" << r << "L" << q << ";\n";
     }
@@ -1066,7 +1068,7 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
         for (int k : inputs_before(g, cp.sub[r], cp.sub[r + 1]))
             o << "  pf" << r << "_" << k << " = EMO_AT(ck, " << cp.ck_row[k] << ");\n";
         int lo, hi;
-        word_range(cp.sub[r], cp.sub[r + 1], &lo, &hi);
+        sub_words(g, cp.sub[r], cp.sub[r + 1], width, &lo, &hi);
         for (int q = lo; q < hi && width > 1; ++q) o << "  P" << r << "L" << q << " = rowp[" << q << "];\n";
     };
     std::vector<std::string> level_expr(g.ops.size());
@@ -1090,7 +1092,7 @@ void emit_chain_backward(std::ostringstream &o, const JitGraph &g, const ChainPl
         ro.time_only = true;
         if (fetched && width > 1) {
             ro.pfx = "P" + std::to_string(r) + "L";
-            word_range(c, d, &ro.pre_lo, &ro.pre_hi);
+            sub_words(g, c, d, width, &ro.pre_lo, &ro.pre_hi);
         }
         LevelPlan lp = emit_forward_range(o, g, ro, &level_expr);
         lp.launder();
