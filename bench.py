@@ -39,7 +39,7 @@ VALU_PEAK_TOPS = 39.3   # 256 CUs x 64 fp32 lanes x 2.4 GHz, one op per lane per
 KIND_SOURCES = {0: ("emo_kernels.hip",), 1: ("emo_jit.cpp",), 2: ("emo_jit.cpp",),
                 3: ("emo_chains.hip", "emo_kernels.hip"), 4: ("emo_chains.hip", "emo_kernels.hip"),
                 5: ("emo_jit.cpp",), 6: ("emo_chains.hip", "emo_kernels.hip"),
-                7: ("emo_jit.cpp",), 8: ("emo_chains.hip",)}
+                7: ("emo_jit.cpp",), 8: ("emo_chains.hip", "emo_kernels.hip")}
 
 
 def kernel_source_hash(kind: int) -> str:
