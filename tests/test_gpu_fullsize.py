@@ -1,9 +1,10 @@
 """The benchmark's step at each workload's full size, against the oracle (needs an MI355X).
 
-The step is the calls bench.py times: one emo_evaluate over the whole batch (makespan, energy,
-slack of every pack when the workload has the backward pass, mask and selection at the first
-target), then emo_select_from_results for every further target.  Makespans, energies, masks and
-selections are compared on every candidate.  Slack is compared element by element on every row
+The step is the call bench.py times: one evaluation of the whole batch (makespan, energy, slack
+of every pack when the workload has the backward pass, and a mask and a selection for every
+latency target), through emo_evaluate with one target and emo_evaluate_targets with several.
+Makespans, energies, masks and selections are compared on every candidate; emo_select_from_results
+on the stored makespans and energies is checked against the same selections.  Slack is compared element by element on every row
 of the two smaller workloads, and on a leading slice plus every row of the last workgroups of
 the three larger ones (65,536 rows of the 512- and 4096-pack graphs, 4,096 of the 65,536-kernel
 graph), the oracle computing them on all host cores.
@@ -86,12 +87,14 @@ def test_bench_step_full_size(torch, emo, k):
     E = torch.empty(B, dtype=torch.float32, device=dev)
     S = torch.empty((B, P), dtype=torch.float32, device=dev) if spec.slack else None
     masks = [torch.empty((B + 31) // 32, dtype=torch.int32, device=dev) for _ in targets]
-    results = [torch.empty(3, dtype=torch.int64, device=dev) for _ in targets]
-    # the benchmark's calls, in its order
-    gh.evaluate(lv, makespan=T, energy=E, slack=S, latency_target=targets[0], mask=masks[0],
-                result=results[0])
-    for j in range(1, len(targets)):
-        emo.select_from_results(T, E, targets[j], mask=masks[j], result=results[j])
+    res_all = torch.empty((len(targets), 3), dtype=torch.int64, device=dev)
+    results = [res_all[j] for j in range(len(targets))]
+    # the benchmark's call
+    if len(targets) == 1:
+        gh.evaluate(lv, makespan=T, energy=E, slack=S, latency_target=targets[0], mask=masks[0],
+                    result=results[0])
+    else:
+        gh.evaluate_targets(lv, targets, makespan=T, energy=E, slack=S, masks=masks, results=res_all)
     torch.cuda.synchronize()
     print(f"  device step done (kernels {gh.info()['last_kernels']})", flush=True)
 
@@ -99,6 +102,9 @@ def test_bench_step_full_size(torch, emo, k):
     for tgt, m, r in zip(targets, masks, results):
         parity.assert_selection(emo.parse_selection(r), emo.unpack_mask(m, B), T_or, E_or, tgt,
                                 True, f"{spec.name} select@{tgt}")
+    for tgt, m, r in zip(targets, masks, results):
+        r2, m2 = emo.select_from_results(T, E, tgt)
+        assert np.array_equal(host(r2), host(r)) and np.array_equal(host(m2), host(m)), tgt
     print("  makespan, energy, masks and selections ok", flush=True)
 
     if S_or_all is not None:
