@@ -887,6 +887,11 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
                     if (FIXED) pre += A.dur[i];
                 }
             }
+            // fp32 energy blocks of at most 64 steps, as in the other kernels
+            if ((g & 15) == 15) {
+                ed += static_cast<double>(eb);
+                eb = 0.f;
+            }
         };
         WinGroup<FIXED> G0, G1, G2;
         G0.read(rs, k0);
@@ -1228,6 +1233,11 @@ chains_scan_full(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ b
                     pre += A.dur[i];
                 }
                 eb += te[i].y;
+            }
+            // fp32 energy blocks of at most 64 steps, as in the other kernels
+            if ((gi & 15) == 15) {
+                ed += static_cast<double>(eb);
+                eb = 0.f;
             }
         };
         WinGroup<FIXED> G0, G1, G2;

@@ -169,8 +169,8 @@ def test_intervals_argument_errors(torch, emo):
 
 @pytest.mark.parametrize("K", [1, 16, 17, 256])
 def test_intervals_workload_kernels(torch, emo, K):
-    """The 64-pack graph's specialised time-interval kernel (row in LDS for K <= 16, read from
-    device memory above) on 200,000 candidates with K intervals evenly over [0, 1.05 T0): every
+    """The 64-pack graph's specialised time-interval kernel (rows and the bucket table of the
+    change points in LDS) on 200,003 candidates with K intervals evenly over [0, 1.05 T0): every
     row bit for bit against the interpreting kernel, sampled rows against the oracle, invalid
     levels and a ragged batch included."""
     g = synth.config_graph(2)
