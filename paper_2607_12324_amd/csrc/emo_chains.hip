@@ -887,24 +887,24 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
                     if (FIXED) pre += A.dur[i];
                 }
             }
-            // fp32 energy blocks of at most 64 steps, as in the other kernels
-            if ((g & 15) == 15) {
-                ed += static_cast<double>(eb);
-                eb = 0.f;
-            }
         };
         WinGroup<FIXED> G0, G1, G2;
         G0.read(rs, k0);
         G1.read(rs, k0 + 4);
         G0.levels(lrow);
-        for (int g = 0; g < ng; g += 3) {
-            stage(G0, G1, G2, g);
-            if (g + 1 >= ng) break;
-            stage(G1, G2, G0, g + 1);
-            if (g + 2 >= ng) break;
-            stage(G2, G0, G1, g + 2);
+        // fp32 energy blocks of at most 60 steps (15 groups, a whole number of rotations)
+        for (int c0 = 0; c0 < ng; c0 += 15) {
+            const int c1 = ng < c0 + 15 ? ng : c0 + 15;
+            for (int g = c0; g < c1; g += 3) {
+                stage(G0, G1, G2, g);
+                if (g + 1 >= c1) break;
+                stage(G1, G2, G0, g + 1);
+                if (g + 2 >= c1) break;
+                stage(G2, G0, G1, g + 2);
+            }
+            ed += static_cast<double>(eb);
+            eb = 0.f;
         }
-        ed += static_cast<double>(eb);
         if (w + 1 < nwin) win_store(a, lds, buf ^ 1, tab2 + (buf ^ 1) * L.tab_elems, 8, bad, addf, cm);
         lds_barrier();
     };
@@ -1234,24 +1234,24 @@ chains_scan_full(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ b
                 }
                 eb += te[i].y;
             }
-            // fp32 energy blocks of at most 64 steps, as in the other kernels
-            if ((gi & 15) == 15) {
-                ed += static_cast<double>(eb);
-                eb = 0.f;
-            }
         };
         WinGroup<FIXED> G0, G1, G2;
         G0.read(rs, k0);
         G1.read(rs, k0 + 4);
         G0.levels(lrow);
-        for (int gi = 0; gi < ng; gi += 3) {
-            stage(G0, G1, G2, gi);
-            if (gi + 1 >= ng) break;
-            stage(G1, G2, G0, gi + 1);
-            if (gi + 2 >= ng) break;
-            stage(G2, G0, G1, gi + 2);
+        // fp32 energy blocks of at most 60 steps (15 groups, a whole number of rotations)
+        for (int c0 = 0; c0 < ng; c0 += 15) {
+            const int c1 = ng < c0 + 15 ? ng : c0 + 15;
+            for (int gi = c0; gi < c1; gi += 3) {
+                stage(G0, G1, G2, gi);
+                if (gi + 1 >= c1) break;
+                stage(G1, G2, G0, gi + 1);
+                if (gi + 2 >= c1) break;
+                stage(G2, G0, G1, gi + 2);
+            }
+            ed += static_cast<double>(eb);
+            eb = 0.f;
         }
-        ed += static_cast<double>(eb);
         // (after the last window: a copy of it into the idle buffer, which nothing reads)
         win_store_full<NT8>(plan, buf ? plan.dst0 : plan.dst1, lds, &badbits, addf, hib, cm);
         lds_barrier();
