@@ -54,18 +54,12 @@ __device__ __forceinline__ void emo_wave_min_key(unsigned long long *key, float 
 
 // Stage 1 for the workgroup's current group of EMO_BLOCK consecutive candidates (group index
 // `group`, candidates group * EMO_BLOCK + threadIdx.x).  Must be called by every thread of the
-// workgroup.  `part` (one record per group) and `mask` may be NULL.  The per-wave values go to
-// one of two LDS slots by the group's parity: a workgroup that walks several groups may start
-// writing the next group's values while thread 0 still reads this group's, and the barrier of
-// the next group orders them before the slot is used again.
+// workgroup.  `part` (one record per group) and `mask` may be NULL.
 __device__ void emo_select_block(long long group, bool active, float T, float E, long long c,
                                  long long B, float target, unsigned int *mask, EmoPartial *part) {
-    __shared__ unsigned long long s_key2[2][EMO_WAVES_PER_BLOCK];
-    __shared__ float s_T2[2][EMO_WAVES_PER_BLOCK];
-    __shared__ unsigned int s_cnt2[2][EMO_WAVES_PER_BLOCK];
-    unsigned long long *s_key = s_key2[group & 1];
-    float *s_T = s_T2[group & 1];
-    unsigned int *s_cnt = s_cnt2[group & 1];
+    __shared__ unsigned long long s_key[EMO_WAVES_PER_BLOCK];
+    __shared__ float s_T[EMO_WAVES_PER_BLOCK];
+    __shared__ unsigned int s_cnt[EMO_WAVES_PER_BLOCK];
     const bool feas = active && (T <= target);   // false for NaN
     const unsigned long long bal = __ballot(feas);
     const int lane = threadIdx.x % EMO_WAVE;
@@ -131,5 +125,8 @@ __device__ void emo_select_all(long long group, bool active, float T, float E, l
         emo_select_block(group, active, T, E, c, B, tg.t[k], tg.mask[k],
                          tg.part ? tg.part + k * tg.nparts : (EmoPartial *)0);
     }
+    // thread 0 has read the last target's per-wave values before any wave of this workgroup
+    // goes on (a workgroup that walks several groups writes them again for the next group)
+    if (tg.part) __syncthreads();
 }
 
