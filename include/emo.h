@@ -22,8 +22,11 @@
  *   feasible= T <= latency_target
  *   selected= the feasible candidate of least E, the lower index on equal E; -1 if none.
  *
- * Arithmetic is IEEE fp32 with round-to-nearest-even for times; the pack-energy sum is
- * accumulated in fp32 blocks of at most 64 packs added into an fp64 total, then rounded to fp32.
+ * Arithmetic is IEEE fp32 with round-to-nearest-even for times, in the order of the recurrence
+ * above, except that the cut-segment kernels time the nodes between two cut nodes from the
+ * earlier cut and add the segments' spans (the same values whenever every time sum is exact,
+ * emo_graph_info.exact_time_sums); the pack-energy sum is accumulated in fp32 blocks of at
+ * most 64 packs added into an fp64 total, then rounded to fp32.
  *
  * Units are the caller's (the tests use microseconds and power units with energy =
  * power * time).  Level F-1 is conventionally the maximum frequency; nothing here depends on it.
@@ -130,22 +133,22 @@ typedef struct {
                                      finish time of the cut before them, the finish times and
                                      slack of the nodes between two cuts depend on those
                                      nodes' levels only (Eq. 1; slack as in Sec. III-A:
-                                     time off the critical path).  The kernels cut the graph there, in segments of
-                                     at most 256 packs, when packs are visited in increasing
-                                     id, segments start at multiples of 32 packs, and every
-                                     time value is a multiple of one power of two u with the
-                                     sum of all nodes' largest durations below 2^24 u (every
-                                     sum is then exact in fp32 in any order).  Batch calls of
-                                     graphs too large for one specialised kernel use them
-                                     when levels (and slack) are 16-byte aligned and fewer
-                                     than 2^30 candidates are evaluated. */
+                                     time off the critical path).  The kernels cut the graph
+                                     there, in segments of at most 256 packs, when packs are
+                                     visited in increasing id and segments start at multiples
+                                     of 32 packs.  Batch calls of graphs too large for one
+                                     specialised kernel use them when levels (and slack) are
+                                     16-byte aligned and fewer than 2^30 candidates are
+                                     evaluated.  They time each segment from its own start, so
+                                     their results are those of the other kernels bit for bit
+                                     when exact_time_sums is 1, and agree with them to fp32
+                                     rounding otherwise. */
     int32_t chain_scan_window;    /* packs per window of the two-pass chain scan kernels
                                      (last_kernels 6 and 8), 0 when it does not apply: the
                                      candidate-dependent nodes must form at most 16 disjoint
                                      chains visiting the windows in increasing order, P a
-                                     multiple of 16, and every time sum exact as for
-                                     cut_segments; calls use it when levels and slack are
-                                     16-byte aligned */
+                                     multiple of 16, and exact_time_sums 1; calls use it when
+                                     levels and slack are 16-byte aligned */
     int32_t chain_scan_full;      /* 1 when slack calls of the two-pass chain scan run the
                                      kernel with per-thread copy plans (last_kernels 8): every
                                      window lies wholly inside the graph (P a multiple of
@@ -158,6 +161,13 @@ typedef struct {
                                      of the specialised kernels is the hiprtc of that same
                                      runtime, so this also names the compiler that builds
                                      them. */
+    int32_t exact_time_sums;      /* 1 when every time value (table times, fixed durations) is
+                                     a multiple of one power of two u and the sum of all
+                                     nodes' largest durations is below 2^24 u: every sum and
+                                     difference of times along paths is then exact in fp32 in
+                                     any order, and every kernel kind computes bit-identical
+                                     makespans and slack.  0 otherwise: the cut-segment
+                                     kernels then agree with the others to rounding. */
 } emo_graph_info;
 
 /* Which kernels evaluate a graph.
@@ -167,7 +177,8 @@ typedef struct {
  *   EMO_KERNELS_INTERPRETED  always the precompiled kernels that interpret a compiled program.
  *   EMO_KERNELS_SPECIALIZED  like AUTO, but a failed specialisation is reported as
  *                            EMO_ERR_DEVICE by the batch call instead of falling back.
- * Both kinds compute bit-identical results. */
+ * Both kinds compute bit-identical results, except that the cut-segment kernels round
+ * differently on graphs whose time sums are not exact (emo_graph_info.exact_time_sums 0). */
 typedef enum {
     EMO_KERNELS_AUTO = 0,
     EMO_KERNELS_INTERPRETED = 1,

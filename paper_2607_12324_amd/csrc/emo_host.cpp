@@ -1222,8 +1222,11 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     g->chain_eval = narrow && nops > kJitMaxOps && nops <= kChainMaxOps;
     g->chain_slack = narrow && nops > kJitMaxSlackOps && nops <= kChainMaxOps;
     g->cut_plan = emo::jit_cut_plan(g->jg, cut_steps(*g, sf), kCutMaxPacks, kCutSubPacks);
-    g->cut_ok = g->cut_plan.segments() >= 2 && nops <= kChainMaxOps && exact_sums;
+    // (off the exact-sum grid the segment-local times round differently from the program order
+    // of the other kinds: results agree with them to rounding, not bit for bit)
+    g->cut_ok = g->cut_plan.segments() >= 2 && nops <= kChainMaxOps;
     in.cut_segments = g->cut_ok ? g->cut_plan.segments() : 0;
+    in.exact_time_sums = exact_sums ? 1 : 0;
     int rt = 0;
     in.hip_runtime_version = hipRuntimeGetVersion(&rt) == hipSuccess ? rt : 0;
 

@@ -49,7 +49,8 @@ class GraphInfo(ctypes.Structure):
                 ("last_kernels", ctypes.c_int32), ("chain_lanes", ctypes.c_int32),
                 ("num_implied_edges", ctypes.c_int32), ("chain_window", ctypes.c_int32),
                 ("cut_segments", ctypes.c_int32), ("chain_scan_window", ctypes.c_int32),
-                ("chain_scan_full", ctypes.c_int32), ("hip_runtime_version", ctypes.c_int32)]
+                ("chain_scan_full", ctypes.c_int32), ("hip_runtime_version", ctypes.c_int32),
+                ("exact_time_sums", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

@@ -260,7 +260,9 @@ def test_cut_segments(emo):
     segment, ends after a multiple of 32 packs, packs visited in increasing id."""
     expect = {1: 0, 2: 0, 3: 0, 4: 16, 5: 0}
     for k, m in expect.items():
-        assert _load(emo, synth.config_graph(k)).info()["cut_segments"] == m, k
+        info = _load(emo, synth.config_graph(k)).info()
+        # every workload's times lie on the 2^-4 us grid with small enough sums
+        assert info["cut_segments"] == m and info["exact_time_sums"] == 1, k
     for (P, S, F, se), m in (((1024, 8, 16, 256), 4), ((2048, 4, 8, 128), 8), ((1056, 8, 16, 256), 5),
                              ((960, 6, 5, 96), 5), ((1024, 4, 32, 128), 8), ((1024, 4, 32, 256), 0),
                              ((1000, 4, 16, 100), 0), ((1024, 4, 200, 128), 0), ((2048, 8, 16, 64), 8)):
@@ -268,13 +270,18 @@ def test_cut_segments(emo):
         assert _load(emo, g).info()["cut_segments"] == m, (P, S, F, se)
     g = synth.packed_graph(11, 1024, 8, 16, sync_every=256, cross_p=0.05, shuffle_pack_ids=True)
     assert _load(emo, g).info()["cut_segments"] == 0
-    # times off a common dyadic grid with a sum of largest durations of 2^24 grid units or more
+    # the segments do not depend on the times; whether every time sum is exact does: times off a
+    # common dyadic grid with a sum of largest durations of 2^24 grid units or more are not
     g = synth.packed_graph(11, 1024, 8, 16, sync_every=256, cross_p=0.05)
-    assert _load(emo, _mod(g, pack_time=(g.pack_time * 64.0).astype(np.float32))).info()["cut_segments"] == 0
+    info = _load(emo, g).info()
+    assert info["cut_segments"] == 4 and info["exact_time_sums"] == 1
+    for scale in (64.0, 8.0, 1.1):
+        info = _load(emo, _mod(g, pack_time=(g.pack_time * scale).astype(np.float32))).info()
+        assert info["cut_segments"] == 4 and info["exact_time_sums"] == (scale == 8.0), scale
     t = g.pack_time.copy()
     t[5, 3] += np.float32(2.0 ** -12)   # grid 2^-12: the sum bound becomes 4096 us
-    assert _load(emo, _mod(g, pack_time=t)).info()["cut_segments"] == 0
-    assert _load(emo, _mod(g, pack_time=(g.pack_time * 8.0).astype(np.float32))).info()["cut_segments"] == 4
+    info = _load(emo, _mod(g, pack_time=t)).info()
+    assert info["cut_segments"] == 4 and info["exact_time_sums"] == 0
 
 
 @pytest.mark.parametrize("seed", range(4))

@@ -309,6 +309,59 @@ def test_cut_segment_kernels(torch, emo, case):
         assert np.array_equal(host(a).view(np.uint32), host(b).view(np.uint32)), case
 
 
+@pytest.mark.parametrize("case", ["sync-256-F16", "sync-96-F5", "host-source"])
+def test_cut_segments_off_grid(torch, emo, case):
+    """Times off the exact-sum grid (every table time scaled by 1.1): the cut-segment kernels still
+    apply, timing each segment from its start, so they round differently from the program
+    order.  Makespan, energy and every slack element against the oracle within 1e-5 of the
+    makespan, every mask bit whose candidate's makespan is not within that bound of the target,
+    the selection, and the interpreted kernels to the same bound."""
+    P, S_, F, se, m = CUT_CASES[case]
+    g = synth.packed_graph(P + F + se, P, S_, F, sync_every=se, cross_p=0.05)
+    if case == "host-source":
+        g = with_host_source(g)
+    g = dataclasses.replace(g, name=g.name + "-x1.1", pack_time=(g.pack_time * np.float32(1.1)).astype(np.float32))
+    rng = np.random.default_rng(P + se + 1)
+    rows = pins.random_rows(rng, g, 1000 - 23)
+    rows[7, P // 2] = F
+    rows[300, -1] = 255
+    print(f"[case] cut segments off the grid {case}: V={g.num_nodes} P={P} B={len(rows)}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    info = gh.info()
+    assert info["cut_segments"] == m and info["exact_time_sums"] == 0, info
+    lv = dev(torch, rows)
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    ok = ~np.isnan(T_or)
+    tgt = float(np.float32(np.median(T_or[ok])))
+    B = len(rows)
+    T = torch.empty(B, dtype=torch.float32, device="cuda")
+    E = torch.empty_like(T)
+    S = torch.empty((B, P), dtype=torch.float32, device="cuda")
+    mk = torch.empty((B + 31) // 32, dtype=torch.int32, device="cuda")
+    r = torch.empty(3, dtype=torch.int64, device="cuda")
+    gh.evaluate(lv, makespan=T, energy=E, slack=S, latency_target=tgt, mask=mk, result=r)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == 5
+    parity.assert_eval(host(T), host(E), T_or, E_or, False, case)
+    Sh = host(S)
+    assert np.all(np.isnan(Sh[~ok]))
+    S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in np.nonzero(ok)[0]])
+    parity.assert_slack(Sh[ok], S_or, T_or[ok], False, case + " pack slack")
+    bits = emo.unpack_mask(mk, B)
+    _, feas_or, _ = oracle.select(T_or, E_or, tgt)
+    clear = ~ok | (np.abs(T_or - tgt) > parity.REL * np.abs(T_or))
+    assert np.array_equal(bits[clear], feas_or[clear]), case + " mask"
+    parity.assert_selection(emo.parse_selection(r), bits, T_or, E_or, tgt, False, case + " select")
+    run_all(torch, emo, g, rows, [tgt], exact=False, per_node=False, what="cut off the grid " + case)
+    gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+    Ti, Ei = gi.eval_policies(lv)
+    Si = gi.slack(lv)
+    torch.cuda.synchronize()
+    parity.assert_eval(host(T), host(E), host(Ti).astype(np.float64), host(Ei).astype(np.float64), False,
+                       case + " vs interpreted")
+    parity.assert_slack(Sh[ok], host(Si)[ok], T_or[ok], False, case + " slack vs interpreted")
+
+
 def test_cut_segments_small_batches(torch, emo):
     """Cut-segment kernels with batches smaller than a workgroup and one past it (lanes past the
     batch repeat the last row and store nothing), repeated calls bit for bit."""
