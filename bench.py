@@ -477,6 +477,8 @@ def main():
                          "(65,536 kernels) as the headline and the others under 'configs'")
     ap.add_argument("--copies", type=int, default=5, help="rotated copies of the level batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the 4096-pack graph's off-grid and no-cut variants (default run)")
     ap.add_argument("--time-every", type=int, default=8,
                     help="time the main launch with a HIP event pair on every N-th timed step "
                          "(an event record costs a few microseconds of device time; default 8)")
@@ -540,6 +542,16 @@ def main():
         recs[k] = run_workload(k, args, emo, synth, np, torch)
         print(f"# workload {k} done: {recs[k]['ms_per_step']:.4f} ms/step, "
               f"{recs[k]['value']:.4g} policies/s", file=sys.stderr, flush=True)
+    # the 4096-pack workload's graph off the exact-sum time grid (cut-segment kernels, segment-
+    # local rounding) and without cut nodes (segmented kernels): the same step and batch
+    variants = {}
+    if args.workload == 0 and not args.no_variants:
+        g4 = synth.config_graph(4)
+        for gv in (synth.scaled_times(g4, 1.1), synth.without_cuts(g4)):
+            r = run_workload(4, args, emo, synth, np, torch, graph=gv, cpu_budget_s=3.0)
+            print(f"# variant {gv.name} done: {r['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
+            variants[gv.name] = {x: r.get(x) for x in ("value", "ms_per_step", "config", "roofline", "kernels",
+                                                       "parity", "compile_seconds", "selected")}
     h = recs[head]
     out = {
         "metric": METRIC,
@@ -564,16 +576,19 @@ def main():
         "kernel_source_hash": h["kernel_source_hash"],
         "configs": {synth.CONFIGS[k].name: {x: v for x, v in recs[k].items() if x != "config"} |
                     {"config": recs[k]["config"]} for k in ks if k != head},
+        "variants": variants,
         "wall_s": time.perf_counter() - t_all,
     }
     print(json.dumps(out), flush=True)
 
 
-def run_workload(k, args, emo, synth, np, torch):
+def run_workload(k, args, emo, synth, np, torch, graph=None, cpu_budget_s=20.0):
     """One workload's step timed over args.steps steps (after args.warmup), its roofline, and,
-    unless disabled, the oracle baseline with parity statistics.  Frees its device memory."""
+    unless disabled, the oracle baseline with parity statistics.  Frees its device memory.
+    `graph`: a variant of the workload's graph (same packs and levels) to run instead; its
+    traffic is not looked up (the committed counters are the workload's own graph's)."""
     spec = synth.CONFIGS[k]
-    g = synth.config_graph(k)
+    g = synth.config_graph(k) if graph is None else graph
     B = spec.num_candidates
     P = g.num_packs
     torch.cuda.set_device(0)
@@ -660,11 +675,11 @@ def run_workload(k, args, emo, synth, np, torch):
     valu_tops = B * ops_per_cand / (main_ms / 1e3) / 1e12
     src_hash = kernel_source_hash(info["last_kernels"])
     kname = kernel_name(info["last_kernels"], spec.slack)
-    traffic = measured_traffic(spec.name, kname, src_hash)
+    traffic = measured_traffic(spec.name, kname, src_hash) if graph is None else None
     rec = {
         "value": value,
         "ms_per_step": ms_step,
-        "config": {"workload": spec.name, "candidates": B, "nodes": g.num_nodes,
+        "config": {"workload": g.name, "candidates": B, "nodes": g.num_nodes,
                    "edges": g.num_edges, "packs": P, "levels": g.num_levels,
                    "target_ratios": list(spec.targets), "slack": spec.slack,
                    "step": "emo_evaluate" if len(targets) == 1 else f"emo_evaluate_targets ({len(targets)} targets)",
@@ -690,7 +705,7 @@ def run_workload(k, args, emo, synth, np, torch):
     }
     if not args.no_cpu_baseline:
         out = {"T": T, "E": E, "S": S, "masks": masks, "results": results}
-        rec["cpu_baseline"], rec["parity"] = cpu_baseline(k, g, rows, out, targets)
+        rec["cpu_baseline"], rec["parity"] = cpu_baseline(k, g, rows, out, targets, budget_s=cpu_budget_s)
     del lv, S, T, E, rows
     gh.close()
     torch.cuda.synchronize()

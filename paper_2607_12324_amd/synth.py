@@ -329,6 +329,28 @@ def config_graph(k: int) -> Graph:
     raise ValueError(f"unknown config {k}")
 
 
+def without_cuts(g: Graph) -> Graph:
+    """The same graph plus a zero-duration source node into the node of the last pack: no node
+    before that pack is a cut node any more (the new node is neither before nor after it)."""
+    v = int(np.nonzero(g.node_pack == g.num_packs - 1)[0][0])
+    V = g.num_nodes
+    return dataclasses.replace(
+        g, name=g.name + "-nocut", num_nodes=V + 1,
+        edge_src=np.append(g.edge_src, np.int32(V)).astype(np.int32),
+        edge_dst=np.append(g.edge_dst, np.int32(v)).astype(np.int32),
+        node_pack=np.append(g.node_pack, np.int32(-1)).astype(np.int32),
+        node_duration=np.append(g.node_duration, np.float32(0)).astype(np.float32),
+        node_stream=None if g.node_stream is None else np.append(g.node_stream, np.int32(-1)).astype(np.int32))
+
+
+def scaled_times(g: Graph, factor: float) -> Graph:
+    """The same graph with every table time multiplied by `factor` (rounded to fp32): 1.1 takes
+    the times off any common power-of-two grid, as durations measured in integer nanoseconds
+    are."""
+    return dataclasses.replace(g, name=f"{g.name}-t{factor:g}",
+                               pack_time=(g.pack_time * np.float32(factor)).astype(np.float32))
+
+
 # ----------------------------------------------------------------------------- policies
 
 def exhaustive_policies(num_packs: int, num_levels: int, start: int, count: int) -> np.ndarray:

@@ -154,18 +154,9 @@ def test_interpreter_table_windows(torch, emo, F, P):
 
 
 def without_cuts(g):
-    """The same graph plus a zero-duration source node into the node of the last pack: no node
-    before that pack is a cut any more (the new node is neither before nor after it), so the
-    cut-segment kernels do not apply."""
-    v = int(np.nonzero(g.node_pack == g.num_packs - 1)[0][0])
-    V = g.num_nodes
-    return dataclasses.replace(
-        g, name=g.name + "-nocut", num_nodes=V + 1,
-        edge_src=np.append(g.edge_src, np.int32(V)).astype(np.int32),
-        edge_dst=np.append(g.edge_dst, np.int32(v)).astype(np.int32),
-        node_pack=np.append(g.node_pack, np.int32(-1)).astype(np.int32),
-        node_duration=np.append(g.node_duration, np.float32(0)).astype(np.float32),
-        node_stream=None if g.node_stream is None else np.append(g.node_stream, np.int32(-1)).astype(np.int32))
+    """The same graph without cut nodes (a zero-duration source into the last pack's node), so
+    that the cut-segment kernels do not apply."""
+    return synth.without_cuts(g)
 
 
 def with_host_source(g, dur=7.5):
@@ -320,7 +311,7 @@ def test_cut_segments_off_grid(torch, emo, case):
     g = synth.packed_graph(P + F + se, P, S_, F, sync_every=se, cross_p=0.05)
     if case == "host-source":
         g = with_host_source(g)
-    g = dataclasses.replace(g, name=g.name + "-x1.1", pack_time=(g.pack_time * np.float32(1.1)).astype(np.float32))
+    g = synth.scaled_times(g, 1.1)
     rng = np.random.default_rng(P + se + 1)
     rows = pins.random_rows(rng, g, 1000 - 23)
     rows[7, P // 2] = F
