@@ -478,7 +478,8 @@ def main():
     ap.add_argument("--copies", type=int, default=5, help="rotated copies of the level batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",
-                    help="skip the 4096-pack graph's off-grid and no-cut variants (default run)")
+                    help="skip the graph variants of the default run (4096-pack graph off the time "
+                         "grid and without cut nodes, 65,536-kernel graph off the grid)")
     ap.add_argument("--time-every", type=int, default=8,
                     help="time the main launch with a HIP event pair on every N-th timed step "
                          "(an event record costs a few microseconds of device time; default 8)")
@@ -543,12 +544,14 @@ def main():
         print(f"# workload {k} done: {recs[k]['ms_per_step']:.4f} ms/step, "
               f"{recs[k]['value']:.4g} policies/s", file=sys.stderr, flush=True)
     # the 4096-pack workload's graph off the exact-sum time grid (cut-segment kernels, segment-
-    # local rounding) and without cut nodes (segmented kernels): the same step and batch
+    # local rounding) and without cut nodes (segmented kernels), and the 65,536-kernel graph off
+    # the grid (chain scan, prefix-sum rounding): the same steps and batches
     variants = {}
     if args.workload == 0 and not args.no_variants:
-        g4 = synth.config_graph(4)
-        for gv in (synth.scaled_times(g4, 1.1), synth.without_cuts(g4)):
-            r = run_workload(4, args, emo, synth, np, torch, graph=gv, cpu_budget_s=3.0)
+        g4, g5 = synth.config_graph(4), synth.config_graph(5)
+        for k, gv in ((4, synth.scaled_times(g4, 1.1)), (4, synth.without_cuts(g4)),
+                      (5, synth.scaled_times(g5, 1.1))):
+            r = run_workload(k, args, emo, synth, np, torch, graph=gv, cpu_budget_s=3.0)
             print(f"# variant {gv.name} done: {r['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
             variants[gv.name] = {x: r.get(x) for x in ("value", "ms_per_step", "config", "roofline", "kernels",
                                                        "parity", "compile_seconds", "selected")}

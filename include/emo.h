@@ -24,9 +24,11 @@
  *
  * Arithmetic is IEEE fp32 with round-to-nearest-even for times, in the order of the recurrence
  * above, except that the cut-segment kernels time the nodes between two cut nodes from the
- * earlier cut and add the segments' spans (the same values whenever every time sum is exact,
- * emo_graph_info.exact_time_sums); the pack-energy sum is accumulated in fp32 blocks of at
- * most 64 packs added into an fp64 total, then rounded to fp32.
+ * earlier cut and add the segments' spans, and the chain scan kernels (last_kernels 6 and 8)
+ * take slack from prefix sums of durations along each chain instead of the backward recurrence
+ * (the same values whenever every time sum is exact, emo_graph_info.exact_time_sums); the
+ * pack-energy sum is accumulated in fp32 blocks of at most 64 packs added into an fp64 total,
+ * then rounded to fp32.
  *
  * Units are the caller's (the tests use microseconds and power units with energy =
  * power * time).  Level F-1 is conventionally the maximum frequency; nothing here depends on it.
@@ -107,11 +109,12 @@ typedef struct {
                                      specialised kernel, 2 segmented specialised kernels,
                                      3 chain lanes (one lane per chain and candidate),
                                      4 windowed chain lanes (a wave per chain, 64 candidates;
-                                     pack windows staged in LDS), 5 cut segments (the
+                                     pack windows staged in LDS; calls without slack), 5 cut
+                                     segments (the
                                      segments between cut nodes evaluated in parallel),
                                      6 two-pass chain scan (windowed chain lanes whose slack
-                                     comes from a second forward pass, for chains with exact
-                                     time sums; only calls with slack), 7 time-interval kernel
+                                     comes from a second forward pass; calls with slack), 7
+                                     time-interval kernel
                                      specialised to the graph (emo_eval_intervals; 0 there
                                      means the interpreting kernel), 8 two-pass chain scan
                                      whose window copies and slack stores follow per-thread
@@ -146,9 +149,9 @@ typedef struct {
     int32_t chain_scan_window;    /* packs per window of the two-pass chain scan kernels
                                      (last_kernels 6 and 8), 0 when it does not apply: the
                                      candidate-dependent nodes must form at most 16 disjoint
-                                     chains visiting the windows in increasing order, P a
-                                     multiple of 16, and exact_time_sums 1; calls use it when
-                                     levels and slack are 16-byte aligned */
+                                     chains visiting the windows in increasing order and P a
+                                     multiple of 16 (the windowed layout); calls with slack use
+                                     it when levels and slack are 16-byte aligned */
     int32_t chain_scan_full;      /* 1 when slack calls of the two-pass chain scan run the
                                      kernel with per-thread copy plans (last_kernels 8): every
                                      window lies wholly inside the graph (P a multiple of
@@ -166,8 +169,9 @@ typedef struct {
                                      nodes' largest durations is below 2^24 u: every sum and
                                      difference of times along paths is then exact in fp32 in
                                      any order, and every kernel kind computes bit-identical
-                                     makespans and slack.  0 otherwise: the cut-segment
-                                     kernels then agree with the others to rounding. */
+                                     makespans and slack.  0 otherwise: the cut-segment and
+                                     chain scan kernels then agree with the others to
+                                     rounding. */
 } emo_graph_info;
 
 /* Which kernels evaluate a graph.
@@ -177,8 +181,9 @@ typedef struct {
  *   EMO_KERNELS_INTERPRETED  always the precompiled kernels that interpret a compiled program.
  *   EMO_KERNELS_SPECIALIZED  like AUTO, but a failed specialisation is reported as
  *                            EMO_ERR_DEVICE by the batch call instead of falling back.
- * Both kinds compute bit-identical results, except that the cut-segment kernels round
- * differently on graphs whose time sums are not exact (emo_graph_info.exact_time_sums 0). */
+ * Both kinds compute bit-identical results, except that the cut-segment and chain scan kernels
+ * round differently on graphs whose time sums are not exact (emo_graph_info.exact_time_sums
+ * 0). */
 typedef enum {
     EMO_KERNELS_AUTO = 0,
     EMO_KERNELS_INTERPRETED = 1,

@@ -361,13 +361,12 @@ gather_slack(const float *__restrict__ tmp, const int32_t *__restrict__ pos, int
 // workgroup is G groups of 64 candidates x nc chains.  Per window the workgroup copies into
 // LDS, with 16-byte loads issued two windows ahead into registers:
 //   - the G*64 candidates' level bytes of the window (checked against F on the way),
-//   - the window's table rows (time and energy; times only in the backward pass),
+//   - the window's table rows (time and energy; times only in the second pass),
 //   - the window's step block: where each chain's steps start, and the step records.
 // Each wave then walks its chain's steps inside the window (the count varies per chain; waves
-// meet at the window's barrier).  The backward pass recomputes the window's finish times from
-// the checkpoint taken at the window's start into an LDS tile [candidate][column], turns them
-// into slack in place while walking the steps in reverse, and the workgroup writes the tile out
-// in pack order with 16-byte stores.
+// meet at the window's barrier).  Slack comes from a second pass over the windows (below), which
+// writes each step's slack into an LDS tile [candidate][column] that the workgroup writes out in
+// pack order with 16-byte stores.
 //
 // Column W of every level row is 0 and row W of the table is zero, so a fixed node (column W)
 // reads a zero time and energy and adds its own duration; its tile entry is column W's pad.
@@ -435,11 +434,6 @@ __device__ __forceinline__ float fmax_nonneg(float a, float b) {
     return __uint_as_float(x > y ? x : y);
 }
 
-// min of two non-negative finite floats (their bit patterns order like unsigned integers)
-__device__ __forceinline__ float fmin_nonneg(float a, float b) {
-    const unsigned x = __float_as_uint(a), y = __float_as_uint(b);
-    return __uint_as_float(x < y ? x : y);
-}
 
 struct WinArgs {
     int W, wlog, nc, NC, F;
@@ -461,12 +455,10 @@ __host__ __device__ inline bool win_slots(int W, int NC, int F, int blk_bytes, i
 // One window's copy in flight: the thread's pieces (16 bytes each), slot by slot: the first
 // slots hold level rows, the next table rows, the next the step block (how many of each is the
 // same for every thread, so the category of a slot is uniform); which of them read as zero
-// (level columns past P, table rows past the last pack, pieces past the end); and the wave's
-// checkpoint (backward pass).
+// (level columns past P, table rows past the last pack, pieces past the end).
 struct WinSet {
     uint4 v[kWinPre];
     uint32_t zero;
-    float ck;
 };
 
 // Issues exactly kWinPre loads for window w (a piece past the end reads a valid address and is
@@ -798,22 +790,24 @@ struct WinGroup {
     }
 };
 
-// SCAN (graphs whose time sums are exact: every time a multiple of one power of two u and every
-// path below 2^24 u, so every sum and difference below is exact in fp32 in any order): slack
-// comes from a second forward pass instead of the backward one.  Along a chain with durations
+// Slack (the two-pass scan) comes from a second forward pass instead of a backward one.  Along
+// a chain with durations
 // d_j and start floors cst_j, a step's only successor is the next step, so its latest finish is
 // the makespan minus the durations after it; with Pre_i = d_1 + ... + d_i and Tot = Pre_n,
 //   slack_i = LFT_i - EFT_i = (T - Tot) - (EFT_i - Pre_i),
 // and D_i = EFT_i - Pre_i obeys D_i = max(D_{i-1}, cst_i - Pre_{i-1}), D_0 = 0, because
-// EFT_i = max(EFT_{i-1}, cst_i) + d_i.  With K = T - Tot, Q_i = K + Pre_i and Z_i = K - D_i:
-//   slack_i = Z_i = min(Z_{i-1}, Q_{i-1} - cst_i),  Q_i = Q_{i-1} + d_i,  Z_0 = Q_0 = K.
-// The forward pass also sums Tot per chain; the second pass walks the windows again for Z and
-// writes it through the slack tile.  No finish time is checkpointed or recomputed backwards.
-template <bool SLACK, bool FIXED, bool SCAN>
+// EFT_i = max(EFT_{i-1}, cst_i) + d_i.  The forward pass also sums Tot per chain; the second pass
+// walks the windows again, sums Pre in the same order, carries D and writes K - D (K = T - Tot)
+// through the slack tile.  No finish time is checkpointed or recomputed backwards.  Pre stays
+// below the chain's total time, so off the exact-sum grid its rounding is that of sums of that
+// size, and every other value takes one rounding: slack agrees with the backward recurrence to
+// rounding, and bit for bit when every time sum is exact (every time a multiple of one power of
+// two u and every path below 2^24 u, so every sum and difference is exact in fp32 in any order).
+template <bool SLACK, bool FIXED>
 __global__ void __launch_bounds__(kChainBlockThreads)
 chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ blocks,
                 const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ To,
-                float *__restrict__ Eo, float *__restrict__ S, float *__restrict__ ck, int64_t pitch) {
+                float *__restrict__ Eo, float *__restrict__ S) {
     extern __shared__ float4 smem[];
     char *lds = reinterpret_cast<char *>(smem);
     const int t = threadIdx.x, nt = blockDim.x;
@@ -822,7 +816,7 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     const int lane = t & 63;
     const int cl = grp * 64 + lane;                               // candidate within the workgroup
     const int64_t base = static_cast<int64_t>(blockIdx.x) * a.NC;
-    const int64_t gc = base + cl;                                 // checkpoint column
+    const int64_t gc = base + cl;                                 // the candidate
     const int W = a.W, F = a.F, nc = a.nc, nwin = c.nwin;
     const int32_t P = g.P;
     const WinLayout &L = a.L;
@@ -859,7 +853,6 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     auto forward_window = [&](int w, WinSet &ld, WinSet &cm) {
         const int buf = w & 1;
         win_load(a, levels, g.tab, 8, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
-        if (SLACK && !SCAN) ck[(static_cast<int64_t>(w) * nc + ch) * pitch + gc] = f;
         const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
         const char *tb = reinterpret_cast<const char *>(tab2 + buf * L.tab_elems);
         const ChainWinStep *rs = recs(buf);
@@ -882,7 +875,7 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
                 f = fmax_nonneg(f, A.cst[i]) + te[i].x;
                 if (FIXED) f += A.dur[i];
                 eb += te[i].y;
-                if (SLACK && SCAN) {
+                if (SLACK) {
                     pre += te[i].x;
                     if (FIXED) pre += A.dur[i];
                 }
@@ -958,8 +951,8 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
             }
             const float *src = tile + r * (W + 1) + 4 * kk;
             float4 v = make_float4(src[0], src[1], src[2], src[3]);
-            if (SCAN && tfin[r] != tfin[r]) v = make_float4(__builtin_nanf(""), __builtin_nanf(""),
-                                                           __builtin_nanf(""), __builtin_nanf(""));
+            if (tfin[r] != tfin[r]) v = make_float4(__builtin_nanf(""), __builtin_nanf(""),
+                                                   __builtin_nanf(""), __builtin_nanf(""));
             const int64_t row = base + r;
             const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 4 * kk;
             if (row < B && col < P) *reinterpret_cast<float4 *>(S + row * P + col) = v;
@@ -970,179 +963,68 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
         tabt[L.tab_elems + W * F + i] = 0.f;
     }
 
-    if (SCAN) {
-        // ---------------------------------------------------------------- second forward pass
-        // slack_i = K - D_i with K = T - Tot; carried as Q = K + Pre and Z = K - D:
-        //   Z_i = min(Z_{i-1}, Q_{i-1} - cst_i),  Q_i = Q_{i-1} + d_i,  Z_0 = Q_0 = K
-        // (a candidate with a bad level, K = NaN, gets its NaN row from the flush instead)
-        const float Kc = tfin[cl] - pre;
-        const float K = Kc == Kc ? Kc : 0.f;
-        float Z = K, Q = K;
-        win_load(a, levels, g.tabt, 4, blocks, base, B, P, 0, s0);
-        win_load(a, levels, g.tabt, 4, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
-        win_store(a, lds, 0, tabt, 4, nullptr, addf, s0);
-        lds_barrier();
-        float *trow = tile + cl * (W + 1);
-        auto scan_window = [&](int w, WinSet &ld, WinSet &cm) {
-            const int buf = w & 1;
-            win_load(a, levels, g.tabt, 4, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
-            const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
-            const char *tb = reinterpret_cast<const char *>(tabt + buf * L.tab_elems);
-            const ChainWinStep *rs = recs(buf);
-            int k0, k1;
-            win_range(a, lds, buf, ch, k0, k1);
-            const int ng = (k1 - k0) >> 2;
-            // group g of 4 steps, pipelined like the forward pass: its times are read while the
-            // next group's level bytes and the records of the group after it are in flight
-            auto stage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int g) {
-                float tt[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    tt[i] = *reinterpret_cast<const float *>(tb + (((A.ct[i] >> 16) + A.lv[i]) << 2));
-                    if (FIXED) tt[i] += A.dur[i];
-                }
-                Bn.levels(lrow);
-                C.read(rs, k0 + 4 * (g + 2));
-                win_issue_point();
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    // both operands are >= 0: Q_{i-1} - cst_i >= K - D_i = slack_i
-                    Z = fmin_nonneg(Z, Q - A.cst[i]);
-                    Q += tt[i];
-                    trow[A.ct[i] & 0xffffu] = Z;
-                }
-            };
-            WinGroup<FIXED> G0, G1, G2;
-            G0.read(rs, k0);
-            G1.read(rs, k0 + 4);
-            G0.levels(lrow);
-            for (int g = 0; g < ng; g += 3) {
-                stage(G0, G1, G2, g);
-                if (g + 1 >= ng) break;
-                stage(G1, G2, G0, g + 1);
-                if (g + 2 >= ng) break;
-                stage(G2, G0, G1, g + 2);
-            }
-            if (w + 1 < nwin) win_store(a, lds, buf ^ 1, tabt + (buf ^ 1) * L.tab_elems, 4, nullptr, addf, cm);
-            lds_barrier();
-            flush_tile(w);
-            lds_barrier();
-        };
-        for (int w = 0; w < nwin; w += 2) {
-            scan_window(w, s0, s1);
-            if (w + 1 < nwin) scan_window(w + 1, s1, s0);
-        }
-        return;
-    }
-
-    // ------------------------------------------------------------------ backward
-    const int top = nwin - 1;
-    auto ck_at = [&](int w) { return ck[(static_cast<int64_t>(w) * nc + ch) * pitch + gc]; };
-    win_load(a, levels, g.tabt, 4, blocks, base, B, P, top, s0);
-    s0.ck = ck_at(top);
-    win_load(a, levels, g.tabt, 4, blocks, base, B, P, top >= 1 ? top - 1 : 0, s1);
-    s1.ck = ck_at(top >= 1 ? top - 1 : 0);
-    float lft = tfin[cl];                                   // NaN for a candidate with bad levels
-    win_store(a, lds, top & 1, tabt + (top & 1) * L.tab_elems, 4, nullptr, addf, s0);
-    float fck = s0.ck;
+    // ---------------------------------------------------------------- second forward pass
+    // slack_i = K - D_i with K = T - Tot and D_i = max(D_{i-1}, cst_i - Pre_{i-1}), D_0 = 0
+    // (a candidate with a bad level, K = NaN, gets its NaN row from the flush instead)
+    const float Kc = tfin[cl] - pre;
+    const float K = Kc == Kc ? Kc : 0.f;
+    float D = 0.f, Pr = 0.f;
+    win_load(a, levels, g.tabt, 4, blocks, base, B, P, 0, s0);
+    win_load(a, levels, g.tabt, 4, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
+    win_store(a, lds, 0, tabt, 4, nullptr, addf, s0);
     lds_barrier();
-    // the checkpoint is taken where its load has landed: left to its first use in the next
-    // window, the wait would also cover that window's prefetch loads
-    asm volatile("" : "+v"(fck));
     float *trow = tile + cl * (W + 1);
-    // window w from buffer w & 1; `ld` takes window w - 2, `cm` holds window w - 1
-    auto backward_window = [&](int w, WinSet &ld, WinSet &cm) {
+    auto scan_window = [&](int w, WinSet &ld, WinSet &cm) {
         const int buf = w & 1;
-        win_load(a, levels, g.tabt, 4, blocks, base, B, P, w >= 2 ? w - 2 : 0, ld);
-        ld.ck = ck_at(w >= 2 ? w - 2 : 0);
+        win_load(a, levels, g.tabt, 4, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
         const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
         const char *tb = reinterpret_cast<const char *>(tabt + buf * L.tab_elems);
         const ChainWinStep *rs = recs(buf);
         int k0, k1;
         win_range(a, lds, buf, ch, k0, k1);
         const int ng = (k1 - k0) >> 2;
-        auto times = [&](const WinGroup<FIXED> &A, float (&tt)[4]) {
+        // group g of 4 steps, pipelined like the forward pass: its times are read while the
+        // next group's level bytes and the records of the group after it are in flight
+        auto stage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int g) {
+            float tt[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < 4; ++i)
                 tt[i] = *reinterpret_cast<const float *>(tb + (((A.ct[i] >> 16) + A.lv[i]) << 2));
-                if (FIXED) tt[i] += A.dur[i];
-            }
-        };
-        // finish times of the window's steps, from the checkpoint, into the tile; pipelined like
-        // the forward pass
-        float fb = fck;
-        auto fstage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int g) {
-            float tt[4], fi[4];
-            times(A, tt);
             Bn.levels(lrow);
             C.read(rs, k0 + 4 * (g + 2));
             win_issue_point();
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                fb = fmax_nonneg(fb, A.cst[i]) + tt[i];
-                fi[i] = fb;
+                // (Pre summed as the forward pass sums it: table time, then fixed duration)
+                D = fmaxf(D, A.cst[i] - Pr);
+                Pr += tt[i];
+                if (FIXED) Pr += A.dur[i];
+                trow[A.ct[i] & 0xffffu] = K - D;
             }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) trow[A.ct[i] & 0xffffu] = fi[i];
         };
         WinGroup<FIXED> G0, G1, G2;
         G0.read(rs, k0);
         G1.read(rs, k0 + 4);
         G0.levels(lrow);
         for (int g = 0; g < ng; g += 3) {
-            fstage(G0, G1, G2, g);
+            stage(G0, G1, G2, g);
             if (g + 1 >= ng) break;
-            fstage(G1, G2, G0, g + 1);
+            stage(G1, G2, G0, g + 1);
             if (g + 2 >= ng) break;
-            fstage(G2, G0, G1, g + 2);
+            stage(G2, G0, G1, g + 2);
         }
-        // slack = latest finish - finish, walking the groups and their steps in reverse (the
-        // chain's columns are distinct, except the pad column of fixed nodes and no-op steps,
-        // which is never stored): a group's finish times are read before its slack is written
-        auto bstage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int g) {
-            float tt[4], ef[4];
-            times(A, tt);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) ef[i] = trow[A.ct[i] & 0xffffu];
-            Bn.levels(lrow);
-            C.read(rs, k0 + 4 * (g - 2));
-            win_issue_point();
-#pragma unroll
-            for (int i = 3; i >= 0; --i) {
-                ef[i] = lft - ef[i];
-                lft = lft - tt[i];
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) trow[A.ct[i] & 0xffffu] = ef[i];
-        };
-        G0.read(rs, k0 + 4 * (ng - 1));
-        G1.read(rs, k0 + 4 * (ng - 2));
-        G0.levels(lrow);
-        for (int g = ng - 1; g >= 0; g -= 3) {
-            bstage(G0, G1, G2, g);
-            if (g - 1 < 0) break;
-            bstage(G1, G2, G0, g - 1);
-            if (g - 2 < 0) break;
-            bstage(G2, G0, G1, g - 2);
-        }
-        float fnext = 0.f;
-        if (w >= 1) {
-            win_store(a, lds, buf ^ 1, tabt + (buf ^ 1) * L.tab_elems, 4, nullptr, addf, cm);
-            fnext = cm.ck;
-        }
+        if (w + 1 < nwin) win_store(a, lds, buf ^ 1, tabt + (buf ^ 1) * L.tab_elems, 4, nullptr, addf, cm);
         lds_barrier();
         flush_tile(w);
         lds_barrier();
-        asm volatile("" : "+v"(fnext));
-        fck = fnext;
     };
-    for (int w = top; w >= 0; w -= 2) {
-        backward_window(w, s0, s1);
-        if (w >= 1) backward_window(w - 1, s1, s0);
+    for (int w = 0; w < nwin; w += 2) {
+        scan_window(w, s0, s1);
+        if (w + 1 < nwin) scan_window(w + 1, s1, s0);
     }
 }
 
-// The two-pass chain scan (chains_windowed with SCAN) for the layouts where every window lies
+// The two-pass chain scan (chains_windowed with slack) for the layouts where every window lies
 // wholly inside the graph (P a multiple of W) and a thread holds at most four pieces of the slack
 // tile: every window copy and every flush follows a per-thread plan fixed for the kernel, so the
 // per-window work is the loads, the LDS stores, the flush stores and the barriers, with no bounds
@@ -1288,7 +1170,7 @@ chains_scan_full(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ b
     lds_barrier();
 
     // ---------------------------------------------------------------- second forward pass
-    // slack_i = K - D_i with K = T - Tot, carried as Q = K + Pre and Z = K - D (see
+    // slack_i = K - D_i with K = T - Tot and D_i = max(D_{i-1}, cst_i - Pre_{i-1}) (see
     // chains_windowed); a candidate with an invalid level (K = NaN) gets NaN from the flush
     const FlushPlan fp = flush_plan(a, rows_left, P, tfin);
     const __amdgpu_buffer_rsrc_t srows = win_rsrc(S + base * P, static_cast<uint32_t>(nrows * P * 4));
@@ -1301,7 +1183,7 @@ chains_scan_full(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ b
     }
     const float Kc = tfin[cl] - pre;
     const float K = Kc == Kc ? Kc : 0.f;
-    float Z = K, Q = K;
+    float D = 0.f, Pr = 0.f;
     win_load_full<1>(a, plan, bf, 0, s0);
     win_load_full<1>(a, plan, bf, nwin > 1 ? 1 : 0, s1);
     win_store_full<1>(plan, plan.dst0, lds, nullptr, addf, hib, s0);
@@ -1318,19 +1200,17 @@ chains_scan_full(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ b
         auto stage = [&](WinGroup<FIXED> &A, WinGroup<FIXED> &Bn, WinGroup<FIXED> &C, int gi) {
             float tt[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < 4; ++i)
                 tt[i] = *reinterpret_cast<const float *>(tb + (((A.ct[i] >> 16) + A.lv[i]) << 2));
-                if (FIXED) tt[i] += A.dur[i];
-            }
             Bn.levels(lrow);
             C.read(rs, k0 + 4 * (gi + 2));
             win_issue_point();
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                // both operands are >= 0: Q_{i-1} - cst_i >= K - D_i = slack_i
-                Z = fmin_nonneg(Z, Q - A.cst[i]);
-                Q += tt[i];
-                trow[A.ct[i] & 0xffffu] = Z;
+                D = fmaxf(D, A.cst[i] - Pr);
+                Pr += tt[i];
+                if (FIXED) Pr += A.dur[i];
+                trow[A.ct[i] & 0xffffu] = K - D;
             }
         };
         WinGroup<FIXED> G0, G1, G2;
@@ -1383,7 +1263,7 @@ bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int3
 }
 
 bool chains_scan_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
-    return c.exact && slack && chains_windowed_ok(c, levels, slack);
+    return slack && chains_windowed_ok(c, levels, slack);
 }
 
 bool chains_scan_full_ok(const DevChains &c, const uint8_t *levels, const float *slack) {
@@ -1405,12 +1285,8 @@ int64_t win_grid(const DevChains &c, int64_t B) {
 size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t *levels, int64_t B,
                             const float *slack_ptr) {
     const bool slack = slack_ptr != nullptr;
-    if (chains_scan_ok(c, levels, slack_ptr)) return 2 * round256(static_cast<size_t>(B) * sizeof(float));
-    if (chains_windowed_ok(c, levels, slack_ptr)) {
-        const size_t pitch = static_cast<size_t>(win_grid(c, B)) * 64 * c.groups;
-        const size_t ck = slack ? round256(static_cast<size_t>(c.nwin) * c.nc * pitch * sizeof(float)) : 0;
-        return ck + 2 * round256(static_cast<size_t>(B) * sizeof(float));
-    }
+    // windowed layout: the makespan and energy when the caller does not take them
+    if (chains_windowed_ok(c, levels, slack_ptr)) return 2 * round256(static_cast<size_t>(B) * sizeof(float));
     const size_t lanes = static_cast<size_t>(chain_grid(c, B)) * kChainBlockThreads;
     const size_t ck = slack ? round256(static_cast<size_t>(c.len / K) * lanes * sizeof(float)) : 0;
     const size_t tmp = slack && staged_ok(g, c) && g.P % 4 == 0
@@ -1420,10 +1296,10 @@ size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t
 }
 
 namespace {
-template <bool SLACK, bool FIXED, bool SCAN>
+template <bool SLACK, bool FIXED>
 hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, const DevGraph &g,
                                   const DevChains &c, const WinArgs &a, const uint8_t *levels, int64_t B,
-                                  float *T, float *E, float *S, float *ck, int64_t pitch) {
+                                  float *T, float *E, float *S) {
     // the dynamic LDS limit is raised once per device (the caller made the graph's device current)
     static std::atomic<uint64_t> done{0};
     int dev = 0;
@@ -1431,13 +1307,12 @@ hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, c
     if (e != hipSuccess) return e;
     const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
     if (!bit || !(done.load(std::memory_order_acquire) & bit)) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED, SCAN>),
+        e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kWinLds));
         if (e != hipSuccess) return e;
         done.fetch_or(bit, std::memory_order_acq_rel);
     }
-    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED, SCAN>), gd, bd, lds, s, g, c, a, c.blocks, levels, B, T, E,
-                       S, ck, pitch);
+    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED>), gd, bd, lds, s, g, c, a, c.blocks, levels, B, T, E, S);
     return hipGetLastError();
 }
 
@@ -1477,22 +1352,15 @@ hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t 
               &a.slots_blk);
     a.L = win_layout(a.W, a.NC, a.F, c.groups * c.nc, c.blk_bytes);
     const int64_t grid = win_grid(c, B);
-    const int64_t pitch = grid * a.NC;
     char *p = static_cast<char *>(scratch);
-    float *ck = nullptr;
-    const bool scan = c.exact != 0;
-    if (slack && !scan) {
-        ck = reinterpret_cast<float *>(p);
-        p += round256(static_cast<size_t>(c.nwin) * c.nc * pitch * sizeof(float));
-    }
     const size_t vec = round256(static_cast<size_t>(B) * sizeof(float));
     float *Ts = T ? T : reinterpret_cast<float *>(p);
     float *Es = E ? E : reinterpret_cast<float *>(p + vec);
     const dim3 gd(static_cast<unsigned>(grid)), bd(static_cast<unsigned>(64 * c.groups * c.nc));
     const size_t lds = a.L.total;
     hipError_t e;
-#define EMO_WIN_ARGS gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack, ck, pitch
-    if (slack && scan && c.full) {
+#define EMO_WIN_ARGS gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack
+    if (slack && c.full) {
         // one or two 16-byte forward table pieces per thread (c.full guarantees the rest of the
         // slot layout: one level piece, one block piece, one second-pass table piece)
         const bool two = a.slots_tab8 == 2;
@@ -1500,12 +1368,10 @@ hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t 
                            : launch_scan_full_kernel<true, 1>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack))
                     : (two ? launch_scan_full_kernel<false, 2>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack)
                            : launch_scan_full_kernel<false, 1>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack));
-    } else if (slack && scan) e = c.fixed ? launch_windowed_kernel<true, true, true>(EMO_WIN_ARGS)
-                                   : launch_windowed_kernel<true, false, true>(EMO_WIN_ARGS);
-    else if (slack) e = c.fixed ? launch_windowed_kernel<true, true, false>(EMO_WIN_ARGS)
-                                : launch_windowed_kernel<true, false, false>(EMO_WIN_ARGS);
-    else e = c.fixed ? launch_windowed_kernel<false, true, false>(EMO_WIN_ARGS)
-                     : launch_windowed_kernel<false, false, false>(EMO_WIN_ARGS);
+    } else if (slack) e = c.fixed ? launch_windowed_kernel<true, true>(EMO_WIN_ARGS)
+                                  : launch_windowed_kernel<true, false>(EMO_WIN_ARGS);
+    else e = c.fixed ? launch_windowed_kernel<false, true>(EMO_WIN_ARGS)
+                     : launch_windowed_kernel<false, false>(EMO_WIN_ARGS);
 #undef EMO_WIN_ARGS
     if (e == hipSuccess && tg.n) e = launch_select_results(Ts, Es, B, tg, s);
     return e;

@@ -737,7 +737,7 @@ bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
 }
 
 bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::ChainStep> *steps,
-                  std::vector<int32_t> *pos, emo::DevChains *dc, std::vector<uint4> *blocks, bool exact) {
+                  std::vector<int32_t> *pos, emo::DevChains *dc, std::vector<uint4> *blocks) {
     const int32_t n = static_cast<int32_t>(sc.seq.size());
     if (n == 0) return false;
     std::vector<int32_t> heads;
@@ -783,7 +783,6 @@ bool build_chains(const emo_graph_s &g, const Schedule &sc, std::vector<emo::Cha
         dc->win = 0;
         blocks->clear();
     }
-    dc->exact = exact && dc->win > 0 ? 1 : 0;
     return true;
 }
 
@@ -1209,11 +1208,11 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     std::vector<uint4> cblocks;
     emo::DevChains dc;
     const bool exact_sums = exact_time_sums(*g, pack_time);
-    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc, &cblocks, exact_sums);
+    const bool chains_ok = build_chains(*g, sf, &csteps, &cpos, &dc, &cblocks);
     in.chain_lanes = chains_ok ? dc.lanes : 0;
     in.chain_window = chains_ok ? dc.win : 0;
-    in.chain_scan_window = chains_ok && dc.exact ? dc.win : 0;
-    in.chain_scan_full = chains_ok && dc.exact && dc.full ? 1 : 0;
+    in.chain_scan_window = chains_ok ? dc.win : 0;
+    in.chain_scan_full = chains_ok && dc.win > 0 && dc.full ? 1 : 0;
     const int32_t nops = static_cast<int32_t>(sf.seq.size());
     g->jit_eligible = nops >= 1 && nops <= kJitMaxOps;
     g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;

@@ -188,9 +188,6 @@ struct DevChains {
     int32_t hdr_words = 0;            // nc + 1 rounded up to a multiple of 4
     int32_t blk_bytes = 0;
     const uint4 *blocks = nullptr;    // [nwin][blk_bytes / 16]
-    // slack by a second forward pass (chains_windowed with SCAN): the windowed layout exists and
-    // every time sum is exact
-    int32_t exact = 0;
     // every window lies wholly inside the graph (P a multiple of win), a thread of the windowed
     // kernel holds at most four float4 pieces of the slack tile, and a workgroup's slack rows
     // span less than 2^32 bytes: the second-pass kernel with per-thread copy plans applies
@@ -202,8 +199,8 @@ bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int3
 // Whether a call runs the windowed kernel (the layout exists and the buffers are 16-byte
 // aligned).
 bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *slack);
-// Whether a call runs the windowed kernel with slack from a second forward pass (the windowed
-// layout exists, the graph's time sums are exact and the buffers are 16-byte aligned).
+// Whether a call runs the windowed kernel with slack from a second forward pass (a call with
+// slack on the windowed layout, buffers 16-byte aligned).
 bool chains_scan_ok(const DevChains &c, const uint8_t *levels, const float *slack);
 // Whether that call runs the second-pass kernel with per-thread copy plans (chains_scan_full).
 bool chains_scan_full_ok(const DevChains &c, const uint8_t *levels, const float *slack);

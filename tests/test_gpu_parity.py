@@ -461,9 +461,9 @@ CHAIN_WINDOW = {"1-stream": 16, "16-streams": 256, "3-streams-F8": 64, "9-stream
 
 def off_grid(g):
     """The same graph plus one isolated node of 2^-30 us.  The common power of two of all times
-    drops to 2^-30, so the loader can no longer show that every time sum is exact and the
-    two-pass chain scan gives way to the windowed kernel; every value the chains compute is
-    still on the 2^-4 us grid, so results stay exact."""
+    drops to 2^-30, so the loader can no longer show that every time sum is exact
+    (exact_time_sums 0); every value the chains compute is still on the 2^-4 us grid, so results
+    stay exact and the kernels must still match the oracle bit for bit."""
     V = g.num_nodes
     return dataclasses.replace(
         g, name=g.name + "-offgrid", num_nodes=V + 1,
@@ -473,16 +473,19 @@ def off_grid(g):
 
 
 def check_windowed_off_grid(torch, emo, g, rows, win, what):
-    """The windowed kernel on the off-grid copy of `g`: makespan, energy and slack against the
-    oracle, makespan and slack bit for bit against the interpreter."""
+    """The windowed kernels on the off-grid copy of `g` (the chain scan for slack, whose time
+    sums the loader cannot show exact): makespan, energy and slack against the oracle, makespan
+    and slack bit for bit against the interpreter."""
     g2 = off_grid(g)
     gh = emo.EmoGraph(g2, device=0)
-    assert gh.info()["chain_scan_window"] == 0 and gh.info()["chain_window"] == win
+    info = gh.info()
+    assert info["exact_time_sums"] == 0 and info["chain_window"] == win and info["chain_scan_window"] == win
     lv = dev(torch, rows)
     T, E = gh.eval_policies(lv)
+    assert gh.info()["last_kernels"] == 4, gh.info()
     S = gh.slack(lv)
     torch.cuda.synchronize()
-    assert gh.info()["last_kernels"] == 4, gh.info()
+    assert gh.info()["last_kernels"] == (8 if info["chain_scan_full"] else 6), gh.info()
     T_or, E_or = oracle.eval_batch(g2, rows, nthreads=8)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, what + " off grid")
     ok = ~np.isnan(T_or)
@@ -587,18 +590,19 @@ def test_one_kernel_ragged_batches(torch, emo):
 
 @pytest.mark.parametrize("grid", ["on", "off"])
 def test_chain_windows_small_batches(torch, emo, grid):
-    """Two-pass scan kernel (on the time grid) and windowed kernel (off it) with batches smaller
-    than a workgroup's 64 candidates and one past it (lanes past the batch repeat the last row
-    and store nothing), repeated calls bit for bit."""
+    """Two-pass scan kernel (slack) and windowed kernel (eval), on the time grid and on a graph
+    whose sums the loader cannot show exact, with batches smaller than a workgroup's 64
+    candidates and one past it (lanes past the batch repeat the last row and store nothing),
+    repeated calls bit for bit."""
     g = synth.stream_graph(77, 8208, 16, 16)
     if grid == "off":
         g = off_grid(g)
     rng = np.random.default_rng(77)
     gh = emo.EmoGraph(g, device=0)
     assert gh.info()["chain_window"] == 256
-    assert gh.info()["chain_scan_window"] == (256 if grid == "on" else 0)
+    assert gh.info()["chain_scan_window"] == 256
+    assert gh.info()["exact_time_sums"] == (1 if grid == "on" else 0)
     assert gh.info()["chain_scan_full"] == 0     # 8208 packs: the last window is partial
-    scan = grid == "on"
     for B in (1, 3, 64, 65):
         rows = pins.random_rows(rng, g, B)
         print(f"[case] windowed chains grid={grid} B={B}", flush=True)
@@ -606,7 +610,7 @@ def test_chain_windows_small_batches(torch, emo, grid):
         T, E = gh.eval_policies(lv)
         S = gh.slack(lv)
         torch.cuda.synchronize()
-        assert gh.info()["last_kernels"] == (6 if scan else 4)     # (the slack call)
+        assert gh.info()["last_kernels"] == 6     # (the slack call)
         T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
         parity.assert_eval(host(T), host(E), T_or, E_or, True, f"windowed B={B}")
         S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(B)])
@@ -616,6 +620,44 @@ def test_chain_windows_small_batches(torch, emo, grid):
         assert np.array_equal(host(T).view(np.uint32), host(T2).view(np.uint32))
         assert np.array_equal(host(E).view(np.uint32), host(E2).view(np.uint32))
         assert np.array_equal(host(S).view(np.uint32), host(S2).view(np.uint32))
+
+
+@pytest.mark.parametrize("P", [8208, 8448])
+def test_chain_scan_off_grid(torch, emo, P):
+    """Chain graphs with every table time scaled by 1.1 (off any common power-of-two grid): the
+    two-pass scan takes slack from prefix sums along each chain, so it rounds differently from
+    the backward recurrence.  Makespan, energy and every slack element against the oracle within
+    1e-5 of the makespan, and against the interpreter to the same bound (makespans bit for bit:
+    the forward walk is the recurrence's); 8208 packs run the general scan kernel, 8448 the one
+    with per-thread copy plans (both more than 8192 steps, past the segmented kernels)."""
+    g = synth.scaled_times(synth.stream_graph(78, P, 16, 16), 1.1)
+    rng = np.random.default_rng(P)
+    rows = pins.random_rows(rng, g, 300)
+    rows[9, P // 2] = 16
+    print(f"[case] chain scan off the grid P={P}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    info = gh.info()
+    assert info["exact_time_sums"] == 0 and info["chain_scan_window"] == 256
+    assert info["chain_scan_full"] == (1 if P % 256 == 0 else 0)
+    lv = dev(torch, rows)
+    T = torch.empty(len(rows), dtype=torch.float32, device="cuda")
+    E = torch.empty_like(T)
+    S = gh.slack(lv, makespan=T, energy=E)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == (8 if P % 256 == 0 else 6), gh.info()
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    ok = ~np.isnan(T_or)
+    assert not ok[9]
+    parity.assert_eval(host(T), host(E), T_or, E_or, False, f"scan off grid P={P}")
+    Sh = host(S)
+    assert np.all(np.isnan(Sh[~ok]))
+    _, _, S_or = oracle.slack_batch(g, rows[ok], nthreads=8)
+    parity.assert_slack(Sh[ok], S_or, T_or[ok], False, f"scan off grid P={P} slack")
+    gi = emo.EmoGraph(g, device=0, kernel_mode=1)
+    Ti, _ = gi.eval_policies(lv)
+    Si = gi.slack(lv)
+    assert np.array_equal(host(T).view(np.uint32), host(Ti).view(np.uint32))
+    parity.assert_slack(Sh[ok], host(Si)[ok], T_or[ok], False, f"scan off grid P={P} vs interpreted")
 
 
 @pytest.mark.parametrize("lengths", [[3100, 2900, 3400], [3100, 2900, 3406], [768] * 16],
