@@ -622,52 +622,55 @@ def test_chain_windows_small_batches(torch, emo, grid):
         assert np.array_equal(host(S).view(np.uint32), host(S2).view(np.uint32))
 
 
-@pytest.mark.parametrize("P", [8208, 8448])
-def test_chain_scan_off_grid(torch, emo, P):
+@pytest.mark.parametrize("case", ["8208", "8448", "fixed"])
+def test_chain_scan_off_grid(torch, emo, case):
     """Chain graphs with every table time scaled by 1.1 (off any common power-of-two grid): the
     two-pass scan takes slack from prefix sums along each chain, so it rounds differently from
     the backward recurrence.  Makespan, energy and every slack element against the oracle within
     1e-5 of the makespan, and against the interpreter to the same bound (makespans bit for bit:
-    the forward walk is the recurrence's); 8208 packs run the general scan kernel, 8448 the one
-    with per-thread copy plans (both more than 8192 steps, past the segmented kernels)."""
-    g = synth.scaled_times(synth.stream_graph(78, P, 16, 16), 1.1)
-    rng = np.random.default_rng(P)
+    the forward walk is the recurrence's).  8208 packs on 16 streams run the general scan
+    kernel, 8448 the one with per-thread copy plans (both more than 8192 steps, past the
+    segmented kernels); "fixed" is 16 chains of packs and fixed-duration nodes (the copy-plan
+    kernel with fixed durations)."""
+    rng = np.random.default_rng(len(case) + 78)
+    if case == "fixed":
+        g = fixed_chains_graph(rng, [768] * 16)
+    else:
+        g = synth.stream_graph(78, int(case), 16, 16)
+    g = synth.scaled_times(g, 1.1)
+    P = g.num_packs
     rows = pins.random_rows(rng, g, 300)
-    rows[9, P // 2] = 16
-    print(f"[case] chain scan off the grid P={P}", flush=True)
+    rows[9, P // 2] = g.num_levels
+    print(f"[case] chain scan off the grid {case}: V={g.num_nodes} P={P}", flush=True)
     gh = emo.EmoGraph(g, device=0)
     info = gh.info()
+    full = P % 256 == 0
     assert info["exact_time_sums"] == 0 and info["chain_scan_window"] == 256
-    assert info["chain_scan_full"] == (1 if P % 256 == 0 else 0)
+    assert info["chain_scan_full"] == (1 if full else 0)
     lv = dev(torch, rows)
     T = torch.empty(len(rows), dtype=torch.float32, device="cuda")
     E = torch.empty_like(T)
     S = gh.slack(lv, makespan=T, energy=E)
     torch.cuda.synchronize()
-    assert gh.info()["last_kernels"] == (8 if P % 256 == 0 else 6), gh.info()
+    assert gh.info()["last_kernels"] == (8 if full else 6), gh.info()
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     ok = ~np.isnan(T_or)
     assert not ok[9]
-    parity.assert_eval(host(T), host(E), T_or, E_or, False, f"scan off grid P={P}")
+    parity.assert_eval(host(T), host(E), T_or, E_or, False, f"scan off grid {case}")
     Sh = host(S)
     assert np.all(np.isnan(Sh[~ok]))
     _, _, S_or = oracle.slack_batch(g, rows[ok], nthreads=8)
-    parity.assert_slack(Sh[ok], S_or, T_or[ok], False, f"scan off grid P={P} slack")
+    parity.assert_slack(Sh[ok], S_or, T_or[ok], False, f"scan off grid {case} slack")
     gi = emo.EmoGraph(g, device=0, kernel_mode=1)
     Ti, _ = gi.eval_policies(lv)
     Si = gi.slack(lv)
     assert np.array_equal(host(T).view(np.uint32), host(Ti).view(np.uint32))
-    parity.assert_slack(Sh[ok], host(Si)[ok], T_or[ok], False, f"scan off grid P={P} vs interpreted")
+    parity.assert_slack(Sh[ok], host(Si)[ok], T_or[ok], False, f"scan off grid {case} vs interpreted")
 
 
-@pytest.mark.parametrize("lengths", [[3100, 2900, 3400], [3100, 2900, 3406], [768] * 16],
-                         ids=["lane-per-chain", "windowed", "scan-full"])
-def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
-    """Chains that mix packs with fixed-duration nodes (which depend on the candidate through the
-    pack before them), constant floors from a host node, and chains of different lengths (6268
-    packs: lane-per-chain kernel; 6272 packs: windowed kernels; 16 chains of 512 packs: the
-    two-pass scan with per-thread copy plans, every 256-pack window full)."""
-    rng = np.random.default_rng(42)
+def fixed_chains_graph(rng, lengths):
+    """Chains that mix packs with fixed-duration nodes (a fixed node every third step), constant
+    floors from one host node every 50 steps, and chains of the given lengths."""
     src, dst, pack, dur = [], [], [], []
     h0 = 0   # a host node: candidate-independent floor for some chain nodes
     pack.append(-1)
@@ -697,6 +700,19 @@ def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
     e = (0.7 * t * rng.uniform(0.2, 1.0, (P, F))).astype(np.float32)
     g = synth.Graph("chains-with-fixed", V, np.asarray(src, np.int32), np.asarray(dst, np.int32),
                     np.asarray(pack, np.int32), np.asarray(dur, np.float32), P, F, t, e, 0.3)
+    return g
+
+
+@pytest.mark.parametrize("lengths", [[3100, 2900, 3400], [3100, 2900, 3406], [768] * 16],
+                         ids=["lane-per-chain", "windowed", "scan-full"])
+def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
+    """Chains that mix packs with fixed-duration nodes (which depend on the candidate through the
+    pack before them), constant floors from a host node, and chains of different lengths (6268
+    packs: lane-per-chain kernel; 6272 packs: windowed kernels; 16 chains of 512 packs: the
+    two-pass scan with per-thread copy plans, every 256-pack window full)."""
+    rng = np.random.default_rng(42)
+    g = fixed_chains_graph(rng, lengths)
+    V, P = g.num_nodes, g.num_packs
     rows = pins.random_rows(rng, g, 300)
     print(f"[case] chain lanes with fixed nodes: V={V} P={P}", flush=True)
     gh = emo.EmoGraph(g, device=0)
