@@ -455,16 +455,22 @@ __host__ __device__ inline bool win_slots(int W, int NC, int F, int blk_bytes, i
 // One window's copy in flight: the thread's pieces (16 bytes each), slot by slot: the first
 // slots hold level rows, the next table rows, the next the step block (how many of each is the
 // same for every thread, so the category of a slot is uniform); which of them read as zero
-// (level columns past P, table rows past the last pack, pieces past the end).
+// (level columns past P, table rows past the last pack, pieces past the end).  Rows of a pack
+// count that is not a multiple of 16 are not 16-byte aligned: a level piece is then the five
+// dwords around it (v and x, from its address rounded down to 4 bytes), and meta holds, per
+// slot, its byte shift (2 bits) and its number of bytes before the row's end (5 bits).
 struct WinSet {
     uint4 v[kWinPre];
+    uint32_t x[kWinPre];
     uint32_t zero;
+    uint32_t meta;
 };
 
 // Issues exactly kWinPre loads for window w (a piece past the end reads a valid address and is
 // zeroed when stored; unused slots read the first block piece), with the addresses as scalar
 // bases plus 32-bit lane offsets, so that the compiler counts them and waits at a commit for
 // the older window's loads only.  esize: bytes per table entry (8 forward, 4 backward).
+template <bool ROWS16>
 __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__restrict__ levels,
                                          const void *__restrict__ tab, int esize,
                                          const uint4 *__restrict__ blocks, int64_t base, int64_t B,
@@ -483,7 +489,7 @@ __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__rest
     const char *bbase = reinterpret_cast<const char *>(blocks + static_cast<int64_t>(w) * n_blk);
     const int64_t rows_left = B - base;                             // rows of this workgroup in range
     const int64_t cols_left = P - wcol;
-    uint32_t zero = 0u;
+    uint32_t zero = 0u, meta = 0u;
 #pragma unroll
     for (int i = 0; i < kWinPre; ++i) {
         const char *src;
@@ -496,6 +502,28 @@ __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__rest
             z = q >= n_lvl || 16 * k >= cols_left;
             off = z ? 0u : static_cast<uint32_t>(rr) * static_cast<uint32_t>(P) + 16u * static_cast<uint32_t>(k);
             src = reinterpret_cast<const char *>(lbase);
+            if (!ROWS16) {
+                // the five dwords from the piece's address rounded down to 4 bytes; a dword at or
+                // past the last one of the batch's rows reads that last dword instead (its bytes
+                // are all past the row's end, and masked when stored)
+                const uint64_t at = reinterpret_cast<uint64_t>(src + off);
+                const uint64_t lo = reinterpret_cast<uint64_t>(levels);
+                const uint64_t last = (lo + static_cast<uint64_t>(B * P) + 3u) / 4u * 4u - 4u;
+                const uint64_t al = at & ~static_cast<uint64_t>(3);
+                uint32_t d[5];
+#pragma unroll
+                for (int j = 0; j < 5; ++j) {
+                    const uint64_t aj = al + 4u * j;
+                    d[j] = *reinterpret_cast<const uint32_t *>(aj <= last ? aj : last);
+                }
+                s.v[i] = make_uint4(d[0], d[1], d[2], d[3]);
+                s.x[i] = d[4];
+                const int64_t nb = cols_left - 16 * k;
+                meta |= (static_cast<uint32_t>(at & 3u) | (static_cast<uint32_t>(nb < 16 ? (nb > 0 ? nb : 0) : 16)
+                                                          << 2)) << (7 * i);
+                zero |= z ? 1u << i : 0u;
+                continue;
+            }
         } else if (i < s_lvl + s_tab) {
             const int q = t + (i - s_lvl) * nt;
             z = q >= n_tab || 16u * static_cast<uint32_t>(q) >= tab_left;
@@ -511,6 +539,24 @@ __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__rest
         s.v[i] = *reinterpret_cast<const uint4 *>(src + off);
     }
     s.zero = zero;
+    s.meta = meta;
+}
+
+// A level piece of an unaligned row from its five dwords: the 16 bytes at the piece's shift,
+// with the bytes past the row's end cleared.
+__device__ __forceinline__ uint4 win_piece(const WinSet &s, int i) {
+    const uint32_t m = s.meta >> (7 * i), sh = m & 3u, nb = (m >> 2) & 31u;
+    uint32_t o[4];
+    o[0] = __builtin_amdgcn_alignbyte(s.v[i].y, s.v[i].x, sh);
+    o[1] = __builtin_amdgcn_alignbyte(s.v[i].z, s.v[i].y, sh);
+    o[2] = __builtin_amdgcn_alignbyte(s.v[i].w, s.v[i].z, sh);
+    o[3] = __builtin_amdgcn_alignbyte(s.x[i], s.v[i].w, sh);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t keep = nb >= 4u * j + 4u ? 4u : (nb > 4u * j ? nb - 4u * j : 0u);   // bytes kept
+        o[j] &= keep == 4u ? 0xffffffffu : (1u << (8u * keep)) - 1u;
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // Copies window w's pieces into LDS buffer `buf`; a level byte >= F marks its candidate in `bad`
@@ -518,6 +564,7 @@ __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__rest
 // energy and slack become NaN whatever its lookups read, and a lookup at column c <= W with
 // level l <= 255 stays inside the workgroup's LDS (at most 255 entries past the window's table,
 // which the layout leaves room for).
+template <bool ROWS16>
 __device__ __forceinline__ void win_store(const WinArgs &a, char *lds, int buf, void *tabbuf, int esize,
                                           uint32_t *bad, uint32_t addf, const WinSet &s) {
     const int t = threadIdx.x, nt = blockDim.x;
@@ -530,7 +577,7 @@ __device__ __forceinline__ void win_store(const WinArgs &a, char *lds, int buf, 
     uint4 *blk = reinterpret_cast<uint4 *>(lds + a.L.off_blk + buf * a.blk_bytes);
 #pragma unroll
     for (int i = 0; i < kWinPre; ++i) {
-        uint4 v = s.v[i];
+        uint4 v = !ROWS16 && i < s_lvl ? win_piece(s, i) : s.v[i];
         if ((s.zero >> i) & 1u) v = make_uint4(0u, 0u, 0u, 0u);
         if (i < s_lvl) {
             const int q = t + i * nt;
@@ -803,7 +850,7 @@ struct WinGroup {
 // size, and every other value takes one rounding: slack agrees with the backward recurrence to
 // rounding, and bit for bit when every time sum is exact (every time a multiple of one power of
 // two u and every path below 2^24 u, so every sum and difference is exact in fp32 in any order).
-template <bool SLACK, bool FIXED>
+template <bool SLACK, bool FIXED, bool ROWS16>
 __global__ void __launch_bounds__(kChainBlockThreads)
 chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ blocks,
                 const uint8_t *__restrict__ levels, int64_t B, float *__restrict__ To,
@@ -842,17 +889,17 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
         tab2[L.tab_elems + W * F + i] = make_float2(0.f, 0.f);
     }
     WinSet s0, s1;
-    win_load(a, levels, g.tab, 8, blocks, base, B, P, 0, s0);
-    win_load(a, levels, g.tab, 8, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
+    win_load<ROWS16>(a, levels, g.tab, 8, blocks, base, B, P, 0, s0);
+    win_load<ROWS16>(a, levels, g.tab, 8, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
     lds_barrier();
-    win_store(a, lds, 0, tab2, 8, bad, addf, s0);
+    win_store<ROWS16>(a, lds, 0, tab2, 8, bad, addf, s0);
     lds_barrier();
     float f = 0.f, pre = 0.f;
     double ed = 0.0;
     // window w from buffer w & 1; `ld` takes window w + 2, `cm` holds window w + 1
     auto forward_window = [&](int w, WinSet &ld, WinSet &cm) {
         const int buf = w & 1;
-        win_load(a, levels, g.tab, 8, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
+        win_load<ROWS16>(a, levels, g.tab, 8, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
         const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
         const char *tb = reinterpret_cast<const char *>(tab2 + buf * L.tab_elems);
         const ChainWinStep *rs = recs(buf);
@@ -898,7 +945,7 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
             ed += static_cast<double>(eb);
             eb = 0.f;
         }
-        if (w + 1 < nwin) win_store(a, lds, buf ^ 1, tab2 + (buf ^ 1) * L.tab_elems, 8, bad, addf, cm);
+        if (w + 1 < nwin) win_store<ROWS16>(a, lds, buf ^ 1, tab2 + (buf ^ 1) * L.tab_elems, 8, bad, addf, cm);
         lds_barrier();
     };
     for (int w = 0; w < nwin; w += 2) {
@@ -955,7 +1002,19 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
                                                    __builtin_nanf(""), __builtin_nanf(""));
             const int64_t row = base + r;
             const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 4 * kk;
-            if (row < B && col < P) *reinterpret_cast<float4 *>(S + row * P + col) = v;
+            if (row < B && col < P) {
+                if (ROWS16 || (P & 3) == 0) {
+                    *reinterpret_cast<float4 *>(S + row * P + col) = v;   // 16-byte aligned
+                } else {
+                    // rows of a pack count that is not a multiple of 4: single floats, up to the
+                    // row's end
+                    float *d = S + row * P + col;
+                    d[0] = v.x;
+                    if (col + 1 < P) d[1] = v.y;
+                    if (col + 2 < P) d[2] = v.z;
+                    if (col + 3 < P) d[3] = v.w;
+                }
+            }
         }
     };
     for (int i = t; i < F; i += nt) {
@@ -969,14 +1028,14 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     const float Kc = tfin[cl] - pre;
     const float K = Kc == Kc ? Kc : 0.f;
     float D = 0.f, Pr = 0.f;
-    win_load(a, levels, g.tabt, 4, blocks, base, B, P, 0, s0);
-    win_load(a, levels, g.tabt, 4, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
-    win_store(a, lds, 0, tabt, 4, nullptr, addf, s0);
+    win_load<ROWS16>(a, levels, g.tabt, 4, blocks, base, B, P, 0, s0);
+    win_load<ROWS16>(a, levels, g.tabt, 4, blocks, base, B, P, nwin > 1 ? 1 : 0, s1);
+    win_store<ROWS16>(a, lds, 0, tabt, 4, nullptr, addf, s0);
     lds_barrier();
     float *trow = tile + cl * (W + 1);
     auto scan_window = [&](int w, WinSet &ld, WinSet &cm) {
         const int buf = w & 1;
-        win_load(a, levels, g.tabt, 4, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
+        win_load<ROWS16>(a, levels, g.tabt, 4, blocks, base, B, P, w + 2 < nwin ? w + 2 : nwin - 1, ld);
         const uint8_t *lrow = lvl0 + buf * L.lvl_buf + cl * L.lvl_pitch;
         const char *tb = reinterpret_cast<const char *>(tabt + buf * L.tab_elems);
         const ChainWinStep *rs = recs(buf);
@@ -1013,7 +1072,7 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
             if (g + 2 >= ng) break;
             stage(G2, G0, G1, g + 2);
         }
-        if (w + 1 < nwin) win_store(a, lds, buf ^ 1, tabt + (buf ^ 1) * L.tab_elems, 4, nullptr, addf, cm);
+        if (w + 1 < nwin) win_store<ROWS16>(a, lds, buf ^ 1, tabt + (buf ^ 1) * L.tab_elems, 4, nullptr, addf, cm);
         lds_barrier();
         flush_tile(w);
         lds_barrier();
@@ -1296,7 +1355,7 @@ size_t chains_scratch_bytes(const DevGraph &g, const DevChains &c, const uint8_t
 }
 
 namespace {
-template <bool SLACK, bool FIXED>
+template <bool SLACK, bool FIXED, bool ROWS16>
 hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, const DevGraph &g,
                                   const DevChains &c, const WinArgs &a, const uint8_t *levels, int64_t B,
                                   float *T, float *E, float *S) {
@@ -1307,12 +1366,13 @@ hipError_t launch_windowed_kernel(dim3 gd, dim3 bd, size_t lds, hipStream_t s, c
     if (e != hipSuccess) return e;
     const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
     if (!bit || !(done.load(std::memory_order_acquire) & bit)) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED>),
+        e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chains_windowed<SLACK, FIXED, ROWS16>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kWinLds));
         if (e != hipSuccess) return e;
         done.fetch_or(bit, std::memory_order_acq_rel);
     }
-    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED>), gd, bd, lds, s, g, c, a, c.blocks, levels, B, T, E, S);
+    hipLaunchKernelGGL((chains_windowed<SLACK, FIXED, ROWS16>), gd, bd, lds, s, g, c, a, c.blocks, levels, B, T,
+                       E, S);
     return hipGetLastError();
 }
 
@@ -1368,10 +1428,17 @@ hipError_t launch_windowed(const DevGraph &g, const DevChains &c, const uint8_t 
                            : launch_scan_full_kernel<true, 1>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack))
                     : (two ? launch_scan_full_kernel<false, 2>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack)
                            : launch_scan_full_kernel<false, 1>(gd, bd, lds, s, g, c, a, levels, B, Ts, Es, slack));
-    } else if (slack) e = c.fixed ? launch_windowed_kernel<true, true>(EMO_WIN_ARGS)
-                                  : launch_windowed_kernel<true, false>(EMO_WIN_ARGS);
-    else e = c.fixed ? launch_windowed_kernel<false, true>(EMO_WIN_ARGS)
-                     : launch_windowed_kernel<false, false>(EMO_WIN_ARGS);
+    } else if (g.P % 16 == 0) {
+        e = slack ? (c.fixed ? launch_windowed_kernel<true, true, true>(EMO_WIN_ARGS)
+                             : launch_windowed_kernel<true, false, true>(EMO_WIN_ARGS))
+                  : (c.fixed ? launch_windowed_kernel<false, true, true>(EMO_WIN_ARGS)
+                             : launch_windowed_kernel<false, false, true>(EMO_WIN_ARGS));
+    } else {
+        e = slack ? (c.fixed ? launch_windowed_kernel<true, true, false>(EMO_WIN_ARGS)
+                             : launch_windowed_kernel<true, false, false>(EMO_WIN_ARGS))
+                  : (c.fixed ? launch_windowed_kernel<false, true, false>(EMO_WIN_ARGS)
+                             : launch_windowed_kernel<false, false, false>(EMO_WIN_ARGS));
+    }
 #undef EMO_WIN_ARGS
     if (e == hipSuccess && tg.n) e = launch_select_results(Ts, Es, B, tg, s);
     return e;

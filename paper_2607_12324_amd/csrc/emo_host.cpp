@@ -634,8 +634,9 @@ bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
                          const std::vector<std::vector<int32_t>> &chains,
                          std::vector<uint4> *blocks, emo::DevChains *dc) {
     const int32_t nc = static_cast<int32_t>(chains.size());
-    // (level offsets within a workgroup's rows are 32-bit: at most 1024 rows of P bytes)
-    if (nc < 1 || nc > 16 || g.P < 16 || g.P % 16 != 0 || g.P >= (1 << 21)) return false;
+    // (level offsets within a workgroup's rows are 32-bit: at most 1024 rows of P bytes; rows of
+    // a pack count that is not a multiple of 16 are copied from the dwords around each piece)
+    if (nc < 1 || nc > 16 || g.P < 16 || g.P >= (1 << 21)) return false;
     const int32_t hdr_words = (nc + 1 + 3) / 4 * 4;
     for (int32_t W = 256; W >= 16; W >>= 1) {
         const int32_t nwin = (g.P + W - 1) / W;

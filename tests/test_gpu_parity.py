@@ -449,14 +449,18 @@ CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-strea
                "64-streams": (8300, 64, 5),
                # a block's table rows exceed the LDS stage: every lane reads the table itself
                "64-streams-F16": (8300, 64, 16),
-               # pack count not a multiple of 4: slack stored directly in pack order
+               # pack count not a multiple of 4: the lane-per-chain kernel (unaligned buffers) stores
+               # slack directly in pack order
                "odd-packs": (8301, 7, 8),
                # windowed kernel: 16 chains (one workgroup of 64 candidates), 3 chains (5 groups
                # of 64 candidates), 9 chains with 32 levels (narrower windows); more than 8192
                # steps, so that the segmented kernels do not apply
                "16-streams": (8208, 16, 16), "3-streams-F8": (8224, 3, 8), "9-streams-F32": (8208, 9, 32)}
 # packs per window of the windowed kernel (0: lane-per-chain kernels only)
-CHAIN_WINDOW = {"1-stream": 16, "16-streams": 256, "3-streams-F8": 64, "9-streams-F32": 64}
+# (9000 and 8301 packs: rows that are not 16-byte aligned, copied from the dwords around each
+# piece; 8301: slack rows stored a float at a time)
+CHAIN_WINDOW = {"1-stream": 16, "5-streams": 64, "odd-packs": 128, "16-streams": 256, "3-streams-F8": 64,
+                "9-streams-F32": 64}
 
 
 def off_grid(g):
@@ -704,12 +708,13 @@ def fixed_chains_graph(rng, lengths):
 
 
 @pytest.mark.parametrize("lengths", [[3100, 2900, 3400], [3100, 2900, 3406], [768] * 16],
-                         ids=["lane-per-chain", "windowed", "scan-full"])
+                         ids=["unaligned-rows", "windowed", "scan-full"])
 def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
     """Chains that mix packs with fixed-duration nodes (which depend on the candidate through the
     pack before them), constant floors from a host node, and chains of different lengths (6268
-    packs: lane-per-chain kernel; 6272 packs: windowed kernels; 16 chains of 512 packs: the
-    two-pass scan with per-thread copy plans, every 256-pack window full)."""
+    packs: windowed kernels on rows that are not 16-byte aligned; 6272 packs: windowed kernels;
+    16 chains of 512 packs: the two-pass scan with per-thread copy plans, every 256-pack window
+    full), and the lane-per-chain kernel (unaligned level buffer) bit for bit."""
     rng = np.random.default_rng(42)
     g = fixed_chains_graph(rng, lengths)
     V, P = g.num_nodes, g.num_packs
@@ -718,22 +723,28 @@ def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
     gh = emo.EmoGraph(g, device=0)
     full = len(lengths) == 16
     assert gh.info()["chain_lanes"] == (16 if full else 4)
-    windowed = P % 16 == 0
     win = 256 if full else 64
-    assert gh.info()["chain_window"] == (win if windowed else 0)
-    assert gh.info()["chain_scan_window"] == (win if windowed else 0)
+    assert gh.info()["chain_window"] == win
+    assert gh.info()["chain_scan_window"] == win
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
     S = gh.slack(lv)
     # (3 chains are too few for the per-thread plans of 64-pack windows)
     assert gh.info()["chain_scan_full"] == (1 if full else 0)
-    assert gh.info()["last_kernels"] == ((8 if full else 6) if windowed else 3)
+    assert gh.info()["last_kernels"] == (8 if full else 6)
     parity.assert_eval(host(T), host(E), T_or, E_or, True, "chains with fixed nodes")
     S_or = np.stack([oracle.pack_slack(g, rows[c]) for c in range(len(rows))])
     parity.assert_slack(host(S), S_or, T_or, True, "chains with fixed nodes: pack slack")
-    if windowed:
-        check_windowed_off_grid(torch, emo, g, rows, win, "chains with fixed nodes")
+    # the lane-per-chain kernel on the same rows (an unaligned level buffer): bit for bit
+    lm = misaligned(torch, rows)
+    Tm, _ = gh.eval_policies(lm)
+    Sm = gh.slack(lm)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == 3
+    assert np.array_equal(host(T).view(np.uint32), host(Tm).view(np.uint32))
+    assert np.array_equal(host(S).view(np.uint32), host(Sm).view(np.uint32))
+    check_windowed_off_grid(torch, emo, g, rows, win, "chains with fixed nodes")
 
 
 def skewed_chains(seed, P, S, F, share):

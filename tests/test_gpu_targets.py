@@ -58,7 +58,8 @@ def graph_of(case):
         # the 4096-pack graph: too long for one kernel, synchronised every 256 packs
         return synth.config_graph(4)
     if case == "chain-lanes":
-        return synth.stream_graph(9005, 9000, 5, 16)
+        # more than 16 chains: no windowed layout, one lane per chain
+        return synth.stream_graph(9020, 9000, 20, 16)
     if case == "chain-windows":
         return synth.stream_graph(8224, 8208, 16, 16)
     raise KeyError(case)
