@@ -456,12 +456,13 @@ __host__ __device__ inline bool win_slots(int W, int NC, int F, int blk_bytes, i
 // slots hold level rows, the next table rows, the next the step block (how many of each is the
 // same for every thread, so the category of a slot is uniform); which of them read as zero
 // (level columns past P, table rows past the last pack, pieces past the end).  Rows of a pack
-// count that is not a multiple of 16 are not 16-byte aligned: a level piece is then the five
-// dwords around it (v and x, from its address rounded down to 4 bytes), and meta holds, per
-// slot, its byte shift (2 bits) and its number of bytes before the row's end (5 bits).
+// count that is not a multiple of 16 are not 16-byte aligned (the layout then gives every
+// thread one level piece, in slot 0): the piece is the five dwords around it (v[0] and x, from
+// its address rounded down to 4 bytes), and meta holds its byte shift (2 bits) and its number
+// of bytes before the row's end (5 bits).
 struct WinSet {
     uint4 v[kWinPre];
-    uint32_t x[kWinPre];
+    uint32_t x;
     uint32_t zero;
     uint32_t meta;
 };
@@ -502,7 +503,7 @@ __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__rest
             z = q >= n_lvl || 16 * k >= cols_left;
             off = z ? 0u : static_cast<uint32_t>(rr) * static_cast<uint32_t>(P) + 16u * static_cast<uint32_t>(k);
             src = reinterpret_cast<const char *>(lbase);
-            if (!ROWS16) {
+            if (!ROWS16 && i == 0) {
                 // the five dwords from the piece's address rounded down to 4 bytes; a dword at or
                 // past the last one of the batch's rows reads that last dword instead (its bytes
                 // are all past the row's end, and masked when stored)
@@ -516,11 +517,10 @@ __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__rest
                     const uint64_t aj = al + 4u * j;
                     d[j] = *reinterpret_cast<const uint32_t *>(aj <= last ? aj : last);
                 }
-                s.v[i] = make_uint4(d[0], d[1], d[2], d[3]);
-                s.x[i] = d[4];
+                s.v[0] = make_uint4(d[0], d[1], d[2], d[3]);
+                s.x = d[4];
                 const int64_t nb = cols_left - 16 * k;
-                meta |= (static_cast<uint32_t>(at & 3u) | (static_cast<uint32_t>(nb < 16 ? (nb > 0 ? nb : 0) : 16)
-                                                          << 2)) << (7 * i);
+                meta = static_cast<uint32_t>(at & 3u) | (static_cast<uint32_t>(nb < 16 ? (nb > 0 ? nb : 0) : 16) << 2);
                 zero |= z ? 1u << i : 0u;
                 continue;
             }
@@ -544,13 +544,13 @@ __device__ __forceinline__ void win_load(const WinArgs &a, const uint8_t *__rest
 
 // A level piece of an unaligned row from its five dwords: the 16 bytes at the piece's shift,
 // with the bytes past the row's end cleared.
-__device__ __forceinline__ uint4 win_piece(const WinSet &s, int i) {
-    const uint32_t m = s.meta >> (7 * i), sh = m & 3u, nb = (m >> 2) & 31u;
+__device__ __forceinline__ uint4 win_piece(const WinSet &s) {
+    const uint32_t sh = s.meta & 3u, nb = (s.meta >> 2) & 31u;
     uint32_t o[4];
-    o[0] = __builtin_amdgcn_alignbyte(s.v[i].y, s.v[i].x, sh);
-    o[1] = __builtin_amdgcn_alignbyte(s.v[i].z, s.v[i].y, sh);
-    o[2] = __builtin_amdgcn_alignbyte(s.v[i].w, s.v[i].z, sh);
-    o[3] = __builtin_amdgcn_alignbyte(s.x[i], s.v[i].w, sh);
+    o[0] = __builtin_amdgcn_alignbyte(s.v[0].y, s.v[0].x, sh);
+    o[1] = __builtin_amdgcn_alignbyte(s.v[0].z, s.v[0].y, sh);
+    o[2] = __builtin_amdgcn_alignbyte(s.v[0].w, s.v[0].z, sh);
+    o[3] = __builtin_amdgcn_alignbyte(s.x, s.v[0].w, sh);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const uint32_t keep = nb >= 4u * j + 4u ? 4u : (nb > 4u * j ? nb - 4u * j : 0u);   // bytes kept
@@ -577,7 +577,7 @@ __device__ __forceinline__ void win_store(const WinArgs &a, char *lds, int buf, 
     uint4 *blk = reinterpret_cast<uint4 *>(lds + a.L.off_blk + buf * a.blk_bytes);
 #pragma unroll
     for (int i = 0; i < kWinPre; ++i) {
-        uint4 v = !ROWS16 && i < s_lvl ? win_piece(s, i) : s.v[i];
+        uint4 v = !ROWS16 && i == 0 ? win_piece(s) : s.v[i];
         if ((s.zero >> i) & 1u) v = make_uint4(0u, 0u, 0u, 0u);
         if (i < s_lvl) {
             const int q = t + i * nt;
@@ -1309,7 +1309,7 @@ bool staged_ok(const DevGraph &g, const DevChains &c) {
 size_t round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 }  // namespace
 
-bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int32_t *groups) {
+bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, bool rows16, int32_t *groups) {
     if (nc < 1 || nc > kWinMaxWaves || F < 1 || F > 128 || W < 16 || W > 256 || blk_bytes % 16 != 0)
         return false;
     const int G = kWinMaxWaves / nc;
@@ -1317,6 +1317,9 @@ bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int3
     const WinLayout L = win_layout(W, NC, F, G * nc, blk_bytes);
     int sl, st8, st4, sb;
     if (L.total > kWinLds || !win_slots(W, NC, F, blk_bytes, nthreads, &sl, &st8, &st4, &sb)) return false;
+    // rows that are not 16-byte aligned: one level piece per thread (its five dwords are held
+    // from one window to the next)
+    if (!rows16 && sl > 1) return false;
     *groups = G;
     return true;
 }

@@ -674,7 +674,7 @@ bool build_chain_windows(const emo_graph_s &g, const Schedule &sc,
         }
         const int32_t blk_bytes = 4 * hdr_words + 16 * rec_max;
         int32_t G = 0;
-        if (!emo::chain_window_fits(nc, g.F, W, blk_bytes, &G)) continue;
+        if (!emo::chain_window_fits(nc, g.F, W, blk_bytes, g.P % 16 == 0, &G)) continue;
         const size_t words = static_cast<size_t>(blk_bytes) / 4;
         emo::ChainWinStep noop;
         noop.ct = static_cast<uint32_t>(W) | (static_cast<uint32_t>(W * g.F) << 16);

@@ -194,8 +194,9 @@ struct DevChains {
     int32_t full = 0;
 };
 // Whether the windowed kernel's LDS working set and prefetch fit for `nc` chains, F levels,
-// windows of W packs and step blocks of blk_bytes; sets the candidate groups per workgroup.
-bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, int32_t *groups);
+// windows of W packs and step blocks of blk_bytes (rows16: P is a multiple of 16); sets the
+// candidate groups per workgroup.
+bool chain_window_fits(int32_t nc, int32_t F, int32_t W, int32_t blk_bytes, bool rows16, int32_t *groups);
 // Whether a call runs the windowed kernel (the layout exists and the buffers are 16-byte
 // aligned).
 bool chains_windowed_ok(const DevChains &c, const uint8_t *levels, const float *slack);

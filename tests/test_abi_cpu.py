@@ -176,16 +176,16 @@ def test_chain_windows(emo):
     """Window width of the windowed chain kernel: the widest of 256, 128, ..., 16 packs whose
     LDS working set fits (two level windows of 16 // chains groups of 64 candidates, two table
     windows, two step blocks, the slack tile) and whose copy takes at most 4 pieces of 16 bytes
-    per thread (also for pack counts that are not multiples of 16, whose rows the kernel copies
-    from the dwords around each piece); none with more than 16 chains, more than 128 levels or a
-    chain that goes back to an earlier window."""
+    per thread (one piece for pack counts that are not multiples of 16, whose rows the kernel
+    copies from the dwords around each piece); none with more than 16 chains, more than 128
+    levels or a chain that goes back to an earlier window."""
     expect = {1: 0, 2: 16, 3: 0, 4: 0, 5: 256}
     for k, win in expect.items():
         assert _load(emo, synth.config_graph(k)).info()["chain_window"] == win, k
     for (P, S, F), win in (((8192, 16, 16), 256), ((4096, 3, 8), 64), ((8192, 9, 32), 64),
                            ((10000, 1, 16), 16), ((9008, 5, 16), 64), ((8304, 7, 8), 128),
                            ((4096, 2, 64), 32), ((4096, 16, 128), 32), ((9000, 5, 16), 64),
-                           ((8301, 7, 8), 128),
+                           ((8301, 7, 8), 64),
                            ((8192, 17, 4), 0), ((4096, 2, 200), 0)):
         g = synth.stream_graph(7, P, S, F)
         assert _load(emo, g).info()["chain_window"] == win, (P, S, F)

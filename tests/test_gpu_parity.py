@@ -458,8 +458,9 @@ CHAIN_CASES = {"1-stream": (10000, 1, 16), "5-streams": (9000, 5, 16), "33-strea
                "16-streams": (8208, 16, 16), "3-streams-F8": (8224, 3, 8), "9-streams-F32": (8208, 9, 32)}
 # packs per window of the windowed kernel (0: lane-per-chain kernels only)
 # (9000 and 8301 packs: rows that are not 16-byte aligned, copied from the dwords around each
-# piece; 8301: slack rows stored a float at a time)
-CHAIN_WINDOW = {"1-stream": 16, "5-streams": 64, "odd-packs": 128, "16-streams": 256, "3-streams-F8": 64,
+# piece, with windows narrow enough for one piece per thread; 8301: slack rows stored a float at
+# a time)
+CHAIN_WINDOW = {"1-stream": 16, "5-streams": 64, "odd-packs": 64, "16-streams": 256, "3-streams-F8": 64,
                 "9-streams-F32": 64}
 
 
@@ -723,7 +724,8 @@ def test_chain_lanes_with_fixed_nodes(torch, emo, lengths):
     gh = emo.EmoGraph(g, device=0)
     full = len(lengths) == 16
     assert gh.info()["chain_lanes"] == (16 if full else 4)
-    win = 256 if full else 64
+    # (rows that are not 16-byte aligned: windows narrow enough for one level piece per thread)
+    win = 256 if full else (64 if P % 16 == 0 else 32)
     assert gh.info()["chain_window"] == win
     assert gh.info()["chain_scan_window"] == win
     lv = dev(torch, rows)
