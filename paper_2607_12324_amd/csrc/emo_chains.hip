@@ -984,6 +984,19 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
     // are long enough (conflict-free LDS reads with the odd row pitch), else whole rows
     // (W is a power of two: shifts, no divisions)
     auto flush_tile = [&](int w) {
+        if (!ROWS16 && (P & 3) != 0) {
+            // rows of a pack count that is not a multiple of 4 (4-byte aligned only): one float
+            // per lane, consecutive lanes on consecutive columns of a row (256-byte pieces)
+            const int n1 = a.NC << a.wlog;
+            for (int q = t; q < n1; q += nt) {
+                const int r = q >> a.wlog, cc = q & (W - 1);
+                const int64_t row = base + r;
+                const int64_t col = (static_cast<int64_t>(w) << a.wlog) + cc;
+                const float v = tfin[r] != tfin[r] ? __builtin_nanf("") : tile[r * (W + 1) + cc];
+                if (row < B && col < P) S[row * P + col] = v;
+            }
+            return;
+        }
         const int n = a.NC << prlog;
         for (int q = t; q < n; q += nt) {
             int r, kk;
@@ -1002,19 +1015,7 @@ chains_windowed(DevGraph g, DevChains c, WinArgs a, const uint4 *__restrict__ bl
                                                    __builtin_nanf(""), __builtin_nanf(""));
             const int64_t row = base + r;
             const int64_t col = (static_cast<int64_t>(w) << a.wlog) + 4 * kk;
-            if (row < B && col < P) {
-                if (ROWS16 || (P & 3) == 0) {
-                    *reinterpret_cast<float4 *>(S + row * P + col) = v;   // 16-byte aligned
-                } else {
-                    // rows of a pack count that is not a multiple of 4: single floats, up to the
-                    // row's end
-                    float *d = S + row * P + col;
-                    d[0] = v.x;
-                    if (col + 1 < P) d[1] = v.y;
-                    if (col + 2 < P) d[2] = v.z;
-                    if (col + 3 < P) d[3] = v.w;
-                }
-            }
+            if (row < B && col < P) *reinterpret_cast<float4 *>(S + row * P + col) = v;   // 16-byte aligned
         }
     };
     for (int i = t; i < F; i += nt) {
