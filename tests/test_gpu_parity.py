@@ -593,21 +593,22 @@ def test_one_kernel_ragged_batches(torch, emo):
         run_all(torch, emo, g, rows, [tgt], per_node=False, what=f"one kernel B={B}")
 
 
-@pytest.mark.parametrize("grid", ["on", "off"])
+@pytest.mark.parametrize("grid", ["on", "off", "unaligned"])
 def test_chain_windows_small_batches(torch, emo, grid):
-    """Two-pass scan kernel (slack) and windowed kernel (eval), on the time grid and on a graph
-    whose sums the loader cannot show exact, with batches smaller than a workgroup's 64
-    candidates and one past it (lanes past the batch repeat the last row and store nothing),
-    repeated calls bit for bit."""
-    g = synth.stream_graph(77, 8208, 16, 16)
+    """Two-pass scan kernel (slack) and windowed kernel (eval), on the time grid, on a graph
+    whose sums the loader cannot show exact, and with 8211 packs (rows that are not 4-byte
+    aligned: a batch of one row reads its last piece's dwords up to the batch's end only), with
+    batches smaller than a workgroup's 64 candidates and one past it (lanes past the batch
+    repeat the last row and store nothing), repeated calls bit for bit."""
+    g = synth.stream_graph(77, 8211 if grid == "unaligned" else 8208, 16, 16)
     if grid == "off":
         g = off_grid(g)
     rng = np.random.default_rng(77)
     gh = emo.EmoGraph(g, device=0)
     assert gh.info()["chain_window"] == 256
     assert gh.info()["chain_scan_window"] == 256
-    assert gh.info()["exact_time_sums"] == (1 if grid == "on" else 0)
-    assert gh.info()["chain_scan_full"] == 0     # 8208 packs: the last window is partial
+    assert gh.info()["exact_time_sums"] == (0 if grid == "off" else 1)
+    assert gh.info()["chain_scan_full"] == 0     # 8208 and 8211 packs: the last window is partial
     for B in (1, 3, 64, 65):
         rows = pins.random_rows(rng, g, B)
         print(f"[case] windowed chains grid={grid} B={B}", flush=True)
