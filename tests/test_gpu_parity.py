@@ -674,6 +674,55 @@ def test_chain_scan_off_grid(torch, emo, case):
     parity.assert_slack(Sh[ok], host(Si)[ok], T_or[ok], False, f"scan off grid {case} vs interpreted")
 
 
+# stream-chain graphs short enough for the segmented kernels: (packs, streams, levels) and the
+# kernels their slack call takes (2 segmented, 6 chain scan, 8 chain scan with copy plans)
+SCAN_FIRST_CASES = {"512": (512, 16, 16, 2), "768": (768, 16, 16, 8), "2000-5s": (2000, 5, 16, 6),
+                    "4100-unaligned": (4100, 16, 16, 6), "3000-7s-F8": (3000, 7, 8, 6)}
+
+
+@pytest.mark.parametrize("case", list(SCAN_FIRST_CASES))
+def test_chain_scan_before_segmented(torch, emo, case):
+    """Slack on disjoint stream chains of 768 to 8192 steps takes the windowed chain scan rather
+    than the segmented kernels (512 steps still the segmented ones); calls without slack keep the
+    one-kernel (up to 2048 steps) or segmented kernels, and a slack buffer that is not 16-byte
+    aligned leaves the scan.  Every row against the oracle; makespan and slack bit for bit
+    between the kernel kinds (the graphs are on the exact-sum grid)."""
+    P, S_, F, skind = SCAN_FIRST_CASES[case]
+    g = synth.stream_graph(P + S_, P, S_, F)
+    rng = np.random.default_rng(P + 31 * S_)
+    rows = pins.random_rows(rng, g, 300)
+    rows[11, P // 2] = F
+    print(f"[case] chain scan before segmented {case}: V={g.num_nodes} P={P}", flush=True)
+    gh = emo.EmoGraph(g, device=0)
+    assert gh.info()["exact_time_sums"] == 1 and gh.info()["chain_scan_window"] > 0
+    lv = dev(torch, rows)
+    T = torch.empty(len(rows), dtype=torch.float32, device="cuda")
+    E = torch.empty_like(T)
+    S = gh.slack(lv, makespan=T, energy=E)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == skind, gh.info()
+    T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
+    ok = ~np.isnan(T_or)
+    assert not ok[11]
+    parity.assert_eval(host(T), host(E), T_or, E_or, True, f"scan first {case}")
+    Sh = host(S)
+    assert np.all(np.isnan(Sh[~ok]))
+    _, _, S_or = oracle.slack_batch(g, rows[ok], nthreads=8)
+    parity.assert_slack(Sh[ok], S_or, T_or[ok], True, f"scan first {case} slack")
+    T1, E1 = gh.eval_policies(lv)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] == (1 if P <= 2048 else 2), gh.info()
+    assert np.array_equal(host(T).view(np.uint32), host(T1).view(np.uint32))
+    # (energy blocks are grouped per chain window here, in program order there)
+    parity.assert_eval(host(T1), host(E1), T_or, E_or, True, f"scan first {case} eval")
+    buf = torch.empty(len(rows) * P + 1, dtype=torch.float32, device="cuda")
+    S2 = buf[1:].view(len(rows), P)
+    gh.slack(lv, out=S2)
+    torch.cuda.synchronize()
+    assert gh.info()["last_kernels"] not in (6, 8), gh.info()
+    assert np.array_equal(Sh.view(np.uint32), host(S2).view(np.uint32)), case
+
+
 def fixed_chains_graph(rng, lengths):
     """Chains that mix packs with fixed-duration nodes (a fixed node every third step), constant
     floors from one host node every 50 steps, and chains of the given lengths."""
