@@ -28,7 +28,9 @@
  * take slack from prefix sums of durations along each chain instead of the backward recurrence
  * (the same values whenever every time sum is exact, emo_graph_info.exact_time_sums); the
  * pack-energy sum is accumulated in fp32 blocks of at most 64 packs added into an fp64 total,
- * then rounded to fp32.
+ * then rounded to fp32 (blocks follow the program order in the one-kernel, segmented and
+ * interpreting kernels and each chain's window in the chain kernels, so energies from the two
+ * groups of kinds agree to that rounding, not bit for bit).
  *
  * Units are the caller's (the tests use microseconds and power units with energy =
  * power * time).  Level F-1 is conventionally the maximum frequency; nothing here depends on it.
@@ -185,7 +187,7 @@ typedef struct {
  *                            EMO_ERR_DEVICE by the batch call instead of falling back.
  * Both kinds compute bit-identical results, except that the cut-segment and chain scan kernels
  * round differently on graphs whose time sums are not exact (emo_graph_info.exact_time_sums
- * 0). */
+ * 0) and that chain kernels group the energy sum by chain windows (see the arithmetic above). */
 typedef enum {
     EMO_KERNELS_AUTO = 0,
     EMO_KERNELS_INTERPRETED = 1,
@@ -483,8 +485,9 @@ emo_status emo_pack_model(int32_t num_metrics, int32_t num_benchmarks, const flo
  * EMO_ERR_UNSUPPORTED when the graph is too large for one specialised kernel. */
 emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len);
 
-/* Diagnostics: the HIP source of the segmented specialised kernels of `g`, used for graphs too
- * large for one kernel (eval/select) or to keep every finish time in registers (slack): one
+/* Diagnostics: the HIP source of the segmented specialised kernels of `g`, used for calls
+ * without slack on graphs of more than 512 steps (faster there than one kernel) and for slack on
+ * graphs too large to keep every finish time in registers: one
  * forward kernel per segment of consecutive steps, launched in order, then one backward kernel
  * per segment in reverse order, which recomputes finish times from checkpointed values instead
  * of reading stored ones.  Same buffer convention as emo_graph_specialized_source.
