@@ -486,8 +486,9 @@ emo_status emo_pack_model(int32_t num_metrics, int32_t num_benchmarks, const flo
 emo_status emo_graph_specialized_source(emo_graph_t g, char *buf, int64_t *len);
 
 /* Diagnostics: the HIP source of the segmented specialised kernels of `g`, used for calls
- * without slack on graphs of more than 512 steps (faster there than one kernel) and for slack on
- * graphs too large to keep every finish time in registers: one
+ * without slack on graphs too large for one kernel or whose (time, energy) table exceeds the
+ * 64 KB one kernel holds in LDS, and for slack on graphs too large to keep every finish time in
+ * registers: one
  * forward kernel per segment of consecutive steps, launched in order, then one backward kernel
  * per segment in reverse order, which recomputes finish times from checkpointed values instead
  * of reading stored ones.  Same buffer convention as emo_graph_specialized_source.

@@ -90,10 +90,6 @@ constexpr int32_t kHotSpan = 96;
 
 constexpr int32_t kJitMaxOps = 2048;      // larger graphs compile too slowly as one kernel
 constexpr int32_t kJitMaxSlackOps = 160;  // every finish time stays in a VGPR
-// Calls without slack on graphs of more steps than this take the segmented kernels when the live
-// set allows: at 2^20 candidates 640 steps on 16 chains take 0.26 ms there against 0.93 ms in one
-// kernel, 2,048 steps 0.82 against 3.84, while 512 steps take 0.14 ms in one kernel against 0.19.
-constexpr int32_t kJitEvalMaxOps = 512;
 // Segmented kernels (larger graphs): steps per segment kernel and per recompute sub-segment,
 // and the largest graph compiled this way (compile time grows with the step count).
 constexpr int32_t kChainSegOps = 256;
@@ -263,8 +259,9 @@ struct emo_graph_s {
     int jit_state = 0;                       // 0 not tried, 1 compiled, -1 failed
     emo::JitModule jm;
     std::string jit_log;
-    // segmented kernels: forward kernels for eval/select past kJitEvalMaxOps steps, backward
-    // kernels for slack when the graph is too large to keep every finish time
+    // segmented kernels: forward kernels for eval/select when one kernel would not hold the
+    // table in LDS, backward kernels for slack when the graph is too large to keep every finish
+    // time
     bool chain_eval = false;
     bool chain_slack = false;
     bool chain_scan_first = false;           // slack: windowed chain scan before segmented kernels
@@ -1234,7 +1231,12 @@ emo_status emo_load_graph(int32_t num_nodes, int32_t num_edges, const int32_t *e
     g->jit_slack_eligible = g->jit_eligible && nops <= kJitMaxSlackOps;
     g->jit_slack_staged = sf.monotone && P % 16 == 0;
     const bool narrow = pe.n_hot + pe.n_cold <= kChainMaxLive;
-    g->chain_eval = narrow && nops > kJitEvalMaxOps && nops <= kChainMaxOps;
+    // Without slack, one kernel past kJitTableLds reads the table from global memory: the
+    // segmented kernels (table windows in LDS) are then faster whenever the live set allows.  At
+    // 2^20 candidates and 16 levels, 640 steps on 16 chains (an 80 KB table) take 0.26 ms there
+    // against 0.93 ms in one kernel, 2,048 steps 0.82 against 3.84; 512 steps (64 KB, in LDS)
+    // take 0.14 ms in one kernel against 0.19.
+    g->chain_eval = narrow && nops <= kChainMaxOps && (nops > kJitMaxOps || jit_table_bytes(*g) > kJitTableLds);
     g->chain_slack = narrow && nops > kJitMaxSlackOps && nops <= kChainMaxOps;
     g->chain_scan_first = chains_ok && dc.win > 0 && nops >= kChainScanMinOps;
     g->cut_plan = emo::jit_cut_plan(g->jg, cut_steps(*g, sf), kCutMaxPacks, kCutSubPacks);
