@@ -1051,8 +1051,10 @@ emo_status choose_path(emo_graph_s *g, const uint8_t *levels, const float *slack
         *path = Path::kChainLanes;
         return EMO_OK;
     }
-    // graphs with cut nodes, too large for one kernel: the segments between cuts in parallel
-    const bool single_ok = slack ? g->jit_slack_eligible : g->jit_eligible;
+    // graphs with cut nodes, too large for one kernel (or, without slack, for its table in LDS):
+    // the segments between cuts in parallel (ahead of the segmented kernels: 1,024 packs with 4
+    // cuts, 2^20 candidates without slack, take 0.28 ms there against 0.35)
+    const bool single_ok = slack ? g->jit_slack_eligible : g->jit_eligible && !g->chain_eval;
     if (!single_ok && g->cut_ok && B < (int64_t(1) << 30) && aligned(levels, 16) &&
         (!slack || aligned(slack, 16))) {
         if (ensure_cut(g) == 1) {

@@ -280,6 +280,11 @@ def test_cut_segment_kernels(torch, emo, case):
     lv = dev(torch, rows)
     T_or, E_or = oracle.eval_batch(g, rows, nthreads=8)
     T, E = gh.eval_policies(lv)
+    torch.cuda.synchronize()
+    # without slack: one kernel while its (time, energy) table (plus 256 pad entries when F is not
+    # a power of two) fits its 64 KB of LDS, else the cut kernels
+    tb = (P * F + (0 if F & (F - 1) == 0 else 256)) * 8
+    assert gh.info()["last_kernels"] == (1 if tb <= 65536 else 5), (tb, gh.info())
     S = gh.slack(lv)
     torch.cuda.synchronize()
     info = gh.info()
