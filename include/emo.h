@@ -129,8 +129,10 @@ typedef struct {
                                      minimum; results are unchanged) */
     int32_t chain_window;         /* packs per window of the windowed chain-lane kernel, 0 when
                                      it does not apply (more than 16 chains, a chain that goes
-                                     back to an earlier window, fewer than 16 packs); calls use
-                                     it when levels and slack are 16-byte aligned (rows of a
+                                     back to an earlier window, fewer than 16 packs); calls
+                                     without slack use it on graphs that neither one kernel nor
+                                     the segmented kernels take, when levels and slack are
+                                     16-byte aligned (rows of a
                                      pack count that is not a multiple of 16 are copied from
                                      the dwords around each 16-byte piece) */
     int32_t cut_segments;         /* segments of the cut-segment kernels, 0 when they do not
@@ -154,8 +156,9 @@ typedef struct {
                                      (last_kernels 6 and 8), 0 when it does not apply: the
                                      candidate-dependent nodes must form at most 16 disjoint
                                      chains visiting the windows in increasing order (the
-                                     windowed layout); calls with slack use it when levels and
-                                     slack are 16-byte aligned */
+                                     windowed layout); calls with slack use it on graphs of at
+                                     least 768 steps (the segmented kernels, slower there, take
+                                     161-767) when levels and slack are 16-byte aligned */
     int32_t chain_scan_full;      /* 1 when slack calls of the two-pass chain scan run the
                                      kernel with per-thread copy plans (last_kernels 8): every
                                      window lies wholly inside the graph (P a multiple of
